@@ -1,0 +1,573 @@
+/*
+ * oracle.c -- TEST INFRASTRUCTURE ONLY (see oracle.h).
+ *
+ * Plain CPU reference of one mini-batch of DistDGLv2's vertex-wise neighbour
+ * sampling on a heterogeneous graph, followed by per-hop compaction and the
+ * gather of input-frontier features.  Everything here is written for a reader
+ * checking it against the paper, not for speed: whole-array sorts, binary
+ * searches and one Philox call per edge key.
+ *
+ * What the paper fixes:
+ *  - A mini-batch starts from target ("seed") vertices; each target keeps at
+ *    most K (the fanout) randomly chosen neighbours; this repeats recursively,
+ *    one hop per GNN layer (Sec. 3.2).
+ *  - Sampling goes one hop at a time; after a hop, the unique set of vertices
+ *    (the frontier) seeds the next hop (Sec. 4.2.2).
+ *  - Compaction removes empty vertices and relabels vertices and edges
+ *    (Sec. 4.2.1 pipeline stages, Sec. 4.2.2).
+ *  - Vertex and edge IDs are type-specific, unique only within their type
+ *    (Sec. 4.1.4).
+ *  - Messages flow from in-neighbours to a vertex (Sec. 3.1, Eq. 1), so a
+ *    destination samples among its in-edges (CSC keyed by destination).
+ *  - The input-layer frontier is what the feature copy needs (Sec. 4.2.1).
+ *
+ * Readings where the paper is silent (listed with their reasons in the design
+ * notes of the repository):
+ *  - "at most K randomly picked" is sampling without replacement: every
+ *    in-edge is kept when deg <= K or K == -1; none when K == 0.
+ *  - The random choice is made deterministic: the kept edges are the K with
+ *    the smallest (key, edge ID), key = a 32-bit Philox4x32-10 output word of
+ *    counter (g lo, g hi, hop, etype), g = eid >> 2, word eid & 3, under the
+ *    64-bit key sigma; with key_bits < 32 only the top key_bits bits count
+ *    (a test knob that makes ties common).
+ *  - Fanouts are indexed by hop (hop 0 starts from the seeds) and edge type.
+ *  - Edges of a block are grouped by destination in frontier order, and by
+ *    ascending edge ID within one destination.
+ *  - Source numbering of a block: the destination frontier first, in its
+ *    given order, then the newly reached vertices in ascending vertex ID.
+ *    Frontier vertices stay even when they sampled nothing.
+ */
+#include "oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------ */
+/* Philox4x32-10.  Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As
+ * Easy as 1, 2, 3", SC'11, Sec. 3 (Philox): each round multiplies counter
+ * words 0 and 2 by two fixed odd constants, xors the high halves of the
+ * products with the other two counter words and the round key, and permutes
+ * the words; the round key advances by a Weyl sequence (golden ratio and
+ * sqrt(3)-1 constants) between rounds.  Ten rounds.                    */
+
+static const uint32_t PHILOX_M0 = 0xD2511F53u;
+static const uint32_t PHILOX_M1 = 0xCD9E8D57u;
+static const uint32_t PHILOX_W0 = 0x9E3779B9u;
+static const uint32_t PHILOX_W1 = 0xBB67AE85u;
+
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                          uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += PHILOX_W0;
+      k1 += PHILOX_W1;
+    }
+    uint64_t p0 = (uint64_t)PHILOX_M0 * (uint64_t)x0;
+    uint64_t p1 = (uint64_t)PHILOX_M1 * (uint64_t)x2;
+    uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    uint32_t y0 = hi1 ^ x1 ^ k0;
+    uint32_t y1 = lo1;
+    uint32_t y2 = hi0 ^ x3 ^ k1;
+    uint32_t y3 = lo0;
+    x0 = y0;
+    x1 = y1;
+    x2 = y2;
+    x3 = y3;
+  }
+  out[0] = x0;
+  out[1] = x1;
+  out[2] = x2;
+  out[3] = x3;
+}
+
+uint32_t oracle_edge_key(uint64_t sigma, int32_t hop, int32_t etype,
+                         int64_t eid, int32_t key_bits) {
+  uint64_t g = (uint64_t)eid >> 2;
+  uint32_t ctr[4] = {(uint32_t)g, (uint32_t)(g >> 32), (uint32_t)hop,
+                     (uint32_t)etype};
+  uint32_t key[2] = {(uint32_t)sigma, (uint32_t)(sigma >> 32)};
+  uint32_t out[4];
+  oracle_philox4x32_10(ctr, key, out);
+  uint32_t k = out[eid & 3];
+  if (key_bits < 32) k >>= (32 - key_bits);
+  return k;
+}
+
+/* ------------------------------------------------------------------ */
+/* Choosing the neighbours of one (destination, edge type) pair.        */
+
+typedef struct {
+  uint32_t key;
+  int64_t eid;
+} keyed_edge;
+
+static int cmp_keyed_edge(const void *a, const void *b) {
+  const keyed_edge *x = (const keyed_edge *)a, *y = (const keyed_edge *)b;
+  if (x->key != y->key) return x->key < y->key ? -1 : 1;
+  if (x->eid != y->eid) return x->eid < y->eid ? -1 : 1;
+  return 0;
+}
+
+static int cmp_i64(const void *a, const void *b) {
+  int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+int oracle_select(uint64_t sigma, int32_t hop, int32_t etype, int64_t lo,
+                  int64_t hi, int32_t fanout, int32_t key_bits,
+                  int64_t *out_eids, int64_t *n_out) {
+  if (hi < lo || fanout < -1 || key_bits < 1 || key_bits > 32)
+    return ORACLE_EINVAL;
+  int64_t deg = hi - lo;
+  if (fanout < 0 || deg <= fanout) {
+    /* keep every in-edge, in slot order */
+    for (int64_t j = 0; j < deg; ++j) out_eids[j] = lo + j;
+    *n_out = deg;
+    return ORACLE_OK;
+  }
+  /* key every in-edge, order by (key, eid), keep the first `fanout` */
+  keyed_edge *all = (keyed_edge *)malloc(sizeof(keyed_edge) * (size_t)deg);
+  if (!all) return ORACLE_ENOMEM;
+  for (int64_t j = 0; j < deg; ++j) {
+    all[j].eid = lo + j;
+    all[j].key = oracle_edge_key(sigma, hop, etype, lo + j, key_bits);
+  }
+  qsort(all, (size_t)deg, sizeof(keyed_edge), cmp_keyed_edge);
+  for (int64_t j = 0; j < fanout; ++j) out_eids[j] = all[j].eid;
+  free(all);
+  qsort(out_eids, (size_t)fanout, sizeof(int64_t), cmp_i64);
+  *n_out = fanout;
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Input checks.                                                        */
+
+int oracle_check_graph(const oracle_ntype *ntypes, int32_t n_ntypes,
+                       const oracle_etype *etypes, int32_t n_etypes) {
+  if (n_ntypes < 1 || n_etypes < 0 || !ntypes || (n_etypes > 0 && !etypes))
+    return ORACLE_EINVAL;
+  for (int32_t t = 0; t < n_ntypes; ++t) {
+    if (ntypes[t].num_nodes < 0 || ntypes[t].row_bytes < 0)
+      return ORACLE_EINVAL;
+    if (ntypes[t].row_bytes > 0 && ntypes[t].num_nodes > 0 && !ntypes[t].feat)
+      return ORACLE_EINVAL;
+  }
+  for (int32_t e = 0; e < n_etypes; ++e) {
+    const oracle_etype *et = &etypes[e];
+    if (et->src_type < 0 || et->src_type >= n_ntypes || et->dst_type < 0 ||
+        et->dst_type >= n_ntypes || et->nnz < 0 || !et->indptr ||
+        (et->nnz > 0 && !et->indices))
+      return ORACLE_EINVAL;
+    int64_t n_dst = ntypes[et->dst_type].num_nodes;
+    int64_t n_src = ntypes[et->src_type].num_nodes;
+    if (et->indptr[0] != 0 || et->indptr[n_dst] != et->nnz)
+      return ORACLE_EINVAL;
+    for (int64_t v = 0; v < n_dst; ++v)
+      if (et->indptr[v + 1] < et->indptr[v]) return ORACLE_EINVAL;
+    for (int64_t j = 0; j < et->nnz; ++j)
+      if (et->indices[j] < 0 || et->indices[j] >= n_src)
+        return ORACLE_EINVAL;
+  }
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Result container.                                                    */
+
+typedef struct {
+  int64_t n_dst, n_src;
+  int64_t *src_gid; /* n_src entries, the first n_dst being the frontier */
+} onodes;
+
+typedef struct {
+  int64_t n_edges;
+  int64_t *indptr; /* n_dst + 1 */
+  int32_t *src_local;
+  int32_t *dst_local;
+  int64_t *eid;
+} oedges;
+
+struct oracle_blocks {
+  int32_t n_hops, n_ntypes, n_etypes;
+  onodes *nodes;   /* [n_hops * n_ntypes] */
+  oedges *edges;   /* [n_hops * n_etypes] */
+  int64_t *in_n;   /* [n_ntypes] */
+  int64_t **in_gid;
+};
+
+void oracle_blocks_free(oracle_blocks *b) {
+  if (!b) return;
+  if (b->nodes)
+    for (int64_t i = 0; i < (int64_t)b->n_hops * b->n_ntypes; ++i)
+      free(b->nodes[i].src_gid);
+  if (b->edges)
+    for (int64_t i = 0; i < (int64_t)b->n_hops * b->n_etypes; ++i) {
+      free(b->edges[i].indptr);
+      free(b->edges[i].src_local);
+      free(b->edges[i].dst_local);
+      free(b->edges[i].eid);
+    }
+  if (b->in_gid)
+    for (int32_t t = 0; t < b->n_ntypes; ++t) free(b->in_gid[t]);
+  free(b->nodes);
+  free(b->edges);
+  free(b->in_n);
+  free(b->in_gid);
+  free(b);
+}
+
+/* a vertex of the frontier with its position, for lookups by vertex ID */
+typedef struct {
+  int64_t gid;
+  int64_t pos;
+} gid_pos;
+
+static int cmp_gid_pos(const void *a, const void *b) {
+  const gid_pos *x = (const gid_pos *)a, *y = (const gid_pos *)b;
+  return x->gid < y->gid ? -1 : (x->gid > y->gid ? 1 : 0);
+}
+
+/* position of gid in the sorted table, or -1 */
+static int64_t find_gid_pos(const gid_pos *tab, int64_t n, int64_t gid) {
+  int64_t a = 0, b = n;
+  while (a < b) {
+    int64_t m = a + (b - a) / 2;
+    if (tab[m].gid < gid)
+      a = m + 1;
+    else
+      b = m;
+  }
+  return (a < n && tab[a].gid == gid) ? tab[a].pos : -1;
+}
+
+/* index of gid in the ascending array, or -1 */
+static int64_t find_sorted(const int64_t *arr, int64_t n, int64_t gid) {
+  int64_t a = 0, b = n;
+  while (a < b) {
+    int64_t m = a + (b - a) / 2;
+    if (arr[m] < gid)
+      a = m + 1;
+    else
+      b = m;
+  }
+  return (a < n && arr[a] == gid) ? a : -1;
+}
+
+/* one sampled edge before relabelling */
+typedef struct {
+  int64_t src_gid;
+  int32_t dst_local;
+  int64_t eid;
+} raw_edge;
+
+/* ------------------------------------------------------------------ */
+/* The mini-batch.                                                      */
+
+int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
+                         const oracle_etype *etypes, int32_t n_etypes,
+                         const int64_t *const *seeds, const int64_t *n_seeds,
+                         int32_t n_hops, const int32_t *fanouts, uint64_t sigma,
+                         int32_t key_bits, oracle_blocks **out) {
+  if (!out) return ORACLE_EINVAL;
+  *out = NULL;
+  if (n_ntypes < 1 || n_etypes < 0 || !ntypes || (n_etypes > 0 && !etypes))
+    return ORACLE_EINVAL;
+  if (n_hops < 0 || key_bits < 1 || key_bits > 32 || !n_seeds)
+    return ORACLE_EINVAL;
+  if (n_hops > 0 && n_etypes > 0 && !fanouts) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < (int64_t)n_hops * n_etypes; ++i)
+    if (fanouts[i] < -1) return ORACLE_EINVAL;
+  for (int32_t e = 0; e < n_etypes; ++e)
+    if (etypes[e].src_type < 0 || etypes[e].src_type >= n_ntypes ||
+        etypes[e].dst_type < 0 || etypes[e].dst_type >= n_ntypes)
+      return ORACLE_EINVAL;
+
+  /* Seeds: present, in range and unique within their type (the targets of a
+   * mini-batch are a set of vertices, Sec. 3.2). */
+  for (int32_t t = 0; t < n_ntypes; ++t) {
+    if (n_seeds[t] < 0) return ORACLE_EINVAL;
+    if (n_seeds[t] == 0) continue;
+    if (!seeds || !seeds[t]) return ORACLE_EINVAL;
+    int64_t *tmp = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_seeds[t]);
+    if (!tmp) return ORACLE_ENOMEM;
+    memcpy(tmp, seeds[t], sizeof(int64_t) * (size_t)n_seeds[t]);
+    qsort(tmp, (size_t)n_seeds[t], sizeof(int64_t), cmp_i64);
+    int bad = 0;
+    for (int64_t i = 0; i < n_seeds[t]; ++i) {
+      if (tmp[i] < 0 || tmp[i] >= ntypes[t].num_nodes) bad = 1;
+      if (i > 0 && tmp[i] == tmp[i - 1]) bad = 1;
+    }
+    free(tmp);
+    if (bad) return ORACLE_EINVAL;
+  }
+
+  oracle_blocks *b = (oracle_blocks *)calloc(1, sizeof(oracle_blocks));
+  if (!b) return ORACLE_ENOMEM;
+  b->n_hops = n_hops;
+  b->n_ntypes = n_ntypes;
+  b->n_etypes = n_etypes;
+  b->nodes = (onodes *)calloc((size_t)n_hops * n_ntypes + 1, sizeof(onodes));
+  b->edges = (oedges *)calloc((size_t)n_hops * n_etypes + 1, sizeof(oedges));
+  b->in_n = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
+  b->in_gid = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
+  if (!b->nodes || !b->edges || !b->in_n || !b->in_gid) {
+    oracle_blocks_free(b);
+    return ORACLE_ENOMEM;
+  }
+
+  /* frontier of the current hop, per node type: F[0][t] = seeds of t */
+  int64_t *fn = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
+  int64_t **fr = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
+  int status = ORACLE_OK;
+  if (!fn || !fr) status = ORACLE_ENOMEM;
+  for (int32_t t = 0; t < n_ntypes && status == ORACLE_OK; ++t) {
+    fn[t] = n_seeds[t];
+    fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
+    if (!fr[t]) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    if (fn[t] > 0) memcpy(fr[t], seeds[t], sizeof(int64_t) * (size_t)fn[t]);
+  }
+
+  for (int32_t h = 0; h < n_hops && status == ORACLE_OK; ++h) {
+    /* ---- Step 1: sample the neighbours of every (destination, etype)
+     * pair of this hop's frontier, each pair independently. */
+    raw_edge **sampled =
+        (raw_edge **)calloc((size_t)n_etypes + 1, sizeof(raw_edge *));
+    int64_t *n_sampled = (int64_t *)calloc((size_t)n_etypes + 1, sizeof(int64_t));
+    if (!sampled || !n_sampled) {
+      free(sampled);
+      free(n_sampled);
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    for (int32_t e = 0; e < n_etypes && status == ORACLE_OK; ++e) {
+      const oracle_etype *et = &etypes[e];
+      int32_t t = et->dst_type;
+      int32_t k = fanouts[(int64_t)h * n_etypes + e];
+      oedges *blk = &b->edges[(int64_t)h * n_etypes + e];
+      blk->indptr = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
+      /* at most min(deg, k) per destination; total bounded by nnz */
+      int64_t cap = 0;
+      for (int64_t i = 0; i < fn[t]; ++i) {
+        int64_t deg = et->indptr[fr[t][i] + 1] - et->indptr[fr[t][i]];
+        cap += (k < 0 || deg <= k) ? deg : k;
+      }
+      sampled[e] = (raw_edge *)malloc(sizeof(raw_edge) * (size_t)(cap + 1));
+      if (!blk->indptr || !sampled[e]) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      blk->indptr[0] = 0;
+      int64_t cnt = 0;
+      for (int64_t i = 0; i < fn[t]; ++i) {
+        int64_t v = fr[t][i];
+        int64_t lo = et->indptr[v], hi = et->indptr[v + 1];
+        int64_t *chosen = (int64_t *)malloc(sizeof(int64_t) * (size_t)(hi - lo + 1));
+        int64_t nc = 0;
+        if (!chosen) {
+          status = ORACLE_ENOMEM;
+          break;
+        }
+        status = oracle_select(sigma, h, e, lo, hi, k, key_bits, chosen, &nc);
+        if (status != ORACLE_OK) {
+          free(chosen);
+          break;
+        }
+        for (int64_t c = 0; c < nc; ++c) {
+          sampled[e][cnt].src_gid = et->indices[chosen[c]];
+          sampled[e][cnt].dst_local = (int32_t)i;
+          sampled[e][cnt].eid = chosen[c];
+          ++cnt;
+        }
+        free(chosen);
+        blk->indptr[i + 1] = cnt;
+      }
+      n_sampled[e] = cnt;
+    }
+
+    /* ---- Step 2: the frontier of the next hop, per node type: the unique
+     * set of this hop's vertices -- the current frontier (kept in its order)
+     * followed by the newly reached sources in ascending ID. */
+    int64_t **nf = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
+    int64_t *nfn = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
+    gid_pos **ftab = (gid_pos **)calloc((size_t)n_ntypes, sizeof(gid_pos *));
+    int64_t *n_new = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
+    if (!nf || !nfn || !ftab || !n_new) status = ORACLE_ENOMEM;
+    for (int32_t t = 0; t < n_ntypes && status == ORACLE_OK; ++t) {
+      /* the current frontier as a (gid, position) lookup table */
+      ftab[t] = (gid_pos *)malloc(sizeof(gid_pos) * (size_t)(fn[t] + 1));
+      if (!ftab[t]) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      for (int64_t i = 0; i < fn[t]; ++i) {
+        ftab[t][i].gid = fr[t][i];
+        ftab[t][i].pos = i;
+      }
+      qsort(ftab[t], (size_t)fn[t], sizeof(gid_pos), cmp_gid_pos);
+      /* every sampled source of type t */
+      int64_t total = 0;
+      for (int32_t e = 0; e < n_etypes; ++e)
+        if (etypes[e].src_type == t) total += n_sampled[e];
+      int64_t *srcs = (int64_t *)malloc(sizeof(int64_t) * (size_t)(total + 1));
+      if (!srcs) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      int64_t m = 0;
+      for (int32_t e = 0; e < n_etypes; ++e)
+        if (etypes[e].src_type == t)
+          for (int64_t j = 0; j < n_sampled[e]; ++j)
+            srcs[m++] = sampled[e][j].src_gid;
+      qsort(srcs, (size_t)m, sizeof(int64_t), cmp_i64);
+      /* unique, and not already in the frontier */
+      int64_t u = 0;
+      for (int64_t j = 0; j < m; ++j) {
+        if (j > 0 && srcs[j] == srcs[j - 1]) continue;
+        if (find_gid_pos(ftab[t], fn[t], srcs[j]) >= 0) continue;
+        srcs[u++] = srcs[j];
+      }
+      n_new[t] = u;
+      nfn[t] = fn[t] + u;
+      if (nfn[t] > INT32_MAX) {
+        free(srcs);
+        status = ORACLE_EUNSUPPORTED;
+        break;
+      }
+      nf[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nfn[t] + 1));
+      if (!nf[t]) {
+        free(srcs);
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      if (fn[t] > 0) memcpy(nf[t], fr[t], sizeof(int64_t) * (size_t)fn[t]);
+      if (u > 0) memcpy(nf[t] + fn[t], srcs, sizeof(int64_t) * (size_t)u);
+      free(srcs);
+    }
+
+    /* ---- Step 3: compaction -- relabel every sampled edge's source with
+     * its position in the source list of its type; the destination already
+     * carries its frontier position. */
+    for (int32_t e = 0; e < n_etypes && status == ORACLE_OK; ++e) {
+      int32_t s = etypes[e].src_type;
+      oedges *blk = &b->edges[(int64_t)h * n_etypes + e];
+      int64_t n = n_sampled[e];
+      blk->n_edges = n;
+      blk->src_local = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
+      blk->dst_local = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
+      blk->eid = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n + 1));
+      if (!blk->src_local || !blk->dst_local || !blk->eid) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      for (int64_t j = 0; j < n; ++j) {
+        int64_t g = sampled[e][j].src_gid;
+        int64_t pos = find_gid_pos(ftab[s], fn[s], g);
+        if (pos < 0) pos = fn[s] + find_sorted(nf[s] + fn[s], n_new[s], g);
+        blk->src_local[j] = (int32_t)pos;
+        blk->dst_local[j] = sampled[e][j].dst_local;
+        blk->eid[j] = sampled[e][j].eid;
+      }
+    }
+
+    /* record the hop's vertex lists; the next hop starts from them */
+    for (int32_t t = 0; t < n_ntypes && status == ORACLE_OK; ++t) {
+      onodes *nd = &b->nodes[(int64_t)h * n_ntypes + t];
+      nd->n_dst = fn[t];
+      nd->n_src = nfn[t];
+      nd->src_gid = nf[t];
+      nf[t] = NULL;
+      free(fr[t]);
+      fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nfn[t] + 1));
+      if (!fr[t]) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      if (nfn[t] > 0)
+        memcpy(fr[t], nd->src_gid, sizeof(int64_t) * (size_t)nfn[t]);
+      fn[t] = nfn[t];
+    }
+
+    for (int32_t e = 0; e < n_etypes; ++e) free(sampled[e]);
+    free(sampled);
+    free(n_sampled);
+    if (nf)
+      for (int32_t t = 0; t < n_ntypes; ++t) free(nf[t]);
+    if (ftab)
+      for (int32_t t = 0; t < n_ntypes; ++t) free(ftab[t]);
+    free(nf);
+    free(nfn);
+    free(ftab);
+    free(n_new);
+  }
+
+  /* the input frontier: what the feature gather reads */
+  for (int32_t t = 0; t < n_ntypes && status == ORACLE_OK; ++t) {
+    b->in_n[t] = fn[t];
+    b->in_gid[t] = fr[t];
+    fr[t] = NULL;
+  }
+  if (fr)
+    for (int32_t t = 0; t < n_ntypes; ++t) free(fr[t]);
+  free(fr);
+  free(fn);
+  if (status != ORACLE_OK) {
+    oracle_blocks_free(b);
+    return status;
+  }
+  *out = b;
+  return ORACLE_OK;
+}
+
+int oracle_blocks_nodes(const oracle_blocks *b, int32_t hop, int32_t ntype,
+                        int64_t *n_dst, int64_t *n_src,
+                        const int64_t **src_gid) {
+  if (!b || hop < 0 || hop >= b->n_hops || ntype < 0 || ntype >= b->n_ntypes)
+    return ORACLE_EINVAL;
+  const onodes *nd = &b->nodes[(int64_t)hop * b->n_ntypes + ntype];
+  if (n_dst) *n_dst = nd->n_dst;
+  if (n_src) *n_src = nd->n_src;
+  if (src_gid) *src_gid = nd->src_gid;
+  return ORACLE_OK;
+}
+
+int oracle_blocks_edges(const oracle_blocks *b, int32_t hop, int32_t etype,
+                        int64_t *n_edges, const int64_t **indptr,
+                        const int32_t **src_local, const int32_t **dst_local,
+                        const int64_t **eid) {
+  if (!b || hop < 0 || hop >= b->n_hops || etype < 0 || etype >= b->n_etypes)
+    return ORACLE_EINVAL;
+  const oedges *ed = &b->edges[(int64_t)hop * b->n_etypes + etype];
+  if (n_edges) *n_edges = ed->n_edges;
+  if (indptr) *indptr = ed->indptr;
+  if (src_local) *src_local = ed->src_local;
+  if (dst_local) *dst_local = ed->dst_local;
+  if (eid) *eid = ed->eid;
+  return ORACLE_OK;
+}
+
+int oracle_blocks_input_nodes(const oracle_blocks *b, int32_t ntype,
+                              int64_t *n, const int64_t **gid) {
+  if (!b || ntype < 0 || ntype >= b->n_ntypes) return ORACLE_EINVAL;
+  if (n) *n = b->in_n[ntype];
+  if (gid) *gid = b->in_gid[ntype];
+  return ORACLE_OK;
+}
+
+int oracle_gather_rows(const void *feat, int64_t n_rows, int64_t row_bytes,
+                       const int64_t *ids, int64_t n, void *out) {
+  if (n < 0 || row_bytes <= 0 || (n > 0 && (!feat || !ids || !out)))
+    return ORACLE_EINVAL;
+  for (int64_t i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= n_rows) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < n; ++i)
+    memcpy((char *)out + i * row_bytes,
+           (const char *)feat + ids[i] * row_bytes, (size_t)row_bytes);
+  return ORACLE_OK;
+}

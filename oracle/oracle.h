@@ -1,0 +1,109 @@
+/*
+ * oracle.h -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-threaded CPU reference for heterogeneous multi-hop
+ * fanout neighbour sampling, per-hop compaction into relabelled bipartite
+ * blocks, and the gather of input-frontier features, as DistDGLv2 describes
+ * them (arXiv 2112.15345: Sec. 3.2 "Mini-batch training", Sec. 4.2.2
+ * "Distributed hybrid CPU/GPU sampling", Sec. 4.1.4 type-specific IDs).
+ *
+ * Only the test suite, the smoke check and the benchmark's CPU-baseline leg
+ * may call it.  It shares no code, header, table or helper with the GPU
+ * library; the two agree only through the written definition of the method.
+ *
+ * Status codes are plain ints with the same meaning as the GPU library's:
+ *   0 ok, -1 invalid argument, -2 out of memory, -4 unsupported size.
+ */
+#ifndef ORACLE_H
+#define ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ENOMEM (-2)
+#define ORACLE_EUNSUPPORTED (-4)
+
+/* One node type: its vertex count and (optionally) a row-major feature table
+ * of num_nodes rows of row_bytes bytes each.  feat == NULL or row_bytes == 0
+ * means the type carries no features. */
+typedef struct {
+  int64_t num_nodes;
+  const void *feat;
+  int64_t row_bytes;
+} oracle_ntype;
+
+/* One edge type (src_type -> dst_type) stored as CSC keyed by destination:
+ * the in-edges of destination v are slots indptr[v] .. indptr[v+1]-1, and
+ * indices[slot] is the source vertex (a type-specific ID of src_type).
+ * The slot number is the edge ID. */
+typedef struct {
+  int32_t src_type;
+  int32_t dst_type;
+  int64_t nnz;
+  const int64_t *indptr;  /* num_nodes(dst_type) + 1 entries */
+  const int64_t *indices; /* nnz entries */
+} oracle_etype;
+
+typedef struct oracle_blocks oracle_blocks;
+
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) on one 128-bit counter
+ * and a 64-bit key; writes the four 32-bit output words. */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                          uint32_t out[4]);
+
+/* The random key of edge `eid` of edge type `etype` at hop `hop` under
+ * sampling seed `sigma`, truncated to its top `key_bits` bits. */
+uint32_t oracle_edge_key(uint64_t sigma, int32_t hop, int32_t etype,
+                         int64_t eid, int32_t key_bits);
+
+/* Sampling of one (destination, edge type) pair whose in-edges are slots
+ * lo .. hi-1: writes the chosen edge IDs, ascending, to out_eids (capacity
+ * at least hi-lo) and their count to *n_out. */
+int oracle_select(uint64_t sigma, int32_t hop, int32_t etype, int64_t lo,
+                  int64_t hi, int32_t fanout, int32_t key_bits,
+                  int64_t *out_eids, int64_t *n_out);
+
+/* Checks a graph (types in range, indptr starts at 0, is non-decreasing and
+ * ends at nnz, indices in range). */
+int oracle_check_graph(const oracle_ntype *ntypes, int32_t n_ntypes,
+                       const oracle_etype *etypes, int32_t n_etypes);
+
+/* Full multi-hop sampling + compaction.  seeds[t] holds n_seeds[t] unique
+ * vertex IDs of type t (seeds[t] may be NULL when n_seeds[t] == 0);
+ * fanouts is hop-major [n_hops * n_etypes], -1 meaning "all in-edges". */
+int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
+                         const oracle_etype *etypes, int32_t n_etypes,
+                         const int64_t *const *seeds, const int64_t *n_seeds,
+                         int32_t n_hops, const int32_t *fanouts, uint64_t sigma,
+                         int32_t key_bits, oracle_blocks **out);
+
+void oracle_blocks_free(oracle_blocks *b);
+
+int oracle_blocks_nodes(const oracle_blocks *b, int32_t hop, int32_t ntype,
+                        int64_t *n_dst, int64_t *n_src,
+                        const int64_t **src_gid);
+
+int oracle_blocks_edges(const oracle_blocks *b, int32_t hop, int32_t etype,
+                        int64_t *n_edges, const int64_t **indptr,
+                        const int32_t **src_local, const int32_t **dst_local,
+                        const int64_t **eid);
+
+/* The input frontier of type t: the source list of the last hop (the seeds
+ * when n_hops == 0). */
+int oracle_blocks_input_nodes(const oracle_blocks *b, int32_t ntype,
+                              int64_t *n, const int64_t **gid);
+
+/* out[i] = bytes of row ids[i] of a table of n_rows rows of row_bytes. */
+int oracle_gather_rows(const void *feat, int64_t n_rows, int64_t row_bytes,
+                       const int64_t *ids, int64_t n, void *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

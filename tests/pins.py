@@ -1,0 +1,344 @@
+"""Checks that pin the CPU oracle to things other than itself.
+
+- Philox4x32-10 and the edge key are compared with rocRAND's engine (an
+  independent implementation, reached through tests/rocrand_ref.cpp).
+- The selection of one (destination, etype) pair is compared with brute force:
+  numpy's lexsort over the rocRAND keys of every in-edge.
+- Whole mini-batches are checked against the definitions of the method
+  (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2.2): sampled degree =
+  min(deg, K); every kept edge exists and is one of the K smallest; the next
+  frontier is the unique set of this hop's vertices (numpy set operations); the
+  relabel maps each edge back to its endpoints.
+- Gather against numpy fancy indexing; error codes; uniformity statistics.
+
+Each pin returns a list of failure messages (empty = pass), so the same checks
+can run against deliberately broken builds of the oracle.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+
+import numpy as np
+
+import oracle
+import workloads
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+_RR_SRC = os.path.join(HERE, "rocrand_ref.cpp")
+_RR_LIB = os.path.join(ROOT, "_build", "tests", "librocrand_ref.so")
+M32 = (1 << 32) - 1
+
+_rr = None
+
+
+def rocrand_ref():
+    """rocRAND's Philox4x32-10 engine on the host (built on first use)."""
+    global _rr
+    if _rr is None:
+        if not os.path.exists(_RR_LIB) or os.path.getmtime(_RR_LIB) < os.path.getmtime(_RR_SRC):
+            os.makedirs(os.path.dirname(_RR_LIB), exist_ok=True)
+            subprocess.run(["/opt/rocm/bin/hipcc", "-x", "hip", "-O1", "-fPIC", "-shared",
+                            "--offload-arch=gfx950", "-I/opt/rocm/include", _RR_SRC, "-o",
+                            _RR_LIB + ".tmp"], check=True, capture_output=True)
+            os.replace(_RR_LIB + ".tmp", _RR_LIB)
+        lib = ctypes.CDLL(_RR_LIB)
+        lib.rr_word.argtypes = [ctypes.c_uint64] * 3
+        lib.rr_word.restype = ctypes.c_uint32
+        lib.rr_block.argtypes = [ctypes.c_uint64] * 3 + [ctypes.c_void_p]
+        lib.rr_block.restype = None
+        _rr = lib
+    return _rr
+
+
+def rr_key(sigma: int, hop: int, etype: int, eid: int, key_bits: int = 32) -> int:
+    """The edge key by its definition, computed by rocRAND: word (eid % 4) at
+    counter (eid / 4, hop, etype), key sigma, truncated to key_bits bits."""
+    w = rocrand_ref().rr_word(sigma & ((1 << 64) - 1), (hop & M32) | ((etype & M32) << 32), eid)
+    return int(w) >> (32 - key_bits)
+
+
+def rr_block(seed: int, subsequence: int, counter_lo64: int) -> np.ndarray:
+    out = np.zeros(4, dtype=np.uint32)
+    rocrand_ref().rr_block(seed, subsequence, counter_lo64, out.ctypes.data)
+    return out
+
+
+def brute_select(sigma, hop, etype, lo, hi, fanout, key_bits=32):
+    """The kept edge IDs of one pair: all when deg <= K or K == -1, else the K
+    smallest by (key, eid), in ascending eid."""
+    eids = np.arange(lo, hi, dtype=np.int64)
+    if fanout < 0 or hi - lo <= fanout:
+        return eids
+    keys = np.array([rr_key(sigma, hop, etype, int(x), key_bits) for x in eids], dtype=np.int64)
+    order = np.lexsort((eids, keys))
+    return np.sort(eids[order[:fanout]])
+
+
+# ---------------------------------------------------------------------------
+# pins
+
+def pin_philox(lib, rng, n=200):
+    fails = []
+    cases = [(0, 0, 0), ((1 << 64) - 1, (1 << 64) - 1, (1 << 62) - 1)]
+    for _ in range(n):
+        cases.append((int(rng.integers(0, 1 << 63)) * 2 + int(rng.integers(0, 2)),
+                      int(rng.integers(0, 1 << 63)), int(rng.integers(0, 1 << 62))))
+    for seed, sub, c in cases:
+        ref = rr_block(seed, sub, c)
+        got = oracle.philox4x32_10([c & M32, c >> 32, sub & M32, sub >> 32],
+                                   [seed & M32, seed >> 32], lib)
+        if not np.array_equal(ref, got):
+            fails.append(f"philox seed={seed} sub={sub} ctr={c}: {got} != {ref}")
+    return fails
+
+
+def pin_edge_key(lib, rng, n=300):
+    fails = []
+    for i in range(n):
+        sigma = int(rng.integers(0, 1 << 63)) * 2 + int(rng.integers(0, 2))
+        hop, et = int(rng.integers(0, 8)), int(rng.integers(0, 400))
+        eid = int(rng.integers(0, 1 << 40)) if i % 2 else int(rng.integers(0, 64))
+        bits = [32, 16, 4, 1][i % 4]
+        ref = rr_key(sigma, hop, et, eid, bits)
+        got = oracle.edge_key(sigma, hop, et, eid, bits, lib)
+        if ref != got:
+            fails.append(f"edge_key({sigma},{hop},{et},{eid},{bits}) = {got} != {ref}")
+    return fails
+
+
+def pin_select(lib, rng, n=300):
+    fails = []
+    for i in range(n):
+        lo = int(rng.integers(0, 1000))
+        deg = int(rng.integers(0, 120))
+        choices = [-1, 0, 1, 2, 3, 5, 10, 25, deg, deg + 1, max(deg - 1, 0)]
+        k = choices[int(rng.integers(0, len(choices)))]
+        sigma = int(rng.integers(0, 1 << 62))
+        hop, et = int(rng.integers(0, 4)), int(rng.integers(0, 6))
+        bits = [32, 32, 8, 3, 1][i % 5]
+        ref = brute_select(sigma, hop, et, lo, lo + deg, k, bits)
+        got = oracle.select(sigma, hop, et, lo, lo + deg, k, bits, lib)
+        if not np.array_equal(ref, got):
+            fails.append(f"select lo={lo} deg={deg} K={k} bits={bits}: {got} != {ref}")
+    return fails
+
+
+def check_blocks(ntypes, etypes, seeds, fanouts, sigma, key_bits, res, brute=True):
+    """Checks one mini-batch result against the definitions.
+
+    ntypes: [num_nodes]; etypes: [(s, d, indptr, indices)] numpy; seeds: per
+    type array or None; res: dict as returned by oracle.HostGraph.sample_blocks
+    (or the same layout from the GPU path)."""
+    fails = []
+    T, R, H = len(ntypes), len(etypes), len(fanouts)
+    F = [np.zeros(0, np.int64) if s is None else np.asarray(s, np.int64) for s in seeds]
+    for h in range(H):
+        src_lists = []
+        for t in range(T):
+            n_dst, sg = res["nodes"][(h, t)]
+            if n_dst != F[t].size or not np.array_equal(sg[:n_dst], F[t]):
+                fails.append(f"hop {h} type {t}: destination prefix is not the frontier")
+            src_lists.append(sg)
+        sampled_by_type = [[] for _ in range(T)]
+        for e, (s, d, indptr, indices) in enumerate(etypes):
+            ip, sl, dl, eid = res["edges"][(h, e)]
+            k = fanouts[h][e]
+            if ip.size != F[d].size + 1 or (ip.size and (ip[0] != 0 or ip[-1] != eid.size)):
+                fails.append(f"hop {h} etype {e}: bad block indptr")
+                continue
+            if np.any(np.diff(ip) < 0):
+                fails.append(f"hop {h} etype {e}: decreasing block indptr")
+                continue
+            for i, v in enumerate(F[d]):
+                a, b = int(ip[i]), int(ip[i + 1])
+                lo, hi = int(indptr[v]), int(indptr[v + 1])
+                deg = hi - lo
+                want_n = deg if (k < 0 or deg <= k) else k
+                if b - a != want_n:
+                    fails.append(f"hop {h} etype {e} dst {i}: {b - a} edges, want min(deg,K)={want_n}")
+                    continue
+                got = eid[a:b]
+                if np.any(dl[a:b] != i):
+                    fails.append(f"hop {h} etype {e} dst {i}: wrong dst_local")
+                if np.any(got < lo) or np.any(got >= hi):
+                    fails.append(f"hop {h} etype {e} dst {i}: edge not an in-edge of the vertex")
+                    continue
+                if np.any(np.diff(got) <= 0):
+                    fails.append(f"hop {h} etype {e} dst {i}: edge IDs not strictly ascending")
+                if brute and deg > 0:
+                    ref = brute_select(sigma, h, e, lo, hi, k, key_bits)
+                    if not np.array_equal(ref, got):
+                        fails.append(f"hop {h} etype {e} dst {i}: kept {got}, brute force {ref}")
+            if eid.size:
+                srcg = indices[eid]
+                sampled_by_type[s].append(srcg)
+                sl_ok = (sl >= 0) & (sl < src_lists[s].size)
+                if not np.all(sl_ok) or not np.array_equal(src_lists[s][sl], srcg):
+                    fails.append(f"hop {h} etype {e}: relabelled sources do not map back")
+        for t in range(T):
+            allsrc = np.concatenate(sampled_by_type[t]) if sampled_by_type[t] else np.zeros(0, np.int64)
+            want_new = np.setdiff1d(np.unique(allsrc), F[t])
+            got_new = src_lists[t][F[t].size:]
+            if not np.array_equal(want_new, got_new):
+                fails.append(f"hop {h} type {t}: new vertices {got_new[:8]}... != unique set "
+                             f"minus frontier {want_new[:8]}...")
+            F[t] = src_lists[t]
+    for t in range(T):
+        if not np.array_equal(res["input"][t], F[t]):
+            fails.append(f"type {t}: input frontier differs from the last source list")
+    return fails
+
+
+def random_case(rng, max_nodes=40, max_deg=25):
+    nn, ets, feats = workloads.random_hetero(rng, max_nodes=max_nodes, max_deg=max_deg)
+    T, R = len(nn), len(ets)
+    seeds = []
+    for t in range(T):
+        if nn[t] == 0 or rng.random() < 0.25:
+            seeds.append(None if rng.random() < 0.5 else np.zeros(0, np.int64))
+        else:
+            seeds.append(rng.choice(nn[t], size=int(rng.integers(1, nn[t] + 1)), replace=False)
+                         .astype(np.int64))
+    H = int(rng.integers(0, 4))
+    fchoices = [-1, 0, 1, 2, 3, 5, 8, 100]
+    fanouts = [[fchoices[int(rng.integers(0, len(fchoices)))] for _ in range(R)] for _ in range(H)]
+    sigma = int(rng.integers(0, 1 << 63))
+    bits = 32 if rng.random() < 0.7 else int(rng.integers(1, 5))
+    return nn, ets, feats, seeds, fanouts, sigma, bits
+
+
+def pin_blocks(lib, rng, n=60):
+    fails = []
+    for c in range(n):
+        nn, ets, feats, seeds, fanouts, sigma, bits = random_case(rng)
+        hg = oracle.HostGraph(list(zip(nn, feats)), ets, lib=lib)
+        res = hg.sample_blocks(seeds, fanouts, sigma, bits)
+        f = check_blocks(nn, ets, seeds, fanouts, sigma, bits, res)
+        fails += [f"case {c}: {m}" for m in f[:3]]
+    return fails
+
+
+def pin_gather(lib, rng, n=20):
+    fails = []
+    for c in range(n):
+        rows = int(rng.integers(1, 50))
+        dim = int(rng.integers(1, 9))
+        dt = [np.float32, np.float16, np.uint16, np.int8][c % 4]
+        feat = (rng.standard_normal((rows, dim)) * 100).astype(dt)
+        ids = rng.integers(0, rows, size=int(rng.integers(0, 80))).astype(np.int64)
+        hg = oracle.HostGraph([(rows, feat)], [], lib=lib)
+        got = hg.gather(0, ids)
+        if got.tobytes() != feat[ids].tobytes():
+            fails.append(f"gather case {c}: bytes differ from feat[ids]")
+    return fails
+
+
+def pin_errors(lib):
+    fails = []
+    indptr = np.array([0, 1, 3, 3], np.int64)
+    indices = np.array([2, 0, 1], np.int64)
+    hg = oracle.HostGraph([(3, None)], [(0, 0, indptr, indices)], lib=lib)
+
+    def expect(status, fn):
+        try:
+            fn()
+        except oracle.OracleError as ex:
+            if ex.status != status:
+                fails.append(f"expected status {status}, got {ex.status}")
+            return
+        fails.append(f"expected status {status}, call succeeded")
+
+    expect(oracle.EINVAL, lambda: hg.sample_blocks([np.array([1, 1])], [[2]], 0))
+    expect(oracle.EINVAL, lambda: hg.sample_blocks([np.array([3])], [[2]], 0))
+    expect(oracle.EINVAL, lambda: hg.sample_blocks([np.array([-1])], [[2]], 0))
+    expect(oracle.EINVAL, lambda: hg.sample_blocks([np.array([0])], [[-2]], 0))
+    expect(oracle.EINVAL, lambda: hg.sample_blocks([np.array([0])], [[1]], 0, key_bits=0))
+    expect(oracle.EINVAL, lambda: hg.sample_blocks([np.array([0])], [[1]], 0, key_bits=33))
+    expect(oracle.EINVAL, lambda: hg.gather(0, np.array([0])))
+    expect(oracle.EINVAL, lambda: oracle.HostGraph([(3, None)], [(0, 0, np.array([0, 1, 3, 2]),
+                                                                     indices)], lib=lib))
+    expect(oracle.EINVAL, lambda: oracle.HostGraph([(3, None)], [(0, 0, indptr,
+                                                                 np.array([2, 0, 3]))], lib=lib))
+    expect(oracle.EINVAL, lambda: oracle.HostGraph([(3, None)], [(0, 1, indptr, indices)], lib=lib))
+    f3 = np.arange(6, dtype=np.float32).reshape(3, 2)
+    hgf = oracle.HostGraph([(3, f3)], [], lib=lib)
+    expect(oracle.EINVAL, lambda: hgf.gather(0, np.array([3])))
+    # H = 0: the input frontier is the seeds
+    r = hg.sample_blocks([np.array([2, 0])], [], 5)
+    if not np.array_equal(r["input"][0], [2, 0]):
+        fails.append("n_hops = 0: input frontier is not the seeds")
+    return fails
+
+
+def pin_special_fanouts(lib, rng):
+    """-1 keeps all, 0 keeps none, K >= deg keeps all (closed forms)."""
+    fails = []
+    for _ in range(20):
+        lo, deg = int(rng.integers(0, 100)), int(rng.integers(0, 40))
+        sigma = int(rng.integers(0, 1 << 60))
+        all_e = np.arange(lo, lo + deg)
+        if not np.array_equal(oracle.select(sigma, 0, 0, lo, lo + deg, -1, 32, lib), all_e):
+            fails.append("K=-1 does not keep every edge")
+        if oracle.select(sigma, 0, 0, lo, lo + deg, 0, 32, lib).size != 0:
+            fails.append("K=0 keeps an edge")
+        if not np.array_equal(oracle.select(sigma, 1, 2, lo, lo + deg, deg, 32, lib), all_e):
+            fails.append("K=deg does not keep every edge")
+    return fails
+
+
+def chi2_sf(x, k):
+    """Survival function of the chi-squared distribution (scipy when present)."""
+    try:
+        from scipy.stats import chi2
+        return float(chi2.sf(x, k))
+    except Exception:  # pragma: no cover
+        # Wilson-Hilferty approximation
+        z = ((x / k) ** (1 / 3) - (1 - 2 / (9 * k))) / math.sqrt(2 / (9 * k))
+        return 0.5 * math.erfc(z / math.sqrt(2))
+
+
+def pin_statistics(lib, n_sigma=6000):
+    """"Randomly pick at most K" (Sec. 3.2): every K-subset of the in-edges is
+    equally likely over seeds, each edge is kept with probability K/deg, and the
+    draws of different hops are independent."""
+    fails = []
+    deg, k = 6, 2
+    counts = {}
+    incl = np.zeros(deg)
+    same = 0
+    for sigma in range(n_sigma):
+        a = tuple(oracle.select(sigma, 0, 3, 100, 100 + deg, k, 32, lib) - 100)
+        b = tuple(oracle.select(sigma, 1, 3, 100, 100 + deg, k, 32, lib) - 100)
+        counts[a] = counts.get(a, 0) + 1
+        incl[list(a)] += 1
+        same += a == b
+    n_sub = math.comb(deg, k)
+    if len(counts) != n_sub:
+        fails.append(f"only {len(counts)} of {n_sub} subsets ever drawn")
+    exp = n_sigma / n_sub
+    x2 = sum((c - exp) ** 2 / exp for c in counts.values()) + (n_sub - len(counts)) * exp
+    p = chi2_sf(x2, n_sub - 1)
+    if p < 1e-3:
+        fails.append(f"subset frequencies not uniform: chi2={x2:.1f}, p={p:.2g}")
+    frac = incl / n_sigma
+    if np.max(np.abs(frac - k / deg)) > 0.03:
+        fails.append(f"per-edge inclusion {frac} far from K/deg={k / deg:.3f}")
+    if abs(same / n_sigma - 1 / n_sub) > 0.02:
+        fails.append(f"hop 0 and hop 1 agree {same / n_sigma:.3f}, independent draws agree "
+                     f"{1 / n_sub:.3f}")
+    return fails
+
+
+ALL_PINS = {
+    "philox": pin_philox,
+    "edge_key": pin_edge_key,
+    "select": pin_select,
+    "special_fanouts": pin_special_fanouts,
+    "blocks": pin_blocks,
+    "gather": lambda lib, rng: pin_gather(lib, rng),
+    "errors": lambda lib, rng: pin_errors(lib),
+}
