@@ -1,0 +1,192 @@
+/*
+ * hg.h -- C ABI of the MI355X (gfx950) heterogeneous mini-batch generator.
+ *
+ * One mini-batch of DistDGLv2's vertex-wise neighbour sampling on a
+ * heterogeneous graph (arXiv 2112.15345): multi-hop, per-edge-type fanout
+ * sampling of the seeds' in-neighbourhoods over CSC adjacency (Sec. 3.2,
+ * Sec. 4.2.2), compaction of every hop into a relabelled bipartite block
+ * (Sec. 4.2.1 pipeline stages, Sec. 4.2.2), and the gather of the input
+ * frontier's feature rows (Sec. 4.2.1, the feature-copy stage, here a copy
+ * inside HBM).  Vertex and edge IDs are type-specific (Sec. 4.1.4).
+ *
+ * Conventions shared by every call:
+ *  - Pointers marked "device" are HIP device addresses on the current device;
+ *    "host" pointers are read before the call returns.
+ *  - All device work goes on the caller's `stream`.  hg_sample_blocks waits on
+ *    that stream (twice per hop, to size its outputs); the gathers are fully
+ *    asynchronous.
+ *  - Functions return hg_status; no C++ exception crosses this boundary.
+ *    After a failure, hg_last_error() describes it (thread-local text, valid
+ *    until the next call on the same thread).
+ *  - Node types and edge types are the positions in the arrays given to
+ *    hg_create; these indices enter the random key.
+ */
+#ifndef HG_H
+#define HG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hg_status {
+  HG_OK = 0,
+  HG_EINVAL = -1,       /* an argument or an input value is invalid */
+  HG_ENOMEM = -2,       /* an allocation failed */
+  HG_EDEVICE = -3,      /* a HIP runtime call failed */
+  HG_EUNSUPPORTED = -4  /* a size exceeds what the library supports */
+} hg_status;
+
+/* Element type of a feature table.  The gather copies bytes; the type only
+ * fixes the element size (4, 2, 2 bytes). */
+typedef enum hg_dtype {
+  HG_DT_NONE = 0,
+  HG_DT_F32 = 1,
+  HG_DT_F16 = 2,
+  HG_DT_BF16 = 3
+} hg_dtype;
+
+/* One node type (Sec. 4.1.4: features are stored per node type, in an ID
+ * space of that type).  feat: device, row-major [num_nodes, dim] of `dtype`,
+ * rows contiguous; NULL with dtype HG_DT_NONE for a featureless type.
+ * Borrowed: it must stay valid until hg_destroy. */
+typedef struct hg_ntype_desc {
+  int64_t num_nodes;
+  const void *feat;
+  int32_t dtype; /* hg_dtype */
+  int32_t dim;
+} hg_ntype_desc;
+
+/* One edge type src_type -> dst_type as CSC keyed by destination: the
+ * in-edges of destination v are slots indptr[v] .. indptr[v+1]-1 and
+ * indices[slot] is the source vertex.  The slot number is the edge's ID.
+ * Messages flow from in-neighbours to a vertex (Sec. 3.1, Eq. 1), so a
+ * destination samples among its in-edges.
+ * indptr: device int64 [num_nodes(dst_type) + 1]; indices: device int64 [nnz].
+ * Borrowed until hg_destroy.  nnz must be below 2^32. */
+typedef struct hg_etype_desc {
+  int32_t src_type;
+  int32_t dst_type;
+  int64_t nnz;
+  const int64_t *indptr;
+  const int64_t *indices;
+} hg_etype_desc;
+
+/* Optional device allocator for the blocks' arrays and per-call scratch.
+ * alloc returns NULL on failure (hg_sample_blocks then returns HG_ENOMEM and
+ * releases what it took).  A NULL allocator means stream-ordered
+ * hipMallocAsync / hipFreeAsync from the device's default pool. */
+typedef struct hg_allocator {
+  void *ctx;
+  void *(*alloc)(void *ctx, size_t bytes, hipStream_t stream);
+  void (*free)(void *ctx, void *ptr, hipStream_t stream);
+} hg_allocator;
+
+typedef struct hg_graph hg_graph;
+typedef struct hg_blocks hg_blocks;
+
+/* Creates an immutable graph handle over borrowed device arrays.
+ * Checks the descriptors on the host and the arrays on the device (indptr
+ * starts at 0, never decreases and ends at nnz; every index is a valid
+ * source), synchronising `stream` once.  Returns HG_EINVAL on a bad
+ * descriptor or array.  The handle may be used from several threads and
+ * streams at once (the graph is read-only, Sec. 4.2.1 ahead-of-time work on
+ * immutable data). */
+hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
+                    const hg_etype_desc *etypes, int32_t n_etypes,
+                    const hg_allocator *allocator, hipStream_t stream,
+                    hg_graph **out);
+
+/* Releases the handle and its workspaces (synchronises the device). */
+void hg_destroy(hg_graph *graph);
+
+/* One mini-batch (Sec. 3.2, Sec. 4.2.2).
+ * seeds: host array of n_ntypes device pointers; seeds[t] holds n_seeds[t]
+ *   int64 vertex IDs of type t, which must be unique and in range
+ *   (HG_EINVAL otherwise); seeds[t] may be NULL when n_seeds[t] == 0.
+ * n_seeds: host int64 [n_ntypes].
+ * fanouts: host int32 [n_hops * n_etypes], hop-major; hop 0 starts from the
+ *   seeds.  -1 keeps every in-edge, 0 none, K keeps min(deg, K).
+ * rng_seed: sigma of the random key.  The kept in-edges of a destination are
+ *   the K with the smallest (key, edge ID), key = output word (eid & 3) of
+ *   Philox4x32-10 at counter (g lo32, g hi32, hop, etype), g = eid >> 2,
+ *   with key (sigma lo32, sigma hi32).
+ * Block h: per node type, the destination list is the hop's frontier and the
+ *   source list is that frontier followed by the newly reached vertices in
+ *   ascending ID; per edge type, the edges grouped by destination in frontier
+ *   order and by ascending edge ID within a destination.  The source list of
+ *   block h is the frontier of hop h+1 (Sec. 4.2.2).
+ * On success *out owns every output array until hg_blocks_free.  On failure
+ *   nothing is returned and every intermediate is released. */
+hg_status hg_sample_blocks(hg_graph *graph, const int64_t *const *seeds,
+                           const int64_t *n_seeds, int32_t n_hops,
+                           const int32_t *fanouts, uint64_t rng_seed,
+                           hipStream_t stream, hg_blocks **out);
+
+/* hg_sample_blocks with only the top `key_bits` (1..32) bits of each key
+ * compared, ties still broken by edge ID.  key_bits = 32 is hg_sample_blocks.
+ * Small values make equal keys common; tests use it to exercise ties. */
+hg_status hg_sample_blocks_ex(hg_graph *graph, const int64_t *const *seeds,
+                              const int64_t *n_seeds, int32_t n_hops,
+                              const int32_t *fanouts, uint64_t rng_seed,
+                              int32_t key_bits, hipStream_t stream,
+                              hg_blocks **out);
+
+/* Number of hops of a blocks handle (-1 for NULL). */
+int32_t hg_blocks_num_hops(const hg_blocks *blocks);
+
+/* Vertices of node type `ntype` in block `hop`: n_dst frontier vertices and
+ * n_src source vertices; *src_gid: device int64 [n_src] whose first n_dst
+ * entries are the frontier (local ID = position). Owned by the handle. */
+hg_status hg_blocks_nodes(const hg_blocks *blocks, int32_t hop, int32_t ntype,
+                          int64_t *n_dst, int64_t *n_src,
+                          const int64_t **src_gid);
+
+/* Edges of edge type `etype` in block `hop`, all device, owned by the handle:
+ * indptr int64 [n_dst(dst_type) + 1] (block CSC by destination local ID),
+ * src_local / dst_local int32 [n_edges] (COO with local IDs), eid int64
+ * [n_edges] (edge IDs of the input graph).  Any output pointer may be NULL. */
+hg_status hg_blocks_edges(const hg_blocks *blocks, int32_t hop, int32_t etype,
+                          int64_t *n_edges, const int64_t **indptr,
+                          const int32_t **src_local, const int32_t **dst_local,
+                          const int64_t **eid);
+
+/* The input frontier of node type `ntype`: the source list of the last hop,
+ * or the seeds when n_hops == 0 (device int64 [n], owned by the handle).
+ * These are the rows the feature copy needs (Sec. 4.2.1). */
+hg_status hg_blocks_input_nodes(const hg_blocks *blocks, int32_t ntype,
+                                int64_t *n, const int64_t **gid);
+
+/* out[i, :] = feat_ntype[input_frontier[i], :], bits copied unchanged.
+ * out: device, caller-owned, [n_input(ntype), dim] of the type's dtype.
+ * HG_EINVAL for a featureless type.  Asynchronous on `stream`. */
+hg_status hg_gather_features(hg_graph *graph, const hg_blocks *blocks,
+                             int32_t ntype, void *out, hipStream_t stream);
+
+/* out[i, :] = feat_ntype[ids[i], :] for i < n (ids: device int64 [n]).
+ * Asynchronous; an id outside [0, num_nodes) yields a zero row. */
+hg_status hg_gather_rows(hg_graph *graph, int32_t ntype, const int64_t *ids,
+                         int64_t n, void *out, hipStream_t stream);
+
+/* Releases a blocks handle (stream-ordered on the stream it was made on). */
+void hg_blocks_free(hg_blocks *blocks);
+
+/* Thread-local description of the last failure on this thread. */
+const char *hg_last_error(void);
+
+/* Philox4x32-10 on the device: out[4i..4i+3] = Philox4x32-10 of counter
+ * ctr[4i..4i+3] under key (key lo32, key hi32), for i < n.
+ * ctr, out: device uint32 [4n].  Asynchronous.  Exposes the generator the
+ * sampler uses so that it can be checked on its own. */
+hg_status hg_debug_philox(const uint32_t *ctr, uint64_t key, int64_t n,
+                          uint32_t *out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HG_H */

@@ -1,0 +1,321 @@
+"""Python binding of libhg.so (include/hg.h): heterogeneous mini-batch
+generation on MI355X (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2).
+
+Argument marshalling only: every step of the path runs in the library's gfx950
+kernels.  PyTorch supplies device memory (the graph, feature tables, outputs)
+and the stream (the current torch stream).  Import fails loudly if the library
+is not built; there is no CPU path.
+
+    g = Graph(ntypes=[(num_nodes, feat_or_None), ...],
+              etypes=[(src_type, dst_type, indptr, indices), ...])
+    b = g.sample_blocks(seeds=[ids_or_None per node type], fanouts=[[K]*R]*H,
+                        rng_seed=0)
+    n_dst, src_gid = b.nodes(hop, ntype)
+    indptr, src_local, dst_local, eid = b.edges(hop, etype)
+    x = g.gather_features(b, ntype)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhg.so")
+
+HG_OK, HG_EINVAL, HG_ENOMEM, HG_EDEVICE, HG_EUNSUPPORTED = 0, -1, -2, -3, -4
+HG_DT_NONE, HG_DT_F32, HG_DT_F16, HG_DT_BF16 = 0, 1, 2, 3
+_DTYPE_CODE = {torch.float32: HG_DT_F32, torch.float16: HG_DT_F16,
+               torch.bfloat16: HG_DT_BF16}
+
+# Every entry point declared in include/hg.h.
+ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_ex",
+               "hg_blocks_num_hops", "hg_blocks_nodes", "hg_blocks_edges",
+               "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_rows",
+               "hg_blocks_free", "hg_last_error", "hg_debug_philox")
+
+
+class HGError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"hg status {status}: {message}")
+        self.status = status
+
+
+class NTypeDesc(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_int64), ("feat", ctypes.c_void_p),
+                ("dtype", ctypes.c_int32), ("dim", ctypes.c_int32)]
+
+
+class ETypeDesc(ctypes.Structure):
+    _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
+                ("nnz", ctypes.c_int64), ("indptr", ctypes.c_void_p),
+                ("indices", ctypes.c_void_p)]
+
+
+ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
+FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class Allocator(ctypes.Structure):
+    _fields_ = [("ctx", ctypes.c_void_p), ("alloc", ALLOC_FN), ("free", FREE_FN)]
+
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_PP = ctypes.POINTER(ctypes.c_void_p)
+_PI64 = ctypes.POINTER(ctypes.c_int64)
+
+
+def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
+    sig = {
+        "hg_create": ([_P, _I32, _P, _I32, _P, _P, _PP], _I32),
+        "hg_destroy": ([_P], None),
+        "hg_sample_blocks": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _PP], _I32),
+        "hg_sample_blocks_ex": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _I32, _P, _PP], _I32),
+        "hg_blocks_num_hops": ([_P], _I32),
+        "hg_blocks_nodes": ([_P, _I32, _I32, _PI64, _PI64, _PP], _I32),
+        "hg_blocks_edges": ([_P, _I32, _I32, _PI64, _PP, _PP, _PP, _PP], _I32),
+        "hg_blocks_input_nodes": ([_P, _I32, _PI64, _PP], _I32),
+        "hg_gather_features": ([_P, _P, _I32, _P, _P], _I32),
+        "hg_gather_rows": ([_P, _I32, _P, _I64, _P, _P], _I32),
+        "hg_blocks_free": ([_P], None),
+        "hg_last_error": ([], ctypes.c_char_p),
+        "hg_debug_philox": ([_P, ctypes.c_uint64, _I64, _P, _P], _I32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libhg.so; raises if it has not been built (no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise ImportError(f"{path} is missing: build it with "
+                              "`python -m paper_2112_15345_amd.build`")
+        _lib = _bind(ctypes.CDLL(path))
+    return _lib
+
+
+def _check(st: int):
+    if st != HG_OK:
+        raise HGError(st, load_library().hg_last_error().decode(errors="replace"))
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _dev_i64(x, device) -> torch.Tensor:
+    t = torch.as_tensor(x, dtype=torch.int64, device=device)
+    return t.contiguous()
+
+
+class _DeviceArray:
+    """Presents library-owned device memory through __cuda_array_interface__;
+    holds a reference to the owning handle so that it outlives the view."""
+
+    def __init__(self, ptr: int, n: int, typestr: str, owner):
+        self.__cuda_array_interface__ = {"shape": (n,), "typestr": typestr,
+                                         "data": (ptr, False), "version": 3,
+                                         "strides": None, "stream": None}
+        self._owner = owner
+
+
+_TYPESTR = {torch.int64: "<i8", torch.int32: "<i4"}
+
+
+def _view(ptr: int, n: int, dtype, owner, device) -> torch.Tensor:
+    if n == 0 or not ptr:
+        return torch.empty(0, dtype=dtype, device=device)
+    return torch.as_tensor(_DeviceArray(ptr, n, _TYPESTR[dtype], owner), device=device)
+
+
+class Blocks:
+    """The blocks of one mini-batch; owns the library's output arrays."""
+
+    def __init__(self, graph: "Graph", handle: ctypes.c_void_p, n_hops: int):
+        self.graph = graph
+        self._h = handle
+        self.n_hops = n_hops
+        self.device = graph.device
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.hg_blocks_free(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    def nodes(self, hop: int, ntype: int):
+        """(n_dst, src_gid): src_gid[:n_dst] is the frontier of this hop."""
+        nd, ns, p = _I64(), _I64(), ctypes.c_void_p()
+        _check(load_library().hg_blocks_nodes(self._h, hop, ntype, ctypes.byref(nd),
+                                              ctypes.byref(ns), ctypes.byref(p)))
+        return nd.value, _view(p.value, ns.value, torch.int64, self, self.device)
+
+    def edges(self, hop: int, etype: int):
+        """(indptr, src_local, dst_local, eid) of one edge type in block `hop`."""
+        ne = _I64()
+        pi, ps, pd, pe = (ctypes.c_void_p() for _ in range(4))
+        _check(load_library().hg_blocks_edges(self._h, hop, etype, ctypes.byref(ne),
+                                              ctypes.byref(pi), ctypes.byref(ps),
+                                              ctypes.byref(pd), ctypes.byref(pe)))
+        d = self.graph.etypes[etype][1]
+        n_dst = self.nodes(hop, d)[0]
+        return (_view(pi.value, n_dst + 1, torch.int64, self, self.device),
+                _view(ps.value, ne.value, torch.int32, self, self.device),
+                _view(pd.value, ne.value, torch.int32, self, self.device),
+                _view(pe.value, ne.value, torch.int64, self, self.device))
+
+    def num_edges(self, hop: int, etype: int) -> int:
+        ne = _I64()
+        _check(load_library().hg_blocks_edges(self._h, hop, etype, ctypes.byref(ne),
+                                              None, None, None, None))
+        return ne.value
+
+    def input_nodes(self, ntype: int) -> torch.Tensor:
+        n, p = _I64(), ctypes.c_void_p()
+        _check(load_library().hg_blocks_input_nodes(self._h, ntype, ctypes.byref(n),
+                                                    ctypes.byref(p)))
+        return _view(p.value, n.value, torch.int64, self, self.device)
+
+    def num_input_nodes(self, ntype: int) -> int:
+        n = _I64()
+        _check(load_library().hg_blocks_input_nodes(self._h, ntype, ctypes.byref(n), None))
+        return n.value
+
+
+class Graph:
+    """An immutable heterograph over borrowed device tensors.
+
+    ntypes: [(num_nodes, feat)] with feat a contiguous [num_nodes, dim] float32 /
+    float16 / bfloat16 device tensor or None.  etypes: [(src_type, dst_type,
+    indptr, indices)] with int64 device tensors (CSC keyed by destination)."""
+
+    def __init__(self, ntypes, etypes, device=None, allocator: Allocator | None = None,
+                 stream=None):
+        lib = load_library()
+        self.device = torch.device(device or "cuda")
+        self.ntypes = []
+        self.etypes = []
+        nt = (NTypeDesc * max(len(ntypes), 1))()
+        et = (ETypeDesc * max(len(etypes), 1))()
+        for t, (n, feat) in enumerate(ntypes):
+            if feat is not None:
+                if not feat.is_contiguous() or feat.dim() != 2 or feat.shape[0] != n:
+                    raise ValueError(f"node type {t}: features must be contiguous [n, dim]")
+                if feat.dtype not in _DTYPE_CODE:
+                    raise ValueError(f"node type {t}: unsupported dtype {feat.dtype}")
+                nt[t] = NTypeDesc(int(n), feat.data_ptr() if feat.numel() else None,
+                                  _DTYPE_CODE[feat.dtype], int(feat.shape[1]))
+            else:
+                nt[t] = NTypeDesc(int(n), None, HG_DT_NONE, 0)
+            self.ntypes.append((int(n), feat))
+        for e, (s, d, indptr, indices) in enumerate(etypes):
+            indptr = _dev_i64(indptr, self.device)
+            indices = _dev_i64(indices, self.device)
+            et[e] = ETypeDesc(int(s), int(d), int(indices.numel()), indptr.data_ptr(),
+                              indices.data_ptr() if indices.numel() else None)
+            self.etypes.append((int(s), int(d), indptr, indices))
+        self._allocator = allocator
+        h = ctypes.c_void_p()
+        _check(lib.hg_create(ctypes.addressof(nt), len(ntypes), ctypes.addressof(et),
+                             len(etypes),
+                             ctypes.addressof(allocator) if allocator is not None else None,
+                             _stream(stream), ctypes.byref(h)))
+        self._h = h
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.hg_destroy(h)
+            self._h = None
+
+    @property
+    def T(self) -> int:
+        return len(self.ntypes)
+
+    @property
+    def R(self) -> int:
+        return len(self.etypes)
+
+    def sample_blocks(self, seeds, fanouts, rng_seed: int = 0, key_bits: int = 32,
+                      stream=None) -> Blocks:
+        """seeds: per node type an int64 device tensor or None; fanouts:
+        [n_hops][n_etypes] (hop 0 starts from the seeds; -1 = all)."""
+        lib = load_library()
+        T, R = self.T, self.R
+        if len(seeds) != T:
+            raise ValueError("one seed entry per node type")
+        keep = []
+        ptrs = (ctypes.c_void_p * T)()
+        counts = (ctypes.c_int64 * T)()
+        for t, s in enumerate(seeds):
+            if s is None:
+                counts[t] = 0
+                continue
+            s = _dev_i64(s, self.device)
+            keep.append(s)
+            counts[t] = s.numel()
+            ptrs[t] = s.data_ptr() if s.numel() else None
+        H = len(fanouts)
+        flat = [int(k) for row in fanouts for k in row]
+        if len(flat) != H * R:
+            raise ValueError("fanouts must be [n_hops][n_etypes]")
+        fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        h = ctypes.c_void_p()
+        _check(lib.hg_sample_blocks_ex(self._h, ptrs, counts, H, fo, int(rng_seed) & (2**64 - 1),
+                                       int(key_bits), _stream(stream), ctypes.byref(h)))
+        return Blocks(self, h, H)
+
+    def gather_features(self, blocks: Blocks, ntype: int, out: torch.Tensor | None = None,
+                        stream=None) -> torch.Tensor:
+        n, feat = self.ntypes[ntype]
+        if feat is None:
+            raise HGError(HG_EINVAL, f"node type {ntype} has no features")
+        rows = blocks.num_input_nodes(ntype)
+        if out is None:
+            out = torch.empty((rows, feat.shape[1]), dtype=feat.dtype, device=self.device)
+        _check(load_library().hg_gather_features(self._h, blocks.handle, ntype,
+                                                 out.data_ptr() if out.numel() else None,
+                                                 _stream(stream)))
+        return out
+
+    def gather_rows(self, ntype: int, ids: torch.Tensor, out: torch.Tensor | None = None,
+                    stream=None) -> torch.Tensor:
+        n, feat = self.ntypes[ntype]
+        ids = _dev_i64(ids, self.device)
+        if out is None:
+            if feat is None:
+                raise HGError(HG_EINVAL, f"node type {ntype} has no features")
+            out = torch.empty((ids.numel(), feat.shape[1]), dtype=feat.dtype, device=self.device)
+        _check(load_library().hg_gather_rows(self._h, ntype,
+                                             ids.data_ptr() if ids.numel() else None,
+                                             ids.numel(),
+                                             out.data_ptr() if out.numel() else None,
+                                             _stream(stream)))
+        return out
+
+
+def debug_philox(ctr: torch.Tensor, key: int, stream=None) -> torch.Tensor:
+    """Philox4x32-10 of each row of a [n, 4] counter tensor (int32 bits)."""
+    ctr = ctr.contiguous()
+    out = torch.empty_like(ctr)
+    _check(load_library().hg_debug_philox(ctr.data_ptr() if ctr.numel() else None,
+                                          int(key) & (2**64 - 1), ctr.shape[0],
+                                          out.data_ptr() if out.numel() else None,
+                                          _stream(stream)))
+    return out

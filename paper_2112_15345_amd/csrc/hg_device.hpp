@@ -1,0 +1,113 @@
+// Device-side helpers for the gfx950 kernels: 64-lane wavefront primitives,
+// segment lookup and the Philox4x32-10 counter-based generator.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace hg {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Bit mask of the lanes below this one.
+__device__ __forceinline__ uint64_t lanes_below() {
+  return (uint64_t(1) << lane_id()) - 1;
+}
+
+// Orders LDS traffic between the lanes of one wavefront (no block barrier).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Exclusive prefix over the lanes of a small per-lane count (0..7) and the
+// wave total, from three ballots.
+__device__ __forceinline__ int wave_prefix_small(int v, int *total) {
+  const uint64_t below = lanes_below();
+  const uint64_t b0 = __ballot(v & 1);
+  const uint64_t b1 = __ballot(v & 2);
+  const uint64_t b2 = __ballot(v & 4);
+  *total = __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2);
+  return __popcll(b0 & below) + 2 * __popcll(b1 & below) +
+         4 * __popcll(b2 & below);
+}
+
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, kWave);
+  return v;
+}
+
+// Inclusive scan over the lanes of a wavefront.
+__device__ __forceinline__ int64_t wave_incl_scan_i64(int64_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t o = __shfl_up(v, d, kWave);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Exclusive scan of one value per thread over a 256-thread block; returns the
+// thread's exclusive prefix and writes the block total.  `lds` holds 4 int64.
+__device__ __forceinline__ int64_t block_excl_scan_256(int64_t v, int64_t *lds,
+                                                       int64_t *total) {
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int64_t inc = wave_incl_scan_i64(v);
+  if (lane == kWave - 1) lds[wave] = inc;
+  __syncthreads();
+  int64_t before = 0, sum = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int64_t s = lds[w];
+    if (w < wave) before += s;
+    sum += s;
+  }
+  __syncthreads();
+  *total = sum;
+  return before + inc - v;
+}
+
+// Largest s in [0, n) with base[s] <= x, for a non-decreasing base[0..n]
+// with base[0] <= x < base[n]: the segment that holds item x.
+__device__ __forceinline__ int find_segment(const int64_t *base, int n,
+                                            int64_t x) {
+  int lo = 0, hi = n;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (base[mid] <= x)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32
+// multiplies, with the round key advanced by the Weyl constants.
+struct U32x4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ U32x4 philox4x32_10(U32x4 c, uint32_t k0,
+                                               uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = U32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+}  // namespace hg

@@ -1,0 +1,61 @@
+"""Runs the HIP path and the oracle on the same inputs and compares them."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2112_15345_amd as hg
+
+
+def gpu_graph(nn, etypes, feats, device="cuda"):
+    nts = []
+    for n, f in zip(nn, feats):
+        nts.append((n, None if f is None else torch.as_tensor(f).to(device).contiguous()))
+    ets = [(s, d, torch.as_tensor(ip, device=device), torch.as_tensor(ix, device=device))
+           for s, d, ip, ix in etypes]
+    return hg.Graph(nts, ets, device=device)
+
+
+def result_dict(graph: hg.Graph, blocks: hg.Blocks):
+    """Copies every output of a Blocks handle to numpy (oracle result layout)."""
+    torch.cuda.synchronize()
+    res = {"n_hops": blocks.n_hops, "nodes": {}, "edges": {}, "input": {}}
+    for h in range(blocks.n_hops):
+        for t in range(graph.T):
+            nd, sg = blocks.nodes(h, t)
+            res["nodes"][(h, t)] = (nd, sg.cpu().numpy())
+        for e in range(graph.R):
+            res["edges"][(h, e)] = tuple(a.cpu().numpy() for a in blocks.edges(h, e))
+    for t in range(graph.T):
+        res["input"][t] = blocks.input_nodes(t).cpu().numpy()
+    return res
+
+
+def gpu_seeds(seeds, device="cuda"):
+    return [None if s is None else torch.as_tensor(np.asarray(s, np.int64), device=device)
+            for s in seeds]
+
+
+def compare(ref, got, T, R, H):
+    """Element-by-element comparison; returns a list of differences."""
+    diffs = []
+    for h in range(H):
+        for t in range(T):
+            a, b = ref["nodes"][(h, t)], got["nodes"][(h, t)]
+            if a[0] != b[0] or not np.array_equal(a[1], b[1]):
+                diffs.append(f"hop {h} type {t}: n_dst {a[0]}/{b[0]}, n_src {a[1].size}/{b[1].size}")
+        for e in range(R):
+            for name, x, y in zip(("indptr", "src_local", "dst_local", "eid"),
+                                  ref["edges"][(h, e)], got["edges"][(h, e)]):
+                if x.dtype != y.dtype or not np.array_equal(x, y):
+                    first = None
+                    if x.shape == y.shape:
+                        bad = np.nonzero(x != y)[0]
+                        first = int(bad[0]) if bad.size else None
+                    diffs.append(f"hop {h} etype {e} {name}: sizes {x.size}/{y.size}, "
+                                 f"dtypes {x.dtype}/{y.dtype}, first mismatch at {first}")
+    for t in range(T):
+        if not np.array_equal(ref["input"][t], got["input"][t]):
+            diffs.append(f"input frontier of type {t} differs")
+    return diffs

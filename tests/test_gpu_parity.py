@@ -1,0 +1,235 @@
+"""HIP path (through the C ABI) against the CPU oracle, element by element, on
+random tiny heterographs and the tiny workload.  All outputs are integers or
+copied bits, so the bar is exact equality."""
+import ctypes
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2112_15345_amd as hg
+import pins
+import workloads as W
+from gpu_harness import compare, gpu_graph, gpu_seeds, result_dict
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def olib():
+    return oracle.load()
+
+
+def test_philox_device_matches_oracle(olib):
+    rng = np.random.default_rng(1)
+    n = 4096
+    ctr = rng.integers(0, 1 << 32, size=(n, 4), dtype=np.uint64).astype(np.uint32)
+    ctr[0] = 0
+    ctr[1] = 0xFFFFFFFF
+    key = int(rng.integers(0, 1 << 63)) * 2 + 1
+    got = hg.debug_philox(torch.as_tensor(ctr.view(np.int32), device="cuda"), key)
+    got = got.cpu().numpy().view(np.uint32)
+    for i in range(0, n, 97):
+        ref = oracle.philox4x32_10(ctr[i], [key & 0xFFFFFFFF, key >> 32], olib)
+        assert np.array_equal(got[i], ref), f"counter {ctr[i]}"
+    # and all of them against rocRAND's key definition for the zero-key case
+    z = hg.debug_philox(torch.zeros((1, 4), dtype=torch.int32, device="cuda"), 0)
+    assert np.array_equal(z.cpu().numpy().view(np.uint32)[0], pins.rr_block(0, 0, 0))
+
+
+def run_both(olib, nn, ets, feats, seeds, fanouts, sigma, bits):
+    g = gpu_graph(nn, ets, feats)
+    b = g.sample_blocks(gpu_seeds(seeds), fanouts, sigma, key_bits=bits)
+    got = result_dict(g, b)
+    ref = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib).sample_blocks(seeds, fanouts,
+                                                                              sigma, bits)
+    return g, b, ref, got
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_random_heterographs(olib, chunk):
+    rng = np.random.default_rng(1000 + chunk)
+    for c in range(40):
+        case = pins.random_case(rng, max_nodes=60, max_deg=40)
+        nn, ets, feats, seeds, fanouts, sigma, bits = case
+        say(f"chunk {chunk} case {c}: T={len(nn)} R={len(ets)} H={len(fanouts)} bits={bits}")
+        g, b, ref, got = run_both(olib, *case)
+        diffs = compare(ref, got, len(nn), len(ets), len(fanouts))
+        assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
+        fails = pins.check_blocks(nn, ets, seeds, fanouts, sigma, bits, got, brute=False)
+        assert not fails, "\n".join(fails[:5])
+        # gather of the input frontier, every type with features
+        for t, f in enumerate(feats):
+            if f is None:
+                with pytest.raises(hg.HGError):
+                    g.gather_features(b, t)
+                continue
+            x = g.gather_features(b, t).cpu().numpy()
+            assert x.tobytes() == f[got["input"][t]].tobytes()
+
+
+def hub_graph(deg, n_src=None, extra=(3, 0, 7)):
+    """One node type; destination 0 has `deg` in-edges, a few small ones follow."""
+    n_src = n_src or deg + 10
+    degs = [deg, *extra]
+    indptr = np.concatenate([[0], np.cumsum(degs)]).astype(np.int64)
+    rng = np.random.default_rng(deg)
+    idx = np.concatenate([np.sort(rng.choice(n_src, size=d, replace=False)) for d in degs])
+    n = max(n_src, len(degs))
+    indptr = np.concatenate([indptr, np.full(n - len(degs), indptr[-1])]).astype(np.int64)
+    return [n], [(0, 0, indptr, idx.astype(np.int64))], [None]
+
+
+@pytest.mark.parametrize("deg,k,bits", [
+    (700, 5, 32), (5000, 25, 32), (70000, 15, 32),      # candidate path
+    (3000, 5, 2), (3000, 5, 1), (1200, 600, 32),        # bisection fallback
+    (2000, 400, 4), (640, 639, 32), (64, 63, 32), (65, 64, 32),
+])
+def test_hub_selection(olib, deg, k, bits):
+    nn, ets, feats = hub_graph(deg)
+    seeds = [np.array([0, 1, 2, 3], np.int64)]
+    for sigma in (0, 1, 2**40 + 3):
+        say(f"hub deg={deg} K={k} bits={bits} sigma={sigma}")
+        g, b, ref, got = run_both(olib, nn, ets, feats, seeds, [[k], [k]], sigma, bits)
+        diffs = compare(ref, got, 1, 1, 2)
+        assert not diffs, "\n".join(diffs)
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
+def test_forced_ties(olib, bits):
+    rng = np.random.default_rng(77 + bits)
+    for c in range(15):
+        nn, ets, feats, seeds, fanouts, sigma, _ = pins.random_case(rng, max_nodes=80, max_deg=70)
+        say(f"ties bits={bits} case {c}")
+        g, b, ref, got = run_both(olib, nn, ets, feats, seeds, fanouts, sigma, bits)
+        diffs = compare(ref, got, len(nn), len(ets), len(fanouts))
+        assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
+
+
+def test_tiny_workload_batches(olib):
+    wl = W.WORKLOADS[1]
+    gen = W.make_graph(wl)
+    hgraph = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), lib=olib)
+    g = hg.Graph([(n, f.cuda()) for n, f in zip(gen.num_nodes, gen.feats)],
+                 [(s, d, ip.cuda(), ix.cuda()) for s, d, ip, ix in gen.etypes])
+    for bno in range(10):
+        seeds = W.seeds_per_type(wl, bno)
+        say(f"tiny workload batch {bno}")
+        b = g.sample_blocks(gpu_seeds(seeds), wl.fanout_matrix(), bno)
+        got = result_dict(g, b)
+        ref = hgraph.sample_blocks(seeds, wl.fanout_matrix(), bno)
+        diffs = compare(ref, got, g.T, g.R, len(wl.fanouts))
+        assert not diffs, f"batch {bno}: " + "\n".join(diffs[:10])
+        for t in range(g.T):
+            x = g.gather_features(b, t).cpu().numpy()
+            assert x.tobytes() == hgraph.gather(t, ref["input"][t]).tobytes()
+
+
+def test_error_codes_match_oracle(olib):
+    indptr = np.array([0, 1, 3, 3], np.int64)
+    indices = np.array([2, 0, 1], np.int64)
+    g = gpu_graph([3], [(0, 0, indptr, indices)], [None])
+    ho = oracle.HostGraph([(3, None)], [(0, 0, indptr, indices)], lib=olib)
+    for seeds, fo, kb in [([[1, 1]], [[2]], 32), ([[3]], [[2]], 32), ([[-1]], [[2]], 32),
+                          ([[0]], [[-2]], 32), ([[0]], [[1]], 0), ([[0]], [[1]], 33),
+                          ([[0, 0]], [], 32)]:
+        with pytest.raises(oracle.OracleError) as eo:
+            ho.sample_blocks([np.array(seeds[0])], fo, 0, kb)
+        with pytest.raises(hg.HGError) as eg:
+            g.sample_blocks(gpu_seeds([np.array(seeds[0])]), fo, 0, key_bits=kb)
+        assert eo.value.status == eg.value.status == hg.HG_EINVAL
+    # a featureless type cannot be gathered
+    b = g.sample_blocks(gpu_seeds([np.array([0])]), [[1]], 0)
+    with pytest.raises(hg.HGError):
+        g.gather_features(b, 0)
+    # invalid CSC arrays are refused at creation
+    for ip, ix in [(np.array([0, 1, 3, 2]), indices), (indptr, np.array([2, 0, 3])),
+                   (np.array([1, 1, 3, 3]), indices)]:
+        with pytest.raises(hg.HGError) as e:
+            gpu_graph([3], [(0, 0, ip, ix)], [None])
+        assert e.value.status == hg.HG_EINVAL
+    # the graph still works after failed calls (map and bitmap left clean)
+    b = g.sample_blocks(gpu_seeds([np.array([1, 0])]), [[-1], [-1]], 3)
+    got = result_dict(g, b)
+    ref = ho.sample_blocks([np.array([1, 0])], [[-1], [-1]], 3)
+    assert not compare(ref, got, 1, 1, 2)
+
+
+def test_zero_hops_and_empty_seeds(olib):
+    rng = np.random.default_rng(5)
+    nn, ets, feats = W.random_hetero(rng, max_types=2, max_nodes=30)[:3]
+    seeds = [np.arange(min(3, n), dtype=np.int64) for n in nn]
+    for fanouts in ([], [[2] * len(ets)]):
+        g, b, ref, got = run_both(olib, nn, ets, feats, seeds, fanouts, 9, 32)
+        assert not compare(ref, got, len(nn), len(ets), len(fanouts))
+    empty = [np.zeros(0, np.int64) for _ in nn]
+    g, b, ref, got = run_both(olib, nn, ets, feats, empty, [[3] * len(ets)] * 2, 1, 32)
+    assert not compare(ref, got, len(nn), len(ets), 2)
+
+
+def test_determinism_and_two_streams(olib):
+    wl = W.WORKLOADS[1]
+    gen = W.make_graph(wl)
+    g = hg.Graph([(n, f.cuda()) for n, f in zip(gen.num_nodes, gen.feats)],
+                 [(s, d, ip.cuda(), ix.cuda()) for s, d, ip, ix in gen.etypes])
+    seeds = gpu_seeds(W.seeds_per_type(wl, 3))
+    first = result_dict(g, g.sample_blocks(seeds, wl.fanout_matrix(), 3))
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s1):
+        b1 = g.sample_blocks(seeds, wl.fanout_matrix(), 3, stream=s1)
+    with torch.cuda.stream(s2):
+        b2 = g.sample_blocks(seeds, wl.fanout_matrix(), 3, stream=s2)
+    torch.cuda.synchronize()
+    for b in (b1, b2):
+        assert not compare(first, result_dict(g, b), g.T, g.R, 2)
+
+
+def test_allocator_failure_releases_everything(olib):
+    """An allocator that fails after a few allocations: HG_ENOMEM, every block
+    it handed out is returned, and the graph keeps working."""
+    state = {"live": {}, "budget": 0, "allocs": 0}
+
+    def alloc(ctx, nbytes, stream):
+        if state["allocs"] >= state["budget"]:
+            return None
+        state["allocs"] += 1
+        t = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        state["live"][t.data_ptr()] = t
+        return t.data_ptr()
+
+    def free(ctx, ptr, stream):
+        state["live"].pop(ptr)
+
+    a = hg.Allocator(None, hg.ALLOC_FN(alloc), hg.FREE_FN(free))
+    rng = np.random.default_rng(3)
+    nn, ets, feats = W.random_hetero(rng, max_types=2, max_nodes=40)[:3]
+    nts = [(n, None if f is None else torch.as_tensor(f).cuda()) for n, f in zip(nn, feats)]
+    g = hg.Graph(nts, [(s, d, torch.as_tensor(ip).cuda(), torch.as_tensor(ix).cuda())
+                       for s, d, ip, ix in ets], allocator=a)
+    seeds = [np.arange(min(4, n), dtype=np.int64) for n in nn]
+    fo = [[3] * len(ets)] * 3
+    ref = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib).sample_blocks(seeds, fo, 11)
+    for budget in range(0, 12):
+        state.update(budget=budget, allocs=0)
+        try:
+            b = g.sample_blocks(gpu_seeds(seeds), fo, 11)
+        except hg.HGError as e:
+            assert e.status == hg.HG_ENOMEM
+            torch.cuda.synchronize()
+            assert not state["live"], f"budget {budget}: {len(state['live'])} blocks leaked"
+            continue
+        got = result_dict(g, b)
+        assert not compare(ref, got, len(nn), len(ets), 3)
+        del b
+        torch.cuda.synchronize()
+        assert not state["live"]
+        break
+    else:
+        pytest.fail("sampling never succeeded")
