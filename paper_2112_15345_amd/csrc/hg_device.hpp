@@ -6,6 +6,8 @@
 
 #include <cstdint>
 
+#include "hg_internal.hpp"
+
 namespace hg {
 
 constexpr int kWave = 64;
@@ -87,6 +89,81 @@ __device__ __forceinline__ int find_segment(const int64_t *base, int n,
       hi = mid;
   }
   return lo;
+}
+
+// Takes this block's tile of a single-pass scan: tiles are handed out in the
+// order blocks start, so every lower tile belongs to a block already running.
+__device__ __forceinline__ int64_t take_ticket(int64_t *small,
+                                               uint64_t ticket_base,
+                                               int64_t *lds) {
+  if (threadIdx.x == 0)
+    lds[0] = int64_t(atomicAdd(reinterpret_cast<unsigned long long *>(small + kSlotTicket),
+                               1ull) - ticket_base);
+  __syncthreads();
+  const int64_t t = lds[0];
+  __syncthreads();
+  return t;
+}
+
+// Upper bound on polls of one predecessor's flag (well under a second); past it
+// the scan gives up, flags kErrLookback and the call reports a device error.
+constexpr int kSpinLimit = 1 << 21;
+
+// Decoupled look-back (single-pass prefix scan) of NV int64 values for tile
+// `tile` of a segment whose first tile is `first`: publishes this tile's
+// aggregate, accumulates predecessors' aggregates until one publishes its
+// inclusive prefix, then publishes its own.  Returns the tile's exclusive
+// prefix in every thread.  `agg` must be the same in all threads.
+template <int NV>
+__device__ void tile_lookback(Lookback lb, int64_t tile, int64_t first,
+                              uint32_t epoch, const int64_t (&agg)[NV],
+                              int64_t (&excl)[NV], int64_t *small,
+                              int64_t *lds) {
+  if (threadIdx.x == 0) {
+    int64_t ex[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) ex[k] = 0;
+    int64_t *mine = lb.val + tile * 2 * NV;
+    if (tile > first) {
+#pragma unroll
+      for (int k = 0; k < NV; ++k) mine[k] = agg[k];
+      __threadfence();
+      __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 1u, __ATOMIC_RELEASE,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      for (int64_t j = tile - 1;; --j) {
+        uint32_t f = 0;
+        int spins = 0;
+        for (;;) {
+          f = __hip_atomic_load(&lb.flag[j], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+          if ((f >> 2) == epoch && (f & 3u) != 0) break;
+          if (++spins >= kSpinLimit) break;
+          __builtin_amdgcn_s_sleep(1);
+        }
+        if (spins >= kSpinLimit) {
+          atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), kErrLookback);
+          break;
+        }
+        const int64_t *v = lb.val + j * 2 * NV;
+        const bool inclusive = (f & 3u) == 2;
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+          ex[k] += __hip_atomic_load(v + (inclusive ? NV : 0) + k, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+        if (inclusive || j == first) break;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NV; ++k) mine[NV + k] = ex[k] + agg[k];
+    __threadfence();
+    __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 2u, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) lds[k] = ex[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NV; ++k) excl[k] = lds[k];
+  __syncthreads();
 }
 
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32

@@ -9,105 +9,144 @@
 
 namespace hg {
 
-// Items of one scan / bitmap tile: 256 threads x 8 items.
+// Bitmap tiles: 256 threads x 8 words.
 constexpr int kTileThreads = 256;
 constexpr int kTileItems = 8;
-constexpr int64_t kTile = int64_t(kTileThreads) * kTileItems;  // 2048
+constexpr int64_t kTile = int64_t(kTileThreads) * kTileItems;  // 2048 words
 
-// Candidate capacity of one wavefront's bottom-K selection (LDS entries).
+// Pair tiles of the counting pass: 256 threads x 2 pairs.
+constexpr int kPairItems = 2;
+constexpr int64_t kPairTile = int64_t(kTileThreads) * kPairItems;
+
+// Candidate capacity of one bottom-K selection (LDS entries per wavefront,
+// and per hub in the global candidate lists).
 constexpr int kCandCap = 512;
 
-// Per hop, per edge type: where the pairs (frontier vertex of the
-// destination type x edge type) of this edge type sit and what they read.
-struct HopEtype {
-  const int64_t *frontier;  // frontier of dst_type at this hop (device)
-  const int64_t *indptr;    // CSC of the edge type
+// Pairs whose in-edges are all kept and number at most this many are copied
+// by one thread each; larger ones by a wavefront.
+constexpr int64_t kThreadTakeAll = 32;
+
+// Pairs that keep K < deg edges with deg > kHubChunk ("hubs") are sampled in
+// chunks of kHubChunk edges, one wavefront per chunk.
+constexpr int64_t kHubChunk = 2048;
+
+// Readback slots of the small device buffer (int64 each).
+constexpr int kSlotErr = 0;     // error bits in the low int32
+constexpr int kSlotTicket = 1;  // tile tickets of the single-pass scans
+constexpr int kSlotDone = 2;    // finished blocks of the compaction pass
+constexpr int kSlotPairs = 3;   // pairs of the hop
+constexpr int kSlotEdges = 4;   // kept edges of the hop
+constexpr int kSlotHubs = 5;    // hub pairs
+constexpr int kSlotChunks = 6;  // hub chunks
+constexpr int kSlotWaves = 7;   // pairs sampled by one wavefront each
+constexpr int kSlotNew = 8;     // n_new[T], then ebase[R+1]
+
+constexpr int32_t kErrSeedRange = 1;   // a frontier vertex out of range
+constexpr int32_t kErrSeedRepeat = 2;  // a vertex twice in a frontier
+constexpr int32_t kErrLookback = 4;    // a scan wait exceeded its bound
+constexpr int32_t kErrBound = 8;       // more pairs than the launch was sized for
+
+// Static per edge type (per workspace).
+struct EtypeStatic {
+  const int64_t *indptr;
   const int64_t *indices;
-  int32_t *src_map;         // dense vertex -> local-ID map of src_type
-  uint32_t *src_bitmap;     // new-vertex bitmap of src_type
-  int64_t pair_base;        // global index of this etype's first pair
-  int64_t n_pairs;          // frontier size of dst_type
-  int64_t n_dst_nodes;      // vertex count of dst_type (range check)
-  int32_t fanout;           // -1 = all
+  int32_t *src_map;       // dense vertex -> local-ID map of the source type
+  uint32_t *src_bitmap;   // new-vertex bitmap of the source type
+  int64_t n_dst_nodes;
   int32_t src_type;
+  int32_t dst_type;
 };
 
-// Per hop, per node type.
-struct HopNtype {
-  const int64_t *frontier;  // current frontier (device)
-  int64_t n_frontier;
+// Static per node type (per workspace).
+struct TypeStatic {
+  int32_t *map;
+  uint32_t *bitmap;
   int64_t num_nodes;
-  int32_t *map;             // dense map of the type
-  int64_t *src_out;         // source list being built (frontier ++ new)
-  int64_t new_base;         // running offset of this type in a concatenation
+};
+
+// One hop, as device arrays.  Host-written: frontier, src_out, fanout.
+// nF and pair_base are written by the host for hop 0 and by the previous
+// hop's compaction pass afterwards.
+struct HopView {
+  int64_t *nF;                  // [T] frontier sizes
+  int64_t *pair_base;           // [R+1] pairs of etype e: [pair_base[e], pair_base[e+1])
+  const int64_t *const *frontier;  // [T]
+  int64_t *const *src_out;      // [T] source lists of this hop (frontier ++ new)
+  const int32_t *fanout;        // [R]
+};
+
+// Status and values of a single-pass (decoupled look-back) scan of NV int64
+// values: per tile a flag (epoch << 2 | state, state 1 = aggregate ready,
+// 2 = inclusive prefix ready) and 2*NV values (aggregate, inclusive).
+struct Lookback {
+  uint32_t *flag;
+  int64_t *val;
+};
+
+// Per-pair arrays of one hop (device).  Offsets have n_items entries.
+struct PairArrays {
+  int64_t *plo;      // first in-edge slot
+  int64_t *pdeg;     // in-degree
+  int64_t *off;      // exclusive scan of kept edges
+  int64_t *choff;    // exclusive scan of hub chunks
+  int64_t *woff;     // exclusive scan of wavefront pairs
+  int64_t *hoff;     // exclusive scan of hub flags (= hub ID)
+  int32_t *hub_cnt;  // per hub: candidates appended
+  int32_t *hub_done; // per hub: chunks finished
 };
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
 
-// Seeds of hop 0: map[seed] = position; flags an out-of-range or repeated seed.
-hipError_t launch_insert_frontier(const HopNtype *types, const int64_t *type_base,
-                                  int32_t n_types, int64_t total, int32_t *err,
+// The hop-0 frontier: map[seed] = position; flags range errors and repeats.
+hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
+                                  int32_t n_types, int64_t total, int64_t *small,
                                   hipStream_t stream);
-// map[v] = -1 for every vertex of the given lists (in-range entries only).
-hipError_t launch_reset_map(const HopNtype *types, const int64_t *type_base,
-                            int32_t n_types, int64_t total, hipStream_t stream);
+// map[v] = -1 for every vertex of the hop's frontier (in-range entries only);
+// `bound` >= the frontier's total size, which is read on the device.
+hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
+                            int64_t bound, hipStream_t stream);
 
-// Per pair: its kept-edge count min(deg, K) (deg if K == -1), its first slot
-// and its degree.
-hipError_t launch_count(const HopEtype *et, const int64_t *pair_base,
-                        int32_t n_etypes, int64_t n_pairs, int64_t *cnt,
-                        int64_t *plo, int64_t *pdeg, int32_t *err,
-                        hipStream_t stream);
+// Counting pass over n_items >= P + 1 pair slots (P = pair_base[R]): per pair
+// its in-edge range; exclusive scans of kept edges, hub chunks, wavefront
+// pairs and hub flags; per-etype edge starts (ebase) and the hop totals into
+// `small`.  Single pass, tiles taken by ticket.
+int64_t count_tiles(int64_t n_items);
+hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
+                             int32_t n_types, int64_t n_items, PairArrays pa,
+                             Lookback lb, uint32_t epoch, uint64_t ticket_base,
+                             int64_t *small, hipStream_t stream);
 
-// out[0..n] = exclusive prefix sums of in[0..n-1]; out[n] = total.
-// `scratch` holds at least scan_scratch_elems(n) int64.
-int64_t scan_scratch_elems(int64_t n);
-hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out,
-                           int64_t *scratch, hipStream_t stream);
-
-// ebase[e] = off[pair_base[e]] for e <= n_etypes (edge start of each etype).
-hipError_t launch_edge_bases(const int64_t *pair_base, const int64_t *off,
-                             int32_t n_etypes, int64_t *ebase,
-                             hipStream_t stream);
-
-// The sampler: one wavefront per pair, writes the kept edges of the pair at
-// off[p]: source vertex, edge ID and destination local ID, and marks sources
-// that are not yet in the frontier in the bitmap.
-hipError_t launch_sample(const HopEtype *et, const int64_t *pair_base,
-                         int32_t n_etypes, int64_t n_pairs, const int64_t *cnt,
-                         const int64_t *plo, const int64_t *pdeg,
-                         const int64_t *off, uint64_t sigma, int32_t hop,
+// The sampler, one launch: block CSC entries and small take-all pairs (a
+// thread per pair), wavefront pairs (one wavefront each), hub chunks (one
+// wavefront each, the last chunk of a hub finishing its selection).  Writes
+// each pair's kept edges at off[p], grouped by pair, ascending edge ID;
+// marks sources not yet in the frontier in their type's bitmap.
+hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
+                         int32_t n_types, int64_t n_pairs, int64_t n_wave,
+                         int64_t n_chunks, PairArrays pa, uint64_t *cand,
+                         const int64_t *small, uint64_t sigma, int32_t hop,
                          int32_t key_bits, int64_t *src_gid, int64_t *eid,
-                         int32_t *dst_local, hipStream_t stream);
+                         int32_t *dst_local, int64_t *indptr_all,
+                         hipStream_t stream);
 
-// Block CSC per etype: indptr_all[pair_base[e] + e + i] =
-//   off[pair_base[e] + i] - off[pair_base[e]],  i = 0..n_pairs(e).
-hipError_t launch_block_indptr(const int64_t *pair_base, const int64_t *off,
-                               int32_t n_etypes, int64_t n_pairs,
-                               int64_t *indptr_all, hipStream_t stream);
+// Compaction pass, one launch: per bitmap tile, ranks of the set bits within
+// the node type (single-pass scan) -> local IDs n_frontier + rank, written to
+// the map and the source list, bits cleared; extra blocks copy the frontier
+// into the head of the source lists; the last block to finish writes n_new
+// and the next hop's frontier sizes and pair layout into `next`.
+hipError_t launch_compact(HopView hv, HopView next, const TypeStatic *ts,
+                          const EtypeStatic *es, int32_t n_types,
+                          int32_t n_etypes, uint32_t *bitmap,
+                          const int64_t *tile_base, int64_t n_tiles,
+                          int64_t copy_total, Lookback lb, uint32_t epoch,
+                          uint64_t ticket_base, uint64_t done_base,
+                          int64_t *small, int32_t *blocks_launched,
+                          hipStream_t stream);
 
-// Popcount of each 2048-word bitmap tile.
-hipError_t launch_bitmap_tile_counts(const uint32_t *bitmap, int64_t n_tiles,
-                                     int64_t *tile_cnt, hipStream_t stream);
-// Per node type t owning tiles [tile_base[t], tile_base[t+1]): exclusive scan
-// of its tile counts in place; n_new[t] = its total.
-hipError_t launch_bitmap_scan(int64_t *tile_cnt, const int64_t *tile_base,
-                              int32_t n_types, int64_t *n_new,
-                              hipStream_t stream);
-// For every set bit v of type t: local = n_frontier[t] + rank; map[v] = local;
-// src_out[local] = v; clears the tile.
-hipError_t launch_bitmap_assign(uint32_t *bitmap, int64_t n_tiles,
-                                const int64_t *tile_cnt,
-                                const int64_t *tile_base, const HopNtype *types,
-                                int32_t n_types, hipStream_t stream);
-// src_out[i] = frontier[i] for every type (the destination prefix).
-hipError_t launch_copy_frontier(const HopNtype *types, const int64_t *type_base,
-                                int32_t n_types, int64_t total,
-                                hipStream_t stream);
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
-// which are [ebase[e], ebase[e+1]).
-hipError_t launch_relabel(const HopEtype *et, const int64_t *ebase,
-                          int32_t n_etypes, int64_t n_edges,
+// which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.
+hipError_t launch_relabel(const EtypeStatic *es, const int64_t *small,
+                          int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
                           hipStream_t stream);
 

@@ -2,14 +2,16 @@
 // workspaces, per-hop orchestration of the gfx950 kernels, and error state.
 //
 // One mini-batch (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2.2) runs
-// hop by hop.  Per hop:
-//   1. count + scan   : kept-edge count of every (frontier vertex, etype)
-//                       pair and its output offset;      -> wait #1 (sizes)
-//   2. sample + mark  : the kept edges; new sources set a bitmap bit;
-//      block CSC, popcount scan of the bitmap;           -> wait #2 (sizes)
-//   3. assign + relabel: new vertices get local IDs in ascending ID order,
-//                       edges get local source IDs.
-// The source list of hop h is the frontier of hop h+1.
+// hop by hop, four launches per hop on the caller's stream:
+//   1. counting pass : per (frontier vertex, etype) pair its kept-edge count
+//                      and output offsets (single-pass scan)   -> wait (sizes)
+//   2. sampler       : the kept edges; new sources set a bitmap bit
+//   3. compaction    : new vertices numbered in ascending ID, frontier copied
+//                      to the head of the source lists; the last block plans
+//                      the next hop's pairs on the device
+//   4. relabel       : edges get local source IDs
+// The source list of hop h is the frontier of hop h+1.  The host waits once
+// per hop (after 1, for the output sizes) and once at the end.
 #include "hg.h"
 
 #include <algorithm>
@@ -47,6 +49,10 @@ hg_status fail_hip(hipError_t e, const char *what) {
   return fail(HG_EDEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Launch checks read the thread's last HIP error, so an error that other code
+// left pending on this thread is cleared when a call starts.
+void clear_pending_error() { (void)hipGetLastError(); }
+
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -79,17 +85,49 @@ struct ETypeInfo {
   const int64_t *indices;
 };
 
+// A device buffer that grows (stream-ordered) and is reused across calls.
+struct Scratch {
+  void *p = nullptr;
+  size_t cap = 0;
+  bool fresh = false;  // reallocated by the last ensure()
+  bool ensure(size_t bytes, hipStream_t s) {
+    fresh = false;
+    if (bytes <= cap) return true;
+    fresh = true;
+    if (p) (void)hipFreeAsync(p, s);
+    p = nullptr;
+    cap = 0;
+    const size_t want = align_up(std::max(bytes, bytes + bytes / 2));
+    if (hipMallocAsync(&p, want, s) != hipSuccess) {
+      (void)hipGetLastError();
+      p = nullptr;
+      return false;
+    }
+    cap = want;
+    return true;
+  }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    cap = 0;
+  }
+};
+
 // Per-call device state.  One call uses a workspace at a time; between calls
 // the map is all -1 and the bitmap all 0.
 struct Workspace {
-  int32_t *map = nullptr;        // sum of num_nodes
-  uint32_t *bitmap = nullptr;    // n_tiles * kTile words
-  int64_t *tile_cnt = nullptr;   // n_tiles + 1
-  int64_t *dsmall = nullptr;     // err | n_new[T] | ebase[R+1]
-  int64_t *hsmall = nullptr;     // pinned mirror of dsmall
-  char *dtab = nullptr;          // per-hop tables (device)
-  char *htab = nullptr;          // per-hop tables (pinned host)
-  size_t tab_cap = 0;
+  int32_t *map = nullptr;          // sum of num_nodes
+  uint32_t *bitmap = nullptr;      // n_tiles * kTile words
+  int64_t *dsmall = nullptr;       // readback slots
+  int64_t *hsmall = nullptr;       // pinned mirror of dsmall
+  EtypeStatic *d_es = nullptr;     // static per-etype table
+  TypeStatic *d_ts = nullptr;      // static per-type table
+  Lookback lb_bits{};              // look-back state of the compaction pass
+  Scratch tab;                     // per-hop tables (device)
+  char *htab = nullptr;            // per-hop tables (pinned host)
+  size_t htab_cap = 0;
+  Scratch pairs, lb_flags, lb_vals, edges, cand;
+  uint32_t epoch = 0;              // look-back launches so far
   hipEvent_t done = nullptr;
   bool busy = false;
 };
@@ -104,7 +142,7 @@ struct hg_graph {
   bool has_alloc = false;
   hg_allocator alloc{};
   std::vector<int64_t> map_off;    // [T+1]
-  std::vector<int64_t> tile_base;  // [T+1]
+  std::vector<int64_t> tile_base;  // [T+1] bitmap tiles of each type
   int64_t n_tiles = 0;
   int64_t *d_tile_base = nullptr;  // device copy of tile_base
   std::mutex mu;
@@ -131,6 +169,8 @@ struct hg_blocks {
 
 namespace {
 
+// Output arrays of a blocks handle: the caller's allocator, or the device's
+// stream-ordered pool.
 void *dev_alloc(hg_graph *g, size_t bytes, hipStream_t s) {
   bytes = align_up(bytes ? bytes : 1);
   if (g->has_alloc) return g->alloc.alloc(g->alloc.ctx, bytes, s);
@@ -150,42 +190,55 @@ void dev_free(hg_graph *g, void *p, hipStream_t s) {
     (void)hipFreeAsync(p, s);
 }
 
-// Several arrays carved out of one allocation.
-struct Arena {
+// Several arrays carved out of one buffer.
+struct Carve {
   struct Req {
     void **slot;
     size_t bytes;
   };
   std::vector<Req> reqs;
-  void *base = nullptr;
   template <typename T>
   void add(T **slot, int64_t n) {
     reqs.push_back({reinterpret_cast<void **>(slot),
                     align_up(size_t(std::max<int64_t>(n, 1)) * sizeof(T))});
   }
-  bool allocate(hg_graph *g, hipStream_t s) {
+  size_t bytes() const {
     size_t total = 0;
     for (auto &r : reqs) total += r.bytes;
-    base = dev_alloc(g, total, s);
-    if (!base) return false;
+    return total;
+  }
+  void assign(void *base) const {
     size_t off = 0;
     for (auto &r : reqs) {
       *r.slot = static_cast<char *>(base) + off;
       off += r.bytes;
     }
+  }
+  void *allocate(hg_graph *g, hipStream_t s) const {
+    void *base = dev_alloc(g, bytes(), s);
+    if (base) assign(base);
+    return base;
+  }
+  bool in_scratch(Scratch &sc, hipStream_t s) const {
+    if (!sc.ensure(bytes(), s)) return false;
+    assign(sc.p);
     return true;
   }
 };
 
-// Table layout of one region (one hop, or the seed/final steps).
+// Layout of one hop's table region: [nF T][pair_base R+1][frontier T]
+// [src_out T][fanout R].  The host writes frontier, src_out and fanout; nF
+// and pair_base come from the previous hop's compaction pass (the host
+// writes them for hop 0).
 struct RegionLayout {
-  size_t etype_off, pbase_off, ntype_off, tbase_off, size;
+  size_t nf, pbase, frontier, src_out, fanout, size;
   RegionLayout(int32_t T, int32_t R) {
-    etype_off = 0;
-    pbase_off = etype_off + align_up(sizeof(HopEtype) * size_t(std::max(R, 1)));
-    ntype_off = pbase_off + align_up(sizeof(int64_t) * size_t(R + 1));
-    tbase_off = ntype_off + align_up(sizeof(HopNtype) * size_t(T));
-    size = tbase_off + align_up(sizeof(int64_t) * size_t(T + 1));
+    nf = 0;
+    pbase = nf + sizeof(int64_t) * size_t(T);
+    frontier = pbase + sizeof(int64_t) * size_t(R + 1);
+    src_out = frontier + sizeof(int64_t) * size_t(T);
+    fanout = src_out + sizeof(int64_t) * size_t(T);
+    size = align_up(fanout + sizeof(int32_t) * size_t(std::max(R, 1)));
   }
 };
 
@@ -196,13 +249,23 @@ void free_workspace(Workspace *w) {
   }
   (void)hipFree(w->map);
   (void)hipFree(w->bitmap);
-  (void)hipFree(w->tile_cnt);
   (void)hipFree(w->dsmall);
-  (void)hipFree(w->dtab);
+  (void)hipFree(w->d_es);
+  (void)hipFree(w->d_ts);
+  (void)hipFree(w->lb_bits.flag);
+  (void)hipFree(w->lb_bits.val);
+  w->tab.release();
+  w->pairs.release();
+  w->lb_flags.release();
+  w->lb_vals.release();
+  w->edges.release();
+  w->cand.release();
   if (w->hsmall) (void)hipHostFree(w->hsmall);
   if (w->htab) (void)hipHostFree(w->htab);
   delete w;
 }
+
+size_t small_slots(const hg_graph *g) { return size_t(kSlotNew + g->T + g->R + 1); }
 
 // Takes a free workspace (or makes one) with table room for `tab_bytes`.
 hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
@@ -223,17 +286,38 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (!w) return fail(HG_ENOMEM, "workspace: out of host memory");
     fresh = true;
     const int64_t map_n = g->map_off[g->T];
-    const size_t small_n = size_t(1 + g->T + g->R + 1);
+    const size_t small_n = small_slots(g);
+    const int64_t n_lb = std::max<int64_t>(g->n_tiles, 1);
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(int32_t) * size_t(std::max<int64_t>(map_n, 1)));
     if (e == hipSuccess)
       e = hipMalloc(&w->bitmap, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
-    if (e == hipSuccess) e = hipMalloc(&w->tile_cnt, sizeof(int64_t) * size_t(g->n_tiles + 1));
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
+    if (e == hipSuccess) e = hipMalloc(&w->d_es, sizeof(EtypeStatic) * size_t(std::max(g->R, 1)));
+    if (e == hipSuccess) e = hipMalloc(&w->d_ts, sizeof(TypeStatic) * size_t(g->T));
+    if (e == hipSuccess) e = hipMalloc(&w->lb_bits.flag, sizeof(uint32_t) * size_t(n_lb));
+    if (e == hipSuccess) e = hipMalloc(&w->lb_bits.val, sizeof(int64_t) * 2 * size_t(n_lb));
     if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void **>(&w->hsmall), sizeof(int64_t) * small_n, 0);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming);
     if (e == hipSuccess) e = launch_fill_i32(w->map, map_n, -1, stream);
     if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
+    if (e == hipSuccess) e = launch_fill_u32(w->lb_bits.flag, n_lb, 0u, stream);
+    if (e == hipSuccess) {
+      std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
+      for (int32_t i = 0; i < g->R; ++i) {
+        const ETypeInfo &E = g->et[i];
+        es[i] = EtypeStatic{E.indptr, E.indices, w->map + g->map_off[E.src],
+                            w->bitmap + g->tile_base[E.src] * kTile,
+                            g->nt[E.dst].num_nodes, E.src, E.dst};
+      }
+      std::vector<TypeStatic> ts(g->T);
+      for (int32_t t = 0; t < g->T; ++t)
+        ts[t] = TypeStatic{w->map + g->map_off[t], w->bitmap + g->tile_base[t] * kTile,
+                           g->nt[t].num_nodes};
+      e = hipMemcpy(w->d_es, es.data(), sizeof(EtypeStatic) * es.size(), hipMemcpyHostToDevice);
+      if (e == hipSuccess)
+        e = hipMemcpy(w->d_ts, ts.data(), sizeof(TypeStatic) * ts.size(), hipMemcpyHostToDevice);
+    }
     if (e != hipSuccess) {
       free_workspace(w);
       return fail(HG_ENOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
@@ -247,25 +331,26 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
       return fail_hip(hipGetLastError(), "hipStreamWaitEvent");
     }
   }
-  if (w->tab_cap < tab_bytes) {
-    // the tables of any earlier call were consumed before that call returned
-    (void)hipFree(w->dtab);
+  bool ok = w->tab.ensure(tab_bytes, stream);
+  if (ok && w->htab_cap < tab_bytes) {
+    // tables of earlier calls were consumed before those calls returned
     if (w->htab) (void)hipHostFree(w->htab);
-    w->dtab = nullptr;
     w->htab = nullptr;
-    w->tab_cap = 0;
-    if (hipMalloc(&w->dtab, tab_bytes) != hipSuccess ||
-        hipHostMalloc(reinterpret_cast<void **>(&w->htab), tab_bytes, 0) != hipSuccess) {
-      (void)hipGetLastError();
-      if (fresh) {
-        free_workspace(w);
-      } else {
-        std::lock_guard<std::mutex> lk(g->mu);
-        w->busy = false;
-      }
-      return fail(HG_ENOMEM, "workspace tables: allocation failed");
+    w->htab_cap = 0;
+    if (hipHostMalloc(reinterpret_cast<void **>(&w->htab), tab_bytes, 0) == hipSuccess)
+      w->htab_cap = tab_bytes;
+    else
+      ok = false;
+  }
+  if (!ok) {
+    (void)hipGetLastError();
+    if (fresh) {
+      free_workspace(w);
+    } else {
+      std::lock_guard<std::mutex> lk(g->mu);
+      w->busy = false;
     }
-    w->tab_cap = tab_bytes;
+    return fail(HG_ENOMEM, "workspace tables: allocation failed");
   }
   if (fresh) {
     std::lock_guard<std::mutex> lk(g->mu);
@@ -303,13 +388,13 @@ struct SampleRun {
   int32_t key_bits;
   const int32_t *fanouts;
   RegionLayout lay;
+  uint64_t ticket_base = 0, done_base = 0;
 
-  std::vector<const int64_t *> F;   // current frontier per type
-  std::vector<int64_t> nF;
-  std::vector<void *> scratch;      // per-call temporaries
-  // vertex lists that cover every map entry set so far
-  std::vector<const int64_t *> map_lists;
-  std::vector<int64_t> map_list_n;
+  // the map holds the frontier of region `map_region` (at most map_bound
+  // vertices in all; the exact sizes are in the region) until the call ends;
+  // the bitmap is clean unless bitmap_dirty
+  int map_region = -1;
+  int64_t map_bound = 0;
   bool bitmap_dirty = false;
 
   SampleRun(hg_graph *g_, hipStream_t s, int32_t H_, const int32_t *fo,
@@ -317,63 +402,53 @@ struct SampleRun {
       : g(g_), stream(s), T(g_->T), R(g_->R), H(H_), sigma(sig), key_bits(kb),
         fanouts(fo), lay(g_->T, g_->R) {}
 
-  char *htab(int region) { return ws->htab + size_t(region) * lay.size; }
-  char *dtab(int region) { return ws->dtab + size_t(region) * lay.size; }
+  char *hreg(int r) { return ws->htab + size_t(r) * lay.size; }
+  char *dreg(int r) { return static_cast<char *>(ws->tab.p) + size_t(r) * lay.size; }
 
-  hipError_t upload(int region, size_t off, size_t bytes) {
-    return hipMemcpyAsync(dtab(region) + off, htab(region) + off, bytes,
-                          hipMemcpyHostToDevice, stream);
+  HopView view(int r) {
+    char *d = dreg(r);
+    return HopView{reinterpret_cast<int64_t *>(d + lay.nf),
+                   reinterpret_cast<int64_t *>(d + lay.pbase),
+                   reinterpret_cast<const int64_t *const *>(d + lay.frontier),
+                   reinterpret_cast<int64_t *const *>(d + lay.src_out),
+                   reinterpret_cast<const int32_t *>(d + lay.fanout)};
+  }
+  template <typename T>
+  T *hfield(int r, size_t off) { return reinterpret_cast<T *>(hreg(r) + off); }
+
+  hipError_t upload(size_t from, size_t to) {
+    return hipMemcpyAsync(static_cast<char *>(ws->tab.p) + from, ws->htab + from,
+                          to - from, hipMemcpyHostToDevice, stream);
   }
 
-  // Writes the per-type table of `region` for `lists` and uploads it.
-  hipError_t put_ntypes(int region, const std::vector<const int64_t *> &lists,
-                        const std::vector<int64_t> &n,
-                        const std::vector<int64_t *> &src_out, int64_t *total) {
-    HopNtype *ht = reinterpret_cast<HopNtype *>(htab(region) + lay.ntype_off);
-    int64_t *tb = reinterpret_cast<int64_t *>(htab(region) + lay.tbase_off);
-    int64_t acc = 0;
-    for (int32_t t = 0; t < T; ++t) {
-      ht[t].frontier = lists[t];
-      ht[t].n_frontier = n[t];
-      ht[t].num_nodes = g->nt[t].num_nodes;
-      ht[t].map = ws->map + g->map_off[t];
-      ht[t].src_out = src_out.empty() ? nullptr : src_out[t];
-      ht[t].new_base = 0;
-      tb[t] = acc;
-      acc += n[t];
-    }
-    tb[T] = acc;
-    *total = acc;
-    return upload(region, lay.ntype_off, lay.size - lay.ntype_off);
+  uint32_t next_epoch() {
+    ws->epoch = (ws->epoch + 1) & 0x3FFFFFFFu;
+    if (ws->epoch == 0) ws->epoch = 1;
+    return ws->epoch;
   }
 
-  hipError_t sync_small(size_t first, size_t count) {
-    hipError_t e = hipMemcpyAsync(ws->hsmall + first, ws->dsmall + first,
-                                  sizeof(int64_t) * count, hipMemcpyDeviceToHost,
-                                  stream);
+  hipError_t sync_small() {
+    hipError_t e = hipMemcpyAsync(ws->hsmall, ws->dsmall, sizeof(int64_t) * small_slots(g),
+                                  hipMemcpyDeviceToHost, stream);
     if (e != hipSuccess) return e;
     return hipStreamSynchronize(stream);
   }
 
-  void *alloc_scratch(size_t bytes) {
-    void *p = dev_alloc(g, bytes, stream);
-    if (p) scratch.push_back(p);
-    return p;
+  hg_status check_flags(const char *where) {
+    const int32_t err = int32_t(ws->hsmall[kSlotErr]);
+    if (err & (kErrSeedRange | kErrSeedRepeat))
+      return fail(HG_EINVAL, "seeds: out of range or repeated within a node type");
+    if (err)
+      return fail(HG_EDEVICE, "%s: device check failed (flags %d)", where, err);
+    return HG_OK;
   }
 
-  // Undoes the map and bitmap state; frees what the call took.
-  void cleanup(bool keep_blocks) {
+  // Undoes the map and bitmap state; releases the workspace.
+  void finish(bool ok) {
     if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
-    int64_t total = 0;
-    if (!map_lists.empty() &&
-        put_ntypes(H + 1, map_lists, map_list_n, {}, &total) == hipSuccess) {
-      (void)launch_reset_map(reinterpret_cast<const HopNtype *>(dtab(H + 1) + lay.ntype_off),
-                             reinterpret_cast<const int64_t *>(dtab(H + 1) + lay.tbase_off),
-                             T, total, stream);
-    }
-    for (void *p : scratch) dev_free(g, p, stream);
-    scratch.clear();
-    if (!keep_blocks && b) {
+    if (map_region >= 0)
+      (void)launch_reset_map(view(map_region), ws->d_ts, T, map_bound, stream);
+    if (!ok && b) {
       for (void *p : b->allocs) dev_free(g, p, stream);
       delete b;
       b = nullptr;
@@ -403,167 +478,205 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   b->in_n.assign(T, 0);
   b->in_gid.assign(T, nullptr);
 
-  F.assign(T, nullptr);
-  nF.assign(T, 0);
+  // ---- region 0: the seeds are the first frontier -------------------------
+  std::vector<int64_t> nF(T);
+  int64_t P = 0;
   for (int32_t t = 0; t < T; ++t) {
-    F[t] = n_seeds[t] > 0 ? seeds[t] : nullptr;
     nF[t] = n_seeds[t];
+    hfield<int64_t>(0, lay.nf)[t] = nF[t];
+    hfield<const int64_t *>(0, lay.frontier)[t] = n_seeds[t] > 0 ? seeds[t] : nullptr;
+    hfield<int64_t *>(0, lay.src_out)[t] = nullptr;
   }
+  for (int32_t i = 0; i < R; ++i) {
+    hfield<int64_t>(0, lay.pbase)[i] = P;
+    P += nF[g->et[i].dst];
+    hfield<int32_t>(0, lay.fanout)[i] = H > 0 ? fanouts[i] : 0;
+  }
+  hfield<int64_t>(0, lay.pbase)[R] = P;
+  int64_t n_items = P + 1;  // pair slots of the next counting pass
 
-  // ---- hop 0 frontier: insert the seeds into the map (checks them) -------
-  int32_t *err = reinterpret_cast<int32_t *>(ws->dsmall);
-  if ((e = launch_fill_i32(err, 2, 0, stream)) != hipSuccess) return fail_hip(e, "fill");
+  // the readback slots start at zero (tickets, error flags)
+  if ((e = launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall), 2 * int64_t(small_slots(g)), 0,
+                           stream)) != hipSuccess ||
+      (e = upload(0, lay.size)) != hipSuccess)
+    return fail_hip(e, "start");
   int64_t total = 0;
-  if ((e = put_ntypes(H, F, nF, {}, &total)) != hipSuccess) return fail_hip(e, "upload");
-  map_lists = F;
-  map_list_n = nF;
-  if ((e = launch_insert_frontier(
-           reinterpret_cast<const HopNtype *>(dtab(H) + lay.ntype_off),
-           reinterpret_cast<const int64_t *>(dtab(H) + lay.tbase_off), T, total,
-           err, stream)) != hipSuccess)
+  for (int64_t n : nF) total += n;
+  map_region = 0;
+  map_bound = total;
+  if ((e = launch_insert_frontier(view(0), ws->d_ts, T, total, ws->dsmall, stream)) != hipSuccess)
     return fail_hip(e, "insert seeds");
   if (H == 0) {
-    if ((e = sync_small(0, 1)) != hipSuccess) return fail_hip(e, "sync");
-    if (int32_t(ws->hsmall[0]) != 0)
-      return fail(HG_EINVAL, "seeds: out of range or repeated within a node type");
+    if ((e = sync_small()) != hipSuccess) return fail_hip(e, "sync");
+    hg_status st = check_flags("seeds");
+    if (st != HG_OK) return st;
   }
 
-  const size_t o_new = 1, o_ebase = 1 + size_t(T);
   for (int32_t h = 0; h < H; ++h) {
-    // ---- 1. pair table, count, scan -----------------------------------
-    HopEtype *het = reinterpret_cast<HopEtype *>(htab(h) + lay.etype_off);
-    int64_t *pb = reinterpret_cast<int64_t *>(htab(h) + lay.pbase_off);
-    int64_t P = 0;
-    for (int32_t ei = 0; ei < R; ++ei) {
-      const ETypeInfo &E = g->et[ei];
-      het[ei].frontier = F[E.dst];
-      het[ei].indptr = E.indptr;
-      het[ei].indices = E.indices;
-      het[ei].src_map = ws->map + g->map_off[E.src];
-      het[ei].src_bitmap = ws->bitmap + g->tile_base[E.src] * kTile;
-      het[ei].pair_base = P;
-      het[ei].n_pairs = nF[E.dst];
-      het[ei].n_dst_nodes = g->nt[E.dst].num_nodes;
-      het[ei].fanout = fanouts[size_t(h) * R + ei];
-      het[ei].src_type = E.src;
-      pb[ei] = P;
-      P += nF[E.dst];
+    const HopView hv = view(h), nv = view(h + 1);
+    // ---- 1. counting pass over at most n_items pair slots ----------------
+    const int64_t tiles = count_tiles(n_items);
+    Carve pc;
+    PairArrays pa;
+    pc.add(&pa.plo, n_items);
+    pc.add(&pa.pdeg, n_items);
+    pc.add(&pa.off, n_items);
+    pc.add(&pa.choff, n_items);
+    pc.add(&pa.woff, n_items);
+    pc.add(&pa.hoff, n_items);
+    pc.add(&pa.hub_cnt, n_items);
+    pc.add(&pa.hub_done, n_items);
+    Lookback lb;
+    if (!pc.in_scratch(ws->pairs, stream) ||
+        !ws->lb_flags.ensure(sizeof(uint32_t) * size_t(tiles), stream) ||
+        !ws->lb_vals.ensure(sizeof(int64_t) * 8 * size_t(tiles), stream))
+      return fail(HG_ENOMEM, "hop %d: pair scratch", h);
+    lb.flag = static_cast<uint32_t *>(ws->lb_flags.p);
+    lb.val = static_cast<int64_t *>(ws->lb_vals.p);
+    // a new flag buffer starts with no tile published
+    if (ws->lb_flags.fresh &&
+        (e = launch_fill_u32(lb.flag, int64_t(ws->lb_flags.cap / sizeof(uint32_t)), 0u,
+                             stream)) != hipSuccess)
+      return fail_hip(e, "fill");
+    if ((e = launch_count_scan(hv, ws->d_es, R, T, n_items, pa, lb, next_epoch(), ticket_base,
+                               ws->dsmall, stream)) != hipSuccess)
+      return fail_hip(e, "count");
+    ticket_base += uint64_t(tiles);
+    // wait: this hop's sizes (and the previous hop's new-vertex counts)
+    if ((e = sync_small()) != hipSuccess) return fail_hip(e, "sync");
+    hg_status st = check_flags("count");
+    if (st != HG_OK) return st;
+    const int64_t *hs = ws->hsmall;
+    if (h > 0) {
+      // close the previous hop: its source lists are this hop's frontier
+      for (int32_t t = 0; t < T; ++t) {
+        const int64_t u = hs[kSlotNew + t];
+        const size_t k = size_t(h - 1) * T + t;
+        b->n_src[k] = b->n_dst[k] + u;
+        nF[t] = b->n_src[k];
+        if (nF[t] > INT32_MAX)
+          return fail(HG_EUNSUPPORTED, "hop %d: more than 2^31-1 vertices of type %d", h - 1, t);
+      }
     }
-    pb[R] = P;
-    if ((e = upload(h, 0, lay.ntype_off)) != hipSuccess) return fail_hip(e, "upload");
-    const HopEtype *d_et = reinterpret_cast<const HopEtype *>(dtab(h) + lay.etype_off);
-    const int64_t *d_pb = reinterpret_cast<const int64_t *>(dtab(h) + lay.pbase_off);
+    // pair layout of this hop (the device computed the same from the sizes)
+    std::vector<int64_t> pb(R + 1, 0);
+    for (int32_t i = 0; i < R; ++i) pb[i + 1] = pb[i] + nF[g->et[i].dst];
+    P = hs[kSlotPairs];
+    if (P != pb[R]) return fail(HG_EDEVICE, "hop %d: pair count mismatch", h);
+    const int64_t S = hs[kSlotEdges];
+    const int64_t n_hubs = hs[kSlotHubs], n_chunks = hs[kSlotChunks], n_wave = hs[kSlotWaves];
+    std::vector<int64_t> eb(hs + kSlotNew + T, hs + kSlotNew + T + R + 1);
 
-    Arena sa;
-    int64_t *cnt, *plo, *pdeg, *off, *scan_tmp;
-    sa.add(&cnt, P);
-    sa.add(&plo, P);
-    sa.add(&pdeg, P);
-    sa.add(&off, P + 1);
-    sa.add(&scan_tmp, scan_scratch_elems(P));
-    if (!sa.allocate(g, stream)) return fail(HG_ENOMEM, "hop %d: pair scratch", h);
-    scratch.push_back(sa.base);
-    int64_t *d_ebase = ws->dsmall + o_ebase;
-    if ((e = launch_count(d_et, d_pb, R, P, cnt, plo, pdeg, err, stream)) != hipSuccess ||
-        (e = launch_scan_i64(cnt, P, off, scan_tmp, stream)) != hipSuccess ||
-        (e = launch_edge_bases(d_pb, off, R, d_ebase, stream)) != hipSuccess)
-      return fail_hip(e, "count/scan");
-    // wait #1: error flag and per-etype edge counts
-    if ((e = sync_small(0, 1 + size_t(T) + size_t(R) + 1)) != hipSuccess)
-      return fail_hip(e, "sync");
-    if (int32_t(ws->hsmall[0]) != 0)
-      return fail(HG_EINVAL, "seeds: out of range or repeated within a node type");
-    const int64_t *ebase = ws->hsmall + o_ebase;
-    std::vector<int64_t> eb(ebase, ebase + R + 1);
-    const int64_t S = eb[R];
-
-    // ---- 2. outputs of the hop, sampler, bitmap scan -------------------
+    // ---- outputs of the hop ------------------------------------------------
     std::vector<int64_t> in_by_type(T, 0);
-    for (int32_t ei = 0; ei < R; ++ei) in_by_type[g->et[ei].src] += eb[ei + 1] - eb[ei];
-    Arena out;
+    for (int32_t i = 0; i < R; ++i) in_by_type[g->et[i].src] += eb[i + 1] - eb[i];
+    Carve oc;
     int64_t *indptr_all, *eid_all;
     int32_t *srcl_all, *dstl_all;
     std::vector<int64_t *> src_out(T, nullptr);
-    out.add(&indptr_all, P + R);
-    out.add(&eid_all, S);
-    out.add(&srcl_all, S);
-    out.add(&dstl_all, S);
+    std::vector<int64_t> bound(T);
+    oc.add(&indptr_all, P + R);
+    oc.add(&eid_all, S);
+    oc.add(&srcl_all, S);
+    oc.add(&dstl_all, S);
     for (int32_t t = 0; t < T; ++t) {
-      const int64_t bound = nF[t] + std::min(g->nt[t].num_nodes - nF[t], in_by_type[t]);
-      out.add(&src_out[t], bound);
+      bound[t] = nF[t] + std::min(g->nt[t].num_nodes - nF[t], in_by_type[t]);
+      oc.add(&src_out[t], bound[t]);
     }
-    if (!out.allocate(g, stream)) return fail(HG_ENOMEM, "hop %d: block arrays", h);
-    b->allocs.push_back(out.base);
-    int64_t *gid_tmp = static_cast<int64_t *>(alloc_scratch(sizeof(int64_t) * size_t(std::max<int64_t>(S, 1))));
-    if (!gid_tmp) return fail(HG_ENOMEM, "hop %d: edge scratch", h);
+    void *ob = oc.allocate(g, stream);
+    if (!ob) return fail(HG_ENOMEM, "hop %d: block arrays", h);
+    b->allocs.push_back(ob);
+    Carve ec;
+    int64_t *gid_tmp;
+    ec.add(&gid_tmp, S);
+    Carve cc;
+    uint64_t *cand;
+    cc.add(&cand, n_hubs * kCandCap);
+    if (!ec.in_scratch(ws->edges, stream) || !cc.in_scratch(ws->cand, stream))
+      return fail(HG_ENOMEM, "hop %d: edge scratch", h);
 
+    // tables: this hop's source lists; the next hop's frontier and fanouts
+    for (int32_t t = 0; t < T; ++t) {
+      hfield<int64_t *>(h, lay.src_out)[t] = src_out[t];
+      hfield<const int64_t *>(h + 1, lay.frontier)[t] = src_out[t];
+      hfield<int64_t *>(h + 1, lay.src_out)[t] = nullptr;
+    }
+    for (int32_t i = 0; i < R; ++i)
+      hfield<int32_t>(h + 1, lay.fanout)[i] = h + 1 < H ? fanouts[size_t(h + 1) * R + i] : 0;
+    if ((e = upload(size_t(h) * lay.size + lay.src_out, size_t(h + 2) * lay.size)) != hipSuccess)
+      return fail_hip(e, "upload");
+
+    // ---- 2-4. sample, compact, relabel -------------------------------------
     bitmap_dirty = true;
-    int64_t *d_new = ws->dsmall + o_new;
-    if ((e = launch_sample(d_et, d_pb, R, P, cnt, plo, pdeg, off, sigma, h, key_bits,
-                           gid_tmp, eid_all, dstl_all, stream)) != hipSuccess ||
-        (e = launch_block_indptr(d_pb, off, R, P, indptr_all, stream)) != hipSuccess ||
-        (e = launch_bitmap_tile_counts(ws->bitmap, g->n_tiles, ws->tile_cnt, stream)) != hipSuccess ||
-        (e = launch_bitmap_scan(ws->tile_cnt, g->d_tile_base, T, d_new, stream)) != hipSuccess)
+    int32_t compact_blocks = 0;
+    int64_t copy_total = 0;
+    for (int64_t n : nF) copy_total += n;
+    if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, pa, cand, ws->dsmall, sigma,
+                           h, key_bits, gid_tmp, eid_all, dstl_all, indptr_all, stream)) != hipSuccess)
       return fail_hip(e, "sample");
-    // wait #2: new-vertex counts
-    if ((e = sync_small(o_new, size_t(T))) != hipSuccess) return fail_hip(e, "sync");
-    std::vector<int64_t> U(ws->hsmall + o_new, ws->hsmall + o_new + T);
-    for (int32_t t = 0; t < T; ++t)
-      if (nF[t] + U[t] > INT32_MAX)
-        return fail(HG_EUNSUPPORTED, "hop %d: more than 2^31-1 vertices of type %d", h, t);
-
-    // ---- 3. local IDs of new vertices, destination prefix, relabel ------
-    if ((e = put_ntypes(h, F, nF, src_out, &total)) != hipSuccess) return fail_hip(e, "upload");
-    const HopNtype *d_nt = reinterpret_cast<const HopNtype *>(dtab(h) + lay.ntype_off);
-    const int64_t *d_tb = reinterpret_cast<const int64_t *>(dtab(h) + lay.tbase_off);
-    if ((e = launch_bitmap_assign(ws->bitmap, g->n_tiles, ws->tile_cnt, g->d_tile_base,
-                                  d_nt, T, stream)) != hipSuccess)
-      return fail_hip(e, "assign");
+    if ((e = launch_compact(hv, nv, ws->d_ts, ws->d_es, T, R, ws->bitmap, g->d_tile_base,
+                            g->n_tiles, copy_total, ws->lb_bits, next_epoch(), ticket_base,
+                            done_base, ws->dsmall, &compact_blocks, stream)) != hipSuccess)
+      return fail_hip(e, "compact");
+    ticket_base += uint64_t(compact_blocks);
+    done_base += uint64_t(compact_blocks);
     bitmap_dirty = false;
-    if ((e = launch_copy_frontier(d_nt, d_tb, T, total, stream)) != hipSuccess ||
-        (e = launch_relabel(d_et, d_ebase, R, S, gid_tmp, srcl_all, stream)) != hipSuccess)
+    // the map now holds the source lists of this hop (region h+1's frontier);
+    // their sizes are read at the next wait
+    map_region = h + 1;
+    map_bound = 0;
+    for (int32_t t = 0; t < T; ++t) map_bound += bound[t];
+    if ((e = launch_relabel(ws->d_es, ws->dsmall, T, R, S, gid_tmp, srcl_all, stream)) != hipSuccess)
       return fail_hip(e, "relabel");
 
     for (int32_t t = 0; t < T; ++t) {
       const size_t k = size_t(h) * T + t;
       b->n_dst[k] = nF[t];
-      b->n_src[k] = nF[t] + U[t];
       b->src_gid[k] = src_out[t];
-      F[t] = src_out[t];
-      nF[t] += U[t];
     }
-    map_lists = F;
-    map_list_n = nF;
-    for (int32_t ei = 0; ei < R; ++ei) {
-      const size_t k = size_t(h) * R + ei;
-      b->n_edges[k] = eb[ei + 1] - eb[ei];
-      b->indptr[k] = indptr_all + pb[ei] + ei;
-      b->src_local[k] = srcl_all + eb[ei];
-      b->dst_local[k] = dstl_all + eb[ei];
-      b->eid[k] = eid_all + eb[ei];
+    for (int32_t i = 0; i < R; ++i) {
+      const size_t k = size_t(h) * R + i;
+      b->n_edges[k] = eb[i + 1] - eb[i];
+      b->indptr[k] = indptr_all + pb[i] + i;
+      b->src_local[k] = srcl_all + eb[i];
+      b->dst_local[k] = dstl_all + eb[i];
+      b->eid[k] = eid_all + eb[i];
     }
-    for (void *p : scratch) dev_free(g, p, stream);
-    scratch.clear();
+    // the next counting pass covers at most this many pair slots
+    int64_t next_pairs = 0;
+    for (int32_t i = 0; i < R; ++i) next_pairs += bound[g->et[i].dst];
+    n_items = next_pairs + 1;
   }
 
-  // ---- input frontier ---------------------------------------------------
-  if (H == 0) {
-    Arena a;
+  if (H > 0) {
+    // final wait: new-vertex counts of the last hop
+    if ((e = sync_small()) != hipSuccess) return fail_hip(e, "sync");
+    hg_status st = check_flags("compact");
+    if (st != HG_OK) return st;
+    for (int32_t t = 0; t < T; ++t) {
+      const size_t k = size_t(H - 1) * T + t;
+      b->n_src[k] = b->n_dst[k] + ws->hsmall[kSlotNew + t];
+      nF[t] = b->n_src[k];
+      if (nF[t] > INT32_MAX)
+        return fail(HG_EUNSUPPORTED, "hop %d: more than 2^31-1 vertices of type %d", H - 1, t);
+      b->in_n[t] = nF[t];
+      b->in_gid[t] = b->src_gid[k];
+    }
+  } else {
+    Carve a;
     std::vector<int64_t *> cp(T, nullptr);
     for (int32_t t = 0; t < T; ++t) a.add(&cp[t], nF[t]);
-    if (!a.allocate(g, stream)) return fail(HG_ENOMEM, "seed copy");
-    b->allocs.push_back(a.base);
+    void *base = a.allocate(g, stream);
+    if (!base) return fail(HG_ENOMEM, "seed copy");
+    b->allocs.push_back(base);
     for (int32_t t = 0; t < T; ++t) {
       if (nF[t] > 0 &&
-          (e = hipMemcpyAsync(cp[t], F[t], sizeof(int64_t) * size_t(nF[t]),
+          (e = hipMemcpyAsync(cp[t], seeds[t], sizeof(int64_t) * size_t(nF[t]),
                               hipMemcpyDeviceToDevice, stream)) != hipSuccess)
         return fail_hip(e, "seed copy");
-      F[t] = cp[t];
+      b->in_n[t] = nF[t];
+      b->in_gid[t] = cp[t];
     }
-  }
-  for (int32_t t = 0; t < T; ++t) {
-    b->in_n[t] = nF[t];
-    b->in_gid[t] = F[t];
   }
   return HG_OK;
 }
@@ -583,6 +696,7 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
                     hg_graph **out) {
   if (!out) return fail(HG_EINVAL, "hg_create: out is NULL");
   *out = nullptr;
+  clear_pending_error();
   if (n_ntypes < 1 || !ntypes) return fail(HG_EINVAL, "hg_create: need at least one node type");
   if (n_etypes < 0 || (n_etypes > 0 && !etypes))
     return fail(HG_EINVAL, "hg_create: bad edge-type array");
@@ -692,6 +806,7 @@ hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
                               hg_blocks **out) {
   if (!out) return fail(HG_EINVAL, "hg_sample_blocks: out is NULL");
   *out = nullptr;
+  clear_pending_error();
   if (!g) return fail(HG_EINVAL, "hg_sample_blocks: graph is NULL");
   if (n_hops < 0) return fail(HG_EINVAL, "hg_sample_blocks: n_hops < 0");
   if (key_bits < 1 || key_bits > 32) return fail(HG_EINVAL, "hg_sample_blocks: key_bits not in 1..32");
@@ -712,7 +827,7 @@ hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
   if (st != HG_OK) return st;
   run.b = new (std::nothrow) hg_blocks();
   if (!run.b) {
-    run.cleanup(false);
+    run.finish(false);
     return fail(HG_ENOMEM, "hg_sample_blocks: out of host memory");
   }
   try {
@@ -721,11 +836,11 @@ hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
     st = fail(HG_ENOMEM, "hg_sample_blocks: out of host memory");
   }
   if (st != HG_OK) {
-    run.cleanup(false);
+    run.finish(false);
     return st;
   }
   hg_blocks *b = run.b;
-  run.cleanup(true);
+  run.finish(true);
   *out = b;
   return HG_OK;
 }
@@ -791,6 +906,7 @@ hg_status hg_gather_rows(hg_graph *g, int32_t ntype, const int64_t *ids,
   if (n == 0) return HG_OK;
   if (!ids || !out) return fail(HG_EINVAL, "hg_gather_rows: NULL ids or out");
   DeviceGuard dg(g->device);
+  clear_pending_error();
   hipError_t e = launch_gather(N.feat, N.num_nodes, N.row_bytes, ids, n, out, stream);
   if (e != hipSuccess) return fail_hip(e, "gather");
   return HG_OK;
@@ -815,6 +931,7 @@ void hg_blocks_free(hg_blocks *b) {
 hg_status hg_debug_philox(const uint32_t *ctr, uint64_t key, int64_t n,
                           uint32_t *out, hipStream_t stream) {
   if (n < 0 || (n > 0 && (!ctr || !out))) return fail(HG_EINVAL, "hg_debug_philox: bad arguments");
+  clear_pending_error();
   hipError_t e = launch_philox(ctr, key, n, out, stream);
   if (e != hipSuccess) return fail_hip(e, "philox");
   return HG_OK;

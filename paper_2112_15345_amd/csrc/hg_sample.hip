@@ -1,12 +1,18 @@
-// Per-hop neighbour sampling on gfx950: pair counting, device-wide scan and the
-// fanout sampler (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2.2).
+// Per-hop neighbour sampling on gfx950 (DistDGLv2, arXiv 2112.15345, Sec. 3.2
+// and Sec. 4.2.2): the counting pass over (frontier vertex, edge type) pairs
+// and the fanout sampler.
 //
-// A "pair" is (frontier vertex v of the destination type, edge type e).  Each
-// pair keeps min(deg, K) of its in-edges: all of them when deg <= K (or
+// Each pair keeps min(deg, K) of its in-edges: all of them when deg <= K (or
 // K == -1), else the K with the smallest (key, edge ID), where the key of edge
-// `eid` is word (eid & 3) of Philox4x32-10 at counter (eid >> 2, hop, e) under
-// the sampling seed.  Kept edges are written grouped by pair, ascending edge
-// ID within a pair.
+// `eid` is word (eid & 3) of Philox4x32-10 at counter (eid >> 2, hop, etype)
+// under the sampling seed.  Kept edges are written grouped by pair, ascending
+// edge ID within a pair.
+//
+// Work is split by pair shape: small take-all pairs run one per thread; other
+// pairs one per wavefront; pairs that select among more than kHubChunk edges
+// ("hubs") are cut into chunks of kHubChunk edges, one wavefront per chunk,
+// which append their candidates to a per-hub list; the last chunk of a hub to
+// finish selects from that list.  Every edge key is computed once.
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -28,124 +34,148 @@ unsigned grid_for(int64_t n, int threads, int64_t cap = 1 << 20) {
   return unsigned(b);
 }
 
+// Node type of item x of a concatenation of the hop's frontiers.
+__device__ __forceinline__ int type_of(const int64_t *nF, int32_t n_types,
+                                       int64_t x, int64_t *first) {
+  int64_t acc = 0;
+  int t = 0;
+  for (; t < n_types - 1; ++t) {
+    if (x < acc + nF[t]) break;
+    acc += nF[t];
+  }
+  *first = acc;
+  return t;
+}
+
 // ---- frontier map maintenance --------------------------------------------
 
-__global__ void k_insert_frontier(const HopNtype *types, const int64_t *type_base,
-                                  int32_t n_types, int64_t total, int32_t *err) {
+__global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
+                                  int32_t n_types, int64_t total, int64_t *small) {
+  int32_t *err = reinterpret_cast<int32_t *>(small + kSlotErr);
   for (int64_t x = grid_stride_start(); x < total; x += grid_stride_step()) {
-    const int t = find_segment(type_base, n_types, x);
-    const int64_t i = x - type_base[t];
-    const int64_t v = types[t].frontier[i];
-    if (v < 0 || v >= types[t].num_nodes) {
-      atomicOr(err, 1);
+    int64_t first;
+    const int t = type_of(hv.nF, n_types, x, &first);
+    const int64_t i = x - first;
+    if (i >= hv.nF[t]) continue;
+    const int64_t v = hv.frontier[t][i];
+    if (v < 0 || v >= ts[t].num_nodes) {
+      atomicOr(err, kErrSeedRange);
       continue;
     }
-    const int old = atomicCAS(&types[t].map[v], -1, int(i));
-    if (old != -1) atomicOr(err, 2);
+    if (atomicCAS(&ts[t].map[v], -1, int(i)) != -1) atomicOr(err, kErrSeedRepeat);
   }
 }
 
-__global__ void k_reset_map(const HopNtype *types, const int64_t *type_base,
-                            int32_t n_types, int64_t total) {
+__global__ void k_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
+                            int64_t total) {
   for (int64_t x = grid_stride_start(); x < total; x += grid_stride_step()) {
-    const int t = find_segment(type_base, n_types, x);
-    const int64_t v = types[t].frontier[x - type_base[t]];
-    if (v >= 0 && v < types[t].num_nodes) types[t].map[v] = -1;
+    int64_t first;
+    const int t = type_of(hv.nF, n_types, x, &first);
+    if (x - first >= hv.nF[t]) continue;  // past the end of the lists
+    const int64_t v = hv.frontier[t][x - first];
+    if (v >= 0 && v < ts[t].num_nodes) ts[t].map[v] = -1;
   }
 }
 
-// ---- pair counting -------------------------------------------------------
+// ---- counting pass ---------------------------------------------------------
 
-__global__ void k_count(const HopEtype *et, const int64_t *pair_base,
-                        int32_t n_etypes, int64_t n_pairs, int64_t *cnt,
-                        int64_t *plo, int64_t *pdeg, int32_t *err) {
-  for (int64_t p = grid_stride_start(); p < n_pairs; p += grid_stride_step()) {
-    const int e = find_segment(pair_base, n_etypes, p);
-    const HopEtype &E = et[e];
-    const int64_t v = E.frontier[p - E.pair_base];
+// Per pair: kept edges s, hub chunks, "one wavefront" flag, hub flag.
+struct PairCounts {
+  int64_t s, nch, wave, hub;
+};
+
+__global__ __launch_bounds__(kTileThreads) void k_count_scan(
+    HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
+    int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
+    uint64_t ticket_base, int64_t *small) {
+  __shared__ int64_t lds[8];
+  const int64_t tile = take_ticket(small, ticket_base, lds);
+  const int64_t P = hv.pair_base[n_etypes];
+  const int64_t base = tile * kPairTile + threadIdx.x * kPairItems;
+  int32_t *err = reinterpret_cast<int32_t *>(small + kSlotErr);
+  if (tile == 0 && threadIdx.x == 0 && P + 1 > n_items) atomicOr(err, kErrBound);
+
+  PairCounts c[kPairItems];
+  int etype[kPairItems];
+#pragma unroll
+  for (int k = 0; k < kPairItems; ++k) {
+    const int64_t p = base + k;
+    c[k] = PairCounts{0, 0, 0, 0};
+    etype[k] = 0;
+    if (p >= P) continue;
+    const int e = find_segment(hv.pair_base, n_etypes, p);
+    etype[k] = e;
+    const EtypeStatic &E = es[e];
+    const int64_t v = hv.frontier[E.dst_type][p - hv.pair_base[e]];
     int64_t lo = 0, deg = 0;
     if (v >= 0 && v < E.n_dst_nodes) {
       lo = E.indptr[v];
       deg = E.indptr[v + 1] - lo;
     } else {
-      atomicOr(err, 1);
+      atomicOr(err, kErrSeedRange);
     }
-    const int64_t k = E.fanout;
-    cnt[p] = (k < 0 || deg <= k) ? deg : k;
-    plo[p] = lo;
-    pdeg[p] = deg;
-  }
-}
-
-// ---- device-wide exclusive scan (reduce, scan tile sums, down-sweep) -----
-
-__global__ __launch_bounds__(kTileThreads) void k_scan_reduce(
-    const int64_t *in, int64_t n, int64_t *tile_sum) {
-  __shared__ int64_t lds[4];
-  const int64_t base = int64_t(blockIdx.x) * kTile + threadIdx.x * kTileItems;
-  int64_t s = 0;
-#pragma unroll
-  for (int k = 0; k < kTileItems; ++k)
-    if (base + k < n) s += in[base + k];
-  s = wave_sum_i64(s);
-  if (lane_id() == 0) lds[threadIdx.x / kWave] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) tile_sum[blockIdx.x] = lds[0] + lds[1] + lds[2] + lds[3];
-}
-
-// One block: exclusive scan of ts[0..nt) in place, ts[nt] = total.
-__global__ __launch_bounds__(kTileThreads) void k_scan_tiles(int64_t *ts,
-                                                             int64_t nt) {
-  __shared__ int64_t lds[4];
-  int64_t carry = 0;
-  for (int64_t base = 0; base < nt; base += kTile) {
-    const int64_t b = base + threadIdx.x * kTileItems;
-    int64_t v[kTileItems];
-    int64_t s = 0;
-#pragma unroll
-    for (int k = 0; k < kTileItems; ++k) {
-      v[k] = (b + k < nt) ? ts[b + k] : 0;
-      s += v[k];
+    const int64_t K = hv.fanout[e];
+    const int64_t s = (K < 0 || deg <= K) ? deg : K;
+    c[k].s = s;
+    if (s < deg && deg > kHubChunk) {
+      c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
+      c[k].hub = 1;
+    } else if (s > 0 && !(s == deg && deg <= kThreadTakeAll)) {
+      c[k].wave = 1;
     }
-    int64_t total;
-    int64_t pre = block_excl_scan_256(s, lds, &total) + carry;
+    pa.plo[p] = lo;
+    pa.pdeg[p] = deg;
+  }
+
+  // block scan of the per-thread sums, then the tile's prefix by look-back
+  int64_t sum[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int k = 0; k < kTileItems; ++k) {
-      if (b + k < nt) ts[b + k] = pre;
-      pre += v[k];
+  for (int k = 0; k < kPairItems; ++k) {
+    sum[0] += c[k].s;
+    sum[1] += c[k].nch;
+    sum[2] += c[k].wave;
+    sum[3] += c[k].hub;
+  }
+  int64_t pre[4], agg[4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) pre[a] = block_excl_scan_256(sum[a], lds, &agg[a]);
+  int64_t ex[4];
+  tile_lookback<4>(lb, tile, 0, epoch, agg, ex, small, lds);
+#pragma unroll
+  for (int a = 0; a < 4; ++a) pre[a] += ex[a];
+
+  int64_t *ebase = small + kSlotNew + n_types;
+#pragma unroll
+  for (int k = 0; k < kPairItems; ++k) {
+    const int64_t p = base + k;
+    if (p < n_items) {
+      pa.off[p] = pre[0];
+      pa.choff[p] = pre[1];
+      pa.woff[p] = pre[2];
+      pa.hoff[p] = pre[3];
+      if (c[k].hub) {
+        pa.hub_cnt[pre[3]] = 0;
+        pa.hub_done[pre[3]] = 0;
+      }
+      // edge start of every etype whose first pair (or end, for the last) is p
+      if (p <= P) {
+        const int e = p < P ? etype[k] : n_etypes;
+        for (int e2 = e; e2 >= 0 && hv.pair_base[e2] == p; --e2) ebase[e2] = pre[0];
+      }
     }
-    carry += total;
+    pre[0] += c[k].s;
+    pre[1] += c[k].nch;
+    pre[2] += c[k].wave;
+    pre[3] += c[k].hub;
   }
-  if (threadIdx.x == 0) ts[nt] = carry;
-}
-
-__global__ __launch_bounds__(kTileThreads) void k_scan_down(
-    const int64_t *in, int64_t n, const int64_t *ts, int64_t nt, int64_t *out) {
-  __shared__ int64_t lds[4];
-  const int64_t b = int64_t(blockIdx.x) * kTile + threadIdx.x * kTileItems;
-  int64_t v[kTileItems];
-  int64_t s = 0;
-#pragma unroll
-  for (int k = 0; k < kTileItems; ++k) {
-    v[k] = (b + k < n) ? in[b + k] : 0;
-    s += v[k];
+  // the last tile holds the totals
+  if (tile == int64_t(gridDim.x) - 1 && threadIdx.x == kTileThreads - 1) {
+    small[kSlotPairs] = P;
+    small[kSlotEdges] = pre[0];
+    small[kSlotChunks] = pre[1];
+    small[kSlotWaves] = pre[2];
+    small[kSlotHubs] = pre[3];
   }
-  int64_t total;
-  int64_t pre = block_excl_scan_256(s, lds, &total) + ts[blockIdx.x];
-#pragma unroll
-  for (int k = 0; k < kTileItems; ++k) {
-    if (b + k < n) out[b + k] = pre;
-    pre += v[k];
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) out[n] = ts[nt];
-}
-
-__global__ void k_set_i64(int64_t *p, int64_t v) { *p = v; }
-
-__global__ void k_edge_bases(const int64_t *pair_base, const int64_t *off,
-                             int32_t n_etypes, int64_t *ebase) {
-  for (int64_t e = grid_stride_start(); e <= n_etypes; e += grid_stride_step())
-    ebase[e] = off[pair_base[e]];
 }
 
 // ---- the sampler -----------------------------------------------------------
@@ -159,6 +189,13 @@ struct EmitCtx {
   int32_t *dst_local;
   int32_t dst;
 };
+
+__device__ __forceinline__ EmitCtx make_ctx(const EtypeStatic &E, int64_t *src_gid,
+                                            int64_t *eid, int32_t *dst_local,
+                                            int64_t dst) {
+  return EmitCtx{E.indices, E.src_map, E.src_bitmap, src_gid, eid, dst_local,
+                 int32_t(dst)};
+}
 
 // Writes kept edge `e` at output slot `pos` and marks its source as new when
 // it is not in the frontier of its type yet.
@@ -192,123 +229,30 @@ __device__ __forceinline__ uint32_t word_of(const U32x4 &r, int w) {
   return w == 0 ? r.x : (w == 1 ? r.y : (w == 2 ? r.z : r.w));
 }
 
-constexpr int kSampleWaves = 4;
+// Keys are uniform, so about deg * tau / 2^bits of them fall below tau; tau is
+// set for K + 4 sqrt(K) + 16 expected candidates.  A pure function of
+// (K, deg, bits), so every chunk of a hub uses the same value.
+__device__ __forceinline__ uint64_t cand_threshold(int64_t K, int64_t deg,
+                                                   uint64_t key_space) {
+  uint64_t tau = uint64_t(ceil((double(K) + 4.0 * sqrt(double(K)) + 16.0) /
+                               double(deg) * double(key_space)));
+  if (tau < 1) tau = 1;
+  if (tau > key_space) tau = key_space;
+  return tau;
+}
 
-__global__ __launch_bounds__(kSampleWaves *kWave) void k_sample(
-    const HopEtype *et, const int64_t *pair_base, int32_t n_etypes,
-    int64_t n_pairs, const int64_t *cnt, const int64_t *plo,
-    const int64_t *pdeg, const int64_t *off, uint64_t sigma, int32_t hop,
-    int32_t key_bits, int64_t *src_gid, int64_t *eid_out, int32_t *dst_local) {
-  __shared__ uint32_t s_key[kSampleWaves][kCandCap];
-  __shared__ uint32_t s_j[kSampleWaves][kCandCap];
-  const int wave = threadIdx.x / kWave;
+// The rule on one pair when the candidates could not decide it (too few or
+// too many): bisect the composite (key << 32 | j), j = eid - lo, for the K-th
+// smallest value T within [a, b], then keep every edge with composite <= T,
+// in edge order.  One wavefront; exact.
+__device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
+                                    int64_t K, int64_t o, uint64_t a,
+                                    uint64_t b, int32_t hop, int32_t e,
+                                    uint32_t k0, uint32_t k1, uint32_t shift) {
   const int lane = lane_id();
-  const int64_t p = int64_t(blockIdx.x) * kSampleWaves + wave;
-  if (p >= n_pairs) return;
-  const int64_t s = cnt[p];
-  if (s == 0) return;
-  const int e = find_segment(pair_base, n_etypes, p);
-  EmitCtx c;
-  c.indices = et[e].indices;
-  c.src_map = et[e].src_map;
-  c.src_bitmap = et[e].src_bitmap;
-  c.src_gid = src_gid;
-  c.eid = eid_out;
-  c.dst_local = dst_local;
-  c.dst = int32_t(p - et[e].pair_base);
-  const int64_t lo = plo[p];
-  const int64_t deg = pdeg[p];
-  const int64_t o = off[p];
-
-  if (s == deg) {  // every in-edge is kept
-    for (int64_t j = lane; j < deg; j += kWave) emit_edge(c, o + j, lo + j);
-    return;
-  }
-
-  // ---- keep the K = s in-edges with the smallest (key, edge ID) ----------
-  const int K = int(s);
-  const uint32_t shift = uint32_t(32 - key_bits);
-  const uint64_t key_space = uint64_t(1) << key_bits;
-  const uint32_t k0 = uint32_t(sigma), k1 = uint32_t(sigma >> 32);
   const uint64_t g_first = uint64_t(lo) >> 2;
   const uint64_t g_last = uint64_t(lo + deg - 1) >> 2;
   const uint64_t hi = uint64_t(lo + deg);
-
-  // Pass 1: keys are uniform, so about deg * tau / 2^bits of them fall below
-  // tau; tau is set for K + 4 sqrt(K) + 16 expected candidates.  Candidates
-  // (key < tau) are appended in edge order to this wave's LDS list.
-  uint64_t tau = uint64_t(
-      ceil((double(K) + 4.0 * sqrt(double(K)) + 16.0) / double(deg) *
-           double(key_space)));
-  if (tau < 1) tau = 1;
-  if (tau > key_space) tau = key_space;
-  uint32_t *ck = s_key[wave];
-  uint32_t *cj = s_j[wave];
-  int64_t n_cand = 0;
-  for (uint64_t gb = g_first; gb <= g_last; gb += kWave) {
-    const uint64_t g = gb + lane;
-    int mask = 0;
-    U32x4 r{0, 0, 0, 0};
-    if (g <= g_last) {
-      r = edge_keys(g, hop, e, k0, k1, shift);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const uint64_t ed = 4 * g + w;
-        if (ed >= uint64_t(lo) && ed < hi && uint64_t(word_of(r, w)) < tau)
-          mask |= 1 << w;
-      }
-    }
-    int tot;
-    int64_t pos = n_cand + wave_prefix_small(__popc(mask), &tot);
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      if (mask & (1 << w)) {
-        if (pos < kCandCap) {
-          ck[pos] = word_of(r, w);
-          cj[pos] = uint32_t(4 * g + w - uint64_t(lo));
-        }
-        ++pos;
-      }
-    }
-    n_cand += tot;
-  }
-  wave_sync();
-
-  if (n_cand >= K && n_cand <= kCandCap) {
-    // The K smallest all lie among the candidates: rank each candidate by
-    // counting smaller (key, j) pairs, keep ranks < K, in list (edge) order.
-    const int nc = int(n_cand);
-    int64_t emitted = 0;
-    for (int q0 = 0; q0 < nc; q0 += kWave) {
-      const int q = q0 + lane;
-      bool sel = false;
-      uint32_t jq = 0;
-      if (q < nc) {
-        jq = cj[q];
-        const uint64_t me = (uint64_t(ck[q]) << 32) | jq;
-        int rank = 0;
-        for (int t = 0; t < nc; ++t)
-          rank += ((uint64_t(ck[t]) << 32) | cj[t]) < me ? 1 : 0;
-        sel = rank < K;
-      }
-      const uint64_t bal = __ballot(sel);
-      if (sel) emit_edge(c, o + emitted + __popcll(bal & lanes_below()), lo + jq);
-      emitted += __popcll(bal);
-    }
-    return;
-  }
-
-  // Exact fallback (too few or too many candidates): bisect the composite
-  // (key << 32 | j) for the K-th smallest value T, then keep every edge with
-  // composite <= T, in edge order.
-  uint64_t a = 0;
-  uint64_t b = ((key_space - 1) << 32) | uint64_t(deg - 1);
-  if (tau < key_space) {
-    if (n_cand >= K)
-      b = min(b, (tau << 32) - 1);
-    else
-      a = tau << 32;
-  }
   while (a < b) {
     const uint64_t mid = a + ((b - a) >> 1);
     int64_t le = 0;
@@ -354,30 +298,258 @@ __global__ __launch_bounds__(kSampleWaves *kWave) void k_sample(
   }
 }
 
-// ---- block CSC -------------------------------------------------------------
-
-// Segment starts of the per-etype indptr arrays: st[e] = pair_base[e] + e.
-__device__ __forceinline__ int find_indptr_segment(const int64_t *pair_base,
-                                                   int n, int64_t x) {
-  int lo = 0, hi = n;
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (pair_base[mid] + mid <= x)
-      lo = mid;
+// Bisection bounds that the candidate count already implies.
+__device__ __forceinline__ void bisection_bounds(int64_t n_cand, int64_t K,
+                                                 uint64_t tau, uint64_t key_space,
+                                                 int64_t deg, uint64_t *a,
+                                                 uint64_t *b) {
+  *a = 0;
+  *b = ((key_space - 1) << 32) | uint64_t(deg - 1);
+  if (tau < key_space) {
+    if (n_cand >= K)
+      *b = min(*b, (tau << 32) - 1);  // the K smallest all have key < tau
     else
-      hi = mid;
+      *a = tau << 32;  // fewer than K keys below tau
   }
-  return lo;
 }
 
-__global__ void k_block_indptr(const int64_t *pair_base, const int64_t *off,
-                               int32_t n_etypes, int64_t total,
-                               int64_t *indptr_all) {
-  for (int64_t q = grid_stride_start(); q < total; q += grid_stride_step()) {
-    const int e = find_indptr_segment(pair_base, n_etypes, q);
-    const int64_t first = pair_base[e];
-    const int64_t i = q - (first + e);
-    indptr_all[q] = off[first + i] - off[first];
+constexpr int kSampleWaves = 4;
+constexpr int kSampleThreads = kSampleWaves * kWave;
+
+struct SampleArgs {
+  HopView hv;
+  const EtypeStatic *es;
+  int32_t n_etypes, n_types;
+  int64_t n_pairs, n_wave, n_chunks;
+  int64_t blocks_a, blocks_b;
+  PairArrays pa;
+  uint64_t *cand;
+  const int64_t *small;
+  uint64_t sigma;
+  int32_t hop, key_bits;
+  int64_t *src_gid, *eid;
+  int32_t *dst_local;
+  int64_t *indptr_all;
+};
+
+// Role A: a thread per pair.  Writes the pair's block-CSC entry and copies the
+// in-edges of a small take-all pair.  The first n_etypes+1 threads of block 0
+// also write each etype's closing CSC entry.
+__device__ void role_thread_pairs(const SampleArgs &A) {
+  const int64_t *ebase = A.small + kSlotNew + A.n_types;
+  const int64_t *pb = A.hv.pair_base;
+  if (blockIdx.x == 0)
+    for (int e = threadIdx.x; e < A.n_etypes; e += kSampleThreads)
+      A.indptr_all[pb[e + 1] + e] = ebase[e + 1] - ebase[e];
+  const int64_t p = int64_t(blockIdx.x) * kSampleThreads + threadIdx.x;
+  if (p >= A.n_pairs) return;
+  const int e = find_segment(pb, A.n_etypes, p);
+  const int64_t i = p - pb[e];
+  const int64_t o = A.pa.off[p];
+  A.indptr_all[pb[e] + e + i] = o - ebase[e];
+  const int64_t s = A.pa.off[p + 1] - o;
+  const int64_t deg = A.pa.pdeg[p];
+  if (s == 0 || s != deg || deg > kThreadTakeAll) return;
+  const int64_t lo = A.pa.plo[p];
+  const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local, i);
+  for (int64_t j = 0; j < deg; ++j) emit_edge(c, o + j, lo + j);
+}
+
+// Role B: a wavefront per pair (large take-all, or selection among at most
+// kHubChunk edges with the candidate list in LDS).
+__device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
+                                int64_t w) {
+  const int lane = lane_id();
+  const int64_t p = find_segment(A.pa.woff, int(A.n_pairs), w);
+  const int e = find_segment(A.hv.pair_base, A.n_etypes, p);
+  const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
+                             p - A.hv.pair_base[e]);
+  const int64_t lo = A.pa.plo[p];
+  const int64_t deg = A.pa.pdeg[p];
+  const int64_t o = A.pa.off[p];
+  const int64_t s = A.pa.off[p + 1] - o;
+  if (s == deg) {  // every in-edge is kept
+    for (int64_t j = lane; j < deg; j += kWave) emit_edge(c, o + j, lo + j);
+    return;
+  }
+  const int64_t K = s;
+  const uint32_t shift = uint32_t(32 - A.key_bits);
+  const uint64_t key_space = uint64_t(1) << A.key_bits;
+  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
+  const uint64_t g_first = uint64_t(lo) >> 2;
+  const uint64_t g_last = uint64_t(lo + deg - 1) >> 2;
+  const uint64_t hi = uint64_t(lo + deg);
+
+  // candidates (key < tau), appended in edge order
+  const uint64_t tau = cand_threshold(K, deg, key_space);
+  int64_t n_cand = 0;
+  for (uint64_t gb = g_first; gb <= g_last; gb += kWave) {
+    const uint64_t g = gb + lane;
+    int mask = 0;
+    U32x4 r{0, 0, 0, 0};
+    if (g <= g_last) {
+      r = edge_keys(g, A.hop, e, k0, k1, shift);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint64_t ed = 4 * g + q;
+        if (ed >= uint64_t(lo) && ed < hi && uint64_t(word_of(r, q)) < tau)
+          mask |= 1 << q;
+      }
+    }
+    int tot;
+    int64_t pos = n_cand + wave_prefix_small(__popc(mask), &tot);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (mask & (1 << q)) {
+        if (pos < kCandCap) {
+          ck[pos] = word_of(r, q);
+          cj[pos] = uint32_t(4 * g + q - uint64_t(lo));
+        }
+        ++pos;
+      }
+    }
+    n_cand += tot;
+  }
+  wave_sync();
+
+  if (n_cand >= K && n_cand <= kCandCap) {
+    // rank each candidate by counting smaller (key, j); keep ranks < K, in
+    // list (= edge) order
+    const int nc = int(n_cand);
+    int64_t emitted = 0;
+    for (int q0 = 0; q0 < nc; q0 += kWave) {
+      const int q = q0 + lane;
+      bool sel = false;
+      uint32_t jq = 0;
+      if (q < nc) {
+        jq = cj[q];
+        const uint64_t me = (uint64_t(ck[q]) << 32) | jq;
+        int rank = 0;
+        for (int t = 0; t < nc; ++t)
+          rank += ((uint64_t(ck[t]) << 32) | cj[t]) < me ? 1 : 0;
+        sel = rank < K;
+      }
+      const uint64_t bal = __ballot(sel);
+      if (sel) emit_edge(c, o + emitted + __popcll(bal & lanes_below()), lo + jq);
+      emitted += __popcll(bal);
+    }
+    return;
+  }
+  uint64_t a, b;
+  bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
+  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, e, k0, k1, shift);
+}
+
+// Role C: a wavefront per hub chunk.  Appends the chunk's candidates to the
+// hub's list; the wavefront finishing the hub's last chunk selects the K
+// smallest of the list and writes them in edge order.
+__device__ void role_hub_chunks(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
+                                uint8_t *sel, int64_t chunk) {
+  const int lane = lane_id();
+  const int64_t p = find_segment(A.pa.choff, int(A.n_pairs), chunk);
+  const int e = find_segment(A.hv.pair_base, A.n_etypes, p);
+  const int64_t lo = A.pa.plo[p];
+  const int64_t deg = A.pa.pdeg[p];
+  const int64_t o = A.pa.off[p];
+  const int64_t K = A.pa.off[p + 1] - o;
+  const int64_t nch = A.pa.choff[p + 1] - A.pa.choff[p];
+  const int64_t hub = A.pa.hoff[p];
+  const uint32_t shift = uint32_t(32 - A.key_bits);
+  const uint64_t key_space = uint64_t(1) << A.key_bits;
+  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
+  const uint64_t tau = cand_threshold(K, deg, key_space);
+
+  const int64_t c_lo = lo + (chunk - A.pa.choff[p]) * kHubChunk;
+  const int64_t c_hi = min(c_lo + kHubChunk, lo + deg);
+  const uint64_t g_first = uint64_t(c_lo) >> 2;
+  const uint64_t g_last = uint64_t(c_hi - 1) >> 2;
+  uint64_t *list = A.cand + hub * kCandCap;
+  int32_t *cnt = A.pa.hub_cnt + hub;
+  for (uint64_t gb = g_first; gb <= g_last; gb += kWave) {
+    const uint64_t g = gb + lane;
+    int mask = 0;
+    U32x4 r{0, 0, 0, 0};
+    if (g <= g_last) {
+      r = edge_keys(g, A.hop, e, k0, k1, shift);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint64_t ed = 4 * g + q;
+        if (ed >= uint64_t(c_lo) && ed < uint64_t(c_hi) && uint64_t(word_of(r, q)) < tau)
+          mask |= 1 << q;
+      }
+    }
+    int tot;
+    const int pre = wave_prefix_small(__popc(mask), &tot);
+    if (tot == 0) continue;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(cnt, tot);
+    base = __shfl(base, 0, kWave);
+    int pos = base + pre;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (mask & (1 << q)) {
+        if (pos < kCandCap)
+          list[pos] = (uint64_t(word_of(r, q)) << 32) | (4 * g + q - uint64_t(lo));
+        ++pos;
+      }
+    }
+  }
+  // publish this chunk's candidates, then count it as done
+  __threadfence();
+  int last = 0;
+  if (lane == 0) last = atomicAdd(A.pa.hub_done + hub, 1) == int(nch - 1);
+  last = __shfl(last, 0, kWave);
+  if (!last) return;
+  __threadfence();
+
+  const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
+                             p - A.hv.pair_base[e]);
+  const int64_t n_cand = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (n_cand >= K && n_cand <= kCandCap) {
+    const int nc = int(n_cand);
+    for (int q = lane; q < nc; q += kWave) {
+      const uint64_t v = __hip_atomic_load(list + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ck[q] = uint32_t(v >> 32);
+      cj[q] = uint32_t(v);
+    }
+    wave_sync();
+    // rank by (key, j): the K smallest are kept
+    for (int q = lane; q < nc; q += kWave) {
+      const uint64_t me = (uint64_t(ck[q]) << 32) | cj[q];
+      int rank = 0;
+      for (int t = 0; t < nc; ++t) rank += ((uint64_t(ck[t]) << 32) | cj[t]) < me ? 1 : 0;
+      sel[q] = rank < K ? 1 : 0;
+    }
+    wave_sync();
+    // output position = kept candidates with a smaller edge ID
+    for (int q = lane; q < nc; q += kWave) {
+      if (!sel[q]) continue;
+      const uint32_t jq = cj[q];
+      int pos = 0;
+      for (int t = 0; t < nc; ++t) pos += (sel[t] && cj[t] < jq) ? 1 : 0;
+      emit_edge(c, o + pos, lo + jq);
+    }
+    return;
+  }
+  uint64_t a, b;
+  bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
+  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, e, k0, k1, shift);
+}
+
+__global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
+  __shared__ uint32_t s_key[kSampleWaves][kCandCap];
+  __shared__ uint32_t s_j[kSampleWaves][kCandCap];
+  __shared__ uint8_t s_sel[kSampleWaves][kCandCap];
+  const int64_t b = blockIdx.x;
+  const int wave = threadIdx.x / kWave;
+  if (b < A.blocks_a) {
+    role_thread_pairs(A);
+  } else if (b < A.blocks_a + A.blocks_b) {
+    const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
+    if (w < A.n_wave) role_wave_pairs(A, s_key[wave], s_j[wave], w);
+  } else {
+    const int64_t chunk = (b - A.blocks_a - A.blocks_b) * kSampleWaves + wave;
+    if (chunk < A.n_chunks) role_hub_chunks(A, s_key[wave], s_j[wave], s_sel[wave], chunk);
   }
 }
 
@@ -419,80 +591,70 @@ __global__ void k_philox(const uint32_t *ctr, uint32_t k0, uint32_t k1,
 
 // ---- launchers ---------------------------------------------------------------
 
-hipError_t launch_insert_frontier(const HopNtype *types, const int64_t *type_base,
-                                  int32_t n_types, int64_t total, int32_t *err,
+hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
+                                  int32_t n_types, int64_t total, int64_t *small,
                                   hipStream_t stream) {
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_insert_frontier, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, types, type_base, n_types, total, err);
+                     stream, hv, ts, n_types, total, small);
   return hipGetLastError();
 }
 
-hipError_t launch_reset_map(const HopNtype *types, const int64_t *type_base,
-                            int32_t n_types, int64_t total, hipStream_t stream) {
+hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
+                            int64_t total, hipStream_t stream) {
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_reset_map, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, types, type_base, n_types, total);
+                     stream, hv, ts, n_types, total);
   return hipGetLastError();
 }
 
-hipError_t launch_count(const HopEtype *et, const int64_t *pair_base,
-                        int32_t n_etypes, int64_t n_pairs, int64_t *cnt,
-                        int64_t *plo, int64_t *pdeg, int32_t *err,
-                        hipStream_t stream) {
-  if (n_pairs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_count, dim3(grid_for(n_pairs, 256)), dim3(256), 0, stream,
-                     et, pair_base, n_etypes, n_pairs, cnt, plo, pdeg, err);
+int64_t count_tiles(int64_t n_items) {
+  const int64_t t = (n_items + kPairTile - 1) / kPairTile;
+  return t < 1 ? 1 : t;
+}
+
+hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
+                             int32_t n_types, int64_t n_items, PairArrays pa,
+                             Lookback lb, uint32_t epoch, uint64_t ticket_base,
+                             int64_t *small, hipStream_t stream) {
+  hipLaunchKernelGGL(k_count_scan, dim3(unsigned(count_tiles(n_items))),
+                     dim3(kTileThreads), 0, stream, hv, es, n_etypes, n_types,
+                     n_items, pa, lb, epoch, ticket_base, small);
   return hipGetLastError();
 }
 
-int64_t scan_scratch_elems(int64_t n) { return (n + kTile - 1) / kTile + 1; }
-
-hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out,
-                           int64_t *scratch, hipStream_t stream) {
-  if (n <= 0) {
-    hipLaunchKernelGGL(k_set_i64, dim3(1), dim3(1), 0, stream, out, int64_t(0));
-    return hipGetLastError();
-  }
-  const int64_t nt = (n + kTile - 1) / kTile;
-  hipLaunchKernelGGL(k_scan_reduce, dim3(unsigned(nt)), dim3(kTileThreads), 0,
-                     stream, in, n, scratch);
-  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(kTileThreads), 0, stream,
-                     scratch, nt);
-  hipLaunchKernelGGL(k_scan_down, dim3(unsigned(nt)), dim3(kTileThreads), 0,
-                     stream, in, n, scratch, nt, out);
-  return hipGetLastError();
-}
-
-hipError_t launch_edge_bases(const int64_t *pair_base, const int64_t *off,
-                             int32_t n_etypes, int64_t *ebase,
-                             hipStream_t stream) {
-  hipLaunchKernelGGL(k_edge_bases, dim3(grid_for(n_etypes + 1, 256)), dim3(256),
-                     0, stream, pair_base, off, n_etypes, ebase);
-  return hipGetLastError();
-}
-
-hipError_t launch_sample(const HopEtype *et, const int64_t *pair_base,
-                         int32_t n_etypes, int64_t n_pairs, const int64_t *cnt,
-                         const int64_t *plo, const int64_t *pdeg,
-                         const int64_t *off, uint64_t sigma, int32_t hop,
+hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
+                         int32_t n_types, int64_t n_pairs, int64_t n_wave,
+                         int64_t n_chunks, PairArrays pa, uint64_t *cand,
+                         const int64_t *small, uint64_t sigma, int32_t hop,
                          int32_t key_bits, int64_t *src_gid, int64_t *eid,
-                         int32_t *dst_local, hipStream_t stream) {
-  if (n_pairs <= 0) return hipSuccess;
-  const int64_t blocks = (n_pairs + kSampleWaves - 1) / kSampleWaves;
-  hipLaunchKernelGGL(k_sample, dim3(unsigned(blocks)), dim3(kSampleWaves * kWave),
-                     0, stream, et, pair_base, n_etypes, n_pairs, cnt, plo, pdeg,
-                     off, sigma, hop, key_bits, src_gid, eid, dst_local);
-  return hipGetLastError();
-}
-
-hipError_t launch_block_indptr(const int64_t *pair_base, const int64_t *off,
-                               int32_t n_etypes, int64_t n_pairs,
-                               int64_t *indptr_all, hipStream_t stream) {
-  const int64_t total = n_pairs + n_etypes;
-  if (total <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_block_indptr, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, pair_base, off, n_etypes, total, indptr_all);
+                         int32_t *dst_local, int64_t *indptr_all,
+                         hipStream_t stream) {
+  SampleArgs A;
+  A.hv = hv;
+  A.es = es;
+  A.n_etypes = n_etypes;
+  A.n_types = n_types;
+  A.n_pairs = n_pairs;
+  A.n_wave = n_wave;
+  A.n_chunks = n_chunks;
+  // role A always has a block, for the closing CSC entries
+  A.blocks_a = std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads);
+  A.blocks_b = (n_wave + kSampleWaves - 1) / kSampleWaves;
+  const int64_t blocks_c = (n_chunks + kSampleWaves - 1) / kSampleWaves;
+  A.pa = pa;
+  A.cand = cand;
+  A.small = small;
+  A.sigma = sigma;
+  A.hop = hop;
+  A.key_bits = key_bits;
+  A.src_gid = src_gid;
+  A.eid = eid;
+  A.dst_local = dst_local;
+  A.indptr_all = indptr_all;
+  const int64_t blocks = A.blocks_a + A.blocks_b + blocks_c;
+  hipLaunchKernelGGL(k_sample, dim3(unsigned(blocks)), dim3(kSampleThreads), 0,
+                     stream, A);
   return hipGetLastError();
 }
 

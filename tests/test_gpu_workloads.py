@@ -1,0 +1,78 @@
+"""HIP path against the oracle on full-size workloads, with the same calls and
+launch configuration that bench.py times: every block array of every hop and
+the gathered feature bytes, element by element."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2112_15345_amd as hg
+import pins
+import workloads as W
+from gpu_harness import compare, gpu_seeds, result_dict
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+_cache = {}
+
+
+def workload_graph(idx):
+    """(generated graph on the GPU, library graph, oracle host graph), cached."""
+    if idx not in _cache:
+        _cache.clear()
+        torch.cuda.empty_cache()
+        wl = W.WORKLOADS[idx]
+        say(f"generating workload {idx}: {wl.name}")
+        gen = W.make_graph(wl, device="cuda")
+        g = hg.Graph(list(zip(gen.num_nodes, gen.feats)), gen.etypes)
+        host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), check=False)
+        _cache[idx] = (wl, gen, g, host)
+    return _cache[idx]
+
+
+@pytest.mark.parametrize("idx,batches", [(2, (0, 1, 7)), (5, (0, 4))])
+def test_workload_parity(idx, batches):
+    wl, gen, g, host = workload_graph(idx)
+    fan = wl.fanout_matrix()
+    for b in batches:
+        seeds = W.seeds_per_type(wl, b)
+        say(f"workload {idx} batch {b}: GPU")
+        blocks = g.sample_blocks(gpu_seeds(seeds), fan, b)
+        got = result_dict(g, blocks)
+        say(f"workload {idx} batch {b}: oracle")
+        ref = host.sample_blocks(seeds, fan, b)
+        diffs = compare(ref, got, g.T, g.R, len(fan))
+        assert not diffs, f"batch {b}: " + "\n".join(diffs[:10])
+        for t, f in enumerate(gen.feats):
+            if f is None:
+                continue
+            x = g.gather_features(blocks, t)
+            ids = ref["input"][t]
+            want = host.gather(t, ids)
+            assert x.contiguous().view(torch.uint8).cpu().numpy().tobytes() == want.tobytes(), \
+                f"batch {b} type {t}: gathered bytes differ"
+        say(f"workload {idx} batch {b}: equal "
+            f"({sum(v[3].size for v in ref['edges'].values())} edges)")
+
+
+def test_workload_invariants_with_forced_ties():
+    """Academic workload with 4-bit keys (ties everywhere, hub fallbacks), one
+    batch: GPU == oracle, and the definition checks hold on the GPU result."""
+    wl, gen, g, host = workload_graph(2)
+    fan = [[10] * g.R]
+    seeds = W.seeds_per_type(wl, 3)
+    blocks = g.sample_blocks(gpu_seeds(seeds), fan, 3, key_bits=4)
+    got = result_dict(g, blocks)
+    ref = host.sample_blocks(seeds, fan, 3, key_bits=4)
+    assert not compare(ref, got, g.T, g.R, 1)
+    ets = gen.host_etypes()
+    fails = pins.check_blocks(gen.num_nodes, ets, seeds, fan, 3, 4, got, brute=False)
+    assert not fails, "\n".join(fails[:5])
