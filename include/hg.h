@@ -13,8 +13,8 @@
  *  - Pointers marked "device" are HIP device addresses on the current device;
  *    "host" pointers are read before the call returns.
  *  - All device work goes on the caller's `stream`.  hg_sample_blocks waits on
- *    that stream (twice per hop, to size its outputs); the gathers are fully
- *    asynchronous.
+ *    that stream once per hop and once at the end, to size its outputs; the
+ *    gathers are fully asynchronous.
  *  - Functions return hg_status; no C++ exception crosses this boundary.
  *    After a failure, hg_last_error() describes it (thread-local text, valid
  *    until the next call on the same thread).
@@ -76,10 +76,13 @@ typedef struct hg_etype_desc {
   const int64_t *indices;
 } hg_etype_desc;
 
-/* Optional device allocator for the blocks' arrays and per-call scratch.
+/* Optional device allocator for the output arrays of hg_sample_blocks.
  * alloc returns NULL on failure (hg_sample_blocks then returns HG_ENOMEM and
  * releases what it took).  A NULL allocator means stream-ordered
- * hipMallocAsync / hipFreeAsync from the device's default pool. */
+ * hipMallocAsync / hipFreeAsync from the device's default pool.  Working
+ * memory (a per-vertex map and bitmap, per-pair and per-edge scratch) belongs
+ * to the graph handle: it comes from the device's pool, grows to the largest
+ * call and is released by hg_destroy; concurrent calls each get their own. */
 typedef struct hg_allocator {
   void *ctx;
   void *(*alloc)(void *ctx, size_t bytes, hipStream_t stream);
@@ -166,6 +169,15 @@ hg_status hg_blocks_input_nodes(const hg_blocks *blocks, int32_t ntype,
  * HG_EINVAL for a featureless type.  Asynchronous on `stream`. */
 hg_status hg_gather_features(hg_graph *graph, const hg_blocks *blocks,
                              int32_t ntype, void *out, hipStream_t stream);
+
+/* hg_gather_features for several node types at once, in as few launches as
+ * possible: for k < n, outs[k] (device, caller-owned) receives the input
+ * frontier rows of node type ntypes[k].  ntypes: host int32 [n]; outs: host
+ * array of n device pointers.  HG_EINVAL if any type is featureless.
+ * Asynchronous on `stream`. */
+hg_status hg_gather_features_multi(hg_graph *graph, const hg_blocks *blocks,
+                                   const int32_t *ntypes, void *const *outs,
+                                   int32_t n, hipStream_t stream);
 
 /* out[i, :] = feat_ntype[ids[i], :] for i < n (ids: device int64 [n]).
  * Asynchronous; an id outside [0, num_nodes) yields a zero row. */

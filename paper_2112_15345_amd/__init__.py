@@ -32,7 +32,8 @@ _DTYPE_CODE = {torch.float32: HG_DT_F32, torch.float16: HG_DT_F16,
 # Every entry point declared in include/hg.h.
 ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_ex",
                "hg_blocks_num_hops", "hg_blocks_nodes", "hg_blocks_edges",
-               "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_rows",
+               "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_features_multi",
+               "hg_gather_rows",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 
@@ -79,6 +80,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_edges": ([_P, _I32, _I32, _PI64, _PP, _PP, _PP, _PP], _I32),
         "hg_blocks_input_nodes": ([_P, _I32, _PI64, _PP], _I32),
         "hg_gather_features": ([_P, _P, _I32, _P, _P], _I32),
+        "hg_gather_features_multi": ([_P, _P, _P, _P, _I32, _P], _I32),
         "hg_gather_rows": ([_P, _I32, _P, _I64, _P, _P], _I32),
         "hg_blocks_free": ([_P], None),
         "hg_last_error": ([], ctypes.c_char_p),
@@ -293,6 +295,25 @@ class Graph:
                                                  out.data_ptr() if out.numel() else None,
                                                  _stream(stream)))
         return out
+
+    def gather_features_all(self, blocks: Blocks, ntypes=None, stream=None):
+        """Input-frontier rows of every featured node type (or of `ntypes`), in
+        as few launches as possible.  Returns {ntype: tensor}."""
+        if ntypes is None:
+            ntypes = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
+        outs = {}
+        for t in ntypes:
+            feat = self.ntypes[t][1]
+            if feat is None:
+                raise HGError(HG_EINVAL, f"node type {t} has no features")
+            outs[t] = torch.empty((blocks.num_input_nodes(t), feat.shape[1]), dtype=feat.dtype,
+                                  device=self.device)
+        ts = (ctypes.c_int32 * max(len(ntypes), 1))(*ntypes)
+        ps = (ctypes.c_void_p * max(len(ntypes), 1))(
+            *[outs[t].data_ptr() if outs[t].numel() else None for t in ntypes])
+        _check(load_library().hg_gather_features_multi(self._h, blocks.handle, ts, ps,
+                                                       len(ntypes), _stream(stream)))
+        return outs
 
     def gather_rows(self, ntype: int, ids: torch.Tensor, out: torch.Tensor | None = None,
                     stream=None) -> torch.Tensor:

@@ -111,54 +111,76 @@ constexpr int kSpinLimit = 1 << 21;
 
 // Decoupled look-back (single-pass prefix scan) of NV int64 values for tile
 // `tile` of a segment whose first tile is `first`: publishes this tile's
-// aggregate, accumulates predecessors' aggregates until one publishes its
-// inclusive prefix, then publishes its own.  Returns the tile's exclusive
+// aggregate, then wavefront 0 inspects 64 predecessors at a time, summing
+// aggregates back to the nearest predecessor that has published its inclusive
+// prefix; publishes its own inclusive prefix.  Returns the tile's exclusive
 // prefix in every thread.  `agg` must be the same in all threads.
 template <int NV>
 __device__ void tile_lookback(Lookback lb, int64_t tile, int64_t first,
                               uint32_t epoch, const int64_t (&agg)[NV],
                               int64_t (&excl)[NV], int64_t *small,
                               int64_t *lds) {
-  if (threadIdx.x == 0) {
+  int64_t *mine = lb.val + tile * 2 * NV;
+  if (threadIdx.x < kWave) {
+    const int lane = lane_id();
     int64_t ex[NV];
 #pragma unroll
     for (int k = 0; k < NV; ++k) ex[k] = 0;
-    int64_t *mine = lb.val + tile * 2 * NV;
     if (tile > first) {
+      if (lane == 0) {
 #pragma unroll
-      for (int k = 0; k < NV; ++k) mine[k] = agg[k];
-      __threadfence();
-      __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 1u, __ATOMIC_RELEASE,
-                         __HIP_MEMORY_SCOPE_AGENT);
-      for (int64_t j = tile - 1;; --j) {
-        uint32_t f = 0;
-        int spins = 0;
-        for (;;) {
-          f = __hip_atomic_load(&lb.flag[j], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-          if ((f >> 2) == epoch && (f & 3u) != 0) break;
-          if (++spins >= kSpinLimit) break;
-          __builtin_amdgcn_s_sleep(1);
-        }
-        if (spins >= kSpinLimit) {
-          atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), kErrLookback);
-          break;
-        }
-        const int64_t *v = lb.val + j * 2 * NV;
-        const bool inclusive = (f & 3u) == 2;
-#pragma unroll
-        for (int k = 0; k < NV; ++k)
-          ex[k] += __hip_atomic_load(v + (inclusive ? NV : 0) + k, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
-        if (inclusive || j == first) break;
+        for (int k = 0; k < NV; ++k) mine[k] = agg[k];
+        __threadfence();
+        __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 1u, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
       }
+      bool timed_out = false;
+      for (int64_t top = tile - 1;; top -= kWave) {
+        // lane l looks at predecessor top - l; tiles before the segment
+        // count as published with nothing to add
+        const int64_t j = top - lane;
+        uint32_t state = 2;
+        if (j >= first) {
+          int spins = 0;
+          for (;;) {
+            const uint32_t f = __hip_atomic_load(&lb.flag[j], __ATOMIC_ACQUIRE,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+            state = ((f >> 2) == epoch) ? (f & 3u) : 0u;
+            if (state != 0 || ++spins >= kSpinLimit) break;
+            __builtin_amdgcn_s_sleep(1);
+          }
+          if (state == 0) {
+            timed_out = true;
+            state = 2;  // give up on this predecessor
+          }
+        }
+        const uint64_t incl = __ballot(state == 2);
+        // the nearest predecessor with an inclusive prefix ends the walk
+        const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : kWave;
+        int64_t v[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          v[k] = 0;
+          if (lane <= stop && j >= first)
+            v[k] = __hip_atomic_load(lb.val + j * 2 * NV + (state == 2 ? NV : 0) + k,
+                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ex[k] += wave_sum_i64(v[k]);
+        }
+        if (incl) break;
+      }
+      if (__ballot(timed_out) && lane == 0)
+        atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), kErrLookback);
     }
+    if (lane == 0) {
 #pragma unroll
-    for (int k = 0; k < NV; ++k) mine[NV + k] = ex[k] + agg[k];
-    __threadfence();
-    __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 2u, __ATOMIC_RELEASE,
-                       __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-    for (int k = 0; k < NV; ++k) lds[k] = ex[k];
+      for (int k = 0; k < NV; ++k) {
+        mine[NV + k] = ex[k] + agg[k];
+        lds[k] = ex[k];
+      }
+      __threadfence();
+      __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 2u, __ATOMIC_RELEASE,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   __syncthreads();
 #pragma unroll

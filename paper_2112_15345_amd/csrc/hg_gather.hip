@@ -93,24 +93,119 @@ hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
   return hipGetLastError();
 }
 
+// Several gathers in one launch: segment s owns blocks
+// [block_base[s], block_base[s+1]) and moves its rows as k_gather does.
+constexpr int kMaxSegs = 8;
+
+struct GatherSeg {
+  const void *table;
+  int64_t n_rows;
+  const int64_t *ids;
+  int64_t n;
+  void *out;
+  int64_t rv;
+  int64_t block_base;
+};
+
+struct GatherBatch {
+  GatherSeg seg[kMaxSegs];
+  int64_t block_end;
+  int32_t n_seg;
+};
+
+template <typename V>
+__global__ __launch_bounds__(kThreads) void k_gather_multi(GatherBatch B) {
+  int s = 0;
+  while (s + 1 < B.n_seg && int64_t(blockIdx.x) >= B.seg[s + 1].block_base) ++s;
+  const GatherSeg &G = B.seg[s];
+  const int64_t nb = (s + 1 < B.n_seg ? B.seg[s + 1].block_base : B.block_end) - G.block_base;
+  const int64_t blk = int64_t(blockIdx.x) - G.block_base;
+  const int rv = int(G.rv);
+  const V *__restrict__ table = static_cast<const V *>(G.table);
+  V *__restrict__ out = static_cast<V *>(G.out);
+  const int rpp = kThreads / rv;
+  const int r_in = threadIdx.x / rv;
+  const int col = threadIdx.x - r_in * rv;
+  if (r_in >= rpp) return;
+  const int64_t rows_per_block = int64_t(rpp) * kUnroll;
+  for (int64_t r0 = blk * rows_per_block; r0 < G.n; r0 += nb * rows_per_block) {
+    V v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t row = r0 + int64_t(u) * rpp + r_in;
+      v[u] = zero_vec<V>();
+      if (row < G.n) {
+        const int64_t id = G.ids[row];
+        if (id >= 0 && id < G.n_rows) v[u] = table[id * rv + col];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t row = r0 + int64_t(u) * rpp + r_in;
+      if (row < G.n) __builtin_nontemporal_store(v[u], out + row * rv + col);
+    }
+  }
+}
+
+int vec_bytes(const void *table, const void *out, int64_t row_bytes) {
+  const uint64_t align = uint64_t(reinterpret_cast<uintptr_t>(table)) |
+                         uint64_t(reinterpret_cast<uintptr_t>(out)) | uint64_t(row_bytes);
+  if ((align & 15) == 0) return 16;
+  if ((align & 7) == 0) return 8;
+  if ((align & 3) == 0) return 4;
+  if ((align & 1) == 0) return 2;
+  return 1;
+}
+
 }  // namespace
 
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
                          hipStream_t stream) {
   if (n <= 0 || row_bytes <= 0) return hipSuccess;
-  const uint64_t align = uint64_t(reinterpret_cast<uintptr_t>(table)) |
-                         uint64_t(reinterpret_cast<uintptr_t>(out)) |
-                         uint64_t(row_bytes);
-  if ((align & 15) == 0)
-    return launch_typed<u32x4>(table, n_rows, row_bytes, ids, n, out, stream);
-  if ((align & 7) == 0)
-    return launch_typed<u32x2>(table, n_rows, row_bytes, ids, n, out, stream);
-  if ((align & 3) == 0)
-    return launch_typed<uint32_t>(table, n_rows, row_bytes, ids, n, out, stream);
-  if ((align & 1) == 0)
-    return launch_typed<uint16_t>(table, n_rows, row_bytes, ids, n, out, stream);
-  return launch_typed<uint8_t>(table, n_rows, row_bytes, ids, n, out, stream);
+  switch (vec_bytes(table, out, row_bytes)) {
+    case 16: return launch_typed<u32x4>(table, n_rows, row_bytes, ids, n, out, stream);
+    case 8: return launch_typed<u32x2>(table, n_rows, row_bytes, ids, n, out, stream);
+    case 4: return launch_typed<uint32_t>(table, n_rows, row_bytes, ids, n, out, stream);
+    case 2: return launch_typed<uint16_t>(table, n_rows, row_bytes, ids, n, out, stream);
+    default: return launch_typed<uint8_t>(table, n_rows, row_bytes, ids, n, out, stream);
+  }
+}
+
+hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream) {
+  // 16-byte rows of at most kThreads vectors share one launch, up to kMaxSegs
+  // per launch; anything else goes through launch_gather
+  GatherBatch B{};
+  int64_t blocks = 0;
+  auto flush = [&]() -> hipError_t {
+    if (B.n_seg == 0) return hipSuccess;
+    B.block_end = blocks;
+    hipLaunchKernelGGL(k_gather_multi<u32x4>, dim3(unsigned(blocks)), dim3(kThreads), 0,
+                       stream, B);
+    B = GatherBatch{};
+    blocks = 0;
+    return hipGetLastError();
+  };
+  for (int32_t k = 0; k < n_jobs; ++k) {
+    const GatherJob &J = jobs[k];
+    if (J.n <= 0 || J.row_bytes <= 0) continue;
+    const int64_t rv = J.row_bytes / 16;
+    if (vec_bytes(J.table, J.out, J.row_bytes) != 16 || rv > kThreads) {
+      hipError_t e = launch_gather(J.table, J.n_rows, J.row_bytes, J.ids, J.n, J.out, stream);
+      if (e != hipSuccess) return e;
+      continue;
+    }
+    if (B.n_seg == kMaxSegs) {
+      hipError_t e = flush();
+      if (e != hipSuccess) return e;
+    }
+    const int64_t rows_per_block = int64_t(kThreads / rv) * kUnroll;
+    int64_t nb = (J.n + rows_per_block - 1) / rows_per_block;
+    if (nb > 65536) nb = 65536;
+    B.seg[B.n_seg++] = GatherSeg{J.table, J.n_rows, J.ids, J.n, J.out, rv, blocks};
+    blocks += nb;
+  }
+  return flush();
 }
 
 }  // namespace hg

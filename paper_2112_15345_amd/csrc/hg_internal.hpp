@@ -23,7 +23,7 @@ constexpr int64_t kPairTile = int64_t(kTileThreads) * kPairItems;
 constexpr int kCandCap = 512;
 
 // Pairs whose in-edges are all kept and number at most this many are copied
-// by one thread each; larger ones by a wavefront.
+// 64 pairs per wavefront; larger ones by a wavefront each.
 constexpr int64_t kThreadTakeAll = 32;
 
 // Pairs that keep K < deg edges with deg > kHubChunk ("hubs") are sampled in
@@ -117,10 +117,10 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
                              int64_t *small, hipStream_t stream);
 
 // The sampler, one launch: block CSC entries and small take-all pairs (a
-// thread per pair), wavefront pairs (one wavefront each), hub chunks (one
-// wavefront each, the last chunk of a hub finishing its selection).  Writes
-// each pair's kept edges at off[p], grouped by pair, ascending edge ID;
-// marks sources not yet in the frontier in their type's bitmap.
+// wavefront per 64 pairs), wavefront pairs (one wavefront each), hub chunks
+// (one wavefront each, the last chunk of a hub finishing its selection).
+// Writes each pair's kept edges at off[p], grouped by pair, ascending edge
+// ID: source vertex, edge ID, destination local ID.
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t n_types, int64_t n_pairs, int64_t n_wave,
                          int64_t n_chunks, PairArrays pa, uint64_t *cand,
@@ -128,6 +128,13 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t key_bits, int64_t *src_gid, int64_t *eid,
                          int32_t *dst_local, int64_t *indptr_all,
                          hipStream_t stream);
+
+// Sets the bitmap bit of every kept edge's source that is not in the
+// frontier of its type yet (edges of etype e are [ebase[e], ebase[e+1]),
+// ebase = small + kSlotNew + n_types).
+hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
+                       int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
+                       hipStream_t stream);
 
 // Compaction pass, one launch: per bitmap tile, ranks of the set bits within
 // the node type (single-pass scan) -> local IDs n_frontier + rank, written to
@@ -166,6 +173,18 @@ hipError_t launch_check_etype(const int64_t *indptr, int64_t n_dst,
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
                          hipStream_t stream);
+
+// One row gather of launch_gather_multi.
+struct GatherJob {
+  const void *table;
+  int64_t n_rows;
+  int64_t row_bytes;
+  const int64_t *ids;
+  int64_t n;
+  void *out;
+};
+// Several row gathers, as few launches as possible.
+hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream);
 
 // Philox4x32-10 on n counters.
 hipError_t launch_philox(const uint32_t *ctr, uint64_t key, int64_t n,

@@ -2,14 +2,15 @@
 // workspaces, per-hop orchestration of the gfx950 kernels, and error state.
 //
 // One mini-batch (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2.2) runs
-// hop by hop, four launches per hop on the caller's stream:
+// hop by hop, five launches per hop on the caller's stream:
 //   1. counting pass : per (frontier vertex, etype) pair its kept-edge count
 //                      and output offsets (single-pass scan)   -> wait (sizes)
-//   2. sampler       : the kept edges; new sources set a bitmap bit
-//   3. compaction    : new vertices numbered in ascending ID, frontier copied
+//   2. sampler       : the kept edges
+//   3. marks         : sources not yet in the frontier set a bitmap bit
+//   4. compaction    : new vertices numbered in ascending ID, frontier copied
 //                      to the head of the source lists; the last block plans
 //                      the next hop's pairs on the device
-//   4. relabel       : edges get local source IDs
+//   5. relabel       : edges get local source IDs
 // The source list of hop h is the frontier of hop h+1.  The host waits once
 // per hop (after 1, for the output sizes) and once at the end.
 #include "hg.h"
@@ -614,6 +615,8 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, pa, cand, ws->dsmall, sigma,
                            h, key_bits, gid_tmp, eid_all, dstl_all, indptr_all, stream)) != hipSuccess)
       return fail_hip(e, "sample");
+    if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
+      return fail_hip(e, "mark");
     if ((e = launch_compact(hv, nv, ws->d_ts, ws->d_es, T, R, ws->bitmap, g->d_tile_base,
                             g->n_tiles, copy_total, ws->lb_bits, next_epoch(), ticket_base,
                             done_base, ws->dsmall, &compact_blocks, stream)) != hipSuccess)
@@ -919,6 +922,32 @@ hg_status hg_gather_features(hg_graph *g, const hg_blocks *b, int32_t ntype,
   if (ntype < 0 || ntype >= g->T)
     return fail(HG_EINVAL, "hg_gather_features: node type %d out of range", ntype);
   return hg_gather_rows(g, ntype, b->in_gid[ntype], b->in_n[ntype], out, stream);
+}
+
+hg_status hg_gather_features_multi(hg_graph *g, const hg_blocks *b,
+                                   const int32_t *ntypes, void *const *outs,
+                                   int32_t n, hipStream_t stream) {
+  if (!g || !b) return fail(HG_EINVAL, "hg_gather_features_multi: NULL graph or blocks");
+  if (b->g != g) return fail(HG_EINVAL, "hg_gather_features_multi: blocks come from another graph");
+  if (n < 0 || (n > 0 && (!ntypes || !outs)))
+    return fail(HG_EINVAL, "hg_gather_features_multi: bad type or output arrays");
+  std::vector<GatherJob> jobs;
+  for (int32_t k = 0; k < n; ++k) {
+    const int32_t t = ntypes[k];
+    if (t < 0 || t >= g->T)
+      return fail(HG_EINVAL, "hg_gather_features_multi: node type %d out of range", t);
+    const NTypeInfo &N = g->nt[t];
+    if (N.dtype == HG_DT_NONE || N.row_bytes <= 0)
+      return fail(HG_EINVAL, "hg_gather_features_multi: node type %d has no features", t);
+    if (b->in_n[t] > 0 && !outs[k])
+      return fail(HG_EINVAL, "hg_gather_features_multi: output %d is NULL", k);
+    jobs.push_back(GatherJob{N.feat, N.num_nodes, N.row_bytes, b->in_gid[t], b->in_n[t], outs[k]});
+  }
+  DeviceGuard dg(g->device);
+  clear_pending_error();
+  hipError_t e = launch_gather_multi(jobs.data(), int32_t(jobs.size()), stream);
+  if (e != hipSuccess) return fail_hip(e, "gather");
+  return HG_OK;
 }
 
 void hg_blocks_free(hg_blocks *b) {

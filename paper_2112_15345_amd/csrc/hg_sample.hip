@@ -182,8 +182,6 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 
 struct EmitCtx {
   const int64_t *indices;
-  const int32_t *src_map;
-  uint32_t *src_bitmap;
   int64_t *src_gid;
   int64_t *eid;
   int32_t *dst_local;
@@ -193,23 +191,15 @@ struct EmitCtx {
 __device__ __forceinline__ EmitCtx make_ctx(const EtypeStatic &E, int64_t *src_gid,
                                             int64_t *eid, int32_t *dst_local,
                                             int64_t dst) {
-  return EmitCtx{E.indices, E.src_map, E.src_bitmap, src_gid, eid, dst_local,
-                 int32_t(dst)};
+  return EmitCtx{E.indices, src_gid, eid, dst_local, int32_t(dst)};
 }
 
-// Writes kept edge `e` at output slot `pos` and marks its source as new when
-// it is not in the frontier of its type yet.
+// Writes kept edge `e` at output slot `pos`.
 __device__ __forceinline__ void emit_edge(const EmitCtx &c, int64_t pos,
                                           int64_t e) {
-  const int64_t g = c.indices[e];
-  c.src_gid[pos] = g;
+  c.src_gid[pos] = c.indices[e];
   c.eid[pos] = e;
   c.dst_local[pos] = c.dst;
-  if (c.src_map[g] < 0) {
-    uint32_t *w = c.src_bitmap + (g >> 5);
-    const uint32_t bit = 1u << (g & 31);
-    if ((*w & bit) == 0) atomicOr(w, bit);
-  }
 }
 
 // Keys of the four edges 4g .. 4g+3.
@@ -332,27 +322,67 @@ struct SampleArgs {
   int64_t *indptr_all;
 };
 
-// Role A: a thread per pair.  Writes the pair's block-CSC entry and copies the
-// in-edges of a small take-all pair.  The first n_etypes+1 threads of block 0
-// also write each etype's closing CSC entry.
-__device__ void role_thread_pairs(const SampleArgs &A) {
+// Role A: a wavefront per 64 consecutive pairs.  Each lane writes its pair's
+// block-CSC entry; then the wavefront copies the in-edges of the small
+// take-all pairs among the 64, one output slot per lane.  Block 0 also writes
+// each etype's closing CSC entry.
+struct GroupLds {
+  int64_t start[kWave];   // first output slot of the pair
+  int64_t lo[kWave];      // first in-edge slot
+  int32_t tpre[kWave + 1];  // prefix of take-all slots over the group
+  int32_t dst[kWave];
+  int32_t etype[kWave];
+};
+
+__device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group) {
+  const int lane = lane_id();
   const int64_t *ebase = A.small + kSlotNew + A.n_types;
   const int64_t *pb = A.hv.pair_base;
   if (blockIdx.x == 0)
     for (int e = threadIdx.x; e < A.n_etypes; e += kSampleThreads)
       A.indptr_all[pb[e + 1] + e] = ebase[e + 1] - ebase[e];
-  const int64_t p = int64_t(blockIdx.x) * kSampleThreads + threadIdx.x;
-  if (p >= A.n_pairs) return;
-  const int e = find_segment(pb, A.n_etypes, p);
-  const int64_t i = p - pb[e];
-  const int64_t o = A.pa.off[p];
-  A.indptr_all[pb[e] + e + i] = o - ebase[e];
-  const int64_t s = A.pa.off[p + 1] - o;
-  const int64_t deg = A.pa.pdeg[p];
-  if (s == 0 || s != deg || deg > kThreadTakeAll) return;
-  const int64_t lo = A.pa.plo[p];
-  const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local, i);
-  for (int64_t j = 0; j < deg; ++j) emit_edge(c, o + j, lo + j);
+  const int64_t p = group * kWave + lane;
+  int take = 0;
+  if (p < A.n_pairs) {
+    const int e = find_segment(pb, A.n_etypes, p);
+    const int64_t i = p - pb[e];
+    const int64_t o = A.pa.off[p];
+    A.indptr_all[pb[e] + e + i] = o - ebase[e];
+    const int64_t s = A.pa.off[p + 1] - o;
+    if (s > 0 && s == A.pa.pdeg[p] && s <= kThreadTakeAll) {
+      take = int(s);
+      L.start[lane] = o;
+      L.lo[lane] = A.pa.plo[p];
+      L.dst[lane] = int32_t(i);
+      L.etype[lane] = e;
+    }
+  }
+  int total;
+  // exclusive prefix of the take-all slot counts over the lanes
+  const int64_t inc = wave_incl_scan_i64(take);
+  L.tpre[lane] = int32_t(inc - take);
+  total = __shfl(int(inc), kWave - 1, kWave);
+  if (lane == kWave - 1) L.tpre[kWave] = total;
+  wave_sync();
+  for (int t0 = 0; t0 < total; t0 += kWave) {
+    const int t = t0 + lane;
+    if (t >= total) break;
+    // the lane q whose take-all range holds slot t
+    int a = 0, b = kWave;
+    while (b - a > 1) {
+      const int m = (a + b) >> 1;
+      if (L.tpre[m] <= t)
+        a = m;
+      else
+        b = m;
+    }
+    const int k = t - L.tpre[a];
+    const int64_t ed = L.lo[a] + k;
+    const int64_t pos = L.start[a] + k;
+    A.src_gid[pos] = A.es[L.etype[a]].indices[ed];
+    A.eid[pos] = ed;
+    A.dst_local[pos] = L.dst[a];
+  }
 }
 
 // Role B: a wavefront per pair (large take-all, or selection among at most
@@ -537,19 +567,39 @@ __device__ void role_hub_chunks(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
 }
 
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
-  __shared__ uint32_t s_key[kSampleWaves][kCandCap];
+  __shared__ __align__(16) uint32_t s_key[kSampleWaves][kCandCap];
   __shared__ uint32_t s_j[kSampleWaves][kCandCap];
   __shared__ uint8_t s_sel[kSampleWaves][kCandCap];
   const int64_t b = blockIdx.x;
   const int wave = threadIdx.x / kWave;
   if (b < A.blocks_a) {
-    role_thread_pairs(A);
+    // the candidate lists are not used by this role: reuse their LDS
+    GroupLds *g = reinterpret_cast<GroupLds *>(&s_key[wave][0]);
+    role_pair_groups(A, *g, b * kSampleWaves + wave);
   } else if (b < A.blocks_a + A.blocks_b) {
     const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
     if (w < A.n_wave) role_wave_pairs(A, s_key[wave], s_j[wave], w);
   } else {
     const int64_t chunk = (b - A.blocks_a - A.blocks_b) * kSampleWaves + wave;
     if (chunk < A.n_chunks) role_hub_chunks(A, s_key[wave], s_j[wave], s_sel[wave], chunk);
+  }
+}
+
+// ---- new-vertex marks ----------------------------------------------------------
+
+// Sets bit v of the source type's bitmap for every kept edge whose source v
+// is not in the frontier of its type yet (map[v] < 0).
+__global__ void k_mark(const EtypeStatic *es, const int64_t *ebase,
+                       int32_t n_etypes, int64_t n_edges,
+                       const int64_t *src_gid) {
+  for (int64_t j = grid_stride_start(); j < n_edges; j += grid_stride_step()) {
+    const int e = find_segment(ebase, n_etypes, j);
+    const int64_t g = src_gid[j];
+    if (es[e].src_map[g] < 0) {
+      uint32_t *w = es[e].src_bitmap + (g >> 5);
+      const uint32_t bit = 1u << (g & 31);
+      if ((*w & bit) == 0) atomicOr(w, bit);
+    }
   }
 }
 
@@ -640,6 +690,8 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.n_chunks = n_chunks;
   // role A always has a block, for the closing CSC entries
   A.blocks_a = std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads);
+  static_assert(sizeof(GroupLds) <= sizeof(uint32_t) * kCandCap,
+                "a group's LDS fits in one wavefront's candidate list");
   A.blocks_b = (n_wave + kSampleWaves - 1) / kSampleWaves;
   const int64_t blocks_c = (n_chunks + kSampleWaves - 1) / kSampleWaves;
   A.pa = pa;
@@ -655,6 +707,15 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   const int64_t blocks = A.blocks_a + A.blocks_b + blocks_c;
   hipLaunchKernelGGL(k_sample, dim3(unsigned(blocks)), dim3(kSampleThreads), 0,
                      stream, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
+                       int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
+                       hipStream_t stream) {
+  if (n_edges <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_mark, dim3(grid_for(n_edges, 256)), dim3(256), 0, stream, es,
+                     small + kSlotNew + n_types, n_etypes, n_edges, src_gid);
   return hipGetLastError();
 }
 

@@ -65,7 +65,12 @@ def test_random_heterographs(olib, chunk):
         assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
         fails = pins.check_blocks(nn, ets, seeds, fanouts, sigma, bits, got, brute=False)
         assert not fails, "\n".join(fails[:5])
-        # gather of the input frontier, every type with features
+        # gather of the input frontier, every type with features (one call)
+        featured = [t for t, f in enumerate(feats) if f is not None]
+        allx = g.gather_features_all(b, featured)
+        for t in featured:
+            assert allx[t].cpu().numpy().tobytes() == feats[t][got["input"][t]].tobytes()
+        # and per type
         for t, f in enumerate(feats):
             if f is None:
                 with pytest.raises(hg.HGError):

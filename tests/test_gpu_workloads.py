@@ -51,10 +51,11 @@ def test_workload_parity(idx, batches):
         ref = host.sample_blocks(seeds, fan, b)
         diffs = compare(ref, got, g.T, g.R, len(fan))
         assert not diffs, f"batch {b}: " + "\n".join(diffs[:10])
+        allx = g.gather_features_all(blocks)
         for t, f in enumerate(gen.feats):
             if f is None:
                 continue
-            x = g.gather_features(blocks, t)
+            x = allx[t]
             ids = ref["input"][t]
             want = host.gather(t, ids)
             assert x.contiguous().view(torch.uint8).cpu().numpy().tobytes() == want.tobytes(), \
