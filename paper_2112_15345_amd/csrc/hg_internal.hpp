@@ -9,10 +9,10 @@
 
 namespace hg {
 
-// Bitmap tiles: 256 threads x 8 words.
+// Bitmap tiles: 256 threads x 2 words.
 constexpr int kTileThreads = 256;
-constexpr int kTileItems = 8;
-constexpr int64_t kTile = int64_t(kTileThreads) * kTileItems;  // 2048 words
+constexpr int kTileItems = 2;
+constexpr int64_t kTile = int64_t(kTileThreads) * kTileItems;  // 512 words
 
 // Pair tiles of the counting pass: 256 threads x 2 pairs.
 constexpr int kPairItems = 2;
@@ -33,7 +33,7 @@ constexpr int64_t kHubChunk = 2048;
 // Readback slots of the small device buffer (int64 each).
 constexpr int kSlotErr = 0;     // error bits in the low int32
 constexpr int kSlotTicket = 1;  // tile tickets of the single-pass scans
-constexpr int kSlotDone = 2;    // finished blocks of the compaction pass
+constexpr int kSlotSpare = 2;
 constexpr int kSlotPairs = 3;   // pairs of the hop
 constexpr int kSlotEdges = 4;   // kept edges of the hop
 constexpr int kSlotHubs = 5;    // hub pairs
@@ -44,7 +44,7 @@ constexpr int kSlotNew = 8;     // n_new[T], then ebase[R+1]
 constexpr int32_t kErrSeedRange = 1;   // a frontier vertex out of range
 constexpr int32_t kErrSeedRepeat = 2;  // a vertex twice in a frontier
 constexpr int32_t kErrLookback = 4;    // a scan wait exceeded its bound
-constexpr int32_t kErrBound = 8;       // more pairs than the launch was sized for
+constexpr int32_t kErrBound = 8;       // more pairs or chunks than buffers were sized for
 
 // Static per edge type (per workspace).
 struct EtypeStatic {
@@ -66,7 +66,7 @@ struct TypeStatic {
 
 // One hop, as device arrays.  Host-written: frontier, src_out, fanout.
 // nF and pair_base are written by the host for hop 0 and by the previous
-// hop's compaction pass afterwards.
+// hop's relabel pass afterwards.
 struct HopView {
   int64_t *nF;                  // [T] frontier sizes
   int64_t *pair_base;           // [R+1] pairs of etype e: [pair_base[e], pair_base[e+1])
@@ -75,15 +75,17 @@ struct HopView {
   const int32_t *fanout;        // [R]
 };
 
-// Status and values of a single-pass (decoupled look-back) scan of NV int64
-// values: per tile a flag (epoch << 2 | state, state 1 = aggregate ready,
-// 2 = inclusive prefix ready) and 2*NV values (aggregate, inclusive).
+// Words of a single-pass (decoupled look-back) scan of NV values: per tile
+// 2*NV 64-bit words, each epoch (20 bits) | state (2 bits) | value (42
+// bits); state 1 = aggregate, 2 = inclusive prefix.  Epochs run 1 .. 2^20-1;
+// the words are zeroed before an epoch is reused.
 struct Lookback {
-  uint32_t *flag;
-  int64_t *val;
+  uint64_t *word;
 };
+constexpr uint32_t kEpochLimit = 1u << 20;
 
-// Per-pair arrays of one hop (device).  Offsets have n_items entries.
+// Per-pair arrays of one hop (device).  Per-pair arrays have n_items
+// entries; clist has clist_cap.
 struct PairArrays {
   int64_t *plo;      // first in-edge slot
   int64_t *pdeg;     // in-degree
@@ -91,8 +93,12 @@ struct PairArrays {
   int64_t *choff;    // exclusive scan of hub chunks
   int64_t *woff;     // exclusive scan of wavefront pairs
   int64_t *hoff;     // exclusive scan of hub flags (= hub ID)
+  int32_t *pet;      // edge type of the pair
+  int64_t *wlist;    // the pair of each wavefront pair, in pair order
+  int64_t *clist;    // the pair of each hub chunk, in pair order
+  int64_t clist_cap;
   int32_t *hub_cnt;  // per hub: candidates appended
-  int32_t *hub_done; // per hub: chunks finished
+  int64_t *hub_pair; // per hub: its pair
 };
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
@@ -116,17 +122,18 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
                              Lookback lb, uint32_t epoch, uint64_t ticket_base,
                              int64_t *small, hipStream_t stream);
 
-// The sampler, one launch: block CSC entries and small take-all pairs (a
-// wavefront per 64 pairs), wavefront pairs (one wavefront each), hub chunks
-// (one wavefront each, the last chunk of a hub finishing its selection).
-// Writes each pair's kept edges at off[p], grouped by pair, ascending edge
-// ID: source vertex, edge ID, destination local ID.
+// The sampler, two launches.  First: block CSC entries and small take-all
+// pairs (a wavefront per 64 pairs), wavefront pairs (one wavefront each) and
+// hub chunks (one wavefront each, appending candidates to the hub's list).
+// Then one wavefront per hub selects from its list.  Writes each pair's kept
+// edges at off[p], grouped by pair, ascending edge ID: source vertex, edge
+// ID, destination local ID.
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t n_types, int64_t n_pairs, int64_t n_wave,
-                         int64_t n_chunks, PairArrays pa, uint64_t *cand,
-                         const int64_t *small, uint64_t sigma, int32_t hop,
-                         int32_t key_bits, int64_t *src_gid, int64_t *eid,
-                         int32_t *dst_local, int64_t *indptr_all,
+                         int64_t n_chunks, int64_t n_hubs, PairArrays pa,
+                         uint64_t *cand, const int64_t *small, uint64_t sigma,
+                         int32_t hop, int32_t key_bits, int64_t *src_gid,
+                         int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          hipStream_t stream);
 
 // Sets the bitmap bit of every kept edge's source that is not in the
@@ -138,21 +145,21 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
 
 // Compaction pass, one launch: per bitmap tile, ranks of the set bits within
 // the node type (single-pass scan) -> local IDs n_frontier + rank, written to
-// the map and the source list, bits cleared; extra blocks copy the frontier
-// into the head of the source lists; the last block to finish writes n_new
-// and the next hop's frontier sizes and pair layout into `next`.
-hipError_t launch_compact(HopView hv, HopView next, const TypeStatic *ts,
-                          const EtypeStatic *es, int32_t n_types,
-                          int32_t n_etypes, uint32_t *bitmap,
-                          const int64_t *tile_base, int64_t n_tiles,
-                          int64_t copy_total, Lookback lb, uint32_t epoch,
-                          uint64_t ticket_base, uint64_t done_base,
-                          int64_t *small, int32_t *blocks_launched,
-                          hipStream_t stream);
+// the map and the source list, bits cleared; the last tile of each type
+// writes its new-vertex count to small[kSlotNew + t]; extra blocks copy the
+// frontier into the head of the source lists.
+hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
+                          uint32_t *bitmap, const int64_t *tile_base,
+                          int64_t n_tiles, int64_t copy_total, Lookback lb,
+                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
+                          int32_t *blocks_launched, hipStream_t stream);
 
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.
-hipError_t launch_relabel(const EtypeStatic *es, const int64_t *small,
+// Block 0 also writes the next hop's frontier sizes (this hop's plus its new
+// vertices) and pair layout into `next`.
+hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
+                          const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
                           hipStream_t stream);

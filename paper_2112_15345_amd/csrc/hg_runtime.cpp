@@ -123,14 +123,15 @@ struct Workspace {
   int64_t *hsmall = nullptr;       // pinned mirror of dsmall
   EtypeStatic *d_es = nullptr;     // static per-etype table
   TypeStatic *d_ts = nullptr;      // static per-type table
-  Lookback lb_bits{};              // look-back state of the compaction pass
+  uint64_t *lb_bits = nullptr;     // look-back words of the compaction pass
   Scratch tab;                     // per-hop tables (device)
   char *htab = nullptr;            // per-hop tables (pinned host)
   size_t htab_cap = 0;
-  Scratch pairs, lb_flags, lb_vals, edges, cand;
-  uint32_t epoch = 0;              // look-back launches so far
+  Scratch pairs, lb_pairs, edges, cand;
+  uint32_t epoch = 0;              // look-back launches so far (mod kEpochLimit)
   hipEvent_t done = nullptr;
   bool busy = false;
+  bool poisoned = false;           // device state unknown: never reuse
 };
 
 }  // namespace
@@ -146,6 +147,7 @@ struct hg_graph {
   std::vector<int64_t> tile_base;  // [T+1] bitmap tiles of each type
   int64_t n_tiles = 0;
   int64_t *d_tile_base = nullptr;  // device copy of tile_base
+  int64_t total_nnz = 0;
   std::mutex mu;
   std::vector<Workspace *> ws;
 };
@@ -253,12 +255,10 @@ void free_workspace(Workspace *w) {
   (void)hipFree(w->dsmall);
   (void)hipFree(w->d_es);
   (void)hipFree(w->d_ts);
-  (void)hipFree(w->lb_bits.flag);
-  (void)hipFree(w->lb_bits.val);
+  (void)hipFree(w->lb_bits);
   w->tab.release();
   w->pairs.release();
-  w->lb_flags.release();
-  w->lb_vals.release();
+  w->lb_pairs.release();
   w->edges.release();
   w->cand.release();
   if (w->hsmall) (void)hipHostFree(w->hsmall);
@@ -296,13 +296,12 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
     if (e == hipSuccess) e = hipMalloc(&w->d_es, sizeof(EtypeStatic) * size_t(std::max(g->R, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->d_ts, sizeof(TypeStatic) * size_t(g->T));
-    if (e == hipSuccess) e = hipMalloc(&w->lb_bits.flag, sizeof(uint32_t) * size_t(n_lb));
-    if (e == hipSuccess) e = hipMalloc(&w->lb_bits.val, sizeof(int64_t) * 2 * size_t(n_lb));
+    if (e == hipSuccess) e = hipMalloc(&w->lb_bits, sizeof(uint64_t) * 2 * size_t(n_lb));
     if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void **>(&w->hsmall), sizeof(int64_t) * small_n, 0);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming);
     if (e == hipSuccess) e = launch_fill_i32(w->map, map_n, -1, stream);
     if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
-    if (e == hipSuccess) e = launch_fill_u32(w->lb_bits.flag, n_lb, 0u, stream);
+    if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t *>(w->lb_bits), 4 * n_lb, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
       for (int32_t i = 0; i < g->R; ++i) {
@@ -362,6 +361,16 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
 }
 
 void release_workspace(hg_graph *g, Workspace *w, hipStream_t stream) {
+  if (w->poisoned) {
+    // its map or bitmap may be dirty: drop it; the next call makes a new one
+    (void)hipStreamSynchronize(stream);
+    {
+      std::lock_guard<std::mutex> lk(g->mu);
+      g->ws.erase(std::remove(g->ws.begin(), g->ws.end(), w), g->ws.end());
+    }
+    free_workspace(w);
+    return;
+  }
   (void)hipEventRecord(w->done, stream);
   std::lock_guard<std::mutex> lk(g->mu);
   w->busy = false;
@@ -389,7 +398,7 @@ struct SampleRun {
   int32_t key_bits;
   const int32_t *fanouts;
   RegionLayout lay;
-  uint64_t ticket_base = 0, done_base = 0;
+  uint64_t ticket_base = 0;
 
   // the map holds the frontier of region `map_region` (at most map_bound
   // vertices in all; the exact sizes are in the region) until the call ends;
@@ -422,10 +431,21 @@ struct SampleRun {
                           to - from, hipMemcpyHostToDevice, stream);
   }
 
-  uint32_t next_epoch() {
-    ws->epoch = (ws->epoch + 1) & 0x3FFFFFFFu;
-    if (ws->epoch == 0) ws->epoch = 1;
-    return ws->epoch;
+  // A fresh epoch for a look-back launch.  Before epochs repeat, every
+  // look-back word is zeroed, so no stale word can pass for a current one.
+  hipError_t next_epoch(uint32_t *epoch) {
+    ws->epoch += 1;
+    if (ws->epoch >= kEpochLimit) {
+      ws->epoch = 1;
+      hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t *>(ws->lb_bits),
+                                     4 * std::max<int64_t>(g->n_tiles, 1), 0u, stream);
+      if (e == hipSuccess && ws->lb_pairs.p)
+        e = launch_fill_u32(static_cast<uint32_t *>(ws->lb_pairs.p),
+                            int64_t(ws->lb_pairs.cap / sizeof(uint32_t)), 0u, stream);
+      if (e != hipSuccess) return e;
+    }
+    *epoch = ws->epoch;
+    return hipSuccess;
   }
 
   hipError_t sync_small() {
@@ -439,16 +459,20 @@ struct SampleRun {
     const int32_t err = int32_t(ws->hsmall[kSlotErr]);
     if (err & (kErrSeedRange | kErrSeedRepeat))
       return fail(HG_EINVAL, "seeds: out of range or repeated within a node type");
-    if (err)
+    if (err) {
+      ws->poisoned = true;
       return fail(HG_EDEVICE, "%s: device check failed (flags %d)", where, err);
+    }
     return HG_OK;
   }
 
   // Undoes the map and bitmap state; releases the workspace.
   void finish(bool ok) {
-    if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
-    if (map_region >= 0)
-      (void)launch_reset_map(view(map_region), ws->d_ts, T, map_bound, stream);
+    if (!ws->poisoned) {
+      if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
+      if (map_region >= 0)
+        (void)launch_reset_map(view(map_region), ws->d_ts, T, map_bound, stream);
+    }
     if (!ok && b) {
       for (void *p : b->allocs) dev_free(g, p, stream);
       delete b;
@@ -456,6 +480,12 @@ struct SampleRun {
     }
     release_workspace(g, ws, stream);
     ws = nullptr;
+  }
+
+  // A failed launch, copy or wait: the device state is unknown.
+  hg_status fail_device(hipError_t e, const char *what) {
+    ws->poisoned = true;
+    return fail_hip(e, what);
   }
 
   hg_status run(const int64_t *const *seeds, const int64_t *n_seeds);
@@ -500,15 +530,15 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   if ((e = launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall), 2 * int64_t(small_slots(g)), 0,
                            stream)) != hipSuccess ||
       (e = upload(0, lay.size)) != hipSuccess)
-    return fail_hip(e, "start");
+    return fail_device(e, "start");
   int64_t total = 0;
   for (int64_t n : nF) total += n;
   map_region = 0;
   map_bound = total;
   if ((e = launch_insert_frontier(view(0), ws->d_ts, T, total, ws->dsmall, stream)) != hipSuccess)
-    return fail_hip(e, "insert seeds");
+    return fail_device(e, "insert seeds");
   if (H == 0) {
-    if ((e = sync_small()) != hipSuccess) return fail_hip(e, "sync");
+    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
     hg_status st = check_flags("seeds");
     if (st != HG_OK) return st;
   }
@@ -525,26 +555,30 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     pc.add(&pa.choff, n_items);
     pc.add(&pa.woff, n_items);
     pc.add(&pa.hoff, n_items);
+    pc.add(&pa.pet, n_items);
+    pc.add(&pa.wlist, n_items);
+    // hub chunks: at most one per pair plus one per kHubChunk edges
+    pa.clist_cap = n_items + g->total_nnz / kHubChunk + 1;
+    pc.add(&pa.clist, pa.clist_cap);
     pc.add(&pa.hub_cnt, n_items);
-    pc.add(&pa.hub_done, n_items);
-    Lookback lb;
+    pc.add(&pa.hub_pair, n_items);
     if (!pc.in_scratch(ws->pairs, stream) ||
-        !ws->lb_flags.ensure(sizeof(uint32_t) * size_t(tiles), stream) ||
-        !ws->lb_vals.ensure(sizeof(int64_t) * 8 * size_t(tiles), stream))
+        !ws->lb_pairs.ensure(sizeof(uint64_t) * 8 * size_t(tiles), stream))
       return fail(HG_ENOMEM, "hop %d: pair scratch", h);
-    lb.flag = static_cast<uint32_t *>(ws->lb_flags.p);
-    lb.val = static_cast<int64_t *>(ws->lb_vals.p);
-    // a new flag buffer starts with no tile published
-    if (ws->lb_flags.fresh &&
-        (e = launch_fill_u32(lb.flag, int64_t(ws->lb_flags.cap / sizeof(uint32_t)), 0u,
-                             stream)) != hipSuccess)
-      return fail_hip(e, "fill");
-    if ((e = launch_count_scan(hv, ws->d_es, R, T, n_items, pa, lb, next_epoch(), ticket_base,
+    Lookback lb{static_cast<uint64_t *>(ws->lb_pairs.p)};
+    // new look-back words start with no tile published
+    if (ws->lb_pairs.fresh &&
+        (e = launch_fill_u32(static_cast<uint32_t *>(ws->lb_pairs.p),
+                             int64_t(ws->lb_pairs.cap / sizeof(uint32_t)), 0u, stream)) != hipSuccess)
+      return fail_device(e, "fill");
+    uint32_t epoch;
+    if ((e = next_epoch(&epoch)) != hipSuccess ||
+        (e = launch_count_scan(hv, ws->d_es, R, T, n_items, pa, lb, epoch, ticket_base,
                                ws->dsmall, stream)) != hipSuccess)
-      return fail_hip(e, "count");
+      return fail_device(e, "count");
     ticket_base += uint64_t(tiles);
     // wait: this hop's sizes (and the previous hop's new-vertex counts)
-    if ((e = sync_small()) != hipSuccess) return fail_hip(e, "sync");
+    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
     hg_status st = check_flags("count");
     if (st != HG_OK) return st;
     const int64_t *hs = ws->hsmall;
@@ -605,32 +639,34 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     for (int32_t i = 0; i < R; ++i)
       hfield<int32_t>(h + 1, lay.fanout)[i] = h + 1 < H ? fanouts[size_t(h + 1) * R + i] : 0;
     if ((e = upload(size_t(h) * lay.size + lay.src_out, size_t(h + 2) * lay.size)) != hipSuccess)
-      return fail_hip(e, "upload");
+      return fail_device(e, "upload");
 
     // ---- 2-4. sample, compact, relabel -------------------------------------
     bitmap_dirty = true;
     int32_t compact_blocks = 0;
     int64_t copy_total = 0;
     for (int64_t n : nF) copy_total += n;
-    if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, pa, cand, ws->dsmall, sigma,
-                           h, key_bits, gid_tmp, eid_all, dstl_all, indptr_all, stream)) != hipSuccess)
-      return fail_hip(e, "sample");
+    if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
+                           sigma, h, key_bits, gid_tmp, eid_all, dstl_all, indptr_all,
+                           stream)) != hipSuccess)
+      return fail_device(e, "sample");
     if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
-      return fail_hip(e, "mark");
-    if ((e = launch_compact(hv, nv, ws->d_ts, ws->d_es, T, R, ws->bitmap, g->d_tile_base,
-                            g->n_tiles, copy_total, ws->lb_bits, next_epoch(), ticket_base,
-                            done_base, ws->dsmall, &compact_blocks, stream)) != hipSuccess)
-      return fail_hip(e, "compact");
+      return fail_device(e, "mark");
+    if ((e = next_epoch(&epoch)) != hipSuccess ||
+        (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
+                            Lookback{ws->lb_bits}, epoch, ticket_base, ws->dsmall,
+                            &compact_blocks, stream)) != hipSuccess)
+      return fail_device(e, "compact");
     ticket_base += uint64_t(compact_blocks);
-    done_base += uint64_t(compact_blocks);
     bitmap_dirty = false;
-    // the map now holds the source lists of this hop (region h+1's frontier);
-    // their sizes are read at the next wait
+    if ((e = launch_relabel(hv, nv, ws->d_es, g->d_tile_base, ws->dsmall, T, R, S, gid_tmp,
+                            srcl_all, stream)) != hipSuccess)
+      return fail_device(e, "relabel");
+    // the map now holds the source lists of this hop, which are region h+1's
+    // frontier; the relabel pass wrote their sizes into that region
     map_region = h + 1;
     map_bound = 0;
     for (int32_t t = 0; t < T; ++t) map_bound += bound[t];
-    if ((e = launch_relabel(ws->d_es, ws->dsmall, T, R, S, gid_tmp, srcl_all, stream)) != hipSuccess)
-      return fail_hip(e, "relabel");
 
     for (int32_t t = 0; t < T; ++t) {
       const size_t k = size_t(h) * T + t;
@@ -653,7 +689,7 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
 
   if (H > 0) {
     // final wait: new-vertex counts of the last hop
-    if ((e = sync_small()) != hipSuccess) return fail_hip(e, "sync");
+    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
     hg_status st = check_flags("compact");
     if (st != HG_OK) return st;
     for (int32_t t = 0; t < T; ++t) {
@@ -676,7 +712,7 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
       if (nF[t] > 0 &&
           (e = hipMemcpyAsync(cp[t], seeds[t], sizeof(int64_t) * size_t(nF[t]),
                               hipMemcpyDeviceToDevice, stream)) != hipSuccess)
-        return fail_hip(e, "seed copy");
+        return fail_device(e, "seed copy");
       b->in_n[t] = nF[t];
       b->in_gid[t] = cp[t];
     }
@@ -749,6 +785,7 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
   for (int32_t i = 0; i < n_etypes; ++i) {
     const hg_etype_desc &d = etypes[i];
     g->et.push_back({d.src_type, d.dst_type, d.nnz, d.indptr, d.indices});
+    g->total_nnz += d.nnz;
   }
   if (!allocator) {
     // keep freed blocks in the stream-ordered pool between calls

@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
     int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
     uint64_t ticket_base, int64_t *small) {
-  __shared__ int64_t lds[8];
+  __shared__ int64_t lds[16];
   const int64_t tile = take_ticket(small, ticket_base, lds);
   const int64_t P = hv.pair_base[n_etypes];
   const int64_t base = tile * kPairTile + threadIdx.x * kPairItems;
@@ -137,8 +137,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     sum[3] += c[k].hub;
   }
   int64_t pre[4], agg[4];
-#pragma unroll
-  for (int a = 0; a < 4; ++a) pre[a] = block_excl_scan_256(sum[a], lds, &agg[a]);
+  block_excl_scan4_256(sum, pre, agg, lds);
   int64_t ex[4];
   tile_lookback<4>(lb, tile, 0, epoch, agg, ex, small, lds);
 #pragma unroll
@@ -153,9 +152,16 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
       pa.choff[p] = pre[1];
       pa.woff[p] = pre[2];
       pa.hoff[p] = pre[3];
+      pa.pet[p] = etype[k];
+      if (c[k].wave) pa.wlist[pre[2]] = p;
       if (c[k].hub) {
         pa.hub_cnt[pre[3]] = 0;
-        pa.hub_done[pre[3]] = 0;
+        pa.hub_pair[pre[3]] = p;
+        if (pre[1] + c[k].nch > pa.clist_cap) {
+          atomicOr(err, kErrBound);
+        } else {
+          for (int64_t q = 0; q < c[k].nch; ++q) pa.clist[pre[1] + q] = p;
+        }
       }
       // edge start of every etype whose first pair (or end, for the last) is p
       if (p <= P) {
@@ -310,7 +316,7 @@ struct SampleArgs {
   HopView hv;
   const EtypeStatic *es;
   int32_t n_etypes, n_types;
-  int64_t n_pairs, n_wave, n_chunks;
+  int64_t n_pairs, n_wave, n_chunks, n_hubs;
   int64_t blocks_a, blocks_b;
   PairArrays pa;
   uint64_t *cand;
@@ -344,7 +350,7 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
   const int64_t p = group * kWave + lane;
   int take = 0;
   if (p < A.n_pairs) {
-    const int e = find_segment(pb, A.n_etypes, p);
+    const int e = A.pa.pet[p];
     const int64_t i = p - pb[e];
     const int64_t o = A.pa.off[p];
     A.indptr_all[pb[e] + e + i] = o - ebase[e];
@@ -390,8 +396,8 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
 __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
                                 int64_t w) {
   const int lane = lane_id();
-  const int64_t p = find_segment(A.pa.woff, int(A.n_pairs), w);
-  const int e = find_segment(A.hv.pair_base, A.n_etypes, p);
+  const int64_t p = A.pa.wlist[w];
+  const int e = A.pa.pet[p];
   const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
                              p - A.hv.pair_base[e]);
   const int64_t lo = A.pa.plo[p];
@@ -470,19 +476,15 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   select_by_bisection(c, lo, deg, K, o, a, b, A.hop, e, k0, k1, shift);
 }
 
-// Role C: a wavefront per hub chunk.  Appends the chunk's candidates to the
-// hub's list; the wavefront finishing the hub's last chunk selects the K
-// smallest of the list and writes them in edge order.
-__device__ void role_hub_chunks(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
-                                uint8_t *sel, int64_t chunk) {
+// Role C: a wavefront per hub chunk appends the chunk's candidates
+// (key < tau) to the hub's list.
+__device__ void role_hub_chunks(const SampleArgs &A, int64_t chunk) {
   const int lane = lane_id();
-  const int64_t p = find_segment(A.pa.choff, int(A.n_pairs), chunk);
-  const int e = find_segment(A.hv.pair_base, A.n_etypes, p);
+  const int64_t p = A.pa.clist[chunk];
+  const int e = A.pa.pet[p];
   const int64_t lo = A.pa.plo[p];
   const int64_t deg = A.pa.pdeg[p];
-  const int64_t o = A.pa.off[p];
-  const int64_t K = A.pa.off[p + 1] - o;
-  const int64_t nch = A.pa.choff[p + 1] - A.pa.choff[p];
+  const int64_t K = A.pa.off[p + 1] - A.pa.off[p];
   const int64_t hub = A.pa.hoff[p];
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
@@ -524,21 +526,40 @@ __device__ void role_hub_chunks(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
       }
     }
   }
-  // publish this chunk's candidates, then count it as done
-  __threadfence();
-  int last = 0;
-  if (lane == 0) last = atomicAdd(A.pa.hub_done + hub, 1) == int(nch - 1);
-  last = __shfl(last, 0, kWave);
-  if (!last) return;
-  __threadfence();
+}
 
+// A wavefront per hub: the K smallest (key, j) of the hub's candidate list,
+// written in edge order.  The list holds every edge with key < tau, so when
+// it has at least K entries they include the K smallest.
+__global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
+  __shared__ uint32_t s_key[kSampleWaves][kCandCap];
+  __shared__ uint32_t s_j[kSampleWaves][kCandCap];
+  __shared__ uint8_t s_sel[kSampleWaves][kCandCap];
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int64_t hub = int64_t(blockIdx.x) * kSampleWaves + wave;
+  if (hub >= A.n_hubs) return;
+  uint32_t *ck = s_key[wave];
+  uint32_t *cj = s_j[wave];
+  uint8_t *sel = s_sel[wave];
+  const int64_t p = A.pa.hub_pair[hub];
+  const int e = A.pa.pet[p];
+  const int64_t lo = A.pa.plo[p];
+  const int64_t deg = A.pa.pdeg[p];
+  const int64_t o = A.pa.off[p];
+  const int64_t K = A.pa.off[p + 1] - o;
+  const uint32_t shift = uint32_t(32 - A.key_bits);
+  const uint64_t key_space = uint64_t(1) << A.key_bits;
+  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
+  const uint64_t tau = cand_threshold(K, deg, key_space);
   const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
                              p - A.hv.pair_base[e]);
-  const int64_t n_cand = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int64_t n_cand = A.pa.hub_cnt[hub];
   if (n_cand >= K && n_cand <= kCandCap) {
+    const uint64_t *list = A.cand + hub * kCandCap;
     const int nc = int(n_cand);
     for (int q = lane; q < nc; q += kWave) {
-      const uint64_t v = __hip_atomic_load(list + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t v = list[q];
       ck[q] = uint32_t(v >> 32);
       cj[q] = uint32_t(v);
     }
@@ -569,7 +590,6 @@ __device__ void role_hub_chunks(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   __shared__ __align__(16) uint32_t s_key[kSampleWaves][kCandCap];
   __shared__ uint32_t s_j[kSampleWaves][kCandCap];
-  __shared__ uint8_t s_sel[kSampleWaves][kCandCap];
   const int64_t b = blockIdx.x;
   const int wave = threadIdx.x / kWave;
   if (b < A.blocks_a) {
@@ -581,25 +601,91 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
     if (w < A.n_wave) role_wave_pairs(A, s_key[wave], s_j[wave], w);
   } else {
     const int64_t chunk = (b - A.blocks_a - A.blocks_b) * kSampleWaves + wave;
-    if (chunk < A.n_chunks) role_hub_chunks(A, s_key[wave], s_j[wave], s_sel[wave], chunk);
+    if (chunk < A.n_chunks) role_hub_chunks(A, chunk);
   }
 }
 
 // ---- new-vertex marks ----------------------------------------------------------
 
 // Sets bit v of the source type's bitmap for every kept edge whose source v
-// is not in the frontier of its type yet (map[v] < 0).
-__global__ void k_mark(const EtypeStatic *es, const int64_t *ebase,
-                       int32_t n_etypes, int64_t n_edges,
-                       const int64_t *src_gid) {
-  for (int64_t j = grid_stride_start(); j < n_edges; j += grid_stride_step()) {
-    const int e = find_segment(ebase, n_etypes, j);
-    const int64_t g = src_gid[j];
-    if (es[e].src_map[g] < 0) {
-      uint32_t *w = es[e].src_bitmap + (g >> 5);
-      const uint32_t bit = 1u << (g & 31);
-      if ((*w & bit) == 0) atomicOr(w, bit);
+// is not in the frontier of its type yet (map[v] < 0).  Popular sources recur
+// across many edges, and atomics on one word serialize, so each block first
+// merges its edges' bits per bitmap word in an LDS hash table and then
+// issues one atomic per distinct word.
+constexpr int kMarkPerThread = 4;
+constexpr int kMarkEdges = 256 * kMarkPerThread;  // edges per block
+constexpr int kMarkSlots = 2048;                  // hash slots (power of two)
+constexpr int kMarkMaxEtypes = 256;               // etype table staged in LDS
+constexpr uint64_t kEmptySlot = ~uint64_t(0);
+
+__global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64_t *ebase,
+                                              int32_t n_etypes, int64_t n_edges,
+                                              const int64_t *src_gid) {
+  __shared__ uint64_t s_key[kMarkSlots];   // word address
+  __shared__ uint32_t s_bits[kMarkSlots];
+  __shared__ int64_t s_eb[kMarkMaxEtypes + 1];
+  __shared__ const int32_t *s_map[kMarkMaxEtypes];
+  __shared__ uint32_t *s_bm[kMarkMaxEtypes];
+  const bool staged = n_etypes <= kMarkMaxEtypes;
+  for (int i = threadIdx.x; i < kMarkSlots; i += blockDim.x) {
+    s_key[i] = kEmptySlot;
+    s_bits[i] = 0;
+  }
+  if (staged)
+    for (int e = threadIdx.x; e <= n_etypes; e += blockDim.x) {
+      s_eb[e] = ebase[e];
+      if (e < n_etypes) {
+        s_map[e] = es[e].src_map;
+        s_bm[e] = es[e].src_bitmap;
+      }
     }
+  __syncthreads();
+  const int64_t j0 = int64_t(blockIdx.x) * kMarkEdges + threadIdx.x;
+  // loads first, all independent, then the table updates
+  int64_t g[kMarkPerThread];
+  int et[kMarkPerThread];
+#pragma unroll
+  for (int k = 0; k < kMarkPerThread; ++k) {
+    const int64_t j = j0 + k * 256;
+    g[k] = -1;
+    et[k] = 0;
+    if (j < n_edges) {
+      et[k] = staged ? find_segment(s_eb, n_etypes, j) : find_segment(ebase, n_etypes, j);
+      g[k] = src_gid[j];
+    }
+  }
+  bool need[kMarkPerThread];
+#pragma unroll
+  for (int k = 0; k < kMarkPerThread; ++k) {
+    need[k] = false;
+    if (g[k] >= 0) {
+      const int32_t *map = staged ? s_map[et[k]] : es[et[k]].src_map;
+      need[k] = map[g[k]] < 0;  // not in the frontier yet
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kMarkPerThread; ++k) {
+    if (!need[k]) continue;
+    uint32_t *bm = staged ? s_bm[et[k]] : es[et[k]].src_bitmap;
+    const uint64_t word = reinterpret_cast<uint64_t>(bm + (g[k] >> 5));
+    const uint32_t bit = 1u << (g[k] & 31);
+    // open addressing on the word address
+    uint32_t h = uint32_t((word >> 2) * 0x9E3779B97F4A7C15ull >> 40) & (kMarkSlots - 1);
+    for (int probe = 0; probe < kMarkSlots; ++probe) {
+      const uint64_t cur = atomicCAS(reinterpret_cast<unsigned long long *>(&s_key[h]),
+                                     (unsigned long long)kEmptySlot,
+                                     (unsigned long long)word);
+      if (cur == kEmptySlot || cur == word) {
+        atomicOr(&s_bits[h], bit);
+        break;
+      }
+      h = (h + 1) & (kMarkSlots - 1);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kMarkSlots; i += blockDim.x) {
+    const uint64_t word = s_key[i];
+    if (word != kEmptySlot) atomicOr(reinterpret_cast<uint32_t *>(word), s_bits[i]);
   }
 }
 
@@ -675,10 +761,10 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
 
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t n_types, int64_t n_pairs, int64_t n_wave,
-                         int64_t n_chunks, PairArrays pa, uint64_t *cand,
-                         const int64_t *small, uint64_t sigma, int32_t hop,
-                         int32_t key_bits, int64_t *src_gid, int64_t *eid,
-                         int32_t *dst_local, int64_t *indptr_all,
+                         int64_t n_chunks, int64_t n_hubs, PairArrays pa,
+                         uint64_t *cand, const int64_t *small, uint64_t sigma,
+                         int32_t hop, int32_t key_bits, int64_t *src_gid,
+                         int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          hipStream_t stream) {
   SampleArgs A;
   A.hv = hv;
@@ -688,6 +774,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.n_pairs = n_pairs;
   A.n_wave = n_wave;
   A.n_chunks = n_chunks;
+  A.n_hubs = n_hubs;
   // role A always has a block, for the closing CSC entries
   A.blocks_a = std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads);
   static_assert(sizeof(GroupLds) <= sizeof(uint32_t) * kCandCap,
@@ -707,6 +794,11 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   const int64_t blocks = A.blocks_a + A.blocks_b + blocks_c;
   hipLaunchKernelGGL(k_sample, dim3(unsigned(blocks)), dim3(kSampleThreads), 0,
                      stream, A);
+  if (n_hubs > 0) {
+    // the hub lists are complete once the first launch has finished
+    const int64_t hb = (n_hubs + kSampleWaves - 1) / kSampleWaves;
+    hipLaunchKernelGGL(k_hub_finish, dim3(unsigned(hb)), dim3(kSampleThreads), 0, stream, A);
+  }
   return hipGetLastError();
 }
 
@@ -714,7 +806,8 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
                        int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
                        hipStream_t stream) {
   if (n_edges <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_mark, dim3(grid_for(n_edges, 256)), dim3(256), 0, stream, es,
+  const int64_t blocks = (n_edges + kMarkEdges - 1) / kMarkEdges;
+  hipLaunchKernelGGL(k_mark, dim3(unsigned(blocks)), dim3(256), 0, stream, es,
                      small + kSlotNew + n_types, n_etypes, n_edges, src_gid);
   return hipGetLastError();
 }
