@@ -73,6 +73,9 @@ def main():
                     help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
                          "5 gather-heavy academic")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="after warm-up (untimed), copy this many MiB device to device "
+                         "once: a copy of known size for scaling memory counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
@@ -99,25 +102,32 @@ def main():
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
     row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
 
+    # HIP events recorded by the gather kernels themselves (on their stream)
+    hip_events = hg.HipEvents(2 * args.steps)
+    rec_events = [(hip_events.events[2 * i], hip_events.events[2 * i + 1])
+                  for i in range(args.steps)][::-1]
+
     def step(b, rec=None):
         blocks = g.sample_blocks(seeds[b], fan, b)
         outs = g.gather_outputs(blocks, feat_types)
+        ev = rec_events.pop() if rec is not None else None
+        g.gather_features_all(blocks, outs=outs, events=ev)
         if rec is not None:
-            e0, e1 = rec_events.pop()
-            e0.record()
-        g.gather_features_all(blocks, outs=outs)
-        if rec is not None:
-            e1.record()
-            rec.append((e0, e1, {t: outs[t].shape[0] for t in feat_types}))
+            rec.append((ev[0], ev[1], {t: outs[t].shape[0] for t in feat_types}))
         return blocks, outs
-
-    rec_events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(args.steps)]
 
     for b in range(args.warmup):
         step(b)
     torch.cuda.synchronize()
     log("warm-up done")
+    if args.copy_calibration_mb > 0:
+        src = torch.ones(args.copy_calibration_mb << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.copy_calibration_mb} MiB done")
+        del src, dst
 
     gather_rec = []
     sample_ms = []
@@ -145,7 +155,7 @@ def main():
 
     # gather kernel (one launch per step for all feature types): algorithmic
     # bytes per row = read its id (8) + read the row + write the row
-    g_ms = sum(e0.elapsed_time(e1) for e0, e1, _ in gather_rec)
+    g_ms = sum(hip_events.elapsed_ms(e0, e1) for e0, e1, _ in gather_rec)
     g_alg = sum(n * (2 * row_bytes[t] + 8) for _, _, rows_t in gather_rec
                 for t, n in rows_t.items())
     g_achieved = g_alg / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0

@@ -179,6 +179,15 @@ hg_status hg_gather_features_multi(hg_graph *graph, const hg_blocks *blocks,
                                    const int32_t *ntypes, void *const *outs,
                                    int32_t n, hipStream_t stream);
 
+/* hg_gather_features_multi, with the 16-byte-vector gather launches
+ * carrying `start` (first launch) and `stop` (last launch) as their own
+ * timestamps (either may be NULL), so that hipEventElapsedTime(start, stop)
+ * is the device time of those kernels.  For benchmarks. */
+hg_status hg_gather_features_multi_timed(hg_graph *graph, const hg_blocks *blocks,
+                                         const int32_t *ntypes, void *const *outs,
+                                         int32_t n, hipStream_t stream,
+                                         hipEvent_t start, hipEvent_t stop);
+
 /* out[i, :] = feat_ntype[ids[i], :] for i < n (ids: device int64 [n]).
  * Asynchronous; an id outside [0, num_nodes) yields a zero row. */
 hg_status hg_gather_rows(hg_graph *graph, int32_t ntype, const int64_t *ids,

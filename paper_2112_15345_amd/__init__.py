@@ -33,7 +33,7 @@ _DTYPE_CODE = {torch.float32: HG_DT_F32, torch.float16: HG_DT_F16,
 ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_ex",
                "hg_blocks_num_hops", "hg_blocks_nodes", "hg_blocks_edges",
                "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_features_multi",
-               "hg_gather_rows",
+               "hg_gather_features_multi_timed", "hg_gather_rows",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 
@@ -81,6 +81,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_input_nodes": ([_P, _I32, _PI64, _PP], _I32),
         "hg_gather_features": ([_P, _P, _I32, _P, _P], _I32),
         "hg_gather_features_multi": ([_P, _P, _P, _P, _I32, _P], _I32),
+        "hg_gather_features_multi_timed": ([_P, _P, _P, _P, _I32, _P, _P, _P], _I32),
         "hg_gather_rows": ([_P, _I32, _P, _I64, _P, _P], _I32),
         "hg_blocks_free": ([_P], None),
         "hg_last_error": ([], ctypes.c_char_p),
@@ -309,10 +310,12 @@ class Graph:
                                   device=self.device)
         return outs
 
-    def gather_features_all(self, blocks: Blocks, ntypes=None, outs=None, stream=None):
+    def gather_features_all(self, blocks: Blocks, ntypes=None, outs=None, stream=None,
+                            events=None):
         """Input-frontier rows of every featured node type (or of `ntypes`), in
         as few launches as possible, into `outs` (made by gather_outputs when
-        not given).  Returns {ntype: tensor}."""
+        not given).  `events`: optional (start, stop) raw hipEvent_t handles
+        that the gather kernels record themselves.  Returns {ntype: tensor}."""
         if outs is None:
             outs = self.gather_outputs(blocks, ntypes)
         ts_list = list(outs.keys())
@@ -320,8 +323,9 @@ class Graph:
         ts = (ctypes.c_int32 * max(n, 1))(*ts_list)
         ps = (ctypes.c_void_p * max(n, 1))(
             *[outs[t].data_ptr() if outs[t].numel() else None for t in ts_list])
-        _check(load_library().hg_gather_features_multi(self._h, blocks.handle, ts, ps, n,
-                                                       _stream(stream)))
+        start, stop = events if events is not None else (None, None)
+        _check(load_library().hg_gather_features_multi_timed(self._h, blocks.handle, ts, ps, n,
+                                                             _stream(stream), start, stop))
         return outs
 
     def gather_rows(self, ntype: int, ids: torch.Tensor, out: torch.Tensor | None = None,
@@ -338,6 +342,36 @@ class Graph:
                                              out.data_ptr() if out.numel() else None,
                                              _stream(stream)))
         return out
+
+
+class HipEvents:
+    """Raw HIP timing events (hipEvent_t) from the HIP runtime, for
+    gather_features_all(events=...)."""
+
+    def __init__(self, n: int):
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                  ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self._hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.events = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            if self._hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise HGError(HG_EDEVICE, "hipEventCreate failed")
+            self.events.append(e.value)
+
+    def elapsed_ms(self, start: int, stop: int) -> float:
+        ms = ctypes.c_float()
+        self._hip.hipEventSynchronize(stop)
+        if self._hip.hipEventElapsedTime(ctypes.byref(ms), start, stop) != 0:
+            raise HGError(HG_EDEVICE, "hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        for e in getattr(self, "events", []):
+            self._hip.hipEventDestroy(e)
 
 
 def debug_philox(ctr: torch.Tensor, key: int, stream=None) -> torch.Tensor:

@@ -8,6 +8,8 @@
 // allow it) of a row; a block covers several rows per pass and keeps kUnroll
 // passes of loads in flight before storing.  Stores bypass the caches
 // (non-temporal), since the output is not re-read by this kernel.
+#include <hip/hip_ext.h>
+
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -172,16 +174,35 @@ hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
   }
 }
 
-hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream) {
+hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream,
+                               hipEvent_t start, hipEvent_t stop) {
   // 16-byte rows of at most kThreads vectors share one launch, up to kMaxSegs
-  // per launch; anything else goes through launch_gather
+  // per launch; anything else goes through launch_gather.  With events, the
+  // batched launches carry them (start on the first, stop on the last), so
+  // they time the kernels themselves.
   GatherBatch B{};
   int64_t blocks = 0;
+  int launches = 0;
+  int64_t pending = 0;  // batched segments still to launch
+  for (int32_t k = 0; k < n_jobs; ++k) {
+    const GatherJob &J = jobs[k];
+    if (J.n > 0 && J.row_bytes > 0 && vec_bytes(J.table, J.out, J.row_bytes) == 16 &&
+        J.row_bytes / 16 <= kThreads)
+      ++pending;
+  }
   auto flush = [&]() -> hipError_t {
     if (B.n_seg == 0) return hipSuccess;
     B.block_end = blocks;
-    hipLaunchKernelGGL(k_gather_multi<u32x4>, dim3(unsigned(blocks)), dim3(kThreads), 0,
-                       stream, B);
+    pending -= B.n_seg;
+    hipEvent_t e0 = launches == 0 ? start : nullptr;
+    hipEvent_t e1 = pending == 0 ? stop : nullptr;
+    if (e0 || e1)
+      hipExtLaunchKernelGGL(k_gather_multi<u32x4>, dim3(unsigned(blocks)), dim3(kThreads), 0,
+                            stream, e0, e1, 0, B);
+    else
+      hipLaunchKernelGGL(k_gather_multi<u32x4>, dim3(unsigned(blocks)), dim3(kThreads), 0,
+                         stream, B);
+    ++launches;
     B = GatherBatch{};
     blocks = 0;
     return hipGetLastError();

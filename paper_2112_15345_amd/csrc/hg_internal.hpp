@@ -190,8 +190,10 @@ struct GatherJob {
   int64_t n;
   void *out;
 };
-// Several row gathers, as few launches as possible.
-hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream);
+// Several row gathers, as few launches as possible.  `start` / `stop` (may be
+// NULL) are recorded by the batched launches themselves.
+hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream,
+                               hipEvent_t start, hipEvent_t stop);
 
 // Philox4x32-10 on n counters.
 hipError_t launch_philox(const uint32_t *ctr, uint64_t key, int64_t n,

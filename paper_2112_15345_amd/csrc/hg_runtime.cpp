@@ -964,6 +964,13 @@ hg_status hg_gather_features(hg_graph *g, const hg_blocks *b, int32_t ntype,
 hg_status hg_gather_features_multi(hg_graph *g, const hg_blocks *b,
                                    const int32_t *ntypes, void *const *outs,
                                    int32_t n, hipStream_t stream) {
+  return hg_gather_features_multi_timed(g, b, ntypes, outs, n, stream, nullptr, nullptr);
+}
+
+hg_status hg_gather_features_multi_timed(hg_graph *g, const hg_blocks *b,
+                                         const int32_t *ntypes, void *const *outs,
+                                         int32_t n, hipStream_t stream, hipEvent_t start,
+                                         hipEvent_t stop) {
   if (!g || !b) return fail(HG_EINVAL, "hg_gather_features_multi: NULL graph or blocks");
   if (b->g != g) return fail(HG_EINVAL, "hg_gather_features_multi: blocks come from another graph");
   if (n < 0 || (n > 0 && (!ntypes || !outs)))
@@ -982,7 +989,7 @@ hg_status hg_gather_features_multi(hg_graph *g, const hg_blocks *b,
   }
   DeviceGuard dg(g->device);
   clear_pending_error();
-  hipError_t e = launch_gather_multi(jobs.data(), int32_t(jobs.size()), stream);
+  hipError_t e = launch_gather_multi(jobs.data(), int32_t(jobs.size()), stream, start, stop);
   if (e != hipSuccess) return fail_hip(e, "gather");
   return HG_OK;
 }
