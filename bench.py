@@ -26,6 +26,25 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 
+# Measured HBM traffic of one gather launch on the default run (academic
+# workload, 3 warm-up + 20 timed mini-batches): FETCH_SIZE and WRITE_SIZE
+# from two rocprofv3 --pmc passes, scaled by what the counters read for a
+# 1 GiB device copy (profiles/gather_academic_traffic.md).  Valid only for
+# the gather source it was measured on.
+GATHER_TRAFFIC = {"source_sha256_16": "321cb231c9462224", "workload": 2, "steps": 20, "warmup": 3,
+                  "bytes_per_launch": 248912521.6}
+
+
+def measured_gather_traffic(workload, steps, warmup):
+    import hashlib
+    src = os.path.join(ROOT, "paper_2112_15345_amd", "csrc", "hg_gather.hip")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    t = GATHER_TRAFFIC
+    if (digest, workload, steps, warmup) != (t["source_sha256_16"], t["workload"], t["steps"],
+                                              t["warmup"]):
+        return None
+    return t["bytes_per_launch"]
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -186,7 +205,10 @@ def main():
         "gather_kernel_ms_per_step": g_ms / args.steps,
         "roofline": {"bound": "hbm", "kernel": "k_gather_multi (feature gather, all types)",
                      "achieved": g_achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": g_achieved / HBM_PEAK_GBS, "traffic": None},
+                     "frac": g_achieved / HBM_PEAK_GBS,
+                     "traffic": measured_gather_traffic(args.workload, args.steps, args.warmup),
+                     "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
+                     "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(gen, wl, first_batch=args.warmup)
