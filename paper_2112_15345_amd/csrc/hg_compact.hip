@@ -4,11 +4,13 @@
 //
 // The newly reached vertices of a node type are deduplicated and put in
 // ascending ID order with one bit per vertex: the sampler sets bit v for every
-// kept source v that is not in the frontier yet; here a single-pass prefix
-// count of the set bits (per node type) gives each one its rank, which is its
-// position among the new vertices.  A dense int32 map (vertex -> local ID,
-// -1 when absent) holds the local IDs of the frontier and of the new vertices
-// for the relabel.
+// kept source v that is not in the frontier yet; a prefix count of the set
+// bits (per node type) then gives each one its rank, which is its position
+// among the new vertices.  The count is a reduce-then-scan over kTile-word
+// tiles in three launches (count per tile; scan of the tile counts; rank and
+// assign), which needs no inter-block waiting.  A dense int32 map (vertex ->
+// local ID, -1 when absent) holds the local IDs of the frontier and of the new
+// vertices for the relabel.
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -38,47 +40,13 @@ struct CompactArgs {
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
-  Lookback lb;
-  uint32_t epoch;
-  uint64_t ticket_base;
+  int64_t *tile_pre;  // per tile: set bits of its type in earlier tiles
+  int32_t *tile_cnt;  // per tile: set bits
   int64_t *small;
 };
 
-// Ranks the set bits of one 512-word tile within its node type and gives
-// each new vertex its local ID.
-__device__ void bitmap_tile(const CompactArgs &A, int64_t tile, int64_t *lds) {
-  const int t = find_segment(A.tile_base, A.n_types, tile);
-  const int64_t first = A.tile_base[t];
-  uint32_t *w = A.bitmap + tile * kTile + threadIdx.x * kTileItems;
-  const uint2 ab = *reinterpret_cast<const uint2 *>(w);
-  const uint32_t words[kTileItems] = {ab.x, ab.y};
-  int64_t s = 0;
-#pragma unroll
-  for (int k = 0; k < kTileItems; ++k) s += __popc(words[k]);
-  int64_t agg[1];
-  const int64_t pre = block_excl_scan_256(s, lds, &agg[0]);
-  int64_t ex[1];
-  tile_lookback<1>(A.lb, tile, first, A.epoch, agg, ex, A.small, lds);
-  if (tile == A.tile_base[t + 1] - 1 && threadIdx.x == 0)
-    A.small[kSlotNew + t] = ex[0] + agg[0];  // new vertices of type t
-  if (s == 0) return;
-  int32_t *map = A.ts[t].map;
-  int64_t *out = A.hv.src_out[t];
-  int64_t local = A.hv.nF[t] + ex[0] + pre;
-  const int64_t v0 = ((tile - first) * kTile + threadIdx.x * kTileItems) * 32;
-#pragma unroll
-  for (int k = 0; k < kTileItems; ++k) {
-    uint32_t m = words[k];
-    while (m) {
-      const int bit = __ffs(m) - 1;
-      m &= m - 1;
-      const int64_t v = v0 + k * 32 + bit;
-      map[v] = int32_t(local);
-      out[local] = v;
-      ++local;
-    }
-  }
-  *reinterpret_cast<uint2 *>(w) = uint2{0, 0};
+__device__ __forceinline__ uint2 tile_words(const CompactArgs &A, int64_t tile) {
+  return *reinterpret_cast<const uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems);
 }
 
 // Copies kTile frontier entries into the head of the source lists.
@@ -96,13 +64,82 @@ __device__ void copy_tile(const CompactArgs &A, int64_t ct) {
   }
 }
 
-__global__ __launch_bounds__(kTileThreads) void k_compact(CompactArgs A) {
+// 1. Set bits per tile; the blocks past the tiles copy the frontier.
+__global__ __launch_bounds__(kTileThreads) void k_bits_count(CompactArgs A) {
   __shared__ int64_t lds[8];
-  const int64_t tile = take_ticket(A.small, A.ticket_base, lds);
-  if (tile < A.n_tiles)
-    bitmap_tile(A, tile, lds);
-  else
+  const int64_t tile = blockIdx.x;
+  if (tile >= A.n_tiles) {
     copy_tile(A, tile - A.n_tiles);
+    return;
+  }
+  static_assert(kTileItems == 2, "one 8-byte load per thread");
+  const uint2 w = tile_words(A, tile);
+  int64_t total;
+  block_excl_scan_256(__popc(w.x) + __popc(w.y), lds, &total);
+  if (threadIdx.x == 0) A.tile_cnt[tile] = int32_t(total);
+}
+
+// 2. Exclusive scan of the tile counts within each node type, in one block;
+// the type's total is its number of new vertices.
+constexpr int kScanThreads = 1024;
+__global__ __launch_bounds__(kScanThreads) void k_bits_scan(CompactArgs A) {
+  constexpr int kWaves = kScanThreads / kWave;
+  __shared__ int64_t s_wave[kWaves];
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  for (int t = 0; t < A.n_types; ++t) {
+    const int64_t b0 = A.tile_base[t], b1 = A.tile_base[t + 1];
+    int64_t carry = 0;
+    for (int64_t c0 = b0; c0 < b1; c0 += kScanThreads) {
+      const int64_t i = c0 + threadIdx.x;
+      const int64_t x = i < b1 ? A.tile_cnt[i] : 0;
+      const int64_t inc = wave_incl_scan_i64(x);
+      if (lane == kWave - 1) s_wave[wave] = inc;
+      __syncthreads();
+      int64_t before = 0, sum = 0;
+      for (int v = 0; v < kWaves; ++v) {
+        const int64_t y = s_wave[v];
+        if (v < wave) before += y;
+        sum += y;
+      }
+      if (i < b1) A.tile_pre[i] = carry + before + inc - x;
+      carry += sum;
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) A.small[kSlotNew + t] = carry;  // new vertices of type t
+  }
+}
+
+// 3. Ranks the set bits of a tile within its node type, gives each new vertex
+// its local ID and clears the tile's words.
+__global__ __launch_bounds__(kTileThreads) void k_bits_assign(CompactArgs A) {
+  __shared__ int64_t lds[8];
+  const int64_t tile = blockIdx.x;
+  if (A.tile_cnt[tile] == 0) return;
+  const int t = find_segment(A.tile_base, A.n_types, tile);
+  const int64_t first = A.tile_base[t];
+  const uint2 ab = tile_words(A, tile);
+  const uint32_t words[kTileItems] = {ab.x, ab.y};
+  int64_t total;
+  const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &total);
+  if ((ab.x | ab.y) == 0) return;
+  int32_t *map = A.ts[t].map;
+  int64_t *out = A.hv.src_out[t];
+  int64_t local = A.hv.nF[t] + A.tile_pre[tile] + pre;
+  const int64_t v0 = ((tile - first) * kTile + threadIdx.x * kTileItems) * 32;
+#pragma unroll
+  for (int k = 0; k < kTileItems; ++k) {
+    uint32_t m = words[k];
+    while (m) {
+      const int bit = __ffs(m) - 1;
+      m &= m - 1;
+      const int64_t v = v0 + k * 32 + bit;
+      map[v] = int32_t(local);
+      out[local] = v;
+      ++local;
+    }
+  }
+  *reinterpret_cast<uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems) = uint2{0, 0};
 }
 
 // Next hop's frontier sizes (this hop's plus the new vertices of each type)
@@ -141,17 +178,18 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
 
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, const int64_t *tile_base,
-                          int64_t n_tiles, int64_t copy_total, Lookback lb,
-                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int32_t *blocks_launched, hipStream_t stream) {
-  CompactArgs A{hv, ts, n_types, bitmap, tile_base, n_tiles, copy_total, lb, epoch,
-                ticket_base, small};
+                          int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
+                          int64_t *small, hipStream_t stream) {
+  CompactArgs A{hv, ts, n_types, bitmap, tile_base, n_tiles, copy_total, tile_sums,
+                reinterpret_cast<int32_t *>(tile_sums + n_tiles), small};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
-  const int64_t blocks = n_tiles + copy_blocks;
-  *blocks_launched = int32_t(blocks);
-  if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_compact, dim3(unsigned(blocks)), dim3(kTileThreads), 0,
-                     stream, A);
+  if (n_tiles + copy_blocks > 0)
+    hipLaunchKernelGGL(k_bits_count, dim3(unsigned(n_tiles + copy_blocks)),
+                       dim3(kTileThreads), 0, stream, A);
+  hipLaunchKernelGGL(k_bits_scan, dim3(1), dim3(kScanThreads), 0, stream, A);
+  if (n_tiles > 0)
+    hipLaunchKernelGGL(k_bits_assign, dim3(unsigned(n_tiles)), dim3(kTileThreads), 0,
+                       stream, A);
   return hipGetLastError();
 }
 

@@ -106,6 +106,14 @@ __device__ __forceinline__ void block_excl_scan4_256(const int64_t (&v)[4],
   __syncthreads();
 }
 
+// A load through a pointer known to address global memory (device memory),
+// so that the compiler issues a global rather than a flat access and does
+// not wait on LDS traffic for it.
+template <typename T>
+__device__ __forceinline__ T load_global(const T *p) {
+  return *(const __attribute__((address_space(1))) T *)(p);
+}
+
 // Largest s in [0, n) with base[s] <= x, for a non-decreasing base[0..n]
 // with base[0] <= x < base[n]: the segment that holds item x.
 __device__ __forceinline__ int find_segment(const int64_t *base, int n,
@@ -141,14 +149,20 @@ constexpr int kSpinLimit = 1 << 21;
 
 // A look-back word: epoch (20 bits) | state (2 bits) | value (42 bits).
 // Each word carries its own epoch, so a reader needs no fence: it polls the
-// word until it carries the current epoch.
+// word until it carries the current epoch.  A tile has one word per scanned
+// value: first its aggregate (state 1), later overwritten in place by its
+// inclusive prefix (state 2); a reader sees one or the other.
 constexpr int kLbValueBits = 42;
+constexpr uint32_t kLbAggregate = 1, kLbInclusive = 2;
 __device__ __forceinline__ uint64_t lb_word(uint32_t epoch, uint32_t state, int64_t v) {
   return (uint64_t(epoch) << (kLbValueBits + 2)) | (uint64_t(state) << kLbValueBits) |
          (uint64_t(v) & ((uint64_t(1) << kLbValueBits) - 1));
 }
 __device__ __forceinline__ bool lb_ready(uint64_t w, uint32_t epoch) {
   return uint32_t(w >> (kLbValueBits + 2)) == epoch;
+}
+__device__ __forceinline__ uint32_t lb_state(uint64_t w) {
+  return uint32_t(w >> kLbValueBits) & 3u;
 }
 __device__ __forceinline__ int64_t lb_value(uint64_t w) {
   return int64_t(w & ((uint64_t(1) << kLbValueBits) - 1));
@@ -160,92 +174,105 @@ __device__ __forceinline__ uint64_t lb_load(const uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Polls *p until it carries `epoch` (or the spin bound); returns the word.
-__device__ __forceinline__ uint64_t lb_wait(const uint64_t *p, uint32_t epoch,
-                                            bool *timed_out) {
-  uint64_t w = lb_load(p);
-  int spins = 0;
-  while (!lb_ready(w, epoch)) {
-    if (++spins >= kSpinLimit) {
-      *timed_out = true;
-      return w;
-    }
-    __builtin_amdgcn_s_sleep(1);
-    w = lb_load(p);
-  }
-  return w;
-}
-
 // Decoupled look-back (single-pass prefix scan) of NV values for tile `tile`
-// of a segment whose first tile is `first`.  Per tile 2*NV words: aggregates
-// (state 1), then inclusive prefixes (state 2).  The tile publishes its
-// aggregates; wavefront 0 then inspects 64 predecessors at a time and sums
-// aggregates back to the nearest predecessor whose inclusive prefix is out;
-// the tile publishes its own inclusive prefix.  Returns the exclusive prefix
-// in every thread.  `agg` must be the same in all threads.
+// of a segment whose first tile is `first`, in a block of kTileThreads
+// threads.  The tile publishes its aggregates; then every thread inspects one
+// predecessor per step (kTileThreads predecessors at a time, one round trip),
+// and for each value the block sums the aggregates back to the nearest
+// predecessor whose inclusive prefix is out, which ends that value's walk.
+// The tile then publishes its own inclusive prefixes.  Returns the exclusive
+// prefix in every thread.  `agg` must be the same in all threads; every
+// thread of the block must call this.
 template <int NV>
 __device__ void tile_lookback(Lookback lb, int64_t tile, int64_t first,
                               uint32_t epoch, const int64_t (&agg)[NV],
-                              int64_t (&excl)[NV], int64_t *small,
-                              int64_t *lds) {
-  uint64_t *mine = lb.word + tile * 2 * NV;
-  if (threadIdx.x < kWave) {
-    const int lane = lane_id();
-    int64_t ex[NV];
+                              int64_t (&excl)[NV], int64_t *small) {
+  constexpr int kWaves = kTileThreads / kWave;
+  __shared__ int32_t s_stop[kWaves][NV];
+  __shared__ int64_t s_sum[kWaves][NV];
+  uint64_t *mine = lb.word + tile * NV;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
 #pragma unroll
-    for (int k = 0; k < NV; ++k) ex[k] = 0;
-    if (tile > first) {
-      if (lane < NV) {
-#pragma unroll
-        for (int k = 0; k < NV; ++k)
-          if (k == lane) lb_store(mine + k, lb_word(epoch, 1, agg[k]));
-      }
-      bool timed_out = false;
-      for (int64_t top = tile - 1;; top -= kWave) {
-        // lane l looks at predecessor top - l; tiles before the segment count
-        // as published inclusive prefixes of nothing
-        const int64_t j = top - lane;
-        bool inclusive = true;
-        if (j >= first) {
-          const uint64_t *wj = lb.word + j * 2 * NV;
-          int spins = 0;
-          for (;;) {
-            if (lb_ready(lb_load(wj + NV), epoch)) break;           // inclusive
-            if (lb_ready(lb_load(wj), epoch)) { inclusive = false; break; }
-            if (++spins >= kSpinLimit) { timed_out = true; break; }
-            __builtin_amdgcn_s_sleep(1);
-          }
-        }
-        const uint64_t incl = __ballot(inclusive);
-        // the nearest predecessor with an inclusive prefix ends the walk
-        const int stop = incl ? __ffsll((unsigned long long)incl) - 1 : kWave;
-#pragma unroll
-        for (int k = 0; k < NV; ++k) {
-          int64_t v = 0;
-          if (lane <= stop && j >= first)
-            v = lb_value(lb_wait(lb.word + j * 2 * NV + (inclusive ? NV : 0) + k, epoch,
-                                 &timed_out));
-          ex[k] += wave_sum_i64(v);
-        }
-        if (incl) break;
-      }
-      if (__ballot(timed_out) && lane == 0)
-        atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), kErrLookback);
-    }
-    if (lane < NV) {
+  for (int k = 0; k < NV; ++k) excl[k] = 0;
+  if (tile <= first) {
+    if (tid < NV) {
 #pragma unroll
       for (int k = 0; k < NV; ++k)
-        if (k == lane) lb_store(mine + NV + k, lb_word(epoch, 2, ex[k] + agg[k]));
+        if (k == tid) lb_store(mine + k, lb_word(epoch, kLbInclusive, agg[k]));
     }
-    if (lane == 0) {
-#pragma unroll
-      for (int k = 0; k < NV; ++k) lds[k] = ex[k];
-    }
+    return;
   }
-  __syncthreads();
+  if (tid < NV) {
 #pragma unroll
-  for (int k = 0; k < NV; ++k) excl[k] = lds[k];
-  __syncthreads();
+    for (int k = 0; k < NV; ++k)
+      if (k == tid) lb_store(mine + k, lb_word(epoch, kLbAggregate, agg[k]));
+  }
+  bool done[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) done[k] = false;
+  bool timed_out = false;
+  for (int64_t top = tile - 1;; top -= kTileThreads) {
+    // thread i looks at predecessor top - i; tiles before the segment count
+    // as published inclusive prefixes of nothing
+    const int64_t j = top - tid;
+    const bool valid = j >= first;
+    uint64_t w[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) w[k] = 0;
+    if (valid) {
+      const uint64_t *wj = lb.word + j * NV;
+      int spins = 0;
+      for (;;) {
+#pragma unroll
+        for (int k = 0; k < NV; ++k) w[k] = lb_load(wj + k);
+        bool ready = true;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) ready = ready && lb_ready(w[k], epoch);
+        if (ready) break;
+        if (++spins >= kSpinLimit) { timed_out = true; break; }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      // a timed-out word ends the walk too; the call then reports an error
+      const bool inc = !valid || timed_out || lb_state(w[k]) == kLbInclusive;
+      const uint64_t bal = __ballot(inc);
+      if (lane == 0) s_stop[wave][k] = bal ? __ffsll((unsigned long long)bal) - 1 : kWave;
+    }
+    __syncthreads();
+    int stop[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      stop[k] = kTileThreads;
+      for (int v = kWaves - 1; v >= 0; --v)
+        if (s_stop[v][k] < kWave) stop[k] = v * kWave + s_stop[v][k];
+      const int64_t x = (!done[k] && valid && tid <= stop[k]) ? lb_value(w[k]) : 0;
+      const int64_t ws = wave_sum_i64(x);
+      if (lane == 0) s_sum[wave][k] = ws;
+    }
+    __syncthreads();
+    bool all = true;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      if (!done[k]) {
+        for (int v = 0; v < kWaves; ++v) excl[k] += s_sum[v][k];
+        done[k] = stop[k] < kTileThreads;
+      }
+      all = all && done[k];
+    }
+    __syncthreads();  // s_stop and s_sum are rewritten by the next step
+    if (all) break;
+  }
+  if (__ballot(timed_out) && lane == 0)
+    atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), kErrLookback);
+  if (tid < NV) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+      if (k == tid) lb_store(mine + k, lb_word(epoch, kLbInclusive, excl[k] + agg[k]));
+  }
 }
 
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32
@@ -258,11 +285,11 @@ __device__ __forceinline__ U32x4 philox4x32_10(U32x4 c, uint32_t k0,
                                                uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t lo0 = 0xD2511F53u * c.x;
-    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z;
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z);
-    c = U32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+    // full 64-bit products: one multiply instruction gives both halves
+    const uint64_t p0 = uint64_t(0xD2511F53u) * c.x;
+    const uint64_t p1 = uint64_t(0xCD9E8D57u) * c.z;
+    c = U32x4{uint32_t(p1 >> 32) ^ c.y ^ k0, uint32_t(p1), uint32_t(p0 >> 32) ^ c.w ^ k1,
+              uint32_t(p0)};
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
   }

@@ -15,8 +15,14 @@ constexpr int kTileItems = 2;
 constexpr int64_t kTile = int64_t(kTileThreads) * kTileItems;  // 512 words
 
 // Pair tiles of the counting pass: 256 threads x 2 pairs.
-constexpr int kPairItems = 2;
-constexpr int64_t kPairTile = int64_t(kTileThreads) * kPairItems;
+// Pairs per thread of the counting pass: few for small hops (more blocks in
+// flight), more for large ones (fewer tiles, whose tickets serialize).
+constexpr int kPairItemsSmall = 2;
+constexpr int kPairItemsLarge = 8;
+constexpr int64_t kPairLargeFrom = int64_t(kTileThreads) * kPairItemsSmall * 512;
+inline int pair_items(int64_t n_items) {
+  return n_items >= kPairLargeFrom ? kPairItemsLarge : kPairItemsSmall;
+}
 
 // Candidate capacity of one bottom-K selection (LDS entries per wavefront,
 // and per hub in the global candidate lists).
@@ -76,29 +82,24 @@ struct HopView {
 };
 
 // Words of a single-pass (decoupled look-back) scan of NV values: per tile
-// 2*NV 64-bit words, each epoch (20 bits) | state (2 bits) | value (42
-// bits); state 1 = aggregate, 2 = inclusive prefix.  Epochs run 1 .. 2^20-1;
+// NV 64-bit words, each epoch (20 bits) | state (2 bits) | value (42 bits);
+// state 1 = aggregate, overwritten by state 2 = inclusive prefix.  Epochs run 1 .. 2^20-1;
 // the words are zeroed before an epoch is reused.
 struct Lookback {
   uint64_t *word;
 };
 constexpr uint32_t kEpochLimit = 1u << 20;
 
-// Per-pair arrays of one hop (device).  Per-pair arrays have n_items
-// entries; clist has clist_cap.
+// Per-pair arrays of one hop (device), n_items entries each.
 struct PairArrays {
   int64_t *plo;      // first in-edge slot
   int64_t *pdeg;     // in-degree
   int64_t *off;      // exclusive scan of kept edges
-  int64_t *choff;    // exclusive scan of hub chunks
-  int64_t *woff;     // exclusive scan of wavefront pairs
-  int64_t *hoff;     // exclusive scan of hub flags (= hub ID)
   int32_t *pet;      // edge type of the pair
   int64_t *wlist;    // the pair of each wavefront pair, in pair order
-  int64_t *clist;    // the pair of each hub chunk, in pair order
-  int64_t clist_cap;
   int32_t *hub_cnt;  // per hub: candidates appended
   int64_t *hub_pair; // per hub: its pair
+  int64_t *hub_choff; // per hub: its first chunk (strictly increasing)
 };
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
@@ -143,16 +144,16 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
                        int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
                        hipStream_t stream);
 
-// Compaction pass, one launch: per bitmap tile, ranks of the set bits within
-// the node type (single-pass scan) -> local IDs n_frontier + rank, written to
-// the map and the source list, bits cleared; the last tile of each type
-// writes its new-vertex count to small[kSlotNew + t]; extra blocks copy the
-// frontier into the head of the source lists.
+// Compaction pass, three launches: per bitmap tile, ranks of the set bits
+// within the node type (reduce, scan, rank) -> local IDs n_frontier + rank,
+// written to the map and the source list, bits cleared; the scan writes each
+// type's new-vertex count to small[kSlotNew + t]; extra blocks copy the
+// frontier into the head of the source lists.  tile_sums: device scratch of
+// 2 * n_tiles 64-bit words.
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, const int64_t *tile_base,
-                          int64_t n_tiles, int64_t copy_total, Lookback lb,
-                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int32_t *blocks_launched, hipStream_t stream);
+                          int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
+                          int64_t *small, hipStream_t stream);
 
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.
@@ -165,6 +166,13 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           hipStream_t stream);
 
 // Fill helpers (kernels, so that they are safe under graph capture).
+// One block copies small[0..n) to pinned host memory host[0..n) and then
+// writes `seq` to host[n] (system scope, after the slots).
+hipError_t launch_publish(const int64_t *small, int64_t *host, int32_t n, uint64_t seq,
+                          hipStream_t stream);
+// dst[i] = vals[i] for i < n (device pointer table), stream-ordered, with the
+// values passed in the launches.
+hipError_t launch_store_ptrs(void **dst, void *const *vals, int32_t n, hipStream_t stream);
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream);
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t stream);
 

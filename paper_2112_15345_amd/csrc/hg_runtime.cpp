@@ -19,7 +19,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
 #include <mutex>
+#include <thread>
 #include <new>
 #include <string>
 #include <vector>
@@ -120,10 +122,11 @@ struct Workspace {
   int32_t *map = nullptr;          // sum of num_nodes
   uint32_t *bitmap = nullptr;      // n_tiles * kTile words
   int64_t *dsmall = nullptr;       // readback slots
-  int64_t *hsmall = nullptr;       // pinned mirror of dsmall
+  int64_t *hsmall = nullptr;       // pinned, coherent mirror of dsmall + a flag word
+  uint64_t publish_seq = 0;        // flag value of the last publish
   EtypeStatic *d_es = nullptr;     // static per-etype table
   TypeStatic *d_ts = nullptr;      // static per-type table
-  uint64_t *lb_bits = nullptr;     // look-back words of the compaction pass
+  int64_t *tile_sums = nullptr;    // per bitmap tile: prefix and count (compaction)
   Scratch tab;                     // per-hop tables (device)
   char *htab = nullptr;            // per-hop tables (pinned host)
   size_t htab_cap = 0;
@@ -255,7 +258,7 @@ void free_workspace(Workspace *w) {
   (void)hipFree(w->dsmall);
   (void)hipFree(w->d_es);
   (void)hipFree(w->d_ts);
-  (void)hipFree(w->lb_bits);
+  (void)hipFree(w->tile_sums);
   w->tab.release();
   w->pairs.release();
   w->lb_pairs.release();
@@ -296,12 +299,15 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
     if (e == hipSuccess) e = hipMalloc(&w->d_es, sizeof(EtypeStatic) * size_t(std::max(g->R, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->d_ts, sizeof(TypeStatic) * size_t(g->T));
-    if (e == hipSuccess) e = hipMalloc(&w->lb_bits, sizeof(uint64_t) * 2 * size_t(n_lb));
-    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void **>(&w->hsmall), sizeof(int64_t) * small_n, 0);
+    if (e == hipSuccess) e = hipMalloc(&w->tile_sums, sizeof(int64_t) * 2 * size_t(n_lb));
+    // coherent: the device writes it while the host polls the flag word
+    if (e == hipSuccess)
+      e = hipHostMalloc(reinterpret_cast<void **>(&w->hsmall), sizeof(int64_t) * (small_n + 1),
+                        hipHostMallocCoherent);
+    if (e == hipSuccess) std::memset(w->hsmall, 0, sizeof(int64_t) * (small_n + 1));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming);
     if (e == hipSuccess) e = launch_fill_i32(w->map, map_n, -1, stream);
     if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
-    if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t *>(w->lb_bits), 4 * n_lb, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
       for (int32_t i = 0; i < g->R; ++i) {
@@ -415,11 +421,14 @@ struct SampleRun {
   char *hreg(int r) { return ws->htab + size_t(r) * lay.size; }
   char *dreg(int r) { return static_cast<char *>(ws->tab.p) + size_t(r) * lay.size; }
 
+  // Region r's frontier is region r-1's source lists (the same table words);
+  // region 0's is the seeds.
   HopView view(int r) {
     char *d = dreg(r);
+    char *f = r == 0 ? d + lay.frontier : dreg(r - 1) + lay.src_out;
     return HopView{reinterpret_cast<int64_t *>(d + lay.nf),
                    reinterpret_cast<int64_t *>(d + lay.pbase),
-                   reinterpret_cast<const int64_t *const *>(d + lay.frontier),
+                   reinterpret_cast<const int64_t *const *>(f),
                    reinterpret_cast<int64_t *const *>(d + lay.src_out),
                    reinterpret_cast<const int32_t *>(d + lay.fanout)};
   }
@@ -437,9 +446,8 @@ struct SampleRun {
     ws->epoch += 1;
     if (ws->epoch >= kEpochLimit) {
       ws->epoch = 1;
-      hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t *>(ws->lb_bits),
-                                     4 * std::max<int64_t>(g->n_tiles, 1), 0u, stream);
-      if (e == hipSuccess && ws->lb_pairs.p)
+      hipError_t e = hipSuccess;
+      if (ws->lb_pairs.p)
         e = launch_fill_u32(static_cast<uint32_t *>(ws->lb_pairs.p),
                             int64_t(ws->lb_pairs.cap / sizeof(uint32_t)), 0u, stream);
       if (e != hipSuccess) return e;
@@ -448,11 +456,30 @@ struct SampleRun {
     return hipSuccess;
   }
 
+  // Waits until the stream has reached this point and the readback slots are
+  // in ws->hsmall: a one-block kernel copies them to the coherent host buffer
+  // and then sets its flag word, which the host polls (cheaper than a copy
+  // plus a stream wait).  Every few hundred polls the stream is queried, so
+  // a failed kernel (whose successors never run) ends the wait with its error.
   hipError_t sync_small() {
-    hipError_t e = hipMemcpyAsync(ws->hsmall, ws->dsmall, sizeof(int64_t) * small_slots(g),
-                                  hipMemcpyDeviceToHost, stream);
+    const int32_t n = int32_t(small_slots(g));
+    const uint64_t seq = ++ws->publish_seq;
+    hipError_t e = launch_publish(ws->dsmall, ws->hsmall, n, seq, stream);
     if (e != hipSuccess) return e;
-    return hipStreamSynchronize(stream);
+    const volatile int64_t *flag = ws->hsmall + n;
+    for (uint32_t i = 1; uint64_t(*flag) != seq; ++i) {
+      if ((i & 255) == 0) {
+        e = hipStreamQuery(stream);
+        if (e == hipSuccess) {
+          if (uint64_t(*flag) == seq) break;
+          return hipErrorUnknown;  // the stream drained without the flag
+        }
+        if (e != hipErrorNotReady) return e;
+        if (i >= (1u << 16)) std::this_thread::yield();  // a long kernel
+      }
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    return hipSuccess;
   }
 
   hg_status check_flags(const char *where) {
@@ -521,15 +548,21 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   for (int32_t i = 0; i < R; ++i) {
     hfield<int64_t>(0, lay.pbase)[i] = P;
     P += nF[g->et[i].dst];
-    hfield<int32_t>(0, lay.fanout)[i] = H > 0 ? fanouts[i] : 0;
   }
   hfield<int64_t>(0, lay.pbase)[R] = P;
+  // every region's fanouts and empty source lists go up now; a hop's nF and
+  // pair_base are written by the device, its source lists once allocated
+  for (int32_t r = 0; r <= H; ++r) {
+    for (int32_t i = 0; i < R; ++i)
+      hfield<int32_t>(r, lay.fanout)[i] = r < H ? fanouts[size_t(r) * R + i] : 0;
+    for (int32_t t = 0; t < T; ++t) hfield<int64_t *>(r, lay.src_out)[t] = nullptr;
+  }
   int64_t n_items = P + 1;  // pair slots of the next counting pass
 
   // the readback slots start at zero (tickets, error flags)
   if ((e = launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall), 2 * int64_t(small_slots(g)), 0,
                            stream)) != hipSuccess ||
-      (e = upload(0, lay.size)) != hipSuccess)
+      (e = upload(0, size_t(H + 1) * lay.size)) != hipSuccess)
     return fail_device(e, "start");
   int64_t total = 0;
   for (int64_t n : nF) total += n;
@@ -552,18 +585,13 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     pc.add(&pa.plo, n_items);
     pc.add(&pa.pdeg, n_items);
     pc.add(&pa.off, n_items);
-    pc.add(&pa.choff, n_items);
-    pc.add(&pa.woff, n_items);
-    pc.add(&pa.hoff, n_items);
     pc.add(&pa.pet, n_items);
     pc.add(&pa.wlist, n_items);
-    // hub chunks: at most one per pair plus one per kHubChunk edges
-    pa.clist_cap = n_items + g->total_nnz / kHubChunk + 1;
-    pc.add(&pa.clist, pa.clist_cap);
     pc.add(&pa.hub_cnt, n_items);
     pc.add(&pa.hub_pair, n_items);
+    pc.add(&pa.hub_choff, n_items);
     if (!pc.in_scratch(ws->pairs, stream) ||
-        !ws->lb_pairs.ensure(sizeof(uint64_t) * 8 * size_t(tiles), stream))
+        !ws->lb_pairs.ensure(sizeof(uint64_t) * 4 * size_t(tiles), stream))
       return fail(HG_ENOMEM, "hop %d: pair scratch", h);
     Lookback lb{static_cast<uint64_t *>(ws->lb_pairs.p)};
     // new look-back words start with no tile published
@@ -630,20 +658,14 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     if (!ec.in_scratch(ws->edges, stream) || !cc.in_scratch(ws->cand, stream))
       return fail(HG_ENOMEM, "hop %d: edge scratch", h);
 
-    // tables: this hop's source lists; the next hop's frontier and fanouts
-    for (int32_t t = 0; t < T; ++t) {
-      hfield<int64_t *>(h, lay.src_out)[t] = src_out[t];
-      hfield<const int64_t *>(h + 1, lay.frontier)[t] = src_out[t];
-      hfield<int64_t *>(h + 1, lay.src_out)[t] = nullptr;
-    }
-    for (int32_t i = 0; i < R; ++i)
-      hfield<int32_t>(h + 1, lay.fanout)[i] = h + 1 < H ? fanouts[size_t(h + 1) * R + i] : 0;
-    if ((e = upload(size_t(h) * lay.size + lay.src_out, size_t(h + 2) * lay.size)) != hipSuccess)
-      return fail_device(e, "upload");
+    // this hop's source lists (also the next hop's frontier)
+    if ((e = launch_store_ptrs(reinterpret_cast<void **>(dreg(h) + lay.src_out),
+                               reinterpret_cast<void *const *>(src_out.data()), T, stream)) !=
+        hipSuccess)
+      return fail_device(e, "tables");
 
     // ---- 2-4. sample, compact, relabel -------------------------------------
     bitmap_dirty = true;
-    int32_t compact_blocks = 0;
     int64_t copy_total = 0;
     for (int64_t n : nF) copy_total += n;
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
@@ -652,12 +674,9 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
       return fail_device(e, "sample");
     if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
       return fail_device(e, "mark");
-    if ((e = next_epoch(&epoch)) != hipSuccess ||
-        (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
-                            Lookback{ws->lb_bits}, epoch, ticket_base, ws->dsmall,
-                            &compact_blocks, stream)) != hipSuccess)
+    if ((e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
+                            ws->tile_sums, ws->dsmall, stream)) != hipSuccess)
       return fail_device(e, "compact");
-    ticket_base += uint64_t(compact_blocks);
     bitmap_dirty = false;
     if ((e = launch_relabel(hv, nv, ws->d_es, g->d_tile_base, ws->dsmall, T, R, S, gid_tmp,
                             srcl_all, stream)) != hipSuccess)

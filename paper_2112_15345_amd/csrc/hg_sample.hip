@@ -10,9 +10,10 @@
 //
 // Work is split by pair shape: small take-all pairs run one per thread; other
 // pairs one per wavefront; pairs that select among more than kHubChunk edges
-// ("hubs") are cut into chunks of kHubChunk edges, one wavefront per chunk,
-// which append their candidates to a per-hub list; the last chunk of a hub to
-// finish selects from that list.  Every edge key is computed once.
+// ("hubs") are cut into chunks of kHubChunk edges, handed to wavefronts in
+// runs of consecutive chunks, which append their candidates to a per-hub
+// list; a second launch then selects each hub's K edges from its list.  Every
+// edge key is computed once.
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -84,37 +85,117 @@ struct PairCounts {
   int64_t s, nch, wave, hub;
 };
 
+// Per edge type, what the counting pass reads for every pair; staged in LDS
+// when the graph has at most kCountMaxEtypes edge types.
+constexpr int kCountMaxEtypes = 256;
+struct CountTable {
+  int64_t pbase[kCountMaxEtypes + 1];
+  const int64_t *indptr[kCountMaxEtypes];
+  const int64_t *front[kCountMaxEtypes];
+  int64_t n_dst[kCountMaxEtypes];
+  int32_t fanout[kCountMaxEtypes];
+};
+
+template <bool kStaged>
+struct CountView {
+  const CountTable *t;
+  const HopView *hv;
+  const EtypeStatic *es;
+  __device__ int64_t pbase(int e) const { return kStaged ? t->pbase[e] : hv->pair_base[e]; }
+  __device__ const int64_t *indptr(int e) const { return kStaged ? t->indptr[e] : es[e].indptr; }
+  __device__ const int64_t *front(int e) const {
+    return kStaged ? t->front[e] : hv->frontier[es[e].dst_type];
+  }
+  __device__ int64_t n_dst(int e) const { return kStaged ? t->n_dst[e] : es[e].n_dst_nodes; }
+  __device__ int32_t fanout(int e) const { return kStaged ? t->fanout[e] : hv->fanout[e]; }
+};
+
+// Thread i of a tile owns kPairItems consecutive pairs.  The pair's edge type
+// comes from the (staged) table; the frontier vertices of all items are
+// loaded together, then their indptr entries, so a thread waits on two
+// rounds of memory accesses.
+template <bool kStaged, int kPairItems>
 __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
     int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
     uint64_t ticket_base, int64_t *small) {
   __shared__ int64_t lds[16];
-  const int64_t tile = take_ticket(small, ticket_base, lds);
-  const int64_t P = hv.pair_base[n_etypes];
-  const int64_t base = tile * kPairTile + threadIdx.x * kPairItems;
+  __shared__ CountTable table;
+  if (kStaged) {
+    for (int e = threadIdx.x; e <= n_etypes; e += kTileThreads) {
+      table.pbase[e] = hv.pair_base[e];
+      if (e < n_etypes) {
+        const EtypeStatic &E = es[e];
+        table.indptr[e] = E.indptr;
+        table.front[e] = hv.frontier[E.dst_type];
+        table.n_dst[e] = E.n_dst_nodes;
+        table.fanout[e] = hv.fanout[e];
+      }
+    }
+  }
+  const int64_t tile = take_ticket(small, ticket_base, lds);  // also a barrier
+  const CountView<kStaged> V{&table, &hv, es};
+  const int64_t P = V.pbase(n_etypes);
+  const int64_t base = (tile * kTileThreads + threadIdx.x) * kPairItems;
   int32_t *err = reinterpret_cast<int32_t *>(small + kSlotErr);
   if (tile == 0 && threadIdx.x == 0 && P + 1 > n_items) atomicOr(err, kErrBound);
 
-  PairCounts c[kPairItems];
+  // edge type and frontier slot of every item
   int etype[kPairItems];
+  const int64_t *fp[kPairItems];
+  {
+    int e = 0;
+    if (base < P) {
+      int lo = 0, hi = n_etypes;  // pbase(lo) <= base < pbase(hi)
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (V.pbase(mid) <= base)
+          lo = mid;
+        else
+          hi = mid;
+      }
+      e = lo;
+    }
+#pragma unroll
+    for (int k = 0; k < kPairItems; ++k) {
+      const int64_t p = base + k;
+      fp[k] = nullptr;
+      if (p < P) {
+        while (V.pbase(e + 1) <= p) ++e;
+        fp[k] = V.front(e) + (p - V.pbase(e));
+      }
+      etype[k] = e;
+    }
+  }
+  int64_t v[kPairItems];
+#pragma unroll
+  for (int k = 0; k < kPairItems; ++k) v[k] = fp[k] ? load_global(fp[k]) : 0;
+  const int64_t *ip[kPairItems];
+#pragma unroll
+  for (int k = 0; k < kPairItems; ++k) {
+    ip[k] = nullptr;
+    if (fp[k]) {
+      if (v[k] >= 0 && v[k] < V.n_dst(etype[k]))
+        ip[k] = V.indptr(etype[k]) + v[k];
+      else
+        atomicOr(err, kErrSeedRange);
+    }
+  }
+  int64_t lo[kPairItems], hi[kPairItems];
+#pragma unroll
+  for (int k = 0; k < kPairItems; ++k) {
+    lo[k] = ip[k] ? load_global(ip[k]) : 0;
+    hi[k] = ip[k] ? load_global(ip[k] + 1) : 0;
+  }
+
+  PairCounts c[kPairItems];
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
     const int64_t p = base + k;
     c[k] = PairCounts{0, 0, 0, 0};
-    etype[k] = 0;
-    if (p >= P) continue;
-    const int e = find_segment(hv.pair_base, n_etypes, p);
-    etype[k] = e;
-    const EtypeStatic &E = es[e];
-    const int64_t v = hv.frontier[E.dst_type][p - hv.pair_base[e]];
-    int64_t lo = 0, deg = 0;
-    if (v >= 0 && v < E.n_dst_nodes) {
-      lo = E.indptr[v];
-      deg = E.indptr[v + 1] - lo;
-    } else {
-      atomicOr(err, kErrSeedRange);
-    }
-    const int64_t K = hv.fanout[e];
+    if (!fp[k]) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
+    const int64_t deg = hi[k] - lo[k];
+    const int64_t K = V.fanout(etype[k]);
     const int64_t s = (K < 0 || deg <= K) ? deg : K;
     c[k].s = s;
     if (s < deg && deg > kHubChunk) {
@@ -123,7 +204,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     } else if (s > 0 && !(s == deg && deg <= kThreadTakeAll)) {
       c[k].wave = 1;
     }
-    pa.plo[p] = lo;
+    pa.plo[p] = lo[k];
     pa.pdeg[p] = deg;
   }
 
@@ -139,7 +220,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
   int64_t pre[4], agg[4];
   block_excl_scan4_256(sum, pre, agg, lds);
   int64_t ex[4];
-  tile_lookback<4>(lb, tile, 0, epoch, agg, ex, small, lds);
+  tile_lookback<4>(lb, tile, 0, epoch, agg, ex, small);
 #pragma unroll
   for (int a = 0; a < 4; ++a) pre[a] += ex[a];
 
@@ -149,24 +230,17 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     const int64_t p = base + k;
     if (p < n_items) {
       pa.off[p] = pre[0];
-      pa.choff[p] = pre[1];
-      pa.woff[p] = pre[2];
-      pa.hoff[p] = pre[3];
       pa.pet[p] = etype[k];
       if (c[k].wave) pa.wlist[pre[2]] = p;
       if (c[k].hub) {
         pa.hub_cnt[pre[3]] = 0;
         pa.hub_pair[pre[3]] = p;
-        if (pre[1] + c[k].nch > pa.clist_cap) {
-          atomicOr(err, kErrBound);
-        } else {
-          for (int64_t q = 0; q < c[k].nch; ++q) pa.clist[pre[1] + q] = p;
-        }
+        pa.hub_choff[pre[3]] = pre[1];
       }
       // edge start of every etype whose first pair (or end, for the last) is p
       if (p <= P) {
         const int e = p < P ? etype[k] : n_etypes;
-        for (int e2 = e; e2 >= 0 && hv.pair_base[e2] == p; --e2) ebase[e2] = pre[0];
+        for (int e2 = e; e2 >= 0 && V.pbase(e2) == p; --e2) ebase[e2] = pre[0];
       }
     }
     pre[0] += c[k].s;
@@ -318,6 +392,7 @@ struct SampleArgs {
   int32_t n_etypes, n_types;
   int64_t n_pairs, n_wave, n_chunks, n_hubs;
   int64_t blocks_a, blocks_b;
+  int64_t chunks_per_wave;
   PairArrays pa;
   uint64_t *cand;
   const int64_t *small;
@@ -476,55 +551,115 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   select_by_bisection(c, lo, deg, K, o, a, b, A.hop, e, k0, k1, shift);
 }
 
-// Role C: a wavefront per hub chunk appends the chunk's candidates
-// (key < tau) to the hub's list.
-__device__ void role_hub_chunks(const SampleArgs &A, int64_t chunk) {
-  const int lane = lane_id();
-  const int64_t p = A.pa.clist[chunk];
-  const int e = A.pa.pet[p];
-  const int64_t lo = A.pa.plo[p];
-  const int64_t deg = A.pa.pdeg[p];
-  const int64_t K = A.pa.off[p + 1] - A.pa.off[p];
-  const int64_t hub = A.pa.hoff[p];
-  const uint32_t shift = uint32_t(32 - A.key_bits);
-  const uint64_t key_space = uint64_t(1) << A.key_bits;
-  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
-  const uint64_t tau = cand_threshold(K, deg, key_space);
+// Role C: wavefront w takes the hub chunks [w * chunks_per_wave, ...) in
+// order and appends each chunk's candidates (key < tau) to its hub's list.
+// The hub of the first chunk is found by binary search (the last hub whose
+// first chunk is not above it); later chunks walk on from there, so the
+// search and the hub's parameters are loaded once per run of chunks.
+constexpr int64_t kHubWaves = 16384;
+constexpr int64_t kMaxChunksPerWave = 16;
 
-  const int64_t c_lo = lo + (chunk - A.pa.choff[p]) * kHubChunk;
-  const int64_t c_hi = min(c_lo + kHubChunk, lo + deg);
-  const uint64_t g_first = uint64_t(c_lo) >> 2;
-  const uint64_t g_last = uint64_t(c_hi - 1) >> 2;
-  uint64_t *list = A.cand + hub * kCandCap;
-  int32_t *cnt = A.pa.hub_cnt + hub;
-  for (uint64_t gb = g_first; gb <= g_last; gb += kWave) {
-    const uint64_t g = gb + lane;
-    int mask = 0;
-    U32x4 r{0, 0, 0, 0};
-    if (g <= g_last) {
-      r = edge_keys(g, A.hop, e, k0, k1, shift);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint64_t ed = 4 * g + q;
-        if (ed >= uint64_t(c_lo) && ed < uint64_t(c_hi) && uint64_t(word_of(r, q)) < tau)
-          mask |= 1 << q;
-      }
-    }
-    int tot;
-    const int pre = wave_prefix_small(__popc(mask), &tot);
-    if (tot == 0) continue;
-    int base = 0;
-    if (lane == 0) base = atomicAdd(cnt, tot);
-    base = __shfl(base, 0, kWave);
-    int pos = base + pre;
+struct HubParams {
+  int64_t hub, first_chunk, end_chunk, lo, deg, K;
+  uint64_t tau;
+  int e;
+};
+
+__device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
+  HubParams H;
+  H.hub = hub;
+  H.first_chunk = A.pa.hub_choff[hub];
+  H.end_chunk = hub + 1 < A.n_hubs ? A.pa.hub_choff[hub + 1] : A.n_chunks;
+  const int64_t p = A.pa.hub_pair[hub];
+  H.e = A.pa.pet[p];
+  H.lo = A.pa.plo[p];
+  H.deg = A.pa.pdeg[p];
+  H.K = A.pa.off[p + 1] - A.pa.off[p];
+  H.tau = cand_threshold(H.K, H.deg, uint64_t(1) << A.key_bits);
+  return H;
+}
+
+// One wavefront step over the 64 key groups gb .. gb+63 of a hub chunk
+// [c_lo, c_hi): appends the edges with key <= lim to the hub's list.
+// kChecked: some lanes' edges may lie outside the chunk.  Otherwise the step
+// first asks whether any key of the wavefront is small enough at all, which
+// is rarely the case.
+template <bool kChecked>
+__device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H,
+                                         uint64_t gb, int64_t c_lo, int64_t c_hi,
+                                         uint32_t lim, uint32_t shift, uint32_t k0,
+                                         uint32_t k1) {
+  const int lane = lane_id();
+  const uint64_t g = gb + lane;
+  const U32x4 r = philox4x32_10(
+      U32x4{uint32_t(g), uint32_t(g >> 32), uint32_t(A.hop), uint32_t(H.e)}, k0, k1);
+  if (!kChecked) {
+    const uint32_t m = min(min(r.x, r.y), min(r.z, r.w));
+    if (__ballot(m <= lim) == 0) return;
+  }
+  int mask = (r.x <= lim ? 1 : 0) | (r.y <= lim ? 2 : 0) | (r.z <= lim ? 4 : 0) |
+             (r.w <= lim ? 8 : 0);
+  if (kChecked) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      if (mask & (1 << q)) {
-        if (pos < kCandCap)
-          list[pos] = (uint64_t(word_of(r, q)) << 32) | (4 * g + q - uint64_t(lo));
-        ++pos;
-      }
+      const uint64_t ed = 4 * g + q;
+      if (ed < uint64_t(c_lo) || ed >= uint64_t(c_hi)) mask &= ~(1 << q);
     }
+    if (__ballot(mask != 0) == 0) return;
+  }
+  int tot;
+  const int pre = wave_prefix_small(__popc(mask), &tot);
+  int base = 0;
+  if (lane == 0) base = atomicAdd(A.pa.hub_cnt + H.hub, tot);
+  base = __shfl(base, 0, kWave);
+  int pos = base + pre;
+  uint64_t *list = A.cand + H.hub * kCandCap;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (mask & (1 << q)) {
+      if (pos < kCandCap)
+        list[pos] = (uint64_t(word_of(r, q) >> shift) << 32) | (4 * g + q - uint64_t(H.lo));
+      ++pos;
+    }
+  }
+}
+
+__device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
+  const int64_t c_first = w * A.chunks_per_wave;
+  const int64_t c_end = min(c_first + A.chunks_per_wave, A.n_chunks);
+  int64_t h_lo = 0, h_hi = A.n_hubs;  // hub_choff[h_lo] <= c_first < hub_choff[h_hi]
+  while (h_hi - h_lo > 1) {
+    const int64_t mid = (h_lo + h_hi) >> 1;
+    if (A.pa.hub_choff[mid] <= c_first)
+      h_lo = mid;
+    else
+      h_hi = mid;
+  }
+  HubParams H = hub_params(A, h_lo);
+  const uint32_t shift = uint32_t(32 - A.key_bits);
+  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
+  for (int64_t chunk = c_first; chunk < c_end; ++chunk) {
+    while (chunk >= H.end_chunk) H = hub_params(A, H.hub + 1);
+    // (key >> shift) < tau  <=>  key < tau << shift  <=>  key <= lim
+    const uint64_t tau_raw = H.tau << shift;
+    const uint32_t lim = tau_raw - 1 >= 0xFFFFFFFFull ? 0xFFFFFFFFu : uint32_t(tau_raw - 1);
+    const int64_t c_lo = H.lo + (chunk - H.first_chunk) * kHubChunk;
+    const int64_t c_hi = min(c_lo + kHubChunk, H.lo + H.deg);
+    // steps k = 0 .. n_it-1 cover groups g_first + 64k ..; steps [k_lo, k_hi)
+    // lie wholly inside the chunk
+    const uint64_t g_first = uint64_t(c_lo) >> 2;
+    const uint64_t g_last = uint64_t(c_hi - 1) >> 2;
+    const int64_t n_it = int64_t((g_last - g_first) / kWave) + 1;
+    const int64_t k_lo = 4 * g_first >= uint64_t(c_lo) ? 0 : 1;
+    int64_t k_hi = int64_t((uint64_t(c_hi) / 4 - g_first) / kWave);
+    if (k_hi > n_it) k_hi = n_it;
+    if (k_hi < k_lo) k_hi = k_lo;
+    for (int64_t k = 0; k < k_lo; ++k)
+      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, k0, k1);
+    for (int64_t k = k_lo; k < k_hi; ++k)
+      hub_step<false>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, k0, k1);
+    for (int64_t k = k_hi; k < n_it; ++k)
+      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, k0, k1);
   }
 }
 
@@ -600,8 +735,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
     const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
     if (w < A.n_wave) role_wave_pairs(A, s_key[wave], s_j[wave], w);
   } else {
-    const int64_t chunk = (b - A.blocks_a - A.blocks_b) * kSampleWaves + wave;
-    if (chunk < A.n_chunks) role_hub_chunks(A, chunk);
+    const int64_t w = (b - A.blocks_a - A.blocks_b) * kSampleWaves + wave;
+    if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
   }
 }
 
@@ -723,6 +858,31 @@ __global__ void k_philox(const uint32_t *ctr, uint32_t k0, uint32_t k1,
   }
 }
 
+// ---- host handshake -----------------------------------------------------------
+
+// Copies the n readback slots to host memory, then sets the flag word
+// host[n] to `seq`: a host that sees `seq` there reads the slots as they are
+// at this point of the stream (every earlier kernel has finished).
+__global__ __launch_bounds__(256) void k_publish(const int64_t *small, int64_t *host,
+                                                 int32_t n, uint64_t seq) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) host[i] = small[i];
+  __threadfence_system();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    __hip_atomic_store(reinterpret_cast<uint64_t *>(host + n), seq, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// dst[i] = v.p[i] for i < n: small tables written in stream order with the
+// values carried in the launch itself.
+constexpr int kPtrBatch = 16;
+struct PtrBatch {
+  void *p[kPtrBatch];
+};
+__global__ void k_store_ptrs(void **dst, PtrBatch v, int32_t n) {
+  if (int(threadIdx.x) < n) dst[threadIdx.x] = v.p[threadIdx.x];
+}
+
 }  // namespace
 
 // ---- launchers ---------------------------------------------------------------
@@ -745,17 +905,38 @@ hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
 }
 
 int64_t count_tiles(int64_t n_items) {
-  const int64_t t = (n_items + kPairTile - 1) / kPairTile;
+  const int64_t per_tile = int64_t(kTileThreads) * pair_items(n_items);
+  const int64_t t = (n_items + per_tile - 1) / per_tile;
   return t < 1 ? 1 : t;
+}
+
+template <bool kStaged, int kItems>
+void count_launch(HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
+                  int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
+                  uint64_t ticket_base, int64_t *small, hipStream_t stream) {
+  hipLaunchKernelGGL((k_count_scan<kStaged, kItems>), dim3(unsigned(count_tiles(n_items))),
+                     dim3(kTileThreads), 0, stream, hv, es, n_etypes, n_types, n_items, pa,
+                     lb, epoch, ticket_base, small);
 }
 
 hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                              int32_t n_types, int64_t n_items, PairArrays pa,
                              Lookback lb, uint32_t epoch, uint64_t ticket_base,
                              int64_t *small, hipStream_t stream) {
-  hipLaunchKernelGGL(k_count_scan, dim3(unsigned(count_tiles(n_items))),
-                     dim3(kTileThreads), 0, stream, hv, es, n_etypes, n_types,
-                     n_items, pa, lb, epoch, ticket_base, small);
+  const bool staged = n_etypes <= kCountMaxEtypes;
+  const bool large = pair_items(n_items) == kPairItemsLarge;
+  if (staged && large)
+    count_launch<true, kPairItemsLarge>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
+                                        ticket_base, small, stream);
+  else if (staged)
+    count_launch<true, kPairItemsSmall>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
+                                        ticket_base, small, stream);
+  else if (large)
+    count_launch<false, kPairItemsLarge>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
+                                         ticket_base, small, stream);
+  else
+    count_launch<false, kPairItemsSmall>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
+                                         ticket_base, small, stream);
   return hipGetLastError();
 }
 
@@ -780,7 +961,11 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   static_assert(sizeof(GroupLds) <= sizeof(uint32_t) * kCandCap,
                 "a group's LDS fits in one wavefront's candidate list");
   A.blocks_b = (n_wave + kSampleWaves - 1) / kSampleWaves;
-  const int64_t blocks_c = (n_chunks + kSampleWaves - 1) / kSampleWaves;
+  // runs of chunks per wavefront: long enough to amortise finding the hub,
+  // short enough to leave about kHubWaves wavefronts for the chip
+  A.chunks_per_wave = std::min<int64_t>(kMaxChunksPerWave, std::max<int64_t>(1, n_chunks / kHubWaves));
+  const int64_t waves_c = (n_chunks + A.chunks_per_wave - 1) / A.chunks_per_wave;
+  const int64_t blocks_c = (waves_c + kSampleWaves - 1) / kSampleWaves;
   A.pa = pa;
   A.cand = cand;
   A.small = small;
@@ -810,6 +995,24 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
   hipLaunchKernelGGL(k_mark, dim3(unsigned(blocks)), dim3(256), 0, stream, es,
                      small + kSlotNew + n_types, n_etypes, n_edges, src_gid);
   return hipGetLastError();
+}
+
+hipError_t launch_publish(const int64_t *small, int64_t *host, int32_t n, uint64_t seq,
+                          hipStream_t stream) {
+  hipLaunchKernelGGL(k_publish, dim3(1), dim3(256), 0, stream, small, host, n, seq);
+  return hipGetLastError();
+}
+
+hipError_t launch_store_ptrs(void **dst, void *const *vals, int32_t n, hipStream_t stream) {
+  for (int32_t i = 0; i < n; i += kPtrBatch) {
+    PtrBatch v{};
+    const int32_t m = n - i < kPtrBatch ? n - i : kPtrBatch;
+    for (int32_t k = 0; k < m; ++k) v.p[k] = vals[i + k];
+    hipLaunchKernelGGL(k_store_ptrs, dim3(1), dim3(64), 0, stream, dst + i, v, m);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream) {
