@@ -33,7 +33,7 @@ constexpr int kCandCap = 512;
 constexpr int64_t kThreadTakeAll = 32;
 
 // Pairs that keep K < deg edges with deg > kHubChunk ("hubs") are sampled in
-// chunks of kHubChunk edges, one wavefront per chunk.
+// chunks of kHubChunk edges, handed to wavefronts in runs of chunks.
 constexpr int64_t kHubChunk = 2048;
 
 // Readback slots of the small device buffer (int64 each).
