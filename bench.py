@@ -1,10 +1,11 @@
 """Benchmark: heterogeneous mini-batch generation on one MI355X.
 
-One step = one mini-batch through the whole path: multi-hop per-edge-type
-fanout sampling, per-hop compaction into relabelled blocks, and the gather of
-the input frontier's features for every node type that has them
-(DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2).  Graph, features and
-seeds are resident in HBM before the timed region.
+One step = one mini-batch through the whole path, in one library call
+(hg_sample_blocks_gather): multi-hop per-edge-type fanout sampling, per-hop
+compaction into relabelled blocks, and the gather of the input frontier's
+features for every node type that has them (DistDGLv2, arXiv 2112.15345,
+Sec. 3.2 and Sec. 4.2).  Graph, features and seeds are resident in HBM before
+the timed region.
 
 Prints one JSON line.  `value` is sampled edges per second over whole steps;
 the gathered feature rate, per-stage times, the roofline of the dominant
@@ -91,6 +92,10 @@ def main():
     ap.add_argument("--workload", type=int, default=2,
                     help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
                          "5 gather-heavy academic")
+    ap.add_argument("--workers", type=int, default=4,
+                    help="pipeline worker threads (own streams); 0 = one direct call per step")
+    ap.add_argument("--depth", type=int, default=0,
+                    help="mini-batches outstanding in the pipeline (default 2 x workers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after warm-up (untimed), copy this many MiB device to device "
@@ -121,25 +126,8 @@ def main():
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
     row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
 
-    # HIP events recorded by the gather kernels themselves (on their stream)
-    hip_events = hg.HipEvents(2 * args.steps)
-    rec_events = [(hip_events.events[2 * i], hip_events.events[2 * i + 1])
-                  for i in range(args.steps)][::-1]
-
-    def step(b, rec=None):
-        blocks = g.sample_blocks(seeds[b], fan, b)
-        outs = g.gather_outputs(blocks, feat_types)
-        ev = rec_events.pop() if rec is not None else None
-        g.gather_features_all(blocks, outs=outs, events=ev)
-        if rec is not None:
-            rec.append((ev[0], ev[1], {t: outs[t].shape[0] for t in feat_types}))
-        return blocks, outs
-
-    for b in range(args.warmup):
-        step(b)
-    torch.cuda.synchronize()
-    log("warm-up done")
     if args.copy_calibration_mb > 0:
+        # a copy of known size, untimed, for scaling the memory counters
         src = torch.ones(args.copy_calibration_mb << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
@@ -148,29 +136,86 @@ def main():
         log(f"calibration copy of {args.copy_calibration_mb} MiB done")
         del src, dst
 
+    # HIP events recorded by the gather kernels themselves (on their stream)
+    hip_events = hg.HipEvents(2 * args.steps)
+    events = {args.warmup + i: (hip_events.events[2 * i], hip_events.events[2 * i + 1])
+              for i in range(args.steps)}
     gather_rec = []
-    sample_ms = []
-    edges = 0
-    rows = 0
-    gbytes = 0
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for i in range(args.steps):
-        b = args.warmup + i
-        ts = time.perf_counter()
-        blocks, outs = step(b, gather_rec)
-        sample_ms.append(None)
-        for h in range(len(fan)):
-            for e in range(g.R):
-                edges += blocks.num_edges(h, e)
-        for t in feat_types:
-            n = blocks.num_input_nodes(t)
-            rows += n
-            gbytes += n * row_bytes[t]
-        del blocks, outs
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
+
+    def consumed(b, blocks):
+        """Bookkeeping of a returned mini-batch: (sampled edges, gathered rows, bytes)."""
+        e = sum(blocks.num_edges(h, r) for h in range(len(fan)) for r in range(g.R))
+        rows_t = {t: blocks.num_input_nodes(t) for t in feat_types}
+        if b in events:
+            gather_rec.append((events[b][0], events[b][1], rows_t))
+        return e, sum(rows_t.values()), sum(n * row_bytes[t] for t, n in rows_t.items())
+
+    if args.workers == 0:
+        # one call per mini-batch on the current stream
+        def run(b):
+            return g.sample_blocks(seeds[b], fan, b, gather=feat_types, events=events.get(b))
+
+        for b in range(args.warmup):
+            consumed(b, run(b))
+        torch.cuda.synchronize()
+        log("warm-up done")
+        totals = [0, 0, 0]
+        t_start = time.perf_counter()
+        for b in range(args.warmup, n_batches):
+            blocks = run(b)
+            for k, v in enumerate(consumed(b, blocks)):
+                totals[k] += v
+            del blocks
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+    else:
+        # the pipeline: mini-batches generated ahead by worker threads, each on
+        # its own stream, returned in order; at most `depth` outstanding
+        depth = args.depth or 2 * args.workers
+        pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=feat_types)
+        nxt = 0
+
+        def submit_more():
+            nonlocal nxt
+            while nxt < n_batches and nxt - done[0] < depth:
+                pipe.submit(seeds[nxt], fan, nxt, events=events.get(nxt))
+                nxt += 1
+
+        done = [0]
+        submit_more()
+        for b in range(args.warmup):
+            consumed(b, pipe.next())
+            done[0] += 1
+            submit_more()
+        torch.cuda.synchronize()
+        log(f"warm-up done ({args.workers} workers, depth {depth})")
+        totals = [0, 0, 0]
+        t_start = time.perf_counter()
+        for b in range(args.warmup, n_batches):
+            blocks = pipe.next()
+            done[0] += 1
+            submit_more()
+            for k, v in enumerate(consumed(b, blocks)):
+                totals[k] += v
+            del blocks
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+        pipe.close()
+    edges, rows, gbytes = totals
     ms_per_step = elapsed / args.steps * 1e3
+
+    # context for the roofline: the same gather with nothing else on the GPU
+    # (a few direct calls after the timed region, untimed)
+    iso = hg.HipEvents(2)
+    iso_ms, iso_bytes = 0.0, 0
+    for b in range(min(3, n_batches)):
+        torch.cuda.synchronize()
+        blocks = g.sample_blocks(seeds[b], fan, b, gather=feat_types,
+                                 events=(iso.events[0], iso.events[1]))
+        iso_ms += iso.elapsed_ms(iso.events[0], iso.events[1])
+        iso_bytes += sum(blocks.num_input_nodes(t) * (2 * row_bytes[t] + 8) for t in feat_types)
+        del blocks
+    iso_gbps = iso_bytes / (iso_ms / 1e3) / 1e9 if iso_ms > 0 else 0.0
 
     # gather kernel (one launch per step for all feature types): algorithmic
     # bytes per row = read its id (8) + read the row + write the row
@@ -198,7 +243,10 @@ def main():
                    "seeds_per_batch": wl.batch, "fanouts_per_hop": list(wl.fanouts),
                    "node_types": len(gen.num_nodes), "edge_types": g.R,
                    "edges_in_graph": int(sum(ix.numel() for _, _, _, ix in gen.etypes)),
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU",
+                   "pipeline": (f"{args.workers} worker streams, depth "
+                                f"{args.depth or 2 * args.workers}" if args.workers
+                                else "one call per step")},
         "gathered_GBps": gbytes / elapsed / 1e9,
         "sampled_edges_per_step": edges / args.steps,
         "gathered_rows_per_step": rows / args.steps,
@@ -208,7 +256,9 @@ def main():
                      "frac": g_achieved / HBM_PEAK_GBS,
                      "traffic": measured_gather_traffic(args.workload, args.steps, args.warmup),
                      "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
-                     "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3},
+                     "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3,
+                     "isolated_achieved": iso_gbps,
+                     "isolated_frac": iso_gbps / HBM_PEAK_GBS},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(gen, wl, first_batch=args.warmup)

@@ -91,6 +91,7 @@ typedef struct hg_allocator {
 
 typedef struct hg_graph hg_graph;
 typedef struct hg_blocks hg_blocks;
+typedef struct hg_pipeline hg_pipeline;
 
 /* Creates an immutable graph handle over borrowed device arrays.
  * Checks the descriptors on the host and the arrays on the device (indptr
@@ -106,6 +107,10 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
 
 /* Releases the handle and its workspaces (synchronises the device). */
 void hg_destroy(hg_graph *graph);
+
+/* Number of node types and edge types of a graph handle (either output may
+ * be NULL). */
+hg_status hg_graph_types(const hg_graph *graph, int32_t *n_ntypes, int32_t *n_etypes);
 
 /* One mini-batch (Sec. 3.2, Sec. 4.2.2).
  * seeds: host array of n_ntypes device pointers; seeds[t] holds n_seeds[t]
@@ -188,13 +193,75 @@ hg_status hg_gather_features_multi_timed(hg_graph *graph, const hg_blocks *block
                                          int32_t n, hipStream_t stream,
                                          hipEvent_t start, hipEvent_t stop);
 
+/* One mini-batch together with its input features (Sec. 4.2.1: a mini-batch
+ * is the sampled blocks plus the features of the input frontier).  Samples as
+ * hg_sample_blocks does, then gathers the input-frontier rows of every node
+ * type in gather_ntypes (host int32 [n_gather], each featured and listed at
+ * most once) into device arrays that the blocks handle owns; read them with
+ * hg_blocks_features.  The outputs come from the graph's allocator like the
+ * block arrays.  start / stop (either may be NULL) are carried by the gather
+ * launches as in hg_gather_features_multi_timed.  HG_EINVAL for a bad type
+ * list; otherwise as hg_sample_blocks.  The gather is asynchronous on
+ * `stream` when the call returns. */
+hg_status hg_sample_blocks_gather(hg_graph *graph, const int64_t *const *seeds,
+                                  const int64_t *n_seeds, int32_t n_hops,
+                                  const int32_t *fanouts, uint64_t rng_seed,
+                                  const int32_t *gather_ntypes, int32_t n_gather,
+                                  hipEvent_t start, hipEvent_t stop, hipStream_t stream,
+                                  hg_blocks **out);
+
+/* The rows gathered for node type `ntype` by hg_sample_blocks_gather:
+ * *rows = n_input(ntype) and *feat = device [rows, dim] of the type's dtype,
+ * owned by the handle; *rows = 0 and *feat = NULL when the type was not
+ * gathered.  Either output pointer may be NULL. */
+hg_status hg_blocks_features(const hg_blocks *blocks, int32_t ntype, int64_t *rows,
+                             const void **feat);
+
 /* out[i, :] = feat_ntype[ids[i], :] for i < n (ids: device int64 [n]).
  * Asynchronous; an id outside [0, num_nodes) yields a zero row. */
 hg_status hg_gather_rows(hg_graph *graph, int32_t ntype, const int64_t *ids,
                          int64_t n, void *out, hipStream_t stream);
 
-/* Releases a blocks handle (stream-ordered on the stream it was made on). */
+/* Releases a blocks handle (stream-ordered on the stream it was made on;
+ * on the null stream for handles returned by hg_pipeline_next). */
 void hg_blocks_free(hg_blocks *blocks);
+
+/* A mini-batch pipeline (Sec. 4.2.1: mini-batches are generated ahead of
+ * their use by concurrent stages with bounded queues between them).
+ * n_workers (1..16) host threads, each with its own HIP stream (created here,
+ * default priority) and its own workspace of the graph, run submitted
+ * mini-batches concurrently with hg_sample_blocks_gather, so that the stream
+ * waits of one overlap the kernels of another.  Mini-batches come back in
+ * submission order; at most `capacity` (>= 1) are submitted and not yet
+ * returned.  gather_ntypes (host int32 [n_gather], copied): the node types
+ * whose input features every mini-batch gathers (may be empty).  The graph
+ * must outlive the pipeline. */
+hg_status hg_pipeline_create(hg_graph *graph, int32_t n_workers, int32_t capacity,
+                             const int32_t *gather_ntypes, int32_t n_gather,
+                             hg_pipeline **out);
+
+/* Queues one mini-batch: seeds, n_seeds, n_hops, fanouts and rng_seed as in
+ * hg_sample_blocks (n_seeds and fanouts are copied; the seed arrays are read
+ * on a worker's stream and must stay valid until the mini-batch has been
+ * returned by hg_pipeline_next).  start / stop: optional events carried by
+ * its gather launches.  Waits while `capacity` mini-batches are outstanding.
+ * Argument errors found later (bad seeds, ...) are returned by
+ * hg_pipeline_next for that mini-batch. */
+hg_status hg_pipeline_submit(hg_pipeline *pipe, const int64_t *const *seeds,
+                             const int64_t *n_seeds, int32_t n_hops,
+                             const int32_t *fanouts, uint64_t rng_seed, hipEvent_t start,
+                             hipEvent_t stop);
+
+/* Waits for the oldest outstanding mini-batch.  On success *out owns its
+ * blocks and gathered features (hg_blocks_free) and all of its device work
+ * has completed.  A mini-batch that failed returns its status (and
+ * hg_last_error its text) with *out = NULL; later ones are unaffected.
+ * HG_EINVAL when none is outstanding. */
+hg_status hg_pipeline_next(hg_pipeline *pipe, hg_blocks **out);
+
+/* Finishes the queued mini-batches, frees those not returned, stops the
+ * workers and releases the streams. */
+void hg_pipeline_destroy(hg_pipeline *pipe);
 
 /* Thread-local description of the last failure on this thread. */
 const char *hg_last_error(void);

@@ -16,6 +16,7 @@ is not built; there is no CPU path.
 """
 from __future__ import annotations
 
+import collections
 import ctypes
 import os
 
@@ -34,6 +35,9 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_blocks_num_hops", "hg_blocks_nodes", "hg_blocks_edges",
                "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_features_multi",
                "hg_gather_features_multi_timed", "hg_gather_rows",
+               "hg_sample_blocks_gather", "hg_blocks_features", "hg_graph_types",
+               "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
+               "hg_pipeline_destroy",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 
@@ -83,6 +87,14 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_gather_features_multi": ([_P, _P, _P, _P, _I32, _P], _I32),
         "hg_gather_features_multi_timed": ([_P, _P, _P, _P, _I32, _P, _P, _P], _I32),
         "hg_gather_rows": ([_P, _I32, _P, _I64, _P, _P], _I32),
+        "hg_sample_blocks_gather": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _P, _P,
+                                     _PP], _I32),
+        "hg_blocks_features": ([_P, _I32, _PI64, _PP], _I32),
+        "hg_graph_types": ([_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)], _I32),
+        "hg_pipeline_create": ([_P, _I32, _I32, _P, _I32, _PP], _I32),
+        "hg_pipeline_submit": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _P], _I32),
+        "hg_pipeline_next": ([_P, _PP], _I32),
+        "hg_pipeline_destroy": ([_P], None),
         "hg_blocks_free": ([_P], None),
         "hg_last_error": ([], ctypes.c_char_p),
         "hg_debug_philox": ([_P, ctypes.c_uint64, _I64, _P, _P], _I32),
@@ -134,7 +146,7 @@ class _DeviceArray:
         self._owner = owner
 
 
-_TYPESTR = {torch.int64: "<i8", torch.int32: "<i4"}
+_TYPESTR = {torch.int64: "<i8", torch.int32: "<i4", torch.uint8: "|u1"}
 
 
 def _view(ptr: int, n: int, dtype, owner, device) -> torch.Tensor:
@@ -194,6 +206,21 @@ class Blocks:
         _check(load_library().hg_blocks_input_nodes(self._h, ntype, ctypes.byref(n),
                                                     ctypes.byref(p)))
         return _view(p.value, n.value, torch.int64, self, self.device)
+
+    def features(self, ntype: int):
+        """Rows gathered for `ntype` by sample_blocks(..., gather=...): a
+        [rows, dim] tensor of the type's dtype (a view of library memory), or
+        None when the type was not gathered."""
+        rows, p = _I64(), ctypes.c_void_p()
+        _check(load_library().hg_blocks_features(self._h, ntype, ctypes.byref(rows),
+                                                 ctypes.byref(p)))
+        if not p.value:
+            return None
+        feat = self.graph.ntypes[ntype][1]
+        dim = feat.shape[1]
+        nbytes = rows.value * dim * feat.element_size()
+        return _view(p.value, nbytes, torch.uint8, self, self.device).view(feat.dtype).view(
+            rows.value, dim)
 
     def num_input_nodes(self, ntype: int) -> int:
         n = _I64()
@@ -256,9 +283,12 @@ class Graph:
         return len(self.etypes)
 
     def sample_blocks(self, seeds, fanouts, rng_seed: int = 0, key_bits: int = 32,
-                      stream=None) -> Blocks:
+                      stream=None, gather=None, events=None) -> Blocks:
         """seeds: per node type an int64 device tensor or None; fanouts:
-        [n_hops][n_etypes] (hop 0 starts from the seeds; -1 = all)."""
+        [n_hops][n_etypes] (hop 0 starts from the seeds; -1 = all).
+        gather: None, "all" (every featured type) or a list of node types whose
+        input-frontier rows the same call gathers (Blocks.features); events:
+        optional (start, stop) raw hipEvent_t handles carried by that gather."""
         lib = load_library()
         T, R = self.T, self.R
         if len(seeds) != T:
@@ -280,8 +310,22 @@ class Graph:
             raise ValueError("fanouts must be [n_hops][n_etypes]")
         fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
         h = ctypes.c_void_p()
-        _check(lib.hg_sample_blocks_ex(self._h, ptrs, counts, H, fo, int(rng_seed) & (2**64 - 1),
-                                       int(key_bits), _stream(stream), ctypes.byref(h)))
+        if gather is None:
+            _check(lib.hg_sample_blocks_ex(self._h, ptrs, counts, H, fo,
+                                           int(rng_seed) & (2**64 - 1), int(key_bits),
+                                           _stream(stream), ctypes.byref(h)))
+            return Blocks(self, h, H)
+        if key_bits != 32:
+            raise ValueError("gather=... samples with full 32-bit keys")
+        if isinstance(gather, str):
+            if gather != "all":
+                raise ValueError('gather must be None, "all" or a list of node types')
+            gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
+        start, stop = events if events is not None else (None, None)
+        _check(lib.hg_sample_blocks_gather(self._h, ptrs, counts, H, fo,
+                                           int(rng_seed) & (2**64 - 1), gt, len(gather),
+                                           start, stop, _stream(stream), ctypes.byref(h)))
         return Blocks(self, h, H)
 
     def gather_features(self, blocks: Blocks, ntype: int, out: torch.Tensor | None = None,
@@ -342,6 +386,76 @@ class Graph:
                                              out.data_ptr() if out.numel() else None,
                                              _stream(stream)))
         return out
+
+
+class Pipeline:
+    """Mini-batches generated ahead of use (hg_pipeline_*): `workers` host
+    threads with their own streams run submitted mini-batches concurrently;
+    next() returns them in submission order, complete on the device.  At most
+    `capacity` are outstanding (submit waits).  gather: node types whose input
+    features every mini-batch gathers ("all": every featured type)."""
+
+    def __init__(self, graph: Graph, workers: int = 2, capacity: int = 4, gather="all"):
+        self.graph = graph
+        if isinstance(gather, str):
+            if gather != "all":
+                raise ValueError('gather must be "all" or a list of node types')
+            gather = [t for t, (_, f) in enumerate(graph.ntypes) if f is not None]
+        gather = [int(t) for t in (gather or [])]
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*gather)
+        h = ctypes.c_void_p()
+        _check(load_library().hg_pipeline_create(graph._h, int(workers), int(capacity), gt,
+                                                 len(gather), ctypes.byref(h)))
+        self._h = h
+        self._held = collections.deque()  # seed tensors of outstanding mini-batches
+
+    def submit(self, seeds, fanouts, rng_seed: int = 0, events=None):
+        g = self.graph
+        T, R = g.T, g.R
+        if len(seeds) != T:
+            raise ValueError("one seed entry per node type")
+        keep = []
+        ptrs = (ctypes.c_void_p * T)()
+        counts = (ctypes.c_int64 * T)()
+        for t, s in enumerate(seeds):
+            if s is None:
+                continue
+            s = _dev_i64(s, g.device)
+            keep.append(s)
+            counts[t] = s.numel()
+            ptrs[t] = s.data_ptr() if s.numel() else None
+        H = len(fanouts)
+        flat = [int(k) for row in fanouts for k in row]
+        if len(flat) != H * R:
+            raise ValueError("fanouts must be [n_hops][n_etypes]")
+        fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        start, stop = events if events is not None else (None, None)
+        self._held.append(keep)
+        try:
+            _check(load_library().hg_pipeline_submit(self._h, ptrs, counts, H, fo,
+                                                     int(rng_seed) & (2**64 - 1), start, stop))
+        except Exception:
+            self._held.pop()
+            raise
+
+    def next(self) -> Blocks:
+        if not self._held:
+            raise HGError(HG_EINVAL, "no mini-batch outstanding")
+        h = ctypes.c_void_p()
+        st = load_library().hg_pipeline_next(self._h, ctypes.byref(h))
+        self._held.popleft()  # the oldest mini-batch is returned, or its error
+        _check(st)
+        return Blocks(self.graph, h, load_library().hg_blocks_num_hops(h))
+
+    def close(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.hg_pipeline_destroy(h)
+            self._h = None
+            self._held.clear()
+
+    def __del__(self):
+        self.close()
 
 
 class HipEvents:

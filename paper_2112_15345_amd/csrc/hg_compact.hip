@@ -40,7 +40,7 @@ struct CompactArgs {
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
-  int64_t *tile_pre;  // per tile: set bits of its type in earlier tiles
+  int64_t *tile_pre;  // per tile: set bits of its type in earlier tiles (or look-back words)
   int32_t *tile_cnt;  // per tile: set bits
   int64_t *small;
 };
@@ -110,22 +110,14 @@ __global__ __launch_bounds__(kScanThreads) void k_bits_scan(CompactArgs A) {
   }
 }
 
-// 3. Ranks the set bits of a tile within its node type, gives each new vertex
-// its local ID and clears the tile's words.
-__global__ __launch_bounds__(kTileThreads) void k_bits_assign(CompactArgs A) {
-  __shared__ int64_t lds[8];
-  const int64_t tile = blockIdx.x;
-  if (A.tile_cnt[tile] == 0) return;
-  const int t = find_segment(A.tile_base, A.n_types, tile);
-  const int64_t first = A.tile_base[t];
-  const uint2 ab = tile_words(A, tile);
-  const uint32_t words[kTileItems] = {ab.x, ab.y};
-  int64_t total;
-  const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &total);
+// Gives the set bits of a tile's words `ab` (thread's share), the first of
+// which has local ID `local`, their local IDs and clears the words.
+__device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t first,
+                                            int64_t tile, uint2 ab, int64_t local) {
   if ((ab.x | ab.y) == 0) return;
   int32_t *map = A.ts[t].map;
   int64_t *out = A.hv.src_out[t];
-  int64_t local = A.hv.nF[t] + A.tile_pre[tile] + pre;
+  const uint32_t words[kTileItems] = {ab.x, ab.y};
   const int64_t v0 = ((tile - first) * kTile + threadIdx.x * kTileItems) * 32;
 #pragma unroll
   for (int k = 0; k < kTileItems; ++k) {
@@ -140,6 +132,44 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_assign(CompactArgs A) {
     }
   }
   *reinterpret_cast<uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems) = uint2{0, 0};
+}
+
+// 3. Ranks the set bits of a tile within its node type, gives each new vertex
+// its local ID and clears the tile's words.
+__global__ __launch_bounds__(kTileThreads) void k_bits_assign(CompactArgs A) {
+  __shared__ int64_t lds[8];
+  const int64_t tile = blockIdx.x;
+  if (A.tile_cnt[tile] == 0) return;
+  const int t = find_segment(A.tile_base, A.n_types, tile);
+  const uint2 ab = tile_words(A, tile);
+  int64_t total;
+  const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &total);
+  assign_bits(A, t, A.tile_base[t], tile, ab, A.hv.nF[t] + A.tile_pre[tile] + pre);
+}
+
+// The three steps in one launch for a few tiles: tiles in ticket order, each
+// tile's prefix within its type by decoupled look-back (words in tile_pre);
+// the last tile of a type writes the type's count.  Tickets past the tiles
+// copy the frontier.
+__global__ __launch_bounds__(kTileThreads) void k_bits_single(CompactArgs A, uint32_t epoch,
+                                                              uint64_t ticket_base) {
+  __shared__ int64_t lds[8];
+  const int64_t tile = take_ticket(A.small, ticket_base, lds);
+  if (tile >= A.n_tiles) {
+    copy_tile(A, tile - A.n_tiles);
+    return;
+  }
+  const int t = find_segment(A.tile_base, A.n_types, tile);
+  const int64_t first = A.tile_base[t];
+  const uint2 ab = tile_words(A, tile);
+  int64_t agg[1];
+  const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &agg[0]);
+  int64_t ex[1];
+  tile_lookback<1>(Lookback{reinterpret_cast<uint64_t *>(A.tile_pre)}, tile, first, epoch, agg,
+                   ex, A.small);
+  if (tile == A.tile_base[t + 1] - 1 && threadIdx.x == 0)
+    A.small[kSlotNew + t] = ex[0] + agg[0];  // new vertices of type t
+  assign_bits(A, t, first, tile, ab, A.hv.nF[t] + ex[0] + pre);
 }
 
 // Next hop's frontier sizes (this hop's plus the new vertices of each type)
@@ -179,17 +209,26 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
-                          int64_t *small, hipStream_t stream) {
+                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
+                          int64_t *ticketed, hipStream_t stream) {
   CompactArgs A{hv, ts, n_types, bitmap, tile_base, n_tiles, copy_total, tile_sums,
                 reinterpret_cast<int32_t *>(tile_sums + n_tiles), small};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
+  *ticketed = 0;
+  if (n_tiles <= kSinglePassTiles) {
+    const int64_t blocks = n_tiles + copy_blocks;
+    if (blocks > 0) {
+      hipLaunchKernelGGL(k_bits_single, dim3(unsigned(blocks)), dim3(kTileThreads), 0, stream,
+                         A, epoch, ticket_base);
+      *ticketed = blocks;
+    }
+    return hipGetLastError();
+  }
   if (n_tiles + copy_blocks > 0)
     hipLaunchKernelGGL(k_bits_count, dim3(unsigned(n_tiles + copy_blocks)),
                        dim3(kTileThreads), 0, stream, A);
   hipLaunchKernelGGL(k_bits_scan, dim3(1), dim3(kScanThreads), 0, stream, A);
-  if (n_tiles > 0)
-    hipLaunchKernelGGL(k_bits_assign, dim3(unsigned(n_tiles)), dim3(kTileThreads), 0,
-                       stream, A);
+  hipLaunchKernelGGL(k_bits_assign, dim3(unsigned(n_tiles)), dim3(kTileThreads), 0, stream, A);
   return hipGetLastError();
 }
 

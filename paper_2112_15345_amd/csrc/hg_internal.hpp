@@ -4,6 +4,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "hg.h"
+
 #include <cstddef>
 #include <cstdint>
 
@@ -27,6 +29,9 @@ inline int pair_items(int64_t n_items) {
 // Candidate capacity of one bottom-K selection (LDS entries per wavefront,
 // and per hub in the global candidate lists).
 constexpr int kCandCap = 512;
+
+// Node types whose per-hop table entries travel inside a launch's arguments.
+constexpr int kInlineTypes = 8;
 
 // Pairs whose in-edges are all kept and number at most this many are copied
 // 64 pairs per wavefront; larger ones by a wavefront each.
@@ -102,6 +107,15 @@ struct PairArrays {
   int64_t *hub_choff; // per hub: its first chunk (strictly increasing)
 };
 
+// ---- runtime hooks (hg_runtime.cpp) for the pipeline ------------------------
+
+// Sets this thread's hg_last_error text; returns st.
+hg_status set_error(hg_status st, const char *msg);
+// Later frees of the handle's arrays are ordered on the null stream (its own
+// stream is going away; its work has completed).
+void blocks_detach_stream(hg_blocks *b);
+int graph_device(const hg_graph *g);
+
 // ---- launchers (all asynchronous on `stream`) -------------------------------
 
 // The hop-0 frontier: map[seed] = position; flags range errors and repeats.
@@ -109,9 +123,11 @@ hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
                                   int32_t n_types, int64_t total, int64_t *small,
                                   hipStream_t stream);
 // map[v] = -1 for every vertex of the hop's frontier (in-range entries only);
-// `bound` >= the frontier's total size, which is read on the device.
+// `bound` >= the frontier's total size, which is read on the device.  Also
+// zeroes small[0..n_small), ready for the next call.
 hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
-                            int64_t bound, hipStream_t stream);
+                            int64_t bound, int64_t *small, int32_t n_small,
+                            hipStream_t stream);
 
 // Counting pass over n_items >= P + 1 pair slots (P = pair_base[R]): per pair
 // its in-edge range; exclusive scans of kept edges, hub chunks, wavefront
@@ -129,12 +145,15 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
 // Then one wavefront per hub selects from its list.  Writes each pair's kept
 // edges at off[p], grouped by pair, ascending edge ID: source vertex, edge
 // ID, destination local ID.
+// The sampler launches.  With n_src_out <= kInlineTypes the first one also
+// stores src_out[0..n_src_out) into src_out_slot (the hop's table entries).
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t n_types, int64_t n_pairs, int64_t n_wave,
                          int64_t n_chunks, int64_t n_hubs, PairArrays pa,
                          uint64_t *cand, const int64_t *small, uint64_t sigma,
                          int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
+                         int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          hipStream_t stream);
 
 // Sets the bitmap bit of every kept edge's source that is not in the
@@ -144,16 +163,20 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
                        int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
                        hipStream_t stream);
 
-// Compaction pass, three launches: per bitmap tile, ranks of the set bits
-// within the node type (reduce, scan, rank) -> local IDs n_frontier + rank,
-// written to the map and the source list, bits cleared; the scan writes each
-// type's new-vertex count to small[kSlotNew + t]; extra blocks copy the
-// frontier into the head of the source lists.  tile_sums: device scratch of
-// 2 * n_tiles 64-bit words.
+// Compaction pass: per bitmap tile, ranks of the set bits within the node
+// type -> local IDs n_frontier + rank, written to the map and the source
+// list, bits cleared; each type's new-vertex count goes to small[kSlotNew + t];
+// extra blocks copy the frontier into the head of the source lists.  Up to
+// kSinglePassTiles tiles: one launch, a single-pass scan whose look-back words
+// are tile_sums (ticketed blocks: *ticketed is their number).  Beyond: three
+// launches (reduce, scan, rank) with no inter-block waits; *ticketed = 0.
+// tile_sums: device scratch of 2 * n_tiles 64-bit words.
+constexpr int64_t kSinglePassTiles = 256;
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
-                          int64_t *small, hipStream_t stream);
+                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
+                          int64_t *ticketed, hipStream_t stream);
 
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.

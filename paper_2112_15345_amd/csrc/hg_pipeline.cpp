@@ -1,0 +1,245 @@
+// Mini-batch pipeline of the C ABI in include/hg.h (DistDGLv2, arXiv
+// 2112.15345, Sec. 4.2.1: mini-batches are generated ahead of their use by
+// concurrent stages with bounded queues between them).
+//
+// Worker threads, each with its own HIP stream (and so its own workspace of the
+// graph handle), take submitted mini-batches in order and run them with
+// hg_sample_blocks_gather.  While one worker waits on its stream (the per-hop
+// size readbacks), the others keep the GPU busy, so the waits and the host's
+// launch work of one mini-batch overlap the kernels of the next.  Results are
+// handed back in submission order.
+#include <condition_variable>
+#include <deque>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "hg.h"
+#include "hg_internal.hpp"
+
+struct hg_pipeline {
+  struct Job {
+    uint64_t seq;
+    std::vector<const int64_t *> seeds;
+    std::vector<int64_t> n_seeds;
+    int32_t n_hops;
+    std::vector<int32_t> fanouts;
+    uint64_t sigma;
+    hipEvent_t start, stop;
+  };
+  struct Result {
+    hg_blocks *b = nullptr;
+    hg_status st = HG_OK;
+    std::string err;
+    hipEvent_t done = nullptr;
+  };
+
+  hg_graph *g = nullptr;
+  int device = 0;
+  int32_t T = 0, R = 0;
+  int32_t capacity = 1;
+  std::vector<int32_t> gather;
+  std::vector<hipStream_t> streams;
+  std::vector<std::thread> workers;
+
+  std::mutex mu;
+  std::condition_variable cv_job, cv_result, cv_space;
+  std::deque<Job> jobs;
+  std::map<uint64_t, Result> results;
+  std::vector<hipEvent_t> free_events;
+  uint64_t submitted = 0, returned = 0;
+  bool stopping = false;
+
+  void work(int k);
+};
+
+void hg_pipeline::work(int k) {
+  (void)hipSetDevice(device);
+  hipStream_t s = streams[size_t(k)];
+  for (;;) {
+    Job j;
+    {
+      std::unique_lock<std::mutex> lk(mu);
+      cv_job.wait(lk, [&] { return stopping || !jobs.empty(); });
+      if (jobs.empty()) return;
+      j = std::move(jobs.front());
+      jobs.pop_front();
+    }
+    Result r;
+    r.st = hg_sample_blocks_gather(g, j.seeds.data(), j.n_seeds.data(), j.n_hops,
+                                   j.fanouts.empty() ? nullptr : j.fanouts.data(), j.sigma,
+                                   gather.empty() ? nullptr : gather.data(),
+                                   int32_t(gather.size()), j.start, j.stop, s, &r.b);
+    if (r.st != HG_OK) {
+      r.err = hg_last_error();
+    } else {
+      {
+        std::lock_guard<std::mutex> lk(mu);
+        if (!free_events.empty()) {
+          r.done = free_events.back();
+          free_events.pop_back();
+        }
+      }
+      hipError_t e = r.done ? hipSuccess : hipEventCreateWithFlags(&r.done, hipEventDisableTiming);
+      if (e == hipSuccess) e = hipEventRecord(r.done, s);
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        r.err = std::string("pipeline: event: ") + hipGetErrorString(e);
+        r.st = HG_EDEVICE;
+      }
+    }
+    {
+      std::lock_guard<std::mutex> lk(mu);
+      results.emplace(j.seq, std::move(r));
+    }
+    cv_result.notify_all();
+  }
+}
+
+extern "C" {
+
+hg_status hg_pipeline_create(hg_graph *g, int32_t n_workers, int32_t capacity,
+                             const int32_t *gather_ntypes, int32_t n_gather,
+                             hg_pipeline **out) {
+  if (!out) return hg::set_error(HG_EINVAL, "hg_pipeline_create: out is NULL");
+  *out = nullptr;
+  if (!g) return hg::set_error(HG_EINVAL, "hg_pipeline_create: graph is NULL");
+  if (n_workers < 1 || n_workers > 16)
+    return hg::set_error(HG_EINVAL, "hg_pipeline_create: n_workers not in 1..16");
+  if (capacity < 1) return hg::set_error(HG_EINVAL, "hg_pipeline_create: capacity < 1");
+  if (n_gather < 0 || (n_gather > 0 && !gather_ntypes))
+    return hg::set_error(HG_EINVAL, "hg_pipeline_create: bad node type list");
+  auto *p = new (std::nothrow) hg_pipeline();
+  if (!p) return hg::set_error(HG_ENOMEM, "hg_pipeline_create: out of host memory");
+  p->g = g;
+  p->device = hg::graph_device(g);
+  p->capacity = capacity;
+  p->gather.assign(gather_ntypes, gather_ntypes + n_gather);
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(p->device);
+  for (int32_t k = 0; k < n_workers; ++k) {
+    hipStream_t s = nullptr;
+    if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) {
+      (void)hipGetLastError();
+      for (hipStream_t x : p->streams) (void)hipStreamDestroy(x);
+      (void)hipSetDevice(prev);
+      delete p;
+      return hg::set_error(HG_EDEVICE, "hg_pipeline_create: stream creation failed");
+    }
+    p->streams.push_back(s);
+  }
+  (void)hipSetDevice(prev);
+  try {
+    for (int32_t k = 0; k < n_workers; ++k) p->workers.emplace_back(&hg_pipeline::work, p, k);
+  } catch (...) {
+    {
+      std::lock_guard<std::mutex> lk(p->mu);
+      p->stopping = true;
+    }
+    p->cv_job.notify_all();
+    for (auto &t : p->workers) t.join();
+    for (hipStream_t x : p->streams) (void)hipStreamDestroy(x);
+    delete p;
+    return hg::set_error(HG_ENOMEM, "hg_pipeline_create: cannot start worker threads");
+  }
+  *out = p;
+  return HG_OK;
+}
+
+hg_status hg_pipeline_submit(hg_pipeline *p, const int64_t *const *seeds,
+                             const int64_t *n_seeds, int32_t n_hops,
+                             const int32_t *fanouts, uint64_t rng_seed, hipEvent_t start,
+                             hipEvent_t stop) {
+  if (!p) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: pipeline is NULL");
+  if (!n_seeds) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: n_seeds is NULL");
+  if (n_hops < 0) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: n_hops < 0");
+  int32_t T = 0, R = 0;
+  if (hg_graph_types(p->g, &T, &R) != HG_OK) return HG_EINVAL;
+  if (n_hops > 0 && R > 0 && !fanouts)
+    return hg::set_error(HG_EINVAL, "hg_pipeline_submit: fanouts is NULL");
+  hg_pipeline::Job j;
+  try {
+    j.seeds.assign(size_t(T), nullptr);
+    if (seeds) j.seeds.assign(seeds, seeds + T);
+    j.n_seeds.assign(n_seeds, n_seeds + T);
+    if (fanouts) j.fanouts.assign(fanouts, fanouts + size_t(n_hops) * size_t(R));
+  } catch (const std::bad_alloc &) {
+    return hg::set_error(HG_ENOMEM, "hg_pipeline_submit: out of host memory");
+  }
+  j.n_hops = n_hops;
+  j.sigma = rng_seed;
+  j.start = start;
+  j.stop = stop;
+  {
+    std::unique_lock<std::mutex> lk(p->mu);
+    p->cv_space.wait(lk, [&] { return p->submitted - p->returned < uint64_t(p->capacity); });
+    j.seq = p->submitted++;
+    p->jobs.push_back(std::move(j));
+  }
+  p->cv_job.notify_one();
+  return HG_OK;
+}
+
+hg_status hg_pipeline_next(hg_pipeline *p, hg_blocks **out) {
+  if (!out) return hg::set_error(HG_EINVAL, "hg_pipeline_next: out is NULL");
+  *out = nullptr;
+  if (!p) return hg::set_error(HG_EINVAL, "hg_pipeline_next: pipeline is NULL");
+  hg_pipeline::Result r;
+  {
+    std::unique_lock<std::mutex> lk(p->mu);
+    if (p->returned == p->submitted)
+      return hg::set_error(HG_EINVAL, "hg_pipeline_next: no mini-batch outstanding");
+    const uint64_t seq = p->returned;
+    p->cv_result.wait(lk, [&] { return p->results.count(seq) != 0; });
+    auto it = p->results.find(seq);
+    r = std::move(it->second);
+    p->results.erase(it);
+    p->returned++;
+  }
+  p->cv_space.notify_all();
+  if (r.st != HG_OK) return hg::set_error(r.st, r.err.c_str());
+  const hipError_t e = hipEventSynchronize(r.done);
+  {
+    std::lock_guard<std::mutex> lk(p->mu);
+    p->free_events.push_back(r.done);
+  }
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    hg_blocks_free(r.b);
+    return hg::set_error(HG_EDEVICE, "hg_pipeline_next: device work of the mini-batch failed");
+  }
+  hg::blocks_detach_stream(r.b);
+  *out = r.b;
+  return HG_OK;
+}
+
+void hg_pipeline_destroy(hg_pipeline *p) {
+  if (!p) return;
+  {
+    std::lock_guard<std::mutex> lk(p->mu);
+    p->stopping = true;
+  }
+  p->cv_job.notify_all();
+  for (auto &t : p->workers) t.join();
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(p->device);
+  for (hipStream_t s : p->streams) (void)hipStreamSynchronize(s);
+  for (auto &kv : p->results) {
+    if (kv.second.b) {
+      hg::blocks_detach_stream(kv.second.b);
+      hg_blocks_free(kv.second.b);
+    }
+    if (kv.second.done) (void)hipEventDestroy(kv.second.done);
+  }
+  for (hipEvent_t e : p->free_events) (void)hipEventDestroy(e);
+  for (hipStream_t s : p->streams) (void)hipStreamDestroy(s);
+  (void)hipSetDevice(prev);
+  delete p;
+}
+
+}  // extern "C"

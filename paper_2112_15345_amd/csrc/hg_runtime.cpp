@@ -167,6 +167,7 @@ struct hg_blocks {
   std::vector<int64_t *> eid;
   std::vector<int64_t> in_n;          // [T]
   std::vector<const int64_t *> in_gid;
+  std::vector<void *> feat;           // [T] gathered rows (hg_sample_blocks_gather), or NULL
   std::vector<void *> allocs;
 };
 
@@ -307,6 +308,11 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (e == hipSuccess) std::memset(w->hsmall, 0, sizeof(int64_t) * (small_n + 1));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming);
     if (e == hipSuccess) e = launch_fill_i32(w->map, map_n, -1, stream);
+    if (e == hipSuccess)
+      e = launch_fill_i32(reinterpret_cast<int32_t *>(w->dsmall), 2 * int64_t(small_n), 0, stream);
+    // look-back words of the single-pass compaction: no stale epoch
+    if (e == hipSuccess)
+      e = launch_fill_i32(reinterpret_cast<int32_t *>(w->tile_sums), 4 * n_lb, 0, stream);
     if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
@@ -446,8 +452,9 @@ struct SampleRun {
     ws->epoch += 1;
     if (ws->epoch >= kEpochLimit) {
       ws->epoch = 1;
-      hipError_t e = hipSuccess;
-      if (ws->lb_pairs.p)
+      hipError_t e = launch_fill_i32(reinterpret_cast<int32_t *>(ws->tile_sums),
+                                     4 * std::max<int64_t>(g->n_tiles, 1), 0, stream);
+      if (e == hipSuccess && ws->lb_pairs.p)
         e = launch_fill_u32(static_cast<uint32_t *>(ws->lb_pairs.p),
                             int64_t(ws->lb_pairs.cap / sizeof(uint32_t)), 0u, stream);
       if (e != hipSuccess) return e;
@@ -498,7 +505,11 @@ struct SampleRun {
     if (!ws->poisoned) {
       if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
       if (map_region >= 0)
-        (void)launch_reset_map(view(map_region), ws->d_ts, T, map_bound, stream);
+        (void)launch_reset_map(view(map_region), ws->d_ts, T, map_bound, ws->dsmall,
+                               int32_t(small_slots(g)), stream);
+      else
+        (void)launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall),
+                              2 * int64_t(small_slots(g)), 0, stream);
     }
     if (!ok && b) {
       for (void *p : b->allocs) dev_free(g, p, stream);
@@ -535,6 +546,7 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   b->eid.assign(size_t(H) * R, nullptr);
   b->in_n.assign(T, 0);
   b->in_gid.assign(T, nullptr);
+  b->feat.assign(T, nullptr);
 
   // ---- region 0: the seeds are the first frontier -------------------------
   std::vector<int64_t> nF(T);
@@ -559,11 +571,9 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   }
   int64_t n_items = P + 1;  // pair slots of the next counting pass
 
-  // the readback slots start at zero (tickets, error flags)
-  if ((e = launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall), 2 * int64_t(small_slots(g)), 0,
-                           stream)) != hipSuccess ||
-      (e = upload(0, size_t(H + 1) * lay.size)) != hipSuccess)
-    return fail_device(e, "start");
+  // (the readback slots are zero: a new workspace starts so, and every call
+  // clears them when it ends)
+  if ((e = upload(0, size_t(H + 1) * lay.size)) != hipSuccess) return fail_device(e, "start");
   int64_t total = 0;
   for (int64_t n : nF) total += n;
   map_region = 0;
@@ -658,10 +668,14 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     if (!ec.in_scratch(ws->edges, stream) || !cc.in_scratch(ws->cand, stream))
       return fail(HG_ENOMEM, "hop %d: edge scratch", h);
 
-    // this hop's source lists (also the next hop's frontier)
-    if ((e = launch_store_ptrs(reinterpret_cast<void **>(dreg(h) + lay.src_out),
+    // this hop's source lists (also the next hop's frontier): written by the
+    // sampler launch itself for a few types, else by their own launches
+    int64_t **src_slot = reinterpret_cast<int64_t **>(dreg(h) + lay.src_out);
+    const bool inline_ptrs = T <= kInlineTypes;
+    if (!inline_ptrs &&
+        (e = launch_store_ptrs(reinterpret_cast<void **>(src_slot),
                                reinterpret_cast<void *const *>(src_out.data()), T, stream)) !=
-        hipSuccess)
+            hipSuccess)
       return fail_device(e, "tables");
 
     // ---- 2-4. sample, compact, relabel -------------------------------------
@@ -670,13 +684,17 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     for (int64_t n : nF) copy_total += n;
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
                            sigma, h, key_bits, gid_tmp, eid_all, dstl_all, indptr_all,
-                           stream)) != hipSuccess)
+                           src_slot, src_out.data(), inline_ptrs ? T : 0, stream)) != hipSuccess)
       return fail_device(e, "sample");
     if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
       return fail_device(e, "mark");
-    if ((e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
-                            ws->tile_sums, ws->dsmall, stream)) != hipSuccess)
+    int64_t ticketed = 0;
+    if ((e = next_epoch(&epoch)) != hipSuccess ||
+        (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
+                            ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
+                            stream)) != hipSuccess)
       return fail_device(e, "compact");
+    ticket_base += uint64_t(ticketed);
     bitmap_dirty = false;
     if ((e = launch_relabel(hv, nv, ws->d_es, g->d_tile_base, ws->dsmall, T, R, S, gid_tmp,
                             srcl_all, stream)) != hipSuccess)
@@ -858,11 +876,41 @@ void hg_destroy(hg_graph *g) {
   delete g;
 }
 
-hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
-                              const int64_t *n_seeds, int32_t n_hops,
-                              const int32_t *fanouts, uint64_t rng_seed,
-                              int32_t key_bits, hipStream_t stream,
-                              hg_blocks **out) {
+}  // extern "C"
+
+namespace {
+
+// The input-frontier rows of node types gtypes[0..n_gather) into one new
+// allocation owned by the blocks handle, gathered on `stream`.
+hg_status gather_into_blocks(hg_graph *g, hg_blocks *b, const int32_t *gtypes,
+                             int32_t n_gather, hipEvent_t start, hipEvent_t stop,
+                             hipStream_t stream) {
+  Carve c;
+  std::vector<uint8_t *> dst(g->T, nullptr);
+  for (int32_t k = 0; k < n_gather; ++k) {
+    const int32_t t = gtypes[k];
+    c.add(&dst[t], b->in_n[t] * g->nt[t].row_bytes);
+  }
+  void *base = c.allocate(g, stream);
+  if (!base) return fail(HG_ENOMEM, "hg_sample_blocks_gather: feature arrays");
+  b->allocs.push_back(base);
+  std::vector<GatherJob> jobs;
+  for (int32_t k = 0; k < n_gather; ++k) {
+    const int32_t t = gtypes[k];
+    const NTypeInfo &N = g->nt[t];
+    b->feat[t] = dst[t];
+    jobs.push_back(GatherJob{N.feat, N.num_nodes, N.row_bytes, b->in_gid[t], b->in_n[t], dst[t]});
+  }
+  hipError_t e = launch_gather_multi(jobs.data(), int32_t(jobs.size()), stream, start, stop);
+  if (e != hipSuccess) return fail_hip(e, "gather");
+  return HG_OK;
+}
+
+hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
+                      int32_t n_hops, const int32_t *fanouts, uint64_t rng_seed,
+                      int32_t key_bits, const int32_t *gtypes, int32_t n_gather,
+                      hipEvent_t start, hipEvent_t stop, hipStream_t stream,
+                      hg_blocks **out) {
   if (!out) return fail(HG_EINVAL, "hg_sample_blocks: out is NULL");
   *out = nullptr;
   clear_pending_error();
@@ -880,6 +928,20 @@ hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
     if (n_seeds[t] > g->nt[t].num_nodes)
       return fail(HG_EINVAL, "seeds of type %d: more seeds than vertices", t);
   }
+  if (n_gather < 0 || (n_gather > 0 && !gtypes))
+    return fail(HG_EINVAL, "hg_sample_blocks_gather: bad node type list");
+  {
+    std::vector<char> seen(g->T, 0);
+    for (int32_t k = 0; k < n_gather; ++k) {
+      const int32_t t = gtypes[k];
+      if (t < 0 || t >= g->T)
+        return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d out of range", t);
+      if (g->nt[t].dtype == HG_DT_NONE || g->nt[t].row_bytes <= 0)
+        return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d has no features", t);
+      if (seen[t]) return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d twice", t);
+      seen[t] = 1;
+    }
+  }
   DeviceGuard dg(g->device);
   SampleRun run(g, stream, n_hops, fanouts, rng_seed, key_bits);
   hg_status st = acquire_workspace(g, run.lay.size * size_t(n_hops + 2), stream, &run.ws);
@@ -891,6 +953,9 @@ hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
   }
   try {
     st = run.run(seeds, n_seeds);
+    // the gather goes first: the map reset of finish() can wait behind it
+    if (st == HG_OK && n_gather > 0)
+      st = gather_into_blocks(g, run.b, gtypes, n_gather, start, stop, stream);
   } catch (const std::bad_alloc &) {
     st = fail(HG_ENOMEM, "hg_sample_blocks: out of host memory");
   }
@@ -904,12 +969,53 @@ hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
   return HG_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+hg_status hg_sample_blocks_ex(hg_graph *g, const int64_t *const *seeds,
+                              const int64_t *n_seeds, int32_t n_hops,
+                              const int32_t *fanouts, uint64_t rng_seed,
+                              int32_t key_bits, hipStream_t stream,
+                              hg_blocks **out) {
+  return sample_impl(g, seeds, n_seeds, n_hops, fanouts, rng_seed, key_bits, nullptr, 0,
+                     nullptr, nullptr, stream, out);
+}
+
+hg_status hg_sample_blocks_gather(hg_graph *g, const int64_t *const *seeds,
+                                  const int64_t *n_seeds, int32_t n_hops,
+                                  const int32_t *fanouts, uint64_t rng_seed,
+                                  const int32_t *gather_ntypes, int32_t n_gather,
+                                  hipEvent_t start, hipEvent_t stop, hipStream_t stream,
+                                  hg_blocks **out) {
+  return sample_impl(g, seeds, n_seeds, n_hops, fanouts, rng_seed, 32, gather_ntypes, n_gather,
+                     start, stop, stream, out);
+}
+
+hg_status hg_blocks_features(const hg_blocks *b, int32_t ntype, int64_t *rows,
+                             const void **feat) {
+  if (!b) return fail(HG_EINVAL, "hg_blocks_features: blocks is NULL");
+  if (ntype < 0 || ntype >= b->T)
+    return fail(HG_EINVAL, "hg_blocks_features: node type %d out of range", ntype);
+  const bool have = b->feat[ntype] != nullptr;
+  if (rows) *rows = have ? b->in_n[ntype] : 0;
+  if (feat) *feat = b->feat[ntype];
+  return HG_OK;
+}
+
 hg_status hg_sample_blocks(hg_graph *g, const int64_t *const *seeds,
                            const int64_t *n_seeds, int32_t n_hops,
                            const int32_t *fanouts, uint64_t rng_seed,
                            hipStream_t stream, hg_blocks **out) {
   return hg_sample_blocks_ex(g, seeds, n_seeds, n_hops, fanouts, rng_seed, 32,
                              stream, out);
+}
+
+hg_status hg_graph_types(const hg_graph *g, int32_t *n_ntypes, int32_t *n_etypes) {
+  if (!g) return fail(HG_EINVAL, "hg_graph_types: graph is NULL");
+  if (n_ntypes) *n_ntypes = g->T;
+  if (n_etypes) *n_etypes = g->R;
+  return HG_OK;
 }
 
 int32_t hg_blocks_num_hops(const hg_blocks *b) { return b ? b->H : -1; }
@@ -1012,6 +1118,23 @@ hg_status hg_gather_features_multi_timed(hg_graph *g, const hg_blocks *b,
   if (e != hipSuccess) return fail_hip(e, "gather");
   return HG_OK;
 }
+
+}  // extern "C"
+
+namespace hg {
+
+hg_status set_error(hg_status st, const char *msg) {
+  g_last_error = msg;
+  return st;
+}
+
+void blocks_detach_stream(hg_blocks *b) { b->stream = nullptr; }
+
+int graph_device(const hg_graph *g) { return g->device; }
+
+}  // namespace hg
+
+extern "C" {
 
 void hg_blocks_free(hg_blocks *b) {
   if (!b) return;

@@ -68,7 +68,10 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
 }
 
 __global__ void k_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
-                            int64_t total) {
+                            int64_t total, int64_t *small, int32_t n_small) {
+  // the call is over: its readback slots start the next call at zero
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < n_small; i += blockDim.x) small[i] = 0;
   for (int64_t x = grid_stride_start(); x < total; x += grid_stride_step()) {
     int64_t first;
     const int t = type_of(hv.nF, n_types, x, &first);
@@ -401,6 +404,11 @@ struct SampleArgs {
   int64_t *src_gid, *eid;
   int32_t *dst_local;
   int64_t *indptr_all;
+  // block 0 stores the hop's source-list pointers into the hop's table (read
+  // only by later launches)
+  int64_t **src_out_slot;
+  int64_t *src_out_new[kInlineTypes];
+  int32_t n_src_out;
 };
 
 // Role A: a wavefront per 64 consecutive pairs.  Each lane writes its pair's
@@ -727,6 +735,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   __shared__ uint32_t s_j[kSampleWaves][kCandCap];
   const int64_t b = blockIdx.x;
   const int wave = threadIdx.x / kWave;
+  if (b == 0 && int(threadIdx.x) < A.n_src_out)
+    A.src_out_slot[threadIdx.x] = A.src_out_new[threadIdx.x];
   if (b < A.blocks_a) {
     // the candidate lists are not used by this role: reuse their LDS
     GroupLds *g = reinterpret_cast<GroupLds *>(&s_key[wave][0]);
@@ -897,10 +907,10 @@ hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
 }
 
 hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
-                            int64_t total, hipStream_t stream) {
-  if (total <= 0) return hipSuccess;
+                            int64_t total, int64_t *small, int32_t n_small,
+                            hipStream_t stream) {
   hipLaunchKernelGGL(k_reset_map, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, hv, ts, n_types, total);
+                     stream, hv, ts, n_types, total, small, n_small);
   return hipGetLastError();
 }
 
@@ -946,8 +956,13 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          uint64_t *cand, const int64_t *small, uint64_t sigma,
                          int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
+                         int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          hipStream_t stream) {
+  if (n_src_out > kInlineTypes) return hipErrorInvalidValue;
   SampleArgs A;
+  A.src_out_slot = src_out_slot;
+  A.n_src_out = n_src_out;
+  for (int32_t t = 0; t < kInlineTypes; ++t) A.src_out_new[t] = t < n_src_out ? src_out[t] : nullptr;
   A.hv = hv;
   A.es = es;
   A.n_etypes = n_etypes;

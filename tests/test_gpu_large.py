@@ -37,8 +37,8 @@ def test_large_workload_parity(idx, batch):
     fan = wl.fanout_matrix()
     seeds = W.seeds_per_type(wl, batch)
     t0 = time.time()
-    blocks = g.sample_blocks(gpu_seeds(seeds), fan, batch)
-    outs = g.gather_features_all(blocks)
+    blocks = g.sample_blocks(gpu_seeds(seeds), fan, batch, gather="all")
+    outs = {t: blocks.features(t) for t, f in enumerate(gen.feats) if f is not None}
     got = result_dict(g, blocks)
     say(f"workload {idx}: GPU mini-batch and copy-out in {time.time() - t0:.1f}s")
 

@@ -78,6 +78,18 @@ def test_random_heterographs(olib, chunk):
                 continue
             x = g.gather_features(b, t).cpu().numpy()
             assert x.tobytes() == f[got["input"][t]].tobytes()
+        # the fused call: same blocks, and the features it gathered itself
+        if bits == 32:
+            bf = g.sample_blocks(gpu_seeds(seeds), fanouts, sigma, gather=featured)
+            diffs = compare(ref, result_dict(g, bf), len(nn), len(ets), len(fanouts))
+            assert not diffs, f"case {c} (fused): " + "\n".join(diffs[:10])
+            for t, f in enumerate(feats):
+                x = bf.features(t)
+                if f is None:
+                    assert x is None
+                    continue
+                assert x.shape == (got["input"][t].size, f.shape[1])
+                assert x.cpu().numpy().tobytes() == f[got["input"][t]].tobytes()
 
 
 def hub_graph(deg, n_src=None, extra=(3, 0, 7)):
@@ -150,10 +162,16 @@ def test_error_codes_match_oracle(olib):
         with pytest.raises(hg.HGError) as eg:
             g.sample_blocks(gpu_seeds([np.array(seeds[0])]), fo, 0, key_bits=kb)
         assert eo.value.status == eg.value.status == hg.HG_EINVAL
-    # a featureless type cannot be gathered
+    # a featureless type cannot be gathered, by either call
     b = g.sample_blocks(gpu_seeds([np.array([0])]), [[1]], 0)
     with pytest.raises(hg.HGError):
         g.gather_features(b, 0)
+    for gl in ([0], [1], [-1]):
+        with pytest.raises(hg.HGError) as e:
+            g.sample_blocks(gpu_seeds([np.array([0])]), [[1]], 0, gather=gl)
+        assert e.value.status == hg.HG_EINVAL
+    with pytest.raises(ValueError):
+        g.sample_blocks(gpu_seeds([np.array([0])]), [[1]], 0, key_bits=8, gather=[])
     # invalid CSC arrays are refused at creation
     for ip, ix in [(np.array([0, 1, 3, 2]), indices), (indptr, np.array([2, 0, 3])),
                    (np.array([1, 1, 3, 3]), indices)]:

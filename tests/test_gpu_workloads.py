@@ -45,7 +45,8 @@ def test_workload_parity(idx, batches):
     for b in batches:
         seeds = W.seeds_per_type(wl, b)
         say(f"workload {idx} batch {b}: GPU")
-        blocks = g.sample_blocks(gpu_seeds(seeds), fan, b)
+        # the call bench.py times: blocks and input features together
+        blocks = g.sample_blocks(gpu_seeds(seeds), fan, b, gather="all")
         got = result_dict(g, blocks)
         say(f"workload {idx} batch {b}: oracle")
         ref = host.sample_blocks(seeds, fan, b)
@@ -54,12 +55,13 @@ def test_workload_parity(idx, batches):
         allx = g.gather_features_all(blocks)
         for t, f in enumerate(gen.feats):
             if f is None:
+                assert blocks.features(t) is None
                 continue
-            x = allx[t]
             ids = ref["input"][t]
-            want = host.gather(t, ids)
-            assert x.contiguous().view(torch.uint8).cpu().numpy().tobytes() == want.tobytes(), \
-                f"batch {b} type {t}: gathered bytes differ"
+            want = host.gather(t, ids).tobytes()
+            for x in (blocks.features(t), allx[t]):
+                assert x.contiguous().view(torch.uint8).cpu().numpy().tobytes() == want, \
+                    f"batch {b} type {t}: gathered bytes differ"
         say(f"workload {idx} batch {b}: equal "
             f"({sum(v[3].size for v in ref['edges'].values())} edges)")
 
