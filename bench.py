@@ -87,13 +87,15 @@ def cpu_baseline(gen, wl, first_batch, budget_s=12.0, max_batches=8):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", type=int, default=2,
                     help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
                          "5 gather-heavy academic")
     ap.add_argument("--workers", type=int, default=4,
                     help="pipeline worker threads (own streams); 0 = one direct call per step")
+    ap.add_argument("--bundle", type=int, default=1,
+                    help="mini-batches per launch sequence (hg_sample_blocks_bundle)")
     ap.add_argument("--depth", type=int, default=0,
                     help="mini-batches outstanding in the pipeline (default 2 x workers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -141,63 +143,88 @@ def main():
     events = {args.warmup + i: (hip_events.events[2 * i], hip_events.events[2 * i + 1])
               for i in range(args.steps)}
     gather_rec = []
+    B = max(1, args.bundle)
+    # units of work: bundles of B consecutive mini-batches (warm-up and timed
+    # mini-batches never share a bundle); a unit's events time its gather
+    units = [list(range(b, min(b + B, args.warmup))) for b in range(0, args.warmup, B)]
+    timed_units = [list(range(b, min(b + B, n_batches)))
+                   for b in range(args.warmup, n_batches, B)]
 
-    def consumed(b, blocks):
-        """Bookkeeping of a returned mini-batch: (sampled edges, gathered rows, bytes)."""
-        e = sum(blocks.num_edges(h, r) for h in range(len(fan)) for r in range(g.R))
-        rows_t = {t: blocks.num_input_nodes(t) for t in feat_types}
-        if b in events:
-            gather_rec.append((events[b][0], events[b][1], rows_t))
-        return e, sum(rows_t.values()), sum(n * row_bytes[t] for t, n in rows_t.items())
+    def account(unit, blist, totals=None):
+        """Bookkeeping of a returned unit; gather bytes and events of timed ones."""
+        rows_all = {t: 0 for t in feat_types}
+        for blocks in blist:
+            e = sum(blocks.num_edges(h, r) for h in range(len(fan)) for r in range(g.R))
+            if totals is not None:
+                totals[0] += e
+            for t in feat_types:
+                n = blocks.num_input_nodes(t)
+                rows_all[t] += n
+                if totals is not None:
+                    totals[1] += n
+                    totals[2] += n * row_bytes[t]
+        if unit[0] in events:
+            gather_rec.append((events[unit[0]][0], events[unit[0]][1], rows_all))
 
+    def unit_events(unit):
+        return events.get(unit[0])
+
+    totals = [0, 0, 0]
     if args.workers == 0:
-        # one call per mini-batch on the current stream
-        def run(b):
-            return g.sample_blocks(seeds[b], fan, b, gather=feat_types, events=events.get(b))
+        # direct calls on the current stream, one per unit
+        def run(unit):
+            if len(unit) == 1:
+                b = unit[0]
+                return [g.sample_blocks(seeds[b], fan, b, gather=feat_types,
+                                        events=unit_events(unit))]
+            return g.sample_bundle([seeds[b] for b in unit], fan, unit, gather=feat_types,
+                                   events=unit_events(unit))
 
-        for b in range(args.warmup):
-            consumed(b, run(b))
+        for u in units:
+            account(u, run(u))
         torch.cuda.synchronize()
-        log("warm-up done")
-        totals = [0, 0, 0]
+        log(f"warm-up done (direct calls, bundles of {B})")
         t_start = time.perf_counter()
-        for b in range(args.warmup, n_batches):
-            blocks = run(b)
-            for k, v in enumerate(consumed(b, blocks)):
-                totals[k] += v
-            del blocks
+        for u in timed_units:
+            blist = run(u)
+            account(u, blist, totals)
+            del blist
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t_start
     else:
-        # the pipeline: mini-batches generated ahead by worker threads, each on
-        # its own stream, returned in order; at most `depth` outstanding
-        depth = args.depth or 2 * args.workers
+        # the pipeline: units generated ahead by worker threads, each on its
+        # own stream, returned in order; at most `depth` mini-batches outstanding
+        depth = max(args.depth or 2 * args.workers * B, B)
         pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=feat_types)
-        nxt = 0
+        queue = units + timed_units
+        state = {"next": 0, "outstanding": 0}
 
         def submit_more():
-            nonlocal nxt
-            while nxt < n_batches and nxt - done[0] < depth:
-                pipe.submit(seeds[nxt], fan, nxt, events=events.get(nxt))
-                nxt += 1
+            while (state["next"] < len(queue) and
+                   state["outstanding"] + len(queue[state["next"]]) <= depth):
+                u = queue[state["next"]]
+                pipe.submit_bundle([seeds[b] for b in u], fan, u, events=unit_events(u))
+                state["outstanding"] += len(u)
+                state["next"] += 1
 
-        done = [0]
+        def take(unit):
+            blist = []
+            for _ in unit:
+                blist.append(pipe.next())
+                state["outstanding"] -= 1
+            submit_more()
+            return blist
+
         submit_more()
-        for b in range(args.warmup):
-            consumed(b, pipe.next())
-            done[0] += 1
-            submit_more()
+        for u in units:
+            account(u, take(u))
         torch.cuda.synchronize()
-        log(f"warm-up done ({args.workers} workers, depth {depth})")
-        totals = [0, 0, 0]
+        log(f"warm-up done ({args.workers} workers, bundles of {B}, depth {depth})")
         t_start = time.perf_counter()
-        for b in range(args.warmup, n_batches):
-            blocks = pipe.next()
-            done[0] += 1
-            submit_more()
-            for k, v in enumerate(consumed(b, blocks)):
-                totals[k] += v
-            del blocks
+        for u in timed_units:
+            blist = take(u)
+            account(u, blist, totals)
+            del blist
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t_start
         pipe.close()
@@ -244,9 +271,9 @@ def main():
                    "node_types": len(gen.num_nodes), "edge_types": g.R,
                    "edges_in_graph": int(sum(ix.numel() for _, _, _, ix in gen.etypes)),
                    "parallelism": "single GPU",
-                   "pipeline": (f"{args.workers} worker streams, depth "
-                                f"{args.depth or 2 * args.workers}" if args.workers
-                                else "one call per step")},
+                   "bundle": max(1, args.bundle),
+                   "pipeline": (f"{args.workers} worker streams" if args.workers
+                                else "direct calls")},
         "gathered_GBps": gbytes / elapsed / 1e9,
         "sampled_edges_per_step": edges / args.steps,
         "gathered_rows_per_step": rows / args.steps,

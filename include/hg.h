@@ -210,6 +210,25 @@ hg_status hg_sample_blocks_gather(hg_graph *graph, const int64_t *const *seeds,
                                   hipEvent_t start, hipEvent_t stop, hipStream_t stream,
                                   hg_blocks **out);
 
+/* n_batches (1..16) mini-batches in one launch sequence (Sec. 4.2.2: the
+ * sampling of several mini-batches is bundled so that it runs in parallel).
+ * Batch b has seeds seeds[b * n_ntypes + t] with counts n_seeds[b * n_ntypes
+ * + t] (host arrays) and sampling seed rng_seeds[b]; all share n_hops and
+ * fanouts.  out: host array of n_batches handles, one per batch, each the
+ * same mini-batch (blocks and gathered features) as
+ * hg_sample_blocks_gather with that batch's arguments would give, each freed
+ * by hg_blocks_free (the arrays of a bundle are released with its last
+ * handle).  The batches are sampled together: each has its own frontier map
+ * and compaction, every pass covers all of them, and the stream waits once
+ * per hop for the whole bundle.  Working memory grows with n_batches.
+ * All-or-nothing: an invalid batch fails the call. */
+hg_status hg_sample_blocks_bundle(hg_graph *graph, int32_t n_batches,
+                                  const int64_t *const *seeds, const int64_t *n_seeds,
+                                  int32_t n_hops, const int32_t *fanouts,
+                                  const uint64_t *rng_seeds, const int32_t *gather_ntypes,
+                                  int32_t n_gather, hipEvent_t start, hipEvent_t stop,
+                                  hipStream_t stream, hg_blocks **out);
+
 /* The rows gathered for node type `ntype` by hg_sample_blocks_gather:
  * *rows = n_input(ntype) and *feat = device [rows, dim] of the type's dtype,
  * owned by the handle; *rows = 0 and *feat = NULL when the type was not
@@ -223,15 +242,18 @@ hg_status hg_gather_rows(hg_graph *graph, int32_t ntype, const int64_t *ids,
                          int64_t n, void *out, hipStream_t stream);
 
 /* Releases a blocks handle (stream-ordered on the stream it was made on;
- * on the null stream for handles returned by hg_pipeline_next). */
+ * on the null stream for handles returned by hg_pipeline_next).  A handle
+ * does not depend on its graph handle: it may be released after
+ * hg_destroy (with a caller allocator, that allocator must still work). */
 void hg_blocks_free(hg_blocks *blocks);
 
 /* A mini-batch pipeline (Sec. 4.2.1: mini-batches are generated ahead of
  * their use by concurrent stages with bounded queues between them).
  * n_workers (1..16) host threads, each with its own HIP stream (created here,
  * default priority) and its own workspace of the graph, run submitted
- * mini-batches concurrently with hg_sample_blocks_gather, so that the stream
- * waits of one overlap the kernels of another.  Mini-batches come back in
+ * mini-batches (single, or bundled as by hg_sample_blocks_bundle)
+ * concurrently, so that the stream waits of one overlap the kernels of
+ * another.  Mini-batches come back in
  * submission order; at most `capacity` (>= 1) are submitted and not yet
  * returned.  gather_ntypes (host int32 [n_gather], copied): the node types
  * whose input features every mini-batch gathers (may be empty).  The graph
@@ -240,17 +262,19 @@ hg_status hg_pipeline_create(hg_graph *graph, int32_t n_workers, int32_t capacit
                              const int32_t *gather_ntypes, int32_t n_gather,
                              hg_pipeline **out);
 
-/* Queues one mini-batch: seeds, n_seeds, n_hops, fanouts and rng_seed as in
- * hg_sample_blocks (n_seeds and fanouts are copied; the seed arrays are read
- * on a worker's stream and must stay valid until the mini-batch has been
+/* Queues n_batches (1..capacity) mini-batches, sampled together as one
+ * bundle when n_batches > 1: arguments as in hg_sample_blocks_bundle
+ * (n_seeds, fanouts and rng_seeds are copied; the seed arrays are read on a
+ * worker's stream and must stay valid until the mini-batches have been
  * returned by hg_pipeline_next).  start / stop: optional events carried by
- * its gather launches.  Waits while `capacity` mini-batches are outstanding.
- * Argument errors found later (bad seeds, ...) are returned by
- * hg_pipeline_next for that mini-batch. */
-hg_status hg_pipeline_submit(hg_pipeline *pipe, const int64_t *const *seeds,
-                             const int64_t *n_seeds, int32_t n_hops,
-                             const int32_t *fanouts, uint64_t rng_seed, hipEvent_t start,
-                             hipEvent_t stop);
+ * the bundle's gather launches.  Each mini-batch is returned separately, in
+ * submission order.  Waits while the outstanding mini-batches would exceed
+ * `capacity`.  Argument errors found later (bad seeds, ...) fail the whole
+ * bundle and are returned by hg_pipeline_next for each of its mini-batches. */
+hg_status hg_pipeline_submit(hg_pipeline *pipe, int32_t n_batches,
+                             const int64_t *const *seeds, const int64_t *n_seeds,
+                             int32_t n_hops, const int32_t *fanouts,
+                             const uint64_t *rng_seeds, hipEvent_t start, hipEvent_t stop);
 
 /* Waits for the oldest outstanding mini-batch.  On success *out owns its
  * blocks and gathered features (hg_blocks_free) and all of its device work

@@ -35,7 +35,8 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_blocks_num_hops", "hg_blocks_nodes", "hg_blocks_edges",
                "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_features_multi",
                "hg_gather_features_multi_timed", "hg_gather_rows",
-               "hg_sample_blocks_gather", "hg_blocks_features", "hg_graph_types",
+               "hg_sample_blocks_gather", "hg_sample_blocks_bundle", "hg_blocks_features",
+               "hg_graph_types",
                "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
                "hg_pipeline_destroy",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
@@ -90,9 +91,11 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_sample_blocks_gather": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _P, _P,
                                      _PP], _I32),
         "hg_blocks_features": ([_P, _I32, _PI64, _PP], _I32),
+        "hg_sample_blocks_bundle": ([_P, _I32, _P, _P, _I32, _P, _P, _P, _I32, _P, _P, _P, _P],
+                                    _I32),
         "hg_graph_types": ([_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)], _I32),
         "hg_pipeline_create": ([_P, _I32, _I32, _P, _I32, _PP], _I32),
-        "hg_pipeline_submit": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _P], _I32),
+        "hg_pipeline_submit": ([_P, _I32, _P, _P, _I32, _P, _P, _P, _P], _I32),
         "hg_pipeline_next": ([_P, _PP], _I32),
         "hg_pipeline_destroy": ([_P], None),
         "hg_blocks_free": ([_P], None),
@@ -328,6 +331,47 @@ class Graph:
                                            start, stop, _stream(stream), ctypes.byref(h)))
         return Blocks(self, h, H)
 
+    def sample_bundle(self, seeds_list, fanouts, rng_seeds, gather="all", events=None,
+                      stream=None):
+        """Several mini-batches in one launch sequence (hg_sample_blocks_bundle):
+        seeds_list[b] per node type as in sample_blocks, rng_seeds[b]; returns
+        one Blocks per batch (with gathered features for `gather`)."""
+        lib = load_library()
+        T, R = self.T, self.R
+        B = len(seeds_list)
+        if len(rng_seeds) != B:
+            raise ValueError("one rng seed per batch")
+        keep = []
+        ptrs = (ctypes.c_void_p * max(B * T, 1))()
+        counts = (ctypes.c_int64 * max(B * T, 1))()
+        for b, seeds in enumerate(seeds_list):
+            if len(seeds) != T:
+                raise ValueError("one seed entry per node type")
+            for t, sd in enumerate(seeds):
+                if sd is None:
+                    continue
+                sd = _dev_i64(sd, self.device)
+                keep.append(sd)
+                counts[b * T + t] = sd.numel()
+                ptrs[b * T + t] = sd.data_ptr() if sd.numel() else None
+        H = len(fanouts)
+        flat = [int(k) for row in fanouts for k in row]
+        if len(flat) != H * R:
+            raise ValueError("fanouts must be [n_hops][n_etypes]")
+        fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        sg = (ctypes.c_uint64 * max(B, 1))(*[int(x) & (2**64 - 1) for x in rng_seeds])
+        if isinstance(gather, str):
+            if gather != "all":
+                raise ValueError('gather must be "all" or a list of node types')
+            gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
+        gather = list(gather or [])
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
+        start, stop = events if events is not None else (None, None)
+        hs = (ctypes.c_void_p * max(B, 1))()
+        _check(lib.hg_sample_blocks_bundle(self._h, B, ptrs, counts, H, fo, sg, gt, len(gather),
+                                           start, stop, _stream(stream), hs))
+        return [Blocks(self, ctypes.c_void_p(hs[b]), H) for b in range(B)]
+
     def gather_features(self, blocks: Blocks, ntype: int, out: torch.Tensor | None = None,
                         stream=None) -> torch.Tensor:
         n, feat = self.ntypes[ntype]
@@ -410,33 +454,41 @@ class Pipeline:
         self._held = collections.deque()  # seed tensors of outstanding mini-batches
 
     def submit(self, seeds, fanouts, rng_seed: int = 0, events=None):
+        """Queues one mini-batch (seeds per node type, as in Graph.sample_blocks)."""
+        self.submit_bundle([seeds], fanouts, [rng_seed], events)
+
+    def submit_bundle(self, seeds_list, fanouts, rng_seeds, events=None):
+        """Queues len(seeds_list) mini-batches sampled together as one bundle
+        (Graph.sample_bundle); next() returns them one by one, in order."""
         g = self.graph
         T, R = g.T, g.R
-        if len(seeds) != T:
-            raise ValueError("one seed entry per node type")
+        B = len(seeds_list)
+        if len(rng_seeds) != B:
+            raise ValueError("one rng seed per mini-batch")
         keep = []
-        ptrs = (ctypes.c_void_p * T)()
-        counts = (ctypes.c_int64 * T)()
-        for t, s in enumerate(seeds):
-            if s is None:
-                continue
-            s = _dev_i64(s, g.device)
-            keep.append(s)
-            counts[t] = s.numel()
-            ptrs[t] = s.data_ptr() if s.numel() else None
+        ptrs = (ctypes.c_void_p * max(B * T, 1))()
+        counts = (ctypes.c_int64 * max(B * T, 1))()
+        for b, seeds in enumerate(seeds_list):
+            if len(seeds) != T:
+                raise ValueError("one seed entry per node type")
+            for t, sd in enumerate(seeds):
+                if sd is None:
+                    continue
+                sd = _dev_i64(sd, g.device)
+                keep.append(sd)
+                counts[b * T + t] = sd.numel()
+                ptrs[b * T + t] = sd.data_ptr() if sd.numel() else None
         H = len(fanouts)
         flat = [int(k) for row in fanouts for k in row]
         if len(flat) != H * R:
             raise ValueError("fanouts must be [n_hops][n_etypes]")
         fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        sg = (ctypes.c_uint64 * max(B, 1))(*[int(x) & (2**64 - 1) for x in rng_seeds])
         start, stop = events if events is not None else (None, None)
-        self._held.append(keep)
-        try:
-            _check(load_library().hg_pipeline_submit(self._h, ptrs, counts, H, fo,
-                                                     int(rng_seed) & (2**64 - 1), start, stop))
-        except Exception:
-            self._held.pop()
-            raise
+        _check(load_library().hg_pipeline_submit(self._h, B, ptrs, counts, H, fo, sg, start,
+                                                 stop))
+        for _ in range(B):
+            self._held.append(keep)
 
     def next(self) -> Blocks:
         if not self._held:

@@ -97,7 +97,7 @@ hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
 
 // Several gathers in one launch: segment s owns blocks
 // [block_base[s], block_base[s+1]) and moves its rows as k_gather does.
-constexpr int kMaxSegs = 8;
+constexpr int kMaxSegs = 32;
 
 struct GatherSeg {
   const void *table;

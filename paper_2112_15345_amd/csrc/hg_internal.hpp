@@ -147,11 +147,12 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
 // ID, destination local ID.
 // The sampler launches.  With n_src_out <= kInlineTypes the first one also
 // stores src_out[0..n_src_out) into src_out_slot (the hop's table entries).
+// Edge type e is keyed as type e % key_R with seed sigmas[e / key_R] (device).
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t n_types, int64_t n_pairs, int64_t n_wave,
                          int64_t n_chunks, int64_t n_hubs, PairArrays pa,
-                         uint64_t *cand, const int64_t *small, uint64_t sigma,
-                         int32_t hop, int32_t key_bits, int64_t *src_gid,
+                         uint64_t *cand, const int64_t *small, const uint64_t *sigmas,
+                         int32_t key_R, int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          hipStream_t stream);

@@ -3,8 +3,8 @@
 // concurrent stages with bounded queues between them).
 //
 // Worker threads, each with its own HIP stream (and so its own workspace of the
-// graph handle), take submitted mini-batches in order and run them with
-// hg_sample_blocks_gather.  While one worker waits on its stream (the per-hop
+// graph handle), take submitted mini-batches (single or bundled) in order and
+// run them with hg_sample_blocks_bundle.  While one worker waits on its stream (the per-hop
 // size readbacks), the others keep the GPU busy, so the waits and the host's
 // launch work of one mini-batch overlap the kernels of the next.  Results are
 // handed back in submission order.
@@ -21,13 +21,15 @@
 #include "hg_internal.hpp"
 
 struct hg_pipeline {
+  // n mini-batches (a bundle when n > 1) with sequence numbers seq .. seq+n-1
   struct Job {
     uint64_t seq;
-    std::vector<const int64_t *> seeds;
-    std::vector<int64_t> n_seeds;
+    int32_t n;
+    std::vector<const int64_t *> seeds;  // [n * T]
+    std::vector<int64_t> n_seeds;        // [n * T]
     int32_t n_hops;
     std::vector<int32_t> fanouts;
-    uint64_t sigma;
+    std::vector<uint64_t> sigmas;        // [n]
     hipEvent_t start, stop;
   };
   struct Result {
@@ -68,14 +70,20 @@ void hg_pipeline::work(int k) {
       j = std::move(jobs.front());
       jobs.pop_front();
     }
-    Result r;
-    r.st = hg_sample_blocks_gather(g, j.seeds.data(), j.n_seeds.data(), j.n_hops,
-                                   j.fanouts.empty() ? nullptr : j.fanouts.data(), j.sigma,
-                                   gather.empty() ? nullptr : gather.data(),
-                                   int32_t(gather.size()), j.start, j.stop, s, &r.b);
-    if (r.st != HG_OK) {
-      r.err = hg_last_error();
-    } else {
+    std::vector<hg_blocks *> out(size_t(j.n), nullptr);
+    hg_status st = hg_sample_blocks_bundle(
+        g, j.n, j.seeds.data(), j.n_seeds.data(), j.n_hops,
+        j.fanouts.empty() ? nullptr : j.fanouts.data(), j.sigmas.data(),
+        gather.empty() ? nullptr : gather.data(), int32_t(gather.size()), j.start, j.stop, s,
+        out.data());
+    std::string err = st != HG_OK ? std::string(hg_last_error()) : std::string();
+    std::vector<Result> rs(size_t(j.n));
+    for (int32_t i = 0; i < j.n; ++i) {
+      Result &r = rs[size_t(i)];
+      r.st = st;
+      r.err = err;
+      r.b = out[size_t(i)];
+      if (st != HG_OK) continue;
       {
         std::lock_guard<std::mutex> lk(mu);
         if (!free_events.empty()) {
@@ -93,7 +101,7 @@ void hg_pipeline::work(int k) {
     }
     {
       std::lock_guard<std::mutex> lk(mu);
-      results.emplace(j.seq, std::move(r));
+      for (int32_t i = 0; i < j.n; ++i) results.emplace(j.seq + uint64_t(i), std::move(rs[size_t(i)]));
     }
     cv_result.notify_all();
   }
@@ -150,34 +158,42 @@ hg_status hg_pipeline_create(hg_graph *g, int32_t n_workers, int32_t capacity,
   return HG_OK;
 }
 
-hg_status hg_pipeline_submit(hg_pipeline *p, const int64_t *const *seeds,
+hg_status hg_pipeline_submit(hg_pipeline *p, int32_t n_batches, const int64_t *const *seeds,
                              const int64_t *n_seeds, int32_t n_hops,
-                             const int32_t *fanouts, uint64_t rng_seed, hipEvent_t start,
-                             hipEvent_t stop) {
+                             const int32_t *fanouts, const uint64_t *rng_seeds,
+                             hipEvent_t start, hipEvent_t stop) {
   if (!p) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: pipeline is NULL");
-  if (!n_seeds) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: n_seeds is NULL");
+  if (n_batches < 1 || n_batches > p->capacity)
+    return hg::set_error(HG_EINVAL, "hg_pipeline_submit: n_batches not in 1..capacity");
+  if (!n_seeds || !rng_seeds)
+    return hg::set_error(HG_EINVAL, "hg_pipeline_submit: NULL n_seeds or rng_seeds");
   if (n_hops < 0) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: n_hops < 0");
   int32_t T = 0, R = 0;
   if (hg_graph_types(p->g, &T, &R) != HG_OK) return HG_EINVAL;
   if (n_hops > 0 && R > 0 && !fanouts)
     return hg::set_error(HG_EINVAL, "hg_pipeline_submit: fanouts is NULL");
+  const size_t nt = size_t(n_batches) * size_t(T);
   hg_pipeline::Job j;
   try {
-    j.seeds.assign(size_t(T), nullptr);
-    if (seeds) j.seeds.assign(seeds, seeds + T);
-    j.n_seeds.assign(n_seeds, n_seeds + T);
+    j.seeds.assign(nt, nullptr);
+    if (seeds) j.seeds.assign(seeds, seeds + nt);
+    j.n_seeds.assign(n_seeds, n_seeds + nt);
     if (fanouts) j.fanouts.assign(fanouts, fanouts + size_t(n_hops) * size_t(R));
+    j.sigmas.assign(rng_seeds, rng_seeds + n_batches);
   } catch (const std::bad_alloc &) {
     return hg::set_error(HG_ENOMEM, "hg_pipeline_submit: out of host memory");
   }
+  j.n = n_batches;
   j.n_hops = n_hops;
-  j.sigma = rng_seed;
   j.start = start;
   j.stop = stop;
   {
     std::unique_lock<std::mutex> lk(p->mu);
-    p->cv_space.wait(lk, [&] { return p->submitted - p->returned < uint64_t(p->capacity); });
-    j.seq = p->submitted++;
+    p->cv_space.wait(lk, [&] {
+      return p->submitted + uint64_t(n_batches) - p->returned <= uint64_t(p->capacity);
+    });
+    j.seq = p->submitted;
+    p->submitted += uint64_t(n_batches);
     p->jobs.push_back(std::move(j));
   }
   p->cv_job.notify_one();

@@ -20,6 +20,8 @@
 #include <cstdio>
 #include <cstring>
 #include <atomic>
+#include <map>
+#include <memory>
 #include <mutex>
 #include <thread>
 #include <new>
@@ -151,8 +153,34 @@ struct hg_graph {
   int64_t n_tiles = 0;
   int64_t *d_tile_base = nullptr;  // device copy of tile_base
   int64_t total_nnz = 0;
+  // A bundle of B mini-batches samples a virtual graph made of B copies of
+  // this one (copy b of type x is type b * T + x, over the same arrays): its
+  // key_R is this graph's R, so that every copy keys its edges as the real
+  // edge type.  Made on first use, kept until hg_destroy.
+  int32_t key_R = 0;
+  std::map<int32_t, hg_graph *> bundles;
   std::mutex mu;
   std::vector<Workspace *> ws;
+};
+
+namespace {
+void dev_free(hg_graph *g, void *p, hipStream_t s);
+void layout_types(hg_graph *g);
+void free_graph(hg_graph *g);
+// Mini-batches per bundle at most.
+constexpr int32_t kMaxBundle = 16;
+}  // namespace
+
+// Output arrays of one sampling call; shared by the handles of a bundle and
+// released with the last of them.  Holds its device and allocator by value:
+// a blocks handle may outlive its graph.
+struct OutAllocs {
+  int device = 0;
+  bool has_alloc = false;
+  hg_allocator alloc{};
+  hipStream_t stream = nullptr;
+  std::vector<void *> ptrs;
+  ~OutAllocs();
 };
 
 struct hg_blocks {
@@ -168,7 +196,7 @@ struct hg_blocks {
   std::vector<int64_t> in_n;          // [T]
   std::vector<const int64_t *> in_gid;
   std::vector<void *> feat;           // [T] gathered rows (hg_sample_blocks_gather), or NULL
-  std::vector<void *> allocs;
+  std::shared_ptr<OutAllocs> mem;     // the arrays above
 };
 
 // ---------------------------------------------------------------------------
@@ -196,6 +224,22 @@ void dev_free(hg_graph *g, void *p, hipStream_t s) {
   else
     (void)hipFreeAsync(p, s);
 }
+
+}  // namespace
+
+OutAllocs::~OutAllocs() {
+  DeviceGuard dg(device);
+  for (void *p : ptrs) {
+    if (!p) continue;
+    if (has_alloc)
+      alloc.free(alloc.ctx, p, stream);
+    else
+      (void)hipFreeAsync(p, stream);
+  }
+  (void)hipGetLastError();
+}
+
+namespace {
 
 // Several arrays carved out of one buffer.
 struct Carve {
@@ -406,10 +450,11 @@ struct SampleRun {
   Workspace *ws = nullptr;
   hg_blocks *b = nullptr;
   int32_t T, R, H;
-  uint64_t sigma;
+  std::vector<uint64_t> sigmas;  // per copy of a bundle (one for a plain call)
   int32_t key_bits;
   const int32_t *fanouts;
   RegionLayout lay;
+  size_t sig_bytes;              // the sigma table heads the call's tables
   uint64_t ticket_base = 0;
 
   // the map holds the frontier of region `map_region` (at most map_bound
@@ -420,12 +465,17 @@ struct SampleRun {
   bool bitmap_dirty = false;
 
   SampleRun(hg_graph *g_, hipStream_t s, int32_t H_, const int32_t *fo,
-            uint64_t sig, int32_t kb)
-      : g(g_), stream(s), T(g_->T), R(g_->R), H(H_), sigma(sig), key_bits(kb),
-        fanouts(fo), lay(g_->T, g_->R) {}
+            const uint64_t *sig, int32_t n_sig, int32_t kb)
+      : g(g_), stream(s), T(g_->T), R(g_->R), H(H_), sigmas(sig, sig + n_sig), key_bits(kb),
+        fanouts(fo), lay(g_->T, g_->R), sig_bytes(align_up(sizeof(uint64_t) * size_t(n_sig))) {}
 
-  char *hreg(int r) { return ws->htab + size_t(r) * lay.size; }
-  char *dreg(int r) { return static_cast<char *>(ws->tab.p) + size_t(r) * lay.size; }
+  // table bytes of a call: the sigma table, then regions 0 .. H+1
+  size_t table_bytes() const { return sig_bytes + lay.size * size_t(H + 2); }
+  char *hreg(int r) { return ws->htab + sig_bytes + size_t(r) * lay.size; }
+  char *dreg(int r) {
+    return static_cast<char *>(ws->tab.p) + sig_bytes + size_t(r) * lay.size;
+  }
+  const uint64_t *dsigmas() { return static_cast<const uint64_t *>(ws->tab.p); }
 
   // Region r's frontier is region r-1's source lists (the same table words);
   // region 0's is the seeds.
@@ -512,8 +562,7 @@ struct SampleRun {
                               2 * int64_t(small_slots(g)), 0, stream);
     }
     if (!ok && b) {
-      for (void *p : b->allocs) dev_free(g, p, stream);
-      delete b;
+      delete b;  // and its arrays
       b = nullptr;
     }
     release_workspace(g, ws, stream);
@@ -533,6 +582,11 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   hipError_t e;
   b->g = g;
   b->stream = stream;
+  b->mem = std::make_shared<OutAllocs>();
+  b->mem->device = g->device;
+  b->mem->has_alloc = g->has_alloc;
+  b->mem->alloc = g->alloc;
+  b->mem->stream = stream;
   b->H = H;
   b->T = T;
   b->R = R;
@@ -573,7 +627,9 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
 
   // (the readback slots are zero: a new workspace starts so, and every call
   // clears them when it ends)
-  if ((e = upload(0, size_t(H + 1) * lay.size)) != hipSuccess) return fail_device(e, "start");
+  std::memcpy(ws->htab, sigmas.data(), sizeof(uint64_t) * sigmas.size());
+  if ((e = upload(0, sig_bytes + size_t(H + 1) * lay.size)) != hipSuccess)
+    return fail_device(e, "start");
   int64_t total = 0;
   for (int64_t n : nF) total += n;
   map_region = 0;
@@ -658,7 +714,7 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     }
     void *ob = oc.allocate(g, stream);
     if (!ob) return fail(HG_ENOMEM, "hop %d: block arrays", h);
-    b->allocs.push_back(ob);
+    b->mem->ptrs.push_back(ob);
     Carve ec;
     int64_t *gid_tmp;
     ec.add(&gid_tmp, S);
@@ -683,7 +739,8 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     int64_t copy_total = 0;
     for (int64_t n : nF) copy_total += n;
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
-                           sigma, h, key_bits, gid_tmp, eid_all, dstl_all, indptr_all,
+                           dsigmas(), g->key_R, h, key_bits, gid_tmp, eid_all, dstl_all,
+                           indptr_all,
                            src_slot, src_out.data(), inline_ptrs ? T : 0, stream)) != hipSuccess)
       return fail_device(e, "sample");
     if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
@@ -744,7 +801,7 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     for (int32_t t = 0; t < T; ++t) a.add(&cp[t], nF[t]);
     void *base = a.allocate(g, stream);
     if (!base) return fail(HG_ENOMEM, "seed copy");
-    b->allocs.push_back(base);
+    b->mem->ptrs.push_back(base);
     for (int32_t t = 0; t < T; ++t) {
       if (nF[t] > 0 &&
           (e = hipMemcpyAsync(cp[t], seeds[t], sizeof(int64_t) * size_t(nF[t]),
@@ -809,16 +866,12 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
     g->has_alloc = true;
     g->alloc = *allocator;
   }
-  g->map_off.assign(n_ntypes + 1, 0);
-  g->tile_base.assign(n_ntypes + 1, 0);
+  g->key_R = n_etypes;
   for (int32_t t = 0; t < n_ntypes; ++t) {
     const hg_ntype_desc &d = ntypes[t];
     g->nt.push_back({d.num_nodes, d.feat, d.dtype, d.dim, dtype_size(d.dtype) * int64_t(d.dim)});
-    g->map_off[t + 1] = g->map_off[t] + d.num_nodes;
-    const int64_t words = (d.num_nodes + 31) / 32;
-    g->tile_base[t + 1] = g->tile_base[t] + (words + kTile - 1) / kTile;
   }
-  g->n_tiles = g->tile_base[n_ntypes];
+  layout_types(g);
   for (int32_t i = 0; i < n_etypes; ++i) {
     const hg_etype_desc &d = etypes[i];
     g->et.push_back({d.src_type, d.dst_type, d.nnz, d.indptr, d.indices});
@@ -871,9 +924,7 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
 void hg_destroy(hg_graph *g) {
   if (!g) return;
   DeviceGuard dg(g->device);
-  for (auto *w : g->ws) free_workspace(w);
-  (void)hipFree(g->d_tile_base);
-  delete g;
+  free_graph(g);
 }
 
 }  // extern "C"
@@ -893,7 +944,7 @@ hg_status gather_into_blocks(hg_graph *g, hg_blocks *b, const int32_t *gtypes,
   }
   void *base = c.allocate(g, stream);
   if (!base) return fail(HG_ENOMEM, "hg_sample_blocks_gather: feature arrays");
-  b->allocs.push_back(base);
+  b->mem->ptrs.push_back(base);
   std::vector<GatherJob> jobs;
   for (int32_t k = 0; k < n_gather; ++k) {
     const int32_t t = gtypes[k];
@@ -906,15 +957,10 @@ hg_status gather_into_blocks(hg_graph *g, hg_blocks *b, const int32_t *gtypes,
   return HG_OK;
 }
 
-hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
-                      int32_t n_hops, const int32_t *fanouts, uint64_t rng_seed,
-                      int32_t key_bits, const int32_t *gtypes, int32_t n_gather,
-                      hipEvent_t start, hipEvent_t stop, hipStream_t stream,
-                      hg_blocks **out) {
-  if (!out) return fail(HG_EINVAL, "hg_sample_blocks: out is NULL");
-  *out = nullptr;
-  clear_pending_error();
-  if (!g) return fail(HG_EINVAL, "hg_sample_blocks: graph is NULL");
+// Argument checks of one mini-batch on graph g (real).
+hg_status check_batch(const hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
+                      int32_t n_hops, const int32_t *fanouts, int32_t key_bits,
+                      const int32_t *gtypes, int32_t n_gather) {
   if (n_hops < 0) return fail(HG_EINVAL, "hg_sample_blocks: n_hops < 0");
   if (key_bits < 1 || key_bits > 32) return fail(HG_EINVAL, "hg_sample_blocks: key_bits not in 1..32");
   if (!n_seeds) return fail(HG_EINVAL, "hg_sample_blocks: n_seeds is NULL");
@@ -930,21 +976,28 @@ hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n
   }
   if (n_gather < 0 || (n_gather > 0 && !gtypes))
     return fail(HG_EINVAL, "hg_sample_blocks_gather: bad node type list");
-  {
-    std::vector<char> seen(g->T, 0);
-    for (int32_t k = 0; k < n_gather; ++k) {
-      const int32_t t = gtypes[k];
-      if (t < 0 || t >= g->T)
-        return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d out of range", t);
-      if (g->nt[t].dtype == HG_DT_NONE || g->nt[t].row_bytes <= 0)
-        return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d has no features", t);
-      if (seen[t]) return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d twice", t);
-      seen[t] = 1;
-    }
+  std::vector<char> seen(g->T, 0);
+  for (int32_t k = 0; k < n_gather; ++k) {
+    const int32_t t = gtypes[k];
+    if (t < 0 || t >= g->T)
+      return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d out of range", t);
+    if (g->nt[t].dtype == HG_DT_NONE || g->nt[t].row_bytes <= 0)
+      return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d has no features", t);
+    if (seen[t]) return fail(HG_EINVAL, "hg_sample_blocks_gather: node type %d twice", t);
+    seen[t] = 1;
   }
+  return HG_OK;
+}
+
+// One sampling run on g (a graph or the virtual graph of a bundle, already
+// checked), then the gather of node types gtypes into the handle.
+hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
+                       int32_t n_hops, const int32_t *fanouts, const uint64_t *sigmas,
+                       int32_t n_sig, int32_t key_bits, const int32_t *gtypes, int32_t n_gather,
+                       hipEvent_t start, hipEvent_t stop, hipStream_t stream, hg_blocks **out) {
   DeviceGuard dg(g->device);
-  SampleRun run(g, stream, n_hops, fanouts, rng_seed, key_bits);
-  hg_status st = acquire_workspace(g, run.lay.size * size_t(n_hops + 2), stream, &run.ws);
+  SampleRun run(g, stream, n_hops, fanouts, sigmas, n_sig, key_bits);
+  hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
   if (st != HG_OK) return st;
   run.b = new (std::nothrow) hg_blocks();
   if (!run.b) {
@@ -969,6 +1022,127 @@ hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n
   return HG_OK;
 }
 
+hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
+                      int32_t n_hops, const int32_t *fanouts, uint64_t rng_seed,
+                      int32_t key_bits, const int32_t *gtypes, int32_t n_gather,
+                      hipEvent_t start, hipEvent_t stop, hipStream_t stream,
+                      hg_blocks **out) {
+  if (!out) return fail(HG_EINVAL, "hg_sample_blocks: out is NULL");
+  *out = nullptr;
+  clear_pending_error();
+  if (!g) return fail(HG_EINVAL, "hg_sample_blocks: graph is NULL");
+  hg_status st = check_batch(g, seeds, n_seeds, n_hops, fanouts, key_bits, gtypes, n_gather);
+  if (st != HG_OK) return st;
+  return run_sampling(g, seeds, n_seeds, n_hops, fanouts, &rng_seed, 1, key_bits, gtypes,
+                      n_gather, start, stop, stream, out);
+}
+
+// Map and bitmap layout of a graph's node types.
+void layout_types(hg_graph *g) {
+  g->map_off.assign(g->T + 1, 0);
+  g->tile_base.assign(g->T + 1, 0);
+  for (int32_t t = 0; t < g->T; ++t) {
+    g->map_off[t + 1] = g->map_off[t] + g->nt[t].num_nodes;
+    const int64_t words = (g->nt[t].num_nodes + 31) / 32;
+    g->tile_base[t + 1] = g->tile_base[t] + (words + kTile - 1) / kTile;
+  }
+  g->n_tiles = g->tile_base[g->T];
+}
+
+void free_graph(hg_graph *g) {
+  for (auto &kv : g->bundles) free_graph(kv.second);
+  for (auto *w : g->ws) free_workspace(w);
+  (void)hipFree(g->d_tile_base);
+  delete g;
+}
+
+// The virtual graph of B copies of g (made once, kept until hg_destroy).
+hg_status bundle_graph(hg_graph *g, int32_t B, hg_graph **out) {
+  std::lock_guard<std::mutex> lk(g->mu);
+  auto it = g->bundles.find(B);
+  if (it != g->bundles.end()) {
+    *out = it->second;
+    return HG_OK;
+  }
+  hg_graph *v = new (std::nothrow) hg_graph();
+  if (!v) return fail(HG_ENOMEM, "bundle: out of host memory");
+  v->device = g->device;
+  v->T = B * g->T;
+  v->R = B * g->R;
+  v->key_R = g->R;
+  v->has_alloc = g->has_alloc;
+  v->alloc = g->alloc;
+  for (int32_t b = 0; b < B; ++b) {
+    for (int32_t t = 0; t < g->T; ++t) v->nt.push_back(g->nt[t]);
+    for (int32_t e = 0; e < g->R; ++e) {
+      ETypeInfo E = g->et[e];
+      E.src += b * g->T;
+      E.dst += b * g->T;
+      v->et.push_back(E);
+    }
+  }
+  v->total_nnz = int64_t(B) * g->total_nnz;
+  layout_types(v);
+  DeviceGuard dg(g->device);
+  hipError_t e = hipMalloc(&v->d_tile_base, sizeof(int64_t) * size_t(v->T + 1));
+  if (e == hipSuccess)
+    e = hipMemcpy(v->d_tile_base, v->tile_base.data(), sizeof(int64_t) * size_t(v->T + 1),
+                  hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(v->d_tile_base);
+    delete v;
+    return fail(HG_ENOMEM, "bundle: device table: %s", hipGetErrorString(e));
+  }
+  g->bundles[B] = v;
+  *out = v;
+  return HG_OK;
+}
+
+// Handle of copy b of a bundle's virtual blocks, as a mini-batch of the real
+// graph g; shares the arrays.
+hg_blocks *split_blocks(hg_graph *g, const hg_blocks *v, int32_t b) {
+  hg_blocks *o = new (std::nothrow) hg_blocks();
+  if (!o) return nullptr;
+  const int32_t T = g->T, R = g->R, H = v->H;
+  o->g = g;
+  o->stream = v->stream;
+  o->H = H;
+  o->T = T;
+  o->R = R;
+  o->n_dst.resize(size_t(H) * T);
+  o->n_src.resize(size_t(H) * T);
+  o->src_gid.resize(size_t(H) * T);
+  o->n_edges.resize(size_t(H) * R);
+  o->indptr.resize(size_t(H) * R);
+  o->src_local.resize(size_t(H) * R);
+  o->dst_local.resize(size_t(H) * R);
+  o->eid.resize(size_t(H) * R);
+  for (int32_t h = 0; h < H; ++h) {
+    for (int32_t t = 0; t < T; ++t) {
+      const size_t k = size_t(h) * T + t, kv = size_t(h) * v->T + size_t(b) * T + t;
+      o->n_dst[k] = v->n_dst[kv];
+      o->n_src[k] = v->n_src[kv];
+      o->src_gid[k] = v->src_gid[kv];
+    }
+    for (int32_t e = 0; e < R; ++e) {
+      const size_t k = size_t(h) * R + e, kv = size_t(h) * v->R + size_t(b) * R + e;
+      o->n_edges[k] = v->n_edges[kv];
+      o->indptr[k] = v->indptr[kv];
+      o->src_local[k] = v->src_local[kv];
+      o->dst_local[k] = v->dst_local[kv];
+      o->eid[k] = v->eid[kv];
+    }
+  }
+  for (int32_t t = 0; t < T; ++t) {
+    o->in_n.push_back(v->in_n[size_t(b) * T + t]);
+    o->in_gid.push_back(v->in_gid[size_t(b) * T + t]);
+    o->feat.push_back(v->feat[size_t(b) * T + t]);
+  }
+  o->mem = v->mem;
+  return o;
+}
+
 }  // namespace
 
 extern "C" {
@@ -990,6 +1164,62 @@ hg_status hg_sample_blocks_gather(hg_graph *g, const int64_t *const *seeds,
                                   hg_blocks **out) {
   return sample_impl(g, seeds, n_seeds, n_hops, fanouts, rng_seed, 32, gather_ntypes, n_gather,
                      start, stop, stream, out);
+}
+
+hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t *const *seeds,
+                                  const int64_t *n_seeds, int32_t n_hops,
+                                  const int32_t *fanouts, const uint64_t *rng_seeds,
+                                  const int32_t *gather_ntypes, int32_t n_gather,
+                                  hipEvent_t start, hipEvent_t stop, hipStream_t stream,
+                                  hg_blocks **out) {
+  if (!out) return fail(HG_EINVAL, "hg_sample_blocks_bundle: out is NULL");
+  clear_pending_error();
+  if (!g) return fail(HG_EINVAL, "hg_sample_blocks_bundle: graph is NULL");
+  if (n_batches < 1 || n_batches > kMaxBundle)
+    return fail(HG_EINVAL, "hg_sample_blocks_bundle: n_batches not in 1..%d", kMaxBundle);
+  for (int32_t b = 0; b < n_batches; ++b) out[b] = nullptr;
+  if (!rng_seeds || !n_seeds) return fail(HG_EINVAL, "hg_sample_blocks_bundle: NULL array");
+  const int32_t T = g->T, R = g->R;
+  for (int32_t b = 0; b < n_batches; ++b) {
+    hg_status st = check_batch(g, seeds ? seeds + size_t(b) * T : nullptr,
+                               n_seeds + size_t(b) * T, n_hops, fanouts, 32, gather_ntypes,
+                               n_gather);
+    if (st != HG_OK) return st;
+  }
+  if (n_batches == 1)
+    return run_sampling(g, seeds, n_seeds, n_hops, fanouts, rng_seeds, 1, 32, gather_ntypes,
+                        n_gather, start, stop, stream, out);
+  hg_graph *v = nullptr;
+  hg_status st = bundle_graph(g, n_batches, &v);
+  if (st != HG_OK) return st;
+  std::vector<const int64_t *> vseeds(size_t(n_batches) * T, nullptr);
+  if (seeds) vseeds.assign(seeds, seeds + size_t(n_batches) * T);
+  std::vector<int32_t> vfan(size_t(n_hops) * v->R);
+  for (int32_t h = 0; h < n_hops; ++h)
+    for (int32_t b = 0; b < n_batches; ++b)
+      for (int32_t e = 0; e < R; ++e)
+        vfan[size_t(h) * v->R + size_t(b) * R + e] = fanouts[size_t(h) * R + e];
+  std::vector<int32_t> vg;
+  for (int32_t b = 0; b < n_batches; ++b)
+    for (int32_t k = 0; k < n_gather; ++k) vg.push_back(b * T + gather_ntypes[k]);
+  hg_blocks *vb = nullptr;
+  st = run_sampling(v, vseeds.data(), n_seeds, n_hops, vfan.empty() ? nullptr : vfan.data(),
+                    rng_seeds, n_batches, 32, vg.empty() ? nullptr : vg.data(),
+                    int32_t(vg.size()), start, stop, stream, &vb);
+  if (st != HG_OK) return st;
+  for (int32_t b = 0; b < n_batches; ++b) {
+    out[b] = split_blocks(g, vb, b);
+    if (!out[b]) {
+      for (int32_t c = 0; c < b; ++c) {
+        delete out[c];
+        out[c] = nullptr;
+      }
+      delete vb;
+      return fail(HG_ENOMEM, "hg_sample_blocks_bundle: out of host memory");
+    }
+  }
+  delete vb;  // the split handles keep the arrays
+  return HG_OK;
 }
 
 hg_status hg_blocks_features(const hg_blocks *b, int32_t ntype, int64_t *rows,
@@ -1128,7 +1358,10 @@ hg_status set_error(hg_status st, const char *msg) {
   return st;
 }
 
-void blocks_detach_stream(hg_blocks *b) { b->stream = nullptr; }
+void blocks_detach_stream(hg_blocks *b) {
+  b->stream = nullptr;
+  if (b->mem) b->mem->stream = nullptr;
+}
 
 int graph_device(const hg_graph *g) { return g->device; }
 
@@ -1137,10 +1370,7 @@ int graph_device(const hg_graph *g) { return g->device; }
 extern "C" {
 
 void hg_blocks_free(hg_blocks *b) {
-  if (!b) return;
-  DeviceGuard dg(b->g->device);
-  for (void *p : b->allocs) dev_free(b->g, p, b->stream);
-  delete b;
+  delete b;  // the arrays go with the last handle that shares them
 }
 
 hg_status hg_debug_philox(const uint32_t *ctr, uint64_t key, int64_t n,

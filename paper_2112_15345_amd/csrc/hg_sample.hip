@@ -399,7 +399,11 @@ struct SampleArgs {
   PairArrays pa;
   uint64_t *cand;
   const int64_t *small;
-  uint64_t sigma;
+  // edge type e of this launch is copy e / key_R of the graph's edge type
+  // e % key_R (a mini-batch of a bundle); its key uses that type index and the
+  // copy's sampling seed sigmas[e / key_R]
+  const uint64_t *sigmas;
+  int32_t key_R;
   int32_t hop, key_bits;
   int64_t *src_gid, *eid;
   int32_t *dst_local;
@@ -410,6 +414,17 @@ struct SampleArgs {
   int64_t *src_out_new[kInlineTypes];
   int32_t n_src_out;
 };
+
+// Philox key words and counter edge type of (virtual) edge type e.
+struct KeyCtx {
+  uint32_t k0, k1;
+  int32_t ke;
+};
+__device__ __forceinline__ KeyCtx key_ctx(const SampleArgs &A, int e) {
+  const int b = e / A.key_R;
+  const uint64_t s = A.sigmas[b];
+  return KeyCtx{uint32_t(s), uint32_t(s >> 32), e - b * A.key_R};
+}
 
 // Role A: a wavefront per 64 consecutive pairs.  Each lane writes its pair's
 // block-CSC entry; then the wavefront copies the in-edges of the small
@@ -494,7 +509,8 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   const int64_t K = s;
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
-  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
+  const KeyCtx kc = key_ctx(A, e);
+  const uint32_t k0 = kc.k0, k1 = kc.k1;
   const uint64_t g_first = uint64_t(lo) >> 2;
   const uint64_t g_last = uint64_t(lo + deg - 1) >> 2;
   const uint64_t hi = uint64_t(lo + deg);
@@ -507,7 +523,7 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
     int mask = 0;
     U32x4 r{0, 0, 0, 0};
     if (g <= g_last) {
-      r = edge_keys(g, A.hop, e, k0, k1, shift);
+      r = edge_keys(g, A.hop, kc.ke, k0, k1, shift);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const uint64_t ed = 4 * g + q;
@@ -556,7 +572,7 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   }
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
-  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, e, k0, k1, shift);
+  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift);
 }
 
 // Role C: wavefront w takes the hub chunks [w * chunks_per_wave, ...) in
@@ -571,6 +587,7 @@ struct HubParams {
   int64_t hub, first_chunk, end_chunk, lo, deg, K;
   uint64_t tau;
   int e;
+  KeyCtx kc;
 };
 
 __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
@@ -580,6 +597,7 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   H.end_chunk = hub + 1 < A.n_hubs ? A.pa.hub_choff[hub + 1] : A.n_chunks;
   const int64_t p = A.pa.hub_pair[hub];
   H.e = A.pa.pet[p];
+  H.kc = key_ctx(A, H.e);
   H.lo = A.pa.plo[p];
   H.deg = A.pa.pdeg[p];
   H.K = A.pa.off[p + 1] - A.pa.off[p];
@@ -595,12 +613,12 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
 template <bool kChecked>
 __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H,
                                          uint64_t gb, int64_t c_lo, int64_t c_hi,
-                                         uint32_t lim, uint32_t shift, uint32_t k0,
-                                         uint32_t k1) {
+                                         uint32_t lim, uint32_t shift) {
   const int lane = lane_id();
   const uint64_t g = gb + lane;
   const U32x4 r = philox4x32_10(
-      U32x4{uint32_t(g), uint32_t(g >> 32), uint32_t(A.hop), uint32_t(H.e)}, k0, k1);
+      U32x4{uint32_t(g), uint32_t(g >> 32), uint32_t(A.hop), uint32_t(H.kc.ke)}, H.kc.k0,
+      H.kc.k1);
   if (!kChecked) {
     const uint32_t m = min(min(r.x, r.y), min(r.z, r.w));
     if (__ballot(m <= lim) == 0) return;
@@ -645,7 +663,6 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
   }
   HubParams H = hub_params(A, h_lo);
   const uint32_t shift = uint32_t(32 - A.key_bits);
-  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
   for (int64_t chunk = c_first; chunk < c_end; ++chunk) {
     while (chunk >= H.end_chunk) H = hub_params(A, H.hub + 1);
     // (key >> shift) < tau  <=>  key < tau << shift  <=>  key <= lim
@@ -663,11 +680,11 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
     if (k_hi > n_it) k_hi = n_it;
     if (k_hi < k_lo) k_hi = k_lo;
     for (int64_t k = 0; k < k_lo; ++k)
-      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, k0, k1);
+      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift);
     for (int64_t k = k_lo; k < k_hi; ++k)
-      hub_step<false>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, k0, k1);
+      hub_step<false>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift);
     for (int64_t k = k_hi; k < n_it; ++k)
-      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, k0, k1);
+      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift);
   }
 }
 
@@ -693,7 +710,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   const int64_t K = A.pa.off[p + 1] - o;
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
-  const uint32_t k0 = uint32_t(A.sigma), k1 = uint32_t(A.sigma >> 32);
+  const KeyCtx kc = key_ctx(A, e);
+  const uint32_t k0 = kc.k0, k1 = kc.k1;
   const uint64_t tau = cand_threshold(K, deg, key_space);
   const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
                              p - A.hv.pair_base[e]);
@@ -727,7 +745,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   }
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
-  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, e, k0, k1, shift);
+  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift);
 }
 
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
@@ -953,8 +971,8 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t n_types, int64_t n_pairs, int64_t n_wave,
                          int64_t n_chunks, int64_t n_hubs, PairArrays pa,
-                         uint64_t *cand, const int64_t *small, uint64_t sigma,
-                         int32_t hop, int32_t key_bits, int64_t *src_gid,
+                         uint64_t *cand, const int64_t *small, const uint64_t *sigmas,
+                         int32_t key_R, int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          hipStream_t stream) {
@@ -984,7 +1002,8 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.pa = pa;
   A.cand = cand;
   A.small = small;
-  A.sigma = sigma;
+  A.sigmas = sigmas;
+  A.key_R = key_R > 0 ? key_R : 1;
   A.hop = hop;
   A.key_bits = key_bits;
   A.src_gid = src_gid;

@@ -52,6 +52,6 @@ def test_library_argument_checks_without_device(lib):
     assert hg._lib.hg_sample_blocks_gather(None, None, None, 1, None, 0, None, 0, None, None,
                                            None, ctypes.byref(out)) == hg.HG_EINVAL
     assert hg._lib.hg_pipeline_create(None, 2, 4, None, 0, ctypes.byref(out)) == hg.HG_EINVAL
-    assert hg._lib.hg_pipeline_submit(None, None, None, 1, None, 0, None, None) == hg.HG_EINVAL
+    assert hg._lib.hg_pipeline_submit(None, 1, None, None, 1, None, None, None, None) == hg.HG_EINVAL
     assert hg._lib.hg_pipeline_next(None, ctypes.byref(out)) == hg.HG_EINVAL
     hg._lib.hg_pipeline_destroy(None)

@@ -105,3 +105,34 @@ def test_pipeline_close_with_outstanding_minibatches(tiny):
     b = g.sample_blocks(gpu_seeds(W.seeds_per_type(wl, 9)), fan, 9)
     assert not compare(host.sample_blocks(W.seeds_per_type(wl, 9), fan, 9), result_dict(g, b),
                        g.T, g.R, len(fan))
+
+
+def test_pipeline_bundles(tiny):
+    """Bundled submits: each mini-batch of a bundle comes back on its own, in
+    order, equal to its single call; a bad mini-batch fails its whole bundle
+    only; a bundle larger than the capacity is refused."""
+    wl, gen, g, host = tiny
+    fan = wl.fanout_matrix()
+    seeds = {b: gpu_seeds(W.seeds_per_type(wl, b)) for b in range(8)}
+    pipe = hg.Pipeline(g, workers=2, capacity=6)
+    pipe.submit_bundle([seeds[0], seeds[1], seeds[2]], fan, [0, 1, 2])
+    pipe.submit(seeds[3], fan, 3)
+    bad = [torch.tensor([7, 7], dtype=torch.int64, device="cuda"), None]
+    pipe.submit_bundle([seeds[4], bad], fan, [4, 5])
+    got = [pipe.next() for _ in range(4)]
+    for b, blocks in zip(range(4), got):
+        direct = g.sample_blocks(seeds[b], fan, b, gather="all")
+        assert not compare(result_dict(g, direct), result_dict(g, blocks), g.T, g.R, len(fan))
+        assert features(g, blocks) == features(g, direct)
+    for _ in range(2):
+        with pytest.raises(hg.HGError) as e:
+            pipe.next()
+        assert e.value.status == hg.HG_EINVAL
+    with pytest.raises(hg.HGError):
+        pipe.submit_bundle([seeds[b] for b in range(7)], fan, list(range(7)))
+    pipe.submit_bundle([seeds[6], seeds[7]], fan, [6, 7])
+    last = [pipe.next(), pipe.next()]
+    pipe.close()
+    for b, blocks in zip((6, 7), last):
+        ref = host.sample_blocks(W.seeds_per_type(wl, b), fan, b)
+        assert not compare(ref, result_dict(g, blocks), g.T, g.R, len(fan))
