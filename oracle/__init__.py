@@ -74,6 +74,20 @@ def _bind(lib):
     lib.oracle_gather_rows.argtypes = [_P, ctypes.c_int64, ctypes.c_int64, _P,
                                        ctypes.c_int64, _P]
     lib.oracle_gather_rows.restype = ctypes.c_int
+    lib.oracle_edge_dst.argtypes = [_P, ctypes.c_int64, ctypes.c_int64, _I64P]
+    lib.oracle_edge_dst.restype = ctypes.c_int
+    lib.oracle_negative_dst.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int64,
+                                        ctypes.c_int32, ctypes.c_int64, _I64P]
+    lib.oracle_negative_dst.restype = ctypes.c_int
+    lib.oracle_sample_edge_blocks.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_int32, _P,
+                                              ctypes.c_int32, _P, ctypes.c_uint64,
+                                              ctypes.c_int32, ctypes.POINTER(_P)]
+    lib.oracle_sample_edge_blocks.restype = ctypes.c_int
+    lib.oracle_blocks_seeds.argtypes = [_P, ctypes.c_int32, _I64P, ctypes.POINTER(_P)]
+    lib.oracle_blocks_seeds.restype = ctypes.c_int
+    lib.oracle_blocks_pairs.argtypes = [_P, ctypes.c_int32, _I64P, ctypes.POINTER(_P),
+                                        ctypes.POINTER(_P), _I64P, ctypes.POINTER(_P)]
+    lib.oracle_blocks_pairs.restype = ctypes.c_int
     return lib
 
 
@@ -121,6 +135,37 @@ def select(sigma, hop, etype, lo, hi, fanout, key_bits=32, lib=None):
     if st != OK:
         raise OracleError(st)
     return out[: n.value].copy()
+
+
+def edge_dst(indptr, eid, lib=None) -> int:
+    """The destination vertex of CSC slot `eid`."""
+    lib = lib or load()
+    ip = _arr_i64(indptr)
+    v = ctypes.c_int64(0)
+    st = lib.oracle_edge_dst(_ptr(ip), ip.size - 1, eid, ctypes.byref(v))
+    if st != OK:
+        raise OracleError(st)
+    return v.value
+
+
+def negative_dst(sigma, etype, eid, k, n_dst, lib=None) -> int:
+    """Negative destination k of target edge `eid` of `etype`."""
+    lib = lib or load()
+    v = ctypes.c_int64(0)
+    st = lib.oracle_negative_dst(sigma, etype, eid, k, n_dst, ctypes.byref(v))
+    if st != OK:
+        raise OracleError(st)
+    return v.value
+
+
+MAX_NEG = 64
+EXCLUDE_NONE, EXCLUDE_SELF, EXCLUDE_REVERSE = 0, 1, 2
+
+
+class _EdgeBatch(ctypes.Structure):
+    _fields_ = [("eids", ctypes.c_void_p), ("n_eids", ctypes.c_void_p),
+                ("n_neg", ctypes.c_int32), ("exclude", ctypes.c_int32),
+                ("rev_etype", ctypes.c_void_p), ("rev_eid", ctypes.c_void_p)]
 
 
 class OracleError(RuntimeError):
@@ -192,6 +237,63 @@ class HostGraph:
             raise OracleError(st)
         try:
             return _result_dict(self.lib, handle, H, T, R, [e[1] for e in self.etypes])
+        finally:
+            self.lib.oracle_blocks_free(handle)
+
+    def sample_edge_blocks(self, targets, fanouts, sigma, n_neg=0, exclude=0, rev_etype=None,
+                           rev_eid=None, key_bits=32):
+        """An edge-seeded mini-batch.  targets: per edge type an int64 array of
+        target edge IDs (or None); rev_etype: per edge type its reverse type or
+        -1; rev_eid: per edge type an int64 array [nnz] (or None).  Returns the
+        result dict of sample_blocks plus "seeds" {t: gids} and "pairs"
+        {e: (pos_src, pos_dst, neg_dst)}."""
+        T, R = self.T, self.R
+        tg = [None if (targets[e] is None) else _arr_i64(targets[e]) for e in range(R)]
+        tptr = (ctypes.c_void_p * max(R, 1))(*[(_ptr(x) if x is not None and x.size else None)
+                                               for x in tg])
+        tn = np.array([0 if x is None else x.size for x in tg] + [0], dtype=np.int64)
+        rv = None
+        rptr = None
+        if rev_etype is not None:
+            rv = np.ascontiguousarray(np.asarray(rev_etype, dtype=np.int32))
+        keep = []
+        if rev_eid is not None:
+            arrs = [None if x is None else _arr_i64(x) for x in rev_eid]
+            keep = arrs
+            rptr = (ctypes.c_void_p * max(R, 1))(*[(_ptr(x) if x is not None and x.size else None)
+                                                   for x in arrs])
+        batch = _EdgeBatch(ctypes.addressof(tptr), _ptr(tn), int(n_neg), int(exclude),
+                           _ptr(rv), None if rptr is None else ctypes.addressof(rptr))
+        H = len(fanouts)
+        fo = np.ascontiguousarray(np.asarray(fanouts, dtype=np.int32).reshape(H * R)) \
+            if H * R > 0 else np.zeros(1, dtype=np.int32)
+        handle = ctypes.c_void_p()
+        st = self.lib.oracle_sample_edge_blocks(ctypes.addressof(self._nt), T,
+                                                ctypes.addressof(self._et), R,
+                                                ctypes.addressof(batch), H, _ptr(fo), sigma,
+                                                key_bits, ctypes.byref(handle))
+        del keep
+        if st != OK:
+            raise OracleError(st)
+        try:
+            res = _result_dict(self.lib, handle, H, T, R, [e[1] for e in self.etypes])
+            res["seeds"] = {}
+            res["pairs"] = {}
+            for t in range(T):
+                n = ctypes.c_int64()
+                p = ctypes.c_void_p()
+                self.lib.oracle_blocks_seeds(handle, t, ctypes.byref(n), ctypes.byref(p))
+                res["seeds"][t] = _copy(p.value, n.value, ctypes.c_int64, np.int64)
+            for e in range(R):
+                npos, nneg = ctypes.c_int64(), ctypes.c_int64()
+                ps, pd, pn = (ctypes.c_void_p() for _ in range(3))
+                self.lib.oracle_blocks_pairs(handle, e, ctypes.byref(npos), ctypes.byref(ps),
+                                             ctypes.byref(pd), ctypes.byref(nneg),
+                                             ctypes.byref(pn))
+                res["pairs"][e] = (_copy(ps.value, npos.value, ctypes.c_int32, np.int32),
+                                   _copy(pd.value, npos.value, ctypes.c_int32, np.int32),
+                                   _copy(pn.value, nneg.value, ctypes.c_int32, np.int32))
+            return res
         finally:
             self.lib.oracle_blocks_free(handle)
 

@@ -116,24 +116,34 @@ static int cmp_i64(const void *a, const void *b) {
   return x < y ? -1 : (x > y ? 1 : 0);
 }
 
-int oracle_select(uint64_t sigma, int32_t hop, int32_t etype, int64_t lo,
-                  int64_t hi, int32_t fanout, int32_t key_bits,
-                  int64_t *out_eids, int64_t *n_out) {
+/* index of x in the ascending array, or -1 */
+static int64_t find_sorted(const int64_t *arr, int64_t n, int64_t x);
+
+/* Sampling of one pair among its in-edges lo..hi-1 that are not in the
+ * ascending list xs[0..nx) of excluded edge IDs: every remaining edge when
+ * at most `fanout` remain (or fanout == -1), else the `fanout` remaining
+ * edges with the smallest (key, eid); written in ascending edge ID. */
+static int select_pair(uint64_t sigma, int32_t hop, int32_t etype, int64_t lo,
+                       int64_t hi, int32_t fanout, int32_t key_bits,
+                       const int64_t *xs, int64_t nx, int64_t *out_eids,
+                       int64_t *n_out) {
   if (hi < lo || fanout < -1 || key_bits < 1 || key_bits > 32)
     return ORACLE_EINVAL;
-  int64_t deg = hi - lo;
+  /* the in-edges that take part: every slot lo..hi-1 not excluded */
+  int64_t deg = 0;
+  for (int64_t j = lo; j < hi; ++j)
+    if (nx == 0 || find_sorted(xs, nx, j) < 0) out_eids[deg++] = j;
   if (fanout < 0 || deg <= fanout) {
-    /* keep every in-edge, in slot order */
-    for (int64_t j = 0; j < deg; ++j) out_eids[j] = lo + j;
+    /* keep every one of them, in slot order */
     *n_out = deg;
     return ORACLE_OK;
   }
-  /* key every in-edge, order by (key, eid), keep the first `fanout` */
+  /* key every one, order by (key, eid), keep the first `fanout` */
   keyed_edge *all = (keyed_edge *)malloc(sizeof(keyed_edge) * (size_t)deg);
   if (!all) return ORACLE_ENOMEM;
   for (int64_t j = 0; j < deg; ++j) {
-    all[j].eid = lo + j;
-    all[j].key = oracle_edge_key(sigma, hop, etype, lo + j, key_bits);
+    all[j].eid = out_eids[j];
+    all[j].key = oracle_edge_key(sigma, hop, etype, out_eids[j], key_bits);
   }
   qsort(all, (size_t)deg, sizeof(keyed_edge), cmp_keyed_edge);
   for (int64_t j = 0; j < fanout; ++j) out_eids[j] = all[j].eid;
@@ -141,6 +151,13 @@ int oracle_select(uint64_t sigma, int32_t hop, int32_t etype, int64_t lo,
   qsort(out_eids, (size_t)fanout, sizeof(int64_t), cmp_i64);
   *n_out = fanout;
   return ORACLE_OK;
+}
+
+int oracle_select(uint64_t sigma, int32_t hop, int32_t etype, int64_t lo,
+                  int64_t hi, int32_t fanout, int32_t key_bits,
+                  int64_t *out_eids, int64_t *n_out) {
+  return select_pair(sigma, hop, etype, lo, hi, fanout, key_bits, NULL, 0,
+                     out_eids, n_out);
 }
 
 /* ------------------------------------------------------------------ */
@@ -197,6 +214,14 @@ struct oracle_blocks {
   oedges *edges;   /* [n_hops * n_etypes] */
   int64_t *in_n;   /* [n_ntypes] */
   int64_t **in_gid;
+  /* edge-seeded mini-batches only (NULL otherwise) */
+  int64_t *seed_n;      /* [n_ntypes] */
+  int64_t **seed_gid;   /* [n_ntypes] ascending */
+  int32_t n_neg;
+  int64_t *pair_n;      /* [n_etypes] target edges */
+  int32_t **pos_src;    /* [n_etypes][pair_n] local IDs among the seeds */
+  int32_t **pos_dst;
+  int32_t **neg_dst;    /* [n_etypes][pair_n * n_neg] */
 };
 
 void oracle_blocks_free(oracle_blocks *b) {
@@ -213,6 +238,20 @@ void oracle_blocks_free(oracle_blocks *b) {
     }
   if (b->in_gid)
     for (int32_t t = 0; t < b->n_ntypes; ++t) free(b->in_gid[t]);
+  if (b->seed_gid)
+    for (int32_t t = 0; t < b->n_ntypes; ++t) free(b->seed_gid[t]);
+  if (b->pos_src)
+    for (int32_t e = 0; e < b->n_etypes; ++e) {
+      free(b->pos_src[e]);
+      free(b->pos_dst[e]);
+      free(b->neg_dst[e]);
+    }
+  free(b->seed_n);
+  free(b->seed_gid);
+  free(b->pair_n);
+  free(b->pos_src);
+  free(b->pos_dst);
+  free(b->neg_dst);
   free(b->nodes);
   free(b->edges);
   free(b->in_n);
@@ -267,73 +306,21 @@ typedef struct {
 /* ------------------------------------------------------------------ */
 /* The mini-batch.                                                      */
 
-int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
-                         const oracle_etype *etypes, int32_t n_etypes,
-                         const int64_t *const *seeds, const int64_t *n_seeds,
-                         int32_t n_hops, const int32_t *fanouts, uint64_t sigma,
-                         int32_t key_bits, oracle_blocks **out) {
-  if (!out) return ORACLE_EINVAL;
-  *out = NULL;
-  if (n_ntypes < 1 || n_etypes < 0 || !ntypes || (n_etypes > 0 && !etypes))
-    return ORACLE_EINVAL;
-  if (n_hops < 0 || key_bits < 1 || key_bits > 32 || !n_seeds)
-    return ORACLE_EINVAL;
-  if (n_hops > 0 && n_etypes > 0 && !fanouts) return ORACLE_EINVAL;
-  for (int64_t i = 0; i < (int64_t)n_hops * n_etypes; ++i)
-    if (fanouts[i] < -1) return ORACLE_EINVAL;
-  for (int32_t e = 0; e < n_etypes; ++e)
-    if (etypes[e].src_type < 0 || etypes[e].src_type >= n_ntypes ||
-        etypes[e].dst_type < 0 || etypes[e].dst_type >= n_ntypes)
-      return ORACLE_EINVAL;
+/* Per edge type, an ascending list of edge IDs that no hop may sample (the
+ * exclusion of an edge-seeded mini-batch); n == 0 excludes nothing. */
+typedef struct {
+  int64_t *eids;
+  int64_t n;
+} excl_list;
 
-  /* Seeds: present, in range and unique within their type (the targets of a
-   * mini-batch are a set of vertices, Sec. 3.2). */
-  for (int32_t t = 0; t < n_ntypes; ++t) {
-    if (n_seeds[t] < 0) return ORACLE_EINVAL;
-    if (n_seeds[t] == 0) continue;
-    if (!seeds || !seeds[t]) return ORACLE_EINVAL;
-    int64_t *tmp = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_seeds[t]);
-    if (!tmp) return ORACLE_ENOMEM;
-    memcpy(tmp, seeds[t], sizeof(int64_t) * (size_t)n_seeds[t]);
-    qsort(tmp, (size_t)n_seeds[t], sizeof(int64_t), cmp_i64);
-    int bad = 0;
-    for (int64_t i = 0; i < n_seeds[t]; ++i) {
-      if (tmp[i] < 0 || tmp[i] >= ntypes[t].num_nodes) bad = 1;
-      if (i > 0 && tmp[i] == tmp[i - 1]) bad = 1;
-    }
-    free(tmp);
-    if (bad) return ORACLE_EINVAL;
-  }
-
-  oracle_blocks *b = (oracle_blocks *)calloc(1, sizeof(oracle_blocks));
-  if (!b) return ORACLE_ENOMEM;
-  b->n_hops = n_hops;
-  b->n_ntypes = n_ntypes;
-  b->n_etypes = n_etypes;
-  b->nodes = (onodes *)calloc((size_t)n_hops * n_ntypes + 1, sizeof(onodes));
-  b->edges = (oedges *)calloc((size_t)n_hops * n_etypes + 1, sizeof(oedges));
-  b->in_n = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
-  b->in_gid = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
-  if (!b->nodes || !b->edges || !b->in_n || !b->in_gid) {
-    oracle_blocks_free(b);
-    return ORACLE_ENOMEM;
-  }
-
-  /* frontier of the current hop, per node type: F[0][t] = seeds of t */
-  int64_t *fn = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
-  int64_t **fr = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
+/* The hops of one mini-batch from a first frontier fr[t][0..fn[t]) that this
+ * function takes over (and frees); fills b's blocks and input frontier. */
+static int run_hops(const oracle_ntype *ntypes, int32_t n_ntypes,
+                    const oracle_etype *etypes, int32_t n_etypes,
+                    int64_t **fr, int64_t *fn, int32_t n_hops,
+                    const int32_t *fanouts, uint64_t sigma, int32_t key_bits,
+                    const excl_list *excl, oracle_blocks *b) {
   int status = ORACLE_OK;
-  if (!fn || !fr) status = ORACLE_ENOMEM;
-  for (int32_t t = 0; t < n_ntypes && status == ORACLE_OK; ++t) {
-    fn[t] = n_seeds[t];
-    fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
-    if (!fr[t]) {
-      status = ORACLE_ENOMEM;
-      break;
-    }
-    if (fn[t] > 0) memcpy(fr[t], seeds[t], sizeof(int64_t) * (size_t)fn[t]);
-  }
-
   for (int32_t h = 0; h < n_hops && status == ORACLE_OK; ++h) {
     /* ---- Step 1: sample the neighbours of every (destination, etype)
      * pair of this hop's frontier, each pair independently. */
@@ -374,7 +361,8 @@ int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
           status = ORACLE_ENOMEM;
           break;
         }
-        status = oracle_select(sigma, h, e, lo, hi, k, key_bits, chosen, &nc);
+        status = select_pair(sigma, h, e, lo, hi, k, key_bits, excl[e].eids,
+                             excl[e].n, chosen, &nc);
         if (status != ORACLE_OK) {
           free(chosen);
           break;
@@ -513,10 +501,100 @@ int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
     b->in_gid[t] = fr[t];
     fr[t] = NULL;
   }
-  if (fr)
+  for (int32_t t = 0; t < n_ntypes; ++t) free(fr[t]);
+  (void)ntypes;
+  return status;
+}
+
+/* A blocks container for n_hops hops (everything zeroed). */
+static oracle_blocks *new_blocks(int32_t n_hops, int32_t n_ntypes, int32_t n_etypes) {
+  oracle_blocks *b = (oracle_blocks *)calloc(1, sizeof(oracle_blocks));
+  if (!b) return NULL;
+  b->n_hops = n_hops;
+  b->n_ntypes = n_ntypes;
+  b->n_etypes = n_etypes;
+  b->nodes = (onodes *)calloc((size_t)n_hops * n_ntypes + 1, sizeof(onodes));
+  b->edges = (oedges *)calloc((size_t)n_hops * n_etypes + 1, sizeof(oedges));
+  b->in_n = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
+  b->in_gid = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
+  if (!b->nodes || !b->edges || !b->in_n || !b->in_gid) {
+    oracle_blocks_free(b);
+    return NULL;
+  }
+  return b;
+}
+
+/* Shared argument checks of both kinds of mini-batch. */
+static int check_common(const oracle_ntype *ntypes, int32_t n_ntypes,
+                        const oracle_etype *etypes, int32_t n_etypes, int32_t n_hops,
+                        const int32_t *fanouts, int32_t key_bits) {
+  if (n_ntypes < 1 || n_etypes < 0 || !ntypes || (n_etypes > 0 && !etypes))
+    return ORACLE_EINVAL;
+  if (n_hops < 0 || key_bits < 1 || key_bits > 32) return ORACLE_EINVAL;
+  if (n_hops > 0 && n_etypes > 0 && !fanouts) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < (int64_t)n_hops * n_etypes; ++i)
+    if (fanouts[i] < -1) return ORACLE_EINVAL;
+  for (int32_t e = 0; e < n_etypes; ++e)
+    if (etypes[e].src_type < 0 || etypes[e].src_type >= n_ntypes ||
+        etypes[e].dst_type < 0 || etypes[e].dst_type >= n_ntypes)
+      return ORACLE_EINVAL;
+  return ORACLE_OK;
+}
+
+int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
+                         const oracle_etype *etypes, int32_t n_etypes,
+                         const int64_t *const *seeds, const int64_t *n_seeds,
+                         int32_t n_hops, const int32_t *fanouts, uint64_t sigma,
+                         int32_t key_bits, oracle_blocks **out) {
+  if (!out) return ORACLE_EINVAL;
+  *out = NULL;
+  int status = check_common(ntypes, n_ntypes, etypes, n_etypes, n_hops, fanouts, key_bits);
+  if (status != ORACLE_OK) return status;
+  if (!n_seeds) return ORACLE_EINVAL;
+
+  /* Seeds: present, in range and unique within their type (the targets of a
+   * mini-batch are a set of vertices, Sec. 3.2). */
+  for (int32_t t = 0; t < n_ntypes; ++t) {
+    if (n_seeds[t] < 0) return ORACLE_EINVAL;
+    if (n_seeds[t] == 0) continue;
+    if (!seeds || !seeds[t]) return ORACLE_EINVAL;
+    int64_t *tmp = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_seeds[t]);
+    if (!tmp) return ORACLE_ENOMEM;
+    memcpy(tmp, seeds[t], sizeof(int64_t) * (size_t)n_seeds[t]);
+    qsort(tmp, (size_t)n_seeds[t], sizeof(int64_t), cmp_i64);
+    int bad = 0;
+    for (int64_t i = 0; i < n_seeds[t]; ++i) {
+      if (tmp[i] < 0 || tmp[i] >= ntypes[t].num_nodes) bad = 1;
+      if (i > 0 && tmp[i] == tmp[i - 1]) bad = 1;
+    }
+    free(tmp);
+    if (bad) return ORACLE_EINVAL;
+  }
+
+  oracle_blocks *b = new_blocks(n_hops, n_ntypes, n_etypes);
+  if (!b) return ORACLE_ENOMEM;
+  /* frontier of the current hop, per node type: F[0][t] = seeds of t */
+  int64_t *fn = (int64_t *)calloc((size_t)n_ntypes, sizeof(int64_t));
+  int64_t **fr = (int64_t **)calloc((size_t)n_ntypes, sizeof(int64_t *));
+  excl_list *none = (excl_list *)calloc((size_t)n_etypes + 1, sizeof(excl_list));
+  if (!fn || !fr || !none) status = ORACLE_ENOMEM;
+  for (int32_t t = 0; t < n_ntypes && status == ORACLE_OK; ++t) {
+    fn[t] = n_seeds[t];
+    fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
+    if (!fr[t]) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    if (fn[t] > 0) memcpy(fr[t], seeds[t], sizeof(int64_t) * (size_t)fn[t]);
+  }
+  if (status == ORACLE_OK)
+    status = run_hops(ntypes, n_ntypes, etypes, n_etypes, fr, fn, n_hops, fanouts, sigma,
+                      key_bits, none, b);
+  else if (fr)
     for (int32_t t = 0; t < n_ntypes; ++t) free(fr[t]);
   free(fr);
   free(fn);
+  free(none);
   if (status != ORACLE_OK) {
     oracle_blocks_free(b);
     return status;
@@ -569,5 +647,278 @@ int oracle_gather_rows(const void *feat, int64_t n_rows, int64_t row_bytes,
   for (int64_t i = 0; i < n; ++i)
     memcpy((char *)out + i * row_bytes,
            (const char *)feat + ids[i] * row_bytes, (size_t)row_bytes);
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Edge-seeded mini-batches (link prediction).  The scheduler of Sec. 4.2.1
+ * picks target edges instead of target vertices; the same neighbour
+ * sampling, compaction and feature gather then run from the targets'
+ * endpoints (Sec. 4.2.2 notes that the decomposition carries over to link
+ * prediction).  Readings where the paper is silent:
+ *  - a target is an edge ID (CSC slot) of an edge type; targets may repeat;
+ *  - its endpoints are indices[eid] (source) and the destination whose
+ *    in-edge slots hold eid;
+ *  - optional negatives: n_neg per target, same source, destination drawn
+ *    uniformly from the destination type by Philox4x32-10 (see
+ *    oracle_negative_dst);
+ *  - seeds of a node type: every endpoint and negative destination of that
+ *    type, each once, in ascending ID;
+ *  - exclusion 1 takes the target edges out of every hop's sampling;
+ *    exclusion 2 also takes out each target's reverse edge, named by a
+ *    caller-given map into a reverse edge type.                         */
+
+int oracle_edge_dst(const int64_t *indptr, int64_t n_dst, int64_t eid, int64_t *dst) {
+  if (!indptr || !dst || n_dst < 1 || eid < 0 || eid >= indptr[n_dst]) return ORACLE_EINVAL;
+  /* the destination v with indptr[v] <= eid < indptr[v+1]: the largest v
+   * whose first slot is not above eid */
+  int64_t a = 0, b = n_dst - 1;
+  while (a < b) {
+    int64_t m = a + (b - a + 1) / 2;
+    if (indptr[m] <= eid)
+      a = m;
+    else
+      b = m - 1;
+  }
+  *dst = a;
+  return ORACLE_OK;
+}
+
+int oracle_negative_dst(uint64_t sigma, int32_t etype, int64_t eid, int32_t k,
+                        int64_t n_dst, int64_t *v) {
+  if (!v || k < 0 || n_dst < 1) return ORACLE_EINVAL;
+  /* counter (eid lo32, eid hi32, 2^31 | k, etype): the third word never has
+   * its top bit set for a sampling key (a hop number), so the two streams
+   * never share a counter */
+  uint32_t ctr[4] = {(uint32_t)eid, (uint32_t)((uint64_t)eid >> 32), 0x80000000u | (uint32_t)k,
+                     (uint32_t)etype};
+  uint32_t seed_words[2] = {(uint32_t)sigma, (uint32_t)(sigma >> 32)};
+  uint32_t out[4];
+  oracle_philox4x32_10(ctr, seed_words, out);
+  /* u uniform on [0, 2^64); v = floor(u * n / 2^64) is uniform on [0, n)
+   * up to n / 2^64 */
+  uint64_t u = (uint64_t)out[0] | ((uint64_t)out[1] << 32);
+  *v = (int64_t)(((unsigned __int128)u * (unsigned __int128)(uint64_t)n_dst) >> 64);
+  return ORACLE_OK;
+}
+
+/* ascending, duplicates removed; returns the new length */
+static int64_t sort_unique(int64_t *a, int64_t n) {
+  if (n == 0) return 0;
+  qsort(a, (size_t)n, sizeof(int64_t), cmp_i64);
+  int64_t u = 1;
+  for (int64_t i = 1; i < n; ++i)
+    if (a[i] != a[u - 1]) a[u++] = a[i];
+  return u;
+}
+
+int oracle_sample_edge_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
+                              const oracle_etype *etypes, int32_t n_etypes,
+                              const oracle_edge_batch *batch, int32_t n_hops,
+                              const int32_t *fanouts, uint64_t sigma, int32_t key_bits,
+                              oracle_blocks **out) {
+  if (!out) return ORACLE_EINVAL;
+  *out = NULL;
+  int status = check_common(ntypes, n_ntypes, etypes, n_etypes, n_hops, fanouts, key_bits);
+  if (status != ORACLE_OK) return status;
+  if (!batch || !batch->n_eids || batch->n_neg < 0 || batch->n_neg > ORACLE_MAX_NEG ||
+      batch->exclude < 0 || batch->exclude > 2)
+    return ORACLE_EINVAL;
+  if (batch->exclude == 2 && (!batch->rev_etype || !batch->rev_eid)) return ORACLE_EINVAL;
+  const int32_t R = n_etypes, T = n_ntypes, Q = batch->n_neg;
+
+  /* every target: in range; with exclusion 2 its reverse must be an edge of
+   * the reverse type that runs the other way */
+  for (int32_t e = 0; e < R; ++e) {
+    const int64_t n = batch->n_eids[e];
+    if (n < 0 || (n > 0 && (!batch->eids || !batch->eids[e]))) return ORACLE_EINVAL;
+    const oracle_etype *et = &etypes[e];
+    const int64_t n_dst = ntypes[et->dst_type].num_nodes;
+    for (int64_t i = 0; i < n; ++i) {
+      const int64_t j = batch->eids[e][i];
+      if (j < 0 || j >= et->nnz) return ORACLE_EINVAL;
+    }
+    if (batch->exclude != 2 || n == 0) continue;
+    const int32_t r = batch->rev_etype[e];
+    if (r < 0) continue;
+    if (r >= R || etypes[r].src_type != et->dst_type || etypes[r].dst_type != et->src_type ||
+        !batch->rev_eid[e])
+      return ORACLE_EINVAL;
+    const int64_t rn_dst = ntypes[etypes[r].dst_type].num_nodes;
+    for (int64_t i = 0; i < n; ++i) {
+      const int64_t j = batch->eids[e][i];
+      const int64_t rj = batch->rev_eid[e][j];
+      int64_t v, rv;
+      if (rj < 0 || rj >= etypes[r].nnz) return ORACLE_EINVAL;
+      if (oracle_edge_dst(et->indptr, n_dst, j, &v) != ORACLE_OK ||
+          oracle_edge_dst(etypes[r].indptr, rn_dst, rj, &rv) != ORACLE_OK)
+        return ORACLE_EINVAL;
+      if (etypes[r].indices[rj] != v || rv != et->indices[j]) return ORACLE_EINVAL;
+    }
+  }
+
+  oracle_blocks *b = new_blocks(n_hops, n_ntypes, n_etypes);
+  if (!b) return ORACLE_ENOMEM;
+  b->n_neg = Q;
+  b->seed_n = (int64_t *)calloc((size_t)T, sizeof(int64_t));
+  b->seed_gid = (int64_t **)calloc((size_t)T, sizeof(int64_t *));
+  b->pair_n = (int64_t *)calloc((size_t)R + 1, sizeof(int64_t));
+  b->pos_src = (int32_t **)calloc((size_t)R + 1, sizeof(int32_t *));
+  b->pos_dst = (int32_t **)calloc((size_t)R + 1, sizeof(int32_t *));
+  b->neg_dst = (int32_t **)calloc((size_t)R + 1, sizeof(int32_t *));
+  /* per etype: endpoint IDs of every target, negative destinations */
+  int64_t **src = (int64_t **)calloc((size_t)R + 1, sizeof(int64_t *));
+  int64_t **dst = (int64_t **)calloc((size_t)R + 1, sizeof(int64_t *));
+  int64_t **neg = (int64_t **)calloc((size_t)R + 1, sizeof(int64_t *));
+  excl_list *excl = (excl_list *)calloc((size_t)R + 1, sizeof(excl_list));
+  int64_t *fn = (int64_t *)calloc((size_t)T, sizeof(int64_t));
+  int64_t **fr = (int64_t **)calloc((size_t)T, sizeof(int64_t *));
+  if (!b->seed_n || !b->seed_gid || !b->pair_n || !b->pos_src || !b->pos_dst ||
+      !b->neg_dst || !src || !dst || !neg || !excl || !fn || !fr)
+    status = ORACLE_ENOMEM;
+
+  /* 1. endpoints and negatives */
+  for (int32_t e = 0; e < R && status == ORACLE_OK; ++e) {
+    const oracle_etype *et = &etypes[e];
+    const int64_t n = batch->n_eids[e];
+    const int64_t n_dst = ntypes[et->dst_type].num_nodes;
+    src[e] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n + 1));
+    dst[e] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n + 1));
+    neg[e] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n * Q + 1));
+    if (!src[e] || !dst[e] || !neg[e]) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    for (int64_t i = 0; i < n && status == ORACLE_OK; ++i) {
+      const int64_t j = batch->eids[e][i];
+      src[e][i] = et->indices[j];
+      status = oracle_edge_dst(et->indptr, n_dst, j, &dst[e][i]);
+      for (int32_t k = 0; k < Q && status == ORACLE_OK; ++k)
+        status = oracle_negative_dst(sigma, e, j, k, n_dst, &neg[e][i * Q + k]);
+    }
+  }
+
+  /* 2. seeds per node type: the endpoints of that type, once each, ascending */
+  for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+    int64_t cap = 0;
+    for (int32_t e = 0; e < R; ++e) {
+      if (etypes[e].src_type == t) cap += batch->n_eids[e];
+      if (etypes[e].dst_type == t) cap += batch->n_eids[e] * (1 + Q);
+    }
+    int64_t *all = (int64_t *)malloc(sizeof(int64_t) * (size_t)(cap + 1));
+    if (!all) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    int64_t m = 0;
+    for (int32_t e = 0; e < R; ++e) {
+      const int64_t n = batch->n_eids[e];
+      if (etypes[e].src_type == t)
+        for (int64_t i = 0; i < n; ++i) all[m++] = src[e][i];
+      if (etypes[e].dst_type == t) {
+        for (int64_t i = 0; i < n; ++i) all[m++] = dst[e][i];
+        for (int64_t i = 0; i < n * Q; ++i) all[m++] = neg[e][i];
+      }
+    }
+    b->seed_n[t] = sort_unique(all, m);
+    b->seed_gid[t] = all;
+  }
+
+  /* 3. the pair graphs: local IDs (positions among the seeds) */
+  for (int32_t e = 0; e < R && status == ORACLE_OK; ++e) {
+    const int32_t s = etypes[e].src_type, d = etypes[e].dst_type;
+    const int64_t n = batch->n_eids[e];
+    b->pair_n[e] = n;
+    b->pos_src[e] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
+    b->pos_dst[e] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n + 1));
+    b->neg_dst[e] = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n * Q + 1));
+    if (!b->pos_src[e] || !b->pos_dst[e] || !b->neg_dst[e]) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+      b->pos_src[e][i] = (int32_t)find_sorted(b->seed_gid[s], b->seed_n[s], src[e][i]);
+      b->pos_dst[e][i] = (int32_t)find_sorted(b->seed_gid[d], b->seed_n[d], dst[e][i]);
+    }
+    for (int64_t i = 0; i < n * Q; ++i)
+      b->neg_dst[e][i] = (int32_t)find_sorted(b->seed_gid[d], b->seed_n[d], neg[e][i]);
+  }
+
+  /* 4. the excluded edges, per edge type, ascending and unique */
+  if (batch->exclude >= 1 && status == ORACLE_OK) {
+    for (int32_t e = 0; e < R && status == ORACLE_OK; ++e) {
+      int64_t cap = batch->n_eids[e];
+      if (batch->exclude == 2)
+        for (int32_t f = 0; f < R; ++f)
+          if (batch->rev_etype[f] == e) cap += batch->n_eids[f];
+      excl[e].eids = (int64_t *)malloc(sizeof(int64_t) * (size_t)(cap + 1));
+      if (!excl[e].eids) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      int64_t m = 0;
+      for (int64_t i = 0; i < batch->n_eids[e]; ++i) excl[e].eids[m++] = batch->eids[e][i];
+      if (batch->exclude == 2)
+        for (int32_t f = 0; f < R; ++f)
+          if (batch->rev_etype[f] == e)
+            for (int64_t i = 0; i < batch->n_eids[f]; ++i)
+              excl[e].eids[m++] = batch->rev_eid[f][batch->eids[f][i]];
+      excl[e].n = sort_unique(excl[e].eids, m);
+    }
+  }
+
+  /* 5. the hops, from the seeds */
+  for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+    fn[t] = b->seed_n[t];
+    fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
+    if (!fr[t]) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    if (fn[t] > 0) memcpy(fr[t], b->seed_gid[t], sizeof(int64_t) * (size_t)fn[t]);
+  }
+  if (status == ORACLE_OK)
+    status = run_hops(ntypes, n_ntypes, etypes, n_etypes, fr, fn, n_hops, fanouts, sigma,
+                      key_bits, excl, b);
+  else if (fr)
+    for (int32_t t = 0; t < T; ++t) free(fr[t]);
+
+  for (int32_t e = 0; e < R; ++e) {
+    if (src) free(src[e]);
+    if (dst) free(dst[e]);
+    if (neg) free(neg[e]);
+    if (excl) free(excl[e].eids);
+  }
+  free(src);
+  free(dst);
+  free(neg);
+  free(excl);
+  free(fr);
+  free(fn);
+  if (status != ORACLE_OK) {
+    oracle_blocks_free(b);
+    return status;
+  }
+  *out = b;
+  return ORACLE_OK;
+}
+
+int oracle_blocks_seeds(const oracle_blocks *b, int32_t ntype, int64_t *n,
+                        const int64_t **gid) {
+  if (!b || !b->seed_n || ntype < 0 || ntype >= b->n_ntypes) return ORACLE_EINVAL;
+  if (n) *n = b->seed_n[ntype];
+  if (gid) *gid = b->seed_gid[ntype];
+  return ORACLE_OK;
+}
+
+int oracle_blocks_pairs(const oracle_blocks *b, int32_t etype, int64_t *n_pos,
+                        const int32_t **pos_src, const int32_t **pos_dst,
+                        int64_t *n_negs, const int32_t **neg_dst) {
+  if (!b || !b->pair_n || etype < 0 || etype >= b->n_etypes) return ORACLE_EINVAL;
+  if (n_pos) *n_pos = b->pair_n[etype];
+  if (pos_src) *pos_src = b->pos_src[etype];
+  if (pos_dst) *pos_dst = b->pos_dst[etype];
+  if (n_negs) *n_negs = b->pair_n[etype] * b->n_neg;
+  if (neg_dst) *neg_dst = b->neg_dst[etype];
   return ORACLE_OK;
 }

@@ -102,6 +102,46 @@ int oracle_blocks_input_nodes(const oracle_blocks *b, int32_t ntype,
 int oracle_gather_rows(const void *feat, int64_t n_rows, int64_t row_bytes,
                        const int64_t *ids, int64_t n, void *out);
 
+
+/* ---- Edge-seeded mini-batches (link prediction; Sec. 4.2.1: the scheduler
+ * picks target vertices or target edges).  See oracle.c for the readings. */
+
+#define ORACLE_MAX_NEG 64
+
+typedef struct {
+  const int64_t *const *eids; /* [n_etypes] target edge IDs per edge type (NULL when none) */
+  const int64_t *n_eids;      /* [n_etypes] */
+  int32_t n_neg;              /* negatives per target, 0..ORACLE_MAX_NEG */
+  int32_t exclude;            /* 0 none, 1 the targets, 2 the targets and their reverses */
+  const int32_t *rev_etype;   /* [n_etypes] reverse edge type or -1 (exclude == 2) */
+  const int64_t *const *rev_eid; /* [n_etypes] reverse edge ID of every edge (exclude == 2) */
+} oracle_edge_batch;
+
+/* The destination of edge `eid` of a CSC: the v with indptr[v] <= eid < indptr[v+1]. */
+int oracle_edge_dst(const int64_t *indptr, int64_t n_dst, int64_t eid, int64_t *dst);
+
+/* Negative k of target edge `eid` of `etype`: a destination uniform on
+ * [0, n_dst), floor(u * n_dst / 2^64) with u = word0 | word1 << 32 of
+ * Philox4x32-10 at counter (eid lo32, eid hi32, 2^31 | k, etype), key sigma. */
+int oracle_negative_dst(uint64_t sigma, int32_t etype, int64_t eid, int32_t k,
+                        int64_t n_dst, int64_t *v);
+
+int oracle_sample_edge_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
+                              const oracle_etype *etypes, int32_t n_etypes,
+                              const oracle_edge_batch *batch, int32_t n_hops,
+                              const int32_t *fanouts, uint64_t sigma, int32_t key_bits,
+                              oracle_blocks **out);
+
+/* Seeds of an edge-seeded result: the endpoints of node type t, ascending. */
+int oracle_blocks_seeds(const oracle_blocks *b, int32_t ntype, int64_t *n,
+                        const int64_t **gid);
+
+/* Pair graph of edge type e: target i joins seeds pos_src[i] -> pos_dst[i];
+ * negative i * n_neg + k joins pos_src[i] -> neg_dst[i * n_neg + k]. */
+int oracle_blocks_pairs(const oracle_blocks *b, int32_t etype, int64_t *n_pos,
+                        const int32_t **pos_src, const int32_t **pos_dst,
+                        int64_t *n_negs, const int32_t **neg_dst);
+
 #ifdef __cplusplus
 }
 #endif

@@ -67,11 +67,14 @@ def rr_block(seed: int, subsequence: int, counter_lo64: int) -> np.ndarray:
     return out
 
 
-def brute_select(sigma, hop, etype, lo, hi, fanout, key_bits=32):
+def brute_select(sigma, hop, etype, lo, hi, fanout, key_bits=32, excluded=None):
     """The kept edge IDs of one pair: all when deg <= K or K == -1, else the K
-    smallest by (key, eid), in ascending eid."""
+    smallest by (key, eid), in ascending eid.  Edge IDs in `excluded` take no
+    part (they are removed before counting deg)."""
     eids = np.arange(lo, hi, dtype=np.int64)
-    if fanout < 0 or hi - lo <= fanout:
+    if excluded is not None and len(excluded):
+        eids = eids[~np.isin(eids, excluded)]
+    if fanout < 0 or eids.size <= fanout:
         return eids
     keys = np.array([rr_key(sigma, hop, etype, int(x), key_bits) for x in eids], dtype=np.int64)
     order = np.lexsort((eids, keys))
@@ -127,12 +130,14 @@ def pin_select(lib, rng, n=300):
     return fails
 
 
-def check_blocks(ntypes, etypes, seeds, fanouts, sigma, key_bits, res, brute=True):
+def check_blocks(ntypes, etypes, seeds, fanouts, sigma, key_bits, res, brute=True,
+                 excluded=None):
     """Checks one mini-batch result against the definitions.
 
     ntypes: [num_nodes]; etypes: [(s, d, indptr, indices)] numpy; seeds: per
     type array or None; res: dict as returned by oracle.HostGraph.sample_blocks
-    (or the same layout from the GPU path)."""
+    (or the same layout from the GPU path); excluded: {etype: edge IDs} that
+    no hop may sample (edge-seeded mini-batches)."""
     fails = []
     T, R, H = len(ntypes), len(etypes), len(fanouts)
     F = [np.zeros(0, np.int64) if s is None else np.asarray(s, np.int64) for s in seeds]
@@ -153,10 +158,15 @@ def check_blocks(ntypes, etypes, seeds, fanouts, sigma, key_bits, res, brute=Tru
             if np.any(np.diff(ip) < 0):
                 fails.append(f"hop {h} etype {e}: decreasing block indptr")
                 continue
+            xs = None if not excluded else excluded.get(e)
+            if xs is not None and eid.size and np.any(np.isin(eid, xs)):
+                fails.append(f"hop {h} etype {e}: an excluded edge was sampled")
             for i, v in enumerate(F[d]):
                 a, b = int(ip[i]), int(ip[i + 1])
                 lo, hi = int(indptr[v]), int(indptr[v + 1])
                 deg = hi - lo
+                if xs is not None:
+                    deg -= int(np.count_nonzero((xs >= lo) & (xs < hi)))
                 want_n = deg if (k < 0 or deg <= k) else k
                 if b - a != want_n:
                     fails.append(f"hop {h} etype {e} dst {i}: {b - a} edges, want min(deg,K)={want_n}")
@@ -170,7 +180,7 @@ def check_blocks(ntypes, etypes, seeds, fanouts, sigma, key_bits, res, brute=Tru
                 if np.any(np.diff(got) <= 0):
                     fails.append(f"hop {h} etype {e} dst {i}: edge IDs not strictly ascending")
                 if brute and deg > 0:
-                    ref = brute_select(sigma, h, e, lo, hi, k, key_bits)
+                    ref = brute_select(sigma, h, e, lo, hi, k, key_bits, xs)
                     if not np.array_equal(ref, got):
                         fails.append(f"hop {h} etype {e} dst {i}: kept {got}, brute force {ref}")
             if eid.size:
@@ -333,6 +343,226 @@ def pin_statistics(lib, n_sigma=6000):
     return fails
 
 
+# ---------------------------------------------------------------------------
+# edge-seeded (link-prediction) mini-batches
+
+def np_edge_dst(indptr, eids):
+    """Destination of CSC slots: numpy's searchsorted (the last v with
+    indptr[v] <= eid)."""
+    return np.searchsorted(np.asarray(indptr), np.asarray(eids, np.int64), side="right") - 1
+
+
+def rr_negative(sigma, etype, eid, k, n):
+    """Negative k of edge eid by its definition, the two Philox words from
+    rocRAND: counter (eid, 2^31 | k, etype), words 0 and 1, then
+    floor(u * n / 2^64)."""
+    rr = rocrand_ref()
+    sub = ((0x80000000 | k) & M32) | ((etype & M32) << 32)
+    w0 = int(rr.rr_word(sigma & ((1 << 64) - 1), sub, 4 * eid))
+    w1 = int(rr.rr_word(sigma & ((1 << 64) - 1), sub, 4 * eid + 1))
+    return ((w0 | (w1 << 32)) * n) >> 64
+
+
+def with_reverses(nn, etypes):
+    """The edge types followed by their transposes, and the reverse maps:
+    rev_etype[e] and rev_eid[e][j] = slot of edge j's reverse (numpy)."""
+    R = len(etypes)
+    out = list(etypes)
+    rev_etype = [R + e for e in range(R)] + list(range(R))
+    fwd_maps, rev_maps = [], []
+    for (s, d, ip, ix) in etypes:
+        dst = np.repeat(np.arange(nn[d], dtype=np.int64), np.diff(ip))
+        order = np.lexsort((dst, ix))  # by source, then destination
+        rip = np.zeros(nn[s] + 1, np.int64)
+        np.cumsum(np.bincount(ix, minlength=nn[s]), out=rip[1:])
+        out.append((d, s, rip, dst[order]))
+        fmap = np.empty(ix.size, np.int64)
+        fmap[order] = np.arange(ix.size, dtype=np.int64)
+        fwd_maps.append(fmap)
+        rev_maps.append(order.astype(np.int64))
+    return out, rev_etype, fwd_maps + rev_maps
+
+
+def edge_batch_expect(nn, etypes, targets, n_neg, exclude, rev_etype, rev_eid, sigma):
+    """Seeds, pair graphs (as global IDs) and excluded edges of an
+    edge-seeded mini-batch, from numpy and rocRAND."""
+    T, R = len(nn), len(etypes)
+    ends = [[] for _ in range(T)]
+    pairs = {}
+    for e, (s, d, ip, ix) in enumerate(etypes):
+        tg = np.zeros(0, np.int64) if targets[e] is None else np.asarray(targets[e], np.int64)
+        src = ix[tg]
+        dst = np_edge_dst(ip, tg)
+        neg = np.array([rr_negative(sigma, e, int(j), k, nn[d]) for j in tg for k in range(n_neg)],
+                       np.int64)
+        ends[s].append(src)
+        ends[d] += [dst, neg]
+        pairs[e] = (src, dst, neg)
+    seeds = [np.unique(np.concatenate(x)) if x else np.zeros(0, np.int64) for x in ends]
+    excluded = {}
+    if exclude >= 1:
+        for e in range(R):
+            x = [np.zeros(0, np.int64) if targets[e] is None else np.asarray(targets[e], np.int64)]
+            if exclude == 2:
+                for f in range(R):
+                    if rev_etype[f] == e and targets[f] is not None:
+                        x.append(rev_eid[f][np.asarray(targets[f], np.int64)])
+            excluded[e] = np.unique(np.concatenate(x))
+    return seeds, pairs, excluded
+
+
+def check_edge_blocks(nn, etypes, targets, n_neg, exclude, rev_etype, rev_eid, fanouts, sigma,
+                      key_bits, res, brute=True):
+    """An edge-seeded result against the definitions: seeds = unique endpoints
+    per type (numpy), the pair graphs map back to the targets' endpoints and
+    negatives, and the blocks satisfy every vertex-seeded check from those
+    seeds with the excluded edges removed."""
+    fails = []
+    seeds, pairs, excluded = edge_batch_expect(nn, etypes, targets, n_neg, exclude, rev_etype,
+                                               rev_eid, sigma)
+    for t in range(len(nn)):
+        if not np.array_equal(res["seeds"][t], seeds[t]):
+            fails.append(f"type {t}: seeds {res['seeds'][t][:8]} != unique endpoints {seeds[t][:8]}")
+            return fails
+    for e, (s, d, ip, ix) in enumerate(etypes):
+        src, dst, neg = pairs[e]
+        ps, pd, pn = res["pairs"][e]
+        for name, loc, want, t in (("pos_src", ps, src, s), ("pos_dst", pd, dst, d),
+                                   ("neg_dst", pn, neg, d)):
+            if loc.size != want.size or np.any(loc < 0) or np.any(loc >= seeds[t].size) or \
+                    not np.array_equal(seeds[t][loc], want):
+                fails.append(f"etype {e}: {name} does not map back to the targets")
+    fails += check_blocks(nn, etypes, seeds, fanouts, sigma, key_bits, res, brute=brute,
+                          excluded=excluded)
+    return fails
+
+
+def random_edge_case(rng, max_nodes=30, max_deg=15):
+    nn, ets, feats = workloads.random_hetero(rng, max_nodes=max_nodes, max_deg=max_deg,
+                                             max_etypes=3)
+    ets, rev_etype, rev_eid = with_reverses(nn, ets)
+    R = len(ets)
+    targets = []
+    for e in range(R):
+        nnz = ets[e][3].size
+        if nnz == 0 or rng.random() < 0.3:
+            targets.append(None)
+        else:
+            targets.append(rng.integers(0, nnz, size=int(rng.integers(1, 6))).astype(np.int64))
+    H = int(rng.integers(0, 3))
+    fchoices = [-1, 0, 1, 2, 3, 5]
+    fanouts = [[fchoices[int(rng.integers(0, len(fchoices)))] for _ in range(R)] for _ in range(H)]
+    sigma = int(rng.integers(0, 1 << 63))
+    bits = 32 if rng.random() < 0.7 else int(rng.integers(1, 5))
+    n_neg = int(rng.choice([0, 1, 3]))
+    exclude = int(rng.integers(0, 3))
+    return nn, ets, feats, targets, n_neg, exclude, rev_etype, rev_eid, fanouts, sigma, bits
+
+
+def pin_edge_dst(lib, rng, n=40):
+    fails = []
+    for c in range(n):
+        deg = rng.integers(0, 5, size=int(rng.integers(1, 30)))
+        deg[rng.random(deg.size) < 0.3] = 0
+        ip = np.concatenate([[0], np.cumsum(deg)]).astype(np.int64)
+        for j in range(int(ip[-1])):
+            got = oracle.edge_dst(ip, j, lib)
+            if got != int(np_edge_dst(ip, [j])[0]):
+                fails.append(f"edge_dst case {c} eid {j}: {got}")
+    return fails
+
+
+def pin_negatives(lib, rng, n=200):
+    fails = []
+    for i in range(n):
+        sigma = int(rng.integers(0, 1 << 63)) * 2 + int(rng.integers(0, 2))
+        e, k = int(rng.integers(0, 300)), int(rng.integers(0, oracle.MAX_NEG))
+        eid = int(rng.integers(0, 1 << 40)) if i % 2 else int(rng.integers(0, 64))
+        nd = [1, 2, 7, 1000, 60_000_000, (1 << 40) + 3][i % 6]
+        want = rr_negative(sigma, e, eid, k, nd)
+        got = oracle.negative_dst(sigma, e, eid, k, nd, lib)
+        if got != want:
+            fails.append(f"negative({sigma},{e},{eid},{k},{nd}) = {got} != {want}")
+    return fails
+
+
+def pin_edge_blocks(lib, rng, n=40):
+    fails = []
+    for c in range(n):
+        nn, ets, feats, tg, q, x, rev_et, rev_eid, fanouts, sigma, bits = random_edge_case(rng)
+        hg = oracle.HostGraph(list(zip(nn, feats)), ets, lib=lib)
+        res = hg.sample_edge_blocks(tg, fanouts, sigma, n_neg=q, exclude=x, rev_etype=rev_et,
+                                    rev_eid=rev_eid, key_bits=bits)
+        f = check_edge_blocks(nn, ets, tg, q, x, rev_et, rev_eid, fanouts, sigma, bits, res)
+        fails += [f"edge case {c} (exclude {x}, neg {q}): {m}" for m in f[:3]]
+    return fails
+
+
+def pin_edge_errors(lib):
+    fails = []
+    nn = [3]
+    ets = [(0, 0, np.array([0, 1, 3, 3], np.int64), np.array([2, 0, 1], np.int64))]
+    ets, rev_et, rev_eid = with_reverses(nn, ets)
+    hg = oracle.HostGraph([(3, None)], ets, lib=lib)
+
+    def expect(fn):
+        try:
+            fn()
+        except oracle.OracleError as ex:
+            if ex.status != oracle.EINVAL:
+                fails.append(f"expected EINVAL, got {ex.status}")
+            return
+        fails.append("expected EINVAL, call succeeded")
+
+    ok = [np.array([1]), None]
+    expect(lambda: hg.sample_edge_blocks([np.array([3]), None], [[1, 1]], 0))
+    expect(lambda: hg.sample_edge_blocks([np.array([-1]), None], [[1, 1]], 0))
+    expect(lambda: hg.sample_edge_blocks(ok, [[1, 1]], 0, n_neg=oracle.MAX_NEG + 1))
+    expect(lambda: hg.sample_edge_blocks(ok, [[1, 1]], 0, exclude=3))
+    expect(lambda: hg.sample_edge_blocks(ok, [[1, 1]], 0, exclude=2))
+    bad = [rev_eid[0].copy(), rev_eid[1]]
+    bad[0][1] = (bad[0][1] + 1) % 3  # the reverse of edge 1 named wrongly
+    expect(lambda: hg.sample_edge_blocks(ok, [[1, 1]], 0, exclude=2, rev_etype=rev_et,
+                                         rev_eid=bad))
+    r = hg.sample_edge_blocks(ok, [[1, 1]], 0, exclude=2, rev_etype=rev_et, rev_eid=rev_eid)
+    if not np.array_equal(r["seeds"][0], [0, 1]):
+        fails.append(f"seeds of target edge 1 (0 -> 1): {r['seeds'][0]}")
+    # a reverse edge type must run between the same node types the other way
+    ets2 = [(0, 1, np.array([0, 1, 2], np.int64), np.array([0, 1], np.int64)),
+            (0, 1, np.array([0, 1, 2], np.int64), np.array([1, 0], np.int64))]
+    hg2 = oracle.HostGraph([(2, None), (2, None)], ets2, lib=lib)
+    ident = [np.array([0, 1], np.int64), np.array([0, 1], np.int64)]
+    expect(lambda: hg2.sample_edge_blocks([np.array([0]), None], [[1, 1]], 0, exclude=2,
+                                          rev_etype=[1, 0], rev_eid=ident))
+    # no hops: the input frontier is the seeds
+    r = hg.sample_edge_blocks(ok, [], 0)
+    if not np.array_equal(r["input"][0], [0, 1]):
+        fails.append("n_hops = 0: input frontier is not the seeds")
+    return fails
+
+
+def pin_negative_uniformity(lib, n=6000):
+    """Negatives are uniform on the destination type (chi-squared) and the
+    draws for different k are independent."""
+    fails = []
+    nd = 7
+    counts = np.zeros(nd)
+    same = 0
+    for eid in range(n):
+        a = oracle.negative_dst(11, 2, eid, 0, nd, lib)
+        b = oracle.negative_dst(11, 2, eid, 1, nd, lib)
+        counts[a] += 1
+        same += a == b
+    exp = n / nd
+    x2 = float(((counts - exp) ** 2 / exp).sum())
+    p = chi2_sf(x2, nd - 1)
+    if p < 1e-3:
+        fails.append(f"negative destinations not uniform: chi2={x2:.1f}, p={p:.2g}")
+    if abs(same / n - 1 / nd) > 0.02:
+        fails.append(f"negatives 0 and 1 agree {same / n:.3f}, independent draws {1 / nd:.3f}")
+    return fails
+
+
 ALL_PINS = {
     "philox": pin_philox,
     "edge_key": pin_edge_key,
@@ -341,4 +571,8 @@ ALL_PINS = {
     "blocks": pin_blocks,
     "gather": lambda lib, rng: pin_gather(lib, rng),
     "errors": lambda lib, rng: pin_errors(lib),
+    "edge_dst": pin_edge_dst,
+    "negatives": pin_negatives,
+    "edge_blocks": pin_edge_blocks,
+    "edge_errors": lambda lib, rng: pin_edge_errors(lib),
 }

@@ -32,8 +32,8 @@ MUTANTS = [
      "for (int64_t j = 0; j < fanout; ++j) out_eids[j] = all[deg - 1 - j].eid;"),
     ("kept edges left in key order", "qsort(out_eids, (size_t)fanout, sizeof(int64_t), cmp_i64);", ""),
     ("hop index shifted in sampling",
-     "status = oracle_select(sigma, h, e, lo, hi, k, key_bits, chosen, &nc);",
-     "status = oracle_select(sigma, h + 1, e, lo, hi, k, key_bits, chosen, &nc);"),
+     "status = select_pair(sigma, h, e, lo, hi, k, key_bits, excl[e].eids,",
+     "status = select_pair(sigma, h + 1, e, lo, hi, k, key_bits, excl[e].eids,"),
     ("frontier not removed from new vertices",
      "if (find_gid_pos(ftab[t], fn[t], srcs[j]) >= 0) continue;", ""),
     ("new vertices left unsorted",
@@ -46,6 +46,24 @@ MUTANTS = [
     ("repeated seeds accepted", "if (i > 0 && tmp[i] == tmp[i - 1]) bad = 1;", ""),
     ("gather reads the mirrored row", "(const char *)feat + ids[i] * row_bytes",
      "(const char *)feat + ids[n - 1 - i] * row_bytes"),
+    # edge-seeded mini-batches
+    ("excluded edges still sampled",
+     "if (nx == 0 || find_sorted(xs, nx, j) < 0) out_eids[deg++] = j;", "out_eids[deg++] = j;"),
+    ("reverse edges not excluded",
+     "excl[e].eids[m++] = batch->rev_eid[f][batch->eids[f][i]];", "(void)f;"),
+    ("edge destination one slot late", "if (indptr[m] <= eid)", "if (indptr[m] < eid)"),
+    ("negative from the wrong word",
+     "uint64_t u = (uint64_t)out[0] | ((uint64_t)out[1] << 32);",
+     "uint64_t u = (uint64_t)out[0] | ((uint64_t)out[2] << 32);"),
+    ("negatives share the sampling counters", "0x80000000u | (uint32_t)k,", "(uint32_t)k,"),
+    ("seeds not deduplicated", "if (a[i] != a[u - 1]) a[u++] = a[i];", "a[u++] = a[i];"),
+    ("negative destinations left out of the seeds",
+     "for (int64_t i = 0; i < n * Q; ++i) all[m++] = neg[e][i];", ""),
+    ("pair source looked up among the destination type's seeds",
+     "b->pos_src[e][i] = (int32_t)find_sorted(b->seed_gid[s], b->seed_n[s], src[e][i]);",
+     "b->pos_src[e][i] = (int32_t)find_sorted(b->seed_gid[d], b->seed_n[d], src[e][i]);"),
+    ("reverse edge not checked against the target",
+     "if (etypes[r].indices[rj] != v || rv != et->indices[j]) return ORACLE_EINVAL;", ""),
 ]
 
 
@@ -59,6 +77,10 @@ def fast_pins(lib):
     fails += pins.pin_blocks(lib, rng, n=15)
     fails += pins.pin_gather(lib, rng, n=8)
     fails += pins.pin_errors(lib)
+    fails += pins.pin_edge_dst(lib, rng, n=10)
+    fails += pins.pin_negatives(lib, rng, n=30)
+    fails += pins.pin_edge_blocks(lib, rng, n=25)
+    fails += pins.pin_edge_errors(lib)
     return fails
 
 

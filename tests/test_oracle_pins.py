@@ -23,6 +23,11 @@ def test_statistics(lib):
     assert not fails, "\n".join(fails)
 
 
+def test_negative_statistics(lib):
+    fails = pins.pin_negative_uniformity(lib)
+    assert not fails, "\n".join(fails)
+
+
 def test_philox_zero_counter_known_answer(lib):
     # Philox4x32-10 with zero counter and zero key, from rocRAND's engine.
     ref = pins.rr_block(0, 0, 0)
