@@ -287,6 +287,64 @@ hg_status hg_pipeline_next(hg_pipeline *pipe, hg_blocks **out);
  * workers and releases the streams. */
 void hg_pipeline_destroy(hg_pipeline *pipe);
 
+/* ---- Edge-seeded mini-batches (link prediction) ----------------------------
+ * DistDGLv2's scheduler picks target vertices or target edges per mini-batch
+ * (Sec. 4.2.1), and the same sampling decomposition runs from either (Sec.
+ * 4.2.2).  From target edges:
+ *  - a target is an edge ID (CSC slot) of an edge type; targets may repeat;
+ *  - its endpoints are indices[eid] (source) and the destination v with
+ *    indptr[v] <= eid < indptr[v+1];
+ *  - n_neg negatives per target keep its source and take a destination
+ *    uniform over the destination type: floor(u * n / 2^64), u = word0 |
+ *    word1 << 32 of Philox4x32-10 at counter (eid lo32, eid hi32, 2^31 | k,
+ *    etype) under key (rng_seed lo32, rng_seed hi32), k = 0 .. n_neg-1;
+ *  - the seeds of a node type are its endpoints and negative destinations,
+ *    each once, in ascending ID; the hops then run from them as in
+ *    hg_sample_blocks;
+ *  - exclusion removes edges from every hop's sampling: HG_EXCLUDE_SELF the
+ *    targets, HG_EXCLUDE_REVERSE also each target's reverse edge
+ *    rev_eid[e][eid] of type rev_etype[e] (which must run from the target's
+ *    destination back to its source).  A pair keeps all its remaining
+ *    in-edges when at most K remain, else the K remaining ones with the
+ *    smallest (key, edge ID); keys are those of hg_sample_blocks. */
+#define HG_MAX_NEG 64
+#define HG_EXCLUDE_NONE 0
+#define HG_EXCLUDE_SELF 1
+#define HG_EXCLUDE_REVERSE 2
+
+typedef struct hg_edge_batch {
+  const int64_t *const *eids;    /* host array [n_etypes] of device int64 target IDs (NULL if none) */
+  const int64_t *n_eids;         /* host int64 [n_etypes] */
+  int32_t n_neg;                 /* negatives per target, 0 .. HG_MAX_NEG */
+  int32_t exclude;               /* HG_EXCLUDE_* */
+  const int32_t *rev_etype;      /* host int32 [n_etypes], -1 = no reverse (HG_EXCLUDE_REVERSE) */
+  const int64_t *const *rev_eid; /* host array [n_etypes] of device int64 [nnz] (HG_EXCLUDE_REVERSE) */
+} hg_edge_batch;
+
+/* One edge-seeded mini-batch with its input features (gather_ntypes as in
+ * hg_sample_blocks_gather).  HG_EINVAL for a bad argument, a target out of
+ * range or a reverse edge that does not run back along its target; else as
+ * hg_sample_blocks.  The target and reverse arrays are read on `stream`. */
+hg_status hg_sample_edge_blocks(hg_graph *graph, const hg_edge_batch *batch, int32_t n_hops,
+                                const int32_t *fanouts, uint64_t rng_seed,
+                                const int32_t *gather_ntypes, int32_t n_gather,
+                                hipStream_t stream, hg_blocks **out);
+
+/* The seeds of node type `ntype` (device int64 [n], owned by the handle): for
+ * an edge-seeded batch its endpoints in ascending ID; otherwise the hop-0
+ * frontier (the given seeds). */
+hg_status hg_blocks_seeds(const hg_blocks *blocks, int32_t ntype, int64_t *n,
+                          const int64_t **gid);
+
+/* The pair graph of edge type `etype` of an edge-seeded batch, as local IDs
+ * among the seeds (device int32, owned by the handle): target i joins
+ * pos_src[i] -> pos_dst[i] (i < n_pos, in target order); negative
+ * i * n_neg + k joins pos_src[i] -> neg_dst[i * n_neg + k] (n_negs = n_pos *
+ * n_neg).  HG_EINVAL for a vertex-seeded batch. */
+hg_status hg_blocks_edge_pairs(const hg_blocks *blocks, int32_t etype, int64_t *n_pos,
+                               const int32_t **pos_src, const int32_t **pos_dst,
+                               int64_t *n_negs, const int32_t **neg_dst);
+
 /* Thread-local description of the last failure on this thread. */
 const char *hg_last_error(void);
 

@@ -38,8 +38,12 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_sample_blocks_gather", "hg_sample_blocks_bundle", "hg_blocks_features",
                "hg_graph_types",
                "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
-               "hg_pipeline_destroy",
+               "hg_pipeline_destroy", "hg_sample_edge_blocks", "hg_blocks_seeds",
+               "hg_blocks_edge_pairs",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
+
+HG_MAX_NEG = 64
+HG_EXCLUDE_NONE, HG_EXCLUDE_SELF, HG_EXCLUDE_REVERSE = 0, 1, 2
 
 
 class HGError(RuntimeError):
@@ -57,6 +61,12 @@ class ETypeDesc(ctypes.Structure):
     _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
                 ("nnz", ctypes.c_int64), ("indptr", ctypes.c_void_p),
                 ("indices", ctypes.c_void_p)]
+
+
+class EdgeBatch(ctypes.Structure):
+    _fields_ = [("eids", ctypes.c_void_p), ("n_eids", ctypes.c_void_p),
+                ("n_neg", ctypes.c_int32), ("exclude", ctypes.c_int32),
+                ("rev_etype", ctypes.c_void_p), ("rev_eid", ctypes.c_void_p)]
 
 
 ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
@@ -101,6 +111,9 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_free": ([_P], None),
         "hg_last_error": ([], ctypes.c_char_p),
         "hg_debug_philox": ([_P, ctypes.c_uint64, _I64, _P, _P], _I32),
+        "hg_sample_edge_blocks": ([_P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
+        "hg_blocks_seeds": ([_P, _I32, _PI64, _PP], _I32),
+        "hg_blocks_edge_pairs": ([_P, _I32, _PI64, _PP, _PP, _PI64, _PP], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -229,6 +242,25 @@ class Blocks:
         n = _I64()
         _check(load_library().hg_blocks_input_nodes(self._h, ntype, ctypes.byref(n), None))
         return n.value
+
+    def seeds(self, ntype: int) -> torch.Tensor:
+        """The seeds of `ntype`: an edge-seeded batch's endpoints in ascending
+        ID, or the given seeds of a vertex-seeded one."""
+        n, p = _I64(), ctypes.c_void_p()
+        _check(load_library().hg_blocks_seeds(self._h, ntype, ctypes.byref(n), ctypes.byref(p)))
+        return _view(p.value, n.value, torch.int64, self, self.device)
+
+    def edge_pairs(self, etype: int):
+        """(pos_src, pos_dst, neg_dst) of an edge-seeded batch: local IDs among
+        the seeds; negative i * n_neg + k has source pos_src[i]."""
+        npos, nneg = _I64(), _I64()
+        ps, pd, pn = (ctypes.c_void_p() for _ in range(3))
+        _check(load_library().hg_blocks_edge_pairs(self._h, etype, ctypes.byref(npos),
+                                                   ctypes.byref(ps), ctypes.byref(pd),
+                                                   ctypes.byref(nneg), ctypes.byref(pn)))
+        return (_view(ps.value, npos.value, torch.int32, self, self.device),
+                _view(pd.value, npos.value, torch.int32, self, self.device),
+                _view(pn.value, nneg.value, torch.int32, self, self.device))
 
 
 class Graph:
@@ -371,6 +403,64 @@ class Graph:
         _check(lib.hg_sample_blocks_bundle(self._h, B, ptrs, counts, H, fo, sg, gt, len(gather),
                                            start, stop, _stream(stream), hs))
         return [Blocks(self, ctypes.c_void_p(hs[b]), H) for b in range(B)]
+
+    def sample_edge_blocks(self, targets, fanouts, rng_seed: int = 0, n_neg: int = 0,
+                           exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None,
+                           gather=None, stream=None) -> Blocks:
+        """An edge-seeded mini-batch (link prediction): targets per edge type an
+        int64 device tensor of edge IDs or None; n_neg negatives per target;
+        exclude HG_EXCLUDE_NONE / _SELF / _REVERSE, the last with rev_etype
+        (per edge type its reverse type or -1) and rev_eid (per edge type an
+        int64 device tensor [nnz] or None).  gather as in sample_blocks."""
+        lib = load_library()
+        T, R = self.T, self.R
+        if len(targets) != R:
+            raise ValueError("one target entry per edge type")
+        keep = []
+        tptr = (ctypes.c_void_p * max(R, 1))()
+        tcnt = (ctypes.c_int64 * max(R, 1))()
+        for e, x in enumerate(targets):
+            if x is None:
+                continue
+            x = _dev_i64(x, self.device)
+            keep.append(x)
+            tcnt[e] = x.numel()
+            tptr[e] = x.data_ptr() if x.numel() else None
+        rv = None
+        rptr = None
+        if rev_etype is not None:
+            rv = (ctypes.c_int32 * max(R, 1))(*[int(r) for r in rev_etype])
+        if rev_eid is not None:
+            rptr = (ctypes.c_void_p * max(R, 1))()
+            for e, x in enumerate(rev_eid):
+                if x is None:
+                    continue
+                x = _dev_i64(x, self.device)
+                keep.append(x)
+                rptr[e] = x.data_ptr() if x.numel() else None
+        batch = EdgeBatch(ctypes.addressof(tptr), ctypes.addressof(tcnt), int(n_neg),
+                          int(exclude), ctypes.addressof(rv) if rv is not None else None,
+                          ctypes.addressof(rptr) if rptr is not None else None)
+        H = len(fanouts)
+        flat = [int(k) for row in fanouts for k in row]
+        if len(flat) != H * R:
+            raise ValueError("fanouts must be [n_hops][n_etypes]")
+        fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        if isinstance(gather, str):
+            if gather != "all":
+                raise ValueError('gather must be None, "all" or a list of node types')
+            gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
+        gather = list(gather or [])
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
+        h = ctypes.c_void_p()
+        st = lib.hg_sample_edge_blocks(self._h, ctypes.addressof(batch), H, fo,
+                                       int(rng_seed) & (2**64 - 1), gt, len(gather),
+                                       _stream(stream), ctypes.byref(h))
+        # the call waits on the stream before it returns, so the target
+        # tensors are read by then
+        del keep
+        _check(st)
+        return Blocks(self, h, H)
 
     def gather_features(self, blocks: Blocks, ntype: int, out: torch.Tensor | None = None,
                         stream=None) -> torch.Tensor:

@@ -56,6 +56,7 @@ constexpr int32_t kErrSeedRange = 1;   // a frontier vertex out of range
 constexpr int32_t kErrSeedRepeat = 2;  // a vertex twice in a frontier
 constexpr int32_t kErrLookback = 4;    // a scan wait exceeded its bound
 constexpr int32_t kErrBound = 8;       // more pairs or chunks than buffers were sized for
+constexpr int32_t kErrTarget = 16;     // a target edge out of range, or a bad reverse edge
 
 // Static per edge type (per workspace).
 struct EtypeStatic {
@@ -94,6 +95,26 @@ struct Lookback {
   uint64_t *word;
 };
 constexpr uint32_t kEpochLimit = 1u << 20;
+
+// Edges that no hop may sample (an edge-seeded mini-batch with exclusion), as
+// two open-addressing hash tables with linear probing: the excluded edges,
+// keyed (etype << 32 | eid), and per pair with excluded in-edges its count,
+// keyed (etype << 32 | destination local ID).  Every excluded edge ends at a
+// seed, and the seeds are the first local IDs of every hop's frontier, so
+// only pairs whose destination local ID is below n_seed[etype] are looked up.
+// edge_keys == nullptr: nothing is excluded.
+constexpr uint64_t kHashEmpty = ~uint64_t(0);
+struct ExclView {
+  const uint64_t *edge_keys;  // [edge_mask + 1]
+  const uint64_t *pair_keys;  // [pair_mask + 1]
+  const int32_t *pair_cnt;    // [pair_mask + 1]
+  const int64_t *n_seed;      // [R] seeds of each etype's destination type
+  uint32_t edge_mask, pair_mask;
+};
+
+__host__ __device__ inline uint32_t hash_slot(uint64_t key, uint32_t mask) {
+  return uint32_t((key * 0x9E3779B97F4A7C15ull) >> 32) & mask;
+}
 
 // Per-pair arrays of one hop (device), n_items entries each.
 struct PairArrays {
@@ -137,7 +158,7 @@ int64_t count_tiles(int64_t n_items);
 hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                              int32_t n_types, int64_t n_items, PairArrays pa,
                              Lookback lb, uint32_t epoch, uint64_t ticket_base,
-                             int64_t *small, hipStream_t stream);
+                             ExclView X, int64_t *small, hipStream_t stream);
 
 // The sampler, two launches.  First: block CSC entries and small take-all
 // pairs (a wavefront per 64 pairs), wavefront pairs (one wavefront each) and
@@ -155,7 +176,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t key_R, int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
-                         hipStream_t stream);
+                         ExclView X, hipStream_t stream);
 
 // Sets the bitmap bit of every kept edge's source that is not in the
 // frontier of its type yet (edges of etype e are [ebase[e], ebase[e+1]),
@@ -226,6 +247,44 @@ struct GatherJob {
 // NULL) are recorded by the batched launches themselves.
 hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_t stream,
                                hipEvent_t start, hipEvent_t stop);
+
+// ---- edge-seeded mini-batches (hg_edges.hip) --------------------------------
+
+// Per edge type of an edge-seeded call (device table).
+struct EdgeEtype {
+  const int64_t *eids;     // target edge IDs
+  const int64_t *rev_eid;  // reverse edge ID of every edge (exclusion 2), or NULL
+  int64_t nnz;
+  int32_t rev;             // reverse edge type, or -1
+};
+
+struct EdgeBatchArgs {
+  const EtypeStatic *es;
+  const TypeStatic *ts;
+  const EdgeEtype *et;     // [n_etypes]
+  const int64_t *tbase;    // [n_etypes + 1] prefix of target counts
+  int32_t n_etypes, n_types;
+  int64_t n_targets;
+  int32_t n_neg, exclude;
+  uint64_t sigma;
+  int64_t *tsrc, *tdst;    // [n_targets] endpoints (-1 for an invalid target)
+  int64_t *tneg;           // [n_targets * n_neg]
+  int64_t *trev;           // [n_targets] reverse edge ID (exclusion 2), -1 when none
+  int32_t *pos_src, *pos_dst, *neg_dst;  // pair graphs, target order
+  uint64_t *edge_keys, *pair_keys;
+  int32_t *pair_cnt;
+  int64_t *n_seed;         // [n_etypes]
+  uint32_t edge_mask, pair_mask;
+  int64_t *small;
+};
+
+// Endpoints and negatives of every target; sets their bitmap bits (the seeds,
+// ranked by the compaction pass); flags bad targets and reverse edges.
+hipError_t launch_edge_targets(const EdgeBatchArgs &A, hipStream_t stream);
+// After the compaction of the seeds: the pair graphs' local IDs, the
+// exclusion tables, and hop 0's frontier sizes and pair layout (`first`).
+hipError_t launch_edge_relabel(const EdgeBatchArgs &A, HopView first,
+                               const int64_t *tile_base, hipStream_t stream);
 
 // Philox4x32-10 on n counters.
 hipError_t launch_philox(const uint32_t *ctr, uint64_t key, int64_t n,

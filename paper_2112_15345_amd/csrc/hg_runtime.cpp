@@ -133,6 +133,7 @@ struct Workspace {
   char *htab = nullptr;            // per-hop tables (pinned host)
   size_t htab_cap = 0;
   Scratch pairs, lb_pairs, edges, cand;
+  Scratch targets;                 // edge-seeded calls: endpoints and exclusion tables
   uint32_t epoch = 0;              // look-back launches so far (mod kEpochLimit)
   hipEvent_t done = nullptr;
   bool busy = false;
@@ -196,6 +197,13 @@ struct hg_blocks {
   std::vector<int64_t> in_n;          // [T]
   std::vector<const int64_t *> in_gid;
   std::vector<void *> feat;           // [T] gathered rows (hg_sample_blocks_gather), or NULL
+  // edge-seeded mini-batches (hg_sample_edge_blocks)
+  bool edge_seeded = false;
+  int32_t n_neg = 0;
+  std::vector<int64_t> seed_n;        // [T]
+  std::vector<const int64_t *> seed_gid;
+  std::vector<int64_t> pair_n;        // [R]
+  std::vector<const int32_t *> pos_src, pos_dst, neg_dst;
   std::shared_ptr<OutAllocs> mem;     // the arrays above
 };
 
@@ -309,6 +317,7 @@ void free_workspace(Workspace *w) {
   w->lb_pairs.release();
   w->edges.release();
   w->cand.release();
+  w->targets.release();
   if (w->hsmall) (void)hipHostFree(w->hsmall);
   if (w->htab) (void)hipHostFree(w->htab);
   delete w;
@@ -464,13 +473,26 @@ struct SampleRun {
   int64_t map_bound = 0;
   bool bitmap_dirty = false;
 
+  // an edge-seeded call: its batch, the excluded edges and its extra tables
+  // (a region for the seeds' compaction after regions 0 .. H+1, then the
+  // per-etype target table)
+  const hg_edge_batch *eb = nullptr;
+  ExclView X{};
+  size_t edge_tab = 0;  // bytes of the per-etype target table
+
   SampleRun(hg_graph *g_, hipStream_t s, int32_t H_, const int32_t *fo,
             const uint64_t *sig, int32_t n_sig, int32_t kb)
       : g(g_), stream(s), T(g_->T), R(g_->R), H(H_), sigmas(sig, sig + n_sig), key_bits(kb),
         fanouts(fo), lay(g_->T, g_->R), sig_bytes(align_up(sizeof(uint64_t) * size_t(n_sig))) {}
 
-  // table bytes of a call: the sigma table, then regions 0 .. H+1
-  size_t table_bytes() const { return sig_bytes + lay.size * size_t(H + 2); }
+  // table bytes of a call: the sigma table, then regions 0 .. H+1 (and for an
+  // edge-seeded call the seeds' region H+2 and the target table)
+  int32_t n_regions() const { return H + 2 + (eb ? 1 : 0); }
+  size_t table_bytes() const {
+    return sig_bytes + lay.size * size_t(n_regions()) + edge_tab;
+  }
+  char *hedge() { return hreg(n_regions()); }
+  char *dedge() { return dreg(n_regions()); }
   char *hreg(int r) { return ws->htab + sig_bytes + size_t(r) * lay.size; }
   char *dreg(int r) {
     return static_cast<char *>(ws->tab.p) + sig_bytes + size_t(r) * lay.size;
@@ -543,6 +565,9 @@ struct SampleRun {
     const int32_t err = int32_t(ws->hsmall[kSlotErr]);
     if (err & (kErrSeedRange | kErrSeedRepeat))
       return fail(HG_EINVAL, "seeds: out of range or repeated within a node type");
+    if (err & kErrTarget)
+      return fail(HG_EINVAL, "target edges: an edge ID out of range, or a reverse edge that "
+                             "does not run back along its target");
     if (err) {
       ws->poisoned = true;
       return fail(HG_EDEVICE, "%s: device check failed (flags %d)", where, err);
@@ -575,11 +600,13 @@ struct SampleRun {
     return fail_hip(e, what);
   }
 
+  void init_blocks();
   hg_status run(const int64_t *const *seeds, const int64_t *n_seeds);
+  hg_status run_edges();
+  hg_status hops(std::vector<int64_t> &nF, int64_t n_items);
 };
 
-hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
-  hipError_t e;
+void SampleRun::init_blocks() {
   b->g = g;
   b->stream = stream;
   b->mem = std::make_shared<OutAllocs>();
@@ -601,6 +628,11 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
   b->in_n.assign(T, 0);
   b->in_gid.assign(T, nullptr);
   b->feat.assign(T, nullptr);
+}
+
+hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
+  hipError_t e;
+  init_blocks();
 
   // ---- region 0: the seeds are the first frontier -------------------------
   std::vector<int64_t> nF(T);
@@ -640,8 +672,179 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
     hg_status st = check_flags("seeds");
     if (st != HG_OK) return st;
+    Carve a;
+    std::vector<int64_t *> cp(T, nullptr);
+    for (int32_t t = 0; t < T; ++t) a.add(&cp[t], nF[t]);
+    void *base = a.allocate(g, stream);
+    if (!base) return fail(HG_ENOMEM, "seed copy");
+    b->mem->ptrs.push_back(base);
+    for (int32_t t = 0; t < T; ++t) {
+      if (nF[t] > 0 &&
+          (e = hipMemcpyAsync(cp[t], seeds[t], sizeof(int64_t) * size_t(nF[t]),
+                              hipMemcpyDeviceToDevice, stream)) != hipSuccess)
+        return fail_device(e, "seed copy");
+      b->in_n[t] = nF[t];
+      b->in_gid[t] = cp[t];
+    }
+    return HG_OK;
+  }
+  return hops(nF, n_items);
+}
+
+// An edge-seeded call: the targets' endpoints become the seeds (ranked by the
+// compaction pass from an empty frontier, in region H+2), then the hops run
+// from them with the excluded edges left out.
+hg_status SampleRun::run_edges() {
+  hipError_t e;
+  init_blocks();
+  const int32_t Q = eb->n_neg;
+  std::vector<int64_t> tbase(R + 1, 0);
+  for (int32_t i = 0; i < R; ++i) tbase[i + 1] = tbase[i] + eb->n_eids[i];
+  const int64_t N = tbase[R];
+  // seeds of a type: at most its vertices, and at most its endpoints
+  std::vector<int64_t> bound(T, 0);
+  for (int32_t i = 0; i < R; ++i) {
+    bound[g->et[i].src] += eb->n_eids[i];
+    bound[g->et[i].dst] += eb->n_eids[i] * (1 + Q);
+  }
+  for (int32_t t = 0; t < T; ++t) bound[t] = std::min(bound[t], g->nt[t].num_nodes);
+
+  // ---- outputs: the seeds and the pair graphs -------------------------------
+  Carve oc;
+  std::vector<int64_t *> seeds(T, nullptr);
+  int32_t *pos_src, *pos_dst, *neg_dst;
+  for (int32_t t = 0; t < T; ++t) oc.add(&seeds[t], bound[t]);
+  oc.add(&pos_src, N);
+  oc.add(&pos_dst, N);
+  oc.add(&neg_dst, N * Q);
+  void *ob = oc.allocate(g, stream);
+  if (!ob) return fail(HG_ENOMEM, "edge batch: seed and pair arrays");
+  b->mem->ptrs.push_back(ob);
+  b->edge_seeded = true;
+  b->n_neg = Q;
+  b->seed_n.assign(T, 0);
+  b->seed_gid.assign(seeds.begin(), seeds.end());
+  b->pair_n.assign(eb->n_eids, eb->n_eids + R);
+  b->pos_src.resize(R);
+  b->pos_dst.resize(R);
+  b->neg_dst.resize(R);
+  for (int32_t i = 0; i < R; ++i) {
+    b->pos_src[i] = pos_src + tbase[i];
+    b->pos_dst[i] = pos_dst + tbase[i];
+    b->neg_dst[i] = neg_dst + tbase[i] * Q;
   }
 
+  // ---- scratch: endpoints, negatives, reverse edges, exclusion tables ---------
+  const int64_t n_x = eb->exclude == 0 ? 0 : N * (eb->exclude == 2 ? 2 : 1);
+  uint64_t cap = 64;
+  while (cap < uint64_t(2 * n_x)) cap <<= 1;  // always an empty slot
+  if (cap > (uint64_t(1) << 31)) return fail(HG_EUNSUPPORTED, "edge batch: too many targets");
+  Carve sc;
+  EdgeBatchArgs A{};
+  sc.add(&A.tsrc, N);
+  sc.add(&A.tdst, N);
+  sc.add(&A.trev, N);
+  sc.add(&A.tneg, N * Q);
+  sc.add(&A.edge_keys, int64_t(cap));
+  sc.add(&A.pair_keys, int64_t(cap));
+  sc.add(&A.pair_cnt, int64_t(cap));
+  sc.add(&A.n_seed, R);
+  if (!sc.in_scratch(ws->targets, stream)) return fail(HG_ENOMEM, "edge batch: scratch");
+
+  // ---- tables: regions 0 .. H+1, the seeds' region H+2, the target table -----
+  const int32_t pre = H + 2;
+  for (int32_t r = 0; r <= pre; ++r) {
+    for (int32_t i = 0; i < R; ++i)
+      hfield<int32_t>(r, lay.fanout)[i] = r < H ? fanouts[size_t(r) * R + i] : 0;
+    for (int32_t t = 0; t < T; ++t) {
+      hfield<int64_t *>(r, lay.src_out)[t] = r == pre ? seeds[t] : nullptr;
+      hfield<const int64_t *>(r, lay.frontier)[t] = r == 0 ? seeds[t] : nullptr;
+      hfield<int64_t>(r, lay.nf)[t] = 0;  // region 0's are written by the device
+    }
+  }
+  int64_t *h_tbase = reinterpret_cast<int64_t *>(hedge());
+  EdgeEtype *h_et = reinterpret_cast<EdgeEtype *>(hedge() + align_up(sizeof(int64_t) * (R + 1)));
+  for (int32_t i = 0; i <= R; ++i) h_tbase[i] = tbase[i];
+  for (int32_t i = 0; i < R; ++i) {
+    const bool rev = eb->exclude == 2 && eb->rev_etype && eb->rev_etype[i] >= 0;
+    h_et[i] = EdgeEtype{eb->n_eids[i] > 0 ? eb->eids[i] : nullptr,
+                        rev ? eb->rev_eid[i] : nullptr, g->et[i].nnz,
+                        rev ? eb->rev_etype[i] : -1};
+  }
+  std::memcpy(ws->htab, sigmas.data(), sizeof(uint64_t) * sigmas.size());
+  if ((e = upload(0, table_bytes())) != hipSuccess) return fail_device(e, "start");
+
+  A.es = ws->d_es;
+  A.ts = ws->d_ts;
+  A.tbase = reinterpret_cast<const int64_t *>(dedge());
+  A.et = reinterpret_cast<const EdgeEtype *>(dedge() + align_up(sizeof(int64_t) * (R + 1)));
+  A.n_etypes = R;
+  A.n_types = T;
+  A.n_targets = N;
+  A.n_neg = Q;
+  A.exclude = eb->exclude;
+  A.sigma = sigmas[0];
+  A.pos_src = pos_src;
+  A.pos_dst = pos_dst;
+  A.neg_dst = neg_dst;
+  A.edge_mask = A.pair_mask = uint32_t(cap - 1);
+  A.small = ws->dsmall;
+  if (eb->exclude >= 1) {
+    if ((e = launch_fill_u32(reinterpret_cast<uint32_t *>(A.edge_keys), 2 * int64_t(cap),
+                             0xFFFFFFFFu, stream)) != hipSuccess ||
+        (e = launch_fill_u32(reinterpret_cast<uint32_t *>(A.pair_keys), 2 * int64_t(cap),
+                             0xFFFFFFFFu, stream)) != hipSuccess ||
+        (e = launch_fill_i32(A.pair_cnt, int64_t(cap), 0, stream)) != hipSuccess)
+      return fail_device(e, "edge batch: tables");
+    X = ExclView{A.edge_keys, A.pair_keys, A.pair_cnt, A.n_seed, A.edge_mask, A.pair_mask};
+  }
+
+  // ---- seeds: mark the endpoints, rank them, relabel the pair graphs --------
+  bitmap_dirty = true;
+  if ((e = launch_edge_targets(A, stream)) != hipSuccess) return fail_device(e, "edge targets");
+  char *d = dreg(pre);
+  const HopView pv{reinterpret_cast<int64_t *>(d + lay.nf),
+                   reinterpret_cast<int64_t *>(d + lay.pbase),
+                   reinterpret_cast<const int64_t *const *>(d + lay.frontier),
+                   reinterpret_cast<int64_t *const *>(d + lay.src_out),
+                   reinterpret_cast<const int32_t *>(d + lay.fanout)};
+  uint32_t epoch;
+  int64_t ticketed = 0;
+  if ((e = next_epoch(&epoch)) != hipSuccess ||
+      (e = launch_compact(pv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, 0,
+                          ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
+                          stream)) != hipSuccess)
+    return fail_device(e, "edge batch: seeds");
+  ticket_base += uint64_t(ticketed);
+  bitmap_dirty = false;
+  if ((e = launch_edge_relabel(A, view(0), g->d_tile_base, stream)) != hipSuccess)
+    return fail_device(e, "edge batch: pairs");
+  std::vector<int64_t> nF(bound);  // bounds until the first wait
+  map_region = 0;
+  map_bound = 0;
+  for (int64_t n : bound) map_bound += n;
+
+  if (H == 0) {
+    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
+    hg_status st = check_flags("targets");
+    if (st != HG_OK) return st;
+    for (int32_t t = 0; t < T; ++t) {
+      b->seed_n[t] = ws->hsmall[kSlotNew + t];
+      b->in_n[t] = b->seed_n[t];
+      b->in_gid[t] = seeds[t];
+    }
+    return HG_OK;
+  }
+  int64_t n_items = 1;
+  for (int32_t i = 0; i < R; ++i) n_items += bound[g->et[i].dst];
+  return hops(nF, n_items);
+}
+
+// The hop loop from region 0's frontier (sizes nF, or their bounds for an
+// edge-seeded call, whose sizes the device wrote); n_items >= pairs + 1.
+hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
+  hipError_t e;
+  int64_t P = 0;
   for (int32_t h = 0; h < H; ++h) {
     const HopView hv = view(h), nv = view(h + 1);
     // ---- 1. counting pass over at most n_items pair slots ----------------
@@ -667,7 +870,7 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
       return fail_device(e, "fill");
     uint32_t epoch;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
-        (e = launch_count_scan(hv, ws->d_es, R, T, n_items, pa, lb, epoch, ticket_base,
+        (e = launch_count_scan(hv, ws->d_es, R, T, n_items, pa, lb, epoch, ticket_base, X,
                                ws->dsmall, stream)) != hipSuccess)
       return fail_device(e, "count");
     ticket_base += uint64_t(tiles);
@@ -676,6 +879,13 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     hg_status st = check_flags("count");
     if (st != HG_OK) return st;
     const int64_t *hs = ws->hsmall;
+    if (h == 0 && eb) {
+      // the seeds of an edge-seeded call: the compaction counted them
+      for (int32_t t = 0; t < T; ++t) {
+        nF[t] = hs[kSlotNew + t];
+        b->seed_n[t] = nF[t];
+      }
+    }
     if (h > 0) {
       // close the previous hop: its source lists are this hop's frontier
       for (int32_t t = 0; t < T; ++t) {
@@ -741,7 +951,8 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
                            dsigmas(), g->key_R, h, key_bits, gid_tmp, eid_all, dstl_all,
                            indptr_all,
-                           src_slot, src_out.data(), inline_ptrs ? T : 0, stream)) != hipSuccess)
+                           src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream)) !=
+        hipSuccess)
       return fail_device(e, "sample");
     if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
       return fail_device(e, "mark");
@@ -781,35 +992,18 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     n_items = next_pairs + 1;
   }
 
-  if (H > 0) {
-    // final wait: new-vertex counts of the last hop
-    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
-    hg_status st = check_flags("compact");
-    if (st != HG_OK) return st;
-    for (int32_t t = 0; t < T; ++t) {
-      const size_t k = size_t(H - 1) * T + t;
-      b->n_src[k] = b->n_dst[k] + ws->hsmall[kSlotNew + t];
-      nF[t] = b->n_src[k];
-      if (nF[t] > INT32_MAX)
-        return fail(HG_EUNSUPPORTED, "hop %d: more than 2^31-1 vertices of type %d", H - 1, t);
-      b->in_n[t] = nF[t];
-      b->in_gid[t] = b->src_gid[k];
-    }
-  } else {
-    Carve a;
-    std::vector<int64_t *> cp(T, nullptr);
-    for (int32_t t = 0; t < T; ++t) a.add(&cp[t], nF[t]);
-    void *base = a.allocate(g, stream);
-    if (!base) return fail(HG_ENOMEM, "seed copy");
-    b->mem->ptrs.push_back(base);
-    for (int32_t t = 0; t < T; ++t) {
-      if (nF[t] > 0 &&
-          (e = hipMemcpyAsync(cp[t], seeds[t], sizeof(int64_t) * size_t(nF[t]),
-                              hipMemcpyDeviceToDevice, stream)) != hipSuccess)
-        return fail_device(e, "seed copy");
-      b->in_n[t] = nF[t];
-      b->in_gid[t] = cp[t];
-    }
+  // final wait: new-vertex counts of the last hop
+  if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
+  hg_status st = check_flags("compact");
+  if (st != HG_OK) return st;
+  for (int32_t t = 0; t < T; ++t) {
+    const size_t k = size_t(H - 1) * T + t;
+    b->n_src[k] = b->n_dst[k] + ws->hsmall[kSlotNew + t];
+    nF[t] = b->n_src[k];
+    if (nF[t] > INT32_MAX)
+      return fail(HG_EUNSUPPORTED, "hop %d: more than 2^31-1 vertices of type %d", H - 1, t);
+    b->in_n[t] = nF[t];
+    b->in_gid[t] = b->src_gid[k];
   }
   return HG_OK;
 }
@@ -1022,6 +1216,65 @@ hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *
   return HG_OK;
 }
 
+// An edge-seeded mini-batch (checked), then the gather.
+hg_status run_edge_sampling(hg_graph *g, const hg_edge_batch *eb, int32_t n_hops,
+                            const int32_t *fanouts, uint64_t rng_seed, const int32_t *gtypes,
+                            int32_t n_gather, hipStream_t stream, hg_blocks **out) {
+  DeviceGuard dg(g->device);
+  SampleRun run(g, stream, n_hops, fanouts, &rng_seed, 1, 32);
+  run.eb = eb;
+  run.edge_tab = align_up(sizeof(int64_t) * size_t(g->R + 1)) +
+                 align_up(sizeof(EdgeEtype) * size_t(std::max(g->R, 1)));
+  hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
+  if (st != HG_OK) return st;
+  run.b = new (std::nothrow) hg_blocks();
+  if (!run.b) {
+    run.finish(false);
+    return fail(HG_ENOMEM, "hg_sample_edge_blocks: out of host memory");
+  }
+  try {
+    st = run.run_edges();
+    if (st == HG_OK && n_gather > 0)
+      st = gather_into_blocks(g, run.b, gtypes, n_gather, nullptr, nullptr, stream);
+  } catch (const std::bad_alloc &) {
+    st = fail(HG_ENOMEM, "hg_sample_edge_blocks: out of host memory");
+  }
+  if (st != HG_OK) {
+    run.finish(false);
+    return st;
+  }
+  hg_blocks *b = run.b;
+  run.finish(true);
+  *out = b;
+  return HG_OK;
+}
+
+hg_status check_edge_batch(const hg_graph *g, const hg_edge_batch *eb) {
+  if (!eb || !eb->n_eids) return fail(HG_EINVAL, "hg_sample_edge_blocks: no batch");
+  if (eb->n_neg < 0 || eb->n_neg > HG_MAX_NEG)
+    return fail(HG_EINVAL, "hg_sample_edge_blocks: n_neg not in 0..%d", HG_MAX_NEG);
+  if (eb->exclude < HG_EXCLUDE_NONE || eb->exclude > HG_EXCLUDE_REVERSE)
+    return fail(HG_EINVAL, "hg_sample_edge_blocks: unknown exclusion %d", eb->exclude);
+  if (eb->exclude == HG_EXCLUDE_REVERSE && (!eb->rev_etype || !eb->rev_eid))
+    return fail(HG_EINVAL, "hg_sample_edge_blocks: reverse exclusion without a reverse map");
+  int64_t total = 0;
+  for (int32_t i = 0; i < g->R; ++i) {
+    const int64_t n = eb->n_eids[i];
+    if (n < 0) return fail(HG_EINVAL, "targets of edge type %d: negative count", i);
+    if (n > 0 && (!eb->eids || !eb->eids[i]))
+      return fail(HG_EINVAL, "targets of edge type %d: NULL pointer", i);
+    total += n;
+    if (total > (int64_t(1) << 30)) return fail(HG_EUNSUPPORTED, "too many target edges");
+    if (eb->exclude != HG_EXCLUDE_REVERSE || n == 0) continue;
+    const int32_t r = eb->rev_etype[i];
+    if (r < 0) continue;
+    if (r >= g->R || g->et[r].src != g->et[i].dst || g->et[r].dst != g->et[i].src)
+      return fail(HG_EINVAL, "edge type %d: reverse type %d does not run the other way", i, r);
+    if (!eb->rev_eid[i]) return fail(HG_EINVAL, "edge type %d: NULL reverse map", i);
+  }
+  return HG_OK;
+}
+
 hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
                       int32_t n_hops, const int32_t *fanouts, uint64_t rng_seed,
                       int32_t key_bits, const int32_t *gtypes, int32_t n_gather,
@@ -1219,6 +1472,60 @@ hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t 
     }
   }
   delete vb;  // the split handles keep the arrays
+  return HG_OK;
+}
+
+hg_status hg_sample_edge_blocks(hg_graph *g, const hg_edge_batch *batch, int32_t n_hops,
+                                const int32_t *fanouts, uint64_t rng_seed,
+                                const int32_t *gather_ntypes, int32_t n_gather,
+                                hipStream_t stream, hg_blocks **out) {
+  if (!out) return fail(HG_EINVAL, "hg_sample_edge_blocks: out is NULL");
+  *out = nullptr;
+  clear_pending_error();
+  if (!g) return fail(HG_EINVAL, "hg_sample_edge_blocks: graph is NULL");
+  std::vector<int64_t> zero(g->T, 0);
+  hg_status st = check_batch(g, nullptr, zero.data(), n_hops, fanouts, 32, gather_ntypes,
+                             n_gather);
+  if (st != HG_OK) return st;
+  st = check_edge_batch(g, batch);
+  if (st != HG_OK) return st;
+  return run_edge_sampling(g, batch, n_hops, fanouts, rng_seed, gather_ntypes, n_gather, stream,
+                           out);
+}
+
+hg_status hg_blocks_seeds(const hg_blocks *b, int32_t ntype, int64_t *n, const int64_t **gid) {
+  if (!b) return fail(HG_EINVAL, "hg_blocks_seeds: blocks is NULL");
+  if (ntype < 0 || ntype >= b->T)
+    return fail(HG_EINVAL, "hg_blocks_seeds: node type %d out of range", ntype);
+  int64_t cnt;
+  const int64_t *p;
+  if (b->edge_seeded) {
+    cnt = b->seed_n[ntype];
+    p = b->seed_gid[ntype];
+  } else if (b->H > 0) {  // the frontier of hop 0, the head of its source list
+    cnt = b->n_dst[ntype];
+    p = b->src_gid[ntype];
+  } else {
+    cnt = b->in_n[ntype];
+    p = b->in_gid[ntype];
+  }
+  if (n) *n = cnt;
+  if (gid) *gid = p;
+  return HG_OK;
+}
+
+hg_status hg_blocks_edge_pairs(const hg_blocks *b, int32_t etype, int64_t *n_pos,
+                               const int32_t **pos_src, const int32_t **pos_dst,
+                               int64_t *n_negs, const int32_t **neg_dst) {
+  if (!b) return fail(HG_EINVAL, "hg_blocks_edge_pairs: blocks is NULL");
+  if (!b->edge_seeded) return fail(HG_EINVAL, "hg_blocks_edge_pairs: not an edge-seeded batch");
+  if (etype < 0 || etype >= b->R)
+    return fail(HG_EINVAL, "hg_blocks_edge_pairs: edge type %d out of range", etype);
+  if (n_pos) *n_pos = b->pair_n[etype];
+  if (pos_src) *pos_src = b->pos_src[etype];
+  if (pos_dst) *pos_dst = b->pos_dst[etype];
+  if (n_negs) *n_negs = b->pair_n[etype] * b->n_neg;
+  if (neg_dst) *neg_dst = b->neg_dst[etype];
   return HG_OK;
 }
 

@@ -48,6 +48,30 @@ __device__ __forceinline__ int type_of(const int64_t *nF, int32_t n_types,
   return t;
 }
 
+// ---- exclusion lookups (edge-seeded mini-batches) ---------------------------
+
+// Excluded in-edges of the pair (etype e, destination local ID i).
+__device__ __forceinline__ int32_t excl_count(const ExclView &X, int e, int64_t i) {
+  if (!X.pair_keys || i >= X.n_seed[e]) return 0;
+  const uint64_t key = (uint64_t(uint32_t(e)) << 32) | uint64_t(i);
+  for (uint32_t h = hash_slot(key, X.pair_mask);; h = (h + 1) & X.pair_mask) {
+    const uint64_t k = X.pair_keys[h];
+    if (k == key) return X.pair_cnt[h];
+    if (k == kHashEmpty) return 0;
+  }
+}
+
+// Whether edge `eid` of etype e is excluded (the table has empty slots, so a
+// probe run always ends).
+__device__ __forceinline__ bool is_excluded(const ExclView &X, int e, uint64_t eid) {
+  const uint64_t key = (uint64_t(uint32_t(e)) << 32) | uint64_t(uint32_t(eid));
+  for (uint32_t h = hash_slot(key, X.edge_mask);; h = (h + 1) & X.edge_mask) {
+    const uint64_t k = X.edge_keys[h];
+    if (k == key) return true;
+    if (k == kHashEmpty) return false;
+  }
+}
+
 // ---- frontier map maintenance --------------------------------------------
 
 __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
@@ -121,7 +145,7 @@ template <bool kStaged, int kPairItems>
 __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
     int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
-    uint64_t ticket_base, int64_t *small) {
+    uint64_t ticket_base, ExclView X, int64_t *small) {
   __shared__ int64_t lds[16];
   __shared__ CountTable table;
   if (kStaged) {
@@ -199,13 +223,16 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     if (!fp[k]) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
     const int64_t deg = hi[k] - lo[k];
     const int64_t K = V.fanout(etype[k]);
-    const int64_t s = (K < 0 || deg <= K) ? deg : K;
+    // in-edges that take part: all but the excluded ones
+    const int32_t nx = excl_count(X, etype[k], p - V.pbase(etype[k]));
+    const int64_t avail = deg - nx;
+    const int64_t s = (K < 0 || avail <= K) ? avail : K;
     c[k].s = s;
-    if (s < deg && deg > kHubChunk) {
+    if (s < avail && deg > kHubChunk) {
       c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
       c[k].hub = 1;
-    } else if (s > 0 && !(s == deg && deg <= kThreadTakeAll)) {
-      c[k].wave = 1;
+    } else if (s > 0 && !(nx == 0 && s == deg && deg <= kThreadTakeAll)) {
+      c[k].wave = 1;  // pairs with excluded edges always take this role
     }
     pa.plo[p] = lo[k];
     pa.pdeg[p] = deg;
@@ -321,7 +348,8 @@ __device__ __forceinline__ uint64_t cand_threshold(int64_t K, int64_t deg,
 __device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
                                     int64_t K, int64_t o, uint64_t a,
                                     uint64_t b, int32_t hop, int32_t e,
-                                    uint32_t k0, uint32_t k1, uint32_t shift) {
+                                    uint32_t k0, uint32_t k1, uint32_t shift,
+                                    const ExclView &X, int xe, bool excl) {
   const int lane = lane_id();
   const uint64_t g_first = uint64_t(lo) >> 2;
   const uint64_t g_last = uint64_t(lo + deg - 1) >> 2;
@@ -337,7 +365,8 @@ __device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
       for (int w = 0; w < 4; ++w) {
         const uint64_t ed = 4 * g + w;
         if (ed >= uint64_t(lo) && ed < hi &&
-            ((uint64_t(word_of(r, w)) << 32) | (ed - uint64_t(lo))) <= mid)
+            ((uint64_t(word_of(r, w)) << 32) | (ed - uint64_t(lo))) <= mid &&
+            !(excl && is_excluded(X, xe, ed)))
           ++le;
       }
     }
@@ -358,7 +387,8 @@ __device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
       for (int w = 0; w < 4; ++w) {
         const uint64_t ed = 4 * g + w;
         if (ed >= uint64_t(lo) && ed < hi &&
-            ((uint64_t(word_of(r, w)) << 32) | (ed - uint64_t(lo))) <= T)
+            ((uint64_t(word_of(r, w)) << 32) | (ed - uint64_t(lo))) <= T &&
+            !(excl && is_excluded(X, xe, ed)))
           mask |= 1 << w;
       }
     }
@@ -413,6 +443,7 @@ struct SampleArgs {
   int64_t **src_out_slot;
   int64_t *src_out_new[kInlineTypes];
   int32_t n_src_out;
+  ExclView X;
 };
 
 // Philox key words and counter edge type of (virtual) edge type e.
@@ -502,8 +533,20 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   const int64_t deg = A.pa.pdeg[p];
   const int64_t o = A.pa.off[p];
   const int64_t s = A.pa.off[p + 1] - o;
+  const int32_t nx = excl_count(A.X, e, p - A.hv.pair_base[e]);
   if (s == deg) {  // every in-edge is kept
     for (int64_t j = lane; j < deg; j += kWave) emit_edge(c, o + j, lo + j);
+    return;
+  }
+  if (nx > 0 && s == deg - nx) {  // every in-edge but the excluded ones
+    int64_t emitted = 0;
+    for (int64_t j0 = 0; j0 < deg; j0 += kWave) {
+      const int64_t j = j0 + lane;
+      const bool keep = j < deg && !is_excluded(A.X, e, uint64_t(lo + j));
+      const uint64_t bal = __ballot(keep);
+      if (keep) emit_edge(c, o + emitted + __popcll(bal & lanes_below()), lo + j);
+      emitted += __popcll(bal);
+    }
     return;
   }
   const int64_t K = s;
@@ -527,7 +570,8 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const uint64_t ed = 4 * g + q;
-        if (ed >= uint64_t(lo) && ed < hi && uint64_t(word_of(r, q)) < tau)
+        if (ed >= uint64_t(lo) && ed < hi && uint64_t(word_of(r, q)) < tau &&
+            !(nx > 0 && is_excluded(A.X, e, ed)))
           mask |= 1 << q;
       }
     }
@@ -572,7 +616,7 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   }
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
-  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift);
+  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift, A.X, e, nx > 0);
 }
 
 // Role C: wavefront w takes the hub chunks [w * chunks_per_wave, ...) in
@@ -587,6 +631,7 @@ struct HubParams {
   int64_t hub, first_chunk, end_chunk, lo, deg, K;
   uint64_t tau;
   int e;
+  int32_t nx;  // excluded in-edges
   KeyCtx kc;
 };
 
@@ -602,6 +647,7 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   H.deg = A.pa.pdeg[p];
   H.K = A.pa.off[p + 1] - A.pa.off[p];
   H.tau = cand_threshold(H.K, H.deg, uint64_t(1) << A.key_bits);
+  H.nx = excl_count(A.X, H.e, p - A.hv.pair_base[H.e]);
   return H;
 }
 
@@ -632,6 +678,11 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
       if (ed < uint64_t(c_lo) || ed >= uint64_t(c_hi)) mask &= ~(1 << q);
     }
     if (__ballot(mask != 0) == 0) return;
+  }
+  if (H.nx > 0) {  // excluded edges are never candidates
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if ((mask & (1 << q)) && is_excluded(A.X, H.e, 4 * g + q)) mask &= ~(1 << q);
   }
   int tot;
   const int pre = wave_prefix_small(__popc(mask), &tot);
@@ -745,7 +796,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   }
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
-  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift);
+  const int32_t nx = excl_count(A.X, e, p - A.hv.pair_base[e]);
+  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift, A.X, e, nx > 0);
 }
 
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
@@ -941,30 +993,30 @@ int64_t count_tiles(int64_t n_items) {
 template <bool kStaged, int kItems>
 void count_launch(HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
                   int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
-                  uint64_t ticket_base, int64_t *small, hipStream_t stream) {
+                  uint64_t ticket_base, ExclView X, int64_t *small, hipStream_t stream) {
   hipLaunchKernelGGL((k_count_scan<kStaged, kItems>), dim3(unsigned(count_tiles(n_items))),
                      dim3(kTileThreads), 0, stream, hv, es, n_etypes, n_types, n_items, pa,
-                     lb, epoch, ticket_base, small);
+                     lb, epoch, ticket_base, X, small);
 }
 
 hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                              int32_t n_types, int64_t n_items, PairArrays pa,
                              Lookback lb, uint32_t epoch, uint64_t ticket_base,
-                             int64_t *small, hipStream_t stream) {
+                             ExclView X, int64_t *small, hipStream_t stream) {
   const bool staged = n_etypes <= kCountMaxEtypes;
   const bool large = pair_items(n_items) == kPairItemsLarge;
   if (staged && large)
     count_launch<true, kPairItemsLarge>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                        ticket_base, small, stream);
+                                        ticket_base, X, small, stream);
   else if (staged)
     count_launch<true, kPairItemsSmall>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                        ticket_base, small, stream);
+                                        ticket_base, X, small, stream);
   else if (large)
     count_launch<false, kPairItemsLarge>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                         ticket_base, small, stream);
+                                         ticket_base, X, small, stream);
   else
     count_launch<false, kPairItemsSmall>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                         ticket_base, small, stream);
+                                         ticket_base, X, small, stream);
   return hipGetLastError();
 }
 
@@ -975,9 +1027,10 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t key_R, int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
-                         hipStream_t stream) {
+                         ExclView X, hipStream_t stream) {
   if (n_src_out > kInlineTypes) return hipErrorInvalidValue;
   SampleArgs A;
+  A.X = X;
   A.src_out_slot = src_out_slot;
   A.n_src_out = n_src_out;
   for (int32_t t = 0; t < kInlineTypes; ++t) A.src_out_new[t] = t < n_src_out ? src_out[t] : nullptr;

@@ -32,6 +32,28 @@ def result_dict(graph: hg.Graph, blocks: hg.Blocks):
     return res
 
 
+def edge_result_dict(graph: hg.Graph, blocks: hg.Blocks):
+    """result_dict plus the seeds and pair graphs of an edge-seeded batch."""
+    res = result_dict(graph, blocks)
+    res["seeds"] = {t: blocks.seeds(t).cpu().numpy() for t in range(graph.T)}
+    res["pairs"] = {e: tuple(a.cpu().numpy() for a in blocks.edge_pairs(e))
+                    for e in range(graph.R)}
+    return res
+
+
+def compare_edges(ref, got, T, R, H):
+    """compare() plus the seeds and the pair graphs."""
+    diffs = compare(ref, got, T, R, H)
+    for t in range(T):
+        if not np.array_equal(ref["seeds"][t], got["seeds"][t]):
+            diffs.append(f"seeds of type {t} differ: {ref['seeds'][t][:6]} / {got['seeds'][t][:6]}")
+    for e in range(R):
+        for name, x, y in zip(("pos_src", "pos_dst", "neg_dst"), ref["pairs"][e], got["pairs"][e]):
+            if x.dtype != y.dtype or not np.array_equal(x, y):
+                diffs.append(f"etype {e} {name} differs: {x[:6]} / {y[:6]}")
+    return diffs
+
+
 def gpu_seeds(seeds, device="cuda"):
     return [None if s is None else torch.as_tensor(np.asarray(s, np.int64), device=device)
             for s in seeds]

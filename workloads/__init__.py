@@ -262,6 +262,50 @@ def seeds_per_type(workload: Workload, b: int):
     return out
 
 
+# Edge-seeded (link-prediction) batches on a workload's graph: the paper's
+# link-prediction runs use two sampling hops of fanout 25 and 15 and the batch
+# size of its other runs (Appendix A.1); the targets are edges of one forward
+# relation, drawn without replacement.
+LINK_FANOUTS = (25, 15)
+LINK_BATCH = 1000
+LINK_NEG = 1
+
+
+def reverse_maps(graph: Graph):
+    """rev_etype[e] and rev_eid[e] (int64 tensor [nnz_e] on the graph's device)
+    for a workload whose reverse edge types are transposes: the slot of every
+    edge's reverse in its reverse type.  None, None when there are no reverses."""
+    wl = graph.workload
+    if not wl.reverse:
+        return None, None
+    R0 = len(wl.etypes)
+    rev_etype = [R0 + e for e in range(R0)] + list(range(R0))
+    fmaps, rmaps = [], []
+    for (s, d, ip, ix) in graph.etypes[:R0]:
+        n_dst = ip.numel() - 1
+        deg = ip[1:] - ip[:-1]
+        dst = torch.repeat_interleave(torch.arange(n_dst, device=ip.device, dtype=torch.int64), deg)
+        # the transpose orders its slots by (source, destination), all distinct
+        order = torch.argsort(ix * n_dst + dst)
+        del dst
+        fmap = torch.empty_like(order)
+        fmap[order] = torch.arange(order.numel(), device=order.device, dtype=torch.int64)
+        fmaps.append(fmap)
+        rmaps.append(order)
+    return rev_etype, fmaps + rmaps
+
+
+def link_targets(graph: Graph, b: int, etype: int, size: int = LINK_BATCH):
+    """Target edge IDs of link-prediction batch b: `size` distinct edges of
+    edge type `etype`, numpy Generator(PCG64(30000*cfg + b)); a list per edge
+    type (None for the others)."""
+    nnz = int(graph.etypes[etype][3].numel())
+    rng = np.random.Generator(np.random.PCG64(30000 * graph.workload.cfg + b))
+    out = [None] * len(graph.etypes)
+    out[etype] = rng.choice(nnz, size=min(size, nnz), replace=False).astype(np.int64)
+    return out
+
+
 def random_hetero(rng: np.random.Generator, max_types=3, max_etypes=4, max_nodes=50,
                   max_deg=30, feat_dim=4):
     """A tiny random heterograph for brute-force and invariant checks (numpy CSC).
@@ -320,5 +364,6 @@ def human_bytes(n: int) -> str:
 
 
 __all__ = ["NodeType", "EdgeType", "Workload", "WORKLOADS", "Graph", "make_graph",
+           "reverse_maps", "link_targets", "LINK_FANOUTS", "LINK_BATCH", "LINK_NEG",
            "batch_seeds", "seeds_per_type", "random_hetero", "graph_stats", "powerlaw_degrees",
            "distinct_sources", "transpose_csc", "random_features"]
