@@ -40,9 +40,10 @@ struct CompactArgs {
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
-  int64_t *tile_pre;  // per tile: set bits of its type in earlier tiles (or look-back words)
+  int64_t *tile_pre;  // [n_tiles + 1] set bits in earlier tiles, of any type (or look-back words)
   int32_t *tile_cnt;  // per tile: set bits
   int64_t *small;
+  uint32_t map_epoch;
 };
 
 __device__ __forceinline__ uint2 tile_words(const CompactArgs &A, int64_t tile) {
@@ -79,35 +80,39 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_count(CompactArgs A) {
   if (threadIdx.x == 0) A.tile_cnt[tile] = int32_t(total);
 }
 
-// 2. Exclusive scan of the tile counts within each node type, in one block;
-// the type's total is its number of new vertices.
+// 2. Exclusive scan of the tile counts over all tiles, in one block: tile_pre
+// gets the set bits of every earlier tile (of any type), and tile_pre[n_tiles]
+// the total.  A tile's prefix within its type is then tile_pre[tile] -
+// tile_pre[first tile of the type]; each type's count of new vertices is the
+// difference at its bounds.
 constexpr int kScanThreads = 1024;
 __global__ __launch_bounds__(kScanThreads) void k_bits_scan(CompactArgs A) {
   constexpr int kWaves = kScanThreads / kWave;
   __shared__ int64_t s_wave[kWaves];
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
-  for (int t = 0; t < A.n_types; ++t) {
-    const int64_t b0 = A.tile_base[t], b1 = A.tile_base[t + 1];
-    int64_t carry = 0;
-    for (int64_t c0 = b0; c0 < b1; c0 += kScanThreads) {
-      const int64_t i = c0 + threadIdx.x;
-      const int64_t x = i < b1 ? A.tile_cnt[i] : 0;
-      const int64_t inc = wave_incl_scan_i64(x);
-      if (lane == kWave - 1) s_wave[wave] = inc;
-      __syncthreads();
-      int64_t before = 0, sum = 0;
-      for (int v = 0; v < kWaves; ++v) {
-        const int64_t y = s_wave[v];
-        if (v < wave) before += y;
-        sum += y;
-      }
-      if (i < b1) A.tile_pre[i] = carry + before + inc - x;
-      carry += sum;
-      __syncthreads();
+  int64_t carry = 0;
+  for (int64_t c0 = 0; c0 < A.n_tiles; c0 += kScanThreads) {
+    const int64_t i = c0 + threadIdx.x;
+    const int64_t x = i < A.n_tiles ? A.tile_cnt[i] : 0;
+    const int64_t inc = wave_incl_scan_i64(x);
+    if (lane == kWave - 1) s_wave[wave] = inc;
+    __syncthreads();
+    int64_t before = 0, sum = 0;
+    for (int v = 0; v < kWaves; ++v) {
+      const int64_t y = s_wave[v];
+      if (v < wave) before += y;
+      sum += y;
     }
-    if (threadIdx.x == 0) A.small[kSlotNew + t] = carry;  // new vertices of type t
+    if (i < A.n_tiles) A.tile_pre[i] = carry + before + inc - x;
+    carry += sum;
+    __syncthreads();
   }
+  if (threadIdx.x == 0) A.tile_pre[A.n_tiles] = carry;
+  __syncthreads();
+  // new vertices of each type (the block's own stores are visible to it)
+  for (int t = threadIdx.x; t < A.n_types; t += kScanThreads)
+    A.small[kSlotNew + t] = A.tile_pre[A.tile_base[t + 1]] - A.tile_pre[A.tile_base[t]];
 }
 
 // Gives the set bits of a tile's words `ab` (thread's share), the first of
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bits_scan(CompactArgs A) {
 __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t first,
                                             int64_t tile, uint2 ab, int64_t local) {
   if ((ab.x | ab.y) == 0) return;
-  int32_t *map = A.ts[t].map;
+  uint64_t *map = A.ts[t].map;
   int64_t *out = A.hv.src_out[t];
   const uint32_t words[kTileItems] = {ab.x, ab.y};
   const int64_t v0 = ((tile - first) * kTile + threadIdx.x * kTileItems) * 32;
@@ -126,7 +131,7 @@ __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t
       const int bit = __ffs(m) - 1;
       m &= m - 1;
       const int64_t v = v0 + k * 32 + bit;
-      map[v] = int32_t(local);
+      map[v] = map_entry(A.map_epoch, local);
       out[local] = v;
       ++local;
     }
@@ -144,7 +149,9 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_assign(CompactArgs A) {
   const uint2 ab = tile_words(A, tile);
   int64_t total;
   const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &total);
-  assign_bits(A, t, A.tile_base[t], tile, ab, A.hv.nF[t] + A.tile_pre[tile] + pre);
+  const int64_t first = A.tile_base[t];
+  assign_bits(A, t, first, tile, ab,
+              A.hv.nF[t] + (A.tile_pre[tile] - A.tile_pre[first]) + pre);
 }
 
 // The three steps in one launch for a few tiles: tiles in ticket order, each
@@ -200,7 +207,7 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
   const int64_t *ebase = small + kSlotNew + n_types;
   for (int64_t j = gs_start(); j < n_edges; j += gs_step()) {
     const int e = find_segment(ebase, n_etypes, j);
-    src_local[j] = es[e].src_map[src_gid[j]];
+    src_local[j] = map_local(es[e].src_map[src_gid[j]]);
   }
 }
 
@@ -209,10 +216,10 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
-                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream) {
+                          uint32_t epoch, uint64_t ticket_base, uint32_t map_epoch,
+                          int64_t *small, int64_t *ticketed, hipStream_t stream) {
   CompactArgs A{hv, ts, n_types, bitmap, tile_base, n_tiles, copy_total, tile_sums,
-                reinterpret_cast<int32_t *>(tile_sums + n_tiles), small};
+                reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small, map_epoch};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
   *ticketed = 0;
   if (n_tiles <= kSinglePassTiles) {

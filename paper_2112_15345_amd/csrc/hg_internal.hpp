@@ -58,11 +58,23 @@ constexpr int32_t kErrLookback = 4;    // a scan wait exceeded its bound
 constexpr int32_t kErrBound = 8;       // more pairs or chunks than buffers were sized for
 constexpr int32_t kErrTarget = 16;     // a target edge out of range, or a bad reverse edge
 
+// The dense vertex -> local-ID map of a workspace holds one 64-bit entry per
+// vertex: the call epoch in the high word, the local ID in the low word.  An
+// entry belongs to the current call only if it carries the call's epoch, so
+// the map never needs clearing between calls.
+__host__ __device__ inline uint64_t map_entry(uint32_t epoch, int64_t local) {
+  return (uint64_t(epoch) << 32) | uint64_t(uint32_t(local));
+}
+__host__ __device__ inline bool map_has(uint64_t w, uint32_t epoch) {
+  return uint32_t(w >> 32) == epoch;
+}
+__host__ __device__ inline int32_t map_local(uint64_t w) { return int32_t(uint32_t(w)); }
+
 // Static per edge type (per workspace).
 struct EtypeStatic {
   const int64_t *indptr;
   const int64_t *indices;
-  int32_t *src_map;       // dense vertex -> local-ID map of the source type
+  uint64_t *src_map;      // vertex -> local-ID map of the source type
   uint32_t *src_bitmap;   // new-vertex bitmap of the source type
   int64_t n_dst_nodes;
   int32_t src_type;
@@ -71,7 +83,7 @@ struct EtypeStatic {
 
 // Static per node type (per workspace).
 struct TypeStatic {
-  int32_t *map;
+  uint64_t *map;
   uint32_t *bitmap;
   int64_t num_nodes;
 };
@@ -139,16 +151,11 @@ int graph_device(const hg_graph *g);
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
 
-// The hop-0 frontier: map[seed] = position; flags range errors and repeats.
+// The hop-0 frontier: map[seed] = (epoch, position); flags range errors and
+// repeats.
 hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
-                                  int32_t n_types, int64_t total, int64_t *small,
-                                  hipStream_t stream);
-// map[v] = -1 for every vertex of the hop's frontier (in-range entries only);
-// `bound` >= the frontier's total size, which is read on the device.  Also
-// zeroes small[0..n_small), ready for the next call.
-hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
-                            int64_t bound, int64_t *small, int32_t n_small,
-                            hipStream_t stream);
+                                  int32_t n_types, int64_t total, uint32_t epoch,
+                                  int64_t *small, hipStream_t stream);
 
 // Counting pass over n_items >= P + 1 pair slots (P = pair_base[R]): per pair
 // its in-edge range; exclusive scans of kept edges, hub chunks, wavefront
@@ -183,7 +190,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
 // ebase = small + kSlotNew + n_types).
 hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
                        int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
-                       hipStream_t stream);
+                       uint32_t map_epoch, hipStream_t stream);
 
 // Compaction pass: per bitmap tile, ranks of the set bits within the node
 // type -> local IDs n_frontier + rank, written to the map and the source
@@ -192,13 +199,13 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
 // kSinglePassTiles tiles: one launch, a single-pass scan whose look-back words
 // are tile_sums (ticketed blocks: *ticketed is their number).  Beyond: three
 // launches (reduce, scan, rank) with no inter-block waits; *ticketed = 0.
-// tile_sums: device scratch of 2 * n_tiles 64-bit words.
+// tile_sums: device scratch of 2 * n_tiles + 2 64-bit words.
 constexpr int64_t kSinglePassTiles = 256;
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
-                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream);
+                          uint32_t epoch, uint64_t ticket_base, uint32_t map_epoch,
+                          int64_t *small, int64_t *ticketed, hipStream_t stream);
 
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.
@@ -212,8 +219,9 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
 
 // Fill helpers (kernels, so that they are safe under graph capture).
 // One block copies small[0..n) to pinned host memory host[0..n) and then
-// writes `seq` to host[n] (system scope, after the slots).
-hipError_t launch_publish(const int64_t *small, int64_t *host, int32_t n, uint64_t seq,
+// writes `seq` to host[n] (system scope, after the slots).  With `clear` it
+// then zeroes small[0..n), ready for the next call.
+hipError_t launch_publish(int64_t *small, int64_t *host, int32_t n, uint64_t seq, bool clear,
                           hipStream_t stream);
 // dst[i] = vals[i] for i < n (device pointer table), stream-ordered, with the
 // values passed in the launches.

@@ -119,9 +119,10 @@ struct Scratch {
 };
 
 // Per-call device state.  One call uses a workspace at a time; between calls
-// the map is all -1 and the bitmap all 0.
+// the bitmap is all 0, and no map entry carries the next call's epoch.
 struct Workspace {
-  int32_t *map = nullptr;          // sum of num_nodes
+  uint64_t *map = nullptr;         // sum of num_nodes: (call epoch, local ID)
+  uint32_t map_epoch = 0;          // epoch of the last call (entries start at epoch 0)
   uint32_t *bitmap = nullptr;      // n_tiles * kTile words
   int64_t *dsmall = nullptr;       // readback slots
   int64_t *hsmall = nullptr;       // pinned, coherent mirror of dsmall + a flag word
@@ -347,25 +348,25 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     const size_t small_n = small_slots(g);
     const int64_t n_lb = std::max<int64_t>(g->n_tiles, 1);
     hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(int32_t) * size_t(std::max<int64_t>(map_n, 1)));
+    if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(uint64_t) * size_t(std::max<int64_t>(map_n, 1)));
     if (e == hipSuccess)
       e = hipMalloc(&w->bitmap, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
     if (e == hipSuccess) e = hipMalloc(&w->d_es, sizeof(EtypeStatic) * size_t(std::max(g->R, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->d_ts, sizeof(TypeStatic) * size_t(g->T));
-    if (e == hipSuccess) e = hipMalloc(&w->tile_sums, sizeof(int64_t) * 2 * size_t(n_lb));
+    if (e == hipSuccess) e = hipMalloc(&w->tile_sums, sizeof(int64_t) * (2 * size_t(n_lb) + 2));
     // coherent: the device writes it while the host polls the flag word
     if (e == hipSuccess)
       e = hipHostMalloc(reinterpret_cast<void **>(&w->hsmall), sizeof(int64_t) * (small_n + 1),
                         hipHostMallocCoherent);
     if (e == hipSuccess) std::memset(w->hsmall, 0, sizeof(int64_t) * (small_n + 1));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming);
-    if (e == hipSuccess) e = launch_fill_i32(w->map, map_n, -1, stream);
+    if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t *>(w->map), 2 * map_n, 0u, stream);
     if (e == hipSuccess)
       e = launch_fill_i32(reinterpret_cast<int32_t *>(w->dsmall), 2 * int64_t(small_n), 0, stream);
     // look-back words of the single-pass compaction: no stale epoch
     if (e == hipSuccess)
-      e = launch_fill_i32(reinterpret_cast<int32_t *>(w->tile_sums), 4 * n_lb, 0, stream);
+      e = launch_fill_i32(reinterpret_cast<int32_t *>(w->tile_sums), 4 * n_lb + 4, 0, stream);
     if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
@@ -466,12 +467,11 @@ struct SampleRun {
   size_t sig_bytes;              // the sigma table heads the call's tables
   uint64_t ticket_base = 0;
 
-  // the map holds the frontier of region `map_region` (at most map_bound
-  // vertices in all; the exact sizes are in the region) until the call ends;
-  // the bitmap is clean unless bitmap_dirty
-  int map_region = -1;
-  int64_t map_bound = 0;
+  // the call's map epoch; the bitmap is clean unless bitmap_dirty; the
+  // readback slots are zero again once a clearing publish has run
+  uint32_t map_epoch = 0;
   bool bitmap_dirty = false;
+  bool small_clean = false;
 
   // an edge-seeded call: its batch, the excluded edges and its extra tables
   // (a region for the seeds' compaction after regions 0 .. H+1, then the
@@ -540,10 +540,11 @@ struct SampleRun {
   // and then sets its flag word, which the host polls (cheaper than a copy
   // plus a stream wait).  Every few hundred polls the stream is queried, so
   // a failed kernel (whose successors never run) ends the wait with its error.
-  hipError_t sync_small() {
+  hipError_t sync_small(bool last = false) {
     const int32_t n = int32_t(small_slots(g));
     const uint64_t seq = ++ws->publish_seq;
-    hipError_t e = launch_publish(ws->dsmall, ws->hsmall, n, seq, stream);
+    hipError_t e = launch_publish(ws->dsmall, ws->hsmall, n, seq, last, stream);
+    if (e == hipSuccess && last) small_clean = true;
     if (e != hipSuccess) return e;
     const volatile int64_t *flag = ws->hsmall + n;
     for (uint32_t i = 1; uint64_t(*flag) != seq; ++i) {
@@ -575,14 +576,24 @@ struct SampleRun {
     return HG_OK;
   }
 
-  // Undoes the map and bitmap state; releases the workspace.
+  // Starts the call's map epoch (refilling the map before epochs repeat).
+  hipError_t begin_map() {
+    if (ws->map_epoch == 0xFFFFFFFFu) {
+      hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t *>(ws->map),
+                                     2 * g->map_off[g->T], 0u, stream);
+      if (e != hipSuccess) return e;
+      ws->map_epoch = 0;
+    }
+    map_epoch = ++ws->map_epoch;
+    return hipSuccess;
+  }
+
+  // Leaves the bitmap and the readback slots clean; releases the workspace.
+  // (The map needs nothing: the next call has a new epoch.)
   void finish(bool ok) {
     if (!ws->poisoned) {
       if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
-      if (map_region >= 0)
-        (void)launch_reset_map(view(map_region), ws->d_ts, T, map_bound, ws->dsmall,
-                               int32_t(small_slots(g)), stream);
-      else
+      if (!small_clean)
         (void)launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall),
                               2 * int64_t(small_slots(g)), 0, stream);
     }
@@ -664,12 +675,12 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     return fail_device(e, "start");
   int64_t total = 0;
   for (int64_t n : nF) total += n;
-  map_region = 0;
-  map_bound = total;
-  if ((e = launch_insert_frontier(view(0), ws->d_ts, T, total, ws->dsmall, stream)) != hipSuccess)
+  if ((e = begin_map()) != hipSuccess ||
+      (e = launch_insert_frontier(view(0), ws->d_ts, T, total, map_epoch, ws->dsmall,
+                                  stream)) != hipSuccess)
     return fail_device(e, "insert seeds");
   if (H == 0) {
-    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
+    if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
     hg_status st = check_flags("seeds");
     if (st != HG_OK) return st;
     Carve a;
@@ -800,6 +811,7 @@ hg_status SampleRun::run_edges() {
   }
 
   // ---- seeds: mark the endpoints, rank them, relabel the pair graphs --------
+  if ((e = begin_map()) != hipSuccess) return fail_device(e, "edge batch: map");
   bitmap_dirty = true;
   if ((e = launch_edge_targets(A, stream)) != hipSuccess) return fail_device(e, "edge targets");
   char *d = dreg(pre);
@@ -812,7 +824,7 @@ hg_status SampleRun::run_edges() {
   int64_t ticketed = 0;
   if ((e = next_epoch(&epoch)) != hipSuccess ||
       (e = launch_compact(pv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, 0,
-                          ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
+                          ws->tile_sums, epoch, ticket_base, map_epoch, ws->dsmall, &ticketed,
                           stream)) != hipSuccess)
     return fail_device(e, "edge batch: seeds");
   ticket_base += uint64_t(ticketed);
@@ -820,12 +832,9 @@ hg_status SampleRun::run_edges() {
   if ((e = launch_edge_relabel(A, view(0), g->d_tile_base, stream)) != hipSuccess)
     return fail_device(e, "edge batch: pairs");
   std::vector<int64_t> nF(bound);  // bounds until the first wait
-  map_region = 0;
-  map_bound = 0;
-  for (int64_t n : bound) map_bound += n;
 
   if (H == 0) {
-    if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
+    if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
     hg_status st = check_flags("targets");
     if (st != HG_OK) return st;
     for (int32_t t = 0; t < T; ++t) {
@@ -954,12 +963,13 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
                            src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream)) !=
         hipSuccess)
       return fail_device(e, "sample");
-    if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
+    if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, map_epoch, stream)) !=
+        hipSuccess)
       return fail_device(e, "mark");
     int64_t ticketed = 0;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
         (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
-                            ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
+                            ws->tile_sums, epoch, ticket_base, map_epoch, ws->dsmall, &ticketed,
                             stream)) != hipSuccess)
       return fail_device(e, "compact");
     ticket_base += uint64_t(ticketed);
@@ -969,9 +979,6 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
       return fail_device(e, "relabel");
     // the map now holds the source lists of this hop, which are region h+1's
     // frontier; the relabel pass wrote their sizes into that region
-    map_region = h + 1;
-    map_bound = 0;
-    for (int32_t t = 0; t < T; ++t) map_bound += bound[t];
 
     for (int32_t t = 0; t < T; ++t) {
       const size_t k = size_t(h) * T + t;
@@ -993,7 +1000,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
   }
 
   // final wait: new-vertex counts of the last hop
-  if ((e = sync_small()) != hipSuccess) return fail_device(e, "sync");
+  if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
   hg_status st = check_flags("compact");
   if (st != HG_OK) return st;
   for (int32_t t = 0; t < T; ++t) {

@@ -75,7 +75,8 @@ __device__ __forceinline__ bool is_excluded(const ExclView &X, int e, uint64_t e
 // ---- frontier map maintenance --------------------------------------------
 
 __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
-                                  int32_t n_types, int64_t total, int64_t *small) {
+                                  int32_t n_types, int64_t total, uint32_t epoch,
+                                  int64_t *small) {
   int32_t *err = reinterpret_cast<int32_t *>(small + kSlotErr);
   for (int64_t x = grid_stride_start(); x < total; x += grid_stride_step()) {
     int64_t first;
@@ -87,21 +88,19 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
       atomicOr(err, kErrSeedRange);
       continue;
     }
-    if (atomicCAS(&ts[t].map[v], -1, int(i)) != -1) atomicOr(err, kErrSeedRepeat);
-  }
-}
-
-__global__ void k_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
-                            int64_t total, int64_t *small, int32_t n_small) {
-  // the call is over: its readback slots start the next call at zero
-  if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i < n_small; i += blockDim.x) small[i] = 0;
-  for (int64_t x = grid_stride_start(); x < total; x += grid_stride_step()) {
-    int64_t first;
-    const int t = type_of(hv.nF, n_types, x, &first);
-    if (x - first >= hv.nF[t]) continue;  // past the end of the lists
-    const int64_t v = hv.frontier[t][x - first];
-    if (v >= 0 && v < ts[t].num_nodes) ts[t].map[v] = -1;
+    // claim the entry unless this call already did (a repeated seed); a
+    // failed exchange means another seed of this call took it
+    unsigned long long *m = reinterpret_cast<unsigned long long *>(&ts[t].map[v]);
+    unsigned long long old = *m;
+    for (;;) {
+      if (map_has(old, epoch)) {
+        atomicOr(err, kErrSeedRepeat);
+        break;
+      }
+      const unsigned long long prev = atomicCAS(m, old, map_entry(epoch, i));
+      if (prev == old) break;
+      old = prev;
+    }
   }
 }
 
@@ -835,11 +834,11 @@ constexpr uint64_t kEmptySlot = ~uint64_t(0);
 
 __global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64_t *ebase,
                                               int32_t n_etypes, int64_t n_edges,
-                                              const int64_t *src_gid) {
+                                              const int64_t *src_gid, uint32_t map_epoch) {
   __shared__ uint64_t s_key[kMarkSlots];   // word address
   __shared__ uint32_t s_bits[kMarkSlots];
   __shared__ int64_t s_eb[kMarkMaxEtypes + 1];
-  __shared__ const int32_t *s_map[kMarkMaxEtypes];
+  __shared__ const uint64_t *s_map[kMarkMaxEtypes];
   __shared__ uint32_t *s_bm[kMarkMaxEtypes];
   const bool staged = n_etypes <= kMarkMaxEtypes;
   for (int i = threadIdx.x; i < kMarkSlots; i += blockDim.x) {
@@ -874,8 +873,8 @@ __global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64
   for (int k = 0; k < kMarkPerThread; ++k) {
     need[k] = false;
     if (g[k] >= 0) {
-      const int32_t *map = staged ? s_map[et[k]] : es[et[k]].src_map;
-      need[k] = map[g[k]] < 0;  // not in the frontier yet
+      const uint64_t *map = staged ? s_map[et[k]] : es[et[k]].src_map;
+      need[k] = !map_has(map[g[k]], map_epoch);  // not in the frontier yet
     }
   }
 #pragma unroll
@@ -943,14 +942,18 @@ __global__ void k_philox(const uint32_t *ctr, uint32_t k0, uint32_t k1,
 // Copies the n readback slots to host memory, then sets the flag word
 // host[n] to `seq`: a host that sees `seq` there reads the slots as they are
 // at this point of the stream (every earlier kernel has finished).
-__global__ __launch_bounds__(256) void k_publish(const int64_t *small, int64_t *host,
-                                                 int32_t n, uint64_t seq) {
+__global__ __launch_bounds__(256) void k_publish(int64_t *small, int64_t *host,
+                                                 int32_t n, uint64_t seq, bool clear) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) host[i] = small[i];
   __threadfence_system();
   __syncthreads();
   if (threadIdx.x == 0)
     __hip_atomic_store(reinterpret_cast<uint64_t *>(host + n), seq, __ATOMIC_RELEASE,
                        __HIP_MEMORY_SCOPE_SYSTEM);
+  // the call is over: its readback slots start the next call at zero (each
+  // thread clears the slots it copied)
+  if (clear)
+    for (int i = threadIdx.x; i < n; i += blockDim.x) small[i] = 0;
 }
 
 // dst[i] = v.p[i] for i < n: small tables written in stream order with the
@@ -968,19 +971,11 @@ __global__ void k_store_ptrs(void **dst, PtrBatch v, int32_t n) {
 // ---- launchers ---------------------------------------------------------------
 
 hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
-                                  int32_t n_types, int64_t total, int64_t *small,
-                                  hipStream_t stream) {
+                                  int32_t n_types, int64_t total, uint32_t epoch,
+                                  int64_t *small, hipStream_t stream) {
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_insert_frontier, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, hv, ts, n_types, total, small);
-  return hipGetLastError();
-}
-
-hipError_t launch_reset_map(HopView hv, const TypeStatic *ts, int32_t n_types,
-                            int64_t total, int64_t *small, int32_t n_small,
-                            hipStream_t stream) {
-  hipLaunchKernelGGL(k_reset_map, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, hv, ts, n_types, total, small, n_small);
+                     stream, hv, ts, n_types, total, epoch, small);
   return hipGetLastError();
 }
 
@@ -1076,17 +1071,17 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
 
 hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
                        int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
-                       hipStream_t stream) {
+                       uint32_t map_epoch, hipStream_t stream) {
   if (n_edges <= 0) return hipSuccess;
   const int64_t blocks = (n_edges + kMarkEdges - 1) / kMarkEdges;
   hipLaunchKernelGGL(k_mark, dim3(unsigned(blocks)), dim3(256), 0, stream, es,
-                     small + kSlotNew + n_types, n_etypes, n_edges, src_gid);
+                     small + kSlotNew + n_types, n_etypes, n_edges, src_gid, map_epoch);
   return hipGetLastError();
 }
 
-hipError_t launch_publish(const int64_t *small, int64_t *host, int32_t n, uint64_t seq,
+hipError_t launch_publish(int64_t *small, int64_t *host, int32_t n, uint64_t seq, bool clear,
                           hipStream_t stream) {
-  hipLaunchKernelGGL(k_publish, dim3(1), dim3(256), 0, stream, small, host, n, seq);
+  hipLaunchKernelGGL(k_publish, dim3(1), dim3(256), 0, stream, small, host, n, seq, clear);
   return hipGetLastError();
 }
 
