@@ -3,14 +3,14 @@
 // compaction relabels vertices and edges).
 //
 // The newly reached vertices of a node type are deduplicated and put in
-// ascending ID order with one bit per vertex: the sampler sets bit v for every
-// kept source v that is not in the frontier yet; a prefix count of the set
-// bits (per node type) then gives each one its rank, which is its position
-// among the new vertices.  The count is a reduce-then-scan over kTile-word
-// tiles in three launches (count per tile; scan of the tile counts; rank and
-// assign), which needs no inter-block waiting.  A dense int32 map (vertex ->
-// local ID, -1 when absent) holds the local IDs of the frontier and of the new
-// vertices for the relabel.
+// ascending ID order with one bit per vertex: the sampler sets bit v in the
+// reached bitmap for every kept source v, and the new vertices are the reached
+// bits not in the frontier bitmap; a prefix count of those bits (per node type)
+// then gives each one its rank, which is its position among the new vertices.
+// The count is a reduce-then-scan over kTile-word tiles in three launches
+// (count per tile; scan of the tile counts; rank and assign), which needs no
+// inter-block waiting.  A dense map (vertex -> call epoch and local ID) holds
+// the local IDs of the frontier and of the new vertices for the relabel.
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -36,7 +36,8 @@ struct CompactArgs {
   HopView hv;
   const TypeStatic *ts;
   int32_t n_types;
-  uint32_t *bitmap;
+  uint32_t *bitmap;  // reached this hop
+  uint32_t *fbits;   // in the frontier
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
@@ -46,8 +47,24 @@ struct CompactArgs {
   uint32_t map_epoch;
 };
 
-__device__ __forceinline__ uint2 tile_words(const CompactArgs &A, int64_t tile) {
-  return *reinterpret_cast<const uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems);
+// A thread's share of a tile: the reached words and the frontier words.
+struct TileWords {
+  uint2 reached, front;
+  __device__ uint2 fresh() const {  // reached, not yet in the frontier
+    return uint2{reached.x & ~front.x, reached.y & ~front.y};
+  }
+};
+__device__ __forceinline__ TileWords tile_words(const CompactArgs &A, int64_t tile) {
+  const int64_t w = tile * kTile + threadIdx.x * kTileItems;
+  return TileWords{*reinterpret_cast<const uint2 *>(A.bitmap + w),
+                   *reinterpret_cast<const uint2 *>(A.fbits + w)};
+}
+// Clears the thread's reached words (when any bit is set).
+__device__ __forceinline__ void clear_reached(const CompactArgs &A, int64_t tile,
+                                              const TileWords &tw) {
+  if ((tw.reached.x | tw.reached.y) != 0)
+    *reinterpret_cast<uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems) =
+        uint2{0, 0};
 }
 
 // Copies kTile frontier entries into the head of the source lists.
@@ -74,10 +91,13 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_count(CompactArgs A) {
     return;
   }
   static_assert(kTileItems == 2, "one 8-byte load per thread");
-  const uint2 w = tile_words(A, tile);
+  const TileWords tw = tile_words(A, tile);
+  const uint2 w = tw.fresh();
   int64_t total;
   block_excl_scan_256(__popc(w.x) + __popc(w.y), lds, &total);
   if (threadIdx.x == 0) A.tile_cnt[tile] = int32_t(total);
+  // a tile without new vertices is done: the assign pass skips it
+  if (total == 0) clear_reached(A, tile, tw);
 }
 
 // 2. Exclusive scan of the tile counts over all tiles, in one block: tile_pre
@@ -115,11 +135,16 @@ __global__ __launch_bounds__(kScanThreads) void k_bits_scan(CompactArgs A) {
     A.small[kSlotNew + t] = A.tile_pre[A.tile_base[t + 1]] - A.tile_pre[A.tile_base[t]];
 }
 
-// Gives the set bits of a tile's words `ab` (thread's share), the first of
-// which has local ID `local`, their local IDs and clears the words.
+// Gives the new vertices of the thread's share of a tile (the first has local
+// ID `local`) their local IDs, adds them to the frontier bits and clears the
+// reached bits.
 __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t first,
-                                            int64_t tile, uint2 ab, int64_t local) {
+                                            int64_t tile, const TileWords &tw, int64_t local) {
+  clear_reached(A, tile, tw);
+  const uint2 ab = tw.fresh();
   if ((ab.x | ab.y) == 0) return;
+  *reinterpret_cast<uint2 *>(A.fbits + tile * kTile + threadIdx.x * kTileItems) =
+      uint2{tw.front.x | ab.x, tw.front.y | ab.y};
   uint64_t *map = A.ts[t].map;
   int64_t *out = A.hv.src_out[t];
   const uint32_t words[kTileItems] = {ab.x, ab.y};
@@ -136,7 +161,6 @@ __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t
       ++local;
     }
   }
-  *reinterpret_cast<uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems) = uint2{0, 0};
 }
 
 // 3. Ranks the set bits of a tile within its node type, gives each new vertex
@@ -146,11 +170,12 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_assign(CompactArgs A) {
   const int64_t tile = blockIdx.x;
   if (A.tile_cnt[tile] == 0) return;
   const int t = find_segment(A.tile_base, A.n_types, tile);
-  const uint2 ab = tile_words(A, tile);
+  const TileWords tw = tile_words(A, tile);
+  const uint2 ab = tw.fresh();
   int64_t total;
   const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &total);
   const int64_t first = A.tile_base[t];
-  assign_bits(A, t, first, tile, ab,
+  assign_bits(A, t, first, tile, tw,
               A.hv.nF[t] + (A.tile_pre[tile] - A.tile_pre[first]) + pre);
 }
 
@@ -168,7 +193,8 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_single(CompactArgs A, uin
   }
   const int t = find_segment(A.tile_base, A.n_types, tile);
   const int64_t first = A.tile_base[t];
-  const uint2 ab = tile_words(A, tile);
+  const TileWords tw = tile_words(A, tile);
+  const uint2 ab = tw.fresh();
   int64_t agg[1];
   const int64_t pre = block_excl_scan_256(__popc(ab.x) + __popc(ab.y), lds, &agg[0]);
   int64_t ex[1];
@@ -176,7 +202,7 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_single(CompactArgs A, uin
                    ex, A.small);
   if (tile == A.tile_base[t + 1] - 1 && threadIdx.x == 0)
     A.small[kSlotNew + t] = ex[0] + agg[0];  // new vertices of type t
-  assign_bits(A, t, first, tile, ab, A.hv.nF[t] + ex[0] + pre);
+  assign_bits(A, t, first, tile, tw, A.hv.nF[t] + ex[0] + pre);
 }
 
 // Next hop's frontier sizes (this hop's plus the new vertices of each type)
@@ -214,11 +240,11 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
 }  // namespace
 
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
-                          uint32_t *bitmap, const int64_t *tile_base,
+                          uint32_t *bitmap, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, uint32_t map_epoch,
                           int64_t *small, int64_t *ticketed, hipStream_t stream) {
-  CompactArgs A{hv, ts, n_types, bitmap, tile_base, n_tiles, copy_total, tile_sums,
+  CompactArgs A{hv, ts, n_types, bitmap, fbits, tile_base, n_tiles, copy_total, tile_sums,
                 reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small, map_epoch};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
   *ticketed = 0;

@@ -75,16 +75,22 @@ struct EtypeStatic {
   const int64_t *indptr;
   const int64_t *indices;
   uint64_t *src_map;      // vertex -> local-ID map of the source type
-  uint32_t *src_bitmap;   // new-vertex bitmap of the source type
+  uint32_t *src_bitmap;   // reached-vertex bitmap of the source type
+  const uint32_t *src_fbits;  // frontier bitmap of the source type
   int64_t n_dst_nodes;
   int32_t src_type;
   int32_t dst_type;
 };
 
 // Static per node type (per workspace).
+// Per node type two bitmaps, one bit per vertex: `bitmap` collects the sources
+// of a hop's kept edges (the sampler sets their bits), `fbits` holds the
+// frontier.  A hop's new vertices are bitmap & ~fbits; the compaction adds them
+// to fbits and clears bitmap.  Both are zero between calls.
 struct TypeStatic {
   uint64_t *map;
   uint32_t *bitmap;
+  uint32_t *fbits;
   int64_t num_nodes;
 };
 
@@ -151,8 +157,8 @@ int graph_device(const hg_graph *g);
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
 
-// The hop-0 frontier: map[seed] = (epoch, position); flags range errors and
-// repeats.
+// The hop-0 frontier: map[seed] = (epoch, position) and its frontier bit;
+// flags range errors and repeats.
 hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
                                   int32_t n_types, int64_t total, uint32_t epoch,
                                   int64_t *small, hipStream_t stream);
@@ -185,12 +191,6 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          ExclView X, hipStream_t stream);
 
-// Sets the bitmap bit of every kept edge's source that is not in the
-// frontier of its type yet (edges of etype e are [ebase[e], ebase[e+1]),
-// ebase = small + kSlotNew + n_types).
-hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
-                       int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
-                       uint32_t map_epoch, hipStream_t stream);
 
 // Compaction pass: per bitmap tile, ranks of the set bits within the node
 // type -> local IDs n_frontier + rank, written to the map and the source
@@ -202,7 +202,7 @@ hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_ty
 // tile_sums: device scratch of 2 * n_tiles + 2 64-bit words.
 constexpr int64_t kSinglePassTiles = 256;
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
-                          uint32_t *bitmap, const int64_t *tile_base,
+                          uint32_t *bitmap, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, uint32_t map_epoch,
                           int64_t *small, int64_t *ticketed, hipStream_t stream);
@@ -211,6 +211,13 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.
 // Block 0 also writes the next hop's frontier sizes (this hop's plus its new
 // vertices) and pair layout into `next`.
+// Sets the reached bit of every kept edge's source that is not in the
+// frontier of its type (edges of etype e are [ebase[e], ebase[e+1]), ebase =
+// small + kSlotNew + n_types).
+hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
+                       int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
+                       hipStream_t stream);
+
 hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,

@@ -2,15 +2,17 @@
 // workspaces, per-hop orchestration of the gfx950 kernels, and error state.
 //
 // One mini-batch (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2.2) runs
-// hop by hop, five launches per hop on the caller's stream:
+// hop by hop, five steps per hop on the caller's stream:
 //   1. counting pass : per (frontier vertex, etype) pair its kept-edge count
 //                      and output offsets (single-pass scan)   -> wait (sizes)
 //   2. sampler       : the kept edges
-//   3. marks         : sources not yet in the frontier set a bitmap bit
-//   4. compaction    : new vertices numbered in ascending ID, frontier copied
-//                      to the head of the source lists; the last block plans
-//                      the next hop's pairs on the device
-//   5. relabel       : edges get local source IDs
+//   3. marks         : kept sources not in the frontier set their bit in the
+//                      reached bitmap of their type
+//   4. compaction    : the reached vertices are numbered in ascending ID and
+//                      join the frontier bitmap; the frontier is copied to the
+//                      head of the source lists
+//   5. relabel       : edges get local source IDs; the first block plans the
+//                      next hop's pairs on the device
 // The source list of hop h is the frontier of hop h+1.  The host waits once
 // per hop (after 1, for the output sizes) and once at the end.
 #include "hg.h"
@@ -123,7 +125,8 @@ struct Scratch {
 struct Workspace {
   uint64_t *map = nullptr;         // sum of num_nodes: (call epoch, local ID)
   uint32_t map_epoch = 0;          // epoch of the last call (entries start at epoch 0)
-  uint32_t *bitmap = nullptr;      // n_tiles * kTile words
+  uint32_t *bitmap = nullptr;      // n_tiles * kTile words: reached this hop
+  uint32_t *fbits = nullptr;       // n_tiles * kTile words: in the frontier
   int64_t *dsmall = nullptr;       // readback slots
   int64_t *hsmall = nullptr;       // pinned, coherent mirror of dsmall + a flag word
   uint64_t publish_seq = 0;        // flag value of the last publish
@@ -309,6 +312,7 @@ void free_workspace(Workspace *w) {
   }
   (void)hipFree(w->map);
   (void)hipFree(w->bitmap);
+  (void)hipFree(w->fbits);
   (void)hipFree(w->dsmall);
   (void)hipFree(w->d_es);
   (void)hipFree(w->d_ts);
@@ -351,6 +355,8 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(uint64_t) * size_t(std::max<int64_t>(map_n, 1)));
     if (e == hipSuccess)
       e = hipMalloc(&w->bitmap, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
+    if (e == hipSuccess)
+      e = hipMalloc(&w->fbits, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
     if (e == hipSuccess) e = hipMalloc(&w->d_es, sizeof(EtypeStatic) * size_t(std::max(g->R, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->d_ts, sizeof(TypeStatic) * size_t(g->T));
@@ -368,18 +374,20 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (e == hipSuccess)
       e = launch_fill_i32(reinterpret_cast<int32_t *>(w->tile_sums), 4 * n_lb + 4, 0, stream);
     if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
+    if (e == hipSuccess) e = launch_fill_u32(w->fbits, g->n_tiles * kTile, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
       for (int32_t i = 0; i < g->R; ++i) {
         const ETypeInfo &E = g->et[i];
         es[i] = EtypeStatic{E.indptr, E.indices, w->map + g->map_off[E.src],
                             w->bitmap + g->tile_base[E.src] * kTile,
+                            w->fbits + g->tile_base[E.src] * kTile,
                             g->nt[E.dst].num_nodes, E.src, E.dst};
       }
       std::vector<TypeStatic> ts(g->T);
       for (int32_t t = 0; t < g->T; ++t)
         ts[t] = TypeStatic{w->map + g->map_off[t], w->bitmap + g->tile_base[t] * kTile,
-                           g->nt[t].num_nodes};
+                           w->fbits + g->tile_base[t] * kTile, g->nt[t].num_nodes};
       e = hipMemcpy(w->d_es, es.data(), sizeof(EtypeStatic) * es.size(), hipMemcpyHostToDevice);
       if (e == hipSuccess)
         e = hipMemcpy(w->d_ts, ts.data(), sizeof(TypeStatic) * ts.size(), hipMemcpyHostToDevice);
@@ -588,11 +596,12 @@ struct SampleRun {
     return hipSuccess;
   }
 
-  // Leaves the bitmap and the readback slots clean; releases the workspace.
+  // Leaves the bitmaps and the readback slots clean; releases the workspace.
   // (The map needs nothing: the next call has a new epoch.)
   void finish(bool ok) {
     if (!ws->poisoned) {
       if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
+      (void)launch_fill_u32(ws->fbits, g->n_tiles * kTile, 0u, stream);
       if (!small_clean)
         (void)launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall),
                               2 * int64_t(small_slots(g)), 0, stream);
@@ -823,7 +832,7 @@ hg_status SampleRun::run_edges() {
   uint32_t epoch;
   int64_t ticketed = 0;
   if ((e = next_epoch(&epoch)) != hipSuccess ||
-      (e = launch_compact(pv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, 0,
+      (e = launch_compact(pv, ws->d_ts, T, ws->bitmap, ws->fbits, g->d_tile_base, g->n_tiles, 0,
                           ws->tile_sums, epoch, ticket_base, map_epoch, ws->dsmall, &ticketed,
                           stream)) != hipSuccess)
     return fail_device(e, "edge batch: seeds");
@@ -953,7 +962,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
             hipSuccess)
       return fail_device(e, "tables");
 
-    // ---- 2-4. sample, compact, relabel -------------------------------------
+    // ---- 2-5. sample, mark, compact, relabel -------------------------------
     bitmap_dirty = true;
     int64_t copy_total = 0;
     for (int64_t n : nF) copy_total += n;
@@ -963,12 +972,12 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
                            src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream)) !=
         hipSuccess)
       return fail_device(e, "sample");
-    if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, map_epoch, stream)) !=
-        hipSuccess)
+    if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
       return fail_device(e, "mark");
     int64_t ticketed = 0;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
-        (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, g->d_tile_base, g->n_tiles, copy_total,
+        (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, ws->fbits, g->d_tile_base, g->n_tiles,
+                            copy_total,
                             ws->tile_sums, epoch, ticket_base, map_epoch, ws->dsmall, &ticketed,
                             stream)) != hipSuccess)
       return fail_device(e, "compact");

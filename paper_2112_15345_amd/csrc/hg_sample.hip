@@ -88,6 +88,7 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
       atomicOr(err, kErrSeedRange);
       continue;
     }
+    atomicOr(ts[t].fbits + (v >> 5), 1u << (v & 31));
     // claim the entry unless this call already did (a repeated seed); a
     // failed exchange means another seed of this call took it
     unsigned long long *m = reinterpret_cast<unsigned long long *>(&ts[t].map[v]);
@@ -821,11 +822,11 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
 
 // ---- new-vertex marks ----------------------------------------------------------
 
-// Sets bit v of the source type's bitmap for every kept edge whose source v
-// is not in the frontier of its type yet (map[v] < 0).  Popular sources recur
-// across many edges, and atomics on one word serialize, so each block first
-// merges its edges' bits per bitmap word in an LDS hash table and then
-// issues one atomic per distinct word.
+// Sets bit v of the source type's reached bitmap for every kept edge whose
+// source v is not in the frontier of its type yet (its frontier bit is clear).
+// Popular sources recur across many edges, and atomics on one word serialize,
+// so each block first merges its edges' bits per bitmap word in an LDS hash
+// table and then issues one atomic per distinct word.
 constexpr int kMarkPerThread = 4;
 constexpr int kMarkEdges = 256 * kMarkPerThread;  // edges per block
 constexpr int kMarkSlots = 2048;                  // hash slots (power of two)
@@ -834,11 +835,11 @@ constexpr uint64_t kEmptySlot = ~uint64_t(0);
 
 __global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64_t *ebase,
                                               int32_t n_etypes, int64_t n_edges,
-                                              const int64_t *src_gid, uint32_t map_epoch) {
+                                              const int64_t *src_gid) {
   __shared__ uint64_t s_key[kMarkSlots];   // word address
   __shared__ uint32_t s_bits[kMarkSlots];
   __shared__ int64_t s_eb[kMarkMaxEtypes + 1];
-  __shared__ const uint64_t *s_map[kMarkMaxEtypes];
+  __shared__ const uint32_t *s_front[kMarkMaxEtypes];
   __shared__ uint32_t *s_bm[kMarkMaxEtypes];
   const bool staged = n_etypes <= kMarkMaxEtypes;
   for (int i = threadIdx.x; i < kMarkSlots; i += blockDim.x) {
@@ -849,7 +850,7 @@ __global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64
     for (int e = threadIdx.x; e <= n_etypes; e += blockDim.x) {
       s_eb[e] = ebase[e];
       if (e < n_etypes) {
-        s_map[e] = es[e].src_map;
+        s_front[e] = es[e].src_fbits;
         s_bm[e] = es[e].src_bitmap;
       }
     }
@@ -873,8 +874,8 @@ __global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64
   for (int k = 0; k < kMarkPerThread; ++k) {
     need[k] = false;
     if (g[k] >= 0) {
-      const uint64_t *map = staged ? s_map[et[k]] : es[et[k]].src_map;
-      need[k] = !map_has(map[g[k]], map_epoch);  // not in the frontier yet
+      const uint32_t *front = staged ? s_front[et[k]] : es[et[k]].src_fbits;
+      need[k] = ((front[g[k] >> 5] >> (g[k] & 31)) & 1u) == 0;  // not in the frontier yet
     }
   }
 #pragma unroll
@@ -1071,11 +1072,11 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
 
 hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
                        int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
-                       uint32_t map_epoch, hipStream_t stream) {
+                       hipStream_t stream) {
   if (n_edges <= 0) return hipSuccess;
   const int64_t blocks = (n_edges + kMarkEdges - 1) / kMarkEdges;
   hipLaunchKernelGGL(k_mark, dim3(unsigned(blocks)), dim3(256), 0, stream, es,
-                     small + kSlotNew + n_types, n_etypes, n_edges, src_gid, map_epoch);
+                     small + kSlotNew + n_types, n_etypes, n_edges, src_gid);
   return hipGetLastError();
 }
 
