@@ -27,22 +27,23 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 
-# Measured HBM traffic of one gather launch on the default run (academic
-# workload, 3 warm-up + 20 timed mini-batches): FETCH_SIZE and WRITE_SIZE
-# from two rocprofv3 --pmc passes, scaled by what the counters read for a
-# 1 GiB device copy (profiles/gather_academic_traffic.md).  Valid only for
-# the gather source it was measured on.
-GATHER_TRAFFIC = {"source_sha256_16": "321cb231c9462224", "workload": 2, "steps": 20, "warmup": 3,
-                  "bytes_per_launch": 248912521.6}
+# Measured HBM traffic of one gather launch of the default run (academic
+# workload, bundles of 16, 32 warm-up + 320 timed mini-batches): FETCH_SIZE
+# and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the counters
+# read for a 1 GiB device copy (profiles/gather_academic_traffic.md).  Valid
+# only for the gather source and the launch configuration it was measured on.
+GATHER_TRAFFIC = {"source_sha256_16": "26e6b8abbb8a5ffb", "workload": 2, "steps": 320,
+                  "warmup": 32, "bundle": 16, "workers": 0, "bytes_per_launch": 3989462851.1}
 
 
-def measured_gather_traffic(workload, steps, warmup):
+def measured_gather_traffic(args):
     import hashlib
     src = os.path.join(ROOT, "paper_2112_15345_amd", "csrc", "hg_gather.hip")
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     t = GATHER_TRAFFIC
-    if (digest, workload, steps, warmup) != (t["source_sha256_16"], t["workload"], t["steps"],
-                                              t["warmup"]):
+    if (digest, args.workload, args.steps, args.warmup, args.bundle, args.workers) != (
+            t["source_sha256_16"], t["workload"], t["steps"], t["warmup"], t["bundle"],
+            t["workers"]):
         return None
     return t["bytes_per_launch"]
 
@@ -84,24 +85,87 @@ def cpu_baseline(gen, wl, first_batch, budget_s=12.0, max_batches=8):
             "gathered_GBps": nbytes / spent / 1e9}
 
 
+def link_main(args, wl, gen, g):
+    """Edge-seeded (link-prediction) mini-batches: targets of one forward
+    relation, their endpoints as seeds, one negative per target, targets and
+    their reverse edges excluded, the paper's link-prediction fanouts [25, 15]
+    per hop, every featured type gathered.  One direct call per step."""
+    import torch
+
+    import paper_2112_15345_amd as hg
+    import workloads as W
+
+    dev = g.device
+    rev_et, rev_eid = W.reverse_maps(gen)
+    exclude = hg.HG_EXCLUDE_REVERSE if rev_et is not None else hg.HG_EXCLUDE_SELF
+    link_et = gen.etype_names.index("cites") if "cites" in gen.etype_names else 0
+    fan = [[k] * g.R for k in W.LINK_FANOUTS]
+    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
+    n_batches = args.warmup + args.steps
+    targets = [[None if x is None else torch.as_tensor(x, device=dev)
+                for x in W.link_targets(gen, b, link_et)] for b in range(n_batches)]
+
+    def step(b):
+        return g.sample_edge_blocks(targets[b], fan, b, n_neg=W.LINK_NEG, exclude=exclude,
+                                    rev_etype=rev_et, rev_eid=rev_eid, gather=feat_types)
+
+    for b in range(args.warmup):
+        step(b)
+    torch.cuda.synchronize()
+    edges = rows = gbytes = 0
+    t_start = time.perf_counter()
+    for b in range(args.warmup, n_batches):
+        blocks = step(b)
+        edges += sum(blocks.num_edges(h, r) for h in range(len(fan)) for r in range(g.R))
+        for t in feat_types:
+            n = blocks.num_input_nodes(t)
+            rows += n
+            gbytes += n * row_bytes[t]
+        del blocks
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    result = {
+        "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
+        "value": edges / elapsed, "unit": "sampled edges/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64",
+        "data": "synthetic (seeded generator shaped like the paper's workloads)",
+        "config": {"workload": wl.name + f"; link prediction: {W.LINK_BATCH} target edges of "
+                               f"'{gen.etype_names[link_et]}', {W.LINK_NEG} negative each, "
+                               f"exclusion {exclude}, fanout {list(W.LINK_FANOUTS)}",
+                   "workload_index": args.workload, "task": "link",
+                   "parallelism": "single GPU", "pipeline": "direct calls"},
+        "gathered_GBps": gbytes / elapsed / 1e9,
+        "sampled_edges_per_step": edges / args.steps,
+        "gathered_rows_per_step": rows / args.steps,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--steps", type=int, default=320)
+    ap.add_argument("--warmup", type=int, default=32)
     ap.add_argument("--workload", type=int, default=2,
                     help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
                          "5 gather-heavy academic")
-    ap.add_argument("--workers", type=int, default=4,
-                    help="pipeline worker threads (own streams); 0 = one direct call per step")
-    ap.add_argument("--bundle", type=int, default=1,
-                    help="mini-batches per launch sequence (hg_sample_blocks_bundle)")
+    ap.add_argument("--workers", type=int, default=0,
+                    help="pipeline worker threads (own streams); 0 = direct calls (default)")
+    ap.add_argument("--bundle", type=int, default=16,
+                    help="mini-batches per launch sequence (hg_sample_blocks_bundle, 1..16)")
     ap.add_argument("--depth", type=int, default=0,
                     help="mini-batches outstanding in the pipeline (default 2 x workers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after warm-up (untimed), copy this many MiB device to device "
                          "once: a copy of known size for scaling memory counters")
+    ap.add_argument("--task", choices=("vertex", "link"), default="vertex",
+                    help="vertex: mini-batches from seed vertices (the default); link: "
+                         "edge-seeded link-prediction mini-batches (hg_sample_edge_blocks, "
+                         "direct calls)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
@@ -121,6 +185,8 @@ def main():
     log(f"generated '{wl.name}' in {time.perf_counter() - t0:.1f}s")
     g = hg.Graph(list(zip(gen.num_nodes, gen.feats)),
                  [(s, d, ip, ix) for s, d, ip, ix in gen.etypes], device=dev)
+    if args.task == "link":
+        return link_main(args, wl, gen, g)
     fan = wl.fanout_matrix()
     n_batches = args.warmup + args.steps
     seeds = [[None if s is None else torch.as_tensor(s, device=dev)
@@ -281,7 +347,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "k_gather_multi (feature gather, all types)",
                      "achieved": g_achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": g_achieved / HBM_PEAK_GBS,
-                     "traffic": measured_gather_traffic(args.workload, args.steps, args.warmup),
+                     "traffic": measured_gather_traffic(args),
                      "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
                      "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3,
                      "isolated_achieved": iso_gbps,
