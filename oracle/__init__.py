@@ -22,10 +22,11 @@ OK, EINVAL, ENOMEM, EUNSUPPORTED = 0, -1, -2, -4
 
 def build(out: str = _LIB, extra_flags=(), src: str = _SRC) -> str:
     """Compile oracle.c with gcc into a shared library (plain C11, -O2)."""
+    tmp = f"{out}.{os.getpid()}.tmp"  # concurrent builders never share a file
     cmd = ["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-I", _HERE, *extra_flags, src, "-o", out + ".tmp"]
+           "-I", _HERE, *extra_flags, src, "-o", tmp]
     subprocess.run(cmd, check=True)
-    os.replace(out + ".tmp", out)
+    os.replace(tmp, out)
     return out
 
 

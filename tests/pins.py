@@ -41,10 +41,11 @@ def rocrand_ref():
     if _rr is None:
         if not os.path.exists(_RR_LIB) or os.path.getmtime(_RR_LIB) < os.path.getmtime(_RR_SRC):
             os.makedirs(os.path.dirname(_RR_LIB), exist_ok=True)
+            tmp = f"{_RR_LIB}.{os.getpid()}.tmp"  # concurrent builders never share a file
             subprocess.run(["/opt/rocm/bin/hipcc", "-x", "hip", "-O1", "-fPIC", "-shared",
                             "--offload-arch=gfx950", "-I/opt/rocm/include", _RR_SRC, "-o",
-                            _RR_LIB + ".tmp"], check=True, capture_output=True)
-            os.replace(_RR_LIB + ".tmp", _RR_LIB)
+                            tmp], check=True, capture_output=True)
+            os.replace(tmp, _RR_LIB)
         lib = ctypes.CDLL(_RR_LIB)
         lib.rr_word.argtypes = [ctypes.c_uint64] * 3
         lib.rr_word.restype = ctypes.c_uint32
