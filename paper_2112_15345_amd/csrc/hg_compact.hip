@@ -9,8 +9,9 @@
 // then gives each one its rank, which is its position among the new vertices.
 // The count is a reduce-then-scan over kTile-word tiles in three launches
 // (count per tile; scan of the tile counts; rank and assign), which needs no
-// inter-block waiting.  A dense map (vertex -> call epoch and local ID) holds
-// the local IDs of the frontier and of the new vertices for the relabel.
+// inter-block waiting.  A dense int32 map (vertex -> local ID, meaningful while
+// the vertex's frontier bit is set) holds the local IDs of the frontier and of
+// the new vertices for the relabel.
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -44,7 +45,6 @@ struct CompactArgs {
   int64_t *tile_pre;  // [n_tiles + 1] set bits in earlier tiles, of any type (or look-back words)
   int32_t *tile_cnt;  // per tile: set bits
   int64_t *small;
-  uint32_t map_epoch;
 };
 
 // A thread's share of a tile: the reached words and the frontier words.
@@ -145,7 +145,7 @@ __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t
   if ((ab.x | ab.y) == 0) return;
   *reinterpret_cast<uint2 *>(A.fbits + tile * kTile + threadIdx.x * kTileItems) =
       uint2{tw.front.x | ab.x, tw.front.y | ab.y};
-  uint64_t *map = A.ts[t].map;
+  int32_t *map = A.ts[t].map;
   int64_t *out = A.hv.src_out[t];
   const uint32_t words[kTileItems] = {ab.x, ab.y};
   const int64_t v0 = ((tile - first) * kTile + threadIdx.x * kTileItems) * 32;
@@ -156,7 +156,7 @@ __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t
       const int bit = __ffs(m) - 1;
       m &= m - 1;
       const int64_t v = v0 + k * 32 + bit;
-      map[v] = map_entry(A.map_epoch, local);
+      map[v] = int32_t(local);
       out[local] = v;
       ++local;
     }
@@ -233,7 +233,7 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
   const int64_t *ebase = small + kSlotNew + n_types;
   for (int64_t j = gs_start(); j < n_edges; j += gs_step()) {
     const int e = find_segment(ebase, n_etypes, j);
-    src_local[j] = map_local(es[e].src_map[src_gid[j]]);
+    src_local[j] = es[e].src_map[src_gid[j]];
   }
 }
 
@@ -242,10 +242,10 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
-                          uint32_t epoch, uint64_t ticket_base, uint32_t map_epoch,
-                          int64_t *small, int64_t *ticketed, hipStream_t stream) {
+                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
+                          int64_t *ticketed, hipStream_t stream) {
   CompactArgs A{hv, ts, n_types, bitmap, fbits, tile_base, n_tiles, copy_total, tile_sums,
-                reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small, map_epoch};
+                reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
   *ticketed = 0;
   if (n_tiles <= kSinglePassTiles) {

@@ -149,12 +149,12 @@ __global__ __launch_bounds__(256) void k_edge_relabel(EdgeBatchArgs A, HopView f
     const EtypeStatic &E = A.es[e];
     const int64_t u = A.tsrc[x], v = A.tdst[x];
     if (u < 0) continue;  // an invalid target: the call fails
-    const int32_t lu = map_local(E.src_map[u]);
-    const int32_t lv = map_local(A.ts[E.dst_type].map[v]);
+    const int32_t lu = E.src_map[u];
+    const int32_t lv = A.ts[E.dst_type].map[v];
     A.pos_src[x] = lu;
     A.pos_dst[x] = lv;
     for (int k = 0; k < A.n_neg; ++k)
-      A.neg_dst[x * A.n_neg + k] = map_local(A.ts[E.dst_type].map[A.tneg[x * A.n_neg + k]]);
+      A.neg_dst[x * A.n_neg + k] = A.ts[E.dst_type].map[A.tneg[x * A.n_neg + k]];
     if (A.exclude >= 1) {
       const int64_t j = A.et[e].eids[x - A.tbase[e]];
       if (edge_insert(A, hkey(e, j))) pair_add(A, hkey(e, lv));

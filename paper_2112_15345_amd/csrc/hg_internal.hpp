@@ -58,23 +58,16 @@ constexpr int32_t kErrLookback = 4;    // a scan wait exceeded its bound
 constexpr int32_t kErrBound = 8;       // more pairs or chunks than buffers were sized for
 constexpr int32_t kErrTarget = 16;     // a target edge out of range, or a bad reverse edge
 
-// The dense vertex -> local-ID map of a workspace holds one 64-bit entry per
-// vertex: the call epoch in the high word, the local ID in the low word.  An
-// entry belongs to the current call only if it carries the call's epoch, so
-// the map never needs clearing between calls.
-__host__ __device__ inline uint64_t map_entry(uint32_t epoch, int64_t local) {
-  return (uint64_t(epoch) << 32) | uint64_t(uint32_t(local));
-}
-__host__ __device__ inline bool map_has(uint64_t w, uint32_t epoch) {
-  return uint32_t(w >> 32) == epoch;
-}
-__host__ __device__ inline int32_t map_local(uint64_t w) { return int32_t(uint32_t(w)); }
+// The dense vertex -> local-ID map of a workspace holds one int32 per vertex.
+// An entry is meaningful only while the vertex's frontier bit is set (see
+// TypeStatic); the frontier bitmap is cleared after every call, so stale
+// entries are never read and the map itself is never cleared.
 
 // Static per edge type (per workspace).
 struct EtypeStatic {
   const int64_t *indptr;
   const int64_t *indices;
-  uint64_t *src_map;      // vertex -> local-ID map of the source type
+  int32_t *src_map;       // vertex -> local-ID map of the source type
   uint32_t *src_bitmap;   // reached-vertex bitmap of the source type
   const uint32_t *src_fbits;  // frontier bitmap of the source type
   int64_t n_dst_nodes;
@@ -88,7 +81,7 @@ struct EtypeStatic {
 // frontier.  A hop's new vertices are bitmap & ~fbits; the compaction adds them
 // to fbits and clears bitmap.  Both are zero between calls.
 struct TypeStatic {
-  uint64_t *map;
+  int32_t *map;
   uint32_t *bitmap;
   uint32_t *fbits;
   int64_t num_nodes;
@@ -157,11 +150,11 @@ int graph_device(const hg_graph *g);
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
 
-// The hop-0 frontier: map[seed] = (epoch, position) and its frontier bit;
-// flags range errors and repeats.
+// The hop-0 frontier: the seed's frontier bit, map[seed] = position; flags
+// range errors and repeats (a frontier bit already set).
 hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
-                                  int32_t n_types, int64_t total, uint32_t epoch,
-                                  int64_t *small, hipStream_t stream);
+                                  int32_t n_types, int64_t total, int64_t *small,
+                                  hipStream_t stream);
 
 // Counting pass over n_items >= P + 1 pair slots (P = pair_base[R]): per pair
 // its in-edge range; exclusive scans of kept edges, hub chunks, wavefront
@@ -204,8 +197,8 @@ constexpr int64_t kSinglePassTiles = 256;
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint32_t *bitmap, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
-                          uint32_t epoch, uint64_t ticket_base, uint32_t map_epoch,
-                          int64_t *small, int64_t *ticketed, hipStream_t stream);
+                          uint32_t epoch, uint64_t ticket_base, int64_t *small,
+                          int64_t *ticketed, hipStream_t stream);
 
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.

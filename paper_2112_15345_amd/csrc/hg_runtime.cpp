@@ -121,10 +121,9 @@ struct Scratch {
 };
 
 // Per-call device state.  One call uses a workspace at a time; between calls
-// the bitmap is all 0, and no map entry carries the next call's epoch.
+// both bitmaps are all 0 (so no map entry is meaningful).
 struct Workspace {
-  uint64_t *map = nullptr;         // sum of num_nodes: (call epoch, local ID)
-  uint32_t map_epoch = 0;          // epoch of the last call (entries start at epoch 0)
+  int32_t *map = nullptr;          // sum of num_nodes: local IDs
   uint32_t *bitmap = nullptr;      // n_tiles * kTile words: reached this hop
   uint32_t *fbits = nullptr;       // n_tiles * kTile words: in the frontier
   int64_t *dsmall = nullptr;       // readback slots
@@ -352,7 +351,7 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     const size_t small_n = small_slots(g);
     const int64_t n_lb = std::max<int64_t>(g->n_tiles, 1);
     hipError_t e = hipSuccess;
-    if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(uint64_t) * size_t(std::max<int64_t>(map_n, 1)));
+    if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(int32_t) * size_t(std::max<int64_t>(map_n, 1)));
     if (e == hipSuccess)
       e = hipMalloc(&w->bitmap, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
     if (e == hipSuccess)
@@ -367,7 +366,6 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
                         hipHostMallocCoherent);
     if (e == hipSuccess) std::memset(w->hsmall, 0, sizeof(int64_t) * (small_n + 1));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&w->done, hipEventDisableTiming);
-    if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t *>(w->map), 2 * map_n, 0u, stream);
     if (e == hipSuccess)
       e = launch_fill_i32(reinterpret_cast<int32_t *>(w->dsmall), 2 * int64_t(small_n), 0, stream);
     // look-back words of the single-pass compaction: no stale epoch
@@ -475,9 +473,8 @@ struct SampleRun {
   size_t sig_bytes;              // the sigma table heads the call's tables
   uint64_t ticket_base = 0;
 
-  // the call's map epoch; the bitmap is clean unless bitmap_dirty; the
-  // readback slots are zero again once a clearing publish has run
-  uint32_t map_epoch = 0;
+  // the reached bitmap is clean unless bitmap_dirty; the readback slots are
+  // zero again once a clearing publish has run
   bool bitmap_dirty = false;
   bool small_clean = false;
 
@@ -584,20 +581,9 @@ struct SampleRun {
     return HG_OK;
   }
 
-  // Starts the call's map epoch (refilling the map before epochs repeat).
-  hipError_t begin_map() {
-    if (ws->map_epoch == 0xFFFFFFFFu) {
-      hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t *>(ws->map),
-                                     2 * g->map_off[g->T], 0u, stream);
-      if (e != hipSuccess) return e;
-      ws->map_epoch = 0;
-    }
-    map_epoch = ++ws->map_epoch;
-    return hipSuccess;
-  }
-
   // Leaves the bitmaps and the readback slots clean; releases the workspace.
-  // (The map needs nothing: the next call has a new epoch.)
+  // (The map needs nothing: with the frontier bits cleared, no entry is
+  // meaningful.)
   void finish(bool ok) {
     if (!ws->poisoned) {
       if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
@@ -684,9 +670,8 @@ hg_status SampleRun::run(const int64_t *const *seeds, const int64_t *n_seeds) {
     return fail_device(e, "start");
   int64_t total = 0;
   for (int64_t n : nF) total += n;
-  if ((e = begin_map()) != hipSuccess ||
-      (e = launch_insert_frontier(view(0), ws->d_ts, T, total, map_epoch, ws->dsmall,
-                                  stream)) != hipSuccess)
+  if ((e = launch_insert_frontier(view(0), ws->d_ts, T, total, ws->dsmall, stream)) !=
+      hipSuccess)
     return fail_device(e, "insert seeds");
   if (H == 0) {
     if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
@@ -820,7 +805,6 @@ hg_status SampleRun::run_edges() {
   }
 
   // ---- seeds: mark the endpoints, rank them, relabel the pair graphs --------
-  if ((e = begin_map()) != hipSuccess) return fail_device(e, "edge batch: map");
   bitmap_dirty = true;
   if ((e = launch_edge_targets(A, stream)) != hipSuccess) return fail_device(e, "edge targets");
   char *d = dreg(pre);
@@ -833,7 +817,7 @@ hg_status SampleRun::run_edges() {
   int64_t ticketed = 0;
   if ((e = next_epoch(&epoch)) != hipSuccess ||
       (e = launch_compact(pv, ws->d_ts, T, ws->bitmap, ws->fbits, g->d_tile_base, g->n_tiles, 0,
-                          ws->tile_sums, epoch, ticket_base, map_epoch, ws->dsmall, &ticketed,
+                          ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
                           stream)) != hipSuccess)
     return fail_device(e, "edge batch: seeds");
   ticket_base += uint64_t(ticketed);
@@ -978,7 +962,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     if ((e = next_epoch(&epoch)) != hipSuccess ||
         (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, ws->fbits, g->d_tile_base, g->n_tiles,
                             copy_total,
-                            ws->tile_sums, epoch, ticket_base, map_epoch, ws->dsmall, &ticketed,
+                            ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
                             stream)) != hipSuccess)
       return fail_device(e, "compact");
     ticket_base += uint64_t(ticketed);

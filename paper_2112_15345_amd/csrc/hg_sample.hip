@@ -75,8 +75,7 @@ __device__ __forceinline__ bool is_excluded(const ExclView &X, int e, uint64_t e
 // ---- frontier map maintenance --------------------------------------------
 
 __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
-                                  int32_t n_types, int64_t total, uint32_t epoch,
-                                  int64_t *small) {
+                                  int32_t n_types, int64_t total, int64_t *small) {
   int32_t *err = reinterpret_cast<int32_t *>(small + kSlotErr);
   for (int64_t x = grid_stride_start(); x < total; x += grid_stride_step()) {
     int64_t first;
@@ -88,20 +87,13 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
       atomicOr(err, kErrSeedRange);
       continue;
     }
-    atomicOr(ts[t].fbits + (v >> 5), 1u << (v & 31));
-    // claim the entry unless this call already did (a repeated seed); a
-    // failed exchange means another seed of this call took it
-    unsigned long long *m = reinterpret_cast<unsigned long long *>(&ts[t].map[v]);
-    unsigned long long old = *m;
-    for (;;) {
-      if (map_has(old, epoch)) {
-        atomicOr(err, kErrSeedRepeat);
-        break;
-      }
-      const unsigned long long prev = atomicCAS(m, old, map_entry(epoch, i));
-      if (prev == old) break;
-      old = prev;
-    }
+    // the first seed to set the frontier bit owns the vertex; a later one
+    // is a repeat
+    const uint32_t bit = 1u << (v & 31);
+    if (atomicOr(ts[t].fbits + (v >> 5), bit) & bit)
+      atomicOr(err, kErrSeedRepeat);
+    else
+      ts[t].map[v] = int32_t(i);
   }
 }
 
@@ -972,11 +964,11 @@ __global__ void k_store_ptrs(void **dst, PtrBatch v, int32_t n) {
 // ---- launchers ---------------------------------------------------------------
 
 hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
-                                  int32_t n_types, int64_t total, uint32_t epoch,
-                                  int64_t *small, hipStream_t stream) {
+                                  int32_t n_types, int64_t total, int64_t *small,
+                                  hipStream_t stream) {
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_insert_frontier, dim3(grid_for(total, 256)), dim3(256), 0,
-                     stream, hv, ts, n_types, total, epoch, small);
+                     stream, hv, ts, n_types, total, small);
   return hipGetLastError();
 }
 
