@@ -3,10 +3,11 @@
 // compaction relabels vertices and edges).
 //
 // The newly reached vertices of a node type are deduplicated and put in
-// ascending ID order with one bit per vertex: the sampler sets bit v in the
-// reached bitmap for every kept source v, and the new vertices are the reached
-// bits not in the frontier bitmap; a prefix count of those bits (per node type)
-// then gives each one its rank, which is its position among the new vertices.
+// ascending ID order with one flag per vertex: the sampler stores 1 into the
+// reached byte of every kept source v, and the new vertices are the reached
+// vertices whose frontier bit is clear; a prefix count of those (per node
+// type) then gives each one its rank, which is its position among the new
+// vertices.
 // The count is a reduce-then-scan over kTile-word tiles in three launches
 // (count per tile; scan of the tile counts; rank and assign), which needs no
 // inter-block waiting.  A dense int32 map (vertex -> local ID, meaningful while
@@ -37,8 +38,8 @@ struct CompactArgs {
   HopView hv;
   const TypeStatic *ts;
   int32_t n_types;
-  uint32_t *bitmap;  // reached this hop
-  uint32_t *fbits;   // in the frontier
+  uint8_t *reached;  // reached this hop (one byte per vertex)
+  uint32_t *fbits;   // in the frontier (one bit per vertex)
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
@@ -47,24 +48,45 @@ struct CompactArgs {
   int64_t *small;
 };
 
-// A thread's share of a tile: the reached words and the frontier words.
+// Four flag bytes (each 0 or 1) as four bits: byte k of x lands on bit 24 + k
+// of x * 0x01020408, with no carries from the other partial products.
+__device__ __forceinline__ uint32_t pack4(uint32_t x) {
+  return ((x & 0x01010101u) * 0x01020408u) >> 24;
+}
+__device__ __forceinline__ uint32_t pack16(uint4 v) {
+  return pack4(v.x) | (pack4(v.y) << 4) | (pack4(v.z) << 8) | (pack4(v.w) << 12);
+}
+
+// A thread's share of a tile (kTileItems * 32 vertices): their reached flags
+// as bits, and their frontier words.
 struct TileWords {
   uint2 reached, front;
   __device__ uint2 fresh() const {  // reached, not yet in the frontier
     return uint2{reached.x & ~front.x, reached.y & ~front.y};
   }
 };
+static_assert(kTileItems == 2, "a thread covers 64 vertices");
+__device__ __forceinline__ const uint4 *reached_of(const CompactArgs &A, int64_t tile) {
+  return reinterpret_cast<const uint4 *>(A.reached + (tile * kTile + threadIdx.x * kTileItems) * 32);
+}
 __device__ __forceinline__ TileWords tile_words(const CompactArgs &A, int64_t tile) {
+  const uint4 *r = reached_of(A, tile);
+  const uint4 r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
   const int64_t w = tile * kTile + threadIdx.x * kTileItems;
-  return TileWords{*reinterpret_cast<const uint2 *>(A.bitmap + w),
+  return TileWords{uint2{pack16(r0) | (pack16(r1) << 16), pack16(r2) | (pack16(r3) << 16)},
                    *reinterpret_cast<const uint2 *>(A.fbits + w)};
 }
-// Clears the thread's reached words (when any bit is set).
+// Clears the thread's reached bytes (when any is set).
 __device__ __forceinline__ void clear_reached(const CompactArgs &A, int64_t tile,
                                               const TileWords &tw) {
-  if ((tw.reached.x | tw.reached.y) != 0)
-    *reinterpret_cast<uint2 *>(A.bitmap + tile * kTile + threadIdx.x * kTileItems) =
-        uint2{0, 0};
+  if ((tw.reached.x | tw.reached.y) != 0) {
+    uint4 *r = const_cast<uint4 *>(reached_of(A, tile));
+    const uint4 z{0, 0, 0, 0};
+    r[0] = z;
+    r[1] = z;
+    r[2] = z;
+    r[3] = z;
+  }
 }
 
 // Copies kTile frontier entries into the head of the source lists.
@@ -240,11 +262,11 @@ __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
 }  // namespace
 
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
-                          uint32_t *bitmap, uint32_t *fbits, const int64_t *tile_base,
+                          uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
                           int64_t *ticketed, hipStream_t stream) {
-  CompactArgs A{hv, ts, n_types, bitmap, fbits, tile_base, n_tiles, copy_total, tile_sums,
+  CompactArgs A{hv, ts, n_types, reached, fbits, tile_base, n_tiles, copy_total, tile_sums,
                 reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
   *ticketed = 0;

@@ -7,11 +7,10 @@
 //     over indptr), its negative destinations (Philox4x32-10 at counter
 //     (eid, 2^31 | k, etype), words 0 and 1 as u, destination
 //     floor(u * n / 2^64)), and its reverse edge under exclusion 2 (checked
-//     to run the other way).  Every endpoint sets its bit in the new-vertex
-//     bitmap of its type.
-//  2. The compaction pass of the hops (hg_compact.hip) then ranks the bits
-//     from an empty frontier: the seeds of each type in ascending ID, with
-//     their local IDs in the map.
+//     to run the other way).  Every endpoint sets its reached flag.
+//  2. The compaction pass of the hops (hg_compact.hip) then ranks the reached
+//     vertices from an empty frontier: the seeds of each type in ascending
+//     ID, with their local IDs in the map.
 //  3. k_edge_relabel: the pair graphs' local IDs, the exclusion hash tables
 //     (the excluded edges, and per pair with excluded in-edges their number),
 //     and hop 0's frontier sizes and pair layout.
@@ -50,9 +49,7 @@ __device__ int64_t edge_dst(const int64_t *indptr, int64_t n_dst, int64_t eid) {
   return a;
 }
 
-__device__ __forceinline__ void mark(uint32_t *bitmap, int64_t v) {
-  atomicOr(bitmap + (v >> 5), 1u << (v & 31));
-}
+__device__ __forceinline__ void mark(uint8_t *reached, int64_t v) { reached[v] = 1; }
 
 __device__ __forceinline__ void flag(int64_t *small, int32_t bits) {
   atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), bits);
@@ -76,8 +73,8 @@ __global__ __launch_bounds__(256) void k_edge_targets(EdgeBatchArgs A) {
     const int64_t v = edge_dst(E.indptr, E.n_dst_nodes, j);
     A.tsrc[x] = u;
     A.tdst[x] = v;
-    mark(E.src_bitmap, u);
-    mark(A.ts[E.dst_type].bitmap, v);
+    mark(E.src_reached, u);
+    mark(A.ts[E.dst_type].reached, v);
     for (int k = 0; k < A.n_neg; ++k) {
       const U32x4 r = philox4x32_10(
           U32x4{uint32_t(j), uint32_t(uint64_t(j) >> 32), 0x80000000u | uint32_t(k), uint32_t(e)},
@@ -85,7 +82,7 @@ __global__ __launch_bounds__(256) void k_edge_targets(EdgeBatchArgs A) {
       const uint64_t w = uint64_t(r.x) | (uint64_t(r.y) << 32);
       const int64_t nv = int64_t(__umul64hi(w, uint64_t(E.n_dst_nodes)));
       A.tneg[x * A.n_neg + k] = nv;
-      mark(A.ts[E.dst_type].bitmap, nv);
+      mark(A.ts[E.dst_type].reached, nv);
     }
     if (A.exclude == 2 && T.rev >= 0) {
       // the reverse edge must run from v back to u in the reverse type

@@ -68,21 +68,23 @@ struct EtypeStatic {
   const int64_t *indptr;
   const int64_t *indices;
   int32_t *src_map;       // vertex -> local-ID map of the source type
-  uint32_t *src_bitmap;   // reached-vertex bitmap of the source type
-  const uint32_t *src_fbits;  // frontier bitmap of the source type
+  uint8_t *src_reached;   // reached flags of the source type
   int64_t n_dst_nodes;
   int32_t src_type;
   int32_t dst_type;
 };
 
 // Static per node type (per workspace).
-// Per node type two bitmaps, one bit per vertex: `bitmap` collects the sources
-// of a hop's kept edges (the sampler sets their bits), `fbits` holds the
-// frontier.  A hop's new vertices are bitmap & ~fbits; the compaction adds them
-// to fbits and clears bitmap.  Both are zero between calls.
+// Per node type one flag byte and one frontier bit per vertex: the sampler
+// stores 1 into the `reached` byte of every kept edge's source (a plain store,
+// so that popular sources cost no atomics), and `fbits` holds the frontier.  A
+// hop's new vertices are the reached vertices whose frontier bit is clear; the
+// compaction adds them to fbits and clears the reached bytes.  Both are zero
+// between calls.  The layouts follow the bitmap tiles: type t starts at tile
+// tile_base[t], a tile covering kTile * 32 vertices.
 struct TypeStatic {
   int32_t *map;
-  uint32_t *bitmap;
+  uint8_t *reached;
   uint32_t *fbits;
   int64_t num_nodes;
 };
@@ -195,7 +197,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
 // tile_sums: device scratch of 2 * n_tiles + 2 64-bit words.
 constexpr int64_t kSinglePassTiles = 256;
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
-                          uint32_t *bitmap, uint32_t *fbits, const int64_t *tile_base,
+                          uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
                           int64_t *ticketed, hipStream_t stream);
@@ -204,13 +206,6 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.
 // Block 0 also writes the next hop's frontier sizes (this hop's plus its new
 // vertices) and pair layout into `next`.
-// Sets the reached bit of every kept edge's source that is not in the
-// frontier of its type (edges of etype e are [ebase[e], ebase[e+1]), ebase =
-// small + kSlotNew + n_types).
-hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
-                       int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
-                       hipStream_t stream);
-
 hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,

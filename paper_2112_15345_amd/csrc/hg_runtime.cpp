@@ -2,16 +2,15 @@
 // workspaces, per-hop orchestration of the gfx950 kernels, and error state.
 //
 // One mini-batch (DistDGLv2, arXiv 2112.15345, Sec. 3.2 and Sec. 4.2.2) runs
-// hop by hop, five steps per hop on the caller's stream:
+// hop by hop, four steps per hop on the caller's stream:
 //   1. counting pass : per (frontier vertex, etype) pair its kept-edge count
 //                      and output offsets (single-pass scan)   -> wait (sizes)
-//   2. sampler       : the kept edges
-//   3. marks         : kept sources not in the frontier set their bit in the
-//                      reached bitmap of their type
-//   4. compaction    : the reached vertices are numbered in ascending ID and
-//                      join the frontier bitmap; the frontier is copied to the
-//                      head of the source lists
-//   5. relabel       : edges get local source IDs; the first block plans the
+//   2. sampler       : the kept edges; each stores 1 into the reached flag
+//                      of its source
+//   3. compaction    : reached vertices not in the frontier are numbered in
+//                      ascending ID and join the frontier bitmap; the frontier
+//                      is copied to the head of the source lists
+//   4. relabel       : edges get local source IDs; the first block plans the
 //                      next hop's pairs on the device
 // The source list of hop h is the frontier of hop h+1.  The host waits once
 // per hop (after 1, for the output sizes) and once at the end.
@@ -124,7 +123,7 @@ struct Scratch {
 // both bitmaps are all 0 (so no map entry is meaningful).
 struct Workspace {
   int32_t *map = nullptr;          // sum of num_nodes: local IDs
-  uint32_t *bitmap = nullptr;      // n_tiles * kTile words: reached this hop
+  uint8_t *reached = nullptr;      // n_tiles * kTile * 32 bytes: reached this hop
   uint32_t *fbits = nullptr;       // n_tiles * kTile words: in the frontier
   int64_t *dsmall = nullptr;       // readback slots
   int64_t *hsmall = nullptr;       // pinned, coherent mirror of dsmall + a flag word
@@ -310,7 +309,7 @@ void free_workspace(Workspace *w) {
     (void)hipEventDestroy(w->done);
   }
   (void)hipFree(w->map);
-  (void)hipFree(w->bitmap);
+  (void)hipFree(w->reached);
   (void)hipFree(w->fbits);
   (void)hipFree(w->dsmall);
   (void)hipFree(w->d_es);
@@ -353,7 +352,7 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMalloc(&w->map, sizeof(int32_t) * size_t(std::max<int64_t>(map_n, 1)));
     if (e == hipSuccess)
-      e = hipMalloc(&w->bitmap, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
+      e = hipMalloc(&w->reached, size_t(std::max<int64_t>(g->n_tiles * kTile * 32, 1)));
     if (e == hipSuccess)
       e = hipMalloc(&w->fbits, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
@@ -371,20 +370,21 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     // look-back words of the single-pass compaction: no stale epoch
     if (e == hipSuccess)
       e = launch_fill_i32(reinterpret_cast<int32_t *>(w->tile_sums), 4 * n_lb + 4, 0, stream);
-    if (e == hipSuccess) e = launch_fill_u32(w->bitmap, g->n_tiles * kTile, 0u, stream);
+    if (e == hipSuccess)
+      e = launch_fill_u32(reinterpret_cast<uint32_t *>(w->reached), g->n_tiles * kTile * 8, 0u,
+                          stream);
     if (e == hipSuccess) e = launch_fill_u32(w->fbits, g->n_tiles * kTile, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
       for (int32_t i = 0; i < g->R; ++i) {
         const ETypeInfo &E = g->et[i];
         es[i] = EtypeStatic{E.indptr, E.indices, w->map + g->map_off[E.src],
-                            w->bitmap + g->tile_base[E.src] * kTile,
-                            w->fbits + g->tile_base[E.src] * kTile,
+                            w->reached + g->tile_base[E.src] * kTile * 32,
                             g->nt[E.dst].num_nodes, E.src, E.dst};
       }
       std::vector<TypeStatic> ts(g->T);
       for (int32_t t = 0; t < g->T; ++t)
-        ts[t] = TypeStatic{w->map + g->map_off[t], w->bitmap + g->tile_base[t] * kTile,
+        ts[t] = TypeStatic{w->map + g->map_off[t], w->reached + g->tile_base[t] * kTile * 32,
                            w->fbits + g->tile_base[t] * kTile, g->nt[t].num_nodes};
       e = hipMemcpy(w->d_es, es.data(), sizeof(EtypeStatic) * es.size(), hipMemcpyHostToDevice);
       if (e == hipSuccess)
@@ -473,9 +473,9 @@ struct SampleRun {
   size_t sig_bytes;              // the sigma table heads the call's tables
   uint64_t ticket_base = 0;
 
-  // the reached bitmap is clean unless bitmap_dirty; the readback slots are
+  // the reached flags are clean unless reached_dirty; the readback slots are
   // zero again once a clearing publish has run
-  bool bitmap_dirty = false;
+  bool reached_dirty = false;
   bool small_clean = false;
 
   // an edge-seeded call: its batch, the excluded edges and its extra tables
@@ -586,7 +586,9 @@ struct SampleRun {
   // meaningful.)
   void finish(bool ok) {
     if (!ws->poisoned) {
-      if (bitmap_dirty) (void)launch_fill_u32(ws->bitmap, g->n_tiles * kTile, 0u, stream);
+      if (reached_dirty)
+        (void)launch_fill_u32(reinterpret_cast<uint32_t *>(ws->reached), g->n_tiles * kTile * 8, 0u,
+                              stream);
       (void)launch_fill_u32(ws->fbits, g->n_tiles * kTile, 0u, stream);
       if (!small_clean)
         (void)launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall),
@@ -805,7 +807,7 @@ hg_status SampleRun::run_edges() {
   }
 
   // ---- seeds: mark the endpoints, rank them, relabel the pair graphs --------
-  bitmap_dirty = true;
+  reached_dirty = true;
   if ((e = launch_edge_targets(A, stream)) != hipSuccess) return fail_device(e, "edge targets");
   char *d = dreg(pre);
   const HopView pv{reinterpret_cast<int64_t *>(d + lay.nf),
@@ -816,12 +818,12 @@ hg_status SampleRun::run_edges() {
   uint32_t epoch;
   int64_t ticketed = 0;
   if ((e = next_epoch(&epoch)) != hipSuccess ||
-      (e = launch_compact(pv, ws->d_ts, T, ws->bitmap, ws->fbits, g->d_tile_base, g->n_tiles, 0,
+      (e = launch_compact(pv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles, 0,
                           ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
                           stream)) != hipSuccess)
     return fail_device(e, "edge batch: seeds");
   ticket_base += uint64_t(ticketed);
-  bitmap_dirty = false;
+  reached_dirty = false;
   if ((e = launch_edge_relabel(A, view(0), g->d_tile_base, stream)) != hipSuccess)
     return fail_device(e, "edge batch: pairs");
   std::vector<int64_t> nF(bound);  // bounds until the first wait
@@ -946,8 +948,8 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
             hipSuccess)
       return fail_device(e, "tables");
 
-    // ---- 2-5. sample, mark, compact, relabel -------------------------------
-    bitmap_dirty = true;
+    // ---- 2-4. sample (and mark), compact, relabel ----------------------------
+    reached_dirty = true;
     int64_t copy_total = 0;
     for (int64_t n : nF) copy_total += n;
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
@@ -956,17 +958,15 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
                            src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream)) !=
         hipSuccess)
       return fail_device(e, "sample");
-    if ((e = launch_mark(ws->d_es, ws->dsmall, T, R, S, gid_tmp, stream)) != hipSuccess)
-      return fail_device(e, "mark");
     int64_t ticketed = 0;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
-        (e = launch_compact(hv, ws->d_ts, T, ws->bitmap, ws->fbits, g->d_tile_base, g->n_tiles,
+        (e = launch_compact(hv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles,
                             copy_total,
                             ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
                             stream)) != hipSuccess)
       return fail_device(e, "compact");
     ticket_base += uint64_t(ticketed);
-    bitmap_dirty = false;
+    reached_dirty = false;
     if ((e = launch_relabel(hv, nv, ws->d_es, g->d_tile_base, ws->dsmall, T, R, S, gid_tmp,
                             srcl_all, stream)) != hipSuccess)
       return fail_device(e, "relabel");

@@ -284,6 +284,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 
 struct EmitCtx {
   const int64_t *indices;
+  uint8_t *src_reached;
   int64_t *src_gid;
   int64_t *eid;
   int32_t *dst_local;
@@ -293,15 +294,17 @@ struct EmitCtx {
 __device__ __forceinline__ EmitCtx make_ctx(const EtypeStatic &E, int64_t *src_gid,
                                             int64_t *eid, int32_t *dst_local,
                                             int64_t dst) {
-  return EmitCtx{E.indices, src_gid, eid, dst_local, int32_t(dst)};
+  return EmitCtx{E.indices, E.src_reached, src_gid, eid, dst_local, int32_t(dst)};
 }
 
-// Writes kept edge `e` at output slot `pos`.
+// Writes kept edge `e` at output slot `pos`; its source is reached.
 __device__ __forceinline__ void emit_edge(const EmitCtx &c, int64_t pos,
                                           int64_t e) {
-  c.src_gid[pos] = c.indices[e];
+  const int64_t g = c.indices[e];
+  c.src_gid[pos] = g;
   c.eid[pos] = e;
   c.dst_local[pos] = c.dst;
+  c.src_reached[g] = 1;
 }
 
 // Keys of the four edges 4g .. 4g+3.
@@ -506,9 +509,12 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
     const int k = t - L.tpre[a];
     const int64_t ed = L.lo[a] + k;
     const int64_t pos = L.start[a] + k;
-    A.src_gid[pos] = A.es[L.etype[a]].indices[ed];
+    const EtypeStatic &E = A.es[L.etype[a]];
+    const int64_t g = E.indices[ed];
+    A.src_gid[pos] = g;
     A.eid[pos] = ed;
     A.dst_local[pos] = L.dst[a];
+    E.src_reached[g] = 1;
   }
 }
 
@@ -812,90 +818,6 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   }
 }
 
-// ---- new-vertex marks ----------------------------------------------------------
-
-// Sets bit v of the source type's reached bitmap for every kept edge whose
-// source v is not in the frontier of its type yet (its frontier bit is clear).
-// Popular sources recur across many edges, and atomics on one word serialize,
-// so each block first merges its edges' bits per bitmap word in an LDS hash
-// table and then issues one atomic per distinct word.
-constexpr int kMarkPerThread = 4;
-constexpr int kMarkEdges = 256 * kMarkPerThread;  // edges per block
-constexpr int kMarkSlots = 2048;                  // hash slots (power of two)
-constexpr int kMarkMaxEtypes = 256;               // etype table staged in LDS
-constexpr uint64_t kEmptySlot = ~uint64_t(0);
-
-__global__ __launch_bounds__(256) void k_mark(const EtypeStatic *es, const int64_t *ebase,
-                                              int32_t n_etypes, int64_t n_edges,
-                                              const int64_t *src_gid) {
-  __shared__ uint64_t s_key[kMarkSlots];   // word address
-  __shared__ uint32_t s_bits[kMarkSlots];
-  __shared__ int64_t s_eb[kMarkMaxEtypes + 1];
-  __shared__ const uint32_t *s_front[kMarkMaxEtypes];
-  __shared__ uint32_t *s_bm[kMarkMaxEtypes];
-  const bool staged = n_etypes <= kMarkMaxEtypes;
-  for (int i = threadIdx.x; i < kMarkSlots; i += blockDim.x) {
-    s_key[i] = kEmptySlot;
-    s_bits[i] = 0;
-  }
-  if (staged)
-    for (int e = threadIdx.x; e <= n_etypes; e += blockDim.x) {
-      s_eb[e] = ebase[e];
-      if (e < n_etypes) {
-        s_front[e] = es[e].src_fbits;
-        s_bm[e] = es[e].src_bitmap;
-      }
-    }
-  __syncthreads();
-  const int64_t j0 = int64_t(blockIdx.x) * kMarkEdges + threadIdx.x;
-  // loads first, all independent, then the table updates
-  int64_t g[kMarkPerThread];
-  int et[kMarkPerThread];
-#pragma unroll
-  for (int k = 0; k < kMarkPerThread; ++k) {
-    const int64_t j = j0 + k * 256;
-    g[k] = -1;
-    et[k] = 0;
-    if (j < n_edges) {
-      et[k] = staged ? find_segment(s_eb, n_etypes, j) : find_segment(ebase, n_etypes, j);
-      g[k] = src_gid[j];
-    }
-  }
-  bool need[kMarkPerThread];
-#pragma unroll
-  for (int k = 0; k < kMarkPerThread; ++k) {
-    need[k] = false;
-    if (g[k] >= 0) {
-      const uint32_t *front = staged ? s_front[et[k]] : es[et[k]].src_fbits;
-      need[k] = ((front[g[k] >> 5] >> (g[k] & 31)) & 1u) == 0;  // not in the frontier yet
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < kMarkPerThread; ++k) {
-    if (!need[k]) continue;
-    uint32_t *bm = staged ? s_bm[et[k]] : es[et[k]].src_bitmap;
-    const uint64_t word = reinterpret_cast<uint64_t>(bm + (g[k] >> 5));
-    const uint32_t bit = 1u << (g[k] & 31);
-    // open addressing on the word address
-    uint32_t h = uint32_t((word >> 2) * 0x9E3779B97F4A7C15ull >> 40) & (kMarkSlots - 1);
-    for (int probe = 0; probe < kMarkSlots; ++probe) {
-      const uint64_t cur = atomicCAS(reinterpret_cast<unsigned long long *>(&s_key[h]),
-                                     (unsigned long long)kEmptySlot,
-                                     (unsigned long long)word);
-      if (cur == kEmptySlot || cur == word) {
-        atomicOr(&s_bits[h], bit);
-        break;
-      }
-      h = (h + 1) & (kMarkSlots - 1);
-    }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < kMarkSlots; i += blockDim.x) {
-    const uint64_t word = s_key[i];
-    if (word != kEmptySlot) atomicOr(reinterpret_cast<uint32_t *>(word), s_bits[i]);
-  }
-}
-
 // ---- small utilities -------------------------------------------------------
 
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
@@ -1059,16 +981,6 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
     const int64_t hb = (n_hubs + kSampleWaves - 1) / kSampleWaves;
     hipLaunchKernelGGL(k_hub_finish, dim3(unsigned(hb)), dim3(kSampleThreads), 0, stream, A);
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_mark(const EtypeStatic *es, const int64_t *small, int32_t n_types,
-                       int32_t n_etypes, int64_t n_edges, const int64_t *src_gid,
-                       hipStream_t stream) {
-  if (n_edges <= 0) return hipSuccess;
-  const int64_t blocks = (n_edges + kMarkEdges - 1) / kMarkEdges;
-  hipLaunchKernelGGL(k_mark, dim3(unsigned(blocks)), dim3(256), 0, stream, es,
-                     small + kSlotNew + n_types, n_etypes, n_edges, src_gid);
   return hipGetLastError();
 }
 
