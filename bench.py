@@ -26,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 
 # Measured HBM traffic of one gather launch of the default run (academic
 # workload, bundles of 16, 32 warm-up + 320 timed mini-batches): FETCH_SIZE
@@ -162,6 +163,9 @@ def main():
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after warm-up (untimed), copy this many MiB device to device "
                          "once: a copy of known size for scaling memory counters")
+    ap.add_argument("--host-features", action="store_true",
+                    help="feature tables in pinned host memory, gathered over the host link "
+                         "(zero-copy); the gather rate then includes that link")
     ap.add_argument("--task", choices=("vertex", "link"), default="vertex",
                     help="vertex: mini-batches from seed vertices (the default); link: "
                          "edge-seeded link-prediction mini-batches (hg_sample_edge_blocks, "
@@ -180,7 +184,11 @@ def main():
     wl = W.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
-    gen = W.make_graph(wl, device=dev)
+    gen = W.make_graph(wl, device=dev, feat_device="cpu" if args.host_features else None)
+    if args.host_features:
+        gen.feats = [None if f is None else
+                     torch.empty(f.shape, dtype=f.dtype, pin_memory=True).copy_(f)
+                     for f in gen.feats]
     torch.cuda.synchronize()
     log(f"generated '{wl.name}' in {time.perf_counter() - t0:.1f}s")
     g = hg.Graph(list(zip(gen.num_nodes, gen.feats)),
@@ -306,7 +314,9 @@ def main():
         blocks = g.sample_blocks(seeds[b], fan, b, gather=feat_types,
                                  events=(iso.events[0], iso.events[1]))
         iso_ms += iso.elapsed_ms(iso.events[0], iso.events[1])
-        iso_bytes += sum(blocks.num_input_nodes(t) * (2 * row_bytes[t] + 8) for t in feat_types)
+        iso_bytes += sum(blocks.num_input_nodes(t) *
+                         (row_bytes[t] if args.host_features else 2 * row_bytes[t] + 8)
+                         for t in feat_types)
         del blocks
     iso_gbps = iso_bytes / (iso_ms / 1e3) / 1e9 if iso_ms > 0 else 0.0
 
@@ -316,9 +326,14 @@ def main():
     g_alg = sum(n * (2 * row_bytes[t] + 8) for _, _, rows_t in gather_rec
                 for t, n in rows_t.items())
     g_achieved = g_alg / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
+    if args.host_features:
+        # the rows cross the host link once; that link is the roof
+        g_alg = sum(n * row_bytes[t] for _, _, rows_t in gather_rec for t, n in rows_t.items())
+        g_achieved = g_alg / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
     log(f"{args.steps} steps: {ms_per_step:.3f} ms/step, gather {g_ms / len(gather_rec):.4f} "
         f"ms/launch, {g_achieved:.0f} GB/s algorithmic")
 
+    peak = HOST_LINK_PEAK_GBS if args.host_features else HBM_PEAK_GBS
     result = {
         "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
         "value": edges / elapsed,
@@ -337,6 +352,7 @@ def main():
                    "node_types": len(gen.num_nodes), "edge_types": g.R,
                    "edges_in_graph": int(sum(ix.numel() for _, _, _, ix in gen.etypes)),
                    "parallelism": "single GPU",
+                   "features": "pinned host memory" if args.host_features else "HBM",
                    "bundle": max(1, args.bundle),
                    "pipeline": (f"{args.workers} worker streams" if args.workers
                                 else "direct calls")},
@@ -344,14 +360,15 @@ def main():
         "sampled_edges_per_step": edges / args.steps,
         "gathered_rows_per_step": rows / args.steps,
         "gather_kernel_ms_per_step": g_ms / args.steps,
-        "roofline": {"bound": "hbm", "kernel": "k_gather_multi (feature gather, all types)",
-                     "achieved": g_achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": g_achieved / HBM_PEAK_GBS,
-                     "traffic": measured_gather_traffic(args),
+        "roofline": {"bound": "host link" if args.host_features else "hbm",
+                     "kernel": "k_gather_multi (feature gather, all types)",
+                     "achieved": g_achieved, "peak": peak, "unit": "GB/s",
+                     "frac": g_achieved / peak,
+                     "traffic": None if args.host_features else measured_gather_traffic(args),
                      "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
                      "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3,
                      "isolated_achieved": iso_gbps,
-                     "isolated_frac": iso_gbps / HBM_PEAK_GBS},
+                     "isolated_frac": iso_gbps / peak},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(gen, wl, first_batch=args.warmup)

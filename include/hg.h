@@ -51,9 +51,12 @@ typedef enum hg_dtype {
 } hg_dtype;
 
 /* One node type (Sec. 4.1.4: features are stored per node type, in an ID
- * space of that type).  feat: device, row-major [num_nodes, dim] of `dtype`,
- * rows contiguous; NULL with dtype HG_DT_NONE for a featureless type.
- * Borrowed: it must stay valid until hg_destroy. */
+ * space of that type).  feat: row-major [num_nodes, dim] of `dtype`, rows
+ * contiguous, in device memory or in pinned host memory (hipHostMalloc; the
+ * paper keeps features in CPU memory, Sec. 4.1): the gathers read a pinned
+ * table through its device mapping, over the host link, with no staging copy.
+ * Pageable host memory is refused (HG_EINVAL).  NULL with dtype HG_DT_NONE for
+ * a featureless type.  Borrowed: it must stay valid until hg_destroy. */
 typedef struct hg_ntype_desc {
   int64_t num_nodes;
   const void *feat;

@@ -78,11 +78,38 @@ struct DeviceGuard {
 
 struct NTypeInfo {
   int64_t num_nodes;
-  const void *feat;
+  const void *feat;  // the address kernels read: device memory, or pinned host
+                     // memory through its device mapping
   int32_t dtype;
   int32_t dim;
   int64_t row_bytes;
+  bool host;         // the table lives in pinned host memory
 };
+
+// A feature table is device memory or pinned host memory (hipHostMalloc):
+// kernels read the latter through its device mapping, over the host link.
+// Pageable host memory is refused.
+hg_status feature_address(int32_t t, const void *feat, const void **addr, bool *host) {
+  hipPointerAttribute_t a{};
+  if (hipPointerGetAttributes(&a, feat) != hipSuccess ||
+      (a.type != hipMemoryTypeHost && a.type != hipMemoryTypeDevice &&
+       a.type != hipMemoryTypeManaged)) {
+    (void)hipGetLastError();
+    return fail(HG_EINVAL, "node type %d: the feature table is neither device memory nor "
+                           "pinned host memory", t);
+  }
+  *host = a.type == hipMemoryTypeHost;
+  *addr = feat;
+  if (*host) {
+    void *d = nullptr;
+    if (hipHostGetDevicePointer(&d, const_cast<void *>(feat), 0) != hipSuccess || !d) {
+      (void)hipGetLastError();
+      return fail(HG_EINVAL, "node type %d: pinned feature table has no device mapping", t);
+    }
+    *addr = d;
+  }
+  return HG_OK;
+}
 
 struct ETypeInfo {
   int32_t src, dst;
@@ -1063,7 +1090,16 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
   g->key_R = n_etypes;
   for (int32_t t = 0; t < n_ntypes; ++t) {
     const hg_ntype_desc &d = ntypes[t];
-    g->nt.push_back({d.num_nodes, d.feat, d.dtype, d.dim, dtype_size(d.dtype) * int64_t(d.dim)});
+    const void *addr = d.feat;
+    bool host = false;
+    if (d.dtype != HG_DT_NONE && d.num_nodes > 0) {
+      hg_status st = feature_address(t, d.feat, &addr, &host);
+      if (st != HG_OK) {
+        delete g;
+        return st;
+      }
+    }
+    g->nt.push_back({d.num_nodes, addr, d.dtype, d.dim, dtype_size(d.dtype) * int64_t(d.dim), host});
   }
   layout_types(g);
   for (int32_t i = 0; i < n_etypes; ++i) {
