@@ -419,7 +419,7 @@ struct SampleArgs {
   const EtypeStatic *es;
   int32_t n_etypes, n_types;
   int64_t n_pairs, n_wave, n_chunks, n_hubs;
-  int64_t blocks_a, blocks_b;
+  int64_t blocks_a, blocks_b, blocks_c;
   int64_t chunks_per_wave;
   PairArrays pa;
   uint64_t *cand;
@@ -454,8 +454,8 @@ __device__ __forceinline__ KeyCtx key_ctx(const SampleArgs &A, int e) {
 
 // Role A: a wavefront per 64 consecutive pairs.  Each lane writes its pair's
 // block-CSC entry; then the wavefront copies the in-edges of the small
-// take-all pairs among the 64, one output slot per lane.  Block 0 also writes
-// each etype's closing CSC entry.
+// take-all pairs among the 64, one output slot per lane.  The first block of
+// this role also writes each etype's closing CSC entry.
 struct GroupLds {
   int64_t start[kWave];   // first output slot of the pair
   int64_t lo[kWave];      // first in-edge slot
@@ -464,11 +464,12 @@ struct GroupLds {
   int32_t etype[kWave];
 };
 
-__device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group) {
+__device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group,
+                                 bool first_block) {
   const int lane = lane_id();
   const int64_t *ebase = A.small + kSlotNew + A.n_types;
   const int64_t *pb = A.hv.pair_base;
-  if (blockIdx.x == 0)
+  if (first_block)
     for (int e = threadIdx.x; e < A.n_etypes; e += kSampleThreads)
       A.indptr_all[pb[e + 1] + e] = ebase[e + 1] - ebase[e];
   const int64_t p = group * kWave + lane;
@@ -619,10 +620,10 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
 
 // Role C: wavefront w takes the hub chunks [w * chunks_per_wave, ...) in
 // order and appends each chunk's candidates (key < tau) to its hub's list.
-// The hub of the first chunk is found by binary search (the last hub whose
-// first chunk is not above it); later chunks walk on from there, so the
-// search and the hub's parameters are loaded once per run of chunks.
-constexpr int64_t kHubWaves = 16384;
+// The hub of the first chunk is found by a wavefront-wide search (the last
+// hub whose first chunk is not above it); later chunks walk on from there, so
+// the search and the hub's parameters are loaded once per run of chunks.
+constexpr int64_t kHubWaves = 65536;
 constexpr int64_t kMaxChunksPerWave = 16;
 
 struct HubParams {
@@ -699,18 +700,30 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
   }
 }
 
+// The last hub whose first chunk is not above chunk c (hub_choff strictly
+// increases from hub_choff[0] == 0).  A 64-ary search: every lane probes one
+// position per round, so the wavefront finds the hub in a few dependent loads
+// instead of one per halving.  All lanes of the wavefront must take part.
+__device__ int64_t find_hub(const SampleArgs &A, int64_t c) {
+  const int lane = lane_id();
+  int64_t lo = 0, hi = A.n_hubs;  // hub_choff[lo] <= c, and c < hub_choff[hi] (or hi = n_hubs)
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + kWave - 1) / kWave;
+    const int64_t pos = lo + int64_t(lane) * step;
+    const bool le = pos < hi && A.pa.hub_choff[pos] <= c;
+    // true on a prefix of the lanes, lane 0 always (its position is lo)
+    const uint64_t bal = __ballot(le);
+    const int last = 63 - __clzll((unsigned long long)bal);
+    lo += int64_t(last) * step;
+    hi = min(hi, lo + step);
+  }
+  return lo;
+}
+
 __device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
   const int64_t c_first = w * A.chunks_per_wave;
   const int64_t c_end = min(c_first + A.chunks_per_wave, A.n_chunks);
-  int64_t h_lo = 0, h_hi = A.n_hubs;  // hub_choff[h_lo] <= c_first < hub_choff[h_hi]
-  while (h_hi - h_lo > 1) {
-    const int64_t mid = (h_lo + h_hi) >> 1;
-    if (A.pa.hub_choff[mid] <= c_first)
-      h_lo = mid;
-    else
-      h_hi = mid;
-  }
-  HubParams H = hub_params(A, h_lo);
+  HubParams H = hub_params(A, find_hub(A, c_first));
   const uint32_t shift = uint32_t(32 - A.key_bits);
   for (int64_t chunk = c_first; chunk < c_end; ++chunk) {
     while (chunk >= H.end_chunk) H = hub_params(A, H.hub + 1);
@@ -805,16 +818,19 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   const int wave = threadIdx.x / kWave;
   if (b == 0 && int(threadIdx.x) < A.n_src_out)
     A.src_out_slot[threadIdx.x] = A.src_out_new[threadIdx.x];
-  if (b < A.blocks_a) {
-    // the candidate lists are not used by this role: reuse their LDS
-    GroupLds *g = reinterpret_cast<GroupLds *>(&s_key[wave][0]);
-    role_pair_groups(A, *g, b * kSampleWaves + wave);
-  } else if (b < A.blocks_a + A.blocks_b) {
-    const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
+  // the longest work first: hub chunks, then wavefront pairs, then groups of
+  // small take-all pairs, so that short blocks fill in behind long ones
+  if (b < A.blocks_c) {
+    const int64_t w = b * kSampleWaves + wave;
+    if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
+  } else if (b < A.blocks_c + A.blocks_b) {
+    const int64_t w = (b - A.blocks_c) * kSampleWaves + wave;
     if (w < A.n_wave) role_wave_pairs(A, s_key[wave], s_j[wave], w);
   } else {
-    const int64_t w = (b - A.blocks_a - A.blocks_b) * kSampleWaves + wave;
-    if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
+    // the candidate lists are not used by this role: reuse their LDS
+    const int64_t ba = b - A.blocks_c - A.blocks_b;
+    GroupLds *g = reinterpret_cast<GroupLds *>(&s_key[wave][0]);
+    role_pair_groups(A, *g, ba * kSampleWaves + wave, ba == 0);
   }
 }
 
@@ -962,6 +978,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.chunks_per_wave = std::min<int64_t>(kMaxChunksPerWave, std::max<int64_t>(1, n_chunks / kHubWaves));
   const int64_t waves_c = (n_chunks + A.chunks_per_wave - 1) / A.chunks_per_wave;
   const int64_t blocks_c = (waves_c + kSampleWaves - 1) / kSampleWaves;
+  A.blocks_c = blocks_c;
   A.pa = pa;
   A.cand = cand;
   A.small = small;
