@@ -89,6 +89,14 @@ def _bind(lib):
     lib.oracle_blocks_pairs.argtypes = [_P, ctypes.c_int32, _I64P, ctypes.POINTER(_P),
                                         ctypes.POINTER(_P), _I64P, ctypes.POINTER(_P)]
     lib.oracle_blocks_pairs.restype = ctypes.c_int
+    lib.oracle_layer_weight.argtypes = [ctypes.c_int64]
+    lib.oracle_layer_weight.restype = ctypes.c_uint64
+    lib.oracle_layer_draw.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int64, ctypes.c_uint64]
+    lib.oracle_layer_draw.restype = ctypes.c_uint64
+    lib.oracle_sample_layers.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P,
+                                         ctypes.c_int32, _P, ctypes.c_uint64, ctypes.POINTER(_P)]
+    lib.oracle_sample_layers.restype = ctypes.c_int
     return lib
 
 
@@ -157,6 +165,18 @@ def negative_dst(sigma, etype, eid, k, n_dst, lib=None) -> int:
     if st != OK:
         raise OracleError(st)
     return v.value
+
+
+def layer_weight(deg, lib=None) -> int:
+    """One edge's share of its source's importance: floor(2^32 / deg^2)."""
+    lib = lib or load()
+    return int(lib.oracle_layer_weight(deg))
+
+
+def layer_draw(sigma, hop, ntype, k, total, lib=None) -> int:
+    """Draw k of a hop and node type: a point in [0, total)."""
+    lib = lib or load()
+    return int(lib.oracle_layer_draw(sigma, hop, ntype, k, total))
 
 
 MAX_NEG = 64
@@ -295,6 +315,29 @@ class HostGraph:
                                    _copy(pd.value, npos.value, ctypes.c_int32, np.int32),
                                    _copy(pn.value, nneg.value, ctypes.c_int32, np.int32))
             return res
+        finally:
+            self.lib.oracle_blocks_free(handle)
+
+    def sample_layers(self, seeds, layer_sizes, sigma):
+        """A layer-wise (LADIES) mini-batch: seeds per node type; layer_sizes
+        [n_hops][n_ntypes] draws per hop and node type (-1: every candidate).
+        Returns the result dict of sample_blocks."""
+        T, R = self.T, self.R
+        seed_arrs = [None if (seeds[t] is None) else _arr_i64(seeds[t]) for t in range(T)]
+        ptrs = (ctypes.c_void_p * T)(*[(_ptr(x) if x is not None and x.size else None)
+                                       for x in seed_arrs])
+        ns = np.array([0 if x is None else x.size for x in seed_arrs], dtype=np.int64)
+        H = len(layer_sizes)
+        ls = np.ascontiguousarray(np.asarray(layer_sizes, dtype=np.int32).reshape(H * T)) \
+            if H > 0 else np.zeros(1, dtype=np.int32)
+        handle = ctypes.c_void_p()
+        st = self.lib.oracle_sample_layers(ctypes.addressof(self._nt), T,
+                                           ctypes.addressof(self._et), R, ptrs, _ptr(ns), H,
+                                           _ptr(ls), sigma, ctypes.byref(handle))
+        if st != OK:
+            raise OracleError(st)
+        try:
+            return _result_dict(self.lib, handle, H, T, R, [e[1] for e in self.etypes])
         finally:
             self.lib.oracle_blocks_free(handle)
 

@@ -541,19 +541,10 @@ static int check_common(const oracle_ntype *ntypes, int32_t n_ntypes,
   return ORACLE_OK;
 }
 
-int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
-                         const oracle_etype *etypes, int32_t n_etypes,
-                         const int64_t *const *seeds, const int64_t *n_seeds,
-                         int32_t n_hops, const int32_t *fanouts, uint64_t sigma,
-                         int32_t key_bits, oracle_blocks **out) {
-  if (!out) return ORACLE_EINVAL;
-  *out = NULL;
-  int status = check_common(ntypes, n_ntypes, etypes, n_etypes, n_hops, fanouts, key_bits);
-  if (status != ORACLE_OK) return status;
-  if (!n_seeds) return ORACLE_EINVAL;
-
-  /* Seeds: present, in range and unique within their type (the targets of a
-   * mini-batch are a set of vertices, Sec. 3.2). */
+/* Seeds: present, in range and unique within their type (the targets of a
+ * mini-batch are a set of vertices, Sec. 3.2). */
+static int check_seeds(const oracle_ntype *ntypes, int32_t n_ntypes,
+                       const int64_t *const *seeds, const int64_t *n_seeds) {
   for (int32_t t = 0; t < n_ntypes; ++t) {
     if (n_seeds[t] < 0) return ORACLE_EINVAL;
     if (n_seeds[t] == 0) continue;
@@ -570,6 +561,22 @@ int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
     free(tmp);
     if (bad) return ORACLE_EINVAL;
   }
+  return ORACLE_OK;
+}
+
+int oracle_sample_blocks(const oracle_ntype *ntypes, int32_t n_ntypes,
+                         const oracle_etype *etypes, int32_t n_etypes,
+                         const int64_t *const *seeds, const int64_t *n_seeds,
+                         int32_t n_hops, const int32_t *fanouts, uint64_t sigma,
+                         int32_t key_bits, oracle_blocks **out) {
+  if (!out) return ORACLE_EINVAL;
+  *out = NULL;
+  int status = check_common(ntypes, n_ntypes, etypes, n_etypes, n_hops, fanouts, key_bits);
+  if (status != ORACLE_OK) return status;
+  if (!n_seeds) return ORACLE_EINVAL;
+
+  status = check_seeds(ntypes, n_ntypes, seeds, n_seeds);
+  if (status != ORACLE_OK) return status;
 
   oracle_blocks *b = new_blocks(n_hops, n_ntypes, n_etypes);
   if (!b) return ORACLE_ENOMEM;
@@ -920,5 +927,271 @@ int oracle_blocks_pairs(const oracle_blocks *b, int32_t etype, int64_t *n_pos,
   if (pos_dst) *pos_dst = b->pos_dst[etype];
   if (n_negs) *n_negs = b->pair_n[etype] * b->n_neg;
   if (neg_dst) *neg_dst = b->neg_dst[etype];
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Layer-wise sampling (LADIES; Sec. 4.2.2 names it as fitting the same
+ * decomposition; the algorithm is Zou et al., NeurIPS 2019, Algorithm 1).
+ * Instead of K neighbours per vertex, each hop draws a fixed number of
+ * vertices per node type for the whole layer, with probability proportional
+ * to their layer-dependent importance, and keeps every edge from the drawn
+ * vertices (and the frontier) into the frontier.  Readings where the papers
+ * leave room (listed in the design notes):
+ *  - candidates of type t: the in-neighbours of the frontier over every edge
+ *    type whose source type is t, minus the frontier itself;
+ *  - importance: LADIES' column norm of the row-normalised adjacency,
+ *    sum over the candidate's edges u -> v into the frontier of 1 / deg_e(v)^2,
+ *    kept in fixed point as floor(2^32 / deg_e(v)^2) so that sums are exact;
+ *  - n[h][t] i.i.d. draws with replacement (LADIES Algorithm 1): draw k takes
+ *    r = floor(x * total / 2^64), x = word0 | word1 << 32 of Philox4x32-10 at
+ *    counter (k lo32, k hi32, 2^30 | h, t) under key sigma, and picks the
+ *    candidate whose interval [prefix, prefix + weight) holds r, candidates in
+ *    ascending ID; n = -1 takes every candidate, 0 none;
+ *  - the next frontier is the frontier followed by the distinct drawn
+ *    vertices in ascending ID; the block of the hop keeps every in-edge of a
+ *    frontier vertex whose source is in the next frontier.               */
+
+uint64_t oracle_layer_weight(int64_t deg) {
+  if (deg <= 0) return 0;
+  const unsigned __int128 d2 = (unsigned __int128)(uint64_t)deg * (uint64_t)deg;
+  return (uint64_t)(((unsigned __int128)1 << 32) / d2);
+}
+
+uint64_t oracle_layer_draw(uint64_t sigma, int32_t hop, int32_t ntype, int64_t k,
+                           uint64_t total) {
+  uint32_t ctr[4] = {(uint32_t)k, (uint32_t)((uint64_t)k >> 32), 0x40000000u | (uint32_t)hop,
+                     (uint32_t)ntype};
+  uint32_t seed_words[2] = {(uint32_t)sigma, (uint32_t)(sigma >> 32)};
+  uint32_t out[4];
+  oracle_philox4x32_10(ctr, seed_words, out);
+  uint64_t x = (uint64_t)out[0] | ((uint64_t)out[1] << 32);
+  return (uint64_t)(((unsigned __int128)x * total) >> 64);
+}
+
+int oracle_sample_layers(const oracle_ntype *ntypes, int32_t n_ntypes,
+                         const oracle_etype *etypes, int32_t n_etypes,
+                         const int64_t *const *seeds, const int64_t *n_seeds, int32_t n_hops,
+                         const int32_t *layer_sizes, uint64_t sigma, oracle_blocks **out) {
+  if (!out) return ORACLE_EINVAL;
+  *out = NULL;
+  if (n_ntypes < 1 || n_etypes < 0 || !ntypes || (n_etypes > 0 && !etypes) || n_hops < 0 ||
+      !n_seeds || (n_hops > 0 && !layer_sizes))
+    return ORACLE_EINVAL;
+  for (int64_t i = 0; i < (int64_t)n_hops * n_ntypes; ++i)
+    if (layer_sizes[i] < -1) return ORACLE_EINVAL;
+  for (int32_t e = 0; e < n_etypes; ++e)
+    if (etypes[e].src_type < 0 || etypes[e].src_type >= n_ntypes || etypes[e].dst_type < 0 ||
+        etypes[e].dst_type >= n_ntypes)
+      return ORACLE_EINVAL;
+  int status = check_seeds(ntypes, n_ntypes, seeds, n_seeds);
+  if (status != ORACLE_OK) return status;
+  const int32_t T = n_ntypes, R = n_etypes;
+  oracle_blocks *b = new_blocks(n_hops, T, R);
+  if (!b) return ORACLE_ENOMEM;
+  int64_t *fn = (int64_t *)calloc((size_t)T, sizeof(int64_t));
+  int64_t **fr = (int64_t **)calloc((size_t)T, sizeof(int64_t *));
+  /* per type: importance of every vertex, and membership of the frontier and
+   * of the candidate set (dense arrays over the type's vertices) */
+  uint64_t **wt = (uint64_t **)calloc((size_t)T, sizeof(uint64_t *));
+  char **in_f = (char **)calloc((size_t)T, sizeof(char *));
+  char **is_c = (char **)calloc((size_t)T, sizeof(char *));
+  if (!fn || !fr || !wt || !in_f || !is_c) status = ORACLE_ENOMEM;
+  for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+    const int64_t n = ntypes[t].num_nodes;
+    fn[t] = n_seeds[t];
+    fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
+    wt[t] = (uint64_t *)calloc((size_t)n + 1, sizeof(uint64_t));
+    in_f[t] = (char *)calloc((size_t)n + 1, 1);
+    is_c[t] = (char *)calloc((size_t)n + 1, 1);
+    if (!fr[t] || !wt[t] || !in_f[t] || !is_c[t]) {
+      status = ORACLE_ENOMEM;
+      break;
+    }
+    if (fn[t] > 0) memcpy(fr[t], seeds[t], sizeof(int64_t) * (size_t)fn[t]);
+  }
+
+  for (int32_t h = 0; h < n_hops && status == ORACLE_OK; ++h) {
+    /* ---- the frontier, as a membership array */
+    for (int32_t t = 0; t < T; ++t)
+      for (int64_t i = 0; i < fn[t]; ++i) in_f[t][fr[t][i]] = 1;
+    /* ---- importance of every candidate: its edges into the frontier */
+    for (int32_t e = 0; e < R; ++e) {
+      const oracle_etype *et = &etypes[e];
+      const int32_t s = et->src_type, d = et->dst_type;
+      for (int64_t i = 0; i < fn[d]; ++i) {
+        const int64_t v = fr[d][i];
+        const int64_t lo = et->indptr[v], hi = et->indptr[v + 1];
+        const uint64_t w = oracle_layer_weight(hi - lo);
+        for (int64_t j = lo; j < hi; ++j) {
+          const int64_t u = et->indices[j];
+          if (in_f[s][u]) continue;
+          is_c[s][u] = 1;
+          wt[s][u] += w;
+        }
+      }
+    }
+    /* ---- draws per node type; the next frontier */
+    int64_t **nf = (int64_t **)calloc((size_t)T, sizeof(int64_t *));
+    int64_t *nfn = (int64_t *)calloc((size_t)T, sizeof(int64_t));
+    if (!nf || !nfn) status = ORACLE_ENOMEM;
+    for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+      const int64_t n = ntypes[t].num_nodes;
+      const int32_t k = layer_sizes[(int64_t)h * T + t];
+      /* candidates in ascending ID, their weight prefix */
+      int64_t nc = 0;
+      for (int64_t u = 0; u < n; ++u) nc += is_c[t][u];
+      int64_t *cand = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nc + 1));
+      uint64_t *pre = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)(nc + 1));
+      char *drawn = (char *)calloc((size_t)nc + 1, 1);
+      if (!cand || !pre || !drawn) {
+        free(cand);
+        free(pre);
+        free(drawn);
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      int64_t m = 0;
+      uint64_t total = 0;
+      for (int64_t u = 0; u < n; ++u)
+        if (is_c[t][u]) {
+          cand[m] = u;
+          pre[m] = total;
+          total += wt[t][u];
+          ++m;
+        }
+      if (k < 0) {
+        for (int64_t i = 0; i < nc; ++i) drawn[i] = 1;
+      } else if (total > 0) {
+        for (int64_t q = 0; q < k; ++q) {
+          const uint64_t r = oracle_layer_draw(sigma, h, t, q, total);
+          /* the candidate whose interval holds r: the last one whose prefix
+           * is not above r (zero-weight candidates have empty intervals) */
+          int64_t a = 0, z = nc - 1;
+          while (a < z) {
+            int64_t mid = a + (z - a + 1) / 2;
+            if (pre[mid] <= r)
+              a = mid;
+            else
+              z = mid - 1;
+          }
+          drawn[a] = 1;
+        }
+      }
+      int64_t nd = 0;
+      for (int64_t i = 0; i < nc; ++i) nd += drawn[i];
+      nfn[t] = fn[t] + nd;
+      if (nfn[t] > INT32_MAX) status = ORACLE_EUNSUPPORTED;
+      nf[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nfn[t] + 1));
+      if (!nf[t] && status == ORACLE_OK) status = ORACLE_ENOMEM;
+      if (status == ORACLE_OK) {
+        if (fn[t] > 0) memcpy(nf[t], fr[t], sizeof(int64_t) * (size_t)fn[t]);
+        int64_t p = fn[t];
+        for (int64_t i = 0; i < nc; ++i)
+          if (drawn[i]) nf[t][p++] = cand[i];
+      }
+      /* clean the dense arrays for the next hop */
+      for (int64_t i = 0; i < nc; ++i) {
+        is_c[t][cand[i]] = 0;
+        wt[t][cand[i]] = 0;
+      }
+      free(cand);
+      free(pre);
+      free(drawn);
+    }
+    for (int32_t t = 0; t < T; ++t)
+      for (int64_t i = 0; i < fn[t]; ++i) in_f[t][fr[t][i]] = 0;
+
+    /* ---- the block: every in-edge of the frontier from the next frontier;
+     * local IDs by lookup in the next frontier */
+    gid_pos **ntab = (gid_pos **)calloc((size_t)T, sizeof(gid_pos *));
+    if (!ntab && status == ORACLE_OK) status = ORACLE_ENOMEM;
+    for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+      ntab[t] = (gid_pos *)malloc(sizeof(gid_pos) * (size_t)(nfn[t] + 1));
+      if (!ntab[t]) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      for (int64_t i = 0; i < nfn[t]; ++i) {
+        ntab[t][i].gid = nf[t][i];
+        ntab[t][i].pos = i;
+      }
+      qsort(ntab[t], (size_t)nfn[t], sizeof(gid_pos), cmp_gid_pos);
+    }
+    for (int32_t e = 0; e < R && status == ORACLE_OK; ++e) {
+      const oracle_etype *et = &etypes[e];
+      const int32_t s = et->src_type, d = et->dst_type;
+      oedges *blk = &b->edges[(int64_t)h * R + e];
+      int64_t cap = 0;
+      for (int64_t i = 0; i < fn[d]; ++i) cap += et->indptr[fr[d][i] + 1] - et->indptr[fr[d][i]];
+      blk->indptr = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[d] + 1));
+      blk->src_local = (int32_t *)malloc(sizeof(int32_t) * (size_t)(cap + 1));
+      blk->dst_local = (int32_t *)malloc(sizeof(int32_t) * (size_t)(cap + 1));
+      blk->eid = (int64_t *)malloc(sizeof(int64_t) * (size_t)(cap + 1));
+      if (!blk->indptr || !blk->src_local || !blk->dst_local || !blk->eid) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      int64_t cnt = 0;
+      blk->indptr[0] = 0;
+      for (int64_t i = 0; i < fn[d]; ++i) {
+        const int64_t v = fr[d][i];
+        for (int64_t j = et->indptr[v]; j < et->indptr[v + 1]; ++j) {
+          const int64_t pos = find_gid_pos(ntab[s], nfn[s], et->indices[j]);
+          if (pos < 0) continue;
+          blk->src_local[cnt] = (int32_t)pos;
+          blk->dst_local[cnt] = (int32_t)i;
+          blk->eid[cnt] = j;
+          ++cnt;
+        }
+        blk->indptr[i + 1] = cnt;
+      }
+      blk->n_edges = cnt;
+    }
+    /* record the hop's vertex lists; the next hop starts from them */
+    for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+      onodes *nd = &b->nodes[(int64_t)h * T + t];
+      nd->n_dst = fn[t];
+      nd->n_src = nfn[t];
+      nd->src_gid = nf[t];
+      nf[t] = NULL;
+      free(fr[t]);
+      fr[t] = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nfn[t] + 1));
+      if (!fr[t]) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      if (nfn[t] > 0) memcpy(fr[t], nd->src_gid, sizeof(int64_t) * (size_t)nfn[t]);
+      fn[t] = nfn[t];
+    }
+    if (ntab)
+      for (int32_t t = 0; t < T; ++t) free(ntab[t]);
+    free(ntab);
+    if (nf)
+      for (int32_t t = 0; t < T; ++t) free(nf[t]);
+    free(nf);
+    free(nfn);
+  }
+  for (int32_t t = 0; t < T && status == ORACLE_OK; ++t) {
+    b->in_n[t] = fn[t];
+    b->in_gid[t] = fr[t];
+    fr[t] = NULL;
+  }
+  for (int32_t t = 0; t < T; ++t) {
+    if (fr) free(fr[t]);
+    if (wt) free(wt[t]);
+    if (in_f) free(in_f[t]);
+    if (is_c) free(is_c[t]);
+  }
+  free(fr);
+  free(fn);
+  free(wt);
+  free(in_f);
+  free(is_c);
+  if (status != ORACLE_OK) {
+    oracle_blocks_free(b);
+    return status;
+  }
+  *out = b;
   return ORACLE_OK;
 }

@@ -142,6 +142,24 @@ int oracle_blocks_pairs(const oracle_blocks *b, int32_t etype, int64_t *n_pos,
                         const int32_t **pos_src, const int32_t **pos_dst,
                         int64_t *n_negs, const int32_t **neg_dst);
 
+/* ---- Layer-wise sampling (LADIES; see oracle.c for the readings). ---- */
+
+/* floor(2^32 / deg^2): one edge's share of its source's importance. */
+uint64_t oracle_layer_weight(int64_t deg);
+
+/* Draw k of hop h and node type t: floor(x * total / 2^64), x = word0 |
+ * word1 << 32 of Philox4x32-10 at counter (k lo32, k hi32, 2^30 | h, t). */
+uint64_t oracle_layer_draw(uint64_t sigma, int32_t hop, int32_t ntype, int64_t k,
+                           uint64_t total);
+
+/* Layer-wise mini-batch: layer_sizes is hop-major [n_hops * n_ntypes], the
+ * draws per hop and node type (-1 every candidate).  Results as
+ * oracle_sample_blocks. */
+int oracle_sample_layers(const oracle_ntype *ntypes, int32_t n_ntypes,
+                         const oracle_etype *etypes, int32_t n_etypes,
+                         const int64_t *const *seeds, const int64_t *n_seeds, int32_t n_hops,
+                         const int32_t *layer_sizes, uint64_t sigma, oracle_blocks **out);
+
 #ifdef __cplusplus
 }
 #endif

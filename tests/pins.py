@@ -564,6 +564,226 @@ def pin_negative_uniformity(lib, n=6000):
     return fails
 
 
+# ---------------------------------------------------------------------------
+# layer-wise (LADIES) mini-batches
+
+def rr_layer_draw(sigma, hop, ntype, k, total):
+    """Draw k by its definition, the two Philox words from rocRAND: counter
+    (k, 2^30 | hop, ntype), words 0 and 1, then floor(x * total / 2^64)."""
+    rr = rocrand_ref()
+    sub = ((0x40000000 | hop) & M32) | ((ntype & M32) << 32)
+    w0 = int(rr.rr_word(sigma & ((1 << 64) - 1), sub, 4 * k))
+    w1 = int(rr.rr_word(sigma & ((1 << 64) - 1), sub, 4 * k + 1))
+    return ((w0 | (w1 << 32)) * total) >> 64
+
+
+def layer_expect(nn, etypes, F, sizes_h, sigma, h):
+    """One layer by numpy: per node type the candidates (ascending), their
+    importance (sum of floor(2^32 / deg^2) over their edges into the
+    frontier) and the drawn set (inverse CDF by searchsorted)."""
+    T = len(nn)
+    cands, weights = [], []
+    for t in range(T):
+        us, ws = [np.zeros(0, np.int64)], [np.zeros(0, np.int64)]
+        for e, (s, d, ip, ix) in enumerate(etypes):
+            if s != t or F[d].size == 0:
+                continue
+            deg = (ip[F[d] + 1] - ip[F[d]]).astype(np.int64)
+            rows = np.repeat(np.arange(F[d].size), deg)
+            slots = np.concatenate([np.arange(ip[v], ip[v + 1]) for v in F[d]]) \
+                if deg.sum() else np.zeros(0, np.int64)
+            w = np.where(deg > 0, (1 << 32) // np.maximum(deg, 1) ** 2, 0)[rows]
+            us.append(ix[slots])
+            ws.append(w)
+        u = np.concatenate(us)
+        w = np.concatenate(ws)
+        keep = ~np.isin(u, F[t])
+        u, w = u[keep], w[keep]
+        c = np.unique(u)
+        wt = np.zeros(c.size, np.int64)
+        np.add.at(wt, np.searchsorted(c, u), w)
+        cands.append(c)
+        weights.append(wt)
+    drawn = []
+    for t in range(T):
+        c, wt = cands[t], weights[t]
+        k = sizes_h[t]
+        if k < 0:
+            drawn.append(c)
+            continue
+        total = int(wt.sum())
+        if total == 0 or k == 0:
+            drawn.append(np.zeros(0, np.int64))
+            continue
+        cum = np.cumsum(wt)  # inclusive: candidate i holds [cum[i] - wt[i], cum[i])
+        r = np.array([rr_layer_draw(sigma, h, t, q, total) for q in range(k)], np.int64)
+        drawn.append(np.unique(c[np.searchsorted(cum, r, side="right")]))
+    return cands, weights, drawn
+
+
+def check_layer_blocks(nn, etypes, seeds, layer_sizes, sigma, res):
+    """A layer-wise result against the definitions: each hop's new vertices
+    are the distinct draws (numpy, rocRAND), ascending after the frontier; the
+    block holds exactly the in-edges of the frontier whose source is in the
+    next frontier, grouped by destination and ascending edge ID."""
+    fails = []
+    T = len(nn)
+    F = [np.zeros(0, np.int64) if s is None else np.asarray(s, np.int64) for s in seeds]
+    for h, sizes in enumerate(layer_sizes):
+        _, _, drawn = layer_expect(nn, etypes, F, sizes, sigma, h)
+        NF = []
+        for t in range(T):
+            n_dst, sg = res["nodes"][(h, t)]
+            want = np.concatenate([F[t], drawn[t]])
+            if n_dst != F[t].size or not np.array_equal(sg, want):
+                fails.append(f"hop {h} type {t}: source list {sg[:8]} != frontier + draws {want[:8]}")
+            NF.append(want)
+        for e, (s, d, ip, ix) in enumerate(etypes):
+            bip, sl, dl, eid = res["edges"][(h, e)]
+            want_eid, want_dl = [], []
+            for i, v in enumerate(F[d]):
+                slots = np.arange(ip[v], ip[v + 1])
+                keep = slots[np.isin(ix[slots], NF[s])]
+                want_eid.append(keep)
+                want_dl.append(np.full(keep.size, i, np.int32))
+            we = np.concatenate(want_eid) if want_eid else np.zeros(0, np.int64)
+            wd = np.concatenate(want_dl) if want_dl else np.zeros(0, np.int32)
+            if not np.array_equal(eid, we) or not np.array_equal(dl, wd):
+                fails.append(f"hop {h} etype {e}: block edges differ from the filtered in-edges")
+                continue
+            counts = np.bincount(wd, minlength=F[d].size) if F[d].size else np.zeros(0, np.int64)
+            if not np.array_equal(bip, np.concatenate([[0], np.cumsum(counts)])):
+                fails.append(f"hop {h} etype {e}: block indptr is not the scan of the counts")
+            if eid.size and not np.array_equal(NF[s][sl], ix[eid]):
+                fails.append(f"hop {h} etype {e}: relabelled sources do not map back")
+        F = NF
+    for t in range(T):
+        if not np.array_equal(res["input"][t], F[t]):
+            fails.append(f"type {t}: input frontier differs from the last source list")
+    return fails
+
+
+def random_layer_case(rng, max_nodes=40, max_deg=20):
+    nn, ets, feats = workloads.random_hetero(rng, max_nodes=max_nodes, max_deg=max_deg)
+    T = len(nn)
+    seeds = []
+    for t in range(T):
+        if nn[t] == 0 or rng.random() < 0.3:
+            seeds.append(None)
+        else:
+            seeds.append(rng.choice(nn[t], size=int(rng.integers(1, nn[t] + 1)), replace=False)
+                         .astype(np.int64))
+    H = int(rng.integers(1, 4))  # weights must be cleared between hops
+    choices = [-1, 0, 1, 2, 5, 12, 40]
+    sizes = [[choices[int(rng.integers(0, len(choices)))] for _ in range(T)] for _ in range(H)]
+    return nn, ets, feats, seeds, sizes, int(rng.integers(0, 1 << 63))
+
+
+def pin_layer_draw(lib, rng, n=200):
+    fails = []
+    for i in range(n):
+        sigma = int(rng.integers(0, 1 << 63)) * 2 + int(rng.integers(0, 2))
+        h, t, k = int(rng.integers(0, 6)), int(rng.integers(0, 50)), int(rng.integers(0, 1 << 20))
+        total = [1, 7, 1 << 32, (1 << 62) + 11, int(rng.integers(1, 1 << 62))][i % 5]
+        want = rr_layer_draw(sigma, h, t, k, total)
+        got = oracle.layer_draw(sigma, h, t, k, total, lib)
+        if got != want:
+            fails.append(f"layer_draw({sigma},{h},{t},{k},{total}) = {got} != {want}")
+    return fails
+
+
+def pin_layer_weight(lib, rng, n=300):
+    """floor(2^32 / d^2): w <= 2^32 / d^2 < w + 1, in exact rationals."""
+    from fractions import Fraction
+    fails = []
+    degs = [1, 2, 3, 255, 256, 65535, 65536, 65537, 1 << 20, 5_000_000] + \
+        [int(x) for x in rng.integers(1, 10_000_000, size=n)]
+    for d in degs:
+        w = oracle.layer_weight(d, lib)
+        q = Fraction(1 << 32, d * d)
+        if not (w <= q < w + 1):
+            fails.append(f"layer_weight({d}) = {w}, 2^32/d^2 = {float(q)}")
+    if oracle.layer_weight(0, lib) != 0:
+        fails.append("layer_weight(0) != 0")
+    return fails
+
+
+def pin_layer_blocks(lib, rng, n=40):
+    fails = []
+    for c in range(n):
+        nn, ets, feats, seeds, sizes, sigma = random_layer_case(rng)
+        hg = oracle.HostGraph(list(zip(nn, feats)), ets, lib=lib)
+        res = hg.sample_layers(seeds, sizes, sigma)
+        f = check_layer_blocks(nn, ets, seeds, sizes, sigma, res)
+        fails += [f"layer case {c}: {m}" for m in f[:3]]
+    return fails
+
+
+def pin_layer_boundaries(lib, n_draw=40):
+    """Draws that land exactly on interval boundaries: one destination of
+    in-degree 65536 gives each of its 65536 distinct sources weight
+    floor(2^32 / 65536^2) = 1, so every draw r is the first point of the
+    interval of candidate r; a second hop draws among those sources' own
+    in-neighbours (a ring), with the first hop's weights cleared."""
+    fails = []
+    n = 65536 + 70000
+    d = 65536
+    # vertex 0 has sources 1 .. 65536; vertex v >= 1 has one in-edge from
+    # 65537 + (v % 69999)
+    indptr = np.concatenate([[0], d + np.arange(0, n, dtype=np.int64)])
+    indices = np.concatenate([np.arange(1, d + 1), 65537 + (np.arange(1, n) % 69999)])
+    indices = indices.astype(np.int64)
+    ets = [(0, 0, indptr.astype(np.int64), indices)]
+    hg = oracle.HostGraph([(n, None)], ets, lib=lib)
+    for sigma in (3, 77):
+        res = hg.sample_layers([np.array([0])], [[n_draw], [n_draw]], sigma)
+        f = check_layer_blocks([n], ets, [np.array([0])], [[n_draw], [n_draw]], sigma, res)
+        fails += [f"boundary sigma {sigma}: {m}" for m in f[:3]]
+    return fails
+
+
+def pin_layer_errors(lib):
+    fails = []
+    indptr = np.array([0, 1, 3, 3], np.int64)
+    indices = np.array([2, 0, 1], np.int64)
+    hg = oracle.HostGraph([(3, None)], [(0, 0, indptr, indices)], lib=lib)
+    for seeds, sizes in (([np.array([1, 1])], [[2]]), ([np.array([3])], [[2]]),
+                         ([np.array([0])], [[-2]])):
+        try:
+            hg.sample_layers(seeds, sizes, 0)
+            fails.append(f"layer batch {seeds} {sizes} accepted")
+        except oracle.OracleError as ex:
+            if ex.status != oracle.EINVAL:
+                fails.append(f"expected EINVAL, got {ex.status}")
+    return fails
+
+
+def pin_layer_statistics(lib, n_sigma=4000):
+    """LADIES' importance sampling: over many sigma, single draws land on each
+    candidate with probability weight / total."""
+    fails = []
+    # one destination of degree 2 and one of degree 4 in the frontier; five
+    # candidate sources with different multiplicities into them
+    indptr = np.array([0, 2, 6, 6, 6, 6, 6, 6], np.int64)
+    indices = np.array([2, 3, 2, 4, 5, 6], np.int64)
+    hg = oracle.HostGraph([(7, None)], [(0, 0, indptr, indices)], lib=lib)
+    w2, w4 = (1 << 32) // 4, (1 << 32) // 16
+    weights = {2: w2 + w4, 3: w2, 4: w4, 5: w4, 6: w4}
+    total = sum(weights.values())
+    counts = {u: 0 for u in weights}
+    for sigma in range(n_sigma):
+        res = hg.sample_layers([np.array([0, 1])], [[1]], sigma)
+        drawn = res["nodes"][(0, 0)][1][2:]
+        for u in drawn:
+            counts[int(u)] += 1
+    x2 = sum((counts[u] - n_sigma * w / total) ** 2 / (n_sigma * w / total)
+             for u, w in weights.items())
+    p = chi2_sf(x2, len(weights) - 1)
+    if p < 1e-3:
+        fails.append(f"draw frequencies {counts} not proportional to importance: p={p:.2g}")
+    return fails
+
+
 ALL_PINS = {
     "philox": pin_philox,
     "edge_key": pin_edge_key,
@@ -576,4 +796,9 @@ ALL_PINS = {
     "negatives": pin_negatives,
     "edge_blocks": pin_edge_blocks,
     "edge_errors": lambda lib, rng: pin_edge_errors(lib),
+    "layer_draw": pin_layer_draw,
+    "layer_weight": pin_layer_weight,
+    "layer_blocks": pin_layer_blocks,
+    "layer_errors": lambda lib, rng: pin_layer_errors(lib),
+    "layer_boundaries": lambda lib, rng: pin_layer_boundaries(lib),
 }

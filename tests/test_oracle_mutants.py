@@ -64,6 +64,18 @@ MUTANTS = [
      "b->pos_src[e][i] = (int32_t)find_sorted(b->seed_gid[d], b->seed_n[d], src[e][i]);"),
     ("reverse edge not checked against the target",
      "if (etypes[r].indices[rj] != v || rv != et->indices[j]) return ORACLE_EINVAL;", ""),
+    # layer-wise (LADIES) mini-batches
+    ("importance from deg, not deg squared",
+     "const unsigned __int128 d2 = (unsigned __int128)(uint64_t)deg * (uint64_t)deg;",
+     "const unsigned __int128 d2 = (unsigned __int128)(uint64_t)deg;"),
+    ("frontier left among the candidates", "if (in_f[s][u]) continue;", "(void)0;"),
+    ("layer draws in the negatives' counter domain", "0x40000000u | (uint32_t)hop",
+     "0x80000000u | (uint32_t)hop"),
+    ("draw lands one candidate early", "if (pre[mid] <= r)", "if (pre[mid] < r)"),
+    ("layer block keeps every in-edge", "if (pos < 0) continue;", "(void)0;"),
+    ("every-candidate layer size ignored", "for (int64_t i = 0; i < nc; ++i) drawn[i] = 1;",
+     "for (int64_t i = 0; i < nc; ++i) drawn[i] = 0;"),
+    ("importance not cleared between hops", "        wt[t][cand[i]] = 0;\n", ""),
 ]
 
 
@@ -81,6 +93,11 @@ def fast_pins(lib):
     fails += pins.pin_negatives(lib, rng, n=30)
     fails += pins.pin_edge_blocks(lib, rng, n=25)
     fails += pins.pin_edge_errors(lib)
+    fails += pins.pin_layer_draw(lib, rng, n=30)
+    fails += pins.pin_layer_weight(lib, rng, n=30)
+    fails += pins.pin_layer_blocks(lib, rng, n=25)
+    fails += pins.pin_layer_errors(lib)
+    fails += pins.pin_layer_boundaries(lib, n_draw=8)
     return fails
 
 

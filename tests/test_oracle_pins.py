@@ -28,6 +28,11 @@ def test_negative_statistics(lib):
     assert not fails, "\n".join(fails)
 
 
+def test_layer_statistics(lib):
+    fails = pins.pin_layer_statistics(lib)
+    assert not fails, "\n".join(fails)
+
+
 def test_philox_zero_counter_known_answer(lib):
     # Philox4x32-10 with zero counter and zero key, from rocRAND's engine.
     ref = pins.rr_block(0, 0, 0)
