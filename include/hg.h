@@ -348,6 +348,37 @@ hg_status hg_blocks_edge_pairs(const hg_blocks *blocks, int32_t etype, int64_t *
                                const int32_t **pos_src, const int32_t **pos_dst,
                                int64_t *n_negs, const int32_t **neg_dst);
 
+/* ---- Layer-wise mini-batches (LADIES) ---------------------------------------
+ * Sec. 4.2.2 names layer-wise sampling as fitting the same decomposition of
+ * sampling, compaction and feature copy; the algorithm is LADIES (Zou et al.,
+ * NeurIPS 2019, Algorithm 1).  Hop h, from its frontier (hop 0: the seeds):
+ *  - the candidates of node type t are the sources of the frontier's in-edges
+ *    (over every edge type whose source type is t) that are not in the
+ *    frontier;
+ *  - a candidate's importance is the sum over its edges u -> v into the
+ *    frontier of floor(2^32 / deg_e(v)^2), deg_e(v) the in-degree of v in
+ *    that edge type (an integer, so the sums are exact in any order);
+ *  - layer_sizes[h * n_ntypes + t] = n draws n times with replacement among
+ *    type t's candidates in ascending ID: draw k takes
+ *    r = floor(x * total / 2^64), x = word0 | word1 << 32 of Philox4x32-10 at
+ *    counter (k lo32, k hi32, 2^30 | h, t) under key (rng_seed lo32,
+ *    rng_seed hi32), total = the candidates' importance sum, and picks the
+ *    candidate whose interval [prefix, prefix + importance) holds r (none
+ *    when total is 0); -1 takes every candidate, 0 none;
+ *  - the hop's source vertices (the next frontier) are the frontier followed
+ *    by the distinct drawn vertices in ascending ID;
+ *  - its block keeps every in-edge of a frontier vertex whose source is in
+ *    the next frontier, per destination in CSC slot order; local IDs as in
+ *    hg_sample_blocks.
+ * Seeds and the output handle are as for hg_sample_blocks (gather_ntypes as
+ * in hg_sample_blocks_gather).  layer_sizes: host int32 [n_hops * n_ntypes],
+ * each >= -1.  HG_EUNSUPPORTED for a graph of more than 8 node types;
+ * otherwise errors as hg_sample_blocks. */
+hg_status hg_sample_layers(hg_graph *graph, const int64_t *const *seeds, const int64_t *n_seeds,
+                           int32_t n_hops, const int32_t *layer_sizes, uint64_t rng_seed,
+                           const int32_t *gather_ntypes, int32_t n_gather, hipStream_t stream,
+                           hg_blocks **out);
+
 /* Thread-local description of the last failure on this thread. */
 const char *hg_last_error(void);
 

@@ -39,7 +39,7 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_graph_types",
                "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
                "hg_pipeline_destroy", "hg_sample_edge_blocks", "hg_blocks_seeds",
-               "hg_blocks_edge_pairs",
+               "hg_blocks_edge_pairs", "hg_sample_layers",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 HG_MAX_NEG = 64
@@ -114,6 +114,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_sample_edge_blocks": ([_P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
         "hg_blocks_seeds": ([_P, _I32, _PI64, _PP], _I32),
         "hg_blocks_edge_pairs": ([_P, _I32, _PI64, _PP, _PP, _PI64, _PP], _I32),
+        "hg_sample_layers": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -403,6 +404,44 @@ class Graph:
         _check(lib.hg_sample_blocks_bundle(self._h, B, ptrs, counts, H, fo, sg, gt, len(gather),
                                            start, stop, _stream(stream), hs))
         return [Blocks(self, ctypes.c_void_p(hs[b]), H) for b in range(B)]
+
+    def sample_layers(self, seeds, layer_sizes, rng_seed: int = 0, gather=None,
+                      stream=None) -> Blocks:
+        """A layer-wise (LADIES) mini-batch (hg_sample_layers): seeds per node
+        type as in sample_blocks; layer_sizes [n_hops][n_ntypes], the draws of
+        each node type per hop (-1 = every candidate).  gather as in
+        sample_blocks."""
+        lib = load_library()
+        T = self.T
+        if len(seeds) != T:
+            raise ValueError("one seed entry per node type")
+        keep = []
+        ptrs = (ctypes.c_void_p * T)()
+        counts = (ctypes.c_int64 * T)()
+        for t, s in enumerate(seeds):
+            if s is None:
+                continue
+            s = _dev_i64(s, self.device)
+            keep.append(s)
+            counts[t] = s.numel()
+            ptrs[t] = s.data_ptr() if s.numel() else None
+        H = len(layer_sizes)
+        flat = [int(k) for row in layer_sizes for k in row]
+        if len(flat) != H * T:
+            raise ValueError("layer_sizes must be [n_hops][n_ntypes]")
+        ls = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        if isinstance(gather, str):
+            if gather != "all":
+                raise ValueError('gather must be None, "all" or a list of node types')
+            gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
+        gather = list(gather or [])
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
+        h = ctypes.c_void_p()
+        st = lib.hg_sample_layers(self._h, ptrs, counts, H, ls, int(rng_seed) & (2**64 - 1), gt,
+                                  len(gather), _stream(stream), ctypes.byref(h))
+        del keep
+        _check(st)
+        return Blocks(self, h, H)
 
     def sample_edge_blocks(self, targets, fanouts, rng_seed: int = 0, n_neg: int = 0,
                            exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None,

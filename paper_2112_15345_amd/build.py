@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libhg.so")
 OBJDIR = os.path.join(REPO, "_build", "hg")
 
 SOURCES = ["hg_sample.hip", "hg_compact.hip", "hg_gather.hip", "hg_edges.hip",
-           "hg_runtime.cpp", "hg_pipeline.cpp"]
+           "hg_layers.hip", "hg_runtime.cpp", "hg_pipeline.cpp"]
 ARCH = "gfx950"
 
 # Packed FP32 instructions stay off (the kernels do no float math; the flag

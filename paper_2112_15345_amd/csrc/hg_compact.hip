@@ -46,6 +46,7 @@ struct CompactArgs {
   int64_t *tile_pre;  // [n_tiles + 1] set bits in earlier tiles, of any type (or look-back words)
   int32_t *tile_cnt;  // per tile: set bits
   int64_t *small;
+  bool collect;       // only list the vertices (no map, no frontier bits)
 };
 
 // Four flag bytes (each 0 or 1) as four bits: byte k of x lands on bit 24 + k
@@ -165,8 +166,9 @@ __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t
   clear_reached(A, tile, tw);
   const uint2 ab = tw.fresh();
   if ((ab.x | ab.y) == 0) return;
-  *reinterpret_cast<uint2 *>(A.fbits + tile * kTile + threadIdx.x * kTileItems) =
-      uint2{tw.front.x | ab.x, tw.front.y | ab.y};
+  if (!A.collect)
+    *reinterpret_cast<uint2 *>(A.fbits + tile * kTile + threadIdx.x * kTileItems) =
+        uint2{tw.front.x | ab.x, tw.front.y | ab.y};
   int32_t *map = A.ts[t].map;
   int64_t *out = A.hv.src_out[t];
   const uint32_t words[kTileItems] = {ab.x, ab.y};
@@ -178,7 +180,7 @@ __device__ __forceinline__ void assign_bits(const CompactArgs &A, int t, int64_t
       const int bit = __ffs(m) - 1;
       m &= m - 1;
       const int64_t v = v0 + k * 32 + bit;
-      map[v] = int32_t(local);
+      if (!A.collect) map[v] = int32_t(local);
       out[local] = v;
       ++local;
     }
@@ -227,25 +229,6 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_single(CompactArgs A, uin
   assign_bits(A, t, first, tile, tw, A.hv.nF[t] + ex[0] + pre);
 }
 
-// Next hop's frontier sizes (this hop's plus the new vertices of each type)
-// and pair layout (pairs of etype e: frontier of its destination type).
-__device__ void plan_next_hop(HopView hv, HopView next, const EtypeStatic *es,
-                              const int64_t *tile_base, const int64_t *small,
-                              int32_t n_types, int32_t n_etypes) {
-  if (threadIdx.x != 0) return;
-  for (int t = 0; t < n_types; ++t) {
-    // a type without bitmap tiles (no vertices) gains nothing
-    const int64_t u = tile_base[t + 1] > tile_base[t] ? small[kSlotNew + t] : 0;
-    next.nF[t] = hv.nF[t] + u;
-  }
-  int64_t acc = 0;
-  for (int e = 0; e < n_etypes; ++e) {
-    next.pair_base[e] = acc;
-    acc += next.nF[es[e].dst_type];
-  }
-  next.pair_base[n_etypes] = acc;
-}
-
 __global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
@@ -265,9 +248,9 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream) {
+                          int64_t *ticketed, hipStream_t stream, bool collect) {
   CompactArgs A{hv, ts, n_types, reached, fbits, tile_base, n_tiles, copy_total, tile_sums,
-                reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small};
+                reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small, collect};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
   *ticketed = 0;
   if (n_tiles <= kSinglePassTiles) {

@@ -275,6 +275,25 @@ __device__ void tile_lookback(Lookback lb, int64_t tile, int64_t first,
   }
 }
 
+// Next hop's frontier sizes (this hop's plus the new vertices of each type)
+// and pair layout (pairs of etype e: frontier of its destination type).
+__device__ inline void plan_next_hop(HopView hv, HopView next, const EtypeStatic *es,
+                              const int64_t *tile_base, const int64_t *small,
+                              int32_t n_types, int32_t n_etypes) {
+  if (threadIdx.x != 0) return;
+  for (int t = 0; t < n_types; ++t) {
+    // a type without bitmap tiles (no vertices) gains nothing
+    const int64_t u = tile_base[t + 1] > tile_base[t] ? small[kSlotNew + t] : 0;
+    next.nF[t] = hv.nF[t] + u;
+  }
+  int64_t acc = 0;
+  for (int e = 0; e < n_etypes; ++e) {
+    next.pair_base[e] = acc;
+    acc += next.nF[es[e].dst_type];
+  }
+  next.pair_base[n_etypes] = acc;
+}
+
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32
 // multiplies, with the round key advanced by the Weyl constants.
 struct U32x4 {

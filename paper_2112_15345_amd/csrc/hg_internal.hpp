@@ -50,7 +50,7 @@ constexpr int kSlotEdges = 4;   // kept edges of the hop
 constexpr int kSlotHubs = 5;    // hub pairs
 constexpr int kSlotChunks = 6;  // hub chunks
 constexpr int kSlotWaves = 7;   // pairs sampled by one wavefront each
-constexpr int kSlotNew = 8;     // n_new[T], then ebase[R+1]
+constexpr int kSlotNew = 8;     // n_new[T], then ebase[R+1], then kept ebase[R+1]
 
 constexpr int32_t kErrSeedRange = 1;   // a frontier vertex out of range
 constexpr int32_t kErrSeedRepeat = 2;  // a vertex twice in a frontier
@@ -194,13 +194,71 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
 // kSinglePassTiles tiles: one launch, a single-pass scan whose look-back words
 // are tile_sums (ticketed blocks: *ticketed is their number).  Beyond: three
 // launches (reduce, scan, rank) with no inter-block waits; *ticketed = 0.
-// tile_sums: device scratch of 2 * n_tiles + 2 64-bit words.
+// tile_sums: device scratch of 2 * n_tiles + 2 64-bit words.  With `collect`
+// the ranked vertices are only listed (in the source lists of hv, from local
+// 0) and their reached flags cleared: the map and the frontier bits are left
+// as they are.
 constexpr int64_t kSinglePassTiles = 256;
 hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream);
+                          int64_t *ticketed, hipStream_t stream, bool collect = false);
+
+// ---- layer-wise (LADIES) sampling (hg_layers.hip) ----------------------------
+
+// One hop of a layer-wise call.  The sampler has emitted every in-edge of the
+// frontier (all_src / all_eid / all_dst_local, grouped by pair at pa.off);
+// per node type t (at most kInlineTypes), wt[t] holds the importance of every
+// vertex (zero between uses), cand[t] and prefix[t] the candidates and the
+// exclusive prefix of their importance, scan tiles cand_tile[t] ..
+// cand_tile[t+1] of the candidate scan, and draws[t] the draws of the hop.
+// Values per tile of the layer-wise scans (256 threads, two values each).
+constexpr int64_t kLayerTile = 512;
+
+struct LayerArgs {
+  HopView hv, next;
+  const EtypeStatic *es;
+  const TypeStatic *ts;
+  const int64_t *tile_base;  // bitmap tiles per type (plans the next hop)
+  int32_t n_types, n_etypes;
+  PairArrays pa;
+  int64_t n_pairs;
+  int64_t n_all;
+  const int64_t *all_src;
+  const int64_t *all_eid;
+  const int32_t *all_dst_local;
+  uint64_t *wt[kInlineTypes];
+  int64_t *cand[kInlineTypes];
+  uint64_t *prefix[kInlineTypes];
+  int64_t cand_tile[kInlineTypes + 1];
+  int64_t draw_base[kInlineTypes + 1];  // threads of the draw launch per type
+  int32_t draws[kInlineTypes];
+  int64_t *tile_sum;   // per scan tile
+  int64_t *tile_pre;   // per scan tile: exclusive scan over all tiles, then the grand total
+  int64_t n_keep_tiles;
+  int64_t *pos;        // [n_all + 1] exclusive scan of the kept flags
+  int64_t *out_eid;
+  int32_t *out_src_local, *out_dst_local;
+  int64_t *out_indptr;  // [P + R]
+  uint64_t sigma;
+  int32_t hop;
+  int64_t *small;
+};
+
+// Importance of every candidate: for each in-edge u -> v of the frontier
+// whose source is not in the frontier, wt[type(u)][u] += floor(2^32 / deg(v)^2).
+hipError_t launch_lw_weights(const LayerArgs &A, hipStream_t stream);
+// Exclusive prefix of the candidates' importance per node type (three
+// launches: tile sums, one scan of the tile sums, apply); zeroes the
+// candidates' importance entries.
+hipError_t launch_lw_prefix(const LayerArgs &A, hipStream_t stream);
+// The draws of every node type: marks the drawn candidates reached.
+hipError_t launch_lw_draw(const LayerArgs &A, hipStream_t stream);
+// The kept in-edges (source in the next frontier): scan of their flags,
+// emitted in order; then the block CSC, the kept edge starts per etype
+// (small slots after ebase) and the next hop's plan.
+hipError_t launch_lw_keep(const LayerArgs &A, hipStream_t stream);
 
 // src_local[j] = map_{src_type(e)}[src_gid[j]] for the edges of etype e,
 // which are [ebase[e], ebase[e+1]), ebase = small + kSlotNew + n_types.

@@ -1,0 +1,292 @@
+// Layer-wise (LADIES) sampling on gfx950.  DistDGLv2 (arXiv 2112.15345, Sec.
+// 4.2.2) names layer-wise sampling as fitting the same decomposition of
+// sampling, compaction and feature copy; the algorithm is LADIES (Zou et al.,
+// NeurIPS 2019, Algorithm 1).  Each hop draws a fixed number of vertices per
+// node type for the whole layer, with probability proportional to their
+// importance, and keeps every in-edge of the frontier from the next frontier.
+//
+// One hop, after the counting pass and the sampler have emitted every in-edge
+// of the frontier (fanout -1) and set the reached flag of every source:
+//  1. k_lw_weights : importance of every candidate (a source not in the
+//                    frontier): sum of floor(2^32 / deg(v)^2) over its edges
+//                    into the frontier, 64-bit atomics (exact in any order);
+//  2. compaction   : (collect mode) the candidates of each type, ascending;
+//  3. k_lw_scan_*  : exclusive prefix of their importance per type
+//                    (reduce-then-scan over 512-candidate tiles);
+//  4. k_lw_draw    : draw k takes r = floor(x * total / 2^64), x from
+//                    Philox4x32-10 at (k, 2^30 | hop, type), and marks the
+//                    candidate whose interval [prefix, prefix + weight) holds
+//                    r (binary search);
+//  5. compaction   : the drawn vertices join the frontier (ascending);
+//  6. k_lw_scan_*  : the kept in-edges (source in the next frontier) by an
+//                    exclusive scan of their flags, emitted in order;
+//  7. k_lw_indptr  : the block CSC, the kept edge starts per etype, and the
+//                    next hop's plan.
+#include "hg_device.hpp"
+#include "hg_internal.hpp"
+
+namespace hg {
+
+namespace {
+
+constexpr int kLwThreads = 256;
+constexpr int kLwItems = 2;
+constexpr int64_t kLwTile = int64_t(kLwThreads) * kLwItems;
+static_assert(kLwTile == kLayerTile, "the runtime sizes the scans in these tiles");
+
+__device__ __forceinline__ int64_t gs_start() {
+  return int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+}
+__device__ __forceinline__ int64_t gs_step() {
+  return int64_t(gridDim.x) * blockDim.x;
+}
+
+unsigned grid_for(int64_t n, int threads, int64_t cap = 1 << 16) {
+  int64_t b = (n + threads - 1) / threads;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return unsigned(b);
+}
+
+__device__ __forceinline__ bool in_frontier(const uint32_t *fbits, int64_t v) {
+  return (fbits[v >> 5] >> (v & 31)) & 1u;
+}
+
+// floor(2^32 / d^2) for d >= 1 (zero once d^2 > 2^32).
+__device__ __forceinline__ uint64_t layer_weight(int64_t d) {
+  const uint64_t d2 = uint64_t(d) * uint64_t(d);
+  return d2 > (uint64_t(1) << 32) ? 0 : (uint64_t(1) << 32) / d2;
+}
+
+__device__ __forceinline__ const int64_t *ebase_of(const LayerArgs &A) {
+  return A.small + kSlotNew + A.n_types;  // starts of each etype's emitted edges
+}
+__device__ __forceinline__ int64_t *kept_base_of(const LayerArgs &A) {
+  return A.small + kSlotNew + A.n_types + A.n_etypes + 1;
+}
+
+__global__ __launch_bounds__(256) void k_lw_weights(LayerArgs A) {
+  const int64_t *ebase = ebase_of(A);
+  for (int64_t j = gs_start(); j < A.n_all; j += gs_step()) {
+    const int e = find_segment(ebase, A.n_etypes, j);
+    const EtypeStatic &E = A.es[e];
+    const int64_t u = A.all_src[j];
+    if (in_frontier(A.ts[E.src_type].fbits, u)) continue;
+    const int64_t p = A.hv.pair_base[e] + A.all_dst_local[j];
+    const uint64_t w = layer_weight(A.pa.pdeg[p]);
+    if (w) atomicAdd(reinterpret_cast<unsigned long long *>(A.wt[E.src_type] + u),
+                     (unsigned long long)w);
+  }
+}
+
+// ---- reduce-then-scan over tiles of kLwTile values --------------------------
+// kind 0: the candidates' importance, one segment per node type (tiles
+//         cand_tile[t] .. cand_tile[t+1]; the type's candidates are counted in
+//         small[kSlotNew + t] by the collect compaction);
+// kind 1: the kept flags of the emitted edges, one segment.
+template <int kKind>
+struct ScanSeg {
+  int seg;
+  int64_t first_tile, n;
+};
+
+template <int kKind>
+__device__ __forceinline__ ScanSeg<kKind> seg_of(const LayerArgs &A, int64_t tile) {
+  if (kKind == 0) {
+    const int t = find_segment(A.cand_tile, A.n_types, tile);
+    return ScanSeg<kKind>{t, A.cand_tile[t], A.small[kSlotNew + t]};
+  }
+  return ScanSeg<kKind>{0, 0, A.n_all};
+}
+
+template <int kKind>
+__device__ __forceinline__ int64_t value_of(const LayerArgs &A, const ScanSeg<kKind> &S,
+                                            int64_t i) {
+  if (i >= S.n) return 0;
+  if (kKind == 0) return int64_t(A.wt[S.seg][A.cand[S.seg][i]]);
+  const int e = find_segment(ebase_of(A), A.n_etypes, i);
+  return in_frontier(A.ts[A.es[e].src_type].fbits, A.all_src[i]) ? 1 : 0;
+}
+
+template <int kKind>
+__global__ __launch_bounds__(kLwThreads) void k_lw_scan_reduce(LayerArgs A) {
+  __shared__ int64_t lds[8];
+  const int64_t tile = blockIdx.x;
+  const ScanSeg<kKind> S = seg_of<kKind>(A, tile);
+  const int64_t i0 = (tile - S.first_tile) * kLwTile + threadIdx.x * kLwItems;
+  int64_t v = 0;
+#pragma unroll
+  for (int k = 0; k < kLwItems; ++k) v += value_of<kKind>(A, S, i0 + k);
+  int64_t total;
+  block_excl_scan_256(v, lds, &total);
+  if (threadIdx.x == 0) A.tile_sum[tile] = total;
+}
+
+// One block: tile_pre = exclusive scan of tile_sum over all n_tiles tiles,
+// tile_pre[n_tiles] = the grand total.
+constexpr int kLwScanThreads = 1024;
+__global__ __launch_bounds__(kLwScanThreads) void k_lw_scan_tiles(int64_t *tile_sum,
+                                                                  int64_t *tile_pre,
+                                                                  int64_t n_tiles) {
+  constexpr int kWaves = kLwScanThreads / kWave;
+  __shared__ int64_t s_wave[kWaves];
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  int64_t carry = 0;
+  for (int64_t c0 = 0; c0 < n_tiles; c0 += kLwScanThreads) {
+    const int64_t i = c0 + threadIdx.x;
+    const int64_t x = i < n_tiles ? tile_sum[i] : 0;
+    const int64_t inc = wave_incl_scan_i64(x);
+    if (lane == kWave - 1) s_wave[wave] = inc;
+    __syncthreads();
+    int64_t before = 0, sum = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      const int64_t y = s_wave[w];
+      if (w < wave) before += y;
+      sum += y;
+    }
+    if (i < n_tiles) tile_pre[i] = carry + before + inc - x;
+    carry += sum;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) tile_pre[n_tiles] = carry;
+}
+
+// Each tile's values get their exclusive prefix within the segment.
+template <int kKind>
+__global__ __launch_bounds__(kLwThreads) void k_lw_scan_apply(LayerArgs A) {
+  __shared__ int64_t lds[8];
+  const int64_t tile = blockIdx.x;
+  const ScanSeg<kKind> S = seg_of<kKind>(A, tile);
+  const int64_t i0 = (tile - S.first_tile) * kLwTile + threadIdx.x * kLwItems;
+  int64_t v[kLwItems];
+  int64_t sum = 0;
+#pragma unroll
+  for (int k = 0; k < kLwItems; ++k) {
+    v[k] = value_of<kKind>(A, S, i0 + k);
+    sum += v[k];
+  }
+  int64_t total;
+  int64_t pre = block_excl_scan_256(sum, lds, &total) +
+                (A.tile_pre[tile] - A.tile_pre[S.first_tile]);
+#pragma unroll
+  for (int k = 0; k < kLwItems; ++k) {
+    const int64_t i = i0 + k;
+    if (i < S.n) {
+      if (kKind == 0) {
+        A.prefix[S.seg][i] = uint64_t(pre);
+        A.wt[S.seg][A.cand[S.seg][i]] = 0;  // clean for the next hop and call
+      } else {
+        A.pos[i] = pre;
+        if (v[k]) {
+          const int e = find_segment(ebase_of(A), A.n_etypes, i);
+          A.out_eid[pre] = A.all_eid[i];
+          A.out_dst_local[pre] = A.all_dst_local[i];
+          A.out_src_local[pre] = A.es[e].src_map[A.all_src[i]];
+        }
+      }
+    }
+    pre += v[k];
+  }
+  if (kKind == 1 && tile == int64_t(gridDim.x) - 1 && threadIdx.x == kLwThreads - 1)
+    A.pos[A.n_all] = pre;  // the last thread of the last tile ends past n_all
+}
+
+// Draws: thread x of type t's range draw_base[t] .. draw_base[t+1] makes draw
+// x - draw_base[t] (or, for a type that takes every candidate, marks
+// candidate x - draw_base[t]).
+__global__ __launch_bounds__(256) void k_lw_draw(LayerArgs A) {
+  const int64_t n = A.draw_base[A.n_types];
+  for (int64_t x = gs_start(); x < n; x += gs_step()) {
+    const int t = find_segment(A.draw_base, A.n_types, x);
+    const int64_t k = x - A.draw_base[t];
+    const int64_t nc = A.small[kSlotNew + t];
+    const int64_t *cand = A.cand[t];
+    uint8_t *reached = A.ts[t].reached;
+    if (A.draws[t] < 0) {
+      if (k < nc) reached[cand[k]] = 1;
+      continue;
+    }
+    const uint64_t total = uint64_t(A.tile_pre[A.cand_tile[t + 1]] - A.tile_pre[A.cand_tile[t]]);
+    if (total == 0 || nc == 0) continue;
+    const U32x4 r4 = philox4x32_10(U32x4{uint32_t(k), uint32_t(uint64_t(k) >> 32),
+                                         0x40000000u | uint32_t(A.hop), uint32_t(t)},
+                                   uint32_t(A.sigma), uint32_t(A.sigma >> 32));
+    const uint64_t r = __umul64hi(uint64_t(r4.x) | (uint64_t(r4.y) << 32), total);
+    // the last candidate whose prefix is not above r (zero-weight candidates
+    // share the prefix of the next one and are never the last)
+    const uint64_t *pre = A.prefix[t];
+    int64_t a = 0, b = nc - 1;
+    while (a < b) {
+      const int64_t m = a + (b - a + 1) / 2;
+      if (pre[m] <= r)
+        a = m;
+      else
+        b = m - 1;
+    }
+    reached[cand[a]] = 1;
+  }
+}
+
+// Per pair its block-CSC entry from the kept positions; the closing entry and
+// the kept edge start of every etype; block 0 plans the next hop.
+__global__ __launch_bounds__(256) void k_lw_indptr(LayerArgs A) {
+  const int64_t *ebase = ebase_of(A);
+  const int64_t *pb = A.hv.pair_base;
+  // kept edges before emitted edge i (no edges: no scan ran, and none are kept)
+  auto pos = [&](int64_t i) { return A.n_all > 0 ? A.pos[i] : int64_t(0); };
+  if (blockIdx.x == 0) {
+    int64_t *kept = kept_base_of(A);
+    for (int e = threadIdx.x; e <= A.n_etypes; e += blockDim.x) {
+      kept[e] = pos(ebase[e]);
+      if (e < A.n_etypes) A.out_indptr[pb[e + 1] + e] = pos(ebase[e + 1]) - pos(ebase[e]);
+    }
+    plan_next_hop(A.hv, A.next, A.es, A.tile_base, A.small, A.n_types, A.n_etypes);
+  }
+  for (int64_t p = gs_start(); p < A.n_pairs; p += gs_step()) {
+    const int e = A.pa.pet[p];
+    A.out_indptr[pb[e] + e + (p - pb[e])] = pos(A.pa.off[p]) - pos(ebase[e]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_lw_weights(const LayerArgs &A, hipStream_t stream) {
+  if (A.n_all <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_lw_weights, dim3(grid_for(A.n_all, 256)), dim3(256), 0, stream, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_lw_prefix(const LayerArgs &A, hipStream_t stream) {
+  const int64_t tiles = A.cand_tile[A.n_types];
+  if (tiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_lw_scan_reduce<0>, dim3(unsigned(tiles)), dim3(kLwThreads), 0, stream, A);
+  hipLaunchKernelGGL(k_lw_scan_tiles, dim3(1), dim3(kLwScanThreads), 0, stream, A.tile_sum,
+                     A.tile_pre, tiles);
+  hipLaunchKernelGGL(k_lw_scan_apply<0>, dim3(unsigned(tiles)), dim3(kLwThreads), 0, stream, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_lw_draw(const LayerArgs &A, hipStream_t stream) {
+  const int64_t n = A.draw_base[A.n_types];
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_lw_draw, dim3(grid_for(n, 256)), dim3(256), 0, stream, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_lw_keep(const LayerArgs &A, hipStream_t stream) {
+  const int64_t tiles = A.n_keep_tiles;
+  if (tiles > 0) {
+    hipLaunchKernelGGL(k_lw_scan_reduce<1>, dim3(unsigned(tiles)), dim3(kLwThreads), 0, stream,
+                       A);
+    hipLaunchKernelGGL(k_lw_scan_tiles, dim3(1), dim3(kLwScanThreads), 0, stream, A.tile_sum,
+                       A.tile_pre, tiles);
+    hipLaunchKernelGGL(k_lw_scan_apply<1>, dim3(unsigned(tiles)), dim3(kLwThreads), 0, stream,
+                       A);
+  }
+  // at least one block: block 0 writes the etype entries and plans the next hop
+  hipLaunchKernelGGL(k_lw_indptr, dim3(grid_for(A.n_pairs, 256)), dim3(256), 0, stream, A);
+  return hipGetLastError();
+}
+
+}  // namespace hg

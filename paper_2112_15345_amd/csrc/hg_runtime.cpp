@@ -163,6 +163,8 @@ struct Workspace {
   size_t htab_cap = 0;
   Scratch pairs, lb_pairs, edges, cand;
   Scratch targets;                 // edge-seeded calls: endpoints and exclusion tables
+  Scratch lw_weight;               // layer-wise calls: importance per vertex (zero between uses)
+  Scratch lw_edges, lw_cand;       // layer-wise calls: every in-edge of a hop; candidates
   uint32_t epoch = 0;              // look-back launches so far (mod kEpochLimit)
   hipEvent_t done = nullptr;
   bool busy = false;
@@ -348,12 +350,16 @@ void free_workspace(Workspace *w) {
   w->edges.release();
   w->cand.release();
   w->targets.release();
+  w->lw_weight.release();
+  w->lw_edges.release();
+  w->lw_cand.release();
   if (w->hsmall) (void)hipHostFree(w->hsmall);
   if (w->htab) (void)hipHostFree(w->htab);
   delete w;
 }
 
-size_t small_slots(const hg_graph *g) { return size_t(kSlotNew + g->T + g->R + 1); }
+// n_new[T], then ebase[R+1], then the kept ebase[R+1] of layer-wise hops
+size_t small_slots(const hg_graph *g) { return size_t(kSlotNew + g->T + 2 * (g->R + 1)); }
 
 // Takes a free workspace (or makes one) with table room for `tab_bytes`.
 hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
@@ -512,6 +518,25 @@ struct SampleRun {
   ExclView X{};
   size_t edge_tab = 0;  // bytes of the per-etype target table
 
+  // a layer-wise call: draws per hop and node type (hop-major [H * T]); its
+  // candidates are listed through region H+2; the importance array is clean
+  // unless wt_dirty
+  const int32_t *layer_sizes = nullptr;
+  bool wt_dirty = false;
+  // a layer-wise hop's kept edges (their per-etype starts are read back at the
+  // next wait): the hop and its output arrays
+  int32_t lw_hop = -1;
+  int64_t *lw_eid = nullptr;
+  int32_t *lw_srcl = nullptr, *lw_dstl = nullptr;
+  hg_status close_layer_edges();
+  hg_status layer_hop(int32_t h, const HopView &hv, const HopView &nv, const PairArrays &pa,
+                      int64_t P, int64_t S, const std::vector<int64_t> &nF,
+                      const std::vector<int64_t> &cbound, int64_t *gid_tmp,
+                      int64_t *indptr_all, int64_t *eid_all, int32_t *srcl_all,
+                      int32_t *dstl_all, int64_t **src_slot, std::vector<int64_t *> &src_out,
+                      bool inline_ptrs, uint64_t *cand, int64_t n_wave, int64_t n_chunks,
+                      int64_t n_hubs);
+
   SampleRun(hg_graph *g_, hipStream_t s, int32_t H_, const int32_t *fo,
             const uint64_t *sig, int32_t n_sig, int32_t kb)
       : g(g_), stream(s), T(g_->T), R(g_->R), H(H_), sigmas(sig, sig + n_sig), key_bits(kb),
@@ -519,7 +544,7 @@ struct SampleRun {
 
   // table bytes of a call: the sigma table, then regions 0 .. H+1 (and for an
   // edge-seeded call the seeds' region H+2 and the target table)
-  int32_t n_regions() const { return H + 2 + (eb ? 1 : 0); }
+  int32_t n_regions() const { return H + 2 + ((eb || layer_sizes) ? 1 : 0); }
   size_t table_bytes() const {
     return sig_bytes + lay.size * size_t(n_regions()) + edge_tab;
   }
@@ -620,6 +645,9 @@ struct SampleRun {
       if (!small_clean)
         (void)launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall),
                               2 * int64_t(small_slots(g)), 0, stream);
+      if (wt_dirty)
+        (void)launch_fill_u32(static_cast<uint32_t *>(ws->lw_weight.p),
+                              2 * g->map_off[g->T], 0u, stream);
     }
     if (!ok && b) {
       delete b;  // and its arrays
@@ -637,6 +665,7 @@ struct SampleRun {
 
   void init_blocks();
   hg_status run(const int64_t *const *seeds, const int64_t *n_seeds);
+  hg_status run_layers(const int64_t *const *seeds, const int64_t *n_seeds);
   hg_status run_edges();
   hg_status hops(std::vector<int64_t> &nF, int64_t n_items);
 };
@@ -871,6 +900,196 @@ hg_status SampleRun::run_edges() {
   return hops(nF, n_items);
 }
 
+// A layer-wise call: the seeds as in run(), every fanout -1 (each hop first
+// lists every in-edge of its frontier), and region H+2 for the candidate lists.
+hg_status SampleRun::run_layers(const int64_t *const *seeds, const int64_t *n_seeds) {
+  hipError_t e;
+  init_blocks();
+  std::vector<int64_t> nF(T);
+  int64_t P = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    nF[t] = n_seeds[t];
+    hfield<int64_t>(0, lay.nf)[t] = nF[t];
+    hfield<const int64_t *>(0, lay.frontier)[t] = n_seeds[t] > 0 ? seeds[t] : nullptr;
+  }
+  for (int32_t i = 0; i < R; ++i) {
+    hfield<int64_t>(0, lay.pbase)[i] = P;
+    P += nF[g->et[i].dst];
+  }
+  hfield<int64_t>(0, lay.pbase)[R] = P;
+  for (int32_t r = 0; r < n_regions(); ++r) {
+    for (int32_t i = 0; i < R; ++i) hfield<int32_t>(r, lay.fanout)[i] = -1;
+    for (int32_t t = 0; t < T; ++t) {
+      hfield<int64_t *>(r, lay.src_out)[t] = nullptr;
+      if (r > 0) hfield<const int64_t *>(r, lay.frontier)[t] = nullptr;
+      if (r == H + 2) hfield<int64_t>(r, lay.nf)[t] = 0;  // candidates are listed from 0
+    }
+  }
+  std::memcpy(ws->htab, sigmas.data(), sizeof(uint64_t) * sigmas.size());
+  if ((e = upload(0, table_bytes())) != hipSuccess) return fail_device(e, "start");
+  int64_t total = 0;
+  for (int64_t n : nF) total += n;
+  if ((e = launch_insert_frontier(view(0), ws->d_ts, T, total, ws->dsmall, stream)) !=
+      hipSuccess)
+    return fail_device(e, "insert seeds");
+  if (H == 0) {
+    if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
+    hg_status st = check_flags("seeds");
+    if (st != HG_OK) return st;
+    Carve a;
+    std::vector<int64_t *> cp(T, nullptr);
+    for (int32_t t = 0; t < T; ++t) a.add(&cp[t], nF[t]);
+    void *base = a.allocate(g, stream);
+    if (!base) return fail(HG_ENOMEM, "seed copy");
+    b->mem->ptrs.push_back(base);
+    for (int32_t t = 0; t < T; ++t) {
+      if (nF[t] > 0 &&
+          (e = hipMemcpyAsync(cp[t], seeds[t], sizeof(int64_t) * size_t(nF[t]),
+                              hipMemcpyDeviceToDevice, stream)) != hipSuccess)
+        return fail_device(e, "seed copy");
+      b->in_n[t] = nF[t];
+      b->in_gid[t] = cp[t];
+    }
+    return HG_OK;
+  }
+  // the importance array: one uint64 per vertex, zero between uses
+  const int64_t map_n = g->map_off[T];
+  if (!ws->lw_weight.ensure(sizeof(uint64_t) * size_t(std::max<int64_t>(map_n, 1)), stream))
+    return fail(HG_ENOMEM, "layer-wise: importance array");
+  if (ws->lw_weight.fresh &&
+      (e = launch_fill_u32(static_cast<uint32_t *>(ws->lw_weight.p),
+                           int64_t(ws->lw_weight.cap / sizeof(uint32_t)), 0u, stream)) !=
+          hipSuccess)
+    return fail_device(e, "fill");
+  return hops(nF, P + 1);
+}
+
+// The kept edges of the last layer-wise hop, from the per-etype starts that
+// its keep pass left in the readback slots.
+hg_status SampleRun::close_layer_edges() {
+  if (lw_hop < 0) return HG_OK;
+  const int64_t *kept = ws->hsmall + kSlotNew + T + R + 1;
+  for (int32_t i = 0; i < R; ++i) {
+    if (kept[i] > kept[i + 1] || kept[i] < 0)
+      return fail(HG_EDEVICE, "hop %d: kept edge count mismatch", lw_hop);
+    const size_t k = size_t(lw_hop) * R + i;
+    b->n_edges[k] = kept[i + 1] - kept[i];
+    b->src_local[k] = lw_srcl + kept[i];
+    b->dst_local[k] = lw_dstl + kept[i];
+    b->eid[k] = lw_eid + kept[i];
+  }
+  lw_hop = -1;
+  return HG_OK;
+}
+
+// One layer-wise hop after its counting pass: every in-edge of the frontier
+// into scratch, the candidates' importance and their per-type lists, the
+// draws, the next frontier, and the kept in-edges into the block arrays.
+hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
+                               const PairArrays &pa, int64_t P, int64_t S,
+                               const std::vector<int64_t> &nF,
+                               const std::vector<int64_t> &cbound, int64_t *gid_tmp,
+                               int64_t *indptr_all, int64_t *eid_all, int32_t *srcl_all,
+                               int32_t *dstl_all, int64_t **src_slot,
+                               std::vector<int64_t *> &src_out, bool inline_ptrs,
+                               uint64_t *cand, int64_t n_wave, int64_t n_chunks,
+                               int64_t n_hubs) {
+  hipError_t e;
+  LayerArgs A{};
+  A.hv = hv;
+  A.next = nv;
+  A.es = ws->d_es;
+  A.ts = ws->d_ts;
+  A.tile_base = g->d_tile_base;
+  A.n_types = T;
+  A.n_etypes = R;
+  A.pa = pa;
+  A.n_pairs = P;
+  A.n_all = S;
+  A.n_keep_tiles = (S + kLayerTile - 1) / kLayerTile;
+  A.sigma = sigmas[0];
+  A.hop = h;
+  A.small = ws->dsmall;
+  A.out_eid = eid_all;
+  A.out_src_local = srcl_all;
+  A.out_dst_local = dstl_all;
+  A.out_indptr = indptr_all;
+  A.cand_tile[0] = 0;
+  A.draw_base[0] = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    const int32_t k = layer_sizes[size_t(h) * T + t];
+    A.draws[t] = k;
+    A.cand_tile[t + 1] = A.cand_tile[t] + (cbound[t] + kLayerTile - 1) / kLayerTile;
+    A.draw_base[t + 1] = A.draw_base[t] + (k < 0 ? cbound[t] : (cbound[t] > 0 ? k : 0));
+    A.wt[t] = static_cast<uint64_t *>(ws->lw_weight.p) + g->map_off[t];
+  }
+  const int64_t scan_tiles = std::max(A.cand_tile[T], A.n_keep_tiles) + 1;
+  Carve ec;
+  int64_t *all_eid;
+  int32_t *all_dstl;
+  ec.add(&all_eid, S);
+  ec.add(&all_dstl, S);
+  ec.add(&A.pos, S + 1);
+  Carve cc;
+  for (int32_t t = 0; t < T; ++t) {
+    cc.add(&A.cand[t], cbound[t]);
+    cc.add(&A.prefix[t], cbound[t]);
+  }
+  cc.add(&A.tile_sum, scan_tiles);
+  cc.add(&A.tile_pre, scan_tiles);
+  if (!ec.in_scratch(ws->lw_edges, stream) || !cc.in_scratch(ws->lw_cand, stream))
+    return fail(HG_ENOMEM, "hop %d: layer-wise scratch", h);
+  A.all_src = gid_tmp;
+  A.all_eid = all_eid;
+  A.all_dst_local = all_dstl;
+
+  // 1. every in-edge of the frontier (fanout -1); the sampler sets the reached
+  // flag of every source
+  reached_dirty = true;
+  if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
+                         dsigmas(), g->key_R, h, key_bits, gid_tmp, all_eid, all_dstl,
+                         indptr_all, src_slot, src_out.data(), inline_ptrs ? T : 0, X,
+                         stream)) != hipSuccess)
+    return fail_device(e, "sample");
+  // 2. importance of the candidates
+  wt_dirty = true;
+  if ((e = launch_lw_weights(A, stream)) != hipSuccess) return fail_device(e, "weights");
+  // 3. the candidates of each type in ascending ID (region H+2 lists them)
+  const HopView cv = view(H + 2);
+  int64_t ticketed = 0;
+  uint32_t epoch;
+  if ((e = launch_store_ptrs(reinterpret_cast<void **>(dreg(H + 2) + lay.src_out),
+                             reinterpret_cast<void *const *>(A.cand), T, stream)) != hipSuccess ||
+      (e = next_epoch(&epoch)) != hipSuccess ||
+      (e = launch_compact(cv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles, 0,
+                          ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed, stream,
+                          true)) != hipSuccess)
+    return fail_device(e, "candidates");
+  ticket_base += uint64_t(ticketed);
+  // 4. their importance prefix per type (which zeroes the importance array)
+  if ((e = launch_lw_prefix(A, stream)) != hipSuccess) return fail_device(e, "prefix");
+  wt_dirty = false;
+  // 5. the draws set the reached flags of the drawn candidates
+  if ((e = launch_lw_draw(A, stream)) != hipSuccess) return fail_device(e, "draw");
+  // 6. the drawn vertices join the frontier: the source lists of the hop
+  int64_t copy_total = 0;
+  for (int64_t n : nF) copy_total += n;
+  if ((e = next_epoch(&epoch)) != hipSuccess ||
+      (e = launch_compact(hv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles,
+                          copy_total, ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
+                          stream)) != hipSuccess)
+    return fail_device(e, "compact");
+  ticket_base += uint64_t(ticketed);
+  reached_dirty = false;
+  // 7. the kept in-edges, the block CSC and the next hop's plan
+  if ((e = launch_lw_keep(A, stream)) != hipSuccess) return fail_device(e, "keep");
+  lw_hop = h;
+  lw_eid = eid_all;
+  lw_srcl = srcl_all;
+  lw_dstl = dstl_all;
+  return HG_OK;
+}
+
 // The hop loop from region 0's frontier (sizes nF, or their bounds for an
 // edge-seeded call, whose sizes the device wrote); n_items >= pairs + 1.
 hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
@@ -910,6 +1129,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     hg_status st = check_flags("count");
     if (st != HG_OK) return st;
     const int64_t *hs = ws->hsmall;
+    if ((st = close_layer_edges()) != HG_OK) return st;
     if (h == 0 && eb) {
       // the seeds of an edge-seeded call: the compaction counted them
       for (int32_t t = 0; t < T; ++t) {
@@ -949,8 +1169,15 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     oc.add(&eid_all, S);
     oc.add(&srcl_all, S);
     oc.add(&dstl_all, S);
+    // candidates of a type: its sources outside the frontier (a layer-wise
+    // hop keeps at most its draws of them)
+    std::vector<int64_t> cbound(T);
     for (int32_t t = 0; t < T; ++t) {
-      bound[t] = nF[t] + std::min(g->nt[t].num_nodes - nF[t], in_by_type[t]);
+      cbound[t] = std::min(g->nt[t].num_nodes - nF[t], in_by_type[t]);
+      int64_t gain = cbound[t];
+      if (layer_sizes && layer_sizes[size_t(h) * T + t] >= 0)
+        gain = std::min<int64_t>(gain, layer_sizes[size_t(h) * T + t]);
+      bound[t] = nF[t] + gain;
       oc.add(&src_out[t], bound[t]);
     }
     void *ob = oc.allocate(g, stream);
@@ -974,6 +1201,23 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
                                reinterpret_cast<void *const *>(src_out.data()), T, stream)) !=
             hipSuccess)
       return fail_device(e, "tables");
+
+    if (layer_sizes) {
+      if ((st = layer_hop(h, hv, nv, pa, P, S, nF, cbound, gid_tmp, indptr_all, eid_all,
+                          srcl_all, dstl_all, src_slot, src_out, inline_ptrs, cand, n_wave,
+                          n_chunks, n_hubs)) != HG_OK)
+        return st;
+      for (int32_t t = 0; t < T; ++t) {
+        const size_t k = size_t(h) * T + t;
+        b->n_dst[k] = nF[t];
+        b->src_gid[k] = src_out[t];
+      }
+      for (int32_t i = 0; i < R; ++i) b->indptr[size_t(h) * R + i] = indptr_all + pb[i] + i;
+      int64_t next_pairs = 0;
+      for (int32_t i = 0; i < R; ++i) next_pairs += bound[g->et[i].dst];
+      n_items = next_pairs + 1;
+      continue;
+    }
 
     // ---- 2-4. sample (and mark), compact, relabel ----------------------------
     reached_dirty = true;
@@ -1023,6 +1267,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
   if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
   hg_status st = check_flags("compact");
   if (st != HG_OK) return st;
+  if ((st = close_layer_edges()) != HG_OK) return st;
   for (int32_t t = 0; t < T; ++t) {
     const size_t k = size_t(H - 1) * T + t;
     b->n_src[k] = b->n_dst[k] + ws->hsmall[kSlotNew + t];
@@ -1285,6 +1530,38 @@ hg_status run_edge_sampling(hg_graph *g, const hg_edge_batch *eb, int32_t n_hops
   return HG_OK;
 }
 
+// A layer-wise mini-batch (checked), then the gather.
+hg_status run_layer_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
+                             int32_t n_hops, const int32_t *layer_sizes, uint64_t rng_seed,
+                             const int32_t *gtypes, int32_t n_gather, hipStream_t stream,
+                             hg_blocks **out) {
+  DeviceGuard dg(g->device);
+  SampleRun run(g, stream, n_hops, nullptr, &rng_seed, 1, 32);
+  run.layer_sizes = layer_sizes;
+  hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
+  if (st != HG_OK) return st;
+  run.b = new (std::nothrow) hg_blocks();
+  if (!run.b) {
+    run.finish(false);
+    return fail(HG_ENOMEM, "hg_sample_layers: out of host memory");
+  }
+  try {
+    st = run.run_layers(seeds, n_seeds);
+    if (st == HG_OK && n_gather > 0)
+      st = gather_into_blocks(g, run.b, gtypes, n_gather, nullptr, nullptr, stream);
+  } catch (const std::bad_alloc &) {
+    st = fail(HG_ENOMEM, "hg_sample_layers: out of host memory");
+  }
+  if (st != HG_OK) {
+    run.finish(false);
+    return st;
+  }
+  hg_blocks *b = run.b;
+  run.finish(true);
+  *out = b;
+  return HG_OK;
+}
+
 hg_status check_edge_batch(const hg_graph *g, const hg_edge_batch *eb) {
   if (!eb || !eb->n_eids) return fail(HG_EINVAL, "hg_sample_edge_blocks: no batch");
   if (eb->n_neg < 0 || eb->n_neg > HG_MAX_NEG)
@@ -1527,6 +1804,28 @@ hg_status hg_sample_edge_blocks(hg_graph *g, const hg_edge_batch *batch, int32_t
   if (st != HG_OK) return st;
   return run_edge_sampling(g, batch, n_hops, fanouts, rng_seed, gather_ntypes, n_gather, stream,
                            out);
+}
+
+hg_status hg_sample_layers(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
+                           int32_t n_hops, const int32_t *layer_sizes, uint64_t rng_seed,
+                           const int32_t *gather_ntypes, int32_t n_gather, hipStream_t stream,
+                           hg_blocks **out) {
+  if (!out) return fail(HG_EINVAL, "hg_sample_layers: out is NULL");
+  *out = nullptr;
+  clear_pending_error();
+  if (!g) return fail(HG_EINVAL, "hg_sample_layers: graph is NULL");
+  if (g->T > kInlineTypes)
+    return fail(HG_EUNSUPPORTED, "hg_sample_layers: more than %d node types", kInlineTypes);
+  if (n_hops > 0 && !layer_sizes) return fail(HG_EINVAL, "hg_sample_layers: layer_sizes is NULL");
+  for (int64_t i = 0; i < int64_t(std::max(n_hops, 0)) * g->T; ++i)
+    if (layer_sizes[i] < -1)
+      return fail(HG_EINVAL, "hg_sample_layers: layer size %d < -1", layer_sizes[i]);
+  std::vector<int32_t> every(size_t(std::max(n_hops, 0)) * g->R + 1, -1);
+  hg_status st = check_batch(g, seeds, n_seeds, n_hops, every.data(), 32, gather_ntypes,
+                             n_gather);
+  if (st != HG_OK) return st;
+  return run_layer_sampling(g, seeds, n_seeds, n_hops, layer_sizes, rng_seed, gather_ntypes,
+                            n_gather, stream, out);
 }
 
 hg_status hg_blocks_seeds(const hg_blocks *b, int32_t ntype, int64_t *n, const int64_t **gid) {

@@ -266,6 +266,11 @@ def seeds_per_type(workload: Workload, b: int):
 # link-prediction runs use two sampling hops of fanout 25 and 15 and the batch
 # size of its other runs (Appendix A.1); the targets are edges of one forward
 # relation, drawn without replacement.
+# Layer-wise (LADIES) batches on a workload's graph: the workload's seeds,
+# 512 draws per node type in each of two hops (LADIES samples 512 vertices
+# per layer in its main experiments).
+LAYER_SIZES = (512, 512)
+
 LINK_FANOUTS = (25, 15)
 LINK_BATCH = 1000
 LINK_NEG = 1
@@ -364,6 +369,6 @@ def human_bytes(n: int) -> str:
 
 
 __all__ = ["NodeType", "EdgeType", "Workload", "WORKLOADS", "Graph", "make_graph",
-           "reverse_maps", "link_targets", "LINK_FANOUTS", "LINK_BATCH", "LINK_NEG",
+           "reverse_maps", "link_targets", "LAYER_SIZES", "LINK_FANOUTS", "LINK_BATCH", "LINK_NEG",
            "batch_seeds", "seeds_per_type", "random_hetero", "graph_stats", "powerlaw_degrees",
            "distinct_sources", "transpose_csc", "random_features"]
