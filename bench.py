@@ -145,6 +145,78 @@ def link_main(args, wl, gen, g):
     print(json.dumps(result), flush=True)
 
 
+def layers_main(args, wl, gen, g):
+    """Layer-wise (LADIES) mini-batches: the workload's seeds, 512 draws per
+    node type in each of two hops, every featured type gathered.  One direct
+    call per step."""
+    import torch
+
+    import workloads as W
+
+    dev = g.device
+    sizes = [[k] * g.T for k in W.LAYER_SIZES]
+    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
+    n_batches = args.warmup + args.steps
+    seeds = [[None if s is None else torch.as_tensor(s, device=dev)
+              for s in W.seeds_per_type(wl, b)] for b in range(n_batches)]
+
+    def step(b):
+        return g.sample_layers(seeds[b], sizes, b, gather=feat_types)
+
+    for b in range(args.warmup):
+        step(b)
+    torch.cuda.synchronize()
+    edges = rows = gbytes = 0
+    t_start = time.perf_counter()
+    for b in range(args.warmup, n_batches):
+        blocks = step(b)
+        edges += sum(blocks.num_edges(h, r) for h in range(len(sizes)) for r in range(g.R))
+        for t in feat_types:
+            n = blocks.num_input_nodes(t)
+            rows += n
+            gbytes += n * row_bytes[t]
+        del blocks
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    result = {
+        "metric": "kept edges/s + gathered feature GB/s per layer-wise mini-batch (1 GPU)",
+        "value": edges / elapsed, "unit": "kept edges/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64",
+        "data": "synthetic (seeded generator shaped like the paper's workloads)",
+        "config": {"workload": wl.name + f"; layer-wise (LADIES): {list(W.LAYER_SIZES)} draws "
+                               f"per node type per hop",
+                   "workload_index": args.workload, "task": "layers",
+                   "parallelism": "single GPU", "pipeline": "direct calls"},
+        "gathered_GBps": gbytes / elapsed / 1e9,
+        "kept_edges_per_step": edges / args.steps,
+        "gathered_rows_per_step": rows / args.steps,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), check=False)
+        spent = 0.0
+        cedges = nb = 0
+        for b in range(args.warmup, n_batches):
+            t = time.perf_counter()
+            res = host.sample_layers(W.seeds_per_type(wl, b), sizes, b)
+            for ti, (n, feat, _) in enumerate(host.ntypes):
+                if feat is not None:
+                    host.gather(ti, res["input"][ti])
+            spent += time.perf_counter() - t
+            cedges += sum(v[3].size for v in res["edges"].values())
+            nb += 1
+            if spent >= 10.0:
+                break
+        result["cpu_baseline"] = {
+            "value": cedges / spent, "unit": "kept edges/s", "cores": 1, "kind": "oracle",
+            "sample": f"{nb} whole layer-wise mini-batches (batches {args.warmup}.."
+                      f"{args.warmup + nb - 1}: sampling, compaction, gather) in {spent:.2f} s"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,10 +238,11 @@ def main():
     ap.add_argument("--host-features", action="store_true",
                     help="feature tables in pinned host memory, gathered over the host link "
                          "(zero-copy); the gather rate then includes that link")
-    ap.add_argument("--task", choices=("vertex", "link"), default="vertex",
+    ap.add_argument("--task", choices=("vertex", "link", "layers"), default="vertex",
                     help="vertex: mini-batches from seed vertices (the default); link: "
                          "edge-seeded link-prediction mini-batches (hg_sample_edge_blocks, "
-                         "direct calls)")
+                         "direct calls); layers: layer-wise LADIES mini-batches "
+                         "(hg_sample_layers, direct calls)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
@@ -195,6 +268,8 @@ def main():
                  [(s, d, ip, ix) for s, d, ip, ix in gen.etypes], device=dev)
     if args.task == "link":
         return link_main(args, wl, gen, g)
+    if args.task == "layers":
+        return layers_main(args, wl, gen, g)
     fan = wl.fanout_matrix()
     n_batches = args.warmup + args.steps
     seeds = [[None if s is None else torch.as_tensor(s, device=dev)

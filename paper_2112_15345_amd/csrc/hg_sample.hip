@@ -13,7 +13,9 @@
 // ("hubs") are cut into chunks of kHubChunk edges, handed to wavefronts in
 // runs of consecutive chunks, which append their candidates to a per-hub
 // list; a second launch then selects each hub's K edges from its list.  Every
-// edge key is computed once.
+// edge key is computed once.  Pairs of more than kHubChunk edges that keep
+// all of them (none excluded) are hubs too: their chunks are copied straight
+// to the output, and the second launch skips them.
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -220,7 +222,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     const int64_t avail = deg - nx;
     const int64_t s = (K < 0 || avail <= K) ? avail : K;
     c[k].s = s;
-    if (s < avail && deg > kHubChunk) {
+    if (deg > kHubChunk && (s < avail || nx == 0)) {
       c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
       c[k].hub = 1;
     } else if (s > 0 && !(nx == 0 && s == deg && deg <= kThreadTakeAll)) {
@@ -627,11 +629,13 @@ constexpr int64_t kHubWaves = 65536;
 constexpr int64_t kMaxChunksPerWave = 16;
 
 struct HubParams {
-  int64_t hub, first_chunk, end_chunk, lo, deg, K;
+  int64_t hub, first_chunk, end_chunk, lo, deg, K, o, dst;
   uint64_t tau;
   int e;
   int32_t nx;  // excluded in-edges
   KeyCtx kc;
+  // every in-edge is kept: chunks are copied to output slots o + (j - lo)
+  __device__ bool take_all() const { return K == deg; }
 };
 
 __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
@@ -644,7 +648,9 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   H.kc = key_ctx(A, H.e);
   H.lo = A.pa.plo[p];
   H.deg = A.pa.pdeg[p];
-  H.K = A.pa.off[p + 1] - A.pa.off[p];
+  H.o = A.pa.off[p];
+  H.K = A.pa.off[p + 1] - H.o;
+  H.dst = p - A.hv.pair_base[H.e];
   H.tau = cand_threshold(H.K, H.deg, uint64_t(1) << A.key_bits);
   H.nx = excl_count(A.X, H.e, p - A.hv.pair_base[H.e]);
   return H;
@@ -732,6 +738,11 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
     const uint32_t lim = tau_raw - 1 >= 0xFFFFFFFFull ? 0xFFFFFFFFu : uint32_t(tau_raw - 1);
     const int64_t c_lo = H.lo + (chunk - H.first_chunk) * kHubChunk;
     const int64_t c_hi = min(c_lo + kHubChunk, H.lo + H.deg);
+    if (H.take_all()) {
+      const EmitCtx c = make_ctx(A.es[H.e], A.src_gid, A.eid, A.dst_local, H.dst);
+      for (int64_t j = c_lo + lane_id(); j < c_hi; j += kWave) emit_edge(c, H.o + (j - H.lo), j);
+      continue;
+    }
     // steps k = 0 .. n_it-1 cover groups g_first + 64k ..; steps [k_lo, k_hi)
     // lie wholly inside the chunk
     const uint64_t g_first = uint64_t(c_lo) >> 2;
@@ -770,6 +781,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   const int64_t deg = A.pa.pdeg[p];
   const int64_t o = A.pa.off[p];
   const int64_t K = A.pa.off[p + 1] - o;
+  if (K == deg) return;  // a take-all hub: its chunks wrote every edge
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
   const KeyCtx kc = key_ctx(A, e);

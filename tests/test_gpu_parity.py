@@ -108,6 +108,8 @@ def hub_graph(deg, n_src=None, extra=(3, 0, 7)):
     (700, 5, 32), (5000, 25, 32), (70000, 15, 32),      # candidate path
     (3000, 5, 2), (3000, 5, 1), (1200, 600, 32),        # bisection fallback
     (2000, 400, 4), (640, 639, 32), (64, 63, 32), (65, 64, 32),
+    # every in-edge kept from more than one chunk's worth: chunked copies
+    (70000, -1, 32), (5000, 5000, 32), (2049, 3000, 32), (4097, -1, 32),
 ])
 def test_hub_selection(olib, deg, k, bits):
     nn, ets, feats = hub_graph(deg)
