@@ -395,6 +395,24 @@ def main():
         del blocks
     iso_gbps = iso_bytes / (iso_ms / 1e3) / 1e9 if iso_ms > 0 else 0.0
 
+    # context for the peak: a plain 1 GiB device-to-device copy (torch's copy
+    # kernel), read + write bytes over its time, best of 5 (untimed region)
+    copy_gbps = None
+    if not args.host_features:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        best = None
+        for _ in range(6):
+            c0.record()
+            dst.copy_(src)
+            c1.record()
+            c1.synchronize()
+            ms = c0.elapsed_time(c1)
+            best = ms if best is None else min(best, ms)
+        copy_gbps = 2 * src.numel() / (best / 1e3) / 1e9
+        del src, dst
+
     # gather kernel (one launch per step for all feature types): algorithmic
     # bytes per row = read its id (8) + read the row + write the row
     g_ms = sum(hip_events.elapsed_ms(e0, e1) for e0, e1, _ in gather_rec)
@@ -443,7 +461,8 @@ def main():
                      "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
                      "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3,
                      "isolated_achieved": iso_gbps,
-                     "isolated_frac": iso_gbps / peak},
+                     "isolated_frac": iso_gbps / peak,
+                     "device_copy_GBps": copy_gbps},
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(gen, wl, first_batch=args.warmup)

@@ -456,15 +456,19 @@ __device__ __forceinline__ KeyCtx key_ctx(const SampleArgs &A, int e) {
 
 // Role A: a wavefront per 64 consecutive pairs.  Each lane writes its pair's
 // block-CSC entry; then the wavefront copies the in-edges of the small
-// take-all pairs among the 64, one output slot per lane.  The first block of
-// this role also writes each etype's closing CSC entry.
+// take-all pairs among the 64, one output slot per lane and kGroupSlots slots
+// per lane at a time (their source loads are issued together, before any
+// store).  The first block of this role also writes each etype's closing CSC
+// entry.
 struct GroupLds {
-  int64_t start[kWave];   // first output slot of the pair
-  int64_t lo[kWave];      // first in-edge slot
-  int32_t tpre[kWave + 1];  // prefix of take-all slots over the group
+  int64_t start[kWave];        // first output slot of the pair
+  int64_t lo[kWave];           // first in-edge slot
+  const int64_t *src[kWave];   // the pair's in-edge sources (indices + lo)
+  uint8_t *reached[kWave];     // reached flags of its source type
+  int32_t tpre[kWave + 1];     // prefix of take-all slots over the group
   int32_t dst[kWave];
-  int32_t etype[kWave];
 };
+constexpr int kGroupSlots = 4;
 
 __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group,
                                  bool first_block) {
@@ -484,10 +488,12 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
     const int64_t s = A.pa.off[p + 1] - o;
     if (s > 0 && s == A.pa.pdeg[p] && s <= kThreadTakeAll) {
       take = int(s);
+      const int64_t lo = A.pa.plo[p];
       L.start[lane] = o;
-      L.lo[lane] = A.pa.plo[p];
+      L.lo[lane] = lo;
+      L.src[lane] = A.es[e].indices + lo;
+      L.reached[lane] = A.es[e].src_reached;
       L.dst[lane] = int32_t(i);
-      L.etype[lane] = e;
     }
   }
   int total;
@@ -497,27 +503,39 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
   total = __shfl(int(inc), kWave - 1, kWave);
   if (lane == kWave - 1) L.tpre[kWave] = total;
   wave_sync();
-  for (int t0 = 0; t0 < total; t0 += kWave) {
-    const int t = t0 + lane;
-    if (t >= total) break;
-    // the lane q whose take-all range holds slot t
-    int a = 0, b = kWave;
-    while (b - a > 1) {
-      const int m = (a + b) >> 1;
-      if (L.tpre[m] <= t)
-        a = m;
-      else
-        b = m;
+  for (int t0 = 0; t0 < total; t0 += kWave * kGroupSlots) {
+    // the lanes q[u] whose take-all ranges hold slots t0 + u * 64 + lane
+    int q[kGroupSlots], k[kGroupSlots];
+#pragma unroll
+    for (int u = 0; u < kGroupSlots; ++u) {
+      const int t = t0 + u * kWave + lane;
+      q[u] = -1;
+      k[u] = 0;
+      if (t < total) {
+        int a = 0, b = kWave;
+        while (b - a > 1) {
+          const int m = (a + b) >> 1;
+          if (L.tpre[m] <= t)
+            a = m;
+          else
+            b = m;
+        }
+        q[u] = a;
+        k[u] = t - L.tpre[a];
+      }
     }
-    const int k = t - L.tpre[a];
-    const int64_t ed = L.lo[a] + k;
-    const int64_t pos = L.start[a] + k;
-    const EtypeStatic &E = A.es[L.etype[a]];
-    const int64_t g = E.indices[ed];
-    A.src_gid[pos] = g;
-    A.eid[pos] = ed;
-    A.dst_local[pos] = L.dst[a];
-    E.src_reached[g] = 1;
+    int64_t g[kGroupSlots];
+#pragma unroll
+    for (int u = 0; u < kGroupSlots; ++u) g[u] = q[u] >= 0 ? L.src[q[u]][k[u]] : 0;
+#pragma unroll
+    for (int u = 0; u < kGroupSlots; ++u) {
+      if (q[u] < 0) continue;
+      const int64_t pos = L.start[q[u]] + k[u];
+      A.src_gid[pos] = g[u];
+      A.eid[pos] = L.lo[q[u]] + k[u];
+      A.dst_local[pos] = L.dst[q[u]];
+      L.reached[q[u]][g[u]] = 1;
+    }
   }
 }
 
@@ -824,8 +842,9 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
 }
 
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
-  __shared__ __align__(16) uint32_t s_key[kSampleWaves][kCandCap];
-  __shared__ uint32_t s_j[kSampleWaves][kCandCap];
+  // per wavefront: its candidate keys and edge offsets (or a GroupLds)
+  __shared__ __align__(16) uint32_t s_cand[kSampleWaves][2][kCandCap];
+  static_assert(sizeof(GroupLds) <= sizeof(s_cand[0]), "a group's table fits a wavefront's LDS");
   const int64_t b = blockIdx.x;
   const int wave = threadIdx.x / kWave;
   if (b == 0 && int(threadIdx.x) < A.n_src_out)
@@ -837,11 +856,11 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
     if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
   } else if (b < A.blocks_c + A.blocks_b) {
     const int64_t w = (b - A.blocks_c) * kSampleWaves + wave;
-    if (w < A.n_wave) role_wave_pairs(A, s_key[wave], s_j[wave], w);
+    if (w < A.n_wave) role_wave_pairs(A, s_cand[wave][0], s_cand[wave][1], w);
   } else {
     // the candidate lists are not used by this role: reuse their LDS
     const int64_t ba = b - A.blocks_c - A.blocks_b;
-    GroupLds *g = reinterpret_cast<GroupLds *>(&s_key[wave][0]);
+    GroupLds *g = reinterpret_cast<GroupLds *>(&s_cand[wave][0][0]);
     role_pair_groups(A, *g, ba * kSampleWaves + wave, ba == 0);
   }
 }
@@ -982,8 +1001,6 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.n_hubs = n_hubs;
   // role A always has a block, for the closing CSC entries
   A.blocks_a = std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads);
-  static_assert(sizeof(GroupLds) <= sizeof(uint32_t) * kCandCap,
-                "a group's LDS fits in one wavefront's candidate list");
   A.blocks_b = (n_wave + kSampleWaves - 1) / kSampleWaves;
   // runs of chunks per wavefront: long enough to amortise finding the hub,
   // short enough to leave about kHubWaves wavefronts for the chip
