@@ -53,7 +53,7 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(gen, wl, first_batch, budget_s=12.0, max_batches=8):
+def cpu_baseline(gen, wl, first_batch, budget_s=12.0, max_batches=32):
     """The oracle, single-threaded, on the host cores: whole mini-batches
     (sampling, compaction, gather) of the same workload until ~budget_s."""
     import oracle
