@@ -118,7 +118,7 @@ def link_main(args, wl, gen, g):
     t_start = time.perf_counter()
     for b in range(args.warmup, n_batches):
         blocks = step(b)
-        edges += sum(blocks.num_edges(h, r) for h in range(len(fan)) for r in range(g.R))
+        edges += blocks.total_edges()
         for t in feat_types:
             n = blocks.num_input_nodes(t)
             rows += n
@@ -171,7 +171,7 @@ def layers_main(args, wl, gen, g):
     t_start = time.perf_counter()
     for b in range(args.warmup, n_batches):
         blocks = step(b)
-        edges += sum(blocks.num_edges(h, r) for h in range(len(sizes)) for r in range(g.R))
+        edges += blocks.total_edges()
         for t in feat_types:
             n = blocks.num_input_nodes(t)
             rows += n
@@ -303,7 +303,7 @@ def main():
         """Bookkeeping of a returned unit; gather bytes and events of timed ones."""
         rows_all = {t: 0 for t in feat_types}
         for blocks in blist:
-            e = sum(blocks.num_edges(h, r) for h in range(len(fan)) for r in range(g.R))
+            e = blocks.total_edges()
             if totals is not None:
                 totals[0] += e
             for t in feat_types:

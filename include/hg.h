@@ -150,6 +150,11 @@ hg_status hg_sample_blocks_ex(hg_graph *graph, const int64_t *const *seeds,
 /* Number of hops of a blocks handle (-1 for NULL). */
 int32_t hg_blocks_num_hops(const hg_blocks *blocks);
 
+/* Kept edges of every block in one call: counts[hop * n_etypes + etype] for
+ * every hop and edge type (host int64 [n_hops * n_etypes], caller-owned), as
+ * hg_blocks_edges reports them one at a time.  HG_EINVAL for NULL arguments. */
+hg_status hg_blocks_edge_counts(const hg_blocks *blocks, int64_t *counts);
+
 /* Vertices of node type `ntype` in block `hop`: n_dst frontier vertices and
  * n_src source vertices; *src_gid: device int64 [n_src] whose first n_dst
  * entries are the frontier (local ID = position). Owned by the handle. */

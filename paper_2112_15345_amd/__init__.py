@@ -39,7 +39,7 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_graph_types",
                "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
                "hg_pipeline_destroy", "hg_sample_edge_blocks", "hg_blocks_seeds",
-               "hg_blocks_edge_pairs", "hg_sample_layers",
+               "hg_blocks_edge_pairs", "hg_sample_layers", "hg_blocks_edge_counts",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 HG_MAX_NEG = 64
@@ -115,6 +115,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_seeds": ([_P, _I32, _PI64, _PP], _I32),
         "hg_blocks_edge_pairs": ([_P, _I32, _PI64, _PP, _PP, _PI64, _PP], _I32),
         "hg_sample_layers": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
+        "hg_blocks_edge_counts": ([_P, _P], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -217,6 +218,17 @@ class Blocks:
         _check(load_library().hg_blocks_edges(self._h, hop, etype, ctypes.byref(ne),
                                               None, None, None, None))
         return ne.value
+
+    def edge_counts(self):
+        """Kept edges of every block: a list [n_hops][n_etypes] (one call)."""
+        R = self.graph.R
+        buf = (ctypes.c_int64 * max(self.n_hops * R, 1))()
+        _check(load_library().hg_blocks_edge_counts(self._h, buf))
+        return [[buf[h * R + e] for e in range(R)] for h in range(self.n_hops)]
+
+    def total_edges(self) -> int:
+        """Kept edges over every hop and edge type."""
+        return sum(sum(row) for row in self.edge_counts())
 
     def input_nodes(self, ntype: int) -> torch.Tensor:
         n, p = _I64(), ctypes.c_void_p()

@@ -1892,6 +1892,12 @@ hg_status hg_graph_types(const hg_graph *g, int32_t *n_ntypes, int32_t *n_etypes
 
 int32_t hg_blocks_num_hops(const hg_blocks *b) { return b ? b->H : -1; }
 
+hg_status hg_blocks_edge_counts(const hg_blocks *b, int64_t *counts) {
+  if (!b || !counts) return fail(HG_EINVAL, "hg_blocks_edge_counts: NULL argument");
+  for (size_t k = 0; k < b->n_edges.size(); ++k) counts[k] = b->n_edges[k];
+  return HG_OK;
+}
+
 hg_status hg_blocks_nodes(const hg_blocks *b, int32_t hop, int32_t ntype,
                           int64_t *n_dst, int64_t *n_src,
                           const int64_t **src_gid) {

@@ -65,6 +65,9 @@ def test_random_heterographs(olib, chunk):
         assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
         fails = pins.check_blocks(nn, ets, seeds, fanouts, sigma, bits, got, brute=False)
         assert not fails, "\n".join(fails[:5])
+        # every block's edge count in one call
+        assert b.edge_counts() == [[ref["edges"][(h, e)][3].size for e in range(len(ets))]
+                                   for h in range(len(fanouts))]
         # gather of the input frontier, every type with features (one call)
         featured = [t for t, f in enumerate(feats) if f is not None]
         allx = g.gather_features_all(b, featured)
