@@ -72,7 +72,15 @@ struct EtypeStatic {
   int64_t n_dst_nodes;
   int32_t src_type;
   int32_t dst_type;
+  // Graphs with many edge types into one node type: per destination vertex a
+  // row of nz_words words whose bit nz_slot says whether this edge type has
+  // an in-edge there (nullptr: no mask, read indptr).
+  const uint32_t *nz_mask;
+  int32_t nz_words, nz_slot;
 };
+
+// Node types with at least this many incoming edge types get the mask above.
+constexpr int32_t kNzMaskMinEtypes = 16;
 
 // Static per node type (per workspace).
 // Per node type one flag byte and one frontier bit per vertex: the sampler
@@ -281,6 +289,12 @@ hipError_t launch_publish(int64_t *small, int64_t *host, int32_t n, uint64_t seq
 hipError_t launch_store_ptrs(void **dst, void *const *vals, int32_t n, hipStream_t stream);
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream);
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t stream);
+
+// The non-empty mask of one destination type: for v < n, bit k of row v
+// (words per row) is set when indptrs[k][v + 1] > indptrs[k][v]; indptrs is a
+// device array of n_etypes pointers.
+hipError_t launch_nonempty_mask(const int64_t *const *indptrs, int32_t n_etypes, int32_t words,
+                                int64_t n, uint32_t *mask, hipStream_t stream);
 
 // Graph check of one edge type: indptr[0] == 0, non-decreasing,
 // indptr[n_dst] == nnz, indices in [0, n_src).  Sets *err on a violation.

@@ -116,6 +116,9 @@ struct ETypeInfo {
   int64_t nnz;
   const int64_t *indptr;
   const int64_t *indices;
+  // the destination type's non-empty mask (owned by the graph), if it has one
+  const uint32_t *nz_mask = nullptr;
+  int32_t nz_words = 0, nz_slot = 0;
 };
 
 // A device buffer that grows (stream-ordered) and is reused across calls.
@@ -185,6 +188,7 @@ struct hg_graph {
   int64_t n_tiles = 0;
   int64_t *d_tile_base = nullptr;  // device copy of tile_base
   int64_t total_nnz = 0;
+  std::vector<uint32_t *> nz_masks;  // owned non-empty masks (not by bundle graphs)
   // A bundle of B mini-batches samples a virtual graph made of B copies of
   // this one (copy b of type x is type b * T + x, over the same arrays): its
   // key_R is this graph's R, so that every copy keys its edges as the real
@@ -413,7 +417,8 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
         const ETypeInfo &E = g->et[i];
         es[i] = EtypeStatic{E.indptr, E.indices, w->map + g->map_off[E.src],
                             w->reached + g->tile_base[E.src] * kTile * 32,
-                            g->nt[E.dst].num_nodes, E.src, E.dst};
+                            g->nt[E.dst].num_nodes, E.src, E.dst,
+                            E.nz_mask, E.nz_words, E.nz_slot};
       }
       std::vector<TypeStatic> ts(g->T);
       for (int32_t t = 0; t < g->T; ++t)
@@ -1285,6 +1290,49 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
 // ---------------------------------------------------------------------------
 // C ABI
 
+namespace {
+
+// Node types with many incoming edge types get a per-vertex mask of the edge
+// types that have in-edges there, so that the counting pass skips the indptr
+// reads of empty (vertex, edge type) pairs.  Built once; a type whose mask
+// cannot be allocated goes without one.
+hipError_t build_nonempty_masks(hg_graph *g, hipStream_t stream) {
+  for (int32_t t = 0; t < g->T; ++t) {
+    std::vector<int32_t> ets;
+    for (int32_t i = 0; i < g->R; ++i)
+      if (g->et[i].dst == t) ets.push_back(i);
+    const int64_t n = g->nt[t].num_nodes;
+    if (int32_t(ets.size()) < kNzMaskMinEtypes || n <= 0) continue;
+    const int32_t words = int32_t((ets.size() + 31) / 32);
+    uint32_t *mask = nullptr;
+    const int64_t **ptrs = nullptr;
+    if (hipMalloc(&mask, sizeof(uint32_t) * size_t(n) * size_t(words)) != hipSuccess) {
+      (void)hipGetLastError();
+      continue;
+    }
+    g->nz_masks.push_back(mask);
+    std::vector<const int64_t *> h(ets.size());
+    for (size_t k = 0; k < ets.size(); ++k) h[k] = g->et[ets[k]].indptr;
+    hipError_t e = hipMalloc(&ptrs, sizeof(int64_t *) * h.size());
+    if (e == hipSuccess)
+      e = hipMemcpy(ptrs, h.data(), sizeof(int64_t *) * h.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = launch_nonempty_mask(ptrs, int32_t(ets.size()), words, n, mask, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    (void)hipFree(ptrs);
+    if (e != hipSuccess) return e;
+    for (size_t k = 0; k < ets.size(); ++k) {
+      ETypeInfo &E = g->et[ets[k]];
+      E.nz_mask = mask;
+      E.nz_words = words;
+      E.nz_slot = int32_t(k);
+    }
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *hg_last_error(void) { return g_last_error.c_str(); }
@@ -1391,6 +1439,11 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
     delete g;
     return fail(HG_EINVAL, "hg_create: CSC arrays are invalid (indptr not starting at 0, "
                            "decreasing, not ending at nnz, or an index out of range)");
+  }
+  if ((e = build_nonempty_masks(g, stream)) != hipSuccess) {
+    hg_status st = fail_hip(e, "hg_create: non-empty masks");
+    free_graph(g);
+    return st;
   }
   *out = g;
   return HG_OK;
@@ -1618,6 +1671,7 @@ void layout_types(hg_graph *g) {
 void free_graph(hg_graph *g) {
   for (auto &kv : g->bundles) free_graph(kv.second);
   for (auto *w : g->ws) free_workspace(w);
+  for (uint32_t *m : g->nz_masks) (void)hipFree(m);
   (void)hipFree(g->d_tile_base);
   delete g;
 }

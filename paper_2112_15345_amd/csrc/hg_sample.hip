@@ -114,7 +114,10 @@ struct CountTable {
   const int64_t *indptr[kCountMaxEtypes];
   const int64_t *front[kCountMaxEtypes];
   int64_t n_dst[kCountMaxEtypes];
+  const uint32_t *nz_mask[kCountMaxEtypes];
   int32_t fanout[kCountMaxEtypes];
+  int32_t nz_words[kCountMaxEtypes];
+  int32_t nz_slot[kCountMaxEtypes];
 };
 
 template <bool kStaged>
@@ -129,6 +132,9 @@ struct CountView {
   }
   __device__ int64_t n_dst(int e) const { return kStaged ? t->n_dst[e] : es[e].n_dst_nodes; }
   __device__ int32_t fanout(int e) const { return kStaged ? t->fanout[e] : hv->fanout[e]; }
+  __device__ const uint32_t *nz_mask(int e) const { return kStaged ? t->nz_mask[e] : es[e].nz_mask; }
+  __device__ int32_t nz_words(int e) const { return kStaged ? t->nz_words[e] : es[e].nz_words; }
+  __device__ int32_t nz_slot(int e) const { return kStaged ? t->nz_slot[e] : es[e].nz_slot; }
 };
 
 // Thread i of a tile owns kPairItems consecutive pairs.  The pair's edge type
@@ -151,6 +157,9 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
         table.front[e] = hv.frontier[E.dst_type];
         table.n_dst[e] = E.n_dst_nodes;
         table.fanout[e] = hv.fanout[e];
+        table.nz_mask[e] = E.nz_mask;
+        table.nz_words[e] = E.nz_words;
+        table.nz_slot[e] = E.nz_slot;
       }
     }
   }
@@ -202,6 +211,17 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
         atomicOr(err, kErrSeedRange);
     }
   }
+  // with a non-empty mask, a pair whose destination has no in-edge of its
+  // type reads no indptr (one mask word, shared by the vertex's edge types)
+#pragma unroll
+  for (int k = 0; k < kPairItems; ++k) {
+    const uint32_t *m = ip[k] ? V.nz_mask(etype[k]) : nullptr;
+    if (m) {
+      const int32_t slot = V.nz_slot(etype[k]);
+      const uint32_t w = load_global(m + v[k] * V.nz_words(etype[k]) + (slot >> 5));
+      if (((w >> (slot & 31)) & 1u) == 0) ip[k] = nullptr;
+    }
+  }
   int64_t lo[kPairItems], hi[kPairItems];
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
@@ -228,8 +248,10 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     } else if (s > 0 && !(nx == 0 && s == deg && deg <= kThreadTakeAll)) {
       c[k].wave = 1;  // pairs with excluded edges always take this role
     }
-    pa.plo[p] = lo[k];
-    pa.pdeg[p] = deg;
+    if (deg > 0) {  // nothing reads these for an empty pair
+      pa.plo[p] = lo[k];
+      pa.pdeg[p] = deg;
+    }
   }
 
   // block scan of the per-thread sums, then the tile's prefix by look-back
@@ -887,6 +909,23 @@ __global__ void k_check_etype(const int64_t *indptr, int64_t n_dst,
   }
 }
 
+// One thread per destination vertex: its row of the non-empty mask, from
+// the indptr of every edge type into its node type (coalesced across threads).
+__global__ void k_nonempty_mask(const int64_t *const *indptrs, int32_t n_etypes, int32_t words,
+                                int64_t n, uint32_t *mask) {
+  for (int64_t v = grid_stride_start(); v < n; v += grid_stride_step()) {
+    uint32_t w = 0;
+    for (int32_t k = 0; k < n_etypes; ++k) {
+      const int64_t *ip = indptrs[k];
+      if (ip[v + 1] > ip[v]) w |= 1u << (k & 31);
+      if ((k & 31) == 31 || k == n_etypes - 1) {
+        mask[v * words + (k >> 5)] = w;
+        w = 0;
+      }
+    }
+  }
+}
+
 __global__ void k_philox(const uint32_t *ctr, uint32_t k0, uint32_t k1,
                          int64_t n, uint32_t *out) {
   for (int64_t i = grid_stride_start(); i < n; i += grid_stride_step()) {
@@ -1068,6 +1107,14 @@ hipError_t launch_check_etype(const int64_t *indptr, int64_t n_dst,
   const int64_t n = n_dst > nnz ? n_dst : nnz;
   hipLaunchKernelGGL(k_check_etype, dim3(grid_for(n, 256, 8192)), dim3(256), 0,
                      stream, indptr, n_dst, indices, nnz, n_src, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_nonempty_mask(const int64_t *const *indptrs, int32_t n_etypes, int32_t words,
+                                int64_t n, uint32_t *mask, hipStream_t stream) {
+  if (n <= 0 || n_etypes <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_nonempty_mask, dim3(grid_for(n, 256, 16384)), dim3(256), 0, stream,
+                     indptrs, n_etypes, words, n, mask);
   return hipGetLastError();
 }
 

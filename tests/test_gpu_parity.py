@@ -124,6 +124,56 @@ def test_hub_selection(olib, deg, k, bits):
         assert not diffs, "\n".join(diffs)
 
 
+def many_relations(rng, R, n0=300, n1=80):
+    """Two node types and R edge types, the first 40 and most others into type
+    0 (so that type 0 gets the per-vertex non-empty mask): per edge type a share of the
+    destinations (none, few, some, all) has in-edges, some edge types empty."""
+    nn = [n0, n1]
+    ets = []
+    for e in range(R):
+        d = 0 if e < 40 or rng.random() < 0.85 else 1
+        s = int(rng.integers(0, 2))
+        share = [0.0, 0.02, 0.2, 1.0][int(rng.integers(0, 4))]
+        indptr, indices = [0], []
+        for _v in range(nn[d]):
+            k = int(rng.integers(1, 12)) if rng.random() < share else 0
+            indices.extend(int(x) for x in np.sort(rng.choice(nn[s], size=k, replace=False)))
+            indptr.append(len(indices))
+        ets.append((s, d, np.array(indptr, np.int64), np.array(indices, np.int64)))
+    feats = [rng.standard_normal((n0, 4)).astype(np.float32), None]
+    return nn, ets, feats
+
+
+# 16 etypes into a type: the smallest with a mask; 33 and 70: rows of 2 and
+# 3 words
+@pytest.mark.parametrize("R", [16, 33, 70])
+def test_many_relations(olib, R):
+    rng = np.random.default_rng(70 + R)
+    nn, ets, feats = many_relations(rng, R)
+    g = gpu_graph(nn, ets, feats)
+    host = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib)
+    for c in range(6):
+        seeds = [rng.choice(nn[0], size=int(rng.integers(1, 60)), replace=False).astype(np.int64),
+                 rng.choice(nn[1], size=int(rng.integers(0, 10)), replace=False).astype(np.int64)]
+        H = int(rng.integers(1, 4))
+        fan = [[[-1, 0, 1, 3, 10][int(rng.integers(0, 5))] for _ in range(R)] for _ in range(H)]
+        sigma = int(rng.integers(0, 1 << 63))
+        say(f"many relations R={R} case {c}: H={H}")
+        b = g.sample_blocks(gpu_seeds(seeds), fan, sigma, gather="all")
+        got = result_dict(g, b)
+        ref = host.sample_blocks(seeds, fan, sigma)
+        diffs = compare(ref, got, 2, R, H)
+        assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
+        assert b.features(0).cpu().numpy().tobytes() == feats[0][got["input"][0]].tobytes()
+        # the same batches bundled (the copies share the masks)
+        bl = g.sample_bundle([gpu_seeds(seeds)] * 3, fan, [sigma, sigma + 1, sigma + 2],
+                             gather=[])
+        for k in range(3):
+            refk = ref if k == 0 else host.sample_blocks(seeds, fan, sigma + k)
+            diffs = compare(refk, result_dict(g, bl[k]), 2, R, H)
+            assert not diffs, f"case {c} bundle copy {k}: " + "\n".join(diffs[:10])
+
+
 @pytest.mark.parametrize("bits", [1, 2, 3, 4, 8])
 def test_forced_ties(olib, bits):
     rng = np.random.default_rng(77 + bits)
