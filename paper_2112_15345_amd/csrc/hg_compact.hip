@@ -229,16 +229,53 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_single(CompactArgs A, uin
   assign_bits(A, t, first, tile, tw, A.hv.nF[t] + ex[0] + pre);
 }
 
-__global__ void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
-                          const int64_t *tile_base, const int64_t *small,
-                          int32_t n_types, int32_t n_etypes, int64_t n_edges,
-                          const int64_t *src_gid, int32_t *src_local) {
+// Edge types whose edge starts and source maps the relabel stages in LDS.
+constexpr int kRelabelMaxEtypes = 2048;
+constexpr int kRelabelItems = 4;
+
+// src_local[j] = map of edge j's source type at src_gid[j].  The etype of an
+// edge is found by binary search over the edge starts (in LDS when staged);
+// each thread looks up kRelabelItems edges at once.
+template <bool kStaged>
+__global__ __launch_bounds__(256) void k_relabel(HopView hv, HopView next, const EtypeStatic *es,
+                                                 const int64_t *tile_base, const int64_t *small,
+                                                 int32_t n_types, int32_t n_etypes,
+                                                 int64_t n_edges, const int64_t *src_gid,
+                                                 int32_t *src_local) {
+  extern __shared__ __align__(16) char relabel_lds[];
   if (blockIdx.x == 0)
     plan_next_hop(hv, next, es, tile_base, small, n_types, n_etypes);
   const int64_t *ebase = small + kSlotNew + n_types;
-  for (int64_t j = gs_start(); j < n_edges; j += gs_step()) {
-    const int e = find_segment(ebase, n_etypes, j);
-    src_local[j] = es[e].src_map[src_gid[j]];
+  int64_t *s_eb = reinterpret_cast<int64_t *>(relabel_lds);
+  int32_t **s_map = reinterpret_cast<int32_t **>(s_eb + n_etypes + 1);
+  if (kStaged) {
+    for (int e = threadIdx.x; e <= n_etypes; e += blockDim.x) {
+      s_eb[e] = ebase[e];
+      if (e < n_etypes) s_map[e] = es[e].src_map;
+    }
+    __syncthreads();
+  }
+  const int64_t step = gs_step();
+  for (int64_t j0 = gs_start(); j0 < n_edges; j0 += kRelabelItems * step) {
+    int64_t g[kRelabelItems];
+    int32_t *m[kRelabelItems];
+#pragma unroll
+    for (int u = 0; u < kRelabelItems; ++u) {
+      const int64_t j = j0 + u * step;
+      g[u] = 0;
+      m[u] = nullptr;
+      if (j < n_edges) {
+        g[u] = src_gid[j];
+        const int e = find_segment(kStaged ? s_eb : ebase, n_etypes, j);
+        m[u] = kStaged ? s_map[e] : es[e].src_map;
+      }
+    }
+    int32_t l[kRelabelItems];
+#pragma unroll
+    for (int u = 0; u < kRelabelItems; ++u) l[u] = m[u] ? m[u][g[u]] : 0;
+#pragma unroll
+    for (int u = 0; u < kRelabelItems; ++u)
+      if (m[u]) src_local[j0 + u * step] = l[u];
   }
 }
 
@@ -276,9 +313,14 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *src_gid, int32_t *src_local,
                           hipStream_t stream) {
   // at least one block: block 0 plans the next hop
-  hipLaunchKernelGGL(k_relabel, dim3(grid_for(n_edges, 256)), dim3(256), 0, stream, hv,
-                     next, es, tile_base, small, n_types, n_etypes, n_edges, src_gid,
-                     src_local);
+  const unsigned grid = grid_for((n_edges + kRelabelItems - 1) / kRelabelItems, 256, 4096);
+  if (n_etypes <= kRelabelMaxEtypes)
+    hipLaunchKernelGGL(k_relabel<true>, dim3(grid), dim3(256),
+                       size_t(16) * (n_etypes + 1), stream, hv, next, es, tile_base, small,
+                       n_types, n_etypes, n_edges, src_gid, src_local);
+  else
+    hipLaunchKernelGGL(k_relabel<false>, dim3(grid), dim3(256), 0, stream, hv, next, es,
+                       tile_base, small, n_types, n_etypes, n_edges, src_gid, src_local);
   return hipGetLastError();
 }
 

@@ -106,19 +106,32 @@ struct PairCounts {
   int64_t s, nch, wave, hub;
 };
 
-// Per edge type, what the counting pass reads for every pair; staged in LDS
-// when the graph has at most kCountMaxEtypes edge types.
-constexpr int kCountMaxEtypes = 256;
+// Per edge type, what the counting pass reads for every pair; staged in
+// (dynamic) LDS, 52 bytes per edge type, when the graph has at most
+// kCountMaxEtypes edge types (a bundle's virtual graph counts each copy).
+constexpr int kCountMaxEtypes = 1200;
 struct CountTable {
-  int64_t pbase[kCountMaxEtypes + 1];
-  const int64_t *indptr[kCountMaxEtypes];
-  const int64_t *front[kCountMaxEtypes];
-  int64_t n_dst[kCountMaxEtypes];
-  const uint32_t *nz_mask[kCountMaxEtypes];
-  int32_t fanout[kCountMaxEtypes];
-  int32_t nz_words[kCountMaxEtypes];
-  int32_t nz_slot[kCountMaxEtypes];
+  int64_t *pbase;  // [n + 1]
+  const int64_t **indptr;
+  const int64_t **front;
+  int64_t *n_dst;
+  const uint32_t **nz_mask;
+  int32_t *fanout, *nz_words, *nz_slot;
+  __host__ __device__ static constexpr size_t bytes(int n) {
+    return size_t(8) * (n + 1) + size_t(8) * 4 * n + size_t(4) * 3 * n;
+  }
+  __device__ void carve(char *p, int n) {
+    pbase = reinterpret_cast<int64_t *>(p);
+    indptr = reinterpret_cast<const int64_t **>(pbase + n + 1);
+    front = reinterpret_cast<const int64_t **>(indptr + n);
+    n_dst = reinterpret_cast<int64_t *>(front + n);
+    nz_mask = reinterpret_cast<const uint32_t **>(n_dst + n);
+    fanout = reinterpret_cast<int32_t *>(nz_mask + n);
+    nz_words = fanout + n;
+    nz_slot = nz_words + n;
+  }
 };
+static_assert(CountTable::bytes(kCountMaxEtypes) <= 64 * 1024, "the table fits 64 KiB of LDS");
 
 template <bool kStaged>
 struct CountView {
@@ -147,8 +160,10 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
     uint64_t ticket_base, ExclView X, int64_t *small) {
   __shared__ int64_t lds[16];
-  __shared__ CountTable table;
+  extern __shared__ __align__(16) char count_lds[];
+  CountTable table;
   if (kStaged) {
+    table.carve(count_lds, n_etypes);
     for (int e = threadIdx.x; e <= n_etypes; e += kTileThreads) {
       table.pbase[e] = hv.pair_base[e];
       if (e < n_etypes) {
@@ -990,8 +1005,9 @@ template <bool kStaged, int kItems>
 void count_launch(HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
                   int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
                   uint64_t ticket_base, ExclView X, int64_t *small, hipStream_t stream) {
+  const size_t lds = kStaged ? CountTable::bytes(n_etypes) : 0;
   hipLaunchKernelGGL((k_count_scan<kStaged, kItems>), dim3(unsigned(count_tiles(n_items))),
-                     dim3(kTileThreads), 0, stream, hv, es, n_etypes, n_types, n_items, pa,
+                     dim3(kTileThreads), lds, stream, hv, es, n_etypes, n_types, n_items, pa,
                      lb, epoch, ticket_base, X, small);
 }
 
