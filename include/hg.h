@@ -100,9 +100,12 @@ typedef struct hg_pipeline hg_pipeline;
  * Checks the descriptors on the host and the arrays on the device (indptr
  * starts at 0, never decreases and ends at nnz; every index is a valid
  * source), synchronising `stream` once.  Returns HG_EINVAL on a bad
- * descriptor or array.  The handle may be used from several threads and
- * streams at once (the graph is read-only, Sec. 4.2.1 ahead-of-time work on
- * immutable data). */
+ * descriptor or array.  A node type with 16 or more incoming edge types gets
+ * a graph-owned mask of ceil(k / 32) 32-bit words per vertex (k = its
+ * incoming edge types) saying which of them have in-edges there; it lets the
+ * sampler skip empty (vertex, edge type) pairs and is freed by hg_destroy.
+ * The handle may be used from several threads and streams at once (the
+ * graph is read-only, Sec. 4.2.1 ahead-of-time work on immutable data). */
 hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
                     const hg_etype_desc *etypes, int32_t n_etypes,
                     const hg_allocator *allocator, hipStream_t stream,
