@@ -231,7 +231,7 @@ __global__ __launch_bounds__(kTileThreads) void k_bits_single(CompactArgs A, uin
 
 // Edge types whose edge starts and source maps the relabel stages in LDS.
 constexpr int kRelabelMaxEtypes = 2048;
-constexpr int kRelabelItems = 4;
+constexpr int kRelabelItems = 1;
 
 // src_local[j] = map of edge j's source type at src_gid[j].  The etype of an
 // edge is found by binary search over the edge starts (in LDS when staged);
@@ -313,7 +313,7 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *src_gid, int32_t *src_local,
                           hipStream_t stream) {
   // at least one block: block 0 plans the next hop
-  const unsigned grid = grid_for((n_edges + kRelabelItems - 1) / kRelabelItems, 256, 4096);
+  const unsigned grid = grid_for((n_edges + kRelabelItems - 1) / kRelabelItems, 256, 1 << 20);
   if (n_etypes <= kRelabelMaxEtypes)
     hipLaunchKernelGGL(k_relabel<true>, dim3(grid), dim3(256),
                        size_t(16) * (n_etypes + 1), stream, hv, next, es, tile_base, small,

@@ -576,20 +576,41 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
   }
 }
 
-// Role B: a wavefront per pair (large take-all, or selection among at most
-// kHubChunk edges with the candidate list in LDS).
-__device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
-                                int64_t w) {
+// Role B: a wavefront per kWavePairs pairs (large take-all, or selection
+// among at most kHubChunk edges with the candidate list in LDS), one after
+// the other; what every pair needs is loaded for all of them first, so the
+// wavefront waits on those loads once.
+constexpr int kWavePairs = 2;
+
+struct WavePair {
+  EmitCtx c;
+  KeyCtx kc;
+  int64_t lo, deg, o, s;
+  int32_t nx;
+  int e;
+};
+
+__device__ __forceinline__ WavePair wave_pair(const SampleArgs &A, int64_t p) {
+  WavePair P;
+  P.e = A.pa.pet[p];
+  const int64_t i = p - A.hv.pair_base[P.e];
+  P.c = make_ctx(A.es[P.e], A.src_gid, A.eid, A.dst_local, i);
+  P.kc = key_ctx(A, P.e);
+  P.lo = A.pa.plo[p];
+  P.deg = A.pa.pdeg[p];
+  P.o = A.pa.off[p];
+  P.s = A.pa.off[p + 1] - P.o;
+  P.nx = excl_count(A.X, P.e, i);
+  return P;
+}
+
+__device__ void wave_pair_run(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
+                              const WavePair &P) {
   const int lane = lane_id();
-  const int64_t p = A.pa.wlist[w];
-  const int e = A.pa.pet[p];
-  const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
-                             p - A.hv.pair_base[e]);
-  const int64_t lo = A.pa.plo[p];
-  const int64_t deg = A.pa.pdeg[p];
-  const int64_t o = A.pa.off[p];
-  const int64_t s = A.pa.off[p + 1] - o;
-  const int32_t nx = excl_count(A.X, e, p - A.hv.pair_base[e]);
+  const int e = P.e;
+  const EmitCtx &c = P.c;
+  const int64_t lo = P.lo, deg = P.deg, o = P.o, s = P.s;
+  const int32_t nx = P.nx;
   if (s == deg) {  // every in-edge is kept
     for (int64_t j = lane; j < deg; j += kWave) emit_edge(c, o + j, lo + j);
     return;
@@ -608,7 +629,7 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   const int64_t K = s;
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
-  const KeyCtx kc = key_ctx(A, e);
+  const KeyCtx kc = P.kc;
   const uint32_t k0 = kc.k0, k1 = kc.k1;
   const uint64_t g_first = uint64_t(lo) >> 2;
   const uint64_t g_last = uint64_t(lo + deg - 1) >> 2;
@@ -673,6 +694,27 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
   select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift, A.X, e, nx > 0);
+}
+
+__device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
+                                int64_t w) {
+  WavePair P[kWavePairs];
+  int n = 0;
+#pragma unroll
+  for (int k = 0; k < kWavePairs; ++k) {
+    const int64_t x = w * kWavePairs + k;
+    if (x < A.n_wave) {
+      P[k] = wave_pair(A, A.pa.wlist[x]);
+      n = k + 1;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kWavePairs; ++k) {
+    if (k < n) {
+      if (k > 0) wave_sync();  // the previous pair's candidate reads are done
+      wave_pair_run(A, ck, cj, P[k]);
+    }
+  }
 }
 
 // Role C: wavefront w takes the hub chunks [w * chunks_per_wave, ...) in
@@ -886,19 +928,19 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   const int wave = threadIdx.x / kWave;
   if (b == 0 && int(threadIdx.x) < A.n_src_out)
     A.src_out_slot[threadIdx.x] = A.src_out_new[threadIdx.x];
-  // the longest work first: hub chunks, then wavefront pairs, then groups of
-  // small take-all pairs, so that short blocks fill in behind long ones
-  if (b < A.blocks_c) {
-    const int64_t w = b * kSampleWaves + wave;
-    if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
-  } else if (b < A.blocks_c + A.blocks_b) {
-    const int64_t w = (b - A.blocks_c) * kSampleWaves + wave;
-    if (w < A.n_wave) role_wave_pairs(A, s_cand[wave][0], s_cand[wave][1], w);
-  } else {
+  // the longest wavefronts first: groups of small take-all pairs (a
+  // wavefront per 64 pairs), then hub chunks, then wavefront pairs, so that
+  // short wavefronts fill in behind long ones
+  if (b < A.blocks_a) {
     // the candidate lists are not used by this role: reuse their LDS
-    const int64_t ba = b - A.blocks_c - A.blocks_b;
     GroupLds *g = reinterpret_cast<GroupLds *>(&s_cand[wave][0][0]);
-    role_pair_groups(A, *g, ba * kSampleWaves + wave, ba == 0);
+    role_pair_groups(A, *g, b * kSampleWaves + wave, b == 0);
+  } else if (b < A.blocks_a + A.blocks_c) {
+    const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
+    if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
+  } else {
+    const int64_t w = (b - A.blocks_a - A.blocks_c) * kSampleWaves + wave;
+    if (w * kWavePairs < A.n_wave) role_wave_pairs(A, s_cand[wave][0], s_cand[wave][1], w);
   }
 }
 
@@ -1056,7 +1098,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.n_hubs = n_hubs;
   // role A always has a block, for the closing CSC entries
   A.blocks_a = std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads);
-  A.blocks_b = (n_wave + kSampleWaves - 1) / kSampleWaves;
+  A.blocks_b = ((n_wave + kWavePairs - 1) / kWavePairs + kSampleWaves - 1) / kSampleWaves;
   // runs of chunks per wavefront: long enough to amortise finding the hub,
   // short enough to leave about kHubWaves wavefronts for the chip
   A.chunks_per_wave = std::min<int64_t>(kMaxChunksPerWave, std::max<int64_t>(1, n_chunks / kHubWaves));
