@@ -28,11 +28,18 @@ __device__ __forceinline__ V zero_vec() {
   return V(0);
 }
 
+// Rows of a gather: n, or min(*n_dev, n) when the count is on the device.
+__device__ __forceinline__ int64_t rows_of(int64_t n, const int64_t *n_dev) {
+  return n_dev ? min(*n_dev, n) : n;
+}
+
 // rv = vectors per row, rv <= kThreads.
 template <typename V>
 __global__ __launch_bounds__(kThreads) void k_gather(
     const V *__restrict__ table, int64_t n_rows, int32_t rv,
-    const int64_t *__restrict__ ids, int64_t n, V *__restrict__ out) {
+    const int64_t *__restrict__ ids, int64_t n_max, V *__restrict__ out,
+    const int64_t *n_dev) {
+  const int64_t n = rows_of(n_max, n_dev);
   const int rpp = kThreads / rv;  // rows per pass
   const int r_in = threadIdx.x / rv;
   const int col = threadIdx.x - r_in * rv;
@@ -62,7 +69,9 @@ __global__ __launch_bounds__(kThreads) void k_gather(
 template <typename V>
 __global__ __launch_bounds__(kThreads) void k_gather_wide(
     const V *__restrict__ table, int64_t n_rows, int64_t rv,
-    const int64_t *__restrict__ ids, int64_t n, V *__restrict__ out) {
+    const int64_t *__restrict__ ids, int64_t n_max, V *__restrict__ out,
+    const int64_t *n_dev) {
+  const int64_t n = rows_of(n_max, n_dev);
   for (int64_t row = blockIdx.x; row < n; row += gridDim.x) {
     const int64_t id = ids[row];
     const bool ok = id >= 0 && id < n_rows;
@@ -77,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_wide(
 template <typename V>
 hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
                         const int64_t *ids, int64_t n, void *out,
-                        hipStream_t stream) {
+                        hipStream_t stream, const int64_t *n_dev) {
   const int64_t rv = row_bytes / int64_t(sizeof(V));
   if (rv <= kThreads) {
     const int64_t rows_per_block = int64_t(kThreads / rv) * kUnroll;
@@ -85,12 +94,12 @@ hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(k_gather<V>, dim3(unsigned(blocks)), dim3(kThreads), 0,
                        stream, static_cast<const V *>(table), n_rows, int32_t(rv),
-                       ids, n, static_cast<V *>(out));
+                       ids, n, static_cast<V *>(out), n_dev);
   } else {
     int64_t blocks = n < 65536 ? n : 65536;
     hipLaunchKernelGGL(k_gather_wide<V>, dim3(unsigned(blocks)), dim3(kThreads),
                        0, stream, static_cast<const V *>(table), n_rows, rv, ids,
-                       n, static_cast<V *>(out));
+                       n, static_cast<V *>(out), n_dev);
   }
   return hipGetLastError();
 }
@@ -98,15 +107,19 @@ hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
 // Several gathers in one launch: segment s owns blocks
 // [block_base[s], block_base[s+1]) and moves its rows as k_gather does.
 constexpr int kMaxSegs = 32;
+// Passes per block (at the capacity) of a segment whose row count is on the
+// device.
+constexpr int64_t kDevCountPasses = 4;
 
 struct GatherSeg {
   const void *table;
   int64_t n_rows;
   const int64_t *ids;
-  int64_t n;
+  int64_t n;  // rows, or their bound with n_dev
   void *out;
   int64_t rv;
   int64_t block_base;
+  const int64_t *n_dev;
 };
 
 struct GatherBatch {
@@ -129,14 +142,17 @@ __global__ __launch_bounds__(kThreads) void k_gather_multi(GatherBatch B) {
   const int r_in = threadIdx.x / rv;
   const int col = threadIdx.x - r_in * rv;
   if (r_in >= rpp) return;
+  // (a device count costs each block one dependent load before its first
+  // rows: such segments get fewer blocks, each looping over more rows)
+  const int64_t n = rows_of(G.n, G.n_dev);
   const int64_t rows_per_block = int64_t(rpp) * kUnroll;
-  for (int64_t r0 = blk * rows_per_block; r0 < G.n; r0 += nb * rows_per_block) {
+  for (int64_t r0 = blk * rows_per_block; r0 < n; r0 += nb * rows_per_block) {
     V v[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t row = r0 + int64_t(u) * rpp + r_in;
       v[u] = zero_vec<V>();
-      if (row < G.n) {
+      if (row < n) {
         const int64_t id = G.ids[row];
         if (id >= 0 && id < G.n_rows) v[u] = table[id * rv + col];
       }
@@ -144,7 +160,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_multi(GatherBatch B) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t row = r0 + int64_t(u) * rpp + r_in;
-      if (row < G.n) __builtin_nontemporal_store(v[u], out + row * rv + col);
+      if (row < n) __builtin_nontemporal_store(v[u], out + row * rv + col);
     }
   }
 }
@@ -163,14 +179,14 @@ int vec_bytes(const void *table, const void *out, int64_t row_bytes) {
 
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
-                         hipStream_t stream) {
+                         hipStream_t stream, const int64_t *n_dev) {
   if (n <= 0 || row_bytes <= 0) return hipSuccess;
   switch (vec_bytes(table, out, row_bytes)) {
-    case 16: return launch_typed<u32x4>(table, n_rows, row_bytes, ids, n, out, stream);
-    case 8: return launch_typed<u32x2>(table, n_rows, row_bytes, ids, n, out, stream);
-    case 4: return launch_typed<uint32_t>(table, n_rows, row_bytes, ids, n, out, stream);
-    case 2: return launch_typed<uint16_t>(table, n_rows, row_bytes, ids, n, out, stream);
-    default: return launch_typed<uint8_t>(table, n_rows, row_bytes, ids, n, out, stream);
+    case 16: return launch_typed<u32x4>(table, n_rows, row_bytes, ids, n, out, stream, n_dev);
+    case 8: return launch_typed<u32x2>(table, n_rows, row_bytes, ids, n, out, stream, n_dev);
+    case 4: return launch_typed<uint32_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev);
+    case 2: return launch_typed<uint16_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev);
+    default: return launch_typed<uint8_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev);
   }
 }
 
@@ -212,7 +228,8 @@ hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_
     if (J.n <= 0 || J.row_bytes <= 0) continue;
     const int64_t rv = J.row_bytes / 16;
     if (vec_bytes(J.table, J.out, J.row_bytes) != 16 || rv > kThreads) {
-      hipError_t e = launch_gather(J.table, J.n_rows, J.row_bytes, J.ids, J.n, J.out, stream);
+      hipError_t e =
+          launch_gather(J.table, J.n_rows, J.row_bytes, J.ids, J.n, J.out, stream, J.n_dev);
       if (e != hipSuccess) return e;
       continue;
     }
@@ -222,8 +239,9 @@ hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_
     }
     const int64_t rows_per_block = int64_t(kThreads / rv) * kUnroll;
     int64_t nb = (J.n + rows_per_block - 1) / rows_per_block;
+    if (J.n_dev) nb = (nb + kDevCountPasses - 1) / kDevCountPasses;
     if (nb > 65536) nb = 65536;
-    B.seg[B.n_seg++] = GatherSeg{J.table, J.n_rows, J.ids, J.n, J.out, rv, blocks};
+    B.seg[B.n_seg++] = GatherSeg{J.table, J.n_rows, J.ids, J.n, J.out, rv, blocks, J.n_dev};
     blocks += nb;
   }
   return flush();

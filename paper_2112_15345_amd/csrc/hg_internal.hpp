@@ -32,6 +32,9 @@ constexpr int kCandCap = 512;
 
 // Node types whose per-hop table entries travel inside a launch's arguments.
 constexpr int kInlineTypes = 8;
+// Node types whose source-list pointers the sampler launch stores into the
+// hop's table itself (a bundle of 16 mini-batches of 4 node types is 64).
+constexpr int kInlineSrcOut = 64;
 
 // Pairs whose in-edges are all kept and number at most this many are copied
 // 64 pairs per wavefront; larger ones by a wavefront each.
@@ -182,7 +185,7 @@ hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes
 // Then one wavefront per hub selects from its list.  Writes each pair's kept
 // edges at off[p], grouped by pair, ascending edge ID: source vertex, edge
 // ID, destination local ID.
-// The sampler launches.  With n_src_out <= kInlineTypes the first one also
+// The sampler launches.  With n_src_out <= kInlineSrcOut the first one also
 // stores src_out[0..n_src_out) into src_out_slot (the hop's table entries).
 // Edge type e is keyed as type e % key_R with seed sigmas[e / key_R] (device).
 hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
@@ -305,9 +308,11 @@ hipError_t launch_check_etype(const int64_t *indptr, int64_t n_dst,
 // Row gather: out[i] = table[ids[i]] (row_bytes bytes), zero row when out of
 // range.  Picks the widest vector width that divides row_bytes and the
 // alignment of both pointers.
+// With n_dev, the rows are min(*n_dev, n) (read on the device; n bounds them
+// and sizes the grid).
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
-                         hipStream_t stream);
+                         hipStream_t stream, const int64_t *n_dev = nullptr);
 
 // One row gather of launch_gather_multi.
 struct GatherJob {
@@ -315,8 +320,9 @@ struct GatherJob {
   int64_t n_rows;
   int64_t row_bytes;
   const int64_t *ids;
-  int64_t n;
+  int64_t n;             // rows (or, with n_dev, their bound)
   void *out;
+  const int64_t *n_dev;  // device row count, or nullptr
 };
 // Several row gathers, as few launches as possible.  `start` / `stop` (may be
 // NULL) are recorded by the batched launches themselves.

@@ -528,6 +528,14 @@ struct SampleRun {
   // unless wt_dirty
   const int32_t *layer_sizes = nullptr;
   bool wt_dirty = false;
+
+  // the feature gather of the input frontier, launched before the last wait:
+  // node types, events carried by its launches, and whether it was launched
+  const int32_t *gtypes = nullptr;
+  int32_t n_gather = 0;
+  hipEvent_t g_start = nullptr, g_stop = nullptr;
+  bool gathered = false;
+  hg_status early_gather(const std::vector<int64_t *> &ids, const std::vector<int64_t> &cap);
   // a layer-wise hop's kept edges (their per-etype starts are read back at the
   // next wait): the hop and its output arrays
   int32_t lw_hop = -1;
@@ -603,11 +611,22 @@ struct SampleRun {
   // plus a stream wait).  Every few hundred polls the stream is queried, so
   // a failed kernel (whose successors never run) ends the wait with its error.
   hipError_t sync_small(bool last = false) {
+    uint64_t seq;
+    hipError_t e = publish(last, &seq);
+    return e == hipSuccess ? wait_published(seq) : e;
+  }
+  // The two halves of sync_small: the copy launch, and the wait for its flag
+  // (work launched in between runs while the host waits).
+  hipError_t publish(bool last, uint64_t *seq) {
     const int32_t n = int32_t(small_slots(g));
-    const uint64_t seq = ++ws->publish_seq;
-    hipError_t e = launch_publish(ws->dsmall, ws->hsmall, n, seq, last, stream);
+    *seq = ++ws->publish_seq;
+    hipError_t e = launch_publish(ws->dsmall, ws->hsmall, n, *seq, last, stream);
     if (e == hipSuccess && last) small_clean = true;
-    if (e != hipSuccess) return e;
+    return e;
+  }
+  hipError_t wait_published(uint64_t seq) {
+    hipError_t e;
+    const int32_t n = int32_t(small_slots(g));
     const volatile int64_t *flag = ws->hsmall + n;
     for (uint32_t i = 1; uint64_t(*flag) != seq; ++i) {
       if ((i & 255) == 0) {
@@ -1095,11 +1114,42 @@ hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
   return HG_OK;
 }
 
+// The gather of the input frontier, launched before the last readback: the
+// rows of type t are the first (device) count of region H's frontier sizes,
+// at most cap[t]; the feature arrays are sized for cap[t] rows.
+hg_status SampleRun::early_gather(const std::vector<int64_t *> &ids,
+                                  const std::vector<int64_t> &cap) {
+  Carve c;
+  std::vector<uint8_t *> dst(T, nullptr);
+  for (int32_t k = 0; k < n_gather; ++k) {
+    const int32_t t = gtypes[k];
+    c.add(&dst[t], cap[t] * g->nt[t].row_bytes);
+  }
+  void *base = c.allocate(g, stream);
+  if (!base) return fail(HG_ENOMEM, "feature arrays");
+  b->mem->ptrs.push_back(base);
+  const int64_t *counts = reinterpret_cast<const int64_t *>(dreg(H) + lay.nf);
+  std::vector<GatherJob> jobs;
+  for (int32_t k = 0; k < n_gather; ++k) {
+    const int32_t t = gtypes[k];
+    const NTypeInfo &N = g->nt[t];
+    b->feat[t] = dst[t];
+    jobs.push_back(GatherJob{N.feat, N.num_nodes, N.row_bytes, ids[t], cap[t], dst[t], counts + t});
+  }
+  hipError_t e = launch_gather_multi(jobs.data(), int32_t(jobs.size()), stream, g_start, g_stop);
+  if (e != hipSuccess) return fail_device(e, "gather");
+  gathered = true;
+  return HG_OK;
+}
+
 // The hop loop from region 0's frontier (sizes nF, or their bounds for an
 // edge-seeded call, whose sizes the device wrote); n_items >= pairs + 1.
 hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
   hipError_t e;
   int64_t P = 0;
+  // the last hop's source lists (the input frontier) and their capacities
+  std::vector<int64_t *> last_src(T, nullptr);
+  std::vector<int64_t> last_bound(T, 0);
   for (int32_t h = 0; h < H; ++h) {
     const HopView hv = view(h), nv = view(h + 1);
     // ---- 1. counting pass over at most n_items pair slots ----------------
@@ -1188,6 +1238,8 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     void *ob = oc.allocate(g, stream);
     if (!ob) return fail(HG_ENOMEM, "hop %d: block arrays", h);
     b->mem->ptrs.push_back(ob);
+    last_src = src_out;
+    last_bound = bound;
     Carve ec;
     int64_t *gid_tmp;
     ec.add(&gid_tmp, S);
@@ -1200,7 +1252,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     // this hop's source lists (also the next hop's frontier): written by the
     // sampler launch itself for a few types, else by their own launches
     int64_t **src_slot = reinterpret_cast<int64_t **>(dreg(h) + lay.src_out);
-    const bool inline_ptrs = T <= kInlineTypes;
+    const bool inline_ptrs = T <= kInlineSrcOut;
     if (!inline_ptrs &&
         (e = launch_store_ptrs(reinterpret_cast<void **>(src_slot),
                                reinterpret_cast<void *const *>(src_out.data()), T, stream)) !=
@@ -1268,8 +1320,18 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     n_items = next_pairs + 1;
   }
 
-  // final wait: new-vertex counts of the last hop
-  if ((e = sync_small(true)) != hipSuccess) return fail_device(e, "sync");
+  // final wait: new-vertex counts of the last hop.  The feature gather goes
+  // in behind the readback, so the device is busy with it during the wait.
+  uint64_t seq;
+  if ((e = publish(true, &seq)) != hipSuccess) return fail_device(e, "sync");
+  if (n_gather > 0) {
+    hg_status gs = early_gather(last_src, last_bound);
+    if (gs != HG_OK) {
+      (void)wait_published(seq);
+      return gs;
+    }
+  }
+  if ((e = wait_published(seq)) != hipSuccess) return fail_device(e, "sync");
   hg_status st = check_flags("compact");
   if (st != HG_OK) return st;
   if ((st = close_layer_edges()) != HG_OK) return st;
@@ -1478,7 +1540,8 @@ hg_status gather_into_blocks(hg_graph *g, hg_blocks *b, const int32_t *gtypes,
     const int32_t t = gtypes[k];
     const NTypeInfo &N = g->nt[t];
     b->feat[t] = dst[t];
-    jobs.push_back(GatherJob{N.feat, N.num_nodes, N.row_bytes, b->in_gid[t], b->in_n[t], dst[t]});
+    jobs.push_back(
+        GatherJob{N.feat, N.num_nodes, N.row_bytes, b->in_gid[t], b->in_n[t], dst[t], nullptr});
   }
   hipError_t e = launch_gather_multi(jobs.data(), int32_t(jobs.size()), stream, start, stop);
   if (e != hipSuccess) return fail_hip(e, "gather");
@@ -1525,6 +1588,10 @@ hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *
                        hipEvent_t start, hipEvent_t stop, hipStream_t stream, hg_blocks **out) {
   DeviceGuard dg(g->device);
   SampleRun run(g, stream, n_hops, fanouts, sigmas, n_sig, key_bits);
+  run.gtypes = gtypes;
+  run.n_gather = n_gather;
+  run.g_start = start;
+  run.g_stop = stop;
   hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
   if (st != HG_OK) return st;
   run.b = new (std::nothrow) hg_blocks();
@@ -1535,7 +1602,8 @@ hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *
   try {
     st = run.run(seeds, n_seeds);
     // the gather goes first: the map reset of finish() can wait behind it
-    if (st == HG_OK && n_gather > 0)
+    // (the hop loop launched it already unless there were no hops)
+    if (st == HG_OK && n_gather > 0 && !run.gathered)
       st = gather_into_blocks(g, run.b, gtypes, n_gather, start, stop, stream);
   } catch (const std::bad_alloc &) {
     st = fail(HG_ENOMEM, "hg_sample_blocks: out of host memory");
@@ -1556,6 +1624,8 @@ hg_status run_edge_sampling(hg_graph *g, const hg_edge_batch *eb, int32_t n_hops
                             int32_t n_gather, hipStream_t stream, hg_blocks **out) {
   DeviceGuard dg(g->device);
   SampleRun run(g, stream, n_hops, fanouts, &rng_seed, 1, 32);
+  run.gtypes = gtypes;
+  run.n_gather = n_gather;
   run.eb = eb;
   run.edge_tab = align_up(sizeof(int64_t) * size_t(g->R + 1)) +
                  align_up(sizeof(EdgeEtype) * size_t(std::max(g->R, 1)));
@@ -1568,7 +1638,7 @@ hg_status run_edge_sampling(hg_graph *g, const hg_edge_batch *eb, int32_t n_hops
   }
   try {
     st = run.run_edges();
-    if (st == HG_OK && n_gather > 0)
+    if (st == HG_OK && n_gather > 0 && !run.gathered)
       st = gather_into_blocks(g, run.b, gtypes, n_gather, nullptr, nullptr, stream);
   } catch (const std::bad_alloc &) {
     st = fail(HG_ENOMEM, "hg_sample_edge_blocks: out of host memory");
@@ -1590,6 +1660,8 @@ hg_status run_layer_sampling(hg_graph *g, const int64_t *const *seeds, const int
                              hg_blocks **out) {
   DeviceGuard dg(g->device);
   SampleRun run(g, stream, n_hops, nullptr, &rng_seed, 1, 32);
+  run.gtypes = gtypes;
+  run.n_gather = n_gather;
   run.layer_sizes = layer_sizes;
   hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
   if (st != HG_OK) return st;
@@ -1600,7 +1672,7 @@ hg_status run_layer_sampling(hg_graph *g, const int64_t *const *seeds, const int
   }
   try {
     st = run.run_layers(seeds, n_seeds);
-    if (st == HG_OK && n_gather > 0)
+    if (st == HG_OK && n_gather > 0 && !run.gathered)
       st = gather_into_blocks(g, run.b, gtypes, n_gather, nullptr, nullptr, stream);
   } catch (const std::bad_alloc &) {
     st = fail(HG_ENOMEM, "hg_sample_layers: out of host memory");
@@ -2042,7 +2114,8 @@ hg_status hg_gather_features_multi_timed(hg_graph *g, const hg_blocks *b,
       return fail(HG_EINVAL, "hg_gather_features_multi: node type %d has no features", t);
     if (b->in_n[t] > 0 && !outs[k])
       return fail(HG_EINVAL, "hg_gather_features_multi: output %d is NULL", k);
-    jobs.push_back(GatherJob{N.feat, N.num_nodes, N.row_bytes, b->in_gid[t], b->in_n[t], outs[k]});
+    jobs.push_back(
+        GatherJob{N.feat, N.num_nodes, N.row_bytes, b->in_gid[t], b->in_n[t], outs[k], nullptr});
   }
   DeviceGuard dg(g->device);
   clear_pending_error();

@@ -475,7 +475,7 @@ struct SampleArgs {
   // block 0 stores the hop's source-list pointers into the hop's table (read
   // only by later launches)
   int64_t **src_out_slot;
-  int64_t *src_out_new[kInlineTypes];
+  int64_t *src_out_new[kInlineSrcOut];
   int32_t n_src_out;
   ExclView X;
 };
@@ -1082,12 +1082,12 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          ExclView X, hipStream_t stream) {
-  if (n_src_out > kInlineTypes) return hipErrorInvalidValue;
+  if (n_src_out > kInlineSrcOut) return hipErrorInvalidValue;
   SampleArgs A;
   A.X = X;
   A.src_out_slot = src_out_slot;
   A.n_src_out = n_src_out;
-  for (int32_t t = 0; t < kInlineTypes; ++t) A.src_out_new[t] = t < n_src_out ? src_out[t] : nullptr;
+  for (int32_t t = 0; t < kInlineSrcOut; ++t) A.src_out_new[t] = t < n_src_out ? src_out[t] : nullptr;
   A.hv = hv;
   A.es = es;
   A.n_etypes = n_etypes;
