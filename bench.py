@@ -33,8 +33,8 @@ HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 # and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the counters
 # read for a 1 GiB device copy (profiles/gather_academic_traffic.md).  Valid
 # only for the gather source and the launch configuration it was measured on.
-GATHER_TRAFFIC = {"source_sha256_16": "26e6b8abbb8a5ffb", "workload": 2, "steps": 320,
-                  "warmup": 32, "bundle": 16, "workers": 0, "bytes_per_launch": 3989462851.1}
+GATHER_TRAFFIC = {"source_sha256_16": "307d950537d4b4f1", "workload": 2, "steps": 320,
+                  "warmup": 32, "bundle": 16, "workers": 0, "bytes_per_launch": 3989129455.2}
 
 
 def measured_gather_traffic(args):

@@ -107,9 +107,12 @@ hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
 // Several gathers in one launch: segment s owns blocks
 // [block_base[s], block_base[s+1]) and moves its rows as k_gather does.
 constexpr int kMaxSegs = 32;
-// Passes per block (at the capacity) of a segment whose row count is on the
-// device.
+// A segment whose row count is on the device pays one dependent load per
+// block before its first rows: when such segments would have more than
+// kDevCountBlocks blocks in all, each block makes up to kDevCountPasses passes
+// (at the capacity) instead of one, so that fewer blocks pay it.
 constexpr int64_t kDevCountPasses = 4;
+constexpr int64_t kDevCountBlocks = 8192;
 
 struct GatherSeg {
   const void *table;
@@ -200,12 +203,18 @@ hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_
   int64_t blocks = 0;
   int launches = 0;
   int64_t pending = 0;  // batched segments still to launch
+  int64_t dev_blocks = 0;  // one-pass blocks of the device-count segments
   for (int32_t k = 0; k < n_jobs; ++k) {
     const GatherJob &J = jobs[k];
     if (J.n > 0 && J.row_bytes > 0 && vec_bytes(J.table, J.out, J.row_bytes) == 16 &&
-        J.row_bytes / 16 <= kThreads)
+        J.row_bytes / 16 <= kThreads) {
       ++pending;
+      const int64_t rpb = int64_t(kThreads / (J.row_bytes / 16)) * kUnroll;
+      if (J.n_dev) dev_blocks += (J.n + rpb - 1) / rpb;
+    }
   }
+  const int64_t passes =
+      std::min<int64_t>(kDevCountPasses, std::max<int64_t>(1, dev_blocks / kDevCountBlocks));
   auto flush = [&]() -> hipError_t {
     if (B.n_seg == 0) return hipSuccess;
     B.block_end = blocks;
@@ -239,7 +248,7 @@ hipError_t launch_gather_multi(const GatherJob *jobs, int32_t n_jobs, hipStream_
     }
     const int64_t rows_per_block = int64_t(kThreads / rv) * kUnroll;
     int64_t nb = (J.n + rows_per_block - 1) / rows_per_block;
-    if (J.n_dev) nb = (nb + kDevCountPasses - 1) / kDevCountPasses;
+    if (J.n_dev) nb = (nb + passes - 1) / passes;
     if (nb > 65536) nb = 65536;
     B.seg[B.n_seg++] = GatherSeg{J.table, J.n_rows, J.ids, J.n, J.out, rv, blocks, J.n_dev};
     blocks += nb;
