@@ -29,12 +29,12 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 
 # Measured HBM traffic of one gather launch of the default run (academic
-# workload, bundles of 16, 32 warm-up + 320 timed mini-batches): FETCH_SIZE
+# workload, bundles of 32, 32 warm-up + 320 timed mini-batches): FETCH_SIZE
 # and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the counters
 # read for a 1 GiB device copy (profiles/gather_academic_traffic.md).  Valid
 # only for the gather source and the launch configuration it was measured on.
 GATHER_TRAFFIC = {"source_sha256_16": "307d950537d4b4f1", "workload": 2, "steps": 320,
-                  "warmup": 32, "bundle": 16, "workers": 0, "bytes_per_launch": 3989129455.2}
+                  "warmup": 32, "bundle": 32, "workers": 0, "bytes_per_launch": 7978287171.2}
 
 
 def measured_gather_traffic(args):
@@ -227,8 +227,8 @@ def main():
                          "5 gather-heavy academic")
     ap.add_argument("--workers", type=int, default=0,
                     help="pipeline worker threads (own streams); 0 = direct calls (default)")
-    ap.add_argument("--bundle", type=int, default=16,
-                    help="mini-batches per launch sequence (hg_sample_blocks_bundle, 1..16)")
+    ap.add_argument("--bundle", type=int, default=32,
+                    help="mini-batches per launch sequence (hg_sample_blocks_bundle, 1..32)")
     ap.add_argument("--depth", type=int, default=0,
                     help="mini-batches outstanding in the pipeline (default 2 x workers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -221,7 +221,7 @@ hg_status hg_sample_blocks_gather(hg_graph *graph, const int64_t *const *seeds,
                                   hipEvent_t start, hipEvent_t stop, hipStream_t stream,
                                   hg_blocks **out);
 
-/* n_batches (1..16) mini-batches in one launch sequence (Sec. 4.2.2: the
+/* n_batches (1..32) mini-batches in one launch sequence (Sec. 4.2.2: the
  * sampling of several mini-batches is bundled so that it runs in parallel).
  * Batch b has seeds seeds[b * n_ntypes + t] with counts n_seeds[b * n_ntypes
  * + t] (host arrays) and sampling seed rng_seeds[b]; all share n_hops and

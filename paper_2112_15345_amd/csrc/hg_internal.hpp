@@ -33,8 +33,8 @@ constexpr int kCandCap = 512;
 // Node types whose per-hop table entries travel inside a launch's arguments.
 constexpr int kInlineTypes = 8;
 // Node types whose source-list pointers the sampler launch stores into the
-// hop's table itself (a bundle of 16 mini-batches of 4 node types is 64).
-constexpr int kInlineSrcOut = 64;
+// hop's table itself (a bundle of 32 mini-batches of 4 node types is 128).
+constexpr int kInlineSrcOut = 128;
 
 // Pairs whose in-edges are all kept and number at most this many are copied
 // 64 pairs per wavefront; larger ones by a wavefront each.

@@ -204,7 +204,7 @@ void dev_free(hg_graph *g, void *p, hipStream_t s);
 void layout_types(hg_graph *g);
 void free_graph(hg_graph *g);
 // Mini-batches per bundle at most.
-constexpr int32_t kMaxBundle = 16;
+constexpr int32_t kMaxBundle = 32;
 }  // namespace
 
 // Output arrays of one sampling call; shared by the handles of a bundle and

@@ -92,7 +92,7 @@ def test_bundle_errors():
         g.sample_bundle([good, bad], [[1]], [0, 1], gather=[])
     assert e.value.status == hg.HG_EINVAL
     with pytest.raises(hg.HGError):
-        g.sample_bundle([good] * 17, [[1]], list(range(17)), gather=[])
+        g.sample_bundle([good] * 33, [[1]], list(range(33)), gather=[])
     # the graph (and its bundle workspaces) still work
     out = g.sample_bundle([good, good], [[1]], [0, 0], gather=[])
     assert not compare(result_dict(g, out[0]), result_dict(g, out[1]), 1, 1, 1)
