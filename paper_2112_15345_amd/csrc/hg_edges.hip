@@ -2,9 +2,9 @@
 // 2112.15345) lets its scheduler pick target edges as well as target vertices
 // (Sec. 4.2.1) and runs the same sampling decomposition from them (Sec.
 // 4.2.2).  The targets' endpoints become the seeds:
-//  1. k_edge_targets: per target edge its source (indices[eid]) and its
-//     destination (the vertex whose in-edge slots hold eid, by binary search
-//     over indptr), its negative destinations (Philox4x32-10 at counter
+//  1. k_edge_targets: a wavefront per target edge: its source (indices[eid])
+//     and its destination (the vertex whose in-edge slots hold eid, by a
+//     64-ary search over indptr), its negative destinations (one per lane) (Philox4x32-10 at counter
 //     (eid, 2^31 | k, etype), words 0 and 1 as u, destination
 //     floor(u * n / 2^64)), and its reverse edge under exclusion 2 (checked
 //     to run the other way).  Every endpoint sets its reached flag.
@@ -36,15 +36,21 @@ unsigned grid_for(int64_t n, int threads, int64_t cap = 1 << 16) {
 }
 
 // The destination of CSC slot eid: the largest v in [0, n_dst) with
-// indptr[v] <= eid (for 0 <= eid < indptr[n_dst]).
-__device__ int64_t edge_dst(const int64_t *indptr, int64_t n_dst, int64_t eid) {
-  int64_t a = 0, b = n_dst - 1;
-  while (a < b) {
-    const int64_t m = a + (b - a + 1) / 2;
-    if (indptr[m] <= eid)
-      a = m;
-    else
-      b = m - 1;
+// indptr[v] <= eid (for 0 <= eid < indptr[n_dst]).  Searched by a wavefront:
+// every lane probes one of 64 positions per round, so about log64(n_dst)
+// dependent loads instead of log2(n_dst).  All lanes take part and get the
+// result.
+__device__ int64_t wave_edge_dst(const int64_t *indptr, int64_t n_dst, int64_t eid) {
+  const int lane = lane_id();
+  int64_t a = 0, b = n_dst;  // indptr[a] <= eid; the answer is in [a, b)
+  while (b - a > 1) {
+    const int64_t step = (b - a + kWave - 1) / kWave;
+    const int64_t pos = a + int64_t(lane) * step;
+    // true on a prefix of the lanes (indptr never decreases), lane 0 always
+    const uint64_t bal = __ballot(pos < b && indptr[pos] <= eid);
+    const int last = 63 - __clzll((unsigned long long)bal);
+    a += int64_t(last) * step;
+    b = min(b, a + step);
   }
   return a;
 }
@@ -55,33 +61,40 @@ __device__ __forceinline__ void flag(int64_t *small, int32_t bits) {
   atomicOr(reinterpret_cast<int32_t *>(small + kSlotErr), bits);
 }
 
+// A wavefront per target (the target index is the same on all its lanes).
 __global__ __launch_bounds__(256) void k_edge_targets(EdgeBatchArgs A) {
-  for (int64_t x = gs_start(); x < A.n_targets; x += gs_step()) {
+  const int lane = lane_id();
+  const int64_t waves = int64_t(gridDim.x) * (blockDim.x / kWave);
+  for (int64_t x = gs_start() / kWave; x < A.n_targets; x += waves) {
     const int e = find_segment(A.tbase, A.n_etypes, x);
     const EdgeEtype &T = A.et[e];
     const EtypeStatic &E = A.es[e];
     const int64_t j = T.eids[x - A.tbase[e]];
-    A.tsrc[x] = -1;
-    A.tdst[x] = -1;
-    A.trev[x] = -1;
-    for (int k = 0; k < A.n_neg; ++k) A.tneg[x * A.n_neg + k] = -1;
+    if (lane == 0) {
+      A.tsrc[x] = -1;
+      A.tdst[x] = -1;
+      A.trev[x] = -1;
+    }
+    if (lane < A.n_neg) A.tneg[x * A.n_neg + lane] = -1;
     if (j < 0 || j >= T.nnz) {
-      flag(A.small, kErrTarget);
+      if (lane == 0) flag(A.small, kErrTarget);
       continue;
     }
     const int64_t u = E.indices[j];
-    const int64_t v = edge_dst(E.indptr, E.n_dst_nodes, j);
-    A.tsrc[x] = u;
-    A.tdst[x] = v;
-    mark(E.src_reached, u);
-    mark(A.ts[E.dst_type].reached, v);
-    for (int k = 0; k < A.n_neg; ++k) {
-      const U32x4 r = philox4x32_10(
-          U32x4{uint32_t(j), uint32_t(uint64_t(j) >> 32), 0x80000000u | uint32_t(k), uint32_t(e)},
-          uint32_t(A.sigma), uint32_t(A.sigma >> 32));
+    const int64_t v = wave_edge_dst(E.indptr, E.n_dst_nodes, j);
+    if (lane == 0) {
+      A.tsrc[x] = u;
+      A.tdst[x] = v;
+      mark(E.src_reached, u);
+      mark(A.ts[E.dst_type].reached, v);
+    }
+    if (lane < A.n_neg) {  // negative k = lane
+      const U32x4 r = philox4x32_10(U32x4{uint32_t(j), uint32_t(uint64_t(j) >> 32),
+                                          0x80000000u | uint32_t(lane), uint32_t(e)},
+                                    uint32_t(A.sigma), uint32_t(A.sigma >> 32));
       const uint64_t w = uint64_t(r.x) | (uint64_t(r.y) << 32);
       const int64_t nv = int64_t(__umul64hi(w, uint64_t(E.n_dst_nodes)));
-      A.tneg[x * A.n_neg + k] = nv;
+      A.tneg[x * A.n_neg + lane] = nv;
       mark(A.ts[E.dst_type].reached, nv);
     }
     if (A.exclude == 2 && T.rev >= 0) {
@@ -90,11 +103,11 @@ __global__ __launch_bounds__(256) void k_edge_targets(EdgeBatchArgs A) {
       const EdgeEtype &RT = A.et[T.rev];
       const EtypeStatic &RE = A.es[T.rev];
       if (rj < 0 || rj >= RT.nnz || RE.indices[rj] != v ||
-          edge_dst(RE.indptr, RE.n_dst_nodes, rj) != u) {
-        flag(A.small, kErrTarget);
+          wave_edge_dst(RE.indptr, RE.n_dst_nodes, rj) != u) {
+        if (lane == 0) flag(A.small, kErrTarget);
         continue;
       }
-      A.trev[x] = rj;
+      if (lane == 0) A.trev[x] = rj;
     }
   }
 }
@@ -169,7 +182,9 @@ __global__ __launch_bounds__(256) void k_edge_relabel(EdgeBatchArgs A, HopView f
 
 hipError_t launch_edge_targets(const EdgeBatchArgs &A, hipStream_t stream) {
   if (A.n_targets <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_edge_targets, dim3(grid_for(A.n_targets, 256)), dim3(256), 0, stream, A);
+  // a wavefront per target
+  hipLaunchKernelGGL(k_edge_targets, dim3(grid_for(A.n_targets * kWave, 256)), dim3(256), 0, stream,
+                     A);
   return hipGetLastError();
 }
 
