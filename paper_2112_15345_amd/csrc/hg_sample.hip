@@ -753,15 +753,39 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   return H;
 }
 
+// A wavefront's candidates for its current hub wait in LDS (kHubBuf
+// entries) and go to the hub's global list in one piece, with one atomic
+// for their positions, when the wavefront moves to the next hub, when the
+// buffer is full, and at the end: one round trip per (wavefront, hub) instead
+// of one per step that finds candidates.
+constexpr int kHubBuf = kCandCap;  // uint64 entries: a wavefront's two candidate arrays
+struct HubBuf {
+  uint64_t *e;  // LDS
+  int n;        // entries held (the same on every lane)
+};
+
+__device__ void hub_flush(const SampleArgs &A, int64_t hub, HubBuf &B) {
+  if (B.n == 0) return;
+  wave_sync();
+  int base = 0;
+  if (lane_id() == 0) base = atomicAdd(A.pa.hub_cnt + hub, B.n);
+  base = __shfl(base, 0, kWave);
+  uint64_t *list = A.cand + hub * kCandCap;
+  for (int i = lane_id(); i < B.n; i += kWave)
+    if (base + i < kCandCap) list[base + i] = B.e[i];
+  wave_sync();
+  B.n = 0;
+}
+
 // One wavefront step over the 64 key groups gb .. gb+63 of a hub chunk
-// [c_lo, c_hi): appends the edges with key <= lim to the hub's list.
+// [c_lo, c_hi): appends the edges with key <= lim to the hub's candidates.
 // kChecked: some lanes' edges may lie outside the chunk.  Otherwise the step
 // first asks whether any key of the wavefront is small enough at all, which
 // is rarely the case.
 template <bool kChecked>
 __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H,
                                          uint64_t gb, int64_t c_lo, int64_t c_hi,
-                                         uint32_t lim, uint32_t shift) {
+                                         uint32_t lim, uint32_t shift, HubBuf &B) {
   const int lane = lane_id();
   const uint64_t g = gb + lane;
   const U32x4 r = philox4x32_10(
@@ -788,19 +812,16 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
   }
   int tot;
   const int pre = wave_prefix_small(__popc(mask), &tot);
-  int base = 0;
-  if (lane == 0) base = atomicAdd(A.pa.hub_cnt + H.hub, tot);
-  base = __shfl(base, 0, kWave);
-  int pos = base + pre;
-  uint64_t *list = A.cand + H.hub * kCandCap;
+  if (B.n + tot > kHubBuf) hub_flush(A, H.hub, B);  // tot <= 256 < kHubBuf
+  int pos = B.n + pre;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     if (mask & (1 << q)) {
-      if (pos < kCandCap)
-        list[pos] = (uint64_t(word_of(r, q) >> shift) << 32) | (4 * g + q - uint64_t(H.lo));
+      B.e[pos] = (uint64_t(word_of(r, q) >> shift) << 32) | (4 * g + q - uint64_t(H.lo));
       ++pos;
     }
   }
+  B.n += tot;
 }
 
 // The last hub whose first chunk is not above chunk c (hub_choff strictly
@@ -823,13 +844,17 @@ __device__ int64_t find_hub(const SampleArgs &A, int64_t c) {
   return lo;
 }
 
-__device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
+__device__ void role_hub_chunks(const SampleArgs &A, int64_t w, uint64_t *buf) {
   const int64_t c_first = w * A.chunks_per_wave;
   const int64_t c_end = min(c_first + A.chunks_per_wave, A.n_chunks);
   HubParams H = hub_params(A, find_hub(A, c_first));
   const uint32_t shift = uint32_t(32 - A.key_bits);
+  HubBuf B{buf, 0};
   for (int64_t chunk = c_first; chunk < c_end; ++chunk) {
-    while (chunk >= H.end_chunk) H = hub_params(A, H.hub + 1);
+    while (chunk >= H.end_chunk) {
+      hub_flush(A, H.hub, B);
+      H = hub_params(A, H.hub + 1);
+    }
     // (key >> shift) < tau  <=>  key < tau << shift  <=>  key <= lim
     const uint64_t tau_raw = H.tau << shift;
     const uint32_t lim = tau_raw - 1 >= 0xFFFFFFFFull ? 0xFFFFFFFFu : uint32_t(tau_raw - 1);
@@ -850,12 +875,13 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w) {
     if (k_hi > n_it) k_hi = n_it;
     if (k_hi < k_lo) k_hi = k_lo;
     for (int64_t k = 0; k < k_lo; ++k)
-      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift);
+      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, B);
     for (int64_t k = k_lo; k < k_hi; ++k)
-      hub_step<false>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift);
+      hub_step<false>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, B);
     for (int64_t k = k_hi; k < n_it; ++k)
-      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift);
+      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, B);
   }
+  hub_flush(A, H.hub, B);
 }
 
 // A wavefront per hub: the K smallest (key, j) of the hub's candidate list,
@@ -937,7 +963,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
     role_pair_groups(A, *g, b * kSampleWaves + wave, b == 0);
   } else if (b < A.blocks_a + A.blocks_c) {
     const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
-    if (w * A.chunks_per_wave < A.n_chunks) role_hub_chunks(A, w);
+    if (w * A.chunks_per_wave < A.n_chunks)
+      role_hub_chunks(A, w, reinterpret_cast<uint64_t *>(&s_cand[wave][0][0]));
   } else {
     const int64_t w = (b - A.blocks_a - A.blocks_c) * kSampleWaves + wave;
     if (w * kWavePairs < A.n_wave) role_wave_pairs(A, s_cand[wave][0], s_cand[wave][1], w);
