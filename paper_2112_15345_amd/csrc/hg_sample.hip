@@ -722,7 +722,7 @@ __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
 // The hub of the first chunk is found by a wavefront-wide search (the last
 // hub whose first chunk is not above it); later chunks walk on from there, so
 // the search and the hub's parameters are loaded once per run of chunks.
-constexpr int64_t kHubWaves = 65536;
+constexpr int64_t kHubWaves = 16384;
 constexpr int64_t kMaxChunksPerWave = 16;
 
 struct HubParams {
