@@ -90,7 +90,8 @@ def link_main(args, wl, gen, g):
     """Edge-seeded (link-prediction) mini-batches: targets of one forward
     relation, their endpoints as seeds, one negative per target, targets and
     their reverse edges excluded, the paper's link-prediction fanouts [25, 15]
-    per hop, every featured type gathered.  One direct call per step."""
+    per hop, every featured type gathered.  Bundles of --bundle mini-batches
+    per call (hg_sample_edge_blocks_bundle), direct calls on one stream."""
     import torch
 
     import paper_2112_15345_amd as hg
@@ -107,23 +108,27 @@ def link_main(args, wl, gen, g):
     targets = [[None if x is None else torch.as_tensor(x, device=dev)
                 for x in W.link_targets(gen, b, link_et)] for b in range(n_batches)]
 
-    def step(b):
-        return g.sample_edge_blocks(targets[b], fan, b, n_neg=W.LINK_NEG, exclude=exclude,
-                                    rev_etype=rev_et, rev_eid=rev_eid, gather=feat_types)
+    B = max(1, args.bundle)
 
-    for b in range(args.warmup):
-        step(b)
+    def unit(first, last):
+        return g.sample_edge_bundle([targets[b] for b in range(first, last)], fan,
+                                    list(range(first, last)), n_neg=W.LINK_NEG,
+                                    exclude=exclude, rev_etype=rev_et, rev_eid=rev_eid,
+                                    gather=feat_types)
+
+    for b in range(0, args.warmup, B):
+        unit(b, min(b + B, args.warmup))
     torch.cuda.synchronize()
     edges = rows = gbytes = 0
     t_start = time.perf_counter()
-    for b in range(args.warmup, n_batches):
-        blocks = step(b)
-        edges += blocks.total_edges()
-        for t in feat_types:
-            n = blocks.num_input_nodes(t)
-            rows += n
-            gbytes += n * row_bytes[t]
-        del blocks
+    for b0 in range(args.warmup, n_batches, B):
+        for blocks in unit(b0, min(b0 + B, n_batches)):
+            edges += blocks.total_edges()
+            for t in feat_types:
+                n = blocks.num_input_nodes(t)
+                rows += n
+                gbytes += n * row_bytes[t]
+            del blocks
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     result = {
@@ -137,7 +142,8 @@ def link_main(args, wl, gen, g):
                                f"'{gen.etype_names[link_et]}', {W.LINK_NEG} negative each, "
                                f"exclusion {exclude}, fanout {list(W.LINK_FANOUTS)}",
                    "workload_index": args.workload, "task": "link",
-                   "parallelism": "single GPU", "pipeline": "direct calls"},
+                   "parallelism": "single GPU", "pipeline": "direct calls",
+                   "bundle": max(1, args.bundle)},
         "gathered_GBps": gbytes / elapsed / 1e9,
         "sampled_edges_per_step": edges / args.steps,
         "gathered_rows_per_step": rows / args.steps,

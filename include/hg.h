@@ -341,6 +341,19 @@ hg_status hg_sample_edge_blocks(hg_graph *graph, const hg_edge_batch *batch, int
                                 const int32_t *gather_ntypes, int32_t n_gather,
                                 hipStream_t stream, hg_blocks **out);
 
+/* n_batches (1..32) edge-seeded mini-batches in one launch sequence, as
+ * hg_sample_blocks_bundle does for vertex seeds: batch b is batches[b] with
+ * seed rng_seeds[b] (host uint64 [n_batches]) and comes back in out[b], each
+ * the mini-batch its own hg_sample_edge_blocks call would make.  All batches
+ * share n_hops, fanouts, gather_ntypes and the batches' n_neg and exclude;
+ * their target and reverse arrays may differ.  On failure no handle is
+ * returned. */
+hg_status hg_sample_edge_blocks_bundle(hg_graph *graph, int32_t n_batches,
+                                       const hg_edge_batch *batches, int32_t n_hops,
+                                       const int32_t *fanouts, const uint64_t *rng_seeds,
+                                       const int32_t *gather_ntypes, int32_t n_gather,
+                                       hipStream_t stream, hg_blocks **out);
+
 /* The seeds of node type `ntype` (device int64 [n], owned by the handle): for
  * an edge-seeded batch its endpoints in ascending ID; otherwise the hop-0
  * frontier (the given seeds). */

@@ -40,6 +40,7 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
                "hg_pipeline_destroy", "hg_sample_edge_blocks", "hg_blocks_seeds",
                "hg_blocks_edge_pairs", "hg_sample_layers", "hg_blocks_edge_counts",
+               "hg_sample_edge_blocks_bundle",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 HG_MAX_NEG = 64
@@ -116,6 +117,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_edge_pairs": ([_P, _I32, _PI64, _PP, _PP, _PI64, _PP], _I32),
         "hg_sample_layers": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
         "hg_blocks_edge_counts": ([_P, _P], _I32),
+        "hg_sample_edge_blocks_bundle": ([_P, _I32, _P, _I32, _P, _P, _P, _I32, _P, _P], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -455,19 +457,11 @@ class Graph:
         _check(st)
         return Blocks(self, h, H)
 
-    def sample_edge_blocks(self, targets, fanouts, rng_seed: int = 0, n_neg: int = 0,
-                           exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None,
-                           gather=None, stream=None) -> Blocks:
-        """An edge-seeded mini-batch (link prediction): targets per edge type an
-        int64 device tensor of edge IDs or None; n_neg negatives per target;
-        exclude HG_EXCLUDE_NONE / _SELF / _REVERSE, the last with rev_etype
-        (per edge type its reverse type or -1) and rev_eid (per edge type an
-        int64 device tensor [nnz] or None).  gather as in sample_blocks."""
-        lib = load_library()
-        T, R = self.T, self.R
+    def _edge_batch(self, targets, n_neg, exclude, rev_etype, rev_eid, keep):
+        """An EdgeBatch over ctypes arrays that `keep` holds alive."""
+        R = self.R
         if len(targets) != R:
             raise ValueError("one target entry per edge type")
-        keep = []
         tptr = (ctypes.c_void_p * max(R, 1))()
         tcnt = (ctypes.c_int64 * max(R, 1))()
         for e, x in enumerate(targets):
@@ -489,19 +483,36 @@ class Graph:
                 x = _dev_i64(x, self.device)
                 keep.append(x)
                 rptr[e] = x.data_ptr() if x.numel() else None
-        batch = EdgeBatch(ctypes.addressof(tptr), ctypes.addressof(tcnt), int(n_neg),
-                          int(exclude), ctypes.addressof(rv) if rv is not None else None,
-                          ctypes.addressof(rptr) if rptr is not None else None)
+        keep.extend([tptr, tcnt, rv, rptr])
+        return EdgeBatch(ctypes.addressof(tptr), ctypes.addressof(tcnt), int(n_neg),
+                         int(exclude), ctypes.addressof(rv) if rv is not None else None,
+                         ctypes.addressof(rptr) if rptr is not None else None)
+
+    def _gather_list(self, gather):
+        if isinstance(gather, str):
+            if gather != "all":
+                raise ValueError('gather must be None, "all" or a list of node types')
+            gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
+        return list(gather or [])
+
+    def sample_edge_blocks(self, targets, fanouts, rng_seed: int = 0, n_neg: int = 0,
+                           exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None,
+                           gather=None, stream=None) -> Blocks:
+        """An edge-seeded mini-batch (link prediction): targets per edge type an
+        int64 device tensor of edge IDs or None; n_neg negatives per target;
+        exclude HG_EXCLUDE_NONE / _SELF / _REVERSE, the last with rev_etype
+        (per edge type its reverse type or -1) and rev_eid (per edge type an
+        int64 device tensor [nnz] or None).  gather as in sample_blocks."""
+        lib = load_library()
+        R = self.R
+        keep = []
+        batch = self._edge_batch(targets, n_neg, exclude, rev_etype, rev_eid, keep)
         H = len(fanouts)
         flat = [int(k) for row in fanouts for k in row]
         if len(flat) != H * R:
             raise ValueError("fanouts must be [n_hops][n_etypes]")
         fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
-        if isinstance(gather, str):
-            if gather != "all":
-                raise ValueError('gather must be None, "all" or a list of node types')
-            gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
-        gather = list(gather or [])
+        gather = self._gather_list(gather)
         gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
         h = ctypes.c_void_p()
         st = lib.hg_sample_edge_blocks(self._h, ctypes.addressof(batch), H, fo,
@@ -512,6 +523,37 @@ class Graph:
         del keep
         _check(st)
         return Blocks(self, h, H)
+
+    def sample_edge_bundle(self, targets_list, fanouts, rng_seeds, n_neg: int = 0,
+                           exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None,
+                           gather=None, stream=None):
+        """Several edge-seeded mini-batches in one launch sequence
+        (hg_sample_edge_blocks_bundle): targets_list[b] per edge type as in
+        sample_edge_blocks, rng_seeds[b]; the same n_neg, exclusion and reverse
+        maps for all.  Returns one Blocks per batch."""
+        lib = load_library()
+        R = self.R
+        B = len(targets_list)
+        if len(rng_seeds) != B:
+            raise ValueError("one rng seed per batch")
+        keep = []
+        batches = (EdgeBatch * max(B, 1))()
+        for b, targets in enumerate(targets_list):
+            batches[b] = self._edge_batch(targets, n_neg, exclude, rev_etype, rev_eid, keep)
+        H = len(fanouts)
+        flat = [int(k) for row in fanouts for k in row]
+        if len(flat) != H * R:
+            raise ValueError("fanouts must be [n_hops][n_etypes]")
+        fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        sg = (ctypes.c_uint64 * max(B, 1))(*[int(s) & (2**64 - 1) for s in rng_seeds])
+        gather = self._gather_list(gather)
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
+        hs = (ctypes.c_void_p * max(B, 1))()
+        st = lib.hg_sample_edge_blocks_bundle(self._h, B, batches, H, fo, sg, gt, len(gather),
+                                              _stream(stream), hs)
+        del keep
+        _check(st)
+        return [Blocks(self, ctypes.c_void_p(hs[b]), H) for b in range(B)]
 
     def gather_features(self, blocks: Blocks, ntype: int, out: torch.Tensor | None = None,
                         stream=None) -> torch.Tensor:

@@ -89,9 +89,11 @@ __global__ __launch_bounds__(256) void k_edge_targets(EdgeBatchArgs A) {
       mark(A.ts[E.dst_type].reached, v);
     }
     if (lane < A.n_neg) {  // negative k = lane
+      const int copy = e / A.key_R;
+      const uint64_t sigma = A.sigmas[copy];
       const U32x4 r = philox4x32_10(U32x4{uint32_t(j), uint32_t(uint64_t(j) >> 32),
-                                          0x80000000u | uint32_t(lane), uint32_t(e)},
-                                    uint32_t(A.sigma), uint32_t(A.sigma >> 32));
+                                          0x80000000u | uint32_t(lane), uint32_t(e - copy * A.key_R)},
+                                    uint32_t(sigma), uint32_t(sigma >> 32));
       const uint64_t w = uint64_t(r.x) | (uint64_t(r.y) << 32);
       const int64_t nv = int64_t(__umul64hi(w, uint64_t(E.n_dst_nodes)));
       A.tneg[x * A.n_neg + lane] = nv;

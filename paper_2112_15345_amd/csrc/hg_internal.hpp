@@ -347,7 +347,10 @@ struct EdgeBatchArgs {
   int32_t n_etypes, n_types;
   int64_t n_targets;
   int32_t n_neg, exclude;
-  uint64_t sigma;
+  // edge type e belongs to copy e / key_R of a bundle (a single batch: key_R
+  // = n_etypes), keyed as type e % key_R with seed sigmas[e / key_R] (device)
+  const uint64_t *sigmas;
+  int32_t key_R;
   int64_t *tsrc, *tdst;    // [n_targets] endpoints (-1 for an invalid target)
   int64_t *tneg;           // [n_targets * n_neg]
   int64_t *trev;           // [n_targets] reverse edge ID (exclusion 2), -1 when none

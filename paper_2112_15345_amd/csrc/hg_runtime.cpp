@@ -870,7 +870,8 @@ hg_status SampleRun::run_edges() {
   A.n_targets = N;
   A.n_neg = Q;
   A.exclude = eb->exclude;
-  A.sigma = sigmas[0];
+  A.sigmas = dsigmas();
+  A.key_R = g->key_R > 0 ? g->key_R : std::max(R, 1);
   A.pos_src = pos_src;
   A.pos_dst = pos_dst;
   A.neg_dst = neg_dst;
@@ -1620,10 +1621,11 @@ hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *
 
 // An edge-seeded mini-batch (checked), then the gather.
 hg_status run_edge_sampling(hg_graph *g, const hg_edge_batch *eb, int32_t n_hops,
-                            const int32_t *fanouts, uint64_t rng_seed, const int32_t *gtypes,
-                            int32_t n_gather, hipStream_t stream, hg_blocks **out) {
+                            const int32_t *fanouts, const uint64_t *sigmas, int32_t n_sig,
+                            const int32_t *gtypes, int32_t n_gather, hipStream_t stream,
+                            hg_blocks **out) {
   DeviceGuard dg(g->device);
-  SampleRun run(g, stream, n_hops, fanouts, &rng_seed, 1, 32);
+  SampleRun run(g, stream, n_hops, fanouts, sigmas, n_sig, 32);
   run.gtypes = gtypes;
   run.n_gather = n_gather;
   run.eb = eb;
@@ -1831,6 +1833,21 @@ hg_blocks *split_blocks(hg_graph *g, const hg_blocks *v, int32_t b) {
     o->in_gid.push_back(v->in_gid[size_t(b) * T + t]);
     o->feat.push_back(v->feat[size_t(b) * T + t]);
   }
+  if (v->edge_seeded) {
+    o->edge_seeded = true;
+    o->n_neg = v->n_neg;
+    for (int32_t t = 0; t < T; ++t) {
+      o->seed_n.push_back(v->seed_n[size_t(b) * T + t]);
+      o->seed_gid.push_back(v->seed_gid[size_t(b) * T + t]);
+    }
+    for (int32_t e = 0; e < R; ++e) {
+      const size_t kv = size_t(b) * R + e;
+      o->pair_n.push_back(v->pair_n[kv]);
+      o->pos_src.push_back(v->pos_src[kv]);
+      o->pos_dst.push_back(v->pos_dst[kv]);
+      o->neg_dst.push_back(v->neg_dst[kv]);
+    }
+  }
   o->mem = v->mem;
   return o;
 }
@@ -1928,8 +1945,8 @@ hg_status hg_sample_edge_blocks(hg_graph *g, const hg_edge_batch *batch, int32_t
   if (st != HG_OK) return st;
   st = check_edge_batch(g, batch);
   if (st != HG_OK) return st;
-  return run_edge_sampling(g, batch, n_hops, fanouts, rng_seed, gather_ntypes, n_gather, stream,
-                           out);
+  return run_edge_sampling(g, batch, n_hops, fanouts, &rng_seed, 1, gather_ntypes, n_gather,
+                           stream, out);
 }
 
 hg_status hg_sample_layers(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
@@ -1952,6 +1969,80 @@ hg_status hg_sample_layers(hg_graph *g, const int64_t *const *seeds, const int64
   if (st != HG_OK) return st;
   return run_layer_sampling(g, seeds, n_seeds, n_hops, layer_sizes, rng_seed, gather_ntypes,
                             n_gather, stream, out);
+}
+
+hg_status hg_sample_edge_blocks_bundle(hg_graph *g, int32_t n_batches,
+                                       const hg_edge_batch *batches, int32_t n_hops,
+                                       const int32_t *fanouts, const uint64_t *rng_seeds,
+                                       const int32_t *gather_ntypes, int32_t n_gather,
+                                       hipStream_t stream, hg_blocks **out) {
+  if (!out) return fail(HG_EINVAL, "hg_sample_edge_blocks_bundle: out is NULL");
+  clear_pending_error();
+  if (!g) return fail(HG_EINVAL, "hg_sample_edge_blocks_bundle: graph is NULL");
+  if (n_batches < 1 || n_batches > kMaxBundle)
+    return fail(HG_EINVAL, "hg_sample_edge_blocks_bundle: n_batches not in 1..%d", kMaxBundle);
+  for (int32_t b = 0; b < n_batches; ++b) out[b] = nullptr;
+  if (!batches || !rng_seeds) return fail(HG_EINVAL, "hg_sample_edge_blocks_bundle: NULL array");
+  const int32_t T = g->T, R = g->R;
+  std::vector<int64_t> zero(T, 0);
+  hg_status st = check_batch(g, nullptr, zero.data(), n_hops, fanouts, 32, gather_ntypes, n_gather);
+  if (st != HG_OK) return st;
+  for (int32_t b = 0; b < n_batches; ++b) {
+    if ((st = check_edge_batch(g, &batches[b])) != HG_OK) return st;
+    if (batches[b].n_neg != batches[0].n_neg || batches[b].exclude != batches[0].exclude)
+      return fail(HG_EINVAL, "hg_sample_edge_blocks_bundle: batches differ in n_neg or exclude");
+  }
+  if (n_batches == 1)
+    return run_edge_sampling(g, &batches[0], n_hops, fanouts, rng_seeds, 1, gather_ntypes,
+                             n_gather, stream, out);
+  hg_graph *v = nullptr;
+  if ((st = bundle_graph(g, n_batches, &v)) != HG_OK) return st;
+  // the batches as one batch of the virtual graph: copy b's edge type e is b * R + e
+  const int32_t X = batches[0].exclude;
+  const size_t VR = size_t(n_batches) * R;
+  std::vector<const int64_t *> eids(VR, nullptr), rev_eid(VR, nullptr);
+  std::vector<int64_t> n_eids(VR, 0);
+  std::vector<int32_t> rev_et(VR, -1);
+  for (int32_t b = 0; b < n_batches; ++b)
+    for (int32_t e = 0; e < R; ++e) {
+      const hg_edge_batch &B = batches[b];
+      const size_t k = size_t(b) * R + e;
+      n_eids[k] = B.n_eids[e];
+      eids[k] = B.n_eids[e] > 0 ? B.eids[e] : nullptr;
+      if (X == HG_EXCLUDE_REVERSE && B.rev_etype[e] >= 0) {
+        rev_et[k] = b * R + B.rev_etype[e];
+        rev_eid[k] = B.rev_eid[e];
+      }
+    }
+  const hg_edge_batch vb{eids.data(), n_eids.data(), batches[0].n_neg, X,
+                         X == HG_EXCLUDE_REVERSE ? rev_et.data() : nullptr,
+                         X == HG_EXCLUDE_REVERSE ? rev_eid.data() : nullptr};
+  std::vector<int32_t> vfan(size_t(n_hops) * VR);
+  for (int32_t h = 0; h < n_hops; ++h)
+    for (int32_t b = 0; b < n_batches; ++b)
+      for (int32_t e = 0; e < R; ++e)
+        vfan[size_t(h) * VR + size_t(b) * R + e] = fanouts[size_t(h) * R + e];
+  std::vector<int32_t> vg;
+  for (int32_t b = 0; b < n_batches; ++b)
+    for (int32_t k = 0; k < n_gather; ++k) vg.push_back(b * T + gather_ntypes[k]);
+  hg_blocks *vbk = nullptr;
+  st = run_edge_sampling(v, &vb, n_hops, vfan.empty() ? nullptr : vfan.data(), rng_seeds,
+                         n_batches, vg.empty() ? nullptr : vg.data(), int32_t(vg.size()), stream,
+                         &vbk);
+  if (st != HG_OK) return st;
+  for (int32_t b = 0; b < n_batches; ++b) {
+    out[b] = split_blocks(g, vbk, b);
+    if (!out[b]) {
+      for (int32_t c = 0; c < b; ++c) {
+        delete out[c];
+        out[c] = nullptr;
+      }
+      delete vbk;
+      return fail(HG_ENOMEM, "hg_sample_edge_blocks_bundle: out of host memory");
+    }
+  }
+  delete vbk;  // the split handles keep the arrays
+  return HG_OK;
 }
 
 hg_status hg_blocks_seeds(const hg_blocks *b, int32_t ntype, int64_t *n, const int64_t **gid) {

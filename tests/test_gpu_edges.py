@@ -170,3 +170,59 @@ def test_edge_workload_academic(olib):
             assert b.features(t).cpu().numpy().tobytes() == want.tobytes(), f"type {t}"
         say(f"academic link batch {bno}: equal "
             f"({sum(v[3].size for v in ref['edges'].values())} sampled edges)")
+
+
+def edge_feats(g, b):
+    return {t: b.features(t).cpu().numpy().tobytes() for t, (_, f) in enumerate(g.ntypes)
+            if f is not None}
+
+
+@pytest.mark.parametrize("chunk", range(2))
+def test_edge_bundles_equal_single_calls(olib, chunk):
+    """Every batch of an edge-seeded bundle is the batch its own call makes
+    (seeds, pair graphs, blocks, gathered bytes), and the oracle's."""
+    rng = np.random.default_rng(9100 + chunk)
+    for c in range(12):
+        case = pins.random_edge_case(rng, max_nodes=60, max_deg=40)
+        nn, ets, feats, tg, q, x, rev_et, rev_eid, fanouts, sigma, bits = case
+        g = gpu_graph(nn, ets, feats)
+        B = [2, 3, 7][c % 3]
+        # other target lists for the other batches: the same edge types, new picks
+        tgs = [tg]
+        for b in range(1, B):
+            tgs.append([None if t is None else
+                        rng.integers(0, max(int(e[3].size), 1), size=t.size).astype(np.int64)
+                        if e[3].size else t for t, e in zip(tg, ets)])
+        sigmas = [sigma + 17 * b for b in range(B)]
+        say(f"edge bundle chunk {chunk} case {c}: B={B} R={len(ets)} neg={q} exclude={x}")
+        bl = g.sample_edge_bundle([dev(t) for t in tgs], fanouts, sigmas, n_neg=q, exclude=x,
+                                  rev_etype=rev_et, rev_eid=dev(rev_eid), gather="all")
+        assert len(bl) == B
+        host = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib)
+        for b in range(B):
+            single = g.sample_edge_blocks(dev(tgs[b]), fanouts, sigmas[b], n_neg=q, exclude=x,
+                                          rev_etype=rev_et, rev_eid=dev(rev_eid), gather="all")
+            got = edge_result_dict(g, bl[b])
+            diffs = compare_edges(edge_result_dict(g, single), got, len(nn), len(ets),
+                                  len(fanouts))
+            assert not diffs, f"case {c} batch {b}: " + "\n".join(diffs[:10])
+            assert edge_feats(g, bl[b]) == edge_feats(g, single)
+            if b == B - 1:
+                ref = host.sample_edge_blocks(tgs[b], fanouts, sigmas[b], n_neg=q, exclude=x,
+                                              rev_etype=rev_et, rev_eid=rev_eid)
+                diffs = compare_edges(ref, got, len(nn), len(ets), len(fanouts))
+                assert not diffs, f"case {c} batch {b} vs oracle: " + "\n".join(diffs[:10])
+
+
+def test_edge_bundle_errors(olib):
+    nn, ets, feats, rev_et, rev_eid = hub_with_reverse(100)
+    g = gpu_graph(nn, ets, feats)
+    good = [torch.tensor([1, 2], device="cuda"), None]
+    bad = [torch.tensor([10_000], device="cuda"), None]
+    with pytest.raises(hg.HGError):
+        g.sample_edge_bundle([good, bad], [[3, 3]], [0, 1])
+    with pytest.raises(hg.HGError):
+        g.sample_edge_bundle([good] * 33, [[3, 3]], list(range(33)))
+    out = g.sample_edge_bundle([good, good], [[3, 3]], [5, 5], n_neg=2)
+    a, b = edge_result_dict(g, out[0]), edge_result_dict(g, out[1])
+    assert not compare_edges(a, b, 1, 2, 1)
