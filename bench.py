@@ -153,8 +153,9 @@ def link_main(args, wl, gen, g):
 
 def layers_main(args, wl, gen, g):
     """Layer-wise (LADIES) mini-batches: the workload's seeds, 512 draws per
-    node type in each of two hops, every featured type gathered.  One direct
-    call per step."""
+    node type in each of two hops, every featured type gathered.  Bundles of
+    --bundle mini-batches per call (hg_sample_layers_bundle), direct calls on
+    one stream."""
     import torch
 
     import workloads as W
@@ -167,22 +168,25 @@ def layers_main(args, wl, gen, g):
     seeds = [[None if s is None else torch.as_tensor(s, device=dev)
               for s in W.seeds_per_type(wl, b)] for b in range(n_batches)]
 
-    def step(b):
-        return g.sample_layers(seeds[b], sizes, b, gather=feat_types)
+    B = max(1, args.bundle)
 
-    for b in range(args.warmup):
-        step(b)
+    def unit(first, last):
+        return g.sample_layers_bundle([seeds[b] for b in range(first, last)], sizes,
+                                      list(range(first, last)), gather=feat_types)
+
+    for b in range(0, args.warmup, B):
+        unit(b, min(b + B, args.warmup))
     torch.cuda.synchronize()
     edges = rows = gbytes = 0
     t_start = time.perf_counter()
-    for b in range(args.warmup, n_batches):
-        blocks = step(b)
-        edges += blocks.total_edges()
-        for t in feat_types:
-            n = blocks.num_input_nodes(t)
-            rows += n
-            gbytes += n * row_bytes[t]
-        del blocks
+    for b0 in range(args.warmup, n_batches, B):
+        for blocks in unit(b0, min(b0 + B, n_batches)):
+            edges += blocks.total_edges()
+            for t in feat_types:
+                n = blocks.num_input_nodes(t)
+                rows += n
+                gbytes += n * row_bytes[t]
+            del blocks
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     result = {
@@ -195,7 +199,8 @@ def layers_main(args, wl, gen, g):
         "config": {"workload": wl.name + f"; layer-wise (LADIES): {list(W.LAYER_SIZES)} draws "
                                f"per node type per hop",
                    "workload_index": args.workload, "task": "layers",
-                   "parallelism": "single GPU", "pipeline": "direct calls"},
+                   "parallelism": "single GPU", "pipeline": "direct calls",
+                   "bundle": max(1, args.bundle)},
         "gathered_GBps": gbytes / elapsed / 1e9,
         "kept_edges_per_step": edges / args.steps,
         "gathered_rows_per_step": rows / args.steps,

@@ -393,12 +393,22 @@ hg_status hg_blocks_edge_pairs(const hg_blocks *blocks, int32_t etype, int64_t *
  *    hg_sample_blocks.
  * Seeds and the output handle are as for hg_sample_blocks (gather_ntypes as
  * in hg_sample_blocks_gather).  layer_sizes: host int32 [n_hops * n_ntypes],
- * each >= -1.  HG_EUNSUPPORTED for a graph of more than 8 node types;
- * otherwise errors as hg_sample_blocks. */
+ * each >= -1.  Errors as hg_sample_blocks. */
 hg_status hg_sample_layers(hg_graph *graph, const int64_t *const *seeds, const int64_t *n_seeds,
                            int32_t n_hops, const int32_t *layer_sizes, uint64_t rng_seed,
                            const int32_t *gather_ntypes, int32_t n_gather, hipStream_t stream,
                            hg_blocks **out);
+
+/* n_batches (1..32) layer-wise mini-batches in one launch sequence: batch b
+ * takes seeds[b * n_ntypes + t] / n_seeds[b * n_ntypes + t] and seed
+ * rng_seeds[b], shares n_hops and layer_sizes, and comes back in out[b] as
+ * its own hg_sample_layers call would make it.  On failure no handle is
+ * returned. */
+hg_status hg_sample_layers_bundle(hg_graph *graph, int32_t n_batches,
+                                  const int64_t *const *seeds, const int64_t *n_seeds,
+                                  int32_t n_hops, const int32_t *layer_sizes,
+                                  const uint64_t *rng_seeds, const int32_t *gather_ntypes,
+                                  int32_t n_gather, hipStream_t stream, hg_blocks **out);
 
 /* Thread-local description of the last failure on this thread. */
 const char *hg_last_error(void);

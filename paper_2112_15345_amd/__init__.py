@@ -40,7 +40,7 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_pipeline_create", "hg_pipeline_submit", "hg_pipeline_next",
                "hg_pipeline_destroy", "hg_sample_edge_blocks", "hg_blocks_seeds",
                "hg_blocks_edge_pairs", "hg_sample_layers", "hg_blocks_edge_counts",
-               "hg_sample_edge_blocks_bundle",
+               "hg_sample_edge_blocks_bundle", "hg_sample_layers_bundle",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 HG_MAX_NEG = 64
@@ -118,6 +118,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_sample_layers": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
         "hg_blocks_edge_counts": ([_P, _P], _I32),
         "hg_sample_edge_blocks_bundle": ([_P, _I32, _P, _I32, _P, _P, _P, _I32, _P, _P], _I32),
+        "hg_sample_layers_bundle": ([_P, _I32, _P, _P, _I32, _P, _P, _P, _I32, _P, _P], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -494,6 +495,45 @@ class Graph:
                 raise ValueError('gather must be None, "all" or a list of node types')
             gather = [t for t, (_, f) in enumerate(self.ntypes) if f is not None]
         return list(gather or [])
+
+    def sample_layers_bundle(self, seeds_list, layer_sizes, rng_seeds, gather=None,
+                             stream=None):
+        """Several layer-wise mini-batches in one launch sequence
+        (hg_sample_layers_bundle): seeds_list[b] per node type as in
+        sample_layers, rng_seeds[b]; the same layer_sizes for all.  Returns one
+        Blocks per batch."""
+        lib = load_library()
+        T = self.T
+        B = len(seeds_list)
+        if len(rng_seeds) != B:
+            raise ValueError("one rng seed per batch")
+        keep = []
+        ptrs = (ctypes.c_void_p * max(B * T, 1))()
+        counts = (ctypes.c_int64 * max(B * T, 1))()
+        for b, seeds in enumerate(seeds_list):
+            if len(seeds) != T:
+                raise ValueError("one seed entry per node type")
+            for t, s in enumerate(seeds):
+                if s is None:
+                    continue
+                s = _dev_i64(s, self.device)
+                keep.append(s)
+                counts[b * T + t] = s.numel()
+                ptrs[b * T + t] = s.data_ptr() if s.numel() else None
+        H = len(layer_sizes)
+        flat = [int(k) for row in layer_sizes for k in row]
+        if len(flat) != H * T:
+            raise ValueError("layer_sizes must be [n_hops][n_ntypes]")
+        ls = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        sg = (ctypes.c_uint64 * max(B, 1))(*[int(s) & (2**64 - 1) for s in rng_seeds])
+        gather = self._gather_list(gather)
+        gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
+        hs = (ctypes.c_void_p * max(B, 1))()
+        st = lib.hg_sample_layers_bundle(self._h, B, ptrs, counts, H, ls, sg, gt, len(gather),
+                                         _stream(stream), hs)
+        del keep
+        _check(st)
+        return [Blocks(self, ctypes.c_void_p(hs[b]), H) for b in range(B)]
 
     def sample_edge_blocks(self, targets, fanouts, rng_seed: int = 0, n_neg: int = 0,
                            exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None,

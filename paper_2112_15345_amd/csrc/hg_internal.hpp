@@ -239,12 +239,14 @@ struct LayerArgs {
   const int64_t *all_src;
   const int64_t *all_eid;
   const int32_t *all_dst_local;
-  uint64_t *wt[kInlineTypes];
-  int64_t *cand[kInlineTypes];
-  uint64_t *prefix[kInlineTypes];
-  int64_t cand_tile[kInlineTypes + 1];
-  int64_t draw_base[kInlineTypes + 1];  // threads of the draw launch per type
-  int32_t draws[kInlineTypes];
+  // per node type, in a device table of the hop (see LayerTable)
+  uint64_t *const *wt;        // [T] importance of every vertex of the type
+  int64_t *const *cand;       // [T] the type's candidates, ascending
+  uint64_t *const *prefix;    // [T] their importance prefix
+  const int64_t *cand_tile;   // [T+1] first scan tile of each type's candidates
+  const int64_t *draw_base;   // [T+1] threads of the draw launch per type
+  const int32_t *draws;       // [T] draws (-1: every candidate)
+  int64_t cand_tiles, draw_threads;  // cand_tile[T], draw_base[T] (host copies)
   int64_t *tile_sum;   // per scan tile
   int64_t *tile_pre;   // per scan tile: exclusive scan over all tiles, then the grand total
   int64_t n_keep_tiles;
@@ -252,10 +254,20 @@ struct LayerArgs {
   int64_t *out_eid;
   int32_t *out_src_local, *out_dst_local;
   int64_t *out_indptr;  // [P + R]
-  uint64_t sigma;
+  // node type t is keyed as type t % key_T with seed sigmas[t / key_T] (a
+  // bundle's copy; a single batch: key_T = n_types)
+  const uint64_t *sigmas;
+  int32_t key_T;
   int32_t hop;
   int64_t *small;
 };
+
+// The per-type arrays of one layer-wise hop, as laid out in the call's
+// tables (8-byte words): wt [T], cand [T], prefix [T], cand_tile [T+1],
+// draw_base [T+1], draws [T] (int32, rounded up to words).
+inline size_t layer_table_bytes(int32_t T) {
+  return sizeof(int64_t) * (3 * size_t(T) + 2 * (size_t(T) + 1) + (size_t(T) + 1) / 2);
+}
 
 // Importance of every candidate: for each in-edge u -> v of the frontier
 // whose source is not in the frontier, wt[type(u)][u] += floor(2^32 / deg(v)^2).

@@ -200,6 +200,8 @@ __global__ __launch_bounds__(256) void k_lw_draw(LayerArgs A) {
   for (int64_t x = gs_start(); x < n; x += gs_step()) {
     const int t = find_segment(A.draw_base, A.n_types, x);
     const int64_t k = x - A.draw_base[t];
+    const int copy = t / A.key_T;
+    const uint64_t sigma = A.sigmas[copy];
     const int64_t nc = A.small[kSlotNew + t];
     const int64_t *cand = A.cand[t];
     uint8_t *reached = A.ts[t].reached;
@@ -210,8 +212,9 @@ __global__ __launch_bounds__(256) void k_lw_draw(LayerArgs A) {
     const uint64_t total = uint64_t(A.tile_pre[A.cand_tile[t + 1]] - A.tile_pre[A.cand_tile[t]]);
     if (total == 0 || nc == 0) continue;
     const U32x4 r4 = philox4x32_10(U32x4{uint32_t(k), uint32_t(uint64_t(k) >> 32),
-                                         0x40000000u | uint32_t(A.hop), uint32_t(t)},
-                                   uint32_t(A.sigma), uint32_t(A.sigma >> 32));
+                                         0x40000000u | uint32_t(A.hop),
+                                         uint32_t(t - copy * A.key_T)},
+                                   uint32_t(sigma), uint32_t(sigma >> 32));
     const uint64_t r = __umul64hi(uint64_t(r4.x) | (uint64_t(r4.y) << 32), total);
     // the last candidate whose prefix is not above r (zero-weight candidates
     // share the prefix of the next one and are never the last)
@@ -258,7 +261,7 @@ hipError_t launch_lw_weights(const LayerArgs &A, hipStream_t stream) {
 }
 
 hipError_t launch_lw_prefix(const LayerArgs &A, hipStream_t stream) {
-  const int64_t tiles = A.cand_tile[A.n_types];
+  const int64_t tiles = A.cand_tiles;
   if (tiles <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_lw_scan_reduce<0>, dim3(unsigned(tiles)), dim3(kLwThreads), 0, stream, A);
   hipLaunchKernelGGL(k_lw_scan_tiles, dim3(1), dim3(kLwScanThreads), 0, stream, A.tile_sum,
@@ -268,7 +271,7 @@ hipError_t launch_lw_prefix(const LayerArgs &A, hipStream_t stream) {
 }
 
 hipError_t launch_lw_draw(const LayerArgs &A, hipStream_t stream) {
-  const int64_t n = A.draw_base[A.n_types];
+  const int64_t n = A.draw_threads;
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_lw_draw, dim3(grid_for(n, 256)), dim3(256), 0, stream, A);
   return hipGetLastError();

@@ -1032,23 +1032,37 @@ hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
   A.n_pairs = P;
   A.n_all = S;
   A.n_keep_tiles = (S + kLayerTile - 1) / kLayerTile;
-  A.sigma = sigmas[0];
+  A.sigmas = dsigmas();
+  A.key_T = T / int32_t(sigmas.size());  // node types of one copy
   A.hop = h;
   A.small = ws->dsmall;
   A.out_eid = eid_all;
   A.out_src_local = srcl_all;
   A.out_dst_local = dstl_all;
   A.out_indptr = indptr_all;
-  A.cand_tile[0] = 0;
-  A.draw_base[0] = 0;
+  // the hop's per-type table, written into its own part of the call's tables
+  // and uploaded once
+  const size_t tab_off = sig_bytes + lay.size * size_t(n_regions()) +
+                         size_t(h) * align_up(layer_table_bytes(T));
+  char *ht = ws->htab + tab_off;
+  uint64_t **h_wt = reinterpret_cast<uint64_t **>(ht);
+  int64_t **h_cand = reinterpret_cast<int64_t **>(h_wt + T);
+  uint64_t **h_prefix = reinterpret_cast<uint64_t **>(h_cand + T);
+  int64_t *h_ctile = reinterpret_cast<int64_t *>(h_prefix + T);
+  int64_t *h_dbase = h_ctile + T + 1;
+  int32_t *h_draws = reinterpret_cast<int32_t *>(h_dbase + T + 1);
+  h_ctile[0] = 0;
+  h_dbase[0] = 0;
   for (int32_t t = 0; t < T; ++t) {
     const int32_t k = layer_sizes[size_t(h) * T + t];
-    A.draws[t] = k;
-    A.cand_tile[t + 1] = A.cand_tile[t] + (cbound[t] + kLayerTile - 1) / kLayerTile;
-    A.draw_base[t + 1] = A.draw_base[t] + (k < 0 ? cbound[t] : (cbound[t] > 0 ? k : 0));
-    A.wt[t] = static_cast<uint64_t *>(ws->lw_weight.p) + g->map_off[t];
+    h_draws[t] = k;
+    h_ctile[t + 1] = h_ctile[t] + (cbound[t] + kLayerTile - 1) / kLayerTile;
+    h_dbase[t + 1] = h_dbase[t] + (k < 0 ? cbound[t] : (cbound[t] > 0 ? k : 0));
+    h_wt[t] = static_cast<uint64_t *>(ws->lw_weight.p) + g->map_off[t];
   }
-  const int64_t scan_tiles = std::max(A.cand_tile[T], A.n_keep_tiles) + 1;
+  A.cand_tiles = h_ctile[T];
+  A.draw_threads = h_dbase[T];
+  const int64_t scan_tiles = std::max(A.cand_tiles, A.n_keep_tiles) + 1;
   Carve ec;
   int64_t *all_eid;
   int32_t *all_dstl;
@@ -1057,13 +1071,22 @@ hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
   ec.add(&A.pos, S + 1);
   Carve cc;
   for (int32_t t = 0; t < T; ++t) {
-    cc.add(&A.cand[t], cbound[t]);
-    cc.add(&A.prefix[t], cbound[t]);
+    cc.add(&h_cand[t], cbound[t]);
+    cc.add(&h_prefix[t], cbound[t]);
   }
   cc.add(&A.tile_sum, scan_tiles);
   cc.add(&A.tile_pre, scan_tiles);
   if (!ec.in_scratch(ws->lw_edges, stream) || !cc.in_scratch(ws->lw_cand, stream))
     return fail(HG_ENOMEM, "hop %d: layer-wise scratch", h);
+  if ((e = upload(tab_off, tab_off + layer_table_bytes(T))) != hipSuccess)
+    return fail_device(e, "layer table");
+  char *dt = static_cast<char *>(ws->tab.p) + tab_off;
+  A.wt = reinterpret_cast<uint64_t *const *>(dt);
+  A.cand = reinterpret_cast<int64_t *const *>(dt + sizeof(void *) * size_t(T));
+  A.prefix = reinterpret_cast<uint64_t *const *>(dt + sizeof(void *) * 2 * size_t(T));
+  A.cand_tile = reinterpret_cast<const int64_t *>(dt + sizeof(void *) * 3 * size_t(T));
+  A.draw_base = A.cand_tile + T + 1;
+  A.draws = reinterpret_cast<const int32_t *>(A.draw_base + T + 1);
   A.all_src = gid_tmp;
   A.all_eid = all_eid;
   A.all_dst_local = all_dstl;
@@ -1084,7 +1107,7 @@ hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
   int64_t ticketed = 0;
   uint32_t epoch;
   if ((e = launch_store_ptrs(reinterpret_cast<void **>(dreg(H + 2) + lay.src_out),
-                             reinterpret_cast<void *const *>(A.cand), T, stream)) != hipSuccess ||
+                             reinterpret_cast<void *const *>(h_cand), T, stream)) != hipSuccess ||
       (e = next_epoch(&epoch)) != hipSuccess ||
       (e = launch_compact(cv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles, 0,
                           ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed, stream,
@@ -1657,14 +1680,15 @@ hg_status run_edge_sampling(hg_graph *g, const hg_edge_batch *eb, int32_t n_hops
 
 // A layer-wise mini-batch (checked), then the gather.
 hg_status run_layer_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
-                             int32_t n_hops, const int32_t *layer_sizes, uint64_t rng_seed,
-                             const int32_t *gtypes, int32_t n_gather, hipStream_t stream,
-                             hg_blocks **out) {
+                             int32_t n_hops, const int32_t *layer_sizes, const uint64_t *sigmas,
+                             int32_t n_sig, const int32_t *gtypes, int32_t n_gather,
+                             hipStream_t stream, hg_blocks **out) {
   DeviceGuard dg(g->device);
-  SampleRun run(g, stream, n_hops, nullptr, &rng_seed, 1, 32);
+  SampleRun run(g, stream, n_hops, nullptr, sigmas, n_sig, 32);
   run.gtypes = gtypes;
   run.n_gather = n_gather;
   run.layer_sizes = layer_sizes;
+  run.edge_tab = size_t(std::max(n_hops, 0)) * align_up(layer_table_bytes(g->T));
   hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
   if (st != HG_OK) return st;
   run.b = new (std::nothrow) hg_blocks();
@@ -1957,8 +1981,6 @@ hg_status hg_sample_layers(hg_graph *g, const int64_t *const *seeds, const int64
   *out = nullptr;
   clear_pending_error();
   if (!g) return fail(HG_EINVAL, "hg_sample_layers: graph is NULL");
-  if (g->T > kInlineTypes)
-    return fail(HG_EUNSUPPORTED, "hg_sample_layers: more than %d node types", kInlineTypes);
   if (n_hops > 0 && !layer_sizes) return fail(HG_EINVAL, "hg_sample_layers: layer_sizes is NULL");
   for (int64_t i = 0; i < int64_t(std::max(n_hops, 0)) * g->T; ++i)
     if (layer_sizes[i] < -1)
@@ -1967,8 +1989,70 @@ hg_status hg_sample_layers(hg_graph *g, const int64_t *const *seeds, const int64
   hg_status st = check_batch(g, seeds, n_seeds, n_hops, every.data(), 32, gather_ntypes,
                              n_gather);
   if (st != HG_OK) return st;
-  return run_layer_sampling(g, seeds, n_seeds, n_hops, layer_sizes, rng_seed, gather_ntypes,
+  return run_layer_sampling(g, seeds, n_seeds, n_hops, layer_sizes, &rng_seed, 1, gather_ntypes,
                             n_gather, stream, out);
+}
+
+hg_status hg_sample_layers_bundle(hg_graph *g, int32_t n_batches, const int64_t *const *seeds,
+                                  const int64_t *n_seeds, int32_t n_hops,
+                                  const int32_t *layer_sizes, const uint64_t *rng_seeds,
+                                  const int32_t *gather_ntypes, int32_t n_gather,
+                                  hipStream_t stream, hg_blocks **out) {
+  if (!out) return fail(HG_EINVAL, "hg_sample_layers_bundle: out is NULL");
+  clear_pending_error();
+  if (!g) return fail(HG_EINVAL, "hg_sample_layers_bundle: graph is NULL");
+  if (n_batches < 1 || n_batches > kMaxBundle)
+    return fail(HG_EINVAL, "hg_sample_layers_bundle: n_batches not in 1..%d", kMaxBundle);
+  for (int32_t b = 0; b < n_batches; ++b) out[b] = nullptr;
+  if (!rng_seeds || !n_seeds) return fail(HG_EINVAL, "hg_sample_layers_bundle: NULL array");
+  if (n_hops > 0 && !layer_sizes)
+    return fail(HG_EINVAL, "hg_sample_layers_bundle: layer_sizes is NULL");
+  const int32_t T = g->T;
+  for (int64_t i = 0; i < int64_t(std::max(n_hops, 0)) * T; ++i)
+    if (layer_sizes[i] < -1)
+      return fail(HG_EINVAL, "hg_sample_layers_bundle: layer size %d < -1", layer_sizes[i]);
+  std::vector<int32_t> every(size_t(std::max(n_hops, 0)) * g->R + 1, -1);
+  for (int32_t b = 0; b < n_batches; ++b) {
+    hg_status st = check_batch(g, seeds ? seeds + size_t(b) * T : nullptr,
+                               n_seeds + size_t(b) * T, n_hops, every.data(), 32, gather_ntypes,
+                               n_gather);
+    if (st != HG_OK) return st;
+  }
+  if (n_batches == 1)
+    return run_layer_sampling(g, seeds, n_seeds, n_hops, layer_sizes, rng_seeds, 1,
+                              gather_ntypes, n_gather, stream, out);
+  hg_graph *v = nullptr;
+  hg_status st = bundle_graph(g, n_batches, &v);
+  if (st != HG_OK) return st;
+  std::vector<const int64_t *> vseeds(size_t(n_batches) * T, nullptr);
+  if (seeds) vseeds.assign(seeds, seeds + size_t(n_batches) * T);
+  // every copy draws the same layer sizes for its own node types
+  std::vector<int32_t> vsizes(size_t(std::max(n_hops, 0)) * v->T);
+  for (int32_t h = 0; h < n_hops; ++h)
+    for (int32_t b = 0; b < n_batches; ++b)
+      for (int32_t t = 0; t < T; ++t)
+        vsizes[size_t(h) * v->T + size_t(b) * T + t] = layer_sizes[size_t(h) * T + t];
+  std::vector<int32_t> vg;
+  for (int32_t b = 0; b < n_batches; ++b)
+    for (int32_t k = 0; k < n_gather; ++k) vg.push_back(b * T + gather_ntypes[k]);
+  hg_blocks *vb = nullptr;
+  st = run_layer_sampling(v, vseeds.data(), n_seeds, n_hops,
+                          vsizes.empty() ? nullptr : vsizes.data(), rng_seeds, n_batches,
+                          vg.empty() ? nullptr : vg.data(), int32_t(vg.size()), stream, &vb);
+  if (st != HG_OK) return st;
+  for (int32_t b = 0; b < n_batches; ++b) {
+    out[b] = split_blocks(g, vb, b);
+    if (!out[b]) {
+      for (int32_t c = 0; c < b; ++c) {
+        delete out[c];
+        out[c] = nullptr;
+      }
+      delete vb;
+      return fail(HG_ENOMEM, "hg_sample_layers_bundle: out of host memory");
+    }
+  }
+  delete vb;  // the split handles keep the arrays
+  return HG_OK;
 }
 
 hg_status hg_sample_edge_blocks_bundle(hg_graph *g, int32_t n_batches,

@@ -129,11 +129,15 @@ def test_layer_errors_and_recovery(olib):
     with pytest.raises(hg.HGError) as ex:
         g.sample_layers(gpu_seeds(far), [[1] * T], 0)
     assert ex.value.status == hg.HG_EINVAL
-    # more than 8 node types
-    many = gpu_graph([2] * 9, [(0, 1, np.array([0, 1, 1]), np.array([1]))], [None] * 9)
-    with pytest.raises(hg.HGError) as ex:
-        many.sample_layers([torch.tensor([0], device="cuda")] + [None] * 8, [[1] * 9], 0)
-    assert ex.value.status == hg.HG_EUNSUPPORTED
+    # nine node types (the per-type tables live on the device, not in the launch)
+    many_nn = [2] * 9
+    many_ets = [(0, 1, np.array([0, 1, 1]), np.array([1])),
+                (1, 0, np.array([0, 1, 1]), np.array([0]))]
+    many = gpu_graph(many_nn, many_ets, [None] * 9)
+    mseeds = [np.array([0])] + [None] * 8
+    _, _, mref, mgot = run_layer_both(olib, many_nn, many_ets, [None] * 9, mseeds,
+                                      [[1] * 9, [-1] * 9], 3, g=many)
+    assert not compare(mref, mgot, 9, 2, 2)
     # the failures left the workspaces clean
     sizes = [[-1] * T, [2] * T]
     _, _, ref, got = run_layer_both(olib, nn, ets, feats, seeds, sizes, 5, g=g)
@@ -169,3 +173,39 @@ def test_layer_workload_academic(olib):
             assert b.features(t).cpu().numpy().tobytes() == want.tobytes(), f"type {t}"
         say(f"academic layer batch {bno}: equal "
             f"({sum(v[3].size for v in ref['edges'].values())} kept edges)")
+
+
+@pytest.mark.parametrize("chunk", range(2))
+def test_layer_bundles_equal_single_calls(olib, chunk):
+    """Every batch of a layer-wise bundle is the batch its own call makes
+    (blocks and gathered bytes), and the oracle's."""
+    rng = np.random.default_rng(9300 + chunk)
+    for c in range(10):
+        nn, ets, feats, seeds, sizes, sigma = pins.random_layer_case(rng, max_nodes=60,
+                                                                     max_deg=40)
+        g = gpu_graph(nn, ets, feats)
+        B = [2, 4, 9][c % 3]
+        seeds_list = [seeds]
+        for b in range(1, B):
+            seeds_list.append([None if s is None else
+                               rng.choice(nn[t], size=s.size, replace=False).astype(np.int64)
+                               for t, s in enumerate(seeds)])
+        sigmas = [sigma + 29 * b for b in range(B)]
+        say(f"layer bundle chunk {chunk} case {c}: B={B} T={len(nn)} sizes={sizes}")
+        bl = g.sample_layers_bundle([gpu_seeds(s) for s in seeds_list], sizes, sigmas,
+                                    gather="all")
+        assert len(bl) == B
+        for b in range(B):
+            single = g.sample_layers(gpu_seeds(seeds_list[b]), sizes, sigmas[b], gather="all")
+            got = result_dict(g, bl[b])
+            diffs = compare(result_dict(g, single), got, len(nn), len(ets), len(sizes))
+            assert not diffs, f"case {c} batch {b}: " + "\n".join(diffs[:10])
+            for t, f in enumerate(feats):
+                if f is not None:
+                    assert bl[b].features(t).cpu().numpy().tobytes() == \
+                        single.features(t).cpu().numpy().tobytes()
+            if b == B - 1:
+                ref = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib).sample_layers(
+                    seeds_list[b], sizes, sigmas[b])
+                diffs = compare(ref, got, len(nn), len(ets), len(sizes))
+                assert not diffs, f"case {c} batch {b} vs oracle: " + "\n".join(diffs[:10])
