@@ -276,22 +276,33 @@ __device__ void tile_lookback(Lookback lb, int64_t tile, int64_t first,
 }
 
 // Next hop's frontier sizes (this hop's plus the new vertices of each type)
-// and pair layout (pairs of etype e: frontier of its destination type).
+// and pair layout (pairs of etype e: frontier of its destination type).  Every
+// thread of one 256-thread block calls it; the per-etype pair counts come from
+// this hop's sizes directly, and a block scan (in chunks of 256 etypes) lays
+// them out.  `next` is another hop's region than `hv`.
+__device__ inline int64_t next_frontier_size(const HopView &hv, const int64_t *tile_base,
+                                             const int64_t *small, int t) {
+  // a type without bitmap tiles (no vertices) gains nothing
+  const int64_t u = tile_base[t + 1] > tile_base[t] ? small[kSlotNew + t] : 0;
+  return hv.nF[t] + u;
+}
+
 __device__ inline void plan_next_hop(HopView hv, HopView next, const EtypeStatic *es,
-                              const int64_t *tile_base, const int64_t *small,
-                              int32_t n_types, int32_t n_etypes) {
-  if (threadIdx.x != 0) return;
-  for (int t = 0; t < n_types; ++t) {
-    // a type without bitmap tiles (no vertices) gains nothing
-    const int64_t u = tile_base[t + 1] > tile_base[t] ? small[kSlotNew + t] : 0;
-    next.nF[t] = hv.nF[t] + u;
+                                     const int64_t *tile_base, const int64_t *small,
+                                     int32_t n_types, int32_t n_etypes) {
+  __shared__ int64_t plan_lds[4];
+  for (int t = threadIdx.x; t < n_types; t += 256)
+    next.nF[t] = next_frontier_size(hv, tile_base, small, t);
+  int64_t carry = 0;
+  for (int e0 = 0; e0 < n_etypes; e0 += 256) {
+    const int e = e0 + int(threadIdx.x);
+    const int64_t c = e < n_etypes ? next_frontier_size(hv, tile_base, small, es[e].dst_type) : 0;
+    int64_t total;
+    const int64_t pre = block_excl_scan_256(c, plan_lds, &total);
+    if (e < n_etypes) next.pair_base[e] = carry + pre;
+    carry += total;
   }
-  int64_t acc = 0;
-  for (int e = 0; e < n_etypes; ++e) {
-    next.pair_base[e] = acc;
-    acc += next.nF[es[e].dst_type];
-  }
-  next.pair_base[n_etypes] = acc;
+  if (threadIdx.x == 0) next.pair_base[n_etypes] = carry;
 }
 
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32

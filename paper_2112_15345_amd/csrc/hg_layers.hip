@@ -9,7 +9,9 @@
 // of the frontier (fanout -1) and set the reached flag of every source:
 //  1. k_lw_weights : importance of every candidate (a source not in the
 //                    frontier): sum of floor(2^32 / deg(v)^2) over its edges
-//                    into the frontier, 64-bit atomics (exact in any order);
+//                    into the frontier, 64-bit atomics (exact in any order),
+//                    blocks over contiguous tiles of edges whose etypes are
+//                    resolved once per tile (as in the kept-edge scans);
 //  2. compaction   : (collect mode) the candidates of each type, ascending;
 //  3. k_lw_scan_*  : exclusive prefix of their importance per type
 //                    (reduce-then-scan over 512-candidate tiles);
@@ -52,10 +54,17 @@ __device__ __forceinline__ bool in_frontier(const uint32_t *fbits, int64_t v) {
   return (fbits[v >> 5] >> (v & 31)) & 1u;
 }
 
-// floor(2^32 / d^2) for d >= 1 (zero once d^2 > 2^32).
+// floor(2^32 / d^2) for d >= 1 (zero once d^2 > 2^32).  The correctly
+// rounded double quotient lies between the two integers around the exact one,
+// so its floor is the exact floor or one above; integer checks settle it.
 __device__ __forceinline__ uint64_t layer_weight(int64_t d) {
   const uint64_t d2 = uint64_t(d) * uint64_t(d);
-  return d2 > (uint64_t(1) << 32) ? 0 : (uint64_t(1) << 32) / d2;
+  constexpr uint64_t kOne = uint64_t(1) << 32;
+  if (d2 > kOne) return 0;
+  uint64_t q = uint64_t(4294967296.0 / double(d2));
+  if (q * d2 > kOne) --q;
+  else if ((q + 1) * d2 <= kOne) ++q;
+  return q;
 }
 
 __device__ __forceinline__ const int64_t *ebase_of(const LayerArgs &A) {
@@ -65,17 +74,90 @@ __device__ __forceinline__ int64_t *kept_base_of(const LayerArgs &A) {
   return A.small + kSlotNew + A.n_types + A.n_etypes + 1;
 }
 
-__global__ __launch_bounds__(256) void k_lw_weights(LayerArgs A) {
+// The etypes that a block's contiguous range [j0, j1) of emitted edges spans,
+// resolved once per block: their starts and what the per-edge work reads of
+// them.  A range over more than kTileSegs etypes leaves n = 0 and its edges
+// search the etype starts one by one.
+constexpr int kTileSegs = 32;
+struct TileSegs {
+  int64_t start[kTileSegs + 1];
+  const uint32_t *fbits[kTileSegs];  // frontier bits of the source type
+  void *per_seg[kTileSegs];          // importance array of the source type, or source map
+  int64_t pair_base[kTileSegs];
+  int e0, n;
+};
+
+// kKind 0: per_seg = importance array of the source type; 1: source map.
+template <int kKind>
+__device__ void tile_segs_load(const LayerArgs &A, int64_t j0, int64_t j1, TileSegs &T) {
   const int64_t *ebase = ebase_of(A);
-  for (int64_t j = gs_start(); j < A.n_all; j += gs_step()) {
-    const int e = find_segment(ebase, A.n_etypes, j);
-    const EtypeStatic &E = A.es[e];
-    const int64_t u = A.all_src[j];
-    if (in_frontier(A.ts[E.src_type].fbits, u)) continue;
-    const int64_t p = A.hv.pair_base[e] + A.all_dst_local[j];
-    const uint64_t w = layer_weight(A.pa.pdeg[p]);
-    if (w) atomicAdd(reinterpret_cast<unsigned long long *>(A.wt[E.src_type] + u),
-                     (unsigned long long)w);
+  if (threadIdx.x == 0) {
+    const int a = find_segment(ebase, A.n_etypes, j0);
+    const int b = find_segment(ebase, A.n_etypes, j1 - 1);
+    T.e0 = a;
+    T.n = b - a + 1 <= kTileSegs ? b - a + 1 : 0;
+  }
+  __syncthreads();
+  const int n = T.n;
+  if (int(threadIdx.x) <= n && n > 0) {
+    const int e = T.e0 + int(threadIdx.x);
+    T.start[threadIdx.x] = ebase[e];
+    if (int(threadIdx.x) < n) {
+      const EtypeStatic &E = A.es[e];
+      T.fbits[threadIdx.x] = A.ts[E.src_type].fbits;
+      if (kKind == 0)
+        T.per_seg[threadIdx.x] = A.wt[E.src_type];
+      else
+        T.per_seg[threadIdx.x] = E.src_map;
+      T.pair_base[threadIdx.x] = A.hv.pair_base[e];
+    }
+  }
+  __syncthreads();
+}
+
+// Segment of edge j in the block's table, from a hint not above it (edges of
+// one thread come in ascending order).
+__device__ __forceinline__ int tile_seg(const TileSegs &T, int s, int64_t j) {
+  while (s + 1 < T.n && T.start[s + 1] <= j) ++s;
+  return s;
+}
+
+// Blocks of 256 threads take tiles of kLwWeightTile emitted edges, each
+// thread every 256th edge of the tile.
+constexpr int kLwWeightItems = 8;
+constexpr int64_t kLwWeightTile = 256 * kLwWeightItems;
+
+__device__ __forceinline__ void add_weight(uint64_t *wt, int64_t u, int64_t deg) {
+  const uint64_t w = layer_weight(deg);
+  if (w) atomicAdd(reinterpret_cast<unsigned long long *>(wt + u), (unsigned long long)w);
+}
+
+__global__ __launch_bounds__(256) void k_lw_weights(LayerArgs A) {
+  __shared__ TileSegs T;
+  const int64_t n_tiles = (A.n_all + kLwWeightTile - 1) / kLwWeightTile;
+  for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    const int64_t j0 = tile * kLwWeightTile;
+    const int64_t j1 = j0 + kLwWeightTile < A.n_all ? j0 + kLwWeightTile : A.n_all;
+    tile_segs_load<0>(A, j0, j1, T);
+    if (T.n > 0) {
+      int s = 0;
+      for (int64_t j = j0 + threadIdx.x; j < j1; j += 256) {
+        s = tile_seg(T, s, j);
+        const int64_t u = A.all_src[j];
+        if (in_frontier(T.fbits[s], u)) continue;
+        add_weight(static_cast<uint64_t *>(T.per_seg[s]), u,
+                   A.pa.pdeg[T.pair_base[s] + A.all_dst_local[j]]);
+      }
+    } else {
+      for (int64_t j = j0 + threadIdx.x; j < j1; j += 256) {
+        const int e = find_segment(ebase_of(A), A.n_etypes, j);
+        const EtypeStatic &E = A.es[e];
+        const int64_t u = A.all_src[j];
+        if (in_frontier(A.ts[E.src_type].fbits, u)) continue;
+        add_weight(A.wt[E.src_type], u, A.pa.pdeg[A.hv.pair_base[e] + A.all_dst_local[j]]);
+      }
+    }
+    __syncthreads();  // T is rebuilt for the next tile
   }
 }
 
@@ -99,44 +181,74 @@ __device__ __forceinline__ ScanSeg<kKind> seg_of(const LayerArgs &A, int64_t til
   return ScanSeg<kKind>{0, 0, A.n_all};
 }
 
+// Value i of the scan; kind 1 reads the etype of edge i from the block's
+// table (hint s, ascending i) or, past kTileSegs etypes, searches for it.
 template <int kKind>
 __device__ __forceinline__ int64_t value_of(const LayerArgs &A, const ScanSeg<kKind> &S,
-                                            int64_t i) {
+                                            const TileSegs &T, int &s, int64_t i) {
   if (i >= S.n) return 0;
   if (kKind == 0) return int64_t(A.wt[S.seg][A.cand[S.seg][i]]);
-  const int e = find_segment(ebase_of(A), A.n_etypes, i);
-  return in_frontier(A.ts[A.es[e].src_type].fbits, A.all_src[i]) ? 1 : 0;
+  const uint32_t *fbits;
+  if (T.n > 0) {
+    s = tile_seg(T, s, i);
+    fbits = T.fbits[s];
+  } else {
+    s = find_segment(ebase_of(A), A.n_etypes, i);
+    fbits = A.ts[A.es[s].src_type].fbits;
+  }
+  return in_frontier(fbits, A.all_src[i]) ? 1 : 0;
+}
+
+template <int kKind>
+__device__ __forceinline__ void scan_tile_segs(const LayerArgs &A, int64_t tile, TileSegs &T) {
+  if (kKind == 1) {
+    const int64_t j0 = tile * kLwTile;
+    const int64_t j1 = j0 + kLwTile < A.n_all ? j0 + kLwTile : A.n_all;
+    tile_segs_load<1>(A, j0, j1, T);
+  }
 }
 
 template <int kKind>
 __global__ __launch_bounds__(kLwThreads) void k_lw_scan_reduce(LayerArgs A) {
   __shared__ int64_t lds[8];
+  __shared__ TileSegs T;
   const int64_t tile = blockIdx.x;
+  scan_tile_segs<kKind>(A, tile, T);
   const ScanSeg<kKind> S = seg_of<kKind>(A, tile);
   const int64_t i0 = (tile - S.first_tile) * kLwTile + threadIdx.x * kLwItems;
   int64_t v = 0;
+  int s = 0;
 #pragma unroll
-  for (int k = 0; k < kLwItems; ++k) v += value_of<kKind>(A, S, i0 + k);
+  for (int k = 0; k < kLwItems; ++k) v += value_of<kKind>(A, S, T, s, i0 + k);
   int64_t total;
   block_excl_scan_256(v, lds, &total);
   if (threadIdx.x == 0) A.tile_sum[tile] = total;
 }
 
 // One block: tile_pre = exclusive scan of tile_sum over all n_tiles tiles,
-// tile_pre[n_tiles] = the grand total.
+// tile_pre[n_tiles] = the grand total.  Each thread takes kLwScanPer
+// consecutive tiles of a chunk.
 constexpr int kLwScanThreads = 1024;
+constexpr int kLwScanPer = 8;
 __global__ __launch_bounds__(kLwScanThreads) void k_lw_scan_tiles(int64_t *tile_sum,
                                                                   int64_t *tile_pre,
                                                                   int64_t n_tiles) {
   constexpr int kWaves = kLwScanThreads / kWave;
+  constexpr int64_t kChunk = int64_t(kLwScanThreads) * kLwScanPer;
   __shared__ int64_t s_wave[kWaves];
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
   int64_t carry = 0;
-  for (int64_t c0 = 0; c0 < n_tiles; c0 += kLwScanThreads) {
-    const int64_t i = c0 + threadIdx.x;
-    const int64_t x = i < n_tiles ? tile_sum[i] : 0;
-    const int64_t inc = wave_incl_scan_i64(x);
+  for (int64_t c0 = 0; c0 < n_tiles; c0 += kChunk) {
+    const int64_t i0 = c0 + int64_t(threadIdx.x) * kLwScanPer;
+    int64_t x[kLwScanPer];
+    int64_t mine = 0;
+#pragma unroll
+    for (int k = 0; k < kLwScanPer; ++k) {
+      x[k] = i0 + k < n_tiles ? tile_sum[i0 + k] : 0;
+      mine += x[k];
+    }
+    const int64_t inc = wave_incl_scan_i64(mine);
     if (lane == kWave - 1) s_wave[wave] = inc;
     __syncthreads();
     int64_t before = 0, sum = 0;
@@ -145,7 +257,12 @@ __global__ __launch_bounds__(kLwScanThreads) void k_lw_scan_tiles(int64_t *tile_
       if (w < wave) before += y;
       sum += y;
     }
-    if (i < n_tiles) tile_pre[i] = carry + before + inc - x;
+    int64_t run = carry + before + inc - mine;
+#pragma unroll
+    for (int k = 0; k < kLwScanPer; ++k) {
+      if (i0 + k < n_tiles) tile_pre[i0 + k] = run;
+      run += x[k];
+    }
     carry += sum;
     __syncthreads();
   }
@@ -156,14 +273,19 @@ __global__ __launch_bounds__(kLwScanThreads) void k_lw_scan_tiles(int64_t *tile_
 template <int kKind>
 __global__ __launch_bounds__(kLwThreads) void k_lw_scan_apply(LayerArgs A) {
   __shared__ int64_t lds[8];
+  __shared__ TileSegs T;
   const int64_t tile = blockIdx.x;
+  scan_tile_segs<kKind>(A, tile, T);
   const ScanSeg<kKind> S = seg_of<kKind>(A, tile);
   const int64_t i0 = (tile - S.first_tile) * kLwTile + threadIdx.x * kLwItems;
   int64_t v[kLwItems];
+  int segs[kLwItems];
   int64_t sum = 0;
+  int s = 0;
 #pragma unroll
   for (int k = 0; k < kLwItems; ++k) {
-    v[k] = value_of<kKind>(A, S, i0 + k);
+    v[k] = value_of<kKind>(A, S, T, s, i0 + k);
+    segs[k] = s;
     sum += v[k];
   }
   int64_t total;
@@ -179,10 +301,11 @@ __global__ __launch_bounds__(kLwThreads) void k_lw_scan_apply(LayerArgs A) {
       } else {
         A.pos[i] = pre;
         if (v[k]) {
-          const int e = find_segment(ebase_of(A), A.n_etypes, i);
+          const int32_t *src_map = T.n > 0 ? static_cast<const int32_t *>(T.per_seg[segs[k]])
+                                           : A.es[segs[k]].src_map;
           A.out_eid[pre] = A.all_eid[i];
           A.out_dst_local[pre] = A.all_dst_local[i];
-          A.out_src_local[pre] = A.es[e].src_map[A.all_src[i]];
+          A.out_src_local[pre] = src_map[A.all_src[i]];
         }
       }
     }
@@ -256,7 +379,8 @@ __global__ __launch_bounds__(256) void k_lw_indptr(LayerArgs A) {
 
 hipError_t launch_lw_weights(const LayerArgs &A, hipStream_t stream) {
   if (A.n_all <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_lw_weights, dim3(grid_for(A.n_all, 256)), dim3(256), 0, stream, A);
+  hipLaunchKernelGGL(k_lw_weights, dim3(grid_for(A.n_all, kLwWeightTile)), dim3(256), 0, stream,
+                     A);
   return hipGetLastError();
 }
 
