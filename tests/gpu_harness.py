@@ -81,3 +81,23 @@ def compare(ref, got, T, R, H):
         if not np.array_equal(ref["input"][t], got["input"][t]):
             diffs.append(f"input frontier of type {t} differs")
     return diffs
+
+
+def many_relations(rng, R, n0=300, n1=80):
+    """Two node types and R edge types, the first 40 and most others into type
+    0 (so that type 0 gets the per-vertex non-empty mask): per edge type a share of the
+    destinations (none, few, some, all) has in-edges, some edge types empty."""
+    nn = [n0, n1]
+    ets = []
+    for e in range(R):
+        d = 0 if e < 40 or rng.random() < 0.85 else 1
+        s = int(rng.integers(0, 2))
+        share = [0.0, 0.02, 0.2, 1.0][int(rng.integers(0, 4))]
+        indptr, indices = [0], []
+        for _v in range(nn[d]):
+            k = int(rng.integers(1, 12)) if rng.random() < share else 0
+            indices.extend(int(x) for x in np.sort(rng.choice(nn[s], size=k, replace=False)))
+            indptr.append(len(indices))
+        ets.append((s, d, np.array(indptr, np.int64), np.array(indices, np.int64)))
+    feats = [rng.standard_normal((n0, 4)).astype(np.float32), None]
+    return nn, ets, feats

@@ -13,7 +13,7 @@ import oracle
 import paper_2112_15345_amd as hg
 import pins
 import workloads as W
-from gpu_harness import compare, gpu_graph, gpu_seeds, result_dict
+from gpu_harness import compare, gpu_graph, gpu_seeds, many_relations, result_dict
 
 pytestmark = pytest.mark.gpu
 
@@ -209,3 +209,53 @@ def test_layer_bundles_equal_single_calls(olib, chunk):
                     seeds_list[b], sizes, sigmas[b])
                 diffs = compare(ref, got, len(nn), len(ets), len(sizes))
                 assert not diffs, f"case {c} batch {b} vs oracle: " + "\n".join(diffs[:10])
+
+
+def sparse_relations(rng, R, n0=300, n1=80):
+    """Two node types and R edge types with a handful of edges each: about 3%
+    of the destinations of an edge type have 1 to 3 in-edges."""
+    nn = [n0, n1]
+    ets = []
+    for _e in range(R):
+        s, d = int(rng.integers(0, 2)), int(rng.integers(0, 2))
+        indptr, indices = [0], []
+        for _v in range(nn[d]):
+            k = int(rng.integers(1, 4)) if rng.random() < 0.03 else 0
+            indices.extend(int(x) for x in np.sort(rng.choice(nn[s], size=k, replace=False)))
+            indptr.append(len(indices))
+        ets.append((s, d, np.array(indptr, np.int64), np.array(indices, np.int64)))
+    feats = [rng.standard_normal((n0, 4)).astype(np.float32), None]
+    return nn, ets, feats
+
+
+@pytest.mark.parametrize("R", [6, 40, 70])
+def test_layer_many_relations(olib, R):
+    """Many sparse edge types: a tile of in-edges (2048 in the importance
+    kernel, 512 in the kept-edge scan) then spans more etypes than the
+    kernels' per-tile tables hold (32), and the etype of each edge is searched
+    for instead; with 6 a tile spans few.  Single calls and a bundle of 4
+    against the oracle."""
+    rng = np.random.default_rng(8800 + R)
+    nn, ets, feats = many_relations(rng, R) if R <= 6 else sparse_relations(rng, R)
+    g = gpu_graph(nn, ets, feats)
+    host = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib)
+    for c in range(4):
+        seeds = [rng.choice(nn[0], size=int(rng.integers(20, 200)), replace=False).astype(np.int64),
+                 rng.choice(nn[1], size=int(rng.integers(0, 30)), replace=False).astype(np.int64)]
+        H = int(rng.integers(1, 4))
+        sizes = [[[-1, 0, 1, 5, 40][int(rng.integers(0, 5))] for _ in range(2)] for _ in range(H)]
+        sigma = int(rng.integers(0, 1 << 63))
+        say(f"layer many relations R={R} case {c}: H={H} sizes={sizes}")
+        b = g.sample_layers(gpu_seeds(seeds), sizes, sigma, gather="all")
+        got = result_dict(g, b)
+        ref = host.sample_layers(seeds, sizes, sigma)
+        diffs = compare(ref, got, 2, R, H)
+        assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
+        assert b.features(0).cpu().numpy().tobytes() == feats[0][got["input"][0]].tobytes()
+        # four copies of 70 etypes: the next-hop plan scans its 280 etypes in two chunks
+        sigmas = [sigma, sigma + 1, sigma + 2, sigma + 3]
+        bl = g.sample_layers_bundle([gpu_seeds(seeds)] * 4, sizes, sigmas, gather=[])
+        for k in range(4):
+            refk = ref if k == 0 else host.sample_layers(seeds, sizes, sigmas[k])
+            diffs = compare(refk, result_dict(g, bl[k]), 2, R, H)
+            assert not diffs, f"case {c} bundle copy {k}: " + "\n".join(diffs[:10])

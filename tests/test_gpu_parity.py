@@ -12,7 +12,7 @@ import oracle
 import paper_2112_15345_amd as hg
 import pins
 import workloads as W
-from gpu_harness import compare, gpu_graph, gpu_seeds, result_dict
+from gpu_harness import many_relations, compare, gpu_graph, gpu_seeds, result_dict
 
 pytestmark = pytest.mark.gpu
 
@@ -124,26 +124,6 @@ def test_hub_selection(olib, deg, k, bits):
         assert not diffs, "\n".join(diffs)
 
 
-def many_relations(rng, R, n0=300, n1=80):
-    """Two node types and R edge types, the first 40 and most others into type
-    0 (so that type 0 gets the per-vertex non-empty mask): per edge type a share of the
-    destinations (none, few, some, all) has in-edges, some edge types empty."""
-    nn = [n0, n1]
-    ets = []
-    for e in range(R):
-        d = 0 if e < 40 or rng.random() < 0.85 else 1
-        s = int(rng.integers(0, 2))
-        share = [0.0, 0.02, 0.2, 1.0][int(rng.integers(0, 4))]
-        indptr, indices = [0], []
-        for _v in range(nn[d]):
-            k = int(rng.integers(1, 12)) if rng.random() < share else 0
-            indices.extend(int(x) for x in np.sort(rng.choice(nn[s], size=k, replace=False)))
-            indptr.append(len(indices))
-        ets.append((s, d, np.array(indptr, np.int64), np.array(indices, np.int64)))
-    feats = [rng.standard_normal((n0, 4)).astype(np.float32), None]
-    return nn, ets, feats
-
-
 # 16 etypes into a type: the smallest with a mask; 33 and 70: rows of 2 and
 # 3 words
 @pytest.mark.parametrize("R", [16, 33, 70])
@@ -165,10 +145,11 @@ def test_many_relations(olib, R):
         diffs = compare(ref, got, 2, R, H)
         assert not diffs, f"case {c}: " + "\n".join(diffs[:10])
         assert b.features(0).cpu().numpy().tobytes() == feats[0][got["input"][0]].tobytes()
-        # the same batches bundled (the copies share the masks)
-        bl = g.sample_bundle([gpu_seeds(seeds)] * 3, fan, [sigma, sigma + 1, sigma + 2],
+        # the same batches bundled (the copies share the masks); four copies of
+        # 70 etypes: the next-hop plan scans its 280 etypes in two chunks
+        bl = g.sample_bundle([gpu_seeds(seeds)] * 4, fan, [sigma + k for k in range(4)],
                              gather=[])
-        for k in range(3):
+        for k in range(4):
             refk = ref if k == 0 else host.sample_blocks(seeds, fan, sigma + k)
             diffs = compare(refk, result_dict(g, bl[k]), 2, R, H)
             assert not diffs, f"case {c} bundle copy {k}: " + "\n".join(diffs[:10])
