@@ -28,13 +28,16 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 
-# Measured HBM traffic of one gather launch of the default run (academic
-# workload, bundles of 32, 32 warm-up + 320 timed mini-batches): FETCH_SIZE
-# and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the counters
-# read for a 1 GiB device copy (profiles/gather_academic_traffic.md).  Valid
-# only for the gather source and the launch configuration it was measured on.
+# Measured HBM traffic of the gather launches of one bundle of the default
+# run (academic workload, bundles of 16, 32 warm-up + 320 timed mini-batches):
+# FETCH_SIZE and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the
+# counters read for a 1 GiB device copy (profiles/gather_academic_traffic.md).
+# Counter collection runs one dispatch at a time, so a bundle's gather moves
+# the same bytes with or without worker streams; the figure is valid only for
+# the gather source, the workload, the batches and the bundle size it was
+# measured on.
 GATHER_TRAFFIC = {"source_sha256_16": "307d950537d4b4f1", "workload": 2, "steps": 320,
-                  "warmup": 32, "bundle": 32, "workers": 0, "bytes_per_launch": 7978287171.2}
+                  "warmup": 32, "bundle": 16, "bytes_per_launch": 3989131815.2}
 
 
 def measured_gather_traffic(args):
@@ -42,9 +45,8 @@ def measured_gather_traffic(args):
     src = os.path.join(ROOT, "paper_2112_15345_amd", "csrc", "hg_gather.hip")
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     t = GATHER_TRAFFIC
-    if (digest, args.workload, args.steps, args.warmup, args.bundle, args.workers) != (
-            t["source_sha256_16"], t["workload"], t["steps"], t["warmup"], t["bundle"],
-            t["workers"]):
+    if (digest, args.workload, args.steps, args.warmup, args.bundle) != (
+            t["source_sha256_16"], t["workload"], t["steps"], t["warmup"], t["bundle"]):
         return None
     return t["bytes_per_launch"]
 
@@ -236,10 +238,12 @@ def main():
     ap.add_argument("--workload", type=int, default=2,
                     help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
                          "5 gather-heavy academic")
-    ap.add_argument("--workers", type=int, default=0,
-                    help="pipeline worker threads (own streams); 0 = direct calls (default)")
-    ap.add_argument("--bundle", type=int, default=32,
-                    help="mini-batches per launch sequence (hg_sample_blocks_bundle, 1..32)")
+    ap.add_argument("--workers", type=int, default=None,
+                    help="pipeline worker threads (own streams); 0 = direct calls on one "
+                         "stream (default: 3 for the vertex task, 0 for the others)")
+    ap.add_argument("--bundle", type=int, default=None,
+                    help="mini-batches per launch sequence (hg_sample_blocks_bundle, 1..32; "
+                         "default: 16 with workers, 32 with direct calls)")
     ap.add_argument("--depth", type=int, default=0,
                     help="mini-batches outstanding in the pipeline (default 2 x workers)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -255,6 +259,10 @@ def main():
                          "direct calls); layers: layer-wise LADIES mini-batches "
                          "(hg_sample_layers, direct calls)")
     args = ap.parse_args()
+    if args.workers is None:
+        args.workers = 3 if args.task == "vertex" else 0
+    if args.bundle is None:
+        args.bundle = 16 if args.workers > 0 else 32
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
@@ -471,6 +479,9 @@ def main():
                      "traffic": None if args.host_features else measured_gather_traffic(args),
                      "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
                      "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3,
+                     "overlap": ("the gather launches of a bundle share the GPU with other "
+                                 "workers' sampling kernels; isolated_* is the same gather "
+                                 "with nothing else running") if args.workers > 1 else "none",
                      "isolated_achieved": iso_gbps,
                      "isolated_frac": iso_gbps / peak,
                      "device_copy_GBps": copy_gbps},

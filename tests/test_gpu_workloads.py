@@ -66,6 +66,47 @@ def test_workload_parity(idx, batches):
             f"({sum(v[3].size for v in ref['edges'].values())} edges)")
 
 
+def test_workload_pipeline_launch():
+    """The academic workload as bench.py runs it by default: bundles of 16
+    mini-batches submitted to a pipeline of 3 worker streams (at most 96
+    outstanding), here the first three timed bundles (batches 32..79).  Every
+    mini-batch comes back in order and equals its own single call (blocks and
+    gathered bytes); the first and last of each bundle also equal the oracle."""
+    wl, gen, g, host = workload_graph(2)
+    fan = wl.fanout_matrix()
+    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    batches = list(range(32, 80))
+    bundles = [batches[i:i + 16] for i in range(0, len(batches), 16)]
+    seeds = {b: gpu_seeds(W.seeds_per_type(wl, b)) for b in batches}
+    pipe = hg.Pipeline(g, workers=3, capacity=96, gather=feat_types)
+    try:
+        for u in bundles:
+            pipe.submit_bundle([seeds[b] for b in u], fan, u)
+        got = {b: pipe.next() for b in batches}
+    finally:
+        pipe.close()
+    for u in bundles:
+        say(f"pipeline bundle {u[0]}..{u[-1]}")
+        for b in u:
+            direct = g.sample_blocks(seeds[b], fan, b, gather="all")
+            mine = result_dict(g, got[b])
+            diffs = compare(result_dict(g, direct), mine, g.T, g.R, len(fan))
+            assert not diffs, f"batch {b}: " + "\n".join(diffs[:10])
+            for t in feat_types:
+                assert torch.equal(got[b].features(t).view(torch.uint8),
+                                   direct.features(t).view(torch.uint8)), f"batch {b} type {t}"
+            if b in (u[0], u[-1]):
+                ref = host.sample_blocks(W.seeds_per_type(wl, b), fan, b)
+                diffs = compare(ref, mine, g.T, g.R, len(fan))
+                assert not diffs, f"batch {b} vs oracle: " + "\n".join(diffs[:10])
+                for t in feat_types:
+                    want = host.gather(t, ref["input"][t]).tobytes()
+                    assert got[b].features(t).contiguous().view(torch.uint8).cpu().numpy() \
+                        .tobytes() == want, f"batch {b} type {t}: gathered bytes differ"
+                say(f"batch {b}: equal to the oracle")
+            del direct
+
+
 def test_workload_invariants_with_forced_ties():
     """Academic workload with 4-bit keys (ties everywhere, hub fallbacks), one
     batch: GPU == oracle, and the definition checks hold on the GPU result."""
