@@ -88,12 +88,79 @@ def cpu_baseline(gen, wl, first_batch, budget_s=12.0, max_batches=32):
             "gathered_GBps": nbytes / spent / 1e9}
 
 
+def pipeline_name(args):
+    return f"{args.workers} worker streams" if args.workers else "direct calls"
+
+
+def drive_units(args, g, n_batches, direct, submit, account, gather):
+    """Warm-up then timed units of --bundle batch indices (first, last): with
+    --workers 0, direct(first, last) returns the unit's Blocks; otherwise
+    submit(pipe, first, last) queues the unit on a pipeline of --workers
+    worker streams (at most --depth, default 2 x workers x bundle, mini-batches
+    outstanding) and the Blocks come back in order.  account(blocks) runs on
+    every timed mini-batch.  Returns the timed region's wall time."""
+    import torch
+
+    import paper_2112_15345_amd as hg
+
+    B = max(1, args.bundle)
+    units = [(b, min(b + B, args.warmup)) for b in range(0, args.warmup, B)]
+    timed = [(b, min(b + B, n_batches)) for b in range(args.warmup, n_batches, B)]
+    if args.workers == 0:
+        for u in units:
+            direct(*u)
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        for u in timed:
+            for blocks in direct(*u):
+                account(blocks)
+                del blocks
+        torch.cuda.synchronize()
+        return time.perf_counter() - t_start
+    depth = max(args.depth or 2 * args.workers * B, B)
+    pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=gather)
+    queue = units + timed
+    state = {"next": 0, "outstanding": 0}
+
+    def submit_more():
+        while state["next"] < len(queue):
+            first, last = queue[state["next"]]
+            if state["outstanding"] + (last - first) > depth:
+                break
+            submit(pipe, first, last)
+            state["outstanding"] += last - first
+            state["next"] += 1
+
+    def take(first, last):
+        out = []
+        for _ in range(last - first):
+            out.append(pipe.next())
+            state["outstanding"] -= 1
+        submit_more()
+        return out
+
+    submit_more()
+    for u in units:
+        take(*u)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for u in timed:
+        for blocks in take(*u):
+            account(blocks)
+            del blocks
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    pipe.close()
+    return elapsed
+
+
 def link_main(args, wl, gen, g):
     """Edge-seeded (link-prediction) mini-batches: targets of one forward
     relation, their endpoints as seeds, one negative per target, targets and
     their reverse edges excluded, the paper's link-prediction fanouts [25, 15]
     per hop, every featured type gathered.  Bundles of --bundle mini-batches
-    per call (hg_sample_edge_blocks_bundle), direct calls on one stream."""
+    (hg_sample_edge_blocks_bundle), made by --workers pipeline workers or by
+    direct calls on one stream."""
     import torch
 
     import paper_2112_15345_amd as hg
@@ -110,29 +177,27 @@ def link_main(args, wl, gen, g):
     targets = [[None if x is None else torch.as_tensor(x, device=dev)
                 for x in W.link_targets(gen, b, link_et)] for b in range(n_batches)]
 
-    B = max(1, args.bundle)
+    kw = dict(n_neg=W.LINK_NEG, exclude=exclude, rev_etype=rev_et, rev_eid=rev_eid)
 
-    def unit(first, last):
+    def direct(first, last):
         return g.sample_edge_bundle([targets[b] for b in range(first, last)], fan,
-                                    list(range(first, last)), n_neg=W.LINK_NEG,
-                                    exclude=exclude, rev_etype=rev_et, rev_eid=rev_eid,
-                                    gather=feat_types)
+                                    list(range(first, last)), gather=feat_types, **kw)
 
-    for b in range(0, args.warmup, B):
-        unit(b, min(b + B, args.warmup))
-    torch.cuda.synchronize()
-    edges = rows = gbytes = 0
-    t_start = time.perf_counter()
-    for b0 in range(args.warmup, n_batches, B):
-        for blocks in unit(b0, min(b0 + B, n_batches)):
-            edges += blocks.total_edges()
-            for t in feat_types:
-                n = blocks.num_input_nodes(t)
-                rows += n
-                gbytes += n * row_bytes[t]
-            del blocks
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
+    def submit(pipe, first, last):
+        pipe.submit_edge_bundle([targets[b] for b in range(first, last)], fan,
+                                list(range(first, last)), **kw)
+
+    totals = [0, 0, 0]
+
+    def account(blocks):
+        totals[0] += blocks.total_edges()
+        for t in feat_types:
+            n = blocks.num_input_nodes(t)
+            totals[1] += n
+            totals[2] += n * row_bytes[t]
+
+    elapsed = drive_units(args, g, n_batches, direct, submit, account, feat_types)
+    edges, rows, gbytes = totals
     result = {
         "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
         "value": edges / elapsed, "unit": "sampled edges/s", "n_gpus": 1,
@@ -144,7 +209,7 @@ def link_main(args, wl, gen, g):
                                f"'{gen.etype_names[link_et]}', {W.LINK_NEG} negative each, "
                                f"exclusion {exclude}, fanout {list(W.LINK_FANOUTS)}",
                    "workload_index": args.workload, "task": "link",
-                   "parallelism": "single GPU", "pipeline": "direct calls",
+                   "parallelism": "single GPU", "pipeline": pipeline_name(args),
                    "bundle": max(1, args.bundle)},
         "gathered_GBps": gbytes / elapsed / 1e9,
         "sampled_edges_per_step": edges / args.steps,
@@ -156,8 +221,8 @@ def link_main(args, wl, gen, g):
 def layers_main(args, wl, gen, g):
     """Layer-wise (LADIES) mini-batches: the workload's seeds, 512 draws per
     node type in each of two hops, every featured type gathered.  Bundles of
-    --bundle mini-batches per call (hg_sample_layers_bundle), direct calls on
-    one stream."""
+    --bundle mini-batches (hg_sample_layers_bundle), made by --workers
+    pipeline workers or by direct calls on one stream."""
     import torch
 
     import workloads as W
@@ -170,27 +235,25 @@ def layers_main(args, wl, gen, g):
     seeds = [[None if s is None else torch.as_tensor(s, device=dev)
               for s in W.seeds_per_type(wl, b)] for b in range(n_batches)]
 
-    B = max(1, args.bundle)
-
-    def unit(first, last):
+    def direct(first, last):
         return g.sample_layers_bundle([seeds[b] for b in range(first, last)], sizes,
                                       list(range(first, last)), gather=feat_types)
 
-    for b in range(0, args.warmup, B):
-        unit(b, min(b + B, args.warmup))
-    torch.cuda.synchronize()
-    edges = rows = gbytes = 0
-    t_start = time.perf_counter()
-    for b0 in range(args.warmup, n_batches, B):
-        for blocks in unit(b0, min(b0 + B, n_batches)):
-            edges += blocks.total_edges()
-            for t in feat_types:
-                n = blocks.num_input_nodes(t)
-                rows += n
-                gbytes += n * row_bytes[t]
-            del blocks
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
+    def submit(pipe, first, last):
+        pipe.submit_layers_bundle([seeds[b] for b in range(first, last)], sizes,
+                                  list(range(first, last)))
+
+    totals = [0, 0, 0]
+
+    def account(blocks):
+        totals[0] += blocks.total_edges()
+        for t in feat_types:
+            n = blocks.num_input_nodes(t)
+            totals[1] += n
+            totals[2] += n * row_bytes[t]
+
+    elapsed = drive_units(args, g, n_batches, direct, submit, account, feat_types)
+    edges, rows, gbytes = totals
     result = {
         "metric": "kept edges/s + gathered feature GB/s per layer-wise mini-batch (1 GPU)",
         "value": edges / elapsed, "unit": "kept edges/s", "n_gpus": 1,
@@ -201,7 +264,7 @@ def layers_main(args, wl, gen, g):
         "config": {"workload": wl.name + f"; layer-wise (LADIES): {list(W.LAYER_SIZES)} draws "
                                f"per node type per hop",
                    "workload_index": args.workload, "task": "layers",
-                   "parallelism": "single GPU", "pipeline": "direct calls",
+                   "parallelism": "single GPU", "pipeline": pipeline_name(args),
                    "bundle": max(1, args.bundle)},
         "gathered_GBps": gbytes / elapsed / 1e9,
         "kept_edges_per_step": edges / args.steps,
@@ -240,12 +303,13 @@ def main():
                          "5 gather-heavy academic")
     ap.add_argument("--workers", type=int, default=None,
                     help="pipeline worker threads (own streams); 0 = direct calls on one "
-                         "stream (default: 3 for the vertex task, 0 for the others)")
+                         "stream (default 3)")
     ap.add_argument("--bundle", type=int, default=None,
-                    help="mini-batches per launch sequence (hg_sample_blocks_bundle, 1..32; "
+                    help="mini-batches per launch sequence (the *_bundle calls, 1..32; "
                          "default: 16 with workers, 32 with direct calls)")
     ap.add_argument("--depth", type=int, default=0,
-                    help="mini-batches outstanding in the pipeline (default 2 x workers)")
+                    help="mini-batches outstanding in the pipeline (default 2 x workers x "
+                         "bundle)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after warm-up (untimed), copy this many MiB device to device "
@@ -255,12 +319,12 @@ def main():
                          "(zero-copy); the gather rate then includes that link")
     ap.add_argument("--task", choices=("vertex", "link", "layers"), default="vertex",
                     help="vertex: mini-batches from seed vertices (the default); link: "
-                         "edge-seeded link-prediction mini-batches (hg_sample_edge_blocks, "
-                         "direct calls); layers: layer-wise LADIES mini-batches "
-                         "(hg_sample_layers, direct calls)")
+                         "edge-seeded link-prediction mini-batches "
+                         "(hg_sample_edge_blocks_bundle); layers: layer-wise LADIES "
+                         "mini-batches (hg_sample_layers_bundle)")
     args = ap.parse_args()
     if args.workers is None:
-        args.workers = 3 if args.task == "vertex" else 0
+        args.workers = 3
     if args.bundle is None:
         args.bundle = 16 if args.workers > 0 else 32
     if args.gpus != 1:

@@ -410,6 +410,26 @@ hg_status hg_sample_layers_bundle(hg_graph *graph, int32_t n_batches,
                                   const uint64_t *rng_seeds, const int32_t *gather_ntypes,
                                   int32_t n_gather, hipStream_t stream, hg_blocks **out);
 
+/* Pipeline submissions of layer-wise and edge-seeded mini-batches (Sec.
+ * 4.2.1 and 4.2.2: the asynchronous pipeline serves every kind of sampling).
+ * As hg_pipeline_submit, with the arguments of hg_sample_layers_bundle and
+ * hg_sample_edge_blocks_bundle: a worker makes the n_batches (1..capacity;
+ * more than 32 fail at the worker) mini-batches as one bundle, gathering the
+ * pipeline's gather_ntypes, and hg_pipeline_next returns them one by one in
+ * submission order.  Host arrays (n_seeds, layer_sizes, fanouts, rng_seeds,
+ * each hg_edge_batch and the host arrays it points to) are copied; the device
+ * arrays they point to (seeds, targets, reverse maps) are read on the
+ * worker's stream and must stay valid until the mini-batches have been
+ * returned.  HG_EINVAL here for a NULL or out-of-range argument; errors found
+ * later fail the whole bundle at hg_pipeline_next. */
+hg_status hg_pipeline_submit_layers(hg_pipeline *pipe, int32_t n_batches,
+                                    const int64_t *const *seeds, const int64_t *n_seeds,
+                                    int32_t n_hops, const int32_t *layer_sizes,
+                                    const uint64_t *rng_seeds);
+hg_status hg_pipeline_submit_edges(hg_pipeline *pipe, int32_t n_batches,
+                                   const hg_edge_batch *batches, int32_t n_hops,
+                                   const int32_t *fanouts, const uint64_t *rng_seeds);
+
 /* Thread-local description of the last failure on this thread. */
 const char *hg_last_error(void);
 

@@ -41,6 +41,7 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_
                "hg_pipeline_destroy", "hg_sample_edge_blocks", "hg_blocks_seeds",
                "hg_blocks_edge_pairs", "hg_sample_layers", "hg_blocks_edge_counts",
                "hg_sample_edge_blocks_bundle", "hg_sample_layers_bundle",
+               "hg_pipeline_submit_layers", "hg_pipeline_submit_edges",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox")
 
 HG_MAX_NEG = 64
@@ -119,6 +120,8 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_edge_counts": ([_P, _P], _I32),
         "hg_sample_edge_blocks_bundle": ([_P, _I32, _P, _I32, _P, _P, _P, _I32, _P, _P], _I32),
         "hg_sample_layers_bundle": ([_P, _I32, _P, _P, _I32, _P, _P, _P, _I32, _P, _P], _I32),
+        "hg_pipeline_submit_layers": ([_P, _I32, _P, _P, _I32, _P, _P], _I32),
+        "hg_pipeline_submit_edges": ([_P, _I32, _P, _I32, _P, _P], _I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -710,6 +713,62 @@ class Pipeline:
         start, stop = events if events is not None else (None, None)
         _check(load_library().hg_pipeline_submit(self._h, B, ptrs, counts, H, fo, sg, start,
                                                  stop))
+        for _ in range(B):
+            self._held.append(keep)
+
+    def submit_layers_bundle(self, seeds_list, layer_sizes, rng_seeds):
+        """Queues len(seeds_list) layer-wise mini-batches made as one bundle
+        (Graph.sample_layers_bundle, hg_pipeline_submit_layers); next()
+        returns them one by one, in order."""
+        g = self.graph
+        T = g.T
+        B = len(seeds_list)
+        if len(rng_seeds) != B:
+            raise ValueError("one rng seed per mini-batch")
+        keep = []
+        ptrs = (ctypes.c_void_p * max(B * T, 1))()
+        counts = (ctypes.c_int64 * max(B * T, 1))()
+        for b, seeds in enumerate(seeds_list):
+            if len(seeds) != T:
+                raise ValueError("one seed entry per node type")
+            for t, sd in enumerate(seeds):
+                if sd is None:
+                    continue
+                sd = _dev_i64(sd, g.device)
+                keep.append(sd)
+                counts[b * T + t] = sd.numel()
+                ptrs[b * T + t] = sd.data_ptr() if sd.numel() else None
+        H = len(layer_sizes)
+        flat = [int(k) for row in layer_sizes for k in row]
+        if len(flat) != H * T:
+            raise ValueError("layer_sizes must be [n_hops][n_ntypes]")
+        ls = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        sg = (ctypes.c_uint64 * max(B, 1))(*[int(x) & (2**64 - 1) for x in rng_seeds])
+        _check(load_library().hg_pipeline_submit_layers(self._h, B, ptrs, counts, H, ls, sg))
+        for _ in range(B):
+            self._held.append(keep)
+
+    def submit_edge_bundle(self, targets_list, fanouts, rng_seeds, n_neg: int = 0,
+                           exclude: int = HG_EXCLUDE_NONE, rev_etype=None, rev_eid=None):
+        """Queues len(targets_list) edge-seeded mini-batches made as one bundle
+        (Graph.sample_edge_bundle, hg_pipeline_submit_edges); next() returns
+        them one by one, in order."""
+        g = self.graph
+        R = g.R
+        B = len(targets_list)
+        if len(rng_seeds) != B:
+            raise ValueError("one rng seed per mini-batch")
+        keep = []
+        batches = (EdgeBatch * max(B, 1))()
+        for b, targets in enumerate(targets_list):
+            batches[b] = g._edge_batch(targets, n_neg, exclude, rev_etype, rev_eid, keep)
+        H = len(fanouts)
+        flat = [int(k) for row in fanouts for k in row]
+        if len(flat) != H * R:
+            raise ValueError("fanouts must be [n_hops][n_etypes]")
+        fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
+        sg = (ctypes.c_uint64 * max(B, 1))(*[int(x) & (2**64 - 1) for x in rng_seeds])
+        _check(load_library().hg_pipeline_submit_edges(self._h, B, batches, H, fo, sg))
         for _ in range(B):
             self._held.append(keep)
 

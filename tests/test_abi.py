@@ -54,4 +54,6 @@ def test_library_argument_checks_without_device(lib):
     assert hg._lib.hg_pipeline_create(None, 2, 4, None, 0, ctypes.byref(out)) == hg.HG_EINVAL
     assert hg._lib.hg_pipeline_submit(None, 1, None, None, 1, None, None, None, None) == hg.HG_EINVAL
     assert hg._lib.hg_pipeline_next(None, ctypes.byref(out)) == hg.HG_EINVAL
+    assert hg._lib.hg_pipeline_submit_layers(None, 1, None, None, 1, None, None) == hg.HG_EINVAL
+    assert hg._lib.hg_pipeline_submit_edges(None, 1, None, 1, None, None) == hg.HG_EINVAL
     hg._lib.hg_pipeline_destroy(None)
