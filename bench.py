@@ -29,7 +29,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 
 # Measured HBM traffic of the gather launches of one bundle of the default
-# run (academic workload, bundles of 16, 32 warm-up + 320 timed mini-batches):
+# run (academic workload, bundles of 16, 96 warm-up + 320 timed mini-batches):
 # FETCH_SIZE and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the
 # counters read for a 1 GiB device copy (profiles/gather_academic_traffic.md).
 # Counter collection runs one dispatch at a time, so a bundle's gather moves
@@ -37,17 +37,17 @@ HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 # the gather source, the workload, the batches and the bundle size it was
 # measured on.
 GATHER_TRAFFIC = {"source_sha256_16": "307d950537d4b4f1", "workload": 2, "steps": 320,
-                  "warmup": 32, "bundle": 16, "bytes_per_launch": 3989131815.2}
+                  "warmup": 96, "bundle": 16, "bytes_per_launch": 3987876718.7}
 
 
 # Measured HBM traffic of a whole mini-batch on the default batches (academic
-# workload, bundles of 16, 32 warm-up + 320 timed mini-batches): FETCH_SIZE and
+# workload, bundles of 16, 96 warm-up + 320 timed mini-batches): FETCH_SIZE and
 # WRITE_SIZE of every dispatch of this library's kernels (graph creation's
-# check aside), scaled as above, summed over the run and divided by its 355
+# check aside), scaled as above, summed over the run and divided by its 419
 # mini-batches (the bundled ones and the three single calls after the timed
 # region).  Valid only for the kernel and runtime sources it was measured on.
-STEP_TRAFFIC = {"sources_sha256_16": "5e7f63355b00054e", "workload": 2, "steps": 320, "warmup": 32,
-                "bundle": 16, "bytes_per_step": 349.1e6}
+STEP_TRAFFIC = {"sources_sha256_16": "4bc3bcef9182dd15", "workload": 2, "steps": 320, "warmup": 96,
+                "bundle": 16, "bytes_per_step": 348.97e6}
 
 
 def kernel_sources_digest():
@@ -327,7 +327,10 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=320)
-    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed mini-batches first (default: two bundles per worker, or "
+                         "two bundles with direct calls), so that every worker's workspace "
+                         "and memory pool have grown before the timed region")
     ap.add_argument("--workload", type=int, default=2,
                     help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
                          "5 gather-heavy academic")
@@ -357,6 +360,8 @@ def main():
         args.workers = 3
     if args.bundle is None:
         args.bundle = 16 if args.workers > 0 else 32
+    if args.warmup is None:
+        args.warmup = 2 * max(args.workers, 1) * max(1, args.bundle)
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)

@@ -82,10 +82,12 @@ typedef struct hg_etype_desc {
 /* Optional device allocator for the output arrays of hg_sample_blocks.
  * alloc returns NULL on failure (hg_sample_blocks then returns HG_ENOMEM and
  * releases what it took).  A NULL allocator means stream-ordered
- * hipMallocAsync / hipFreeAsync from the device's default pool.  Working
- * memory (a per-vertex map and bitmap, per-pair and per-edge scratch) belongs
- * to the graph handle: it comes from the device's pool, grows to the largest
- * call and is released by hg_destroy; concurrent calls each get their own. */
+ * allocations (hipMallocFromPoolAsync / hipFreeAsync) from the library's own
+ * pool on the device, which keeps memory freed into it reserved until the
+ * process ends.  Working memory (a per-vertex map and bitmap, per-pair and
+ * per-edge scratch) belongs to the graph handle: it comes from that pool,
+ * grows to the largest call and is returned to the pool by hg_destroy;
+ * concurrent calls each get their own. */
 typedef struct hg_allocator {
   void *ctx;
   void *(*alloc)(void *ctx, size_t bytes, hipStream_t stream);

@@ -235,10 +235,11 @@ struct LayerArgs {
   int32_t n_types, n_etypes;
   PairArrays pa;
   int64_t n_pairs;
+  // n_all in-edges of the frontier, numbered by the counting pass (pair p's
+  // in-edges are positions off[p] .. off[p+1]-1, CSC slots plo[p] ..); they
+  // are read from the CSC where they are needed, never written out
   int64_t n_all;
-  const int64_t *all_src;
-  const int64_t *all_eid;
-  const int32_t *all_dst_local;
+  int64_t *tile_pair;  // [n_keep_tiles + 1]: the last pair with off <= tile * kLayerTile
   // per node type, in a device table of the hop (see LayerTable)
   uint64_t *const *wt;        // [T] importance of every vertex of the type
   int64_t *const *cand;       // [T] the type's candidates, ascending
@@ -269,8 +270,10 @@ inline size_t layer_table_bytes(int32_t T) {
   return sizeof(int64_t) * (3 * size_t(T) + 2 * (size_t(T) + 1) + (size_t(T) + 1) / 2);
 }
 
-// Importance of every candidate: for each in-edge u -> v of the frontier
-// whose source is not in the frontier, wt[type(u)][u] += floor(2^32 / deg(v)^2).
+// The first pair of every kLayerTile-position tile of the in-edges (tile_pair),
+// then the importance of every candidate: for each in-edge u -> v of the
+// frontier whose source is not in the frontier, u is marked reached and
+// wt[type(u)][u] += floor(2^32 / deg(v)^2).
 hipError_t launch_lw_weights(const LayerArgs &A, hipStream_t stream);
 // Exclusive prefix of the candidates' importance per node type (three
 // launches: tile sums, one scan of the tile sums, apply); zeroes the

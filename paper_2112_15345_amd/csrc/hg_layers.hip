@@ -5,13 +5,16 @@
 // node type for the whole layer, with probability proportional to their
 // importance, and keeps every in-edge of the frontier from the next frontier.
 //
-// One hop, after the counting pass and the sampler have emitted every in-edge
-// of the frontier (fanout -1) and set the reached flag of every source:
-//  1. k_lw_weights : importance of every candidate (a source not in the
-//                    frontier): sum of floor(2^32 / deg(v)^2) over its edges
-//                    into the frontier, 64-bit atomics (exact in any order),
-//                    blocks over contiguous tiles of edges whose etypes are
-//                    resolved once per tile (as in the kept-edge scans);
+// One hop, after the counting pass has numbered every in-edge of the frontier
+// (fanout -1: pair p's in-edges are positions off[p] .. off[p+1]-1); no
+// sampler runs, and the edges are read from the CSC where needed:
+//  1. k_lw_tile_pairs, k_lw_weights : the first pair of every 512-position
+//                    tile; then the importance of every candidate (a source
+//                    not in the frontier, which is marked reached): sum of
+//                    floor(2^32 / deg(v)^2) over its edges into the frontier,
+//                    64-bit atomics (exact in any order), blocks over tiles of
+//                    positions whose etypes and pairs are staged in LDS once
+//                    per tile (as in the kept-edge scans);
 //  2. compaction   : (collect mode) the candidates of each type, ascending;
 //  3. k_lw_scan_*  : exclusive prefix of their importance per type
 //                    (reduce-then-scan over 512-candidate tiles);
@@ -74,7 +77,13 @@ __device__ __forceinline__ int64_t *kept_base_of(const LayerArgs &A) {
   return A.small + kSlotNew + A.n_types + A.n_etypes + 1;
 }
 
-// The etypes that a block's contiguous range [j0, j1) of emitted edges spans,
+// The in-edges of the frontier are never written out.  The counting pass
+// numbers them: pair p's in-edges are positions off[p] .. off[p+1]-1, at CSC
+// slots plo[p] + (i - off[p]); position i lies in the last pair with
+// off[p] <= i (empty pairs share the offset of the pair after them).  The
+// kernels below read the source of position i from the CSC where they need it.
+
+// The etypes that a block's contiguous range [j0, j1) of positions spans,
 // resolved once per block: their starts and what the per-edge work reads of
 // them.  A range over more than kTileSegs etypes leaves n = 0 and its edges
 // search the etype starts one by one.
@@ -83,6 +92,8 @@ struct TileSegs {
   int64_t start[kTileSegs + 1];
   const uint32_t *fbits[kTileSegs];  // frontier bits of the source type
   void *per_seg[kTileSegs];          // importance array of the source type, or source map
+  const int64_t *indices[kTileSegs];
+  uint8_t *reached[kTileSegs];       // reached flags of the source type
   int64_t pair_base[kTileSegs];
   int e0, n;
 };
@@ -109,55 +120,139 @@ __device__ void tile_segs_load(const LayerArgs &A, int64_t j0, int64_t j1, TileS
         T.per_seg[threadIdx.x] = A.wt[E.src_type];
       else
         T.per_seg[threadIdx.x] = E.src_map;
+      T.indices[threadIdx.x] = E.indices;
+      T.reached[threadIdx.x] = E.src_reached;
       T.pair_base[threadIdx.x] = A.hv.pair_base[e];
     }
   }
   __syncthreads();
 }
 
-// Segment of edge j in the block's table, from a hint not above it (edges of
-// one thread come in ascending order).
+// Segment of position j in the block's table, from a hint not above it (the
+// positions of one thread come in ascending order).
 __device__ __forceinline__ int tile_seg(const TileSegs &T, int s, int64_t j) {
   while (s + 1 < T.n && T.start[s + 1] <= j) ++s;
   return s;
 }
 
-// Blocks of 256 threads take tiles of kLwWeightTile emitted edges, each
-// thread every 256th edge of the tile.
+// What a position needs of its etype.
+struct SegView {
+  const uint32_t *fbits;
+  void *per_seg;
+  const int64_t *indices;
+  uint8_t *reached;
+  int64_t pair_base;
+};
+template <int kKind>
+__device__ __forceinline__ SegView seg_view(const LayerArgs &A, const TileSegs &T, int &s,
+                                            int64_t j) {
+  if (T.n > 0) {
+    s = tile_seg(T, s, j);
+    return SegView{T.fbits[s], T.per_seg[s], T.indices[s], T.reached[s], T.pair_base[s]};
+  }
+  const int e = find_segment(ebase_of(A), A.n_etypes, j);
+  const EtypeStatic &E = A.es[e];
+  return SegView{A.ts[E.src_type].fbits,
+                 kKind == 0 ? static_cast<void *>(A.wt[E.src_type]) : static_cast<void *>(E.src_map),
+                 E.indices, E.src_reached, A.hv.pair_base[e]};
+}
+
+// tile_pair[t] = the last pair p with off[p] <= t * kLwTile, for every tile t
+// of positions; tile_pair[n_tiles] = the last pair.  Each non-empty pair writes
+// the tiles that start inside it.
+__global__ __launch_bounds__(256) void k_lw_tile_pairs(LayerArgs A) {
+  for (int64_t p = gs_start(); p < A.n_pairs; p += gs_step()) {
+    const int64_t lo = A.pa.off[p], hi = A.pa.off[p + 1];
+    for (int64_t t = (lo + kLwTile - 1) / kLwTile; t * kLwTile < hi; ++t) A.tile_pair[t] = p;
+  }
+  if (gs_start() == 0) A.tile_pair[A.n_keep_tiles] = A.n_pairs - 1;
+}
+
+// The pairs of a block's positions [j0, j1) in LDS: from tile_pair of the tile
+// holding j0 to tile_pair of the tile after j1 - 1 (which may hold one pair
+// past j1).  More than kTilePairs pairs (runs of empty pairs) leave n = 0, and
+// each position then searches the pair offsets.
+constexpr int kTilePairs = 1024;
+template <int N>
+struct TilePairs {
+  int64_t off[N], plo[N], deg[N];
+};
+struct PairRange {
+  int64_t p0;
+  int n;
+};
+template <int N>
+__device__ PairRange tile_pairs_load(const LayerArgs &A, int64_t j0, int64_t j1,
+                                     TilePairs<N> &Q) {
+  const int64_t pa = A.tile_pair[j0 / kLwTile];
+  const int64_t pb = A.tile_pair[(j1 - 1) / kLwTile + 1];
+  const int n = pb - pa + 1 <= N ? int(pb - pa + 1) : 0;
+  for (int k = threadIdx.x; k < n; k += blockDim.x) {
+    Q.off[k] = A.pa.off[pa + k];
+    Q.plo[k] = A.pa.plo[pa + k];
+    Q.deg[k] = A.pa.pdeg[pa + k];
+  }
+  __syncthreads();
+  return PairRange{pa, n};
+}
+
+// Position j: its pair, its CSC slot and the pair's in-degree.
+struct EdgeAt {
+  int64_t p, slot, deg;
+};
+template <int N>
+__device__ __forceinline__ EdgeAt edge_at(const LayerArgs &A, const TilePairs<N> &Q,
+                                          const PairRange &R, int64_t j) {
+  if (R.n > 0) {
+    int lo = 0, hi = R.n;  // Q.off[lo] <= j
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (Q.off[mid] <= j)
+        lo = mid;
+      else
+        hi = mid;
+    }
+    return EdgeAt{R.p0 + lo, Q.plo[lo] + (j - Q.off[lo]), Q.deg[lo]};
+  }
+  int64_t lo = 0, hi = A.n_pairs;
+  while (hi - lo > 1) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (A.pa.off[mid] <= j)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  return EdgeAt{lo, A.pa.plo[lo] + (j - A.pa.off[lo]), A.pa.pdeg[lo]};
+}
+
+// Blocks of 256 threads take tiles of kLwWeightTile positions (whole scan
+// tiles), each thread every 256th position of the tile.
 constexpr int kLwWeightItems = 8;
 constexpr int64_t kLwWeightTile = 256 * kLwWeightItems;
-
-__device__ __forceinline__ void add_weight(uint64_t *wt, int64_t u, int64_t deg) {
-  const uint64_t w = layer_weight(deg);
-  if (w) atomicAdd(reinterpret_cast<unsigned long long *>(wt + u), (unsigned long long)w);
-}
+static_assert(kLwWeightTile % kLwTile == 0, "weight tiles are whole scan tiles");
 
 __global__ __launch_bounds__(256) void k_lw_weights(LayerArgs A) {
   __shared__ TileSegs T;
+  __shared__ TilePairs<kTilePairs> Q;
   const int64_t n_tiles = (A.n_all + kLwWeightTile - 1) / kLwWeightTile;
   for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
     const int64_t j0 = tile * kLwWeightTile;
     const int64_t j1 = j0 + kLwWeightTile < A.n_all ? j0 + kLwWeightTile : A.n_all;
     tile_segs_load<0>(A, j0, j1, T);
-    if (T.n > 0) {
-      int s = 0;
-      for (int64_t j = j0 + threadIdx.x; j < j1; j += 256) {
-        s = tile_seg(T, s, j);
-        const int64_t u = A.all_src[j];
-        if (in_frontier(T.fbits[s], u)) continue;
-        add_weight(static_cast<uint64_t *>(T.per_seg[s]), u,
-                   A.pa.pdeg[T.pair_base[s] + A.all_dst_local[j]]);
-      }
-    } else {
-      for (int64_t j = j0 + threadIdx.x; j < j1; j += 256) {
-        const int e = find_segment(ebase_of(A), A.n_etypes, j);
-        const EtypeStatic &E = A.es[e];
-        const int64_t u = A.all_src[j];
-        if (in_frontier(A.ts[E.src_type].fbits, u)) continue;
-        add_weight(A.wt[E.src_type], u, A.pa.pdeg[A.hv.pair_base[e] + A.all_dst_local[j]]);
-      }
+    const PairRange R = tile_pairs_load(A, j0, j1, Q);
+    int s = 0;
+    for (int64_t j = j0 + threadIdx.x; j < j1; j += 256) {
+      const SegView v = seg_view<0>(A, T, s, j);
+      const EdgeAt x = edge_at(A, Q, R, j);
+      const int64_t u = v.indices[x.slot];
+      if (in_frontier(v.fbits, u)) continue;
+      v.reached[u] = 1;  // a candidate
+      const uint64_t w = layer_weight(x.deg);
+      if (w)
+        atomicAdd(reinterpret_cast<unsigned long long *>(static_cast<uint64_t *>(v.per_seg) + u),
+                  (unsigned long long)w);
     }
-    __syncthreads();  // T is rebuilt for the next tile
+    __syncthreads();  // T and Q are rebuilt for the next tile
   }
 }
 
@@ -181,45 +276,65 @@ __device__ __forceinline__ ScanSeg<kKind> seg_of(const LayerArgs &A, int64_t til
   return ScanSeg<kKind>{0, 0, A.n_all};
 }
 
-// Value i of the scan; kind 1 reads the etype of edge i from the block's
-// table (hint s, ascending i) or, past kTileSegs etypes, searches for it.
+// Position i of a scan: its value (kind 0: the candidate's importance; kind 1:
+// whether the in-edge's source is in the next frontier) and, for kind 1, what
+// the apply pass writes of a kept edge.
+struct ScanItem {
+  int64_t v;
+  int64_t slot, dst, u;  // kind 1: CSC slot (edge ID), destination local ID, source
+  const int32_t *src_map;
+};
+
+// The pair table of a scan tile: kind 1 only.
 template <int kKind>
-__device__ __forceinline__ int64_t value_of(const LayerArgs &A, const ScanSeg<kKind> &S,
-                                            const TileSegs &T, int &s, int64_t i) {
-  if (i >= S.n) return 0;
-  if (kKind == 0) return int64_t(A.wt[S.seg][A.cand[S.seg][i]]);
-  const uint32_t *fbits;
-  if (T.n > 0) {
-    s = tile_seg(T, s, i);
-    fbits = T.fbits[s];
-  } else {
-    s = find_segment(ebase_of(A), A.n_etypes, i);
-    fbits = A.ts[A.es[s].src_type].fbits;
-  }
-  return in_frontier(fbits, A.all_src[i]) ? 1 : 0;
-}
+using ScanPairs = TilePairs<kKind == 1 ? kTilePairs : 1>;
 
 template <int kKind>
-__device__ __forceinline__ void scan_tile_segs(const LayerArgs &A, int64_t tile, TileSegs &T) {
+__device__ __forceinline__ ScanItem scan_item(const LayerArgs &A, const ScanSeg<kKind> &S,
+                                              const TileSegs &T, const ScanPairs<kKind> &Q,
+                                              const PairRange &R, int &s, int64_t i) {
+  ScanItem it{0, 0, 0, 0, nullptr};
+  if (i >= S.n) return it;
+  if (kKind == 0) {
+    it.v = int64_t(A.wt[S.seg][A.cand[S.seg][i]]);
+    return it;
+  }
+  const SegView sv = seg_view<1>(A, T, s, i);
+  const EdgeAt x = edge_at(A, Q, R, i);
+  it.u = sv.indices[x.slot];
+  it.v = in_frontier(sv.fbits, it.u) ? 1 : 0;
+  it.slot = x.slot;
+  it.dst = x.p - sv.pair_base;
+  it.src_map = static_cast<const int32_t *>(sv.per_seg);
+  return it;
+}
+
+// The block's etype and pair tables for a kind-1 tile.
+template <int kKind>
+__device__ __forceinline__ PairRange scan_tables(const LayerArgs &A, int64_t tile, TileSegs &T,
+                                                 ScanPairs<kKind> &Q) {
   if (kKind == 1) {
     const int64_t j0 = tile * kLwTile;
     const int64_t j1 = j0 + kLwTile < A.n_all ? j0 + kLwTile : A.n_all;
     tile_segs_load<1>(A, j0, j1, T);
+    return tile_pairs_load(A, j0, j1, Q);
   }
+  return PairRange{0, 0};
 }
 
 template <int kKind>
 __global__ __launch_bounds__(kLwThreads) void k_lw_scan_reduce(LayerArgs A) {
   __shared__ int64_t lds[8];
   __shared__ TileSegs T;
+  __shared__ ScanPairs<kKind> Q;
   const int64_t tile = blockIdx.x;
-  scan_tile_segs<kKind>(A, tile, T);
+  const PairRange R = scan_tables<kKind>(A, tile, T, Q);
   const ScanSeg<kKind> S = seg_of<kKind>(A, tile);
   const int64_t i0 = (tile - S.first_tile) * kLwTile + threadIdx.x * kLwItems;
   int64_t v = 0;
   int s = 0;
 #pragma unroll
-  for (int k = 0; k < kLwItems; ++k) v += value_of<kKind>(A, S, T, s, i0 + k);
+  for (int k = 0; k < kLwItems; ++k) v += scan_item<kKind>(A, S, T, Q, R, s, i0 + k).v;
   int64_t total;
   block_excl_scan_256(v, lds, &total);
   if (threadIdx.x == 0) A.tile_sum[tile] = total;
@@ -274,19 +389,18 @@ template <int kKind>
 __global__ __launch_bounds__(kLwThreads) void k_lw_scan_apply(LayerArgs A) {
   __shared__ int64_t lds[8];
   __shared__ TileSegs T;
+  __shared__ ScanPairs<kKind> Q;
   const int64_t tile = blockIdx.x;
-  scan_tile_segs<kKind>(A, tile, T);
+  const PairRange R = scan_tables<kKind>(A, tile, T, Q);
   const ScanSeg<kKind> S = seg_of<kKind>(A, tile);
   const int64_t i0 = (tile - S.first_tile) * kLwTile + threadIdx.x * kLwItems;
-  int64_t v[kLwItems];
-  int segs[kLwItems];
+  ScanItem it[kLwItems];
   int64_t sum = 0;
   int s = 0;
 #pragma unroll
   for (int k = 0; k < kLwItems; ++k) {
-    v[k] = value_of<kKind>(A, S, T, s, i0 + k);
-    segs[k] = s;
-    sum += v[k];
+    it[k] = scan_item<kKind>(A, S, T, Q, R, s, i0 + k);
+    sum += it[k].v;
   }
   int64_t total;
   int64_t pre = block_excl_scan_256(sum, lds, &total) +
@@ -300,16 +414,14 @@ __global__ __launch_bounds__(kLwThreads) void k_lw_scan_apply(LayerArgs A) {
         A.wt[S.seg][A.cand[S.seg][i]] = 0;  // clean for the next hop and call
       } else {
         A.pos[i] = pre;
-        if (v[k]) {
-          const int32_t *src_map = T.n > 0 ? static_cast<const int32_t *>(T.per_seg[segs[k]])
-                                           : A.es[segs[k]].src_map;
-          A.out_eid[pre] = A.all_eid[i];
-          A.out_dst_local[pre] = A.all_dst_local[i];
-          A.out_src_local[pre] = src_map[A.all_src[i]];
+        if (it[k].v) {
+          A.out_eid[pre] = it[k].slot;
+          A.out_dst_local[pre] = int32_t(it[k].dst);
+          A.out_src_local[pre] = it[k].src_map[it[k].u];
         }
       }
     }
-    pre += v[k];
+    pre += it[k].v;
   }
   if (kKind == 1 && tile == int64_t(gridDim.x) - 1 && threadIdx.x == kLwThreads - 1)
     A.pos[A.n_all] = pre;  // the last thread of the last tile ends past n_all
@@ -379,6 +491,7 @@ __global__ __launch_bounds__(256) void k_lw_indptr(LayerArgs A) {
 
 hipError_t launch_lw_weights(const LayerArgs &A, hipStream_t stream) {
   if (A.n_all <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_lw_tile_pairs, dim3(grid_for(A.n_pairs, 256)), dim3(256), 0, stream, A);
   hipLaunchKernelGGL(k_lw_weights, dim3(grid_for(A.n_all, kLwWeightTile)), dim3(256), 0, stream,
                      A);
   return hipGetLastError();

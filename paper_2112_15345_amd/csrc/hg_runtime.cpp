@@ -122,6 +122,45 @@ struct ETypeInfo {
 };
 
 // A device buffer that grows (stream-ordered) and is reused across calls.
+// The library's stream-ordered pool on a device, for the scratch buffers and
+// the default output arrays.  Memory freed into it stays reserved (release
+// threshold at its maximum): a call that needs no more than earlier calls maps
+// no new memory, where a pool that trims at each synchronisation would map
+// gigabytes again (tens of ms) whenever a call outgrows what it kept.  The pool
+// lives until the process ends, since blocks handles may outlive their graph.
+hipMemPool_t library_pool(int device) {
+  static std::mutex mu;
+  static std::map<int, hipMemPool_t> pools;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = pools.find(device);
+  if (it != pools.end()) return it->second;
+  hipMemPoolProps props{};
+  props.allocType = hipMemAllocationTypePinned;
+  props.handleTypes = hipMemHandleTypeNone;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = device;
+  hipMemPool_t pool = nullptr;
+  if (hipMemPoolCreate(&pool, &props) != hipSuccess) {
+    (void)hipGetLastError();
+    pool = nullptr;  // fall back to the device's default pool
+  } else {
+    uint64_t keep = UINT64_MAX;
+    if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep) != hipSuccess)
+      (void)hipGetLastError();
+  }
+  pools[device] = pool;
+  return pool;
+}
+
+// Stream-ordered allocation on the current device from the library's pool.
+hipError_t pool_alloc(void **p, size_t bytes, hipStream_t s) {
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return e;
+  hipMemPool_t pool = library_pool(device);
+  return pool ? hipMallocFromPoolAsync(p, bytes, pool, s) : hipMallocAsync(p, bytes, s);
+}
+
 struct Scratch {
   void *p = nullptr;
   size_t cap = 0;
@@ -134,7 +173,7 @@ struct Scratch {
     p = nullptr;
     cap = 0;
     const size_t want = align_up(std::max(bytes, bytes + bytes / 2));
-    if (hipMallocAsync(&p, want, s) != hipSuccess) {
+    if (pool_alloc(&p, want, s) != hipSuccess) {
       (void)hipGetLastError();
       p = nullptr;
       return false;
@@ -247,13 +286,25 @@ struct hg_blocks {
 
 namespace {
 
-// Output arrays of a blocks handle: the caller's allocator, or the device's
+// Pool requests of 1 MiB and more are rounded up to m * 2^k with m in 8..15
+// (at most 1/8 more): calls of similar size then reuse the blocks that earlier
+// calls freed instead of making the pool map new memory.
+size_t size_class(size_t bytes) {
+  if (bytes < (size_t(1) << 20)) return bytes;
+  int k = 0;
+  while ((bytes >> k) >= 16) ++k;
+  size_t m = bytes >> k;
+  if ((m << k) < bytes) ++m;
+  return m << k;
+}
+
+// Output arrays of a blocks handle: the caller's allocator, or the library's
 // stream-ordered pool.
 void *dev_alloc(hg_graph *g, size_t bytes, hipStream_t s) {
   bytes = align_up(bytes ? bytes : 1);
   if (g->has_alloc) return g->alloc.alloc(g->alloc.ctx, bytes, s);
   void *p = nullptr;
-  if (hipMallocAsync(&p, bytes, s) != hipSuccess) {
+  if (pool_alloc(&p, size_class(bytes), s) != hipSuccess) {
     (void)hipGetLastError();
     return nullptr;
   }
@@ -544,11 +595,9 @@ struct SampleRun {
   hg_status close_layer_edges();
   hg_status layer_hop(int32_t h, const HopView &hv, const HopView &nv, const PairArrays &pa,
                       int64_t P, int64_t S, const std::vector<int64_t> &nF,
-                      const std::vector<int64_t> &cbound, int64_t *gid_tmp,
-                      int64_t *indptr_all, int64_t *eid_all, int32_t *srcl_all,
-                      int32_t *dstl_all, int64_t **src_slot, std::vector<int64_t *> &src_out,
-                      bool inline_ptrs, uint64_t *cand, int64_t n_wave, int64_t n_chunks,
-                      int64_t n_hubs);
+                      const std::vector<int64_t> &cbound, int64_t *indptr_all,
+                      int64_t *eid_all, int32_t *srcl_all, int32_t *dstl_all,
+                      int64_t **src_slot, std::vector<int64_t *> &src_out, bool inline_ptrs);
 
   SampleRun(hg_graph *g_, hipStream_t s, int32_t H_, const int32_t *fo,
             const uint64_t *sig, int32_t n_sig, int32_t kb)
@@ -1007,18 +1056,16 @@ hg_status SampleRun::close_layer_edges() {
   return HG_OK;
 }
 
-// One layer-wise hop after its counting pass: every in-edge of the frontier
-// into scratch, the candidates' importance and their per-type lists, the
+// One layer-wise hop after its counting pass (which numbers every in-edge of
+// the frontier): the candidates' importance and their per-type lists, the
 // draws, the next frontier, and the kept in-edges into the block arrays.
 hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
                                const PairArrays &pa, int64_t P, int64_t S,
                                const std::vector<int64_t> &nF,
-                               const std::vector<int64_t> &cbound, int64_t *gid_tmp,
-                               int64_t *indptr_all, int64_t *eid_all, int32_t *srcl_all,
-                               int32_t *dstl_all, int64_t **src_slot,
-                               std::vector<int64_t *> &src_out, bool inline_ptrs,
-                               uint64_t *cand, int64_t n_wave, int64_t n_chunks,
-                               int64_t n_hubs) {
+                               const std::vector<int64_t> &cbound, int64_t *indptr_all,
+                               int64_t *eid_all, int32_t *srcl_all, int32_t *dstl_all,
+                               int64_t **src_slot, std::vector<int64_t *> &src_out,
+                               bool inline_ptrs) {
   hipError_t e;
   LayerArgs A{};
   A.hv = hv;
@@ -1064,10 +1111,7 @@ hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
   A.draw_threads = h_dbase[T];
   const int64_t scan_tiles = std::max(A.cand_tiles, A.n_keep_tiles) + 1;
   Carve ec;
-  int64_t *all_eid;
-  int32_t *all_dstl;
-  ec.add(&all_eid, S);
-  ec.add(&all_dstl, S);
+  ec.add(&A.tile_pair, A.n_keep_tiles + 1);
   ec.add(&A.pos, S + 1);
   Carve cc;
   for (int32_t t = 0; t < T; ++t) {
@@ -1087,19 +1131,16 @@ hg_status SampleRun::layer_hop(int32_t h, const HopView &hv, const HopView &nv,
   A.cand_tile = reinterpret_cast<const int64_t *>(dt + sizeof(void *) * 3 * size_t(T));
   A.draw_base = A.cand_tile + T + 1;
   A.draws = reinterpret_cast<const int32_t *>(A.draw_base + T + 1);
-  A.all_src = gid_tmp;
-  A.all_eid = all_eid;
-  A.all_dst_local = all_dstl;
-
-  // 1. every in-edge of the frontier (fanout -1); the sampler sets the reached
-  // flag of every source
+  // 1. the hop's source lists (the sampler's launch carries them in the other
+  // modes, and this mode launches no sampler: the in-edges of the frontier,
+  // numbered by the counting pass, are read from the CSC where needed)
+  if (inline_ptrs &&
+      (e = launch_store_ptrs(reinterpret_cast<void **>(src_slot),
+                             reinterpret_cast<void *const *>(src_out.data()), T, stream)) !=
+          hipSuccess)
+    return fail_device(e, "source lists");
+  // 2. importance of the candidates, which marks them reached
   reached_dirty = true;
-  if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
-                         dsigmas(), g->key_R, h, key_bits, gid_tmp, all_eid, all_dstl,
-                         indptr_all, src_slot, src_out.data(), inline_ptrs ? T : 0, X,
-                         stream)) != hipSuccess)
-    return fail_device(e, "sample");
-  // 2. importance of the candidates
   wt_dirty = true;
   if ((e = launch_lw_weights(A, stream)) != hipSuccess) return fail_device(e, "weights");
   // 3. the candidates of each type in ascending ID (region H+2 lists them)
@@ -1264,14 +1305,17 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     b->mem->ptrs.push_back(ob);
     last_src = src_out;
     last_bound = bound;
-    Carve ec;
-    int64_t *gid_tmp;
-    ec.add(&gid_tmp, S);
-    Carve cc;
-    uint64_t *cand;
-    cc.add(&cand, n_hubs * kCandCap);
-    if (!ec.in_scratch(ws->edges, stream) || !cc.in_scratch(ws->cand, stream))
-      return fail(HG_ENOMEM, "hop %d: edge scratch", h);
+    // the sampler's scratch (a layer-wise hop launches no sampler)
+    int64_t *gid_tmp = nullptr;
+    uint64_t *cand = nullptr;
+    if (!layer_sizes) {
+      Carve ec;
+      ec.add(&gid_tmp, S);
+      Carve cc;
+      cc.add(&cand, n_hubs * kCandCap);
+      if (!ec.in_scratch(ws->edges, stream) || !cc.in_scratch(ws->cand, stream))
+        return fail(HG_ENOMEM, "hop %d: edge scratch", h);
+    }
 
     // this hop's source lists (also the next hop's frontier): written by the
     // sampler launch itself for a few types, else by their own launches
@@ -1284,9 +1328,8 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
       return fail_device(e, "tables");
 
     if (layer_sizes) {
-      if ((st = layer_hop(h, hv, nv, pa, P, S, nF, cbound, gid_tmp, indptr_all, eid_all,
-                          srcl_all, dstl_all, src_slot, src_out, inline_ptrs, cand, n_wave,
-                          n_chunks, n_hubs)) != HG_OK)
+      if ((st = layer_hop(h, hv, nv, pa, P, S, nF, cbound, indptr_all, eid_all, srcl_all,
+                          dstl_all, src_slot, src_out, inline_ptrs)) != HG_OK)
         return st;
       for (int32_t t = 0; t < T; ++t) {
         const size_t k = size_t(h) * T + t;
