@@ -29,7 +29,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 
 # Measured HBM traffic of the gather launches of one bundle of the default
-# run (academic workload, bundles of 16, 96 warm-up + 320 timed mini-batches):
+# run (academic workload, bundles of 32, 128 warm-up + 320 timed mini-batches):
 # FETCH_SIZE and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the
 # counters read for a 1 GiB device copy (profiles/gather_academic_traffic.md).
 # Counter collection runs one dispatch at a time, so a bundle's gather moves
@@ -37,17 +37,17 @@ HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 # the gather source, the workload, the batches and the bundle size it was
 # measured on.
 GATHER_TRAFFIC = {"source_sha256_16": "307d950537d4b4f1", "workload": 2, "steps": 320,
-                  "warmup": 96, "bundle": 16, "bytes_per_launch": 3987876718.7}
+                  "warmup": 128, "bundle": 32, "bytes_per_launch": 7975580490.4}
 
 
 # Measured HBM traffic of a whole mini-batch on the default batches (academic
-# workload, bundles of 16, 96 warm-up + 320 timed mini-batches): FETCH_SIZE and
+# workload, bundles of 32, 128 warm-up + 320 timed mini-batches): FETCH_SIZE and
 # WRITE_SIZE of every dispatch of this library's kernels (graph creation's
-# check aside), scaled as above, summed over the run and divided by its 419
+# check aside), scaled as above, summed over the run and divided by its 451
 # mini-batches (the bundled ones and the three single calls after the timed
 # region).  Valid only for the kernel and runtime sources it was measured on.
-STEP_TRAFFIC = {"sources_sha256_16": "4bc3bcef9182dd15", "workload": 2, "steps": 320, "warmup": 96,
-                "bundle": 16, "bytes_per_step": 348.97e6}
+STEP_TRAFFIC = {"sources_sha256_16": "4bc3bcef9182dd15", "workload": 2, "steps": 320, "warmup": 128,
+                "bundle": 32, "bytes_per_step": 348.96e6}
 
 
 def kernel_sources_digest():
@@ -150,10 +150,11 @@ def drive_units(args, g, n_batches, direct, submit, account, gather):
     depth = max(args.depth or 2 * args.workers * B, B)
     pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=gather)
     queue = units + timed
-    state = {"next": 0, "outstanding": 0}
+    # no timed unit is submitted before the timed region starts
+    state = {"next": 0, "outstanding": 0, "limit": len(units)}
 
     def submit_more():
-        while state["next"] < len(queue):
+        while state["next"] < state["limit"]:
             first, last = queue[state["next"]]
             if state["outstanding"] + (last - first) > depth:
                 break
@@ -174,6 +175,8 @@ def drive_units(args, g, n_batches, direct, submit, account, gather):
         take(*u)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
+    state["limit"] = len(queue)
+    submit_more()
     for u in timed:
         for blocks in take(*u):
             account(blocks)
@@ -336,10 +339,10 @@ def main():
                          "5 gather-heavy academic")
     ap.add_argument("--workers", type=int, default=None,
                     help="pipeline worker threads (own streams); 0 = direct calls on one "
-                         "stream (default 3)")
+                         "stream (default 2)")
     ap.add_argument("--bundle", type=int, default=None,
                     help="mini-batches per launch sequence (the *_bundle calls, 1..32; "
-                         "default: 16 with workers, 32 with direct calls)")
+                         "default 32)")
     ap.add_argument("--depth", type=int, default=0,
                     help="mini-batches outstanding in the pipeline (default 2 x workers x "
                          "bundle)")
@@ -357,9 +360,9 @@ def main():
                          "mini-batches (hg_sample_layers_bundle)")
     args = ap.parse_args()
     if args.workers is None:
-        args.workers = 3
+        args.workers = 2
     if args.bundle is None:
-        args.bundle = 16 if args.workers > 0 else 32
+        args.bundle = 32
     if args.warmup is None:
         args.warmup = 2 * max(args.workers, 1) * max(1, args.bundle)
     if args.gpus != 1:
@@ -464,10 +467,11 @@ def main():
         depth = max(args.depth or 2 * args.workers * B, B)
         pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=feat_types)
         queue = units + timed_units
-        state = {"next": 0, "outstanding": 0}
+        # no timed unit is submitted before the timed region starts
+        state = {"next": 0, "outstanding": 0, "limit": len(units)}
 
         def submit_more():
-            while (state["next"] < len(queue) and
+            while (state["next"] < state["limit"] and
                    state["outstanding"] + len(queue[state["next"]]) <= depth):
                 u = queue[state["next"]]
                 pipe.submit_bundle([seeds[b] for b in u], fan, u, events=unit_events(u))
@@ -488,6 +492,8 @@ def main():
         torch.cuda.synchronize()
         log(f"warm-up done ({args.workers} workers, bundles of {B}, depth {depth})")
         t_start = time.perf_counter()
+        state["limit"] = len(queue)
+        submit_more()
         for u in timed_units:
             blist = take(u)
             account(u, blist, totals)
