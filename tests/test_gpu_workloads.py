@@ -67,18 +67,18 @@ def test_workload_parity(idx, batches):
 
 
 def test_workload_pipeline_launch():
-    """The academic workload as bench.py runs it by default: bundles of 16
-    mini-batches submitted to a pipeline of 3 worker streams (at most 96
-    outstanding), here the first three timed bundles (batches 32..79).  Every
+    """The academic workload as bench.py runs it by default: bundles of 32
+    mini-batches submitted to a pipeline of 2 worker streams (at most 128
+    outstanding), here the first three timed bundles (batches 128..223).  Every
     mini-batch comes back in order and equals its own single call (blocks and
     gathered bytes); the first and last of each bundle also equal the oracle."""
     wl, gen, g, host = workload_graph(2)
     fan = wl.fanout_matrix()
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
-    batches = list(range(32, 80))
-    bundles = [batches[i:i + 16] for i in range(0, len(batches), 16)]
+    batches = list(range(128, 224))
+    bundles = [batches[i:i + 32] for i in range(0, len(batches), 32)]
     seeds = {b: gpu_seeds(W.seeds_per_type(wl, b)) for b in batches}
-    pipe = hg.Pipeline(g, workers=3, capacity=96, gather=feat_types)
+    pipe = hg.Pipeline(g, workers=2, capacity=128, gather=feat_types)
     try:
         for u in bundles:
             pipe.submit_bundle([seeds[b] for b in u], fan, u)
