@@ -16,17 +16,23 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# The same source built with OpenMP: independent loops (the pairs of a hop,
+# the relabelled edges, the gathered rows) run on every host core.
+_LIB_OMP = os.path.join(_HERE, "liboracle_omp.so")
 
 OK, EINVAL, ENOMEM, EUNSUPPORTED = 0, -1, -2, -4
 
 
 def build(out: str = _LIB, extra_flags=(), src: str = _SRC) -> str:
-    """Compile oracle.c with gcc into a shared library (plain C11, -O2)."""
+    """Compile oracle.c with gcc into a shared library (plain C11, -O2); with
+    the default output also its OpenMP build (liboracle_omp.so)."""
     tmp = f"{out}.{os.getpid()}.tmp"  # concurrent builders never share a file
     cmd = ["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-I", _HERE, *extra_flags, src, "-o", tmp]
+           "-Wno-unknown-pragmas", "-I", _HERE, *extra_flags, src, "-o", tmp]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
+    if out == _LIB and not extra_flags and src == _SRC:
+        build(_LIB_OMP, extra_flags=("-fopenmp",))
     return out
 
 
@@ -97,6 +103,8 @@ def _bind(lib):
     lib.oracle_sample_layers.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P,
                                          ctypes.c_int32, _P, ctypes.c_uint64, ctypes.POINTER(_P)]
     lib.oracle_sample_layers.restype = ctypes.c_int
+    lib.oracle_threads.argtypes = []
+    lib.oracle_threads.restype = ctypes.c_int
     return lib
 
 
@@ -107,9 +115,19 @@ def load(path: str = _LIB) -> ctypes.CDLL:
     """Load (building first if absent) the oracle library at ``path``."""
     if path not in _lib_cache:
         if not os.path.exists(path):
-            build(path)
+            build(path, extra_flags=("-fopenmp",) if path == _LIB_OMP else ())
         _lib_cache[path] = _bind(ctypes.CDLL(path))
     return _lib_cache[path]
+
+
+def load_omp() -> ctypes.CDLL:
+    """The OpenMP build of the same source (every host core; same results)."""
+    return load(_LIB_OMP)
+
+
+def threads(lib=None) -> int:
+    """Threads the library's parallel loops use (1 for the plain build)."""
+    return int((lib or load()).oracle_threads())
 
 
 def _ptr(a: np.ndarray | None) -> int | None:

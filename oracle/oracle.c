@@ -41,6 +41,9 @@
 
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 /* ------------------------------------------------------------------ */
 /* Philox4x32-10.  Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As
@@ -339,42 +342,58 @@ static int run_hops(const oracle_ntype *ntypes, int32_t n_ntypes,
       int32_t k = fanouts[(int64_t)h * n_etypes + e];
       oedges *blk = &b->edges[(int64_t)h * n_etypes + e];
       blk->indptr = (int64_t *)malloc(sizeof(int64_t) * (size_t)(fn[t] + 1));
-      /* at most min(deg, k) per destination; total bounded by nnz */
-      int64_t cap = 0;
-      for (int64_t i = 0; i < fn[t]; ++i) {
-        int64_t deg = et->indptr[fr[t][i] + 1] - et->indptr[fr[t][i]];
-        cap += (k < 0 || deg <= k) ? deg : k;
-      }
-      sampled[e] = (raw_edge *)malloc(sizeof(raw_edge) * (size_t)(cap + 1));
-      if (!blk->indptr || !sampled[e]) {
+      if (!blk->indptr) {
         status = ORACLE_ENOMEM;
         break;
       }
+      /* the block's CSC: destination i keeps min(avail, k) edges (every one
+       * when k == -1), avail = its in-edges that are not excluded */
       blk->indptr[0] = 0;
-      int64_t cnt = 0;
+      for (int64_t i = 0; i < fn[t]; ++i) {
+        int64_t v = fr[t][i];
+        int64_t avail = et->indptr[v + 1] - et->indptr[v];
+        if (excl[e].n > 0)
+          for (int64_t j = et->indptr[v]; j < et->indptr[v + 1]; ++j)
+            if (find_sorted(excl[e].eids, excl[e].n, j) >= 0) --avail;
+        int64_t kept = (k < 0 || avail <= k) ? avail : k;
+        blk->indptr[i + 1] = blk->indptr[i] + kept;
+      }
+      int64_t cnt = blk->indptr[fn[t]];
+      sampled[e] = (raw_edge *)malloc(sizeof(raw_edge) * (size_t)(cnt + 1));
+      if (!sampled[e]) {
+        status = ORACLE_ENOMEM;
+        break;
+      }
+      /* every destination on its own; they share nothing, so an OpenMP build
+       * runs them in parallel (the paper bundles this step with OpenMP, Sec.
+       * 4.2.2), each writing its own slots of the block */
+      int pair_status = ORACLE_OK;
+#pragma omp parallel for schedule(dynamic, 8)
       for (int64_t i = 0; i < fn[t]; ++i) {
         int64_t v = fr[t][i];
         int64_t lo = et->indptr[v], hi = et->indptr[v + 1];
         int64_t *chosen = (int64_t *)malloc(sizeof(int64_t) * (size_t)(hi - lo + 1));
         int64_t nc = 0;
-        if (!chosen) {
-          status = ORACLE_ENOMEM;
-          break;
-        }
-        status = select_pair(sigma, h, e, lo, hi, k, key_bits, excl[e].eids,
-                             excl[e].n, chosen, &nc);
-        if (status != ORACLE_OK) {
-          free(chosen);
-          break;
-        }
-        for (int64_t c = 0; c < nc; ++c) {
-          sampled[e][cnt].src_gid = et->indices[chosen[c]];
-          sampled[e][cnt].dst_local = (int32_t)i;
-          sampled[e][cnt].eid = chosen[c];
-          ++cnt;
+        int st = chosen ? select_pair(sigma, h, e, lo, hi, k, key_bits, excl[e].eids,
+                                      excl[e].n, chosen, &nc)
+                        : ORACLE_ENOMEM;
+        if (st == ORACLE_OK && nc != blk->indptr[i + 1] - blk->indptr[i]) st = ORACLE_EINVAL;
+        if (st == ORACLE_OK) {
+          for (int64_t c = 0; c < nc; ++c) {
+            raw_edge *r = &sampled[e][blk->indptr[i] + c];
+            r->src_gid = et->indices[chosen[c]];
+            r->dst_local = (int32_t)i;
+            r->eid = chosen[c];
+          }
+        } else {
+#pragma omp atomic write
+          pair_status = st;
         }
         free(chosen);
-        blk->indptr[i + 1] = cnt;
+      }
+      if (pair_status != ORACLE_OK) {
+        status = pair_status;
+        break;
       }
       n_sampled[e] = cnt;
     }
@@ -454,6 +473,7 @@ static int run_hops(const oracle_ntype *ntypes, int32_t n_ntypes,
         status = ORACLE_ENOMEM;
         break;
       }
+#pragma omp parallel for schedule(static)
       for (int64_t j = 0; j < n; ++j) {
         int64_t g = sampled[e][j].src_gid;
         int64_t pos = find_gid_pos(ftab[s], fn[s], g);
@@ -651,10 +671,19 @@ int oracle_gather_rows(const void *feat, int64_t n_rows, int64_t row_bytes,
     return ORACLE_EINVAL;
   for (int64_t i = 0; i < n; ++i)
     if (ids[i] < 0 || ids[i] >= n_rows) return ORACLE_EINVAL;
+#pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i)
     memcpy((char *)out + i * row_bytes,
            (const char *)feat + ids[i] * row_bytes, (size_t)row_bytes);
   return ORACLE_OK;
+}
+
+int oracle_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
 }
 
 /* ------------------------------------------------------------------ */

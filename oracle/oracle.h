@@ -1,11 +1,15 @@
 /*
  * oracle.h -- TEST INFRASTRUCTURE ONLY.
  *
- * A plain, slow, single-threaded CPU reference for heterogeneous multi-hop
+ * A plain, slow CPU reference for heterogeneous multi-hop
  * fanout neighbour sampling, per-hop compaction into relabelled bipartite
  * blocks, and the gather of input-frontier features, as DistDGLv2 describes
  * them (arXiv 2112.15345: Sec. 3.2 "Mini-batch training", Sec. 4.2.2
  * "Distributed hybrid CPU/GPU sampling", Sec. 4.1.4 type-specific IDs).
+ *
+ * It is single-threaded as built for the tests; the same source built with
+ * OpenMP shares independent loops out among threads (see oracle_threads) and
+ * gives the same results.
  *
  * Only the test suite, the smoke check and the benchmark's CPU-baseline leg
  * may call it.  It shares no code, header, table or helper with the GPU
@@ -101,6 +105,12 @@ int oracle_blocks_input_nodes(const oracle_blocks *b, int32_t ntype,
 /* out[i] = bytes of row ids[i] of a table of n_rows rows of row_bytes. */
 int oracle_gather_rows(const void *feat, int64_t n_rows, int64_t row_bytes,
                        const int64_t *ids, int64_t n, void *out);
+
+/* Threads the sampling and gather loops use: 1 in the plain build; in the
+ * OpenMP build (the same source compiled with -fopenmp, where the pairs of a
+ * hop, the relabelled edges and the gathered rows are shared out among the
+ * threads) the OpenMP thread count. */
+int oracle_threads(void);
 
 
 /* ---- Edge-seeded mini-batches (link prediction; Sec. 4.2.1: the scheduler

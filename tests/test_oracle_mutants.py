@@ -32,8 +32,8 @@ MUTANTS = [
      "for (int64_t j = 0; j < fanout; ++j) out_eids[j] = all[deg - 1 - j].eid;"),
     ("kept edges left in key order", "qsort(out_eids, (size_t)fanout, sizeof(int64_t), cmp_i64);", ""),
     ("hop index shifted in sampling",
-     "status = select_pair(sigma, h, e, lo, hi, k, key_bits, excl[e].eids,",
-     "status = select_pair(sigma, h + 1, e, lo, hi, k, key_bits, excl[e].eids,"),
+     "int st = chosen ? select_pair(sigma, h, e, lo, hi, k, key_bits, excl[e].eids,",
+     "int st = chosen ? select_pair(sigma, h + 1, e, lo, hi, k, key_bits, excl[e].eids,"),
     ("frontier not removed from new vertices",
      "if (find_gid_pos(ftab[t], fn[t], srcs[j]) >= 0) continue;", ""),
     ("new vertices left unsorted",
@@ -41,8 +41,8 @@ MUTANTS = [
      "/* unsorted */\n      /* unique"),
     ("new vertices numbered from 0", "if (pos < 0) pos = fn[s] + find_sorted(",
      "if (pos < 0) pos = find_sorted("),
-    ("destination local ID off by one", "sampled[e][cnt].dst_local = (int32_t)i;",
-     "sampled[e][cnt].dst_local = (int32_t)(i + 1);"),
+    ("destination local ID off by one", "r->dst_local = (int32_t)i;",
+     "r->dst_local = (int32_t)(i + 1);"),
     ("repeated seeds accepted", "if (i > 0 && tmp[i] == tmp[i - 1]) bad = 1;", ""),
     ("gather reads the mirrored row", "(const char *)feat + ids[i] * row_bytes",
      "(const char *)feat + ids[n - 1 - i] * row_bytes"),
