@@ -14,7 +14,8 @@
  *    "host" pointers are read before the call returns.
  *  - All device work goes on the caller's `stream`.  hg_sample_blocks waits on
  *    that stream once per hop and once at the end, to size its outputs; the
- *    gathers are fully asynchronous.
+ *    gathers of blocks' input frontiers are fully asynchronous, and
+ *    hg_gather_rows waits once, to report IDs out of range.
  *  - Functions return hg_status; no C++ exception crosses this boundary.
  *    After a failure, hg_last_error() describes it (thread-local text, valid
  *    until the next call on the same thread).
@@ -113,8 +114,21 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
                     const hg_allocator *allocator, hipStream_t stream,
                     hg_graph **out);
 
-/* Releases the handle and its workspaces (synchronises the device). */
+/* Releases the handle and its workspaces: waits for the handle's outstanding
+ * work, frees its device memory, and leaves no HIP error pending on the
+ * calling thread.  Every stream that calls on the handle used must still
+ * exist, or have been passed to hg_retire_stream before it was destroyed. */
 void hg_destroy(hg_graph *graph);
+
+/* Detaches the graph's internal state from `stream` before the caller
+ * destroys that stream.  A call leaves a marker of its working memory on
+ * the stream it ran on, which the next call on another stream (or
+ * hg_destroy) waits for; a marker on a destroyed stream must not be waited
+ * for.  This waits for the graph's work on `stream` and drops those markers.
+ * No call on this graph may be running on `stream` meanwhile.  Leaves no HIP
+ * error pending.  HG_EINVAL for a NULL graph.  hg_pipeline_destroy does this
+ * for its own worker streams. */
+hg_status hg_retire_stream(hg_graph *graph, hipStream_t stream);
 
 /* Number of node types and edge types of a graph handle (either output may
  * be NULL). */
@@ -160,17 +174,26 @@ int32_t hg_blocks_num_hops(const hg_blocks *blocks);
  * hg_blocks_edges reports them one at a time.  HG_EINVAL for NULL arguments. */
 hg_status hg_blocks_edge_counts(const hg_blocks *blocks, int64_t *counts);
 
-/* Vertices of node type `ntype` in block `hop`: n_dst frontier vertices and
- * n_src source vertices; *src_gid: device int64 [n_src] whose first n_dst
- * entries are the frontier (local ID = position). Owned by the handle. */
+/* Vertices of node type `ntype` in block `hop` (Sec. 4.2.2: the frontier of
+ * a hop is the unique set of vertices its sampled edges reach, and it seeds
+ * the next hop; Sec. 4.2.1: compaction relabels the vertices of the
+ * sampled subgraph): n_dst frontier vertices and n_src source vertices;
+ * *src_gid: device int64 [n_src] whose first n_dst entries are the frontier
+ * (local ID = position), followed by the newly reached vertices in ascending
+ * ID.  Owned by the handle.  HG_EINVAL for a NULL handle, a hop outside
+ * [0, n_hops) or a node type out of range; any output pointer may be NULL. */
 hg_status hg_blocks_nodes(const hg_blocks *blocks, int32_t hop, int32_t ntype,
                           int64_t *n_dst, int64_t *n_src,
                           const int64_t **src_gid);
 
-/* Edges of edge type `etype` in block `hop`, all device, owned by the handle:
+/* Edges of edge type `etype` in block `hop` (Sec. 3.2: at most K sampled
+ * in-neighbours per destination; Sec. 4.2.1: compaction remaps the vertex
+ * IDs and edge IDs of the sampled subgraph), all device, owned by the handle:
  * indptr int64 [n_dst(dst_type) + 1] (block CSC by destination local ID),
  * src_local / dst_local int32 [n_edges] (COO with local IDs), eid int64
- * [n_edges] (edge IDs of the input graph).  Any output pointer may be NULL. */
+ * [n_edges] (edge IDs of the input graph, type-specific as in Sec. 4.1.4).
+ * HG_EINVAL for a NULL handle, a hop outside [0, n_hops) or an edge type out
+ * of range.  Any output pointer may be NULL. */
 hg_status hg_blocks_edges(const hg_blocks *blocks, int32_t hop, int32_t etype,
                           int64_t *n_edges, const int64_t **indptr,
                           const int32_t **src_local, const int32_t **dst_local,
@@ -182,9 +205,12 @@ hg_status hg_blocks_edges(const hg_blocks *blocks, int32_t hop, int32_t etype,
 hg_status hg_blocks_input_nodes(const hg_blocks *blocks, int32_t ntype,
                                 int64_t *n, const int64_t **gid);
 
-/* out[i, :] = feat_ntype[input_frontier[i], :], bits copied unchanged.
- * out: device, caller-owned, [n_input(ntype), dim] of the type's dtype.
- * HG_EINVAL for a featureless type.  Asynchronous on `stream`. */
+/* The feature copy of one node type (Sec. 4.2.1: the feature-copy stage
+ * needs the frontier of the input layer; Sec. 4.1.4: features are stored per
+ * node type): out[i, :] = feat_ntype[input_frontier[i], :], bits copied
+ * unchanged.  out: device, caller-owned, [n_input(ntype), dim] of the type's
+ * dtype.  HG_EINVAL for NULL arguments, blocks of another graph, a node type
+ * out of range or a featureless type.  Asynchronous on `stream`. */
 hg_status hg_gather_features(hg_graph *graph, const hg_blocks *blocks,
                              int32_t ntype, void *out, hipStream_t stream);
 
@@ -249,15 +275,23 @@ hg_status hg_sample_blocks_bundle(hg_graph *graph, int32_t n_batches,
 hg_status hg_blocks_features(const hg_blocks *blocks, int32_t ntype, int64_t *rows,
                              const void **feat);
 
-/* out[i, :] = feat_ntype[ids[i], :] for i < n (ids: device int64 [n]).
- * Asynchronous; an id outside [0, num_nodes) yields a zero row. */
+/* A pull of feature rows by vertex ID (Sec. 3.3: the KVStore's pull of
+ * vertex features; Sec. 4.1.4: IDs are type-specific):
+ * out[i, :] = feat_ntype[ids[i], :] for i < n.  ids: device int64 [n];
+ * out: device, caller-owned, [n, dim] of the type's dtype.  Waits for
+ * `stream` once (the kernel checks every ID on the device and the call reads
+ * the result back): HG_EINVAL when an ID lies outside [0, num_nodes) of the
+ * type (out then holds zero rows for those IDs and the other rows as
+ * gathered), for a featureless or out-of-range type, NULL pointers or n < 0.
+ * Concurrent calls on several streams are allowed. */
 hg_status hg_gather_rows(hg_graph *graph, int32_t ntype, const int64_t *ids,
                          int64_t n, void *out, hipStream_t stream);
 
 /* Releases a blocks handle (stream-ordered on the stream it was made on;
- * on the null stream for handles returned by hg_pipeline_next).  A handle
- * does not depend on its graph handle: it may be released after
- * hg_destroy (with a caller allocator, that allocator must still work). */
+ * on the null stream for handles returned by hg_pipeline_next), so that
+ * stream must still exist.  A handle does not depend on its graph handle: it
+ * may be released after hg_destroy (with a caller allocator, that allocator
+ * must still work).  Leaves no HIP error pending. */
 void hg_blocks_free(hg_blocks *blocks);
 
 /* A mini-batch pipeline (Sec. 4.2.1: mini-batches are generated ahead of
@@ -297,7 +331,8 @@ hg_status hg_pipeline_submit(hg_pipeline *pipe, int32_t n_batches,
 hg_status hg_pipeline_next(hg_pipeline *pipe, hg_blocks **out);
 
 /* Finishes the queued mini-batches, frees those not returned, stops the
- * workers and releases the streams. */
+ * workers, detaches the graph from their streams (hg_retire_stream) and
+ * destroys them.  Leaves no HIP error pending. */
 void hg_pipeline_destroy(hg_pipeline *pipe);
 
 /* ---- Edge-seeded mini-batches (link prediction) ----------------------------

@@ -31,7 +31,7 @@ _DTYPE_CODE = {torch.float32: HG_DT_F32, torch.float16: HG_DT_F16,
                torch.bfloat16: HG_DT_BF16}
 
 # Every entry point declared in include/hg.h.
-ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_sample_blocks", "hg_sample_blocks_ex",
+ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_retire_stream", "hg_sample_blocks", "hg_sample_blocks_ex",
                "hg_blocks_num_hops", "hg_blocks_nodes", "hg_blocks_edges",
                "hg_blocks_input_nodes", "hg_gather_features", "hg_gather_features_multi",
                "hg_gather_features_multi_timed", "hg_gather_rows",
@@ -90,6 +90,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     sig = {
         "hg_create": ([_P, _I32, _P, _I32, _P, _P, _PP], _I32),
         "hg_destroy": ([_P], None),
+        "hg_retire_stream": ([_P, _P], _I32),
         "hg_sample_blocks": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _PP], _I32),
         "hg_sample_blocks_ex": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _I32, _P, _PP], _I32),
         "hg_blocks_num_hops": ([_P], _I32),

@@ -320,14 +320,16 @@ hipError_t launch_check_etype(const int64_t *indptr, int64_t n_dst,
                               const int64_t *indices, int64_t nnz,
                               int64_t n_src, int32_t *err, hipStream_t stream);
 
-// Row gather: out[i] = table[ids[i]] (row_bytes bytes), zero row when out of
-// range.  Picks the widest vector width that divides row_bytes and the
+// Row gather: out[i] = table[ids[i]] (row_bytes bytes); a zero row when the
+// ID is out of range, which also sets kErrSeedRange in *err (when err is not
+// NULL).  Picks the widest vector width that divides row_bytes and the
 // alignment of both pointers.
 // With n_dev, the rows are min(*n_dev, n) (read on the device; n bounds them
 // and sizes the grid).
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
-                         hipStream_t stream, const int64_t *n_dev = nullptr);
+                         hipStream_t stream, const int64_t *n_dev = nullptr,
+                         int32_t *err = nullptr);
 
 // One row gather of launch_gather_multi.
 struct GatherJob {

@@ -369,8 +369,13 @@ void hg_pipeline_destroy(hg_pipeline *p) {
     if (kv.second.done) (void)hipEventDestroy(kv.second.done);
   }
   for (hipEvent_t e : p->free_events) (void)hipEventDestroy(e);
+  // the graph's workspaces (and its bundle graphs') last used by the workers
+  // hold events recorded on the worker streams: detach them before the
+  // streams go away
+  for (hipStream_t s : p->streams) (void)hg_retire_stream(p->g, s);
   for (hipStream_t s : p->streams) (void)hipStreamDestroy(s);
   (void)hipSetDevice(prev);
+  (void)hipGetLastError();
   delete p;
 }
 

@@ -208,7 +208,13 @@ struct Workspace {
   Scratch lw_weight;               // layer-wise calls: importance per vertex (zero between uses)
   Scratch lw_edges, lw_cand;       // layer-wise calls: every in-edge of a hop; candidates
   uint32_t epoch = 0;              // look-back launches so far (mod kEpochLimit)
+  // Recorded at the end of every call on that call's stream (`last`); the
+  // next call on another stream waits for it.  An event must never outlive
+  // the stream it was last recorded on (waiting on it afterwards reads the
+  // destroyed stream's state), so retire_stream() re-creates the events of a
+  // stream that is about to be destroyed.
   hipEvent_t done = nullptr;
+  hipStream_t last = nullptr;
   bool busy = false;
   bool poisoned = false;           // device state unknown: never reuse
 };
@@ -389,7 +395,7 @@ struct RegionLayout {
 
 void free_workspace(Workspace *w) {
   if (w->done) {
-    (void)hipEventSynchronize(w->done);
+    if (w->last) (void)hipEventSynchronize(w->done);
     (void)hipEventDestroy(w->done);
   }
   (void)hipFree(w->map);
@@ -411,6 +417,7 @@ void free_workspace(Workspace *w) {
   if (w->hsmall) (void)hipHostFree(w->hsmall);
   if (w->htab) (void)hipHostFree(w->htab);
   delete w;
+  clear_pending_error();
 }
 
 // n_new[T], then ebase[R+1], then the kept ebase[R+1] of layer-wise hops
@@ -484,8 +491,9 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
       return fail(HG_ENOMEM, "workspace allocation failed: %s", hipGetErrorString(e));
     }
     w->busy = true;
-  } else {
-    // the previous user may have run on another stream
+  } else if (w->last && w->last != stream) {
+    // the previous user ran on another stream (on the same stream, stream
+    // order is enough)
     if (hipStreamWaitEvent(stream, w->done, 0) != hipSuccess) {
       std::lock_guard<std::mutex> lk(g->mu);
       w->busy = false;
@@ -532,9 +540,75 @@ void release_workspace(hg_graph *g, Workspace *w, hipStream_t stream) {
     free_workspace(w);
     return;
   }
-  (void)hipEventRecord(w->done, stream);
+  if (hipEventRecord(w->done, stream) == hipSuccess) {
+    w->last = stream;
+  } else {
+    // no event to wait on: wait here, so that the next user finds it idle
+    clear_pending_error();
+    (void)hipStreamSynchronize(stream);
+    clear_pending_error();
+    w->last = nullptr;
+  }
   std::lock_guard<std::mutex> lk(g->mu);
   w->busy = false;
+}
+
+// Detaches the idle workspaces of g (and of its bundle graphs) from `stream`,
+// which the caller is about to destroy: their work on it is waited for and
+// their events, last recorded on it, are replaced by fresh ones (a workspace
+// whose event cannot be re-created is dropped).  Workspaces in use by a call
+// are left alone: no call may be running on a stream that is being retired.
+void retire_stream(hg_graph *g, hipStream_t stream) {
+  std::vector<hg_graph *> bundles;
+  std::vector<Workspace *> dropped;
+  {
+    std::lock_guard<std::mutex> lk(g->mu);
+    for (auto &kv : g->bundles) bundles.push_back(kv.second);
+    for (size_t i = 0; i < g->ws.size();) {
+      Workspace *w = g->ws[i];
+      if (w->busy || w->last != stream) {
+        ++i;
+        continue;
+      }
+      (void)hipEventSynchronize(w->done);
+      (void)hipEventDestroy(w->done);
+      w->done = nullptr;
+      w->last = nullptr;
+      if (hipEventCreateWithFlags(&w->done, hipEventDisableTiming) != hipSuccess) {
+        w->done = nullptr;
+        g->ws.erase(g->ws.begin() + ptrdiff_t(i));
+        dropped.push_back(w);
+        continue;
+      }
+      ++i;
+    }
+  }
+  for (Workspace *w : dropped) free_workspace(w);
+  for (hg_graph *v : bundles) retire_stream(v, stream);
+  clear_pending_error();
+}
+
+// Waits until the publish launch with flag value `seq` has copied the
+// readback slots of w into w->hsmall (it writes the flag word after them).
+// Every few hundred polls the stream is queried, so a failed kernel (whose
+// successors never run) ends the wait with its error.
+hipError_t wait_flag(const hg_graph *g, Workspace *w, uint64_t seq, hipStream_t stream) {
+  hipError_t e;
+  const int32_t n = int32_t(small_slots(g));
+  const volatile int64_t *flag = w->hsmall + n;
+  for (uint32_t i = 1; uint64_t(*flag) != seq; ++i) {
+    if ((i & 255) == 0) {
+      e = hipStreamQuery(stream);
+      if (e == hipSuccess) {
+        if (uint64_t(*flag) == seq) break;
+        return hipErrorUnknown;  // the stream drained without the flag
+      }
+      if (e != hipErrorNotReady) return e;
+      if (i >= (1u << 16)) std::this_thread::yield();  // a long kernel
+    }
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
+  return hipSuccess;
 }
 
 int64_t dtype_size(int32_t dt) {
@@ -673,24 +747,7 @@ struct SampleRun {
     if (e == hipSuccess && last) small_clean = true;
     return e;
   }
-  hipError_t wait_published(uint64_t seq) {
-    hipError_t e;
-    const int32_t n = int32_t(small_slots(g));
-    const volatile int64_t *flag = ws->hsmall + n;
-    for (uint32_t i = 1; uint64_t(*flag) != seq; ++i) {
-      if ((i & 255) == 0) {
-        e = hipStreamQuery(stream);
-        if (e == hipSuccess) {
-          if (uint64_t(*flag) == seq) break;
-          return hipErrorUnknown;  // the stream drained without the flag
-        }
-        if (e != hipErrorNotReady) return e;
-        if (i >= (1u << 16)) std::this_thread::yield();  // a long kernel
-      }
-    }
-    std::atomic_thread_fence(std::memory_order_acquire);
-    return hipSuccess;
-  }
+  hipError_t wait_published(uint64_t seq) { return wait_flag(g, ws, seq, stream); }
 
   hg_status check_flags(const char *where) {
     const int32_t err = int32_t(ws->hsmall[kSlotErr]);
@@ -1580,8 +1637,21 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
 
 void hg_destroy(hg_graph *g) {
   if (!g) return;
-  DeviceGuard dg(g->device);
-  free_graph(g);
+  {
+    DeviceGuard dg(g->device);
+    free_graph(g);
+  }
+  clear_pending_error();
+}
+
+hg_status hg_retire_stream(hg_graph *g, hipStream_t stream) {
+  if (!g) return fail(HG_EINVAL, "hg_retire_stream: graph is NULL");
+  {
+    DeviceGuard dg(g->device);
+    retire_stream(g, stream);
+  }
+  clear_pending_error();
+  return HG_OK;
 }
 
 }  // extern "C"
@@ -2294,8 +2364,28 @@ hg_status hg_gather_rows(hg_graph *g, int32_t ntype, const int64_t *ids,
   if (!ids || !out) return fail(HG_EINVAL, "hg_gather_rows: NULL ids or out");
   DeviceGuard dg(g->device);
   clear_pending_error();
-  hipError_t e = launch_gather(N.feat, N.num_nodes, N.row_bytes, ids, n, out, stream);
-  if (e != hipSuccess) return fail_hip(e, "gather");
+  // a workspace lends its readback slots: the kernel flags an ID out of range
+  // in the error slot, which is read back once the gather has run
+  Workspace *w = nullptr;
+  hg_status st = acquire_workspace(g, 0, stream, &w);
+  if (st != HG_OK) return st;
+  int64_t *err_slot = w->dsmall + kSlotErr;
+  const uint64_t seq = ++w->publish_seq;
+  hipError_t e = launch_gather(N.feat, N.num_nodes, N.row_bytes, ids, n, out, stream, nullptr,
+                               reinterpret_cast<int32_t *>(err_slot));
+  if (e == hipSuccess)
+    e = launch_publish(w->dsmall, w->hsmall, int32_t(small_slots(g)), seq, true, stream);
+  if (e == hipSuccess) e = wait_flag(g, w, seq, stream);
+  if (e != hipSuccess) {
+    w->poisoned = true;
+    release_workspace(g, w, stream);
+    return fail_hip(e, "gather");
+  }
+  const int32_t err = int32_t(w->hsmall[kSlotErr]);
+  release_workspace(g, w, stream);
+  if (err)
+    return fail(HG_EINVAL, "hg_gather_rows: an ID is outside [0, %lld) of node type %d",
+                static_cast<long long>(N.num_nodes), ntype);
   return HG_OK;
 }
 
@@ -2305,7 +2395,18 @@ hg_status hg_gather_features(hg_graph *g, const hg_blocks *b, int32_t ntype,
   if (b->g != g) return fail(HG_EINVAL, "hg_gather_features: blocks come from another graph");
   if (ntype < 0 || ntype >= g->T)
     return fail(HG_EINVAL, "hg_gather_features: node type %d out of range", ntype);
-  return hg_gather_rows(g, ntype, b->in_gid[ntype], b->in_n[ntype], out, stream);
+  const NTypeInfo &N = g->nt[ntype];
+  if (N.dtype == HG_DT_NONE || N.row_bytes <= 0)
+    return fail(HG_EINVAL, "hg_gather_features: node type %d has no features", ntype);
+  const int64_t n = b->in_n[ntype];
+  if (n == 0) return HG_OK;
+  if (!out) return fail(HG_EINVAL, "hg_gather_features: out is NULL");
+  // the input frontier holds valid IDs of the type by construction: no check
+  DeviceGuard dg(g->device);
+  clear_pending_error();
+  hipError_t e = launch_gather(N.feat, N.num_nodes, N.row_bytes, b->in_gid[ntype], n, out, stream);
+  if (e != hipSuccess) return fail_hip(e, "gather");
+  return HG_OK;
 }
 
 hg_status hg_gather_features_multi(hg_graph *g, const hg_blocks *b,
@@ -2364,6 +2465,7 @@ extern "C" {
 
 void hg_blocks_free(hg_blocks *b) {
   delete b;  // the arrays go with the last handle that shares them
+  clear_pending_error();
 }
 
 hg_status hg_debug_philox(const uint32_t *ctr, uint64_t key, int64_t n,

@@ -74,12 +74,33 @@ def test_bundle_random_heterographs():
 
 
 def test_bundle_academic_workload():
+    """Bundles of 4 and of 32 academic mini-batches: each equals its own
+    single call, and every mini-batch of both bundles equals the oracle
+    (blocks and gathered bytes)."""
     wl = W.WORKLOADS[2]
     gen = W.make_graph(wl, device="cuda")
     g = hg.Graph(list(zip(gen.num_nodes, gen.feats)), gen.etypes)
+    host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), check=False,
+                            lib=oracle.load_omp())
     fan = wl.fanout_matrix()
     seeds_list = [gpu_seeds(W.seeds_per_type(wl, b)) for b in (4, 5, 6, 7)]
     check_bundle(g, seeds_list, fan, [4, 5, 6, 7], len(fan))
+    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    for first, B in ((4, 4), (40, 32)):
+        batches = list(range(first, first + B))
+        say(f"academic bundle of {B}: batches {batches[0]}..{batches[-1]} against the oracle")
+        got = g.sample_bundle([gpu_seeds(W.seeds_per_type(wl, b)) for b in batches], fan,
+                              batches, gather="all")
+        for b, blocks in zip(batches, got):
+            seeds = W.seeds_per_type(wl, b)
+            ref = host.sample_blocks(seeds, fan, b)
+            diffs = compare(ref, result_dict(g, blocks), g.T, g.R, len(fan))
+            assert not diffs, f"batch {b}: " + "\n".join(diffs[:10])
+            for t in feat_types:
+                want = host.gather(t, ref["input"][t]).tobytes()
+                assert blocks.features(t).contiguous().view(torch.uint8).cpu().numpy() \
+                    .tobytes() == want, f"batch {b} type {t}: gathered bytes differ"
+        del got
 
 
 def test_bundle_errors():

@@ -49,13 +49,23 @@ def test_host_resident_features(idx, batches):
         outs = g.gather_features_all(blocks, featured)
         for t in featured:
             assert outs[t].cpu().numpy().tobytes() == host.gather(t, ref["input"][t]).tobytes()
-    # arbitrary rows, out-of-range ids give zero rows
+    # arbitrary rows by ID; an ID out of range is reported (HG_EINVAL), with
+    # the valid rows gathered and zero rows for the bad ones
     t = featured[0]
-    ids = torch.tensor([0, gen.num_nodes[t] - 1, 5, gen.num_nodes[t], -3], device="cuda")
-    x = g.gather_rows(t, ids).cpu().numpy()
     f = gen.host_ntypes()[t][1]
+    ok_ids = torch.tensor([0, gen.num_nodes[t] - 1, 5], device="cuda")
+    x = g.gather_rows(t, ok_ids).cpu().numpy()
+    assert x.tobytes() == f[[0, gen.num_nodes[t] - 1, 5]].tobytes()
+    ids = torch.tensor([0, gen.num_nodes[t] - 1, 5, gen.num_nodes[t], -3], device="cuda")
+    out = torch.empty((5, f.shape[1]), dtype=feats[t].dtype, device="cuda")
+    with pytest.raises(hg.HGError) as ex:
+        g.gather_rows(t, ids, out=out)
+    assert ex.value.status == hg.HG_EINVAL
+    x = out.cpu().numpy()
     assert x[:3].tobytes() == f[[0, gen.num_nodes[t] - 1, 5]].tobytes()
     assert not x[3:].view(np.uint8).any()
+    # the error does not stick: the next pull succeeds
+    assert g.gather_rows(t, ok_ids).cpu().numpy().tobytes() == f[[0, gen.num_nodes[t] - 1, 5]].tobytes()
 
 
 def test_pageable_host_features_refused():
