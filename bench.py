@@ -1,17 +1,26 @@
 """Benchmark: heterogeneous mini-batch generation on one MI355X.
 
-One step = one mini-batch through the whole path, in one library call
-(hg_sample_blocks_gather): multi-hop per-edge-type fanout sampling, per-hop
-compaction into relabelled blocks, and the gather of the input frontier's
-features for every node type that has them (DistDGLv2, arXiv 2112.15345,
-Sec. 3.2 and Sec. 4.2).  Graph, features and seeds are resident in HBM before
-the timed region.
+One step = one mini-batch through the whole path: multi-hop per-edge-type
+fanout sampling, per-hop compaction into relabelled blocks, and the gather of
+the input frontier's features for every node type that has them (DistDGLv2,
+arXiv 2112.15345, Sec. 3.2 and Sec. 4.2).  Graph, features and seeds are
+resident in HBM before the timed region.  Mini-batches run in bundles of
+--bundle (hg_sample_blocks_bundle), made by --workers pipeline worker streams
+or, with --workers 0, by direct calls on one stream.
 
-Prints one JSON line.  `value` is sampled edges per second over whole steps;
-the gathered feature rate, per-stage times, the roofline of the dominant
-kernel and the CPU oracle's rate on a bounded sample ride along.
+The default workload is the billion-edge single-GPU share (workload 3: 92M
+vertices, 1.2B edges, fanout [15, 10, 5], 4096 seeds).  Prints one JSON line:
+`value` is sampled edges per second over whole steps; beside it the gathered
+feature rate, the per-step spread, every stage's device time (from HIP events
+carried by the stages' own kernel launches), the HBM rates of sampling and
+compaction (algorithmic bytes and counted bytes), the sampler's random-key
+rate against the vector-ALU roof, the roofline of the dominant kernel, the
+oracle on every host core, and an element-wise check of timed mini-batches
+against the oracle.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload N]
+                    [--workers N] [--bundle B] [--task vertex|link|layers]
+    python bench.py --mode philox      # the sampler's key loop alone
 """
 from __future__ import annotations
 
@@ -28,26 +37,28 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 
-# Measured HBM traffic of the gather launches of one bundle of the default
-# run (academic workload, bundles of 32, 128 warm-up + 320 timed mini-batches):
-# FETCH_SIZE and WRITE_SIZE from two rocprofv3 --pmc passes, scaled by what the
-# counters read for a 1 GiB device copy (profiles/gather_academic_traffic.md).
-# Counter collection runs one dispatch at a time, so a bundle's gather moves
-# the same bytes with or without worker streams; the figure is valid only for
-# the gather source, the workload, the batches and the bundle size it was
-# measured on.
-GATHER_TRAFFIC = {"source_sha256_16": "307d950537d4b4f1", "workload": 2, "steps": 320,
-                  "warmup": 128, "bundle": 32, "bytes_per_launch": 7975580490.4}
+# The vector-ALU roof of the sampler's random keys.  MI355X: 256 CUs x 4 SIMDs
+# x 16 lanes at 2.4 GHz = 39.3e12 32-bit lane operations per second (a wave64
+# instruction occupies its SIMD for 4 cycles).  One Philox4x32-10 call of the
+# sampler (counter (g, 0, hop, etype), the lane-independent parts of rounds 0
+# and 1 in scalar registers) is 37 vector instructions (18 v_mad_u64_u32, 15
+# v_bitop3_b32, 4 v_xor_b32) and gives 4 keys; the hub loop adds 3 per call
+# (min, min3, compare) and 3 of loop control.
+VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+PHILOX_VALU_PER_CALL = 37
+PHILOX_LOOP_VALU_PER_CALL = 43
+PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 
+# Per-workload defaults (workers, bundle, steps): the launch that gives each
+# workload its best throughput on one MI355X.
+DEFAULTS = {1: (2, 32, 320), 2: (2, 32, 320), 3: (2, 2, 20), 4: (0, 8, 64), 5: (2, 8, 64)}
 
-# Measured HBM traffic of a whole mini-batch on the default batches (academic
-# workload, bundles of 32, 128 warm-up + 320 timed mini-batches): FETCH_SIZE and
-# WRITE_SIZE of every dispatch of this library's kernels (graph creation's
-# check aside), scaled as above, summed over the run and divided by its 451
-# mini-batches (the bundled ones and the three single calls after the timed
-# region).  Valid only for the kernel and runtime sources it was measured on.
-STEP_TRAFFIC = {"sources_sha256_16": "4bc3bcef9182dd15", "workload": 2, "steps": 320, "warmup": 128,
-                "bundle": 32, "bytes_per_step": 348.96e6}
+# HBM bytes counted by rocprofv3 (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, the
+# factors a 1 GiB device copy gives) per mini-batch, for the kernel sources and
+# launch they were measured on (profiles/ holds the runs).  Keyed by a digest
+# of the kernel and runtime sources, the workload and the bundle size; any
+# other run reports them as null.
+COUNTER_TRAFFIC = []
 
 
 def kernel_sources_digest():
@@ -55,116 +66,115 @@ def kernel_sources_digest():
     d = os.path.join(ROOT, "paper_2112_15345_amd", "csrc")
     h = hashlib.sha256()
     for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".hpp")) or f == "hg_runtime.cpp":
+        if f.endswith((".hip", ".hpp", ".cpp")):
             h.update(f.encode())
             h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def measured_step_traffic(args):
-    t = STEP_TRAFFIC
-    if args.host_features or (kernel_sources_digest(), args.workload, args.steps, args.warmup,
-                              args.bundle) != (t["sources_sha256_16"], t["workload"],
-                                               t["steps"], t["warmup"], t["bundle"]):
-        return None
-    return t["bytes_per_step"]
-
-
-def measured_gather_traffic(args):
-    import hashlib
-    src = os.path.join(ROOT, "paper_2112_15345_amd", "csrc", "hg_gather.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    t = GATHER_TRAFFIC
-    if (digest, args.workload, args.steps, args.warmup, args.bundle) != (
-            t["source_sha256_16"], t["workload"], t["steps"], t["warmup"], t["bundle"]):
-        return None
-    return t["bytes_per_launch"]
+def counter_traffic(workload, bundle, task="vertex"):
+    digest = kernel_sources_digest()
+    for t in COUNTER_TRAFFIC:
+        if (t["sources"], t["workload"], t["bundle"], t.get("task", "vertex")) == (
+                digest, workload, bundle, task):
+            return t
+    return None
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(gen, wl, first_batch, budget_s=12.0, max_batches=32):
-    """The oracle, single-threaded, on the host cores: whole mini-batches
-    (sampling, compaction, gather) of the same workload until ~budget_s."""
-    import oracle
-    t0 = time.perf_counter()
-    host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), check=False)
-    log(f"oracle host copy ready in {time.perf_counter() - t0:.1f}s")
-    fan = wl.fanout_matrix()
-    edges = 0
-    rows = 0
-    nbytes = 0
-    spent = 0.0
-    nb = 0
-    for b in range(first_batch, first_batch + max_batches):
-        seeds = __import__("workloads").seeds_per_type(wl, b)
-        t = time.perf_counter()
-        res = host.sample_blocks(seeds, fan, b)
-        for ti, (n, feat, row_bytes) in enumerate(host.ntypes):
-            if feat is not None:
-                x = host.gather(ti, res["input"][ti])
-                rows += x.shape[0]
-                nbytes += x.nbytes
-        spent += time.perf_counter() - t
-        edges += sum(v[3].size for v in res["edges"].values())
-        nb += 1
-        if spent >= budget_s:
-            break
-    return {"value": edges / spent, "unit": "sampled edges/s", "cores": 1, "kind": "oracle",
-            "sample": f"{nb} whole mini-batches (batches {first_batch}..{first_batch + nb - 1}: "
-                      f"sampling, compaction, gather of {rows} rows) in {spent:.2f} s",
-            "gathered_GBps": nbytes / spent / 1e9}
+def host_info():
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
 
 def pipeline_name(args):
     return f"{args.workers} worker streams" if args.workers else "direct calls"
 
 
-def drive_units(args, g, n_batches, direct, submit, account, gather):
-    """Warm-up then timed units of --bundle batch indices (first, last): with
-    --workers 0, direct(first, last) returns the unit's Blocks; otherwise
-    submit(pipe, first, last) queues the unit on a pipeline of --workers
-    worker streams (at most --depth, default 2 x workers x bundle, mini-batches
-    outstanding) and the Blocks come back in order.  account(blocks) runs on
-    every timed mini-batch.  Returns the timed region's wall time."""
+def percentiles(xs):
+    import numpy as np
+    if not xs:
+        return None, None, None
+    a = np.asarray(xs, dtype=np.float64)
+    return tuple(float(np.percentile(a, q)) for q in (10, 50, 90))
+
+
+# ---------------------------------------------------------------------------
+# Units of work: warm-up and timed
+
+def make_units(args, B):
+    """Warm-up and timed units (lists of batch indices).  Every unit size the
+    timed region uses is warmed up first, twice per worker stream, so that no
+    bundle graph, workspace or pool growth happens while timing; the warm-up
+    runs at least --warmup mini-batches.  Timed batches follow the warm-up."""
+    K = args.steps
+    timed_sizes = [B] * (K // B) + ([K % B] if K % B else [])
+    per_size = 2 * max(args.workers, 1)
+    warm_sizes = []
+    for size in sorted(set(timed_sizes), reverse=True):
+        warm_sizes += [size] * per_size
+    while sum(warm_sizes) < args.warmup:
+        warm_sizes.append(B)
+    units, b = [], 0
+    for size in warm_sizes:
+        units.append(list(range(b, b + size)))
+        b += size
+    warm_n = b
+    timed = []
+    for size in timed_sizes:
+        timed.append(list(range(b, b + size)))
+        b += size
+    return units, timed, warm_n
+
+
+def run_units(args, g, units, timed, direct, submit, account):
+    """Runs the warm-up units, then the timed ones between two device
+    synchronisations.  direct(unit) returns the unit's Blocks (--workers 0);
+    submit(pipe, unit) queues it on a pipeline of --workers streams (at most
+    --depth mini-batches outstanding; no timed unit is submitted before the
+    clock starts).  account(unit, blocks, t) runs on every returned timed unit
+    with the host time it came back.  Returns the timed region's wall time."""
     import torch
 
     import paper_2112_15345_amd as hg
 
-    B = max(1, args.bundle)
-    units = [(b, min(b + B, args.warmup)) for b in range(0, args.warmup, B)]
-    timed = [(b, min(b + B, n_batches)) for b in range(args.warmup, n_batches, B)]
     if args.workers == 0:
         for u in units:
-            direct(*u)
+            direct(u)
         torch.cuda.synchronize()
         t_start = time.perf_counter()
         for u in timed:
-            for blocks in direct(*u):
-                account(blocks)
-                del blocks
+            account(u, direct(u), time.perf_counter() - t_start)
         torch.cuda.synchronize()
         return time.perf_counter() - t_start
+    B = max(len(u) for u in timed + units)
     depth = max(args.depth or 2 * args.workers * B, B)
-    pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=gather)
+    pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=args.gather_types)
     queue = units + timed
-    # no timed unit is submitted before the timed region starts
     state = {"next": 0, "outstanding": 0, "limit": len(units)}
 
     def submit_more():
-        while state["next"] < state["limit"]:
-            first, last = queue[state["next"]]
-            if state["outstanding"] + (last - first) > depth:
-                break
-            submit(pipe, first, last)
-            state["outstanding"] += last - first
+        while (state["next"] < state["limit"] and
+               state["outstanding"] + len(queue[state["next"]]) <= depth):
+            u = queue[state["next"]]
+            submit(pipe, u)
+            state["outstanding"] += len(u)
             state["next"] += 1
 
-    def take(first, last):
+    def take(u):
         out = []
-        for _ in range(last - first):
+        for _ in u:
             out.append(pipe.next())
             state["outstanding"] -= 1
         submit_more()
@@ -172,28 +182,337 @@ def drive_units(args, g, n_batches, direct, submit, account, gather):
 
     submit_more()
     for u in units:
-        take(*u)
+        take(u)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     state["limit"] = len(queue)
     submit_more()
     for u in timed:
-        for blocks in take(*u):
-            account(blocks)
-            del blocks
+        blist = take(u)
+        account(u, blist, time.perf_counter() - t_start)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     pipe.close()
     return elapsed
 
 
+# ---------------------------------------------------------------------------
+# The vertex-seeded mini-batch (the default task)
+
+def step_bytes_model(g, nd, ns, ne):
+    """Algorithmic HBM bytes of sampling and compaction for one mini-batch:
+    per hop, with D frontier vertices, P (vertex, edge type) pairs, S kept
+    edges and U new vertices: 8 D (read the frontier) + 16 P (indptr pairs) +
+    8 S (read the kept sources) + 8 (P + R) (block CSC) + 16 S (edge ID and the
+    two local IDs) + 8 (D + U) (source lists)."""
+    total = 0
+    for h in range(nd.shape[0]):
+        D = int(nd[h].sum())
+        U = int(ns[h].sum()) - D
+        P = sum(int(nd[h, d]) for (_, d, _, _) in g.etypes)
+        S = int(ne[h].sum())
+        R = g.R
+        total += 8 * D + 16 * P + 8 * S + 8 * (P + R) + 16 * S + 8 * (D + U)
+    return total
+
+
+def oracle_check(args, wl, gen, fan, kept, cpu):
+    """The oracle's OpenMP build (the same oracle.c on every host core) on the
+    first timed mini-batches: their timing is the CPU baseline, and every block
+    array of the GPU's result must equal the oracle's; the gathered feature
+    bytes must equal the rows of the oracle's input frontier."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import workloads as W
+
+    t0 = time.perf_counter()
+    host_nt = [(n, None) for n in gen.num_nodes]
+    host = oracle.HostGraph(host_nt, gen.host_etypes(), check=False, lib=oracle.load_omp())
+    log(f"oracle host copy of the graph in {time.perf_counter() - t0:.1f}s")
+    threads = oracle.threads(host.lib)
+    spent, edges, checked, bad = 0.0, 0, [], []
+    for b, blocks in kept:
+        seeds = W.seeds_per_type(wl, b)
+        t = time.perf_counter()
+        ref = host.sample_blocks(seeds, fan, b)
+        spent += time.perf_counter() - t
+        edges += sum(v[3].size for v in ref["edges"].values())
+        ok = True
+        for h in range(len(fan)):
+            for ti in range(len(gen.num_nodes)):
+                n_dst, sg = blocks.nodes(h, ti)
+                if n_dst != ref["nodes"][(h, ti)][0] or \
+                        not np.array_equal(sg.cpu().numpy(), ref["nodes"][(h, ti)][1]):
+                    ok = False
+            for e in range(len(gen.etypes)):
+                for x, y in zip(blocks.edges(h, e), ref["edges"][(h, e)]):
+                    xn = x.cpu().numpy()
+                    if xn.dtype != y.dtype or not np.array_equal(xn, y):
+                        ok = False
+        for ti, f in enumerate(gen.feats):
+            if f is None:
+                continue
+            ids = torch.as_tensor(ref["input"][ti], device=f.device)
+            got = blocks.features(ti)
+            want = f.index_select(0, ids).to(got.device)
+            if not torch.equal(got.view(torch.uint8), want.view(torch.uint8)):
+                ok = False
+        checked.append(b)
+        if not ok:
+            bad.append(b)
+        log(f"oracle batch {b}: {'equal' if ok else 'DIFFERENT'} "
+            f"({time.perf_counter() - t:.1f}s on {threads} threads)")
+        if cpu and spent >= args.cpu_budget:
+            break
+    parity = {"batches": checked, "equal": not bad, "different": bad,
+              "what": "every block array (frontiers, source lists, CSC, COO local IDs, edge "
+                      "IDs) and every gathered feature byte, element by element"}
+    base = {"value": edges / spent if spent > 0 else None, "unit": "sampled edges/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"{len(checked)} whole timed mini-batches (batches {checked[0]}.."
+                      f"{checked[-1]}) of the same workload: sampling and compaction by the "
+                      f"OpenMP build of the oracle (pairs, relabel and gather loops on every "
+                      f"host core), {edges} sampled edges in {spent:.2f} s; the feature "
+                      f"gather is checked on the GPU against the oracle's input frontier "
+                      f"rather than timed on the host",
+            **host_info()}
+    return parity, base
+
+
+def vertex_main(args, wl, gen, g):
+    import numpy as np
+    import torch
+
+    import paper_2112_15345_amd as hg
+    import workloads as W
+
+    dev = g.device
+    fan = wl.fanout_matrix()
+    H = len(fan)
+    B = max(1, args.bundle)
+    units, timed, warm_n = make_units(args, B)
+    n_batches = warm_n + args.steps
+    seeds = [[None if s is None else torch.as_tensor(s, device=dev)
+              for s in W.seeds_per_type(wl, b)] for b in range(n_batches)]
+    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    args.gather_types = feat_types
+    row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
+    stage_ev = {u[0]: hg.StageEvents(H) for u in timed}
+
+    if args.copy_calibration_mb > 0:
+        # a copy of known size, untimed, for scaling the memory counters
+        src = torch.ones(args.copy_calibration_mb << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.copy_calibration_mb} MiB done")
+        del src, dst
+
+    def direct(u):
+        return g.sample_bundle([seeds[b] for b in u], fan, u, gather=feat_types,
+                               stage_events=stage_ev.get(u[0]))
+
+    def submit(pipe, u):
+        pipe.submit_bundle([seeds[b] for b in u], fan, u, stage_events=stage_ev.get(u[0]))
+
+    rec = []   # per timed unit: (unit, done_s, edges, rows_by_type, nd, ns, keys, ne)
+    kept = []  # (batch, Blocks) checked against the oracle afterwards
+
+    def account(u, blist, t_done):
+        nd = np.zeros((H, g.T), np.int64)
+        ns = np.zeros((H, g.T), np.int64)
+        ne = np.zeros((H, g.R), np.int64)
+        keys = None
+        rows = {t: 0 for t in feat_types}
+        for b, blocks in zip(u, blist):
+            d, s, k = blocks.counts()
+            nd += d
+            ns += s
+            keys = k  # a bundle's handles hold the bundle's totals
+            ne += np.asarray(blocks.edge_counts(), np.int64).reshape(H, g.R)
+            for t in feat_types:
+                rows[t] += blocks.num_input_nodes(t)
+            if len(kept) < args.check_batches:
+                kept.append((b, blocks))
+        rec.append((u, t_done, int(ne.sum()), rows, nd, ns, keys, ne))
+
+    log(f"warm-up: {warm_n} mini-batches in units of {sorted(set(len(u) for u in units))}; "
+        f"timed: {args.steps} in units of {B} ({pipeline_name(args)})")
+    elapsed = run_units(args, g, units, timed, direct, submit, account)
+    steps = args.steps
+    edges = sum(r[2] for r in rec)
+    gbytes = sum(n * row_bytes[t] for r in rec for t, n in r[3].items())
+    ms_per_step = elapsed / steps * 1e3
+    # per-step spread: the interval between successive units' returns
+    per_step, prev = [], 0.0
+    for u, t_done, *_ in rec:
+        per_step.append((t_done - prev) / len(u) * 1e3)
+        prev = t_done
+    p10, p50, p90 = percentiles(per_step)
+
+    # device time of every stage, from the events its own launches carried
+    stage_ms = {name: 0.0 for name in hg.STAGE_NAMES}
+    launches = {name: 0 for name in hg.STAGE_NAMES}
+    gather_ms = 0.0
+    for u in timed:
+        ev = stage_ev[u[0]]
+        for h in range(H):
+            for st, name in enumerate(hg.STAGE_NAMES):
+                stage_ms[name] += ev.stage_ms(h, st)
+                launches[name] += 1
+        gather_ms += ev.gather_ms()
+    sc_ms = sum(stage_ms.values())
+    alg_sc = sum(step_bytes_model(g, r[4], r[5], r[7]) for r in rec)
+    keys = sum(int(r[6].sum()) for r in rec)
+    g_alg = sum(n * (2 * row_bytes[t] + 8) for r in rec for t, n in r[3].items())
+    if args.host_features:
+        g_alg = gbytes  # the rows cross the host link once; that link is the roof
+
+    # the sampler's key loop alone, over as many keys as a timed step
+    hip_ev = hg.HipEvents(2)
+    n_groups = 64 * (1 << 22)
+    hg.bench_philox(1, 0, 0, 64 * 1024, 1000)  # first launch, untimed
+    cnt = hg.bench_philox(7, 1, 2, n_groups, 1 << 20, events=tuple(hip_ev.events))
+    torch.cuda.synchronize()
+    loop_ms = hip_ev.elapsed_ms(*hip_ev.events)
+    loop_keys_s = 4 * n_groups / (loop_ms / 1e3)
+    del cnt
+
+    # context for the peak: a plain 1 GiB device-to-device copy, best of 6
+    copy_gbps = None
+    if not args.host_features:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        best = None
+        for _ in range(6):
+            c0.record()
+            dst.copy_(src)
+            c1.record()
+            c1.synchronize()
+            ms = c0.elapsed_time(c1)
+            best = ms if best is None else min(best, ms)
+        copy_gbps = 2 * src.numel() / (best / 1e3) / 1e9
+        del src, dst
+
+    traffic = counter_traffic(args.workload, B)
+    peak = HOST_LINK_PEAK_GBS if args.host_features else HBM_PEAK_GBS
+    g_gbps = g_alg / (gather_ms / 1e3) / 1e9 if gather_ms > 0 else 0.0
+    gather = {"kernel": "k_gather_multi (all featured types, one launch per bundle)",
+              "achieved": g_gbps, "peak": peak, "unit": "GB/s", "frac": g_gbps / peak,
+              "bound": "host link" if args.host_features else "hbm",
+              "ms_per_step": gather_ms / steps,
+              "algorithmic_bytes_per_step": g_alg / steps,
+              "traffic_per_step": traffic["gather"] if traffic else None}
+    sample_s = stage_ms["sample"] / 1e3
+    philox = {"keys_per_step": keys / steps,
+              "keys_per_s": keys / sample_s if sample_s > 0 else None,
+              "peak_keys_per_s": PHILOX_PEAK_KEYS,
+              "frac": (keys / sample_s) / PHILOX_PEAK_KEYS if sample_s > 0 else None,
+              "loop_alone_keys_per_s": loop_keys_s,
+              "loop_alone_frac": loop_keys_s / PHILOX_PEAK_KEYS,
+              "peak_derivation": f"{VALU_LANE_OPS:.4g} lane-ops/s x 4 keys / "
+                                 f"{PHILOX_VALU_PER_CALL} vector instructions per call"}
+    sc = {"kernels": "counting pass, sampler, hub selection, compaction, relabel",
+          "ms_per_step": sc_ms / steps,
+          "stage_ms_per_step": {k: v / steps for k, v in stage_ms.items()},
+          "algorithmic_bytes_per_step": alg_sc / steps,
+          "algorithmic_GBps": alg_sc / (sc_ms / 1e3) / 1e9 if sc_ms > 0 else None,
+          "algorithmic_frac": alg_sc / (sc_ms / 1e3) / 1e9 / HBM_PEAK_GBS if sc_ms > 0 else None,
+          "counter_bytes_per_step": traffic["sample_compact"] if traffic else None,
+          "sampled_edges_per_s": edges / (sc_ms / 1e3) if sc_ms > 0 else None}
+    if traffic:
+        rate = traffic["sample_compact"] / (sc_ms / steps / 1e3) / 1e9
+        sc["counter_GBps"] = rate
+        sc["counter_frac"] = rate / HBM_PEAK_GBS
+        sc["counter_over_algorithmic"] = traffic["sample_compact"] / (alg_sc / steps)
+    # the roofline of the kernel with the most device time
+    per_kernel = dict(stage_ms, gather=gather_ms)
+    dominant = max(per_kernel, key=per_kernel.get)
+    if dominant == "sample":
+        n_l = launches["sample"]
+        achieved = keys / sample_s / 1e9
+        roofline = {"bound": "alu", "kernel": "k_sample (the sampler: random keys of every "
+                    "in-edge of a selecting pair, then the kept edges)",
+                    "achieved": achieved, "peak": PHILOX_PEAK_KEYS / 1e9, "unit": "Gkeys/s",
+                    "frac": achieved / (PHILOX_PEAK_KEYS / 1e9),
+                    "traffic": traffic["k_sample_per_launch"] if traffic else None,
+                    "algorithmic_per_launch": keys / n_l,
+                    "avg_launch_us": stage_ms["sample"] / n_l * 1e3,
+                    "peak_source": philox["peak_derivation"]}
+    elif dominant == "gather":
+        n_l = len(timed)
+        roofline = {"bound": gather["bound"], "kernel": gather["kernel"],
+                    "achieved": g_gbps, "peak": peak, "unit": "GB/s", "frac": g_gbps / peak,
+                    "traffic": traffic["gather_per_launch"] if traffic else None,
+                    "algorithmic_per_launch": g_alg / n_l,
+                    "avg_launch_us": gather_ms / n_l * 1e3}
+    else:
+        n_l = launches[dominant]
+        roofline = {"bound": "hbm", "kernel": f"{dominant} stage", "achieved": None,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": None, "traffic": None,
+                    "avg_launch_us": per_kernel[dominant] / n_l * 1e3}
+    roofline["device_copy_GBps"] = copy_gbps
+    result = {
+        "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
+        "value": edges / elapsed,
+        "unit": "sampled edges/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "warmup_run": warm_n,
+        "ms_per_step": ms_per_step,
+        "ms_per_step_p10": p10, "ms_per_step_p50": p50, "ms_per_step_p90": p90,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic (seeded generator shaped like the paper's workloads)",
+        "config": {"workload": wl.name, "workload_index": args.workload,
+                   "seeds_per_batch": wl.batch, "fanouts_per_hop": list(wl.fanouts),
+                   "node_types": len(gen.num_nodes), "edge_types": g.R,
+                   "edges_in_graph": int(sum(ix.numel() for _, _, _, ix in gen.etypes)),
+                   "parallelism": "single GPU",
+                   "features": "pinned host memory" if args.host_features else "HBM",
+                   "bundle": B, "pipeline": pipeline_name(args)},
+        "gathered_GBps": gbytes / elapsed / 1e9,
+        "sampled_edges_per_step": edges / steps,
+        "roofline": roofline,
+        "gather": gather,
+        "sample_compact": sc,
+        "philox": philox,
+    }
+    if not args.no_cpu_baseline or args.check_batches > 0:
+        parity, base = oracle_check(args, wl, gen, fan, kept, cpu=not args.no_cpu_baseline)
+        result["parity"] = parity
+        if not args.no_cpu_baseline:
+            result["cpu_baseline"] = base
+    print(json.dumps(result), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Link prediction and layer-wise tasks
+
+def drive_units(args, g, direct, submit, account):
+    units, timed, warm_n = make_units(args, max(1, args.bundle))
+
+    def acc(u, blist, _t):
+        for b in blist:
+            account(b)
+
+    elapsed = run_units(args, g, units, timed, lambda u: direct(u[0], u[-1] + 1),
+                        lambda pipe, u: submit(pipe, u[0], u[-1] + 1), acc)
+    return elapsed, warm_n
+
+
 def link_main(args, wl, gen, g):
     """Edge-seeded (link-prediction) mini-batches: targets of one forward
     relation, their endpoints as seeds, one negative per target, targets and
     their reverse edges excluded, the paper's link-prediction fanouts [25, 15]
-    per hop, every featured type gathered.  Bundles of --bundle mini-batches
-    (hg_sample_edge_blocks_bundle), made by --workers pipeline workers or by
-    direct calls on one stream."""
+    per hop, every featured type gathered."""
     import torch
 
     import paper_2112_15345_amd as hg
@@ -205,11 +524,11 @@ def link_main(args, wl, gen, g):
     link_et = gen.etype_names.index("cites") if "cites" in gen.etype_names else 0
     fan = [[k] * g.R for k in W.LINK_FANOUTS]
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    args.gather_types = feat_types
     row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
-    n_batches = args.warmup + args.steps
+    n_max = make_units(args, max(1, args.bundle))[2] + args.steps
     targets = [[None if x is None else torch.as_tensor(x, device=dev)
-                for x in W.link_targets(gen, b, link_et)] for b in range(n_batches)]
-
+                for x in W.link_targets(gen, b, link_et)] for b in range(n_max)]
     kw = dict(n_neg=W.LINK_NEG, exclude=exclude, rev_etype=rev_et, rev_eid=rev_eid)
 
     def direct(first, last):
@@ -229,12 +548,12 @@ def link_main(args, wl, gen, g):
             totals[1] += n
             totals[2] += n * row_bytes[t]
 
-    elapsed = drive_units(args, g, n_batches, direct, submit, account, feat_types)
+    elapsed, warm_n = drive_units(args, g, direct, submit, account)
     edges, rows, gbytes = totals
-    result = {
+    print(json.dumps({
         "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
         "value": edges / elapsed, "unit": "sampled edges/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup,
+        "steps": args.steps, "warmup": args.warmup, "warmup_run": warm_n,
         "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64",
         "data": "synthetic (seeded generator shaped like the paper's workloads)",
@@ -247,15 +566,12 @@ def link_main(args, wl, gen, g):
         "gathered_GBps": gbytes / elapsed / 1e9,
         "sampled_edges_per_step": edges / args.steps,
         "gathered_rows_per_step": rows / args.steps,
-    }
-    print(json.dumps(result), flush=True)
+    }), flush=True)
 
 
 def layers_main(args, wl, gen, g):
     """Layer-wise (LADIES) mini-batches: the workload's seeds, 512 draws per
-    node type in each of two hops, every featured type gathered.  Bundles of
-    --bundle mini-batches (hg_sample_layers_bundle), made by --workers
-    pipeline workers or by direct calls on one stream."""
+    node type in each of two hops, every featured type gathered."""
     import torch
 
     import workloads as W
@@ -263,10 +579,11 @@ def layers_main(args, wl, gen, g):
     dev = g.device
     sizes = [[k] * g.T for k in W.LAYER_SIZES]
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    args.gather_types = feat_types
     row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
-    n_batches = args.warmup + args.steps
+    n_max = make_units(args, max(1, args.bundle))[2] + args.steps
     seeds = [[None if s is None else torch.as_tensor(s, device=dev)
-              for s in W.seeds_per_type(wl, b)] for b in range(n_batches)]
+              for s in W.seeds_per_type(wl, b)] for b in range(n_max)]
 
     def direct(first, last):
         return g.sample_layers_bundle([seeds[b] for b in range(first, last)], sizes,
@@ -285,12 +602,12 @@ def layers_main(args, wl, gen, g):
             totals[1] += n
             totals[2] += n * row_bytes[t]
 
-    elapsed = drive_units(args, g, n_batches, direct, submit, account, feat_types)
+    elapsed, warm_n = drive_units(args, g, direct, submit, account)
     edges, rows, gbytes = totals
     result = {
         "metric": "kept edges/s + gathered feature GB/s per layer-wise mini-batch (1 GPU)",
         "value": edges / elapsed, "unit": "kept edges/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup,
+        "steps": args.steps, "warmup": args.warmup, "warmup_run": warm_n,
         "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64",
         "data": "synthetic (seeded generator shaped like the paper's workloads)",
@@ -305,10 +622,12 @@ def layers_main(args, wl, gen, g):
     }
     if not args.no_cpu_baseline:
         import oracle
-        host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), check=False)
+        host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), check=False,
+                                lib=oracle.load_omp())
         spent = 0.0
         cedges = nb = 0
-        for b in range(args.warmup, n_batches):
+        first = n_max - args.steps
+        for b in range(first, n_max):
             t = time.perf_counter()
             res = host.sample_layers(W.seeds_per_type(wl, b), sizes, b)
             for ti, (n, feat, _) in enumerate(host.ntypes):
@@ -320,55 +639,101 @@ def layers_main(args, wl, gen, g):
             if spent >= 10.0:
                 break
         result["cpu_baseline"] = {
-            "value": cedges / spent, "unit": "kept edges/s", "cores": 1, "kind": "oracle",
-            "sample": f"{nb} whole layer-wise mini-batches (batches {args.warmup}.."
-                      f"{args.warmup + nb - 1}: sampling, compaction, gather) in {spent:.2f} s"}
+            "value": cedges / spent, "unit": "kept edges/s", "cores": oracle.threads(host.lib),
+            "kind": "oracle",
+            "sample": f"{nb} whole layer-wise mini-batches (batches {first}..{first + nb - 1}: "
+                      f"sampling, compaction, gather) in {spent:.2f} s, OpenMP build",
+            **host_info()}
     print(json.dumps(result), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# The sampler's key loop alone
+
+def philox_main(args):
+    """The sampler's key loop (hg_bench_philox) over 2^30 key groups, timed by
+    HIP events carried by its launch: the measured rate of the random keys
+    beside the vector-ALU roof derived from the chip's unit counts."""
+    import torch
+
+    import paper_2112_15345_amd as hg
+
+    ev = hg.HipEvents(2)
+    n_groups = 1 << 30
+    hg.bench_philox(1, 0, 0, 64 * 1024, 1000)
+    rates = []
+    for rep in range(max(1, args.steps)):
+        hg.bench_philox(rep, 1, 2, n_groups, 1 << 20, events=tuple(ev.events))
+        torch.cuda.synchronize()
+        rates.append(4 * n_groups / (ev.elapsed_ms(*ev.events) / 1e3))
+    best = max(rates)
+    print(json.dumps({
+        "metric": "random keys/s of the sampler's key loop alone (1 GPU)",
+        "value": best, "unit": "keys/s", "n_gpus": 1, "steps": len(rates), "warmup": 1,
+        "higher_is_better": True, "dtype": "u32", "data": "synthetic",
+        "config": {"workload": "Philox4x32-10 edge keys of 2^32 edge IDs, one (seed, hop, edge "
+                               "type) line, candidate threshold 2^20"},
+        "roofline": {"bound": "alu", "achieved": best / 1e9, "peak": PHILOX_PEAK_KEYS / 1e9,
+                     "unit": "Gkeys/s", "frac": best / PHILOX_PEAK_KEYS, "traffic": None,
+                     "peak_source": f"{VALU_LANE_OPS:.4g} lane-ops/s x 4 keys / "
+                                    f"{PHILOX_VALU_PER_CALL} vector instructions per call",
+                     "loop_peak_Gkeys": VALU_LANE_OPS * 4 / PHILOX_LOOP_VALU_PER_CALL / 1e9},
+        "median_keys_per_s": sorted(rates)[len(rates) // 2],
+    }), flush=True)
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=320)
-    ap.add_argument("--warmup", type=int, default=None,
-                    help="untimed mini-batches first (default: two bundles per worker, or "
-                         "two bundles with direct calls), so that every worker's workspace "
-                         "and memory pool have grown before the timed region")
-    ap.add_argument("--workload", type=int, default=2,
-                    help="1 tiny, 2 academic (default), 3 billion-share, 4 knowledge graph, "
-                         "5 gather-heavy academic")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed mini-batches (default per workload: 20 for workload 3)")
+    ap.add_argument("--warmup", type=int, default=5,
+                    help="untimed mini-batches first, at least; every unit size the timed "
+                         "region uses is also warmed up twice per worker stream")
+    ap.add_argument("--workload", type=int, default=3,
+                    help="1 tiny, 2 academic, 3 billion-edge share (default), 4 knowledge "
+                         "graph, 5 gather-heavy academic")
     ap.add_argument("--workers", type=int, default=None,
                     help="pipeline worker threads (own streams); 0 = direct calls on one "
-                         "stream (default 2)")
+                         "stream (default per workload)")
     ap.add_argument("--bundle", type=int, default=None,
-                    help="mini-batches per launch sequence (the *_bundle calls, 1..32; "
-                         "default 32)")
+                    help="mini-batches per launch sequence (1..32; default per workload)")
     ap.add_argument("--depth", type=int, default=0,
                     help="mini-batches outstanding in the pipeline (default 2 x workers x "
                          "bundle)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--check-batches", type=int, default=None,
+                    help="timed mini-batches compared with the oracle (default 2 for workload "
+                         "3, else 8); 0 skips the check")
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="seconds of oracle time after which the check stops")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after warm-up (untimed), copy this many MiB device to device "
                          "once: a copy of known size for scaling memory counters")
     ap.add_argument("--host-features", action="store_true",
                     help="feature tables in pinned host memory, gathered over the host link "
                          "(zero-copy); the gather rate then includes that link")
-    ap.add_argument("--task", choices=("vertex", "link", "layers"), default="vertex",
-                    help="vertex: mini-batches from seed vertices (the default); link: "
-                         "edge-seeded link-prediction mini-batches "
-                         "(hg_sample_edge_blocks_bundle); layers: layer-wise LADIES "
-                         "mini-batches (hg_sample_layers_bundle)")
+    ap.add_argument("--task", choices=("vertex", "link", "layers"), default="vertex")
+    ap.add_argument("--mode", choices=("step", "philox"), default="step",
+                    help="step: mini-batches (default); philox: the sampler's key loop alone")
     args = ap.parse_args()
-    if args.workers is None:
-        args.workers = 2
-    if args.bundle is None:
-        args.bundle = 32
-    if args.warmup is None:
-        args.warmup = 2 * max(args.workers, 1) * max(1, args.bundle)
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
+    if args.mode == "philox":
+        if args.steps is None:
+            args.steps = 5
+        return philox_main(args)
+    dw, db, ds = DEFAULTS.get(args.workload, (2, 32, 320))
+    if args.workers is None:
+        args.workers = dw
+    if args.bundle is None:
+        args.bundle = db
+    if args.steps is None:
+        args.steps = ds
+    if args.check_batches is None:
+        args.check_batches = 2 if args.workload == 3 else 8
 
     import torch
 
@@ -391,217 +756,7 @@ def main():
         return link_main(args, wl, gen, g)
     if args.task == "layers":
         return layers_main(args, wl, gen, g)
-    fan = wl.fanout_matrix()
-    n_batches = args.warmup + args.steps
-    seeds = [[None if s is None else torch.as_tensor(s, device=dev)
-              for s in W.seeds_per_type(wl, b)] for b in range(n_batches)]
-    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
-    row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
-
-    if args.copy_calibration_mb > 0:
-        # a copy of known size, untimed, for scaling the memory counters
-        src = torch.ones(args.copy_calibration_mb << 20, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"calibration copy of {args.copy_calibration_mb} MiB done")
-        del src, dst
-
-    # HIP events recorded by the gather kernels themselves (on their stream)
-    hip_events = hg.HipEvents(2 * args.steps)
-    events = {args.warmup + i: (hip_events.events[2 * i], hip_events.events[2 * i + 1])
-              for i in range(args.steps)}
-    gather_rec = []
-    B = max(1, args.bundle)
-    # units of work: bundles of B consecutive mini-batches (warm-up and timed
-    # mini-batches never share a bundle); a unit's events time its gather
-    units = [list(range(b, min(b + B, args.warmup))) for b in range(0, args.warmup, B)]
-    timed_units = [list(range(b, min(b + B, n_batches)))
-                   for b in range(args.warmup, n_batches, B)]
-
-    def account(unit, blist, totals=None):
-        """Bookkeeping of a returned unit; gather bytes and events of timed ones."""
-        rows_all = {t: 0 for t in feat_types}
-        for blocks in blist:
-            e = blocks.total_edges()
-            if totals is not None:
-                totals[0] += e
-            for t in feat_types:
-                n = blocks.num_input_nodes(t)
-                rows_all[t] += n
-                if totals is not None:
-                    totals[1] += n
-                    totals[2] += n * row_bytes[t]
-        if unit[0] in events:
-            gather_rec.append((events[unit[0]][0], events[unit[0]][1], rows_all))
-
-    def unit_events(unit):
-        return events.get(unit[0])
-
-    totals = [0, 0, 0]
-    if args.workers == 0:
-        # direct calls on the current stream, one per unit
-        def run(unit):
-            if len(unit) == 1:
-                b = unit[0]
-                return [g.sample_blocks(seeds[b], fan, b, gather=feat_types,
-                                        events=unit_events(unit))]
-            return g.sample_bundle([seeds[b] for b in unit], fan, unit, gather=feat_types,
-                                   events=unit_events(unit))
-
-        for u in units:
-            account(u, run(u))
-        torch.cuda.synchronize()
-        log(f"warm-up done (direct calls, bundles of {B})")
-        t_start = time.perf_counter()
-        for u in timed_units:
-            blist = run(u)
-            account(u, blist, totals)
-            del blist
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t_start
-    else:
-        # the pipeline: units generated ahead by worker threads, each on its
-        # own stream, returned in order; at most `depth` mini-batches outstanding
-        depth = max(args.depth or 2 * args.workers * B, B)
-        pipe = hg.Pipeline(g, workers=args.workers, capacity=depth, gather=feat_types)
-        queue = units + timed_units
-        # no timed unit is submitted before the timed region starts
-        state = {"next": 0, "outstanding": 0, "limit": len(units)}
-
-        def submit_more():
-            while (state["next"] < state["limit"] and
-                   state["outstanding"] + len(queue[state["next"]]) <= depth):
-                u = queue[state["next"]]
-                pipe.submit_bundle([seeds[b] for b in u], fan, u, events=unit_events(u))
-                state["outstanding"] += len(u)
-                state["next"] += 1
-
-        def take(unit):
-            blist = []
-            for _ in unit:
-                blist.append(pipe.next())
-                state["outstanding"] -= 1
-            submit_more()
-            return blist
-
-        submit_more()
-        for u in units:
-            account(u, take(u))
-        torch.cuda.synchronize()
-        log(f"warm-up done ({args.workers} workers, bundles of {B}, depth {depth})")
-        t_start = time.perf_counter()
-        state["limit"] = len(queue)
-        submit_more()
-        for u in timed_units:
-            blist = take(u)
-            account(u, blist, totals)
-            del blist
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t_start
-        pipe.close()
-    edges, rows, gbytes = totals
-    ms_per_step = elapsed / args.steps * 1e3
-
-    # context for the roofline: the same gather with nothing else on the GPU
-    # (a few direct calls after the timed region, untimed)
-    iso = hg.HipEvents(2)
-    iso_ms, iso_bytes = 0.0, 0
-    for b in range(min(3, n_batches)):
-        torch.cuda.synchronize()
-        blocks = g.sample_blocks(seeds[b], fan, b, gather=feat_types,
-                                 events=(iso.events[0], iso.events[1]))
-        iso_ms += iso.elapsed_ms(iso.events[0], iso.events[1])
-        iso_bytes += sum(blocks.num_input_nodes(t) *
-                         (row_bytes[t] if args.host_features else 2 * row_bytes[t] + 8)
-                         for t in feat_types)
-        del blocks
-    iso_gbps = iso_bytes / (iso_ms / 1e3) / 1e9 if iso_ms > 0 else 0.0
-
-    # context for the peak: a plain 1 GiB device-to-device copy (torch's copy
-    # kernel), read + write bytes over its time, best of 5 (untimed region)
-    copy_gbps = None
-    if not args.host_features:
-        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        best = None
-        for _ in range(6):
-            c0.record()
-            dst.copy_(src)
-            c1.record()
-            c1.synchronize()
-            ms = c0.elapsed_time(c1)
-            best = ms if best is None else min(best, ms)
-        copy_gbps = 2 * src.numel() / (best / 1e3) / 1e9
-        del src, dst
-
-    # gather kernel (one launch per step for all feature types): algorithmic
-    # bytes per row = read its id (8) + read the row + write the row
-    g_ms = sum(hip_events.elapsed_ms(e0, e1) for e0, e1, _ in gather_rec)
-    g_alg = sum(n * (2 * row_bytes[t] + 8) for _, _, rows_t in gather_rec
-                for t, n in rows_t.items())
-    g_achieved = g_alg / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
-    if args.host_features:
-        # the rows cross the host link once; that link is the roof
-        g_alg = sum(n * row_bytes[t] for _, _, rows_t in gather_rec for t, n in rows_t.items())
-        g_achieved = g_alg / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
-    log(f"{args.steps} steps: {ms_per_step:.3f} ms/step, gather {g_ms / len(gather_rec):.4f} "
-        f"ms/launch, {g_achieved:.0f} GB/s algorithmic")
-
-    peak = HOST_LINK_PEAK_GBS if args.host_features else HBM_PEAK_GBS
-    result = {
-        "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
-        "value": edges / elapsed,
-        "unit": "sampled edges/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "int64",
-        "data": "synthetic (seeded generator shaped like the paper's workloads)",
-        "config": {"workload": wl.name, "workload_index": args.workload,
-                   "seeds_per_batch": wl.batch, "fanouts_per_hop": list(wl.fanouts),
-                   "node_types": len(gen.num_nodes), "edge_types": g.R,
-                   "edges_in_graph": int(sum(ix.numel() for _, _, _, ix in gen.etypes)),
-                   "parallelism": "single GPU",
-                   "features": "pinned host memory" if args.host_features else "HBM",
-                   "bundle": max(1, args.bundle),
-                   "pipeline": (f"{args.workers} worker streams" if args.workers
-                                else "direct calls")},
-        "gathered_GBps": gbytes / elapsed / 1e9,
-        "sampled_edges_per_step": edges / args.steps,
-        "gathered_rows_per_step": rows / args.steps,
-        "gather_kernel_ms_per_step": g_ms / args.steps,
-        "roofline": {"bound": "host link" if args.host_features else "hbm",
-                     "kernel": "k_gather_multi (feature gather, all types)",
-                     "achieved": g_achieved, "peak": peak, "unit": "GB/s",
-                     "frac": g_achieved / peak,
-                     "traffic": None if args.host_features else measured_gather_traffic(args),
-                     "algorithmic_bytes_per_launch": g_alg / max(len(gather_rec), 1),
-                     "avg_launch_us": g_ms / max(len(gather_rec), 1) * 1e3,
-                     "overlap": ("the gather launches of a bundle share the GPU with other "
-                                 "workers' sampling kernels; isolated_* is the same gather "
-                                 "with nothing else running") if args.workers > 1 else "none",
-                     "isolated_achieved": iso_gbps,
-                     "isolated_frac": iso_gbps / peak,
-                     "device_copy_GBps": copy_gbps},
-    }
-    step_bytes = measured_step_traffic(args)
-    if step_bytes is not None:
-        # every kernel of the step together: counted HBM bytes per mini-batch
-        # over the wall time per mini-batch
-        rate = step_bytes / (ms_per_step / 1e3) / 1e9
-        result["step_hbm"] = {"bytes_per_step": step_bytes, "achieved": rate, "unit": "GB/s",
-                              "frac": rate / HBM_PEAK_GBS,
-                              "of_device_copy": rate / copy_gbps if copy_gbps else None}
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(gen, wl, first_batch=args.warmup)
-    print(json.dumps(result), flush=True)
+    return vertex_main(args, wl, gen, g)
 
 
 if __name__ == "__main__":

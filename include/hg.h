@@ -174,6 +174,16 @@ int32_t hg_blocks_num_hops(const hg_blocks *blocks);
  * hg_blocks_edges reports them one at a time.  HG_EINVAL for NULL arguments. */
 hg_status hg_blocks_edge_counts(const hg_blocks *blocks, int64_t *counts);
 
+/* Sizes of every block in one call (any output may be NULL; all host,
+ * caller-owned): n_dst and n_src [n_hops * n_ntypes], hop-major, as
+ * hg_blocks_nodes reports them one at a time; keys [n_hops], the random keys
+ * the sampler evaluated in each hop (the in-degrees summed over every
+ * (vertex, edge type) pair that chose K of more than K available in-edges:
+ * Sec. 3.2 random choice, every candidate edge keyed once).  A handle of a
+ * bundle reports the bundle's key totals.  HG_EINVAL for a NULL handle. */
+hg_status hg_blocks_counts(const hg_blocks *blocks, int64_t *n_dst, int64_t *n_src,
+                           int64_t *keys);
+
 /* Vertices of node type `ntype` in block `hop` (Sec. 4.2.2: the frontier of
  * a hop is the unique set of vertices its sampled edges reach, and it seeds
  * the next hop; Sec. 4.2.1: compaction relabels the vertices of the
@@ -268,6 +278,44 @@ hg_status hg_sample_blocks_bundle(hg_graph *graph, int32_t n_batches,
                                   int32_t n_gather, hipEvent_t start, hipEvent_t stop,
                                   hipStream_t stream, hg_blocks **out);
 
+/* Device timestamps of the stages of a sampling call, for benchmarks.  For
+ * hop h < HG_MAX_TIMED_HOPS and stage s, start[h][s] / stop[h][s] (either may
+ * be NULL) are carried by the first and the last kernel launch of that stage
+ * (hipExtLaunchKernelGGL), so hipEventElapsedTime(start, stop) is the device
+ * time of the stage's own kernels; a stage that launches nothing records both
+ * events back to back.  The stages of one hop, in order: HG_STAGE_COUNT the
+ * counting pass (kept edges per (vertex, edge type) pair and their offsets;
+ * Sec. 3.2 at most K per pair), HG_STAGE_SAMPLE the sampler (the random choice
+ * among in-edges and the emission of kept edges), HG_STAGE_SELECT the
+ * selection of the K smallest keys of pairs with more candidate edges than
+ * one wavefront holds, HG_STAGE_COMPACT the new frontier (the unique set of
+ * reached vertices, Sec. 4.2.2) and HG_STAGE_RELABEL the local IDs of the
+ * kept edges (Sec. 4.2.1 compaction).  gather_start / gather_stop are carried
+ * by the feature gather launches.  The events belong to the caller, who
+ * creates them (with timing) and keeps them until they have completed. */
+#define HG_MAX_TIMED_HOPS 8
+#define HG_STAGE_COUNT 0
+#define HG_STAGE_SAMPLE 1
+#define HG_STAGE_SELECT 2
+#define HG_STAGE_COMPACT 3
+#define HG_STAGE_RELABEL 4
+#define HG_NUM_STAGES 5
+typedef struct hg_stage_events {
+  hipEvent_t start[HG_MAX_TIMED_HOPS][HG_NUM_STAGES];
+  hipEvent_t stop[HG_MAX_TIMED_HOPS][HG_NUM_STAGES];
+  hipEvent_t gather_start, gather_stop;
+} hg_stage_events;
+
+/* hg_sample_blocks_bundle with the stages' device timestamps (events may be
+ * NULL: then it is hg_sample_blocks_bundle without gather events).  For a
+ * bundle the stages cover all its mini-batches at once.  For benchmarks. */
+hg_status hg_sample_blocks_bundle_timed(hg_graph *graph, int32_t n_batches,
+                                        const int64_t *const *seeds, const int64_t *n_seeds,
+                                        int32_t n_hops, const int32_t *fanouts,
+                                        const uint64_t *rng_seeds, const int32_t *gather_ntypes,
+                                        int32_t n_gather, const hg_stage_events *events,
+                                        hipStream_t stream, hg_blocks **out);
+
 /* The rows gathered for node type `ntype` by hg_sample_blocks_gather:
  * *rows = n_input(ntype) and *feat = device [rows, dim] of the type's dtype,
  * owned by the handle; *rows = 0 and *feat = NULL when the type was not
@@ -322,6 +370,14 @@ hg_status hg_pipeline_submit(hg_pipeline *pipe, int32_t n_batches,
                              const int64_t *const *seeds, const int64_t *n_seeds,
                              int32_t n_hops, const int32_t *fanouts,
                              const uint64_t *rng_seeds, hipEvent_t start, hipEvent_t stop);
+
+/* hg_pipeline_submit with the stages' device timestamps of the bundle
+ * (copied; see hg_sample_blocks_bundle_timed).  The events must stay valid
+ * until the mini-batches have been returned. */
+hg_status hg_pipeline_submit_timed(hg_pipeline *pipe, int32_t n_batches,
+                                   const int64_t *const *seeds, const int64_t *n_seeds,
+                                   int32_t n_hops, const int32_t *fanouts,
+                                   const uint64_t *rng_seeds, const hg_stage_events *events);
 
 /* Waits for the oldest outstanding mini-batch.  On success *out owns its
  * blocks and gathered features (hg_blocks_free) and all of its device work
@@ -476,6 +532,19 @@ const char *hg_last_error(void);
  * sampler uses so that it can be checked on its own. */
 hg_status hg_debug_philox(const uint32_t *ctr, uint64_t key, int64_t n,
                           uint32_t *out, hipStream_t stream);
+
+/* The sampler's key loop on its own, for measuring its rate (the roof of the
+ * selection among in-edges when keys must be computed for every candidate
+ * edge, Sec. 3.2 random choice of at most K neighbours): evaluates the keys
+ * of key groups g = 0 .. n_groups-1 of (rng_seed, hop, etype) -- the keys of
+ * edge IDs 0 .. 4 * n_groups - 1, as hg_sample_blocks defines them -- with the
+ * sampler's own code, and adds the number of keys <= lim to *count (device
+ * uint64, caller-owned, not cleared).  n_groups: a positive multiple of 64,
+ * at most 2^32.  start / stop (either may be NULL) are carried by the launch,
+ * so hipEventElapsedTime(start, stop) is its device time.  Asynchronous. */
+hg_status hg_bench_philox(uint64_t rng_seed, int32_t hop, int32_t etype, int64_t n_groups,
+                          uint32_t lim, uint64_t *count, hipEvent_t start, hipEvent_t stop,
+                          hipStream_t stream);
 
 #ifdef __cplusplus
 }

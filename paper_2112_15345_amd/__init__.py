@@ -42,9 +42,14 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_retire_stream", "hg_sample_blocks"
                "hg_blocks_edge_pairs", "hg_sample_layers", "hg_blocks_edge_counts",
                "hg_sample_edge_blocks_bundle", "hg_sample_layers_bundle",
                "hg_pipeline_submit_layers", "hg_pipeline_submit_edges",
-               "hg_blocks_free", "hg_last_error", "hg_debug_philox")
+               "hg_blocks_free", "hg_last_error", "hg_debug_philox", "hg_bench_philox",
+               "hg_sample_blocks_bundle_timed", "hg_pipeline_submit_timed", "hg_blocks_counts")
 
 HG_MAX_NEG = 64
+HG_MAX_TIMED_HOPS = 8
+HG_STAGE_COUNT, HG_STAGE_SAMPLE, HG_STAGE_SELECT, HG_STAGE_COMPACT, HG_STAGE_RELABEL = range(5)
+HG_NUM_STAGES = 5
+STAGE_NAMES = ("count", "sample", "select", "compact", "relabel")
 HG_EXCLUDE_NONE, HG_EXCLUDE_SELF, HG_EXCLUDE_REVERSE = 0, 1, 2
 
 
@@ -63,6 +68,12 @@ class ETypeDesc(ctypes.Structure):
     _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
                 ("nnz", ctypes.c_int64), ("indptr", ctypes.c_void_p),
                 ("indices", ctypes.c_void_p)]
+
+
+class StageEventsStruct(ctypes.Structure):
+    _fields_ = [("start", (ctypes.c_void_p * HG_NUM_STAGES) * HG_MAX_TIMED_HOPS),
+                ("stop", (ctypes.c_void_p * HG_NUM_STAGES) * HG_MAX_TIMED_HOPS),
+                ("gather_start", ctypes.c_void_p), ("gather_stop", ctypes.c_void_p)]
 
 
 class EdgeBatch(ctypes.Structure):
@@ -114,6 +125,12 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_blocks_free": ([_P], None),
         "hg_last_error": ([], ctypes.c_char_p),
         "hg_debug_philox": ([_P, ctypes.c_uint64, _I64, _P, _P], _I32),
+        "hg_sample_blocks_bundle_timed": ([_P, _I32, _P, _P, _I32, _P, _P, _P, _I32, _P, _P,
+                                           _P], _I32),
+        "hg_blocks_counts": ([_P, _P, _P, _P], _I32),
+        "hg_pipeline_submit_timed": ([_P, _I32, _P, _P, _I32, _P, _P, _P], _I32),
+        "hg_bench_philox": ([ctypes.c_uint64, _I32, _I32, _I64, ctypes.c_uint32, _P, _P, _P, _P],
+                            _I32),
         "hg_sample_edge_blocks": ([_P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _PP], _I32),
         "hg_blocks_seeds": ([_P, _I32, _PI64, _PP], _I32),
         "hg_blocks_edge_pairs": ([_P, _I32, _PI64, _PP, _PP, _PI64, _PP], _I32),
@@ -232,6 +249,19 @@ class Blocks:
         buf = (ctypes.c_int64 * max(self.n_hops * R, 1))()
         _check(load_library().hg_blocks_edge_counts(self._h, buf))
         return [[buf[h * R + e] for e in range(R)] for h in range(self.n_hops)]
+
+    def counts(self):
+        """(n_dst, n_src, keys): numpy int64 [n_hops, T], [n_hops, T] and
+        [n_hops] (keys: the random keys the sampler evaluated per hop; a
+        bundle's handles hold the bundle's totals)."""
+        import numpy as np
+        H, T = self.n_hops, self.graph.T
+        nd = np.zeros(max(H * T, 1), np.int64)
+        ns = np.zeros(max(H * T, 1), np.int64)
+        ky = np.zeros(max(H, 1), np.int64)
+        _check(load_library().hg_blocks_counts(self._h, nd.ctypes.data, ns.ctypes.data,
+                                               ky.ctypes.data))
+        return nd[:H * T].reshape(H, T), ns[:H * T].reshape(H, T), ky[:H]
 
     def total_edges(self) -> int:
         """Kept edges over every hop and edge type."""
@@ -384,7 +414,7 @@ class Graph:
         return Blocks(self, h, H)
 
     def sample_bundle(self, seeds_list, fanouts, rng_seeds, gather="all", events=None,
-                      stream=None):
+                      stream=None, stage_events=None):
         """Several mini-batches in one launch sequence (hg_sample_blocks_bundle):
         seeds_list[b] per node type as in sample_blocks, rng_seeds[b]; returns
         one Blocks per batch (with gathered features for `gather`)."""
@@ -420,8 +450,14 @@ class Graph:
         gt = (ctypes.c_int32 * max(len(gather), 1))(*[int(t) for t in gather])
         start, stop = events if events is not None else (None, None)
         hs = (ctypes.c_void_p * max(B, 1))()
-        _check(lib.hg_sample_blocks_bundle(self._h, B, ptrs, counts, H, fo, sg, gt, len(gather),
-                                           start, stop, _stream(stream), hs))
+        if stage_events is not None:
+            _check(lib.hg_sample_blocks_bundle_timed(self._h, B, ptrs, counts, H, fo, sg, gt,
+                                                     len(gather),
+                                                     ctypes.addressof(stage_events.struct),
+                                                     _stream(stream), hs))
+        else:
+            _check(lib.hg_sample_blocks_bundle(self._h, B, ptrs, counts, H, fo, sg, gt,
+                                               len(gather), start, stop, _stream(stream), hs))
         return [Blocks(self, ctypes.c_void_p(hs[b]), H) for b in range(B)]
 
     def sample_layers(self, seeds, layer_sizes, rng_seed: int = 0, gather=None,
@@ -684,7 +720,7 @@ class Pipeline:
         """Queues one mini-batch (seeds per node type, as in Graph.sample_blocks)."""
         self.submit_bundle([seeds], fanouts, [rng_seed], events)
 
-    def submit_bundle(self, seeds_list, fanouts, rng_seeds, events=None):
+    def submit_bundle(self, seeds_list, fanouts, rng_seeds, events=None, stage_events=None):
         """Queues len(seeds_list) mini-batches sampled together as one bundle
         (Graph.sample_bundle); next() returns them one by one, in order."""
         g = self.graph
@@ -712,8 +748,12 @@ class Pipeline:
         fo = (ctypes.c_int32 * max(len(flat), 1))(*flat)
         sg = (ctypes.c_uint64 * max(B, 1))(*[int(x) & (2**64 - 1) for x in rng_seeds])
         start, stop = events if events is not None else (None, None)
-        _check(load_library().hg_pipeline_submit(self._h, B, ptrs, counts, H, fo, sg, start,
-                                                 stop))
+        if stage_events is not None:
+            _check(load_library().hg_pipeline_submit_timed(
+                self._h, B, ptrs, counts, H, fo, sg, ctypes.addressof(stage_events.struct)))
+        else:
+            _check(load_library().hg_pipeline_submit(self._h, B, ptrs, counts, H, fo, sg, start,
+                                                     stop))
         for _ in range(B):
             self._held.append(keep)
 
@@ -823,6 +863,32 @@ class HipEvents:
             self._hip.hipEventDestroy(e)
 
 
+class StageEvents:
+    """Timing events for every stage of up to n_hops hops and the gather of one
+    call (hg_stage_events), created through the HIP runtime; durations in ms."""
+
+    def __init__(self, n_hops: int):
+        if n_hops > HG_MAX_TIMED_HOPS:
+            raise ValueError(f"at most {HG_MAX_TIMED_HOPS} timed hops")
+        self.n_hops = n_hops
+        self._ev = HipEvents(2 * n_hops * HG_NUM_STAGES + 2)
+        self.struct = StageEventsStruct()
+        k = 0
+        for h in range(n_hops):
+            for st in range(HG_NUM_STAGES):
+                self.struct.start[h][st] = self._ev.events[k]
+                self.struct.stop[h][st] = self._ev.events[k + 1]
+                k += 2
+        self.struct.gather_start = self._ev.events[k]
+        self.struct.gather_stop = self._ev.events[k + 1]
+
+    def stage_ms(self, hop: int, stage: int) -> float:
+        return self._ev.elapsed_ms(self.struct.start[hop][stage], self.struct.stop[hop][stage])
+
+    def gather_ms(self) -> float:
+        return self._ev.elapsed_ms(self.struct.gather_start, self.struct.gather_stop)
+
+
 def debug_philox(ctr: torch.Tensor, key: int, stream=None) -> torch.Tensor:
     """Philox4x32-10 of each row of a [n, 4] counter tensor (int32 bits)."""
     ctr = ctr.contiguous()
@@ -832,3 +898,17 @@ def debug_philox(ctr: torch.Tensor, key: int, stream=None) -> torch.Tensor:
                                           out.data_ptr() if out.numel() else None,
                                           _stream(stream)))
     return out
+
+
+def bench_philox(rng_seed: int, hop: int, etype: int, n_groups: int, lim: int,
+                 events=None, stream=None) -> torch.Tensor:
+    """The sampler's key loop alone (hg_bench_philox): the number of keys <=
+    lim among the keys of edge IDs 0 .. 4 * n_groups - 1 of (rng_seed, hop,
+    etype), as a one-element int64 device tensor.  events: optional (start,
+    stop) raw hipEvent_t handles carried by the launch."""
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    start, stop = events if events is not None else (None, None)
+    _check(load_library().hg_bench_philox(int(rng_seed) & (2**64 - 1), int(hop), int(etype),
+                                          int(n_groups), int(lim) & 0xFFFFFFFF,
+                                          count.data_ptr(), start, stop, _stream(stream)))
+    return count

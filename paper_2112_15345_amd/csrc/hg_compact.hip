@@ -285,7 +285,7 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream, bool collect) {
+                          int64_t *ticketed, hipStream_t stream, bool collect, StageEv ev) {
   CompactArgs A{hv, ts, n_types, reached, fbits, tile_base, n_tiles, copy_total, tile_sums,
                 reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small, collect};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
@@ -293,17 +293,21 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
   if (n_tiles <= kSinglePassTiles) {
     const int64_t blocks = n_tiles + copy_blocks;
     if (blocks > 0) {
-      hipLaunchKernelGGL(k_bits_single, dim3(unsigned(blocks)), dim3(kTileThreads), 0, stream,
-                         A, epoch, ticket_base);
+      launch_k(k_bits_single, dim3(unsigned(blocks)), dim3(kTileThreads), 0, stream, ev.start,
+               ev.stop, A, epoch, ticket_base);
       *ticketed = blocks;
+    } else if (ev.any()) {
+      hipError_t e = record_empty_stage(ev, stream);
+      if (e != hipSuccess) return e;
     }
     return hipGetLastError();
   }
-  if (n_tiles + copy_blocks > 0)
-    hipLaunchKernelGGL(k_bits_count, dim3(unsigned(n_tiles + copy_blocks)),
-                       dim3(kTileThreads), 0, stream, A);
+  // n_tiles > kSinglePassTiles here, so every launch has blocks
+  launch_k(k_bits_count, dim3(unsigned(n_tiles + copy_blocks)), dim3(kTileThreads), 0, stream,
+           ev.start, nullptr, A);
   hipLaunchKernelGGL(k_bits_scan, dim3(1), dim3(kScanThreads), 0, stream, A);
-  hipLaunchKernelGGL(k_bits_assign, dim3(unsigned(n_tiles)), dim3(kTileThreads), 0, stream, A);
+  launch_k(k_bits_assign, dim3(unsigned(n_tiles)), dim3(kTileThreads), 0, stream, nullptr,
+           ev.stop, A);
   return hipGetLastError();
 }
 
@@ -311,16 +315,16 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
-                          hipStream_t stream) {
+                          hipStream_t stream, StageEv ev) {
   // at least one block: block 0 plans the next hop
   const unsigned grid = grid_for((n_edges + kRelabelItems - 1) / kRelabelItems, 256, 1 << 20);
   if (n_etypes <= kRelabelMaxEtypes)
-    hipLaunchKernelGGL(k_relabel<true>, dim3(grid), dim3(256),
-                       size_t(16) * (n_etypes + 1), stream, hv, next, es, tile_base, small,
-                       n_types, n_etypes, n_edges, src_gid, src_local);
+    launch_k(k_relabel<true>, dim3(grid), dim3(256), size_t(16) * (n_etypes + 1), stream,
+             ev.start, ev.stop, hv, next, es, tile_base, small, n_types, n_etypes, n_edges,
+             src_gid, src_local);
   else
-    hipLaunchKernelGGL(k_relabel<false>, dim3(grid), dim3(256), 0, stream, hv, next, es,
-                       tile_base, small, n_types, n_etypes, n_edges, src_gid, src_local);
+    launch_k(k_relabel<false>, dim3(grid), dim3(256), 0, stream, ev.start, ev.stop, hv, next,
+             es, tile_base, small, n_types, n_etypes, n_edges, src_gid, src_local);
   return hipGetLastError();
 }
 

@@ -2,6 +2,7 @@
 // segment lookup and the Philox4x32-10 counter-based generator.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -11,6 +12,17 @@
 namespace hg {
 
 constexpr int kWave = 64;
+
+// A kernel launch that carries timestamps when asked (e0 when the kernel
+// starts, e1 when it ends), else a plain launch.
+template <typename K, typename... Args>
+inline void launch_k(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t stream,
+                     hipEvent_t e0, hipEvent_t e1, Args... args) {
+  if (e0 || e1)
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, stream, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
+}
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
@@ -324,6 +336,79 @@ __device__ __forceinline__ U32x4 philox4x32_10(U32x4 c, uint32_t k0,
     k1 += 0xBB67AE85u;
   }
   return c;
+}
+
+// The edge keys of one (sampling seed, hop, edge type): Philox4x32-10 at
+// counter (g, 0, hop, etype) for key groups g < 2^32 (edge IDs are below 2^32,
+// so g = eid >> 2 never has a high word).  With the counter's last three words
+// the same for every g, the first two rounds are partly the same for all
+// lanes: round 0 multiplies the fixed hop word, round 1 the fixed word that
+// round 0 made of it.  Those parts are computed once per line (in scalar
+// registers), and the 3-input XORs of the later rounds are single bitop3
+// instructions (truth table 0x96 = a ^ b ^ c).  The result is exactly
+// philox4x32_10({g, 0, hop, etype}, k0, k1): 37 vector operations per four
+// keys instead of 58.
+struct PhiloxLine {
+  uint32_t ek1;    // etype ^ k1 of round 0
+  uint32_t x1k0;   // round 1: (round 0's x1) ^ k0 of round 1
+  uint32_t hk1;    // round 1: hi(M0 * round 0's x0) ^ k1 of round 1
+  uint32_t x3k1;   // round 2: lo(M0 * round 0's x0) ^ k1 of round 2
+  uint32_t k0[10], k1[10];
+};
+
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+// Every argument must be the same on all active lanes.
+__device__ __forceinline__ PhiloxLine philox_line(uint32_t k0, uint32_t k1, uint32_t hop,
+                                                  uint32_t etype) {
+  PhiloxLine L;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    L.k0[r] = __builtin_amdgcn_readfirstlane(k0 + uint32_t(r) * 0x9E3779B9u);
+    L.k1[r] = __builtin_amdgcn_readfirstlane(k1 + uint32_t(r) * 0xBB67AE85u);
+  }
+  // round 0's lane-independent half: p1 = M1 * hop
+  const uint64_t p1 = uint64_t(0xCD9E8D57u) * uint32_t(hop);
+  const uint32_t x0 = uint32_t(p1 >> 32) ^ L.k0[0];  // counter word 1 is 0
+  const uint32_t x1 = uint32_t(p1);
+  // round 1's lane-independent product: p0 = M0 * x0
+  const uint64_t q0 = uint64_t(0xD2511F53u) * x0;
+  L.ek1 = __builtin_amdgcn_readfirstlane(uint32_t(etype) ^ L.k1[0]);
+  L.x1k0 = __builtin_amdgcn_readfirstlane(x1 ^ L.k0[1]);
+  L.hk1 = __builtin_amdgcn_readfirstlane(uint32_t(q0 >> 32) ^ L.k1[1]);
+  L.x3k1 = __builtin_amdgcn_readfirstlane(uint32_t(q0) ^ L.k1[2]);
+  return L;
+}
+
+__device__ __forceinline__ U32x4 philox_keys(const PhiloxLine &L, uint32_t g) {
+  // round 0: p0 = M0 * g
+  uint64_t p0 = uint64_t(0xD2511F53u) * g;
+  uint32_t x2 = uint32_t(p0 >> 32) ^ L.ek1;
+  uint32_t x3 = uint32_t(p0);
+  // round 1: p1 = M1 * x2 (p0 is the line's)
+  uint64_t p1 = uint64_t(0xCD9E8D57u) * x2;
+  uint32_t x0 = uint32_t(p1 >> 32) ^ L.x1k0;
+  uint32_t x1 = uint32_t(p1);
+  x2 = L.hk1 ^ x3;
+  // round 2: x3 of round 1 is the line's
+  p0 = uint64_t(0xD2511F53u) * x0;
+  p1 = uint64_t(0xCD9E8D57u) * x2;
+  x0 = xor3(uint32_t(p1 >> 32), x1, L.k0[2]);
+  x1 = uint32_t(p1);
+  x2 = uint32_t(p0 >> 32) ^ L.x3k1;
+  x3 = uint32_t(p0);
+#pragma unroll
+  for (int r = 3; r < 10; ++r) {
+    p0 = uint64_t(0xD2511F53u) * x0;
+    p1 = uint64_t(0xCD9E8D57u) * x2;
+    x0 = xor3(uint32_t(p1 >> 32), x1, L.k0[r]);
+    x1 = uint32_t(p1);
+    x2 = xor3(uint32_t(p0 >> 32), x3, L.k1[r]);
+    x3 = uint32_t(p0);
+  }
+  return U32x4{x0, x1, x2, x3};
 }
 
 }  // namespace hg

@@ -15,6 +15,7 @@
 
 namespace hg {
 
+
 namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -38,7 +39,7 @@ template <typename V>
 __global__ __launch_bounds__(kThreads) void k_gather(
     const V *__restrict__ table, int64_t n_rows, int32_t rv,
     const int64_t *__restrict__ ids, int64_t n_max, V *__restrict__ out,
-    const int64_t *n_dev, int32_t *err) {
+    const int64_t *n_dev, unsigned long long *bad) {
   const int64_t n = rows_of(n_max, n_dev);
   const int rpp = kThreads / rv;  // rows per pass
   const int r_in = threadIdx.x / rv;
@@ -56,8 +57,8 @@ __global__ __launch_bounds__(kThreads) void k_gather(
         const int64_t id = ids[row];
         if (id >= 0 && id < n_rows)
           v[u] = table[id * rv + col];
-        else if (err && col == 0)
-          atomicOr(err, kErrSeedRange);
+        else if (bad && col == 0)
+          atomicAdd(bad, 1ull);
       }
     }
 #pragma unroll
@@ -73,12 +74,12 @@ template <typename V>
 __global__ __launch_bounds__(kThreads) void k_gather_wide(
     const V *__restrict__ table, int64_t n_rows, int64_t rv,
     const int64_t *__restrict__ ids, int64_t n_max, V *__restrict__ out,
-    const int64_t *n_dev, int32_t *err) {
+    const int64_t *n_dev, unsigned long long *bad) {
   const int64_t n = rows_of(n_max, n_dev);
   for (int64_t row = blockIdx.x; row < n; row += gridDim.x) {
     const int64_t id = ids[row];
     const bool ok = id >= 0 && id < n_rows;
-    if (!ok && err && threadIdx.x == 0) atomicOr(err, kErrSeedRange);
+    if (!ok && bad && threadIdx.x == 0) atomicAdd(bad, 1ull);
     for (int64_t c = threadIdx.x; c < rv; c += kThreads) {
       V x = zero_vec<V>();
       if (ok) x = table[id * rv + c];
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_wide(
 template <typename V>
 hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
                         const int64_t *ids, int64_t n, void *out,
-                        hipStream_t stream, const int64_t *n_dev, int32_t *err) {
+                        hipStream_t stream, const int64_t *n_dev, unsigned long long *bad) {
   const int64_t rv = row_bytes / int64_t(sizeof(V));
   if (rv <= kThreads) {
     const int64_t rows_per_block = int64_t(kThreads / rv) * kUnroll;
@@ -98,12 +99,12 @@ hipError_t launch_typed(const void *table, int64_t n_rows, int64_t row_bytes,
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(k_gather<V>, dim3(unsigned(blocks)), dim3(kThreads), 0,
                        stream, static_cast<const V *>(table), n_rows, int32_t(rv),
-                       ids, n, static_cast<V *>(out), n_dev, err);
+                       ids, n, static_cast<V *>(out), n_dev, bad);
   } else {
     int64_t blocks = n < 65536 ? n : 65536;
     hipLaunchKernelGGL(k_gather_wide<V>, dim3(unsigned(blocks)), dim3(kThreads),
                        0, stream, static_cast<const V *>(table), n_rows, rv, ids,
-                       n, static_cast<V *>(out), n_dev, err);
+                       n, static_cast<V *>(out), n_dev, bad);
   }
   return hipGetLastError();
 }
@@ -186,14 +187,14 @@ int vec_bytes(const void *table, const void *out, int64_t row_bytes) {
 
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
-                         hipStream_t stream, const int64_t *n_dev, int32_t *err) {
+                         hipStream_t stream, const int64_t *n_dev, unsigned long long *bad) {
   if (n <= 0 || row_bytes <= 0) return hipSuccess;
   switch (vec_bytes(table, out, row_bytes)) {
-    case 16: return launch_typed<u32x4>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, err);
-    case 8: return launch_typed<u32x2>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, err);
-    case 4: return launch_typed<uint32_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, err);
-    case 2: return launch_typed<uint16_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, err);
-    default: return launch_typed<uint8_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, err);
+    case 16: return launch_typed<u32x4>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, bad);
+    case 8: return launch_typed<u32x2>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, bad);
+    case 4: return launch_typed<uint32_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, bad);
+    case 2: return launch_typed<uint16_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, bad);
+    default: return launch_typed<uint8_t>(table, n_rows, row_bytes, ids, n, out, stream, n_dev, bad);
   }
 }
 

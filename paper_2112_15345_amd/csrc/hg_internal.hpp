@@ -47,7 +47,7 @@ constexpr int64_t kHubChunk = 2048;
 // Readback slots of the small device buffer (int64 each).
 constexpr int kSlotErr = 0;     // error bits in the low int32
 constexpr int kSlotTicket = 1;  // tile tickets of the single-pass scans
-constexpr int kSlotSpare = 2;
+constexpr int kSlotKeys = 2;    // random keys the sampler evaluates, summed over the hops so far
 constexpr int kSlotPairs = 3;   // pairs of the hop
 constexpr int kSlotEdges = 4;   // kept edges of the hop
 constexpr int kSlotHubs = 5;    // hub pairs
@@ -163,6 +163,16 @@ int graph_device(const hg_graph *g);
 
 // ---- launchers (all asynchronous on `stream`) -------------------------------
 
+// Device timestamps of one stage: `start` is carried by the stage's first
+// kernel launch and `stop` by its last; a stage that launches nothing records
+// both with hipEventRecord.  Null events: plain launches.
+struct StageEv {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool any() const { return start || stop; }
+};
+// Records an empty stage's events (no kernel to carry them).
+hipError_t record_empty_stage(const StageEv &ev, hipStream_t stream);
+
 // The hop-0 frontier: the seed's frontier bit, map[seed] = position; flags
 // range errors and repeats (a frontier bit already set).
 hipError_t launch_insert_frontier(HopView hv, const TypeStatic *ts,
@@ -177,7 +187,8 @@ int64_t count_tiles(int64_t n_items);
 hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                              int32_t n_types, int64_t n_items, PairArrays pa,
                              Lookback lb, uint32_t epoch, uint64_t ticket_base,
-                             ExclView X, int64_t *small, hipStream_t stream);
+                             ExclView X, int64_t *small, hipStream_t stream,
+                             StageEv ev = {});
 
 // The sampler, two launches.  First: block CSC entries and small take-all
 // pairs (a wavefront per 64 pairs), wavefront pairs (one wavefront each) and
@@ -195,7 +206,8 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t key_R, int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
-                         ExclView X, hipStream_t stream);
+                         ExclView X, hipStream_t stream, StageEv ev_sample = {},
+                         StageEv ev_select = {});
 
 
 // Compaction pass: per bitmap tile, ranks of the set bits within the node
@@ -214,7 +226,8 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream, bool collect = false);
+                          int64_t *ticketed, hipStream_t stream, bool collect = false,
+                          StageEv ev = {});
 
 // ---- layer-wise (LADIES) sampling (hg_layers.hip) ----------------------------
 
@@ -294,7 +307,7 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
-                          hipStream_t stream);
+                          hipStream_t stream, StageEv ev = {});
 
 // Fill helpers (kernels, so that they are safe under graph capture).
 // One block copies small[0..n) to pinned host memory host[0..n) and then
@@ -321,15 +334,14 @@ hipError_t launch_check_etype(const int64_t *indptr, int64_t n_dst,
                               int64_t n_src, int32_t *err, hipStream_t stream);
 
 // Row gather: out[i] = table[ids[i]] (row_bytes bytes); a zero row when the
-// ID is out of range, which also sets kErrSeedRange in *err (when err is not
-// NULL).  Picks the widest vector width that divides row_bytes and the
+// ID is out of range, which also adds 1 to *bad (when bad is not NULL).  Picks the widest vector width that divides row_bytes and the
 // alignment of both pointers.
 // With n_dev, the rows are min(*n_dev, n) (read on the device; n bounds them
 // and sizes the grid).
 hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          const int64_t *ids, int64_t n, void *out,
                          hipStream_t stream, const int64_t *n_dev = nullptr,
-                         int32_t *err = nullptr);
+                         unsigned long long *bad = nullptr);
 
 // One row gather of launch_gather_multi.
 struct GatherJob {
@@ -390,5 +402,12 @@ hipError_t launch_edge_relabel(const EdgeBatchArgs &A, HopView first,
 // Philox4x32-10 on n counters.
 hipError_t launch_philox(const uint32_t *ctr, uint64_t key, int64_t n,
                          uint32_t *out, hipStream_t stream);
+
+// The sampler's key loop alone over key groups 0 .. n_groups-1 (a multiple of
+// 64) of (key, hop, etype): adds the number of keys <= lim to *count (device
+// uint64).  start / stop (may be NULL) are carried by the launch.
+hipError_t launch_philox_rate(uint64_t key, int32_t hop, int32_t etype, int64_t n_groups,
+                              uint32_t lim, uint64_t *count, hipEvent_t start,
+                              hipEvent_t stop, hipStream_t stream);
 
 }  // namespace hg

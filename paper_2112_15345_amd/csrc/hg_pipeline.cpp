@@ -35,6 +35,8 @@ struct hg_pipeline {
     std::vector<int32_t> fanouts;        // [n_hops * R] fanouts, or [n_hops * T] layer sizes
     std::vector<uint64_t> sigmas;        // [n]
     hipEvent_t start = nullptr, stop = nullptr;
+    bool timed = false;       // the stage events below apply
+    hg_stage_events ev{};
     // edge-seeded batches: the host arrays of each hg_edge_batch, copied
     // ([n * R] each; the rev_* arrays only where the batch gives them)
     std::vector<const int64_t *> eids, rev_eid;
@@ -90,6 +92,9 @@ hg_status hg_pipeline::run(Job &j, hipStream_t s, hg_blocks **out) {
     return hg_sample_edge_blocks_bundle(g, j.n, eb.data(), j.n_hops, fo, j.sigmas.data(), gt, ng,
                                         s, out);
   }
+  if (j.timed)
+    return hg_sample_blocks_bundle_timed(g, j.n, j.seeds.data(), j.n_seeds.data(), j.n_hops, fo,
+                                         j.sigmas.data(), gt, ng, &j.ev, s, out);
   return hg_sample_blocks_bundle(g, j.n, j.seeds.data(), j.n_seeds.data(), j.n_hops, fo,
                                  j.sigmas.data(), gt, ng, j.start, j.stop, s, out);
 }
@@ -208,10 +213,10 @@ hg_status hg_pipeline_create(hg_graph *g, int32_t n_workers, int32_t capacity,
   return HG_OK;
 }
 
-hg_status hg_pipeline_submit(hg_pipeline *p, int32_t n_batches, const int64_t *const *seeds,
+static hg_status submit_impl(hg_pipeline *p, int32_t n_batches, const int64_t *const *seeds,
                              const int64_t *n_seeds, int32_t n_hops,
                              const int32_t *fanouts, const uint64_t *rng_seeds,
-                             hipEvent_t start, hipEvent_t stop) {
+                             hipEvent_t start, hipEvent_t stop, const hg_stage_events *ev) {
   if (!p) return hg::set_error(HG_EINVAL, "hg_pipeline_submit: pipeline is NULL");
   if (n_batches < 1 || n_batches > p->capacity)
     return hg::set_error(HG_EINVAL, "hg_pipeline_submit: n_batches not in 1..capacity");
@@ -237,7 +242,27 @@ hg_status hg_pipeline_submit(hg_pipeline *p, int32_t n_batches, const int64_t *c
   j.n_hops = n_hops;
   j.start = start;
   j.stop = stop;
+  if (ev) {
+    j.timed = true;
+    j.ev = *ev;
+  }
   return p->enqueue(std::move(j));
+}
+
+hg_status hg_pipeline_submit(hg_pipeline *p, int32_t n_batches, const int64_t *const *seeds,
+                             const int64_t *n_seeds, int32_t n_hops,
+                             const int32_t *fanouts, const uint64_t *rng_seeds,
+                             hipEvent_t start, hipEvent_t stop) {
+  return submit_impl(p, n_batches, seeds, n_seeds, n_hops, fanouts, rng_seeds, start, stop,
+                     nullptr);
+}
+
+hg_status hg_pipeline_submit_timed(hg_pipeline *p, int32_t n_batches,
+                                   const int64_t *const *seeds, const int64_t *n_seeds,
+                                   int32_t n_hops, const int32_t *fanouts,
+                                   const uint64_t *rng_seeds, const hg_stage_events *events) {
+  return submit_impl(p, n_batches, seeds, n_seeds, n_hops, fanouts, rng_seeds, nullptr, nullptr,
+                     events);
 }
 
 hg_status hg_pipeline_submit_layers(hg_pipeline *p, int32_t n_batches,

@@ -271,6 +271,9 @@ struct hg_blocks {
   std::vector<int64_t> n_dst, n_src;  // [H*T]
   std::vector<int64_t *> src_gid;     // [H*T]
   std::vector<int64_t> n_edges;       // [H*R]
+  // random keys the sampler evaluated per hop, for the whole call (a bundle's
+  // handles each hold the bundle's totals)
+  std::vector<int64_t> keys;          // [H]
   std::vector<int64_t *> indptr;
   std::vector<int32_t *> src_local, dst_local;
   std::vector<int64_t *> eid;
@@ -659,6 +662,12 @@ struct SampleRun {
   const int32_t *gtypes = nullptr;
   int32_t n_gather = 0;
   hipEvent_t g_start = nullptr, g_stop = nullptr;
+  // device timestamps of the stages of every hop (benchmarks), or NULL
+  const hg_stage_events *sev = nullptr;
+  StageEv stage_ev(int32_t h, int s) const {
+    if (!sev || h >= HG_MAX_TIMED_HOPS) return StageEv{};
+    return StageEv{sev->start[h][s], sev->stop[h][s]};
+  }
   bool gathered = false;
   hg_status early_gather(const std::vector<int64_t *> &ids, const std::vector<int64_t> &cap);
   // a layer-wise hop's kept edges (their per-etype starts are read back at the
@@ -815,6 +824,7 @@ void SampleRun::init_blocks() {
   b->n_src.assign(size_t(H) * T, 0);
   b->src_gid.assign(size_t(H) * T, nullptr);
   b->n_edges.assign(size_t(H) * R, 0);
+  b->keys.assign(size_t(H), 0);
   b->indptr.assign(size_t(H) * R, nullptr);
   b->src_local.assign(size_t(H) * R, nullptr);
   b->dst_local.assign(size_t(H) * R, nullptr);
@@ -1272,6 +1282,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
   // the last hop's source lists (the input frontier) and their capacities
   std::vector<int64_t *> last_src(T, nullptr);
   std::vector<int64_t> last_bound(T, 0);
+  int64_t keys_before = 0;
   for (int32_t h = 0; h < H; ++h) {
     const HopView hv = view(h), nv = view(h + 1);
     // ---- 1. counting pass over at most n_items pair slots ----------------
@@ -1298,7 +1309,7 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     uint32_t epoch;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
         (e = launch_count_scan(hv, ws->d_es, R, T, n_items, pa, lb, epoch, ticket_base, X,
-                               ws->dsmall, stream)) != hipSuccess)
+                               ws->dsmall, stream, stage_ev(h, HG_STAGE_COUNT))) != hipSuccess)
       return fail_device(e, "count");
     ticket_base += uint64_t(tiles);
     // wait: this hop's sizes (and the previous hop's new-vertex counts)
@@ -1306,6 +1317,9 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     hg_status st = check_flags("count");
     if (st != HG_OK) return st;
     const int64_t *hs = ws->hsmall;
+    // the keys slot sums over the hops: this hop's share
+    b->keys[h] = hs[kSlotKeys] - keys_before;
+    keys_before = hs[kSlotKeys];
     if ((st = close_layer_edges()) != HG_OK) return st;
     if (h == 0 && eb) {
       // the seeds of an edge-seeded call: the compaction counted them
@@ -1407,7 +1421,8 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
                            dsigmas(), g->key_R, h, key_bits, gid_tmp, eid_all, dstl_all,
                            indptr_all,
-                           src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream)) !=
+                           src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream,
+                           stage_ev(h, HG_STAGE_SAMPLE), stage_ev(h, HG_STAGE_SELECT))) !=
         hipSuccess)
       return fail_device(e, "sample");
     int64_t ticketed = 0;
@@ -1415,12 +1430,12 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
         (e = launch_compact(hv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles,
                             copy_total,
                             ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
-                            stream)) != hipSuccess)
+                            stream, false, stage_ev(h, HG_STAGE_COMPACT))) != hipSuccess)
       return fail_device(e, "compact");
     ticket_base += uint64_t(ticketed);
     reached_dirty = false;
     if ((e = launch_relabel(hv, nv, ws->d_es, g->d_tile_base, ws->dsmall, T, R, S, gid_tmp,
-                            srcl_all, stream)) != hipSuccess)
+                            srcl_all, stream, stage_ev(h, HG_STAGE_RELABEL))) != hipSuccess)
       return fail_device(e, "relabel");
     // the map now holds the source lists of this hop, which are region h+1's
     // frontier; the relabel pass wrote their sizes into that region
@@ -1719,16 +1734,30 @@ hg_status check_batch(const hg_graph *g, const int64_t *const *seeds, const int6
 
 // One sampling run on g (a graph or the virtual graph of a bundle, already
 // checked), then the gather of node types gtypes into the handle.
+// Stage events with only the gather's pair set (NULL when both are NULL).
+struct GatherEvents {
+  hg_stage_events ev{};
+  const hg_stage_events *ptr = nullptr;
+  GatherEvents(hipEvent_t start, hipEvent_t stop) {
+    if (start || stop) {
+      ev.gather_start = start;
+      ev.gather_stop = stop;
+      ptr = &ev;
+    }
+  }
+};
+
 hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *n_seeds,
                        int32_t n_hops, const int32_t *fanouts, const uint64_t *sigmas,
                        int32_t n_sig, int32_t key_bits, const int32_t *gtypes, int32_t n_gather,
-                       hipEvent_t start, hipEvent_t stop, hipStream_t stream, hg_blocks **out) {
+                       const hg_stage_events *sev, hipStream_t stream, hg_blocks **out) {
   DeviceGuard dg(g->device);
   SampleRun run(g, stream, n_hops, fanouts, sigmas, n_sig, key_bits);
   run.gtypes = gtypes;
   run.n_gather = n_gather;
-  run.g_start = start;
-  run.g_stop = stop;
+  run.sev = sev;
+  run.g_start = sev ? sev->gather_start : nullptr;
+  run.g_stop = sev ? sev->gather_stop : nullptr;
   hg_status st = acquire_workspace(g, run.table_bytes(), stream, &run.ws);
   if (st != HG_OK) return st;
   run.b = new (std::nothrow) hg_blocks();
@@ -1741,7 +1770,7 @@ hg_status run_sampling(hg_graph *g, const int64_t *const *seeds, const int64_t *
     // the gather goes first: the map reset of finish() can wait behind it
     // (the hop loop launched it already unless there were no hops)
     if (st == HG_OK && n_gather > 0 && !run.gathered)
-      st = gather_into_blocks(g, run.b, gtypes, n_gather, start, stop, stream);
+      st = gather_into_blocks(g, run.b, gtypes, n_gather, run.g_start, run.g_stop, stream);
   } catch (const std::bad_alloc &) {
     st = fail(HG_ENOMEM, "hg_sample_blocks: out of host memory");
   }
@@ -1863,8 +1892,9 @@ hg_status sample_impl(hg_graph *g, const int64_t *const *seeds, const int64_t *n
   if (!g) return fail(HG_EINVAL, "hg_sample_blocks: graph is NULL");
   hg_status st = check_batch(g, seeds, n_seeds, n_hops, fanouts, key_bits, gtypes, n_gather);
   if (st != HG_OK) return st;
+  const GatherEvents ge(start, stop);
   return run_sampling(g, seeds, n_seeds, n_hops, fanouts, &rng_seed, 1, key_bits, gtypes,
-                      n_gather, start, stop, stream, out);
+                      n_gather, ge.ptr, stream, out);
 }
 
 // Map and bitmap layout of a graph's node types.
@@ -1949,6 +1979,7 @@ hg_blocks *split_blocks(hg_graph *g, const hg_blocks *v, int32_t b) {
   o->src_local.resize(size_t(H) * R);
   o->dst_local.resize(size_t(H) * R);
   o->eid.resize(size_t(H) * R);
+  o->keys = v->keys;
   for (int32_t h = 0; h < H; ++h) {
     for (int32_t t = 0; t < T; ++t) {
       const size_t k = size_t(h) * T + t, kv = size_t(h) * v->T + size_t(b) * T + t;
@@ -2012,12 +2043,10 @@ hg_status hg_sample_blocks_gather(hg_graph *g, const int64_t *const *seeds,
                      start, stop, stream, out);
 }
 
-hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t *const *seeds,
-                                  const int64_t *n_seeds, int32_t n_hops,
-                                  const int32_t *fanouts, const uint64_t *rng_seeds,
-                                  const int32_t *gather_ntypes, int32_t n_gather,
-                                  hipEvent_t start, hipEvent_t stop, hipStream_t stream,
-                                  hg_blocks **out) {
+static hg_status bundle_impl(hg_graph *g, int32_t n_batches, const int64_t *const *seeds,
+                      const int64_t *n_seeds, int32_t n_hops, const int32_t *fanouts,
+                      const uint64_t *rng_seeds, const int32_t *gather_ntypes, int32_t n_gather,
+                      const hg_stage_events *sev, hipStream_t stream, hg_blocks **out) {
   if (!out) return fail(HG_EINVAL, "hg_sample_blocks_bundle: out is NULL");
   clear_pending_error();
   if (!g) return fail(HG_EINVAL, "hg_sample_blocks_bundle: graph is NULL");
@@ -2034,7 +2063,7 @@ hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t 
   }
   if (n_batches == 1)
     return run_sampling(g, seeds, n_seeds, n_hops, fanouts, rng_seeds, 1, 32, gather_ntypes,
-                        n_gather, start, stop, stream, out);
+                        n_gather, sev, stream, out);
   hg_graph *v = nullptr;
   hg_status st = bundle_graph(g, n_batches, &v);
   if (st != HG_OK) return st;
@@ -2051,7 +2080,7 @@ hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t 
   hg_blocks *vb = nullptr;
   st = run_sampling(v, vseeds.data(), n_seeds, n_hops, vfan.empty() ? nullptr : vfan.data(),
                     rng_seeds, n_batches, 32, vg.empty() ? nullptr : vg.data(),
-                    int32_t(vg.size()), start, stop, stream, &vb);
+                    int32_t(vg.size()), sev, stream, &vb);
   if (st != HG_OK) return st;
   for (int32_t b = 0; b < n_batches; ++b) {
     out[b] = split_blocks(g, vb, b);
@@ -2066,6 +2095,27 @@ hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t 
   }
   delete vb;  // the split handles keep the arrays
   return HG_OK;
+}
+
+hg_status hg_sample_blocks_bundle(hg_graph *g, int32_t n_batches, const int64_t *const *seeds,
+                                  const int64_t *n_seeds, int32_t n_hops,
+                                  const int32_t *fanouts, const uint64_t *rng_seeds,
+                                  const int32_t *gather_ntypes, int32_t n_gather,
+                                  hipEvent_t start, hipEvent_t stop, hipStream_t stream,
+                                  hg_blocks **out) {
+  const GatherEvents ge(start, stop);
+  return bundle_impl(g, n_batches, seeds, n_seeds, n_hops, fanouts, rng_seeds, gather_ntypes,
+                     n_gather, ge.ptr, stream, out);
+}
+
+hg_status hg_sample_blocks_bundle_timed(hg_graph *g, int32_t n_batches,
+                                        const int64_t *const *seeds, const int64_t *n_seeds,
+                                        int32_t n_hops, const int32_t *fanouts,
+                                        const uint64_t *rng_seeds, const int32_t *gather_ntypes,
+                                        int32_t n_gather, const hg_stage_events *events,
+                                        hipStream_t stream, hg_blocks **out) {
+  return bundle_impl(g, n_batches, seeds, n_seeds, n_hops, fanouts, rng_seeds, gather_ntypes,
+                     n_gather, events, stream, out);
 }
 
 hg_status hg_sample_edge_blocks(hg_graph *g, const hg_edge_batch *batch, int32_t n_hops,
@@ -2312,6 +2362,17 @@ hg_status hg_blocks_edge_counts(const hg_blocks *b, int64_t *counts) {
   return HG_OK;
 }
 
+hg_status hg_blocks_counts(const hg_blocks *b, int64_t *n_dst, int64_t *n_src, int64_t *keys) {
+  if (!b) return fail(HG_EINVAL, "hg_blocks_counts: blocks is NULL");
+  for (size_t k = 0; k < b->n_dst.size(); ++k) {
+    if (n_dst) n_dst[k] = b->n_dst[k];
+    if (n_src) n_src[k] = b->n_src[k];
+  }
+  if (keys)
+    for (size_t h = 0; h < b->keys.size(); ++h) keys[h] = b->keys[h];
+  return HG_OK;
+}
+
 hg_status hg_blocks_nodes(const hg_blocks *b, int32_t hop, int32_t ntype,
                           int64_t *n_dst, int64_t *n_src,
                           const int64_t **src_gid) {
@@ -2372,7 +2433,7 @@ hg_status hg_gather_rows(hg_graph *g, int32_t ntype, const int64_t *ids,
   int64_t *err_slot = w->dsmall + kSlotErr;
   const uint64_t seq = ++w->publish_seq;
   hipError_t e = launch_gather(N.feat, N.num_nodes, N.row_bytes, ids, n, out, stream, nullptr,
-                               reinterpret_cast<int32_t *>(err_slot));
+                               reinterpret_cast<unsigned long long *>(err_slot));
   if (e == hipSuccess)
     e = launch_publish(w->dsmall, w->hsmall, int32_t(small_slots(g)), seq, true, stream);
   if (e == hipSuccess) e = wait_flag(g, w, seq, stream);
@@ -2381,13 +2442,14 @@ hg_status hg_gather_rows(hg_graph *g, int32_t ntype, const int64_t *ids,
     release_workspace(g, w, stream);
     return fail_hip(e, "gather");
   }
-  const int32_t err = int32_t(w->hsmall[kSlotErr]);
+  const int64_t bad = w->hsmall[kSlotErr];
   release_workspace(g, w, stream);
-  if (err)
-    return fail(HG_EINVAL, "hg_gather_rows: an ID is outside [0, %lld) of node type %d",
-                static_cast<long long>(N.num_nodes), ntype);
+  if (bad)
+    return fail(HG_EINVAL, "hg_gather_rows: %lld IDs are outside [0, %lld) of node type %d",
+                static_cast<long long>(bad), static_cast<long long>(N.num_nodes), ntype);
   return HG_OK;
 }
+
 
 hg_status hg_gather_features(hg_graph *g, const hg_blocks *b, int32_t ntype,
                              void *out, hipStream_t stream) {
@@ -2466,6 +2528,19 @@ extern "C" {
 void hg_blocks_free(hg_blocks *b) {
   delete b;  // the arrays go with the last handle that shares them
   clear_pending_error();
+}
+
+hg_status hg_bench_philox(uint64_t rng_seed, int32_t hop, int32_t etype, int64_t n_groups,
+                          uint32_t lim, uint64_t *count, hipEvent_t start, hipEvent_t stop,
+                          hipStream_t stream) {
+  if (n_groups <= 0 || n_groups % 64 != 0 || n_groups > (int64_t(1) << 32) || !count ||
+      hop < 0 || etype < 0)
+    return fail(HG_EINVAL, "hg_bench_philox: bad arguments");
+  clear_pending_error();
+  hipError_t e = launch_philox_rate(rng_seed, hop, etype, n_groups, lim, count, start, stop,
+                                    stream);
+  if (e != hipSuccess) return fail_hip(e, "philox rate");
+  return HG_OK;
 }
 
 hg_status hg_debug_philox(const uint32_t *ctr, uint64_t key, int64_t n,

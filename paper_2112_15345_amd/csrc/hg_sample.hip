@@ -16,6 +16,10 @@
 // edge key is computed once.  Pairs of more than kHubChunk edges that keep
 // all of them (none excluded) are hubs too: their chunks are copied straight
 // to the output, and the second launch skips them.
+#include <hip/hip_ext.h>
+
+#include <algorithm>
+
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
@@ -104,6 +108,7 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
 // Per pair: kept edges s, hub chunks, "one wavefront" flag, hub flag.
 struct PairCounts {
   int64_t s, nch, wave, hub;
+  int64_t keys;  // random keys the sampler evaluates for the pair
 };
 
 // Per edge type, what the counting pass reads for every pair; staged in
@@ -248,7 +253,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
     const int64_t p = base + k;
-    c[k] = PairCounts{0, 0, 0, 0};
+    c[k] = PairCounts{0, 0, 0, 0, 0};
     if (!fp[k]) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
     const int64_t deg = hi[k] - lo[k];
     const int64_t K = V.fanout(etype[k]);
@@ -257,6 +262,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     const int64_t avail = deg - nx;
     const int64_t s = (K < 0 || avail <= K) ? avail : K;
     c[k].s = s;
+    if (s < avail) c[k].keys = deg;  // a selection keys every in-edge
     if (deg > kHubChunk && (s < avail || nx == 0)) {
       c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
       c[k].hub = 1;
@@ -267,6 +273,18 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
       pa.plo[p] = lo[k];
       pa.pdeg[p] = deg;
     }
+  }
+
+  // the keys the sampler will evaluate: every in-edge of a pair that selects
+  // among its in-edges (one wavefront-wide sum, one atomic per wavefront)
+  {
+    int64_t keys = 0;
+#pragma unroll
+    for (int k = 0; k < kPairItems; ++k) keys += c[k].keys;
+    keys = wave_sum_i64(keys);
+    if (lane_id() == 0 && keys)
+      atomicAdd(reinterpret_cast<unsigned long long *>(small + kSlotKeys),
+                (unsigned long long)keys);
   }
 
   // block scan of the per-thread sums, then the tile's prefix by look-back
@@ -346,12 +364,10 @@ __device__ __forceinline__ void emit_edge(const EmitCtx &c, int64_t pos,
   c.src_reached[g] = 1;
 }
 
-// Keys of the four edges 4g .. 4g+3.
-__device__ __forceinline__ U32x4 edge_keys(uint64_t g, int32_t hop, int32_t e,
-                                           uint32_t k0, uint32_t k1,
+// Keys of the four edges 4g .. 4g+3 (g < 2^30: edge IDs are below 2^32).
+__device__ __forceinline__ U32x4 edge_keys(const PhiloxLine &L, uint64_t g,
                                            uint32_t shift) {
-  U32x4 r = philox4x32_10(
-      U32x4{uint32_t(g), uint32_t(g >> 32), uint32_t(hop), uint32_t(e)}, k0, k1);
+  U32x4 r = philox_keys(L, uint32_t(g));
   r.x >>= shift;
   r.y >>= shift;
   r.z >>= shift;
@@ -381,8 +397,7 @@ __device__ __forceinline__ uint64_t cand_threshold(int64_t K, int64_t deg,
 // in edge order.  One wavefront; exact.
 __device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
                                     int64_t K, int64_t o, uint64_t a,
-                                    uint64_t b, int32_t hop, int32_t e,
-                                    uint32_t k0, uint32_t k1, uint32_t shift,
+                                    uint64_t b, const PhiloxLine &L, uint32_t shift,
                                     const ExclView &X, int xe, bool excl) {
   const int lane = lane_id();
   const uint64_t g_first = uint64_t(lo) >> 2;
@@ -394,7 +409,7 @@ __device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
     for (uint64_t gb = g_first; gb <= g_last; gb += kWave) {
       const uint64_t g = gb + lane;
       if (g > g_last) continue;
-      const U32x4 r = edge_keys(g, hop, e, k0, k1, shift);
+      const U32x4 r = edge_keys(L, g, shift);
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const uint64_t ed = 4 * g + w;
@@ -416,7 +431,7 @@ __device__ void select_by_bisection(const EmitCtx &c, int64_t lo, int64_t deg,
     const uint64_t g = gb + lane;
     int mask = 0;
     if (g <= g_last) {
-      const U32x4 r = edge_keys(g, hop, e, k0, k1, shift);
+      const U32x4 r = edge_keys(L, g, shift);
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const uint64_t ed = 4 * g + w;
@@ -630,7 +645,7 @@ __device__ void wave_pair_run(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
   const KeyCtx kc = P.kc;
-  const uint32_t k0 = kc.k0, k1 = kc.k1;
+  const PhiloxLine L = philox_line(kc.k0, kc.k1, uint32_t(A.hop), uint32_t(kc.ke));
   const uint64_t g_first = uint64_t(lo) >> 2;
   const uint64_t g_last = uint64_t(lo + deg - 1) >> 2;
   const uint64_t hi = uint64_t(lo + deg);
@@ -643,7 +658,7 @@ __device__ void wave_pair_run(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
     int mask = 0;
     U32x4 r{0, 0, 0, 0};
     if (g <= g_last) {
-      r = edge_keys(g, A.hop, kc.ke, k0, k1, shift);
+      r = edge_keys(L, g, shift);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const uint64_t ed = 4 * g + q;
@@ -693,7 +708,7 @@ __device__ void wave_pair_run(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
   }
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
-  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift, A.X, e, nx > 0);
+  select_by_bisection(c, lo, deg, K, o, a, b, L, shift, A.X, e, nx > 0);
 }
 
 __device__ void role_wave_pairs(const SampleArgs &A, uint32_t *ck, uint32_t *cj,
@@ -731,6 +746,7 @@ struct HubParams {
   int e;
   int32_t nx;  // excluded in-edges
   KeyCtx kc;
+  PhiloxLine L;
   // every in-edge is kept: chunks are copied to output slots o + (j - lo)
   __device__ bool take_all() const { return K == deg; }
 };
@@ -743,6 +759,7 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   const int64_t p = A.pa.hub_pair[hub];
   H.e = A.pa.pet[p];
   H.kc = key_ctx(A, H.e);
+  H.L = philox_line(H.kc.k0, H.kc.k1, uint32_t(A.hop), uint32_t(H.kc.ke));
   H.lo = A.pa.plo[p];
   H.deg = A.pa.pdeg[p];
   H.o = A.pa.off[p];
@@ -788,9 +805,7 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
                                          uint32_t lim, uint32_t shift, HubBuf &B) {
   const int lane = lane_id();
   const uint64_t g = gb + lane;
-  const U32x4 r = philox4x32_10(
-      U32x4{uint32_t(g), uint32_t(g >> 32), uint32_t(A.hop), uint32_t(H.kc.ke)}, H.kc.k0,
-      H.kc.k1);
+  const U32x4 r = philox_keys(H.L, uint32_t(g));
   if (!kChecked) {
     const uint32_t m = min(min(r.x, r.y), min(r.z, r.w));
     if (__ballot(m <= lim) == 0) return;
@@ -908,7 +923,6 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   const uint32_t shift = uint32_t(32 - A.key_bits);
   const uint64_t key_space = uint64_t(1) << A.key_bits;
   const KeyCtx kc = key_ctx(A, e);
-  const uint32_t k0 = kc.k0, k1 = kc.k1;
   const uint64_t tau = cand_threshold(K, deg, key_space);
   const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
                              p - A.hv.pair_base[e]);
@@ -943,7 +957,9 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   uint64_t a, b;
   bisection_bounds(n_cand, K, tau, key_space, deg, &a, &b);
   const int32_t nx = excl_count(A.X, e, p - A.hv.pair_base[e]);
-  select_by_bisection(c, lo, deg, K, o, a, b, A.hop, kc.ke, k0, k1, shift, A.X, e, nx > 0);
+  select_by_bisection(c, lo, deg, K, o, a, b,
+                      philox_line(kc.k0, kc.k1, uint32_t(A.hop), uint32_t(kc.ke)), shift, A.X,
+                      e, nx > 0);
 }
 
 __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
@@ -1022,6 +1038,31 @@ __global__ void k_philox(const uint32_t *ctr, uint32_t k0, uint32_t k1,
   }
 }
 
+// The sampler's key loop on its own, for measuring its rate: wavefront w takes
+// steps w, w + waves, ... of 64 key groups (256 keys) each and evaluates them
+// as a hub chunk does (the line-specialised Philox, then one wavefront test
+// whether any key is <= lim); it counts the keys <= lim, so that nothing is
+// dead code, and adds its count to *count once.
+__global__ __launch_bounds__(256) void k_philox_rate(uint32_t k0, uint32_t k1, uint32_t hop,
+                                                     uint32_t etype, int64_t n_steps,
+                                                     uint32_t lim,
+                                                     unsigned long long *count) {
+  const PhiloxLine L = philox_line(k0, k1, hop, etype);
+  const int lane = lane_id();
+  const int64_t waves = int64_t(gridDim.x) * (256 / kWave);
+  uint32_t n = 0;
+  for (int64_t st = int64_t(blockIdx.x) * (256 / kWave) + threadIdx.x / kWave; st < n_steps;
+       st += waves) {
+    const U32x4 r = philox_keys(L, uint32_t(st * kWave + lane));
+    const uint32_t m = min(min(r.x, r.y), min(r.z, r.w));
+    if (__ballot(m <= lim) == 0) continue;
+    n += uint32_t(r.x <= lim) + uint32_t(r.y <= lim) + uint32_t(r.z <= lim) +
+         uint32_t(r.w <= lim);
+  }
+  const int64_t total = wave_sum_i64(int64_t(n));
+  if (lane == 0 && total) atomicAdd(count, (unsigned long long)total);
+}
+
 // ---- host handshake -----------------------------------------------------------
 
 // Copies the n readback slots to host memory, then sets the flag word
@@ -1073,31 +1114,32 @@ int64_t count_tiles(int64_t n_items) {
 template <bool kStaged, int kItems>
 void count_launch(HopView hv, const EtypeStatic *es, int32_t n_etypes, int32_t n_types,
                   int64_t n_items, PairArrays pa, Lookback lb, uint32_t epoch,
-                  uint64_t ticket_base, ExclView X, int64_t *small, hipStream_t stream) {
+                  uint64_t ticket_base, ExclView X, int64_t *small, hipStream_t stream,
+                  StageEv ev) {
   const size_t lds = kStaged ? CountTable::bytes(n_etypes) : 0;
-  hipLaunchKernelGGL((k_count_scan<kStaged, kItems>), dim3(unsigned(count_tiles(n_items))),
-                     dim3(kTileThreads), lds, stream, hv, es, n_etypes, n_types, n_items, pa,
-                     lb, epoch, ticket_base, X, small);
+  launch_k(k_count_scan<kStaged, kItems>, dim3(unsigned(count_tiles(n_items))),
+           dim3(kTileThreads), lds, stream, ev.start, ev.stop, hv, es, n_etypes, n_types,
+           n_items, pa, lb, epoch, ticket_base, X, small);
 }
 
 hipError_t launch_count_scan(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                              int32_t n_types, int64_t n_items, PairArrays pa,
                              Lookback lb, uint32_t epoch, uint64_t ticket_base,
-                             ExclView X, int64_t *small, hipStream_t stream) {
+                             ExclView X, int64_t *small, hipStream_t stream, StageEv ev) {
   const bool staged = n_etypes <= kCountMaxEtypes;
   const bool large = pair_items(n_items) == kPairItemsLarge;
   if (staged && large)
     count_launch<true, kPairItemsLarge>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                        ticket_base, X, small, stream);
+                                        ticket_base, X, small, stream, ev);
   else if (staged)
     count_launch<true, kPairItemsSmall>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                        ticket_base, X, small, stream);
+                                        ticket_base, X, small, stream, ev);
   else if (large)
     count_launch<false, kPairItemsLarge>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                         ticket_base, X, small, stream);
+                                         ticket_base, X, small, stream, ev);
   else
     count_launch<false, kPairItemsSmall>(hv, es, n_etypes, n_types, n_items, pa, lb, epoch,
-                                         ticket_base, X, small, stream);
+                                         ticket_base, X, small, stream, ev);
   return hipGetLastError();
 }
 
@@ -1108,7 +1150,8 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int32_t key_R, int32_t hop, int32_t key_bits, int64_t *src_gid,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
-                         ExclView X, hipStream_t stream) {
+                         ExclView X, hipStream_t stream, StageEv ev_sample,
+                         StageEv ev_select) {
   if (n_src_out > kInlineSrcOut) return hipErrorInvalidValue;
   SampleArgs A;
   A.X = X;
@@ -1144,14 +1187,25 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.dst_local = dst_local;
   A.indptr_all = indptr_all;
   const int64_t blocks = A.blocks_a + A.blocks_b + blocks_c;
-  hipLaunchKernelGGL(k_sample, dim3(unsigned(blocks)), dim3(kSampleThreads), 0,
-                     stream, A);
+  launch_k(k_sample, dim3(unsigned(blocks)), dim3(kSampleThreads), 0, stream, ev_sample.start,
+           ev_sample.stop, A);
   if (n_hubs > 0) {
     // the hub lists are complete once the first launch has finished
     const int64_t hb = (n_hubs + kSampleWaves - 1) / kSampleWaves;
-    hipLaunchKernelGGL(k_hub_finish, dim3(unsigned(hb)), dim3(kSampleThreads), 0, stream, A);
+    launch_k(k_hub_finish, dim3(unsigned(hb)), dim3(kSampleThreads), 0, stream,
+             ev_select.start, ev_select.stop, A);
+  } else if (ev_select.any()) {
+    hipError_t e = record_empty_stage(ev_select, stream);
+    if (e != hipSuccess) return e;
   }
   return hipGetLastError();
+}
+
+hipError_t record_empty_stage(const StageEv &ev, hipStream_t stream) {
+  hipError_t e = hipSuccess;
+  if (ev.start) e = hipEventRecord(ev.start, stream);
+  if (e == hipSuccess && ev.stop) e = hipEventRecord(ev.stop, stream);
+  return e;
 }
 
 hipError_t launch_publish(int64_t *small, int64_t *host, int32_t n, uint64_t seq, bool clear,
@@ -1200,6 +1254,18 @@ hipError_t launch_nonempty_mask(const int64_t *const *indptrs, int32_t n_etypes,
   if (n <= 0 || n_etypes <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_nonempty_mask, dim3(grid_for(n, 256, 16384)), dim3(256), 0, stream,
                      indptrs, n_etypes, words, n, mask);
+  return hipGetLastError();
+}
+
+hipError_t launch_philox_rate(uint64_t key, int32_t hop, int32_t etype, int64_t n_groups,
+                              uint32_t lim, uint64_t *count, hipEvent_t start,
+                              hipEvent_t stop, hipStream_t stream) {
+  const int64_t steps = n_groups / kWave;
+  // as many wavefronts as the hub role launches at most
+  const unsigned blocks = unsigned(std::min<int64_t>(std::max<int64_t>(steps / 4, 1), 4096));
+  hipExtLaunchKernelGGL(k_philox_rate, dim3(blocks), dim3(256), 0, stream, start, stop, 0,
+                        uint32_t(key), uint32_t(key >> 32), uint32_t(hop), uint32_t(etype),
+                        steps, lim, reinterpret_cast<unsigned long long *>(count));
   return hipGetLastError();
 }
 

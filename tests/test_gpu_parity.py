@@ -44,6 +44,22 @@ def test_philox_device_matches_oracle(olib):
     assert np.array_equal(z.cpu().numpy().view(np.uint32)[0], pins.rr_block(0, 0, 0))
 
 
+@pytest.mark.parametrize("sigma,hop,etype,lim", [(0, 0, 0, 1 << 31), (2**64 - 1, 2, 5, 123457),
+                                                  (987654321, 1, 1199, 0xFFFFFFFF),
+                                                  (5, 7, 3, 0)])
+def test_key_loop_counts_match_oracle(olib, sigma, hop, etype, lim):
+    """The sampler's key loop run alone (hg_bench_philox, the key-rate
+    microbenchmark): its count of keys <= lim over edge IDs 0 .. 4n-1 equals
+    the oracle's keys of the same edges."""
+    n_groups = 64 * 160
+    got = int(hg.bench_philox(sigma, hop, etype, n_groups, lim).item())
+    keys = np.array([oracle.edge_key(sigma, hop, etype, eid, 32, olib)
+                     for eid in range(4 * n_groups)], dtype=np.uint64)
+    assert got == int((keys <= lim).sum())
+    with pytest.raises(hg.HGError):
+        hg.bench_philox(sigma, hop, etype, 100, lim)  # not a multiple of 64
+
+
 def run_both(olib, nn, ets, feats, seeds, fanouts, sigma, bits):
     g = gpu_graph(nn, ets, feats)
     b = g.sample_blocks(gpu_seeds(seeds), fanouts, sigma, key_bits=bits)
@@ -292,3 +308,49 @@ def test_allocator_failure_releases_everything(olib):
         break
     else:
         pytest.fail("sampling never succeeded")
+
+
+def expected_keys(ets, ref, fanouts):
+    """Keys the sampler must evaluate per hop: the in-degree of every
+    (frontier vertex, edge type) pair that keeps K of more than K in-edges."""
+    out = []
+    for h, row in enumerate(fanouts):
+        k = 0
+        for e, (s, d, ip, ix) in enumerate(ets):
+            nd, sg = ref["nodes"][(h, d)]
+            deg = ip[sg[:nd] + 1] - ip[sg[:nd]]
+            if row[e] >= 0:
+                k += int(deg[deg > row[e]].sum())
+        out.append(k)
+    return out
+
+
+def test_block_counts_and_keys(olib):
+    """hg_blocks_counts: per-hop frontier and source sizes equal the oracle's,
+    and the sampler's key count equals the in-degrees of the pairs that
+    select (a bundle reports the sum over its batches)."""
+    rng = np.random.default_rng(31)
+    for c in range(6):
+        nn, ets, feats, seeds, fanouts, sigma, bits = pins.random_case(rng, max_nodes=300,
+                                                                       max_deg=3000)
+        g, b, ref, got = run_both(olib, nn, ets, feats, seeds, fanouts, sigma, 32)
+        nd, ns, keys = b.counts()
+        for h in range(len(fanouts)):
+            for t in range(len(nn)):
+                assert nd[h, t] == ref["nodes"][(h, t)][0]
+                assert ns[h, t] == ref["nodes"][(h, t)][1].size
+        assert list(keys) == expected_keys(ets, ref, fanouts), f"case {c}"
+    wl = W.WORKLOADS[1]
+    gen = W.make_graph(wl)
+    host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), lib=olib)
+    g = hg.Graph([(n, f.cuda()) for n, f in zip(gen.num_nodes, gen.feats)],
+                 [(s, d, ip.cuda(), ix.cuda()) for s, d, ip, ix in gen.etypes])
+    fan = wl.fanout_matrix()
+    batches = [3, 4, 5]
+    got = g.sample_bundle([gpu_seeds(W.seeds_per_type(wl, x)) for x in batches], fan, batches)
+    want = np.zeros(len(fan), np.int64)
+    for x in batches:
+        ref = host.sample_blocks(W.seeds_per_type(wl, x), fan, x)
+        want += expected_keys(gen.host_etypes(), ref, fan)
+    for blocks in got:
+        assert list(blocks.counts()[2]) == list(want)
