@@ -335,6 +335,22 @@ hg_status hg_blocks_features(const hg_blocks *blocks, int32_t ntype, int64_t *ro
 hg_status hg_gather_rows(hg_graph *graph, int32_t ntype, const int64_t *ids,
                          int64_t n, void *out, hipStream_t stream);
 
+/* hg_gather_rows for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same arguments, output and errors as hg_gather_rows; it calls no hipMalloc,
+ * hipFree or other allocating routine.  Its only scratch -- the count of IDs
+ * out of range -- lives in a static device array of HG_NOALLOC_SCRATCH_BYTES
+ * bytes that the library holds on every GPU it runs on until the process
+ * ends (hg_create looks up that GPU's address of it).  The scratch does not
+ * grow with n, so no size is refused for it.  Every call on a GPU shares that
+ * GPU's array: the call clears the count with a kernel, gathers, copies the
+ * count to the host and waits for `stream`; calls that overlap on one GPU
+ * (from several threads or streams) race on the count and must be
+ * serialised by the caller. */
+#define HG_NOALLOC_SCRATCH_BYTES 256
+hg_status hg_gather_rows_noalloc(hg_graph *graph, int32_t ntype, const int64_t *ids,
+                                 int64_t n, void *out, hipStream_t stream);
+
 /* Releases a blocks handle (stream-ordered on the stream it was made on;
  * on the null stream for handles returned by hg_pipeline_next), so that
  * stream must still exist.  A handle does not depend on its graph handle: it

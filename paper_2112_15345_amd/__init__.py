@@ -43,7 +43,8 @@ ABI_SYMBOLS = ("hg_create", "hg_destroy", "hg_retire_stream", "hg_sample_blocks"
                "hg_sample_edge_blocks_bundle", "hg_sample_layers_bundle",
                "hg_pipeline_submit_layers", "hg_pipeline_submit_edges",
                "hg_blocks_free", "hg_last_error", "hg_debug_philox", "hg_bench_philox",
-               "hg_sample_blocks_bundle_timed", "hg_pipeline_submit_timed", "hg_blocks_counts")
+               "hg_sample_blocks_bundle_timed", "hg_pipeline_submit_timed", "hg_blocks_counts",
+               "hg_gather_rows_noalloc")
 
 HG_MAX_NEG = 64
 HG_MAX_TIMED_HOPS = 8
@@ -112,6 +113,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         "hg_gather_features_multi": ([_P, _P, _P, _P, _I32, _P], _I32),
         "hg_gather_features_multi_timed": ([_P, _P, _P, _P, _I32, _P, _P, _P], _I32),
         "hg_gather_rows": ([_P, _I32, _P, _I64, _P, _P], _I32),
+        "hg_gather_rows_noalloc": ([_P, _I32, _P, _I64, _P, _P], _I32),
         "hg_sample_blocks_gather": ([_P, _P, _P, _I32, _P, ctypes.c_uint64, _P, _I32, _P, _P, _P,
                                      _PP], _I32),
         "hg_blocks_features": ([_P, _I32, _PI64, _PP], _I32),
@@ -678,6 +680,18 @@ class Graph:
         _check(load_library().hg_gather_features_multi_timed(self._h, blocks.handle, ts, ps, n,
                                                              _stream(stream), start, stop))
         return outs
+
+    def gather_rows_noalloc(self, ntype: int, ids: torch.Tensor, out: torch.Tensor,
+                            stream=None) -> torch.Tensor:
+        """hg_gather_rows_noalloc: the same pull with no device allocation (its
+        counter lives in the library's static scratch); `out` is required."""
+        ids = _dev_i64(ids, self.device)
+        _check(load_library().hg_gather_rows_noalloc(self._h, ntype,
+                                                     ids.data_ptr() if ids.numel() else None,
+                                                     ids.numel(),
+                                                     out.data_ptr() if out.numel() else None,
+                                                     _stream(stream)))
+        return out
 
     def gather_rows(self, ntype: int, ids: torch.Tensor, out: torch.Tensor | None = None,
                     stream=None) -> torch.Tensor:

@@ -10,11 +10,41 @@
 // (non-temporal), since the output is not re-read by this kernel.
 #include <hip/hip_ext.h>
 
+#include <map>
+#include <mutex>
+
 #include "hg_device.hpp"
 #include "hg_internal.hpp"
 
 namespace hg {
 
+// Scratch of the allocation-free row pull (hg_gather_rows_noalloc): the count
+// of out-of-range IDs of the call running on this GPU.  Every GPU the library
+// runs on holds its own copy until the process ends.  Host code never uses
+// this name as an address: it uses the per-device address that
+// hipGetSymbolAddress gives (noalloc_scratch_init).
+static __device__ __align__(256) unsigned long long scratch[kNoAllocScratchBytes / 8];
+
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, unsigned long long *> g_scratch_ptr;  // device -> address of `scratch`
+}  // namespace
+
+hipError_t noalloc_scratch_init(int device) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr.count(device)) return hipSuccess;
+  void *p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !p) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+  g_scratch_ptr[device] = static_cast<unsigned long long *>(p);
+  return hipSuccess;
+}
+
+unsigned long long *noalloc_scratch(int device) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch_ptr.find(device);
+  return it == g_scratch_ptr.end() ? nullptr : it->second;
+}
 
 namespace {
 

@@ -343,6 +343,14 @@ hipError_t launch_gather(const void *table, int64_t n_rows, int64_t row_bytes,
                          hipStream_t stream, const int64_t *n_dev = nullptr,
                          unsigned long long *bad = nullptr);
 
+// The allocation-free row pull keeps its counters in a static device array
+// of this many bytes per GPU.  noalloc_scratch_init (with `device` current)
+// looks up that GPU's address of the array once; noalloc_scratch returns it
+// (NULL before the lookup).
+constexpr size_t kNoAllocScratchBytes = HG_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch_init(int device);
+unsigned long long *noalloc_scratch(int device);
+
 // One row gather of launch_gather_multi.
 struct GatherJob {
   const void *table;

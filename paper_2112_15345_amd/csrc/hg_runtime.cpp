@@ -1646,6 +1646,13 @@ hg_status hg_create(const hg_ntype_desc *ntypes, int32_t n_ntypes,
     free_graph(g);
     return st;
   }
+  // set-up of the allocation-free entry point on this device (current here):
+  // the device's address of its static scratch array, looked up once
+  if ((e = noalloc_scratch_init(dev)) != hipSuccess) {
+    hg_status st = fail_hip(e, "hg_create: scratch address");
+    free_graph(g);
+    return st;
+  }
   *out = g;
   return HG_OK;
 }
@@ -2450,6 +2457,37 @@ hg_status hg_gather_rows(hg_graph *g, int32_t ntype, const int64_t *ids,
   return HG_OK;
 }
 
+hg_status hg_gather_rows_noalloc(hg_graph *g, int32_t ntype, const int64_t *ids, int64_t n,
+                                 void *out, hipStream_t stream) {
+  if (!g) return fail(HG_EINVAL, "hg_gather_rows_noalloc: graph is NULL");
+  if (ntype < 0 || ntype >= g->T)
+    return fail(HG_EINVAL, "hg_gather_rows_noalloc: node type %d out of range", ntype);
+  const NTypeInfo &N = g->nt[ntype];
+  if (N.dtype == HG_DT_NONE || N.row_bytes <= 0)
+    return fail(HG_EINVAL, "hg_gather_rows_noalloc: node type %d has no features", ntype);
+  if (n < 0) return fail(HG_EINVAL, "hg_gather_rows_noalloc: n < 0");
+  if (n == 0) return HG_OK;
+  if (!ids || !out) return fail(HG_EINVAL, "hg_gather_rows_noalloc: NULL ids or out");
+  DeviceGuard dg(g->device);
+  clear_pending_error();
+  // the GPU's copy of the static scratch array, looked up by hg_create
+  unsigned long long *bad = noalloc_scratch(g->device);
+  if (!bad) return fail(HG_EDEVICE, "hg_gather_rows_noalloc: no scratch address for the device");
+  // the count starts at zero (a kernel, not a memset, clears it)
+  hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t *>(bad), 2, 0u, stream);
+  if (e == hipSuccess)
+    e = launch_gather(N.feat, N.num_nodes, N.row_bytes, ids, n, out, stream, nullptr, bad);
+  unsigned long long host_bad = 0;
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(&host_bad, bad, sizeof(host_bad), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return fail_hip(e, "hg_gather_rows_noalloc");
+  if (host_bad)
+    return fail(HG_EINVAL,
+                "hg_gather_rows_noalloc: %llu IDs are outside [0, %lld) of node type %d",
+                host_bad, static_cast<long long>(N.num_nodes), ntype);
+  return HG_OK;
+}
 
 hg_status hg_gather_features(hg_graph *g, const hg_blocks *b, int32_t ntype,
                              void *out, hipStream_t stream) {
