@@ -794,18 +794,19 @@ __device__ void hub_flush(const SampleArgs &A, int64_t hub, HubBuf &B) {
   B.n = 0;
 }
 
-// One wavefront step over the 64 key groups gb .. gb+63 of a hub chunk
+// One wavefront step over the 64 key groups gb .. gb+63 (wave-uniform gb;
+// group g holds edges 4g .. 4g+3, g < 2^30) of a hub's edge range
 // [c_lo, c_hi): appends the edges with key <= lim to the hub's candidates.
-// kChecked: some lanes' edges may lie outside the chunk.  Otherwise the step
+// kChecked: some lanes' edges may lie outside the range.  Otherwise the step
 // first asks whether any key of the wavefront is small enough at all, which
 // is rarely the case.
 template <bool kChecked>
 __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H,
-                                         uint64_t gb, int64_t c_lo, int64_t c_hi,
+                                         uint32_t gb, int64_t c_lo, int64_t c_hi,
                                          uint32_t lim, uint32_t shift, HubBuf &B) {
   const int lane = lane_id();
-  const uint64_t g = gb + lane;
-  const U32x4 r = philox_keys(H.L, uint32_t(g));
+  const uint32_t g = gb + uint32_t(lane);
+  const U32x4 r = philox_keys(H.L, g);
   if (!kChecked) {
     const uint32_t m = min(min(r.x, r.y), min(r.z, r.w));
     if (__ballot(m <= lim) == 0) return;
@@ -815,7 +816,7 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
   if (kChecked) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const uint64_t ed = 4 * g + q;
+      const uint64_t ed = 4 * uint64_t(g) + q;
       if (ed < uint64_t(c_lo) || ed >= uint64_t(c_hi)) mask &= ~(1 << q);
     }
     if (__ballot(mask != 0) == 0) return;
@@ -823,7 +824,7 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
   if (H.nx > 0) {  // excluded edges are never candidates
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if ((mask & (1 << q)) && is_excluded(A.X, H.e, 4 * g + q)) mask &= ~(1 << q);
+      if ((mask & (1 << q)) && is_excluded(A.X, H.e, 4 * uint64_t(g) + q)) mask &= ~(1 << q);
   }
   int tot;
   const int pre = wave_prefix_small(__popc(mask), &tot);
@@ -832,7 +833,7 @@ __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     if (mask & (1 << q)) {
-      B.e[pos] = (uint64_t(word_of(r, q) >> shift) << 32) | (4 * g + q - uint64_t(H.lo));
+      B.e[pos] = (uint64_t(word_of(r, q) >> shift) << 32) | (4 * uint64_t(g) + q - uint64_t(H.lo));
       ++pos;
     }
   }
@@ -865,36 +866,38 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w, uint64_t *buf) {
   HubParams H = hub_params(A, find_hub(A, c_first));
   const uint32_t shift = uint32_t(32 - A.key_bits);
   HubBuf B{buf, 0};
-  for (int64_t chunk = c_first; chunk < c_end; ++chunk) {
+  for (int64_t chunk = c_first; chunk < c_end;) {
     while (chunk >= H.end_chunk) {
       hub_flush(A, H.hub, B);
       H = hub_params(A, H.hub + 1);
     }
+    // this wavefront's chunks of the hub are one contiguous range of in-edges
+    const int64_t run_end = min(c_end, H.end_chunk);
+    const int64_t r_lo = H.lo + (chunk - H.first_chunk) * kHubChunk;
+    const int64_t r_hi = min(H.lo + (run_end - H.first_chunk) * kHubChunk, H.lo + H.deg);
+    chunk = run_end;
+    if (H.take_all()) {
+      const EmitCtx c = make_ctx(A.es[H.e], A.src_gid, A.eid, A.dst_local, H.dst);
+      for (int64_t j = r_lo + lane_id(); j < r_hi; j += kWave) emit_edge(c, H.o + (j - H.lo), j);
+      continue;
+    }
     // (key >> shift) < tau  <=>  key < tau << shift  <=>  key <= lim
     const uint64_t tau_raw = H.tau << shift;
     const uint32_t lim = tau_raw - 1 >= 0xFFFFFFFFull ? 0xFFFFFFFFu : uint32_t(tau_raw - 1);
-    const int64_t c_lo = H.lo + (chunk - H.first_chunk) * kHubChunk;
-    const int64_t c_hi = min(c_lo + kHubChunk, H.lo + H.deg);
-    if (H.take_all()) {
-      const EmitCtx c = make_ctx(A.es[H.e], A.src_gid, A.eid, A.dst_local, H.dst);
-      for (int64_t j = c_lo + lane_id(); j < c_hi; j += kWave) emit_edge(c, H.o + (j - H.lo), j);
-      continue;
+    // steps over the key groups g_first .. g_last, 64 at a time; a step whose
+    // groups all lie inside the range (g_first <= ... < g_in_end) needs no
+    // bounds, so only a partial first and the last steps are checked
+    const uint32_t g_first = uint32_t(uint64_t(r_lo) >> 2);
+    const uint32_t g_last = uint32_t(uint64_t(r_hi - 1) >> 2);
+    const uint32_t g_in_end = uint32_t(uint64_t(r_hi) >> 2);
+    uint32_t gb = g_first;
+    if (4 * uint64_t(gb) < uint64_t(r_lo)) {
+      hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, B);
+      gb += kWave;
     }
-    // steps k = 0 .. n_it-1 cover groups g_first + 64k ..; steps [k_lo, k_hi)
-    // lie wholly inside the chunk
-    const uint64_t g_first = uint64_t(c_lo) >> 2;
-    const uint64_t g_last = uint64_t(c_hi - 1) >> 2;
-    const int64_t n_it = int64_t((g_last - g_first) / kWave) + 1;
-    const int64_t k_lo = 4 * g_first >= uint64_t(c_lo) ? 0 : 1;
-    int64_t k_hi = int64_t((uint64_t(c_hi) / 4 - g_first) / kWave);
-    if (k_hi > n_it) k_hi = n_it;
-    if (k_hi < k_lo) k_hi = k_lo;
-    for (int64_t k = 0; k < k_lo; ++k)
-      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, B);
-    for (int64_t k = k_lo; k < k_hi; ++k)
-      hub_step<false>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, B);
-    for (int64_t k = k_hi; k < n_it; ++k)
-      hub_step<true>(A, H, g_first + kWave * k, c_lo, c_hi, lim, shift, B);
+    for (; gb + kWave <= g_in_end; gb += kWave)
+      hub_step<false>(A, H, gb, r_lo, r_hi, lim, shift, B);
+    for (; gb <= g_last; gb += kWave) hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, B);
   }
   hub_flush(A, H.hub, B);
 }
