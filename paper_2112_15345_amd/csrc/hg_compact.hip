@@ -40,6 +40,7 @@ struct CompactArgs {
   int32_t n_types;
   uint8_t *reached;  // reached this hop (one byte per vertex)
   uint32_t *fbits;   // in the frontier (one bit per vertex)
+  uint32_t *rbits;   // non-NULL: the hop marked reached bits (laid out as fbits) instead
   const int64_t *tile_base;
   int64_t n_tiles;
   int64_t copy_total;
@@ -71,15 +72,23 @@ __device__ __forceinline__ const uint4 *reached_of(const CompactArgs &A, int64_t
   return reinterpret_cast<const uint4 *>(A.reached + (tile * kTile + threadIdx.x * kTileItems) * 32);
 }
 __device__ __forceinline__ TileWords tile_words(const CompactArgs &A, int64_t tile) {
+  const int64_t w = tile * kTile + threadIdx.x * kTileItems;
+  const uint2 front = *reinterpret_cast<const uint2 *>(A.fbits + w);
+  if (A.rbits) return TileWords{*reinterpret_cast<const uint2 *>(A.rbits + w), front};
   const uint4 *r = reached_of(A, tile);
   const uint4 r0 = r[0], r1 = r[1], r2 = r[2], r3 = r[3];
-  const int64_t w = tile * kTile + threadIdx.x * kTileItems;
   return TileWords{uint2{pack16(r0) | (pack16(r1) << 16), pack16(r2) | (pack16(r3) << 16)},
-                   *reinterpret_cast<const uint2 *>(A.fbits + w)};
+                   front};
 }
-// Clears the thread's reached bytes (when any is set).
+// Clears the thread's reached bytes or bits (when any is set).
 __device__ __forceinline__ void clear_reached(const CompactArgs &A, int64_t tile,
                                               const TileWords &tw) {
+  if (A.rbits) {
+    if ((tw.reached.x | tw.reached.y) != 0)
+      *reinterpret_cast<uint2 *>(A.rbits + tile * kTile + threadIdx.x * kTileItems) =
+          uint2{0, 0};
+    return;
+  }
   if ((tw.reached.x | tw.reached.y) != 0) {
     uint4 *r = const_cast<uint4 *>(reached_of(A, tile));
     const uint4 z{0, 0, 0, 0};
@@ -299,8 +308,9 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           uint8_t *reached, uint32_t *fbits, const int64_t *tile_base,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
-                          int64_t *ticketed, hipStream_t stream, bool collect, StageEv ev) {
-  CompactArgs A{hv, ts, n_types, reached, fbits, tile_base, n_tiles, copy_total, tile_sums,
+                          int64_t *ticketed, hipStream_t stream, bool collect, StageEv ev,
+                          uint32_t *rbits) {
+  CompactArgs A{hv, ts, n_types, reached, fbits, rbits, tile_base, n_tiles, copy_total, tile_sums,
                 reinterpret_cast<int32_t *>(tile_sums + n_tiles + 1), small, collect};
   const int64_t copy_blocks = (copy_total + kTile - 1) / kTile;
   *ticketed = 0;

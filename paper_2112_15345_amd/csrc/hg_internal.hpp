@@ -72,6 +72,7 @@ struct EtypeStatic {
   const int64_t *indices;
   int32_t *src_map;       // vertex -> local-ID map of the source type
   uint8_t *src_reached;   // reached flags of the source type
+  uint32_t *src_rbits;    // reached bits of the source type (hops in bit mode)
   int64_t n_dst_nodes;
   int32_t src_type;
   int32_t dst_type;
@@ -98,7 +99,15 @@ struct TypeStatic {
   uint8_t *reached;
   uint32_t *fbits;
   int64_t num_nodes;
+  uint32_t *rbits;  // reached bits (hops in bit mode), laid out as fbits
 };
+
+// A hop marks its kept sources either with the byte flags above (plain
+// stores: no atomics on popular sources) or, when the call's vertices far
+// outnumber the hop's kept edges, with one reached bit per vertex (atomicOr
+// without return), so that the compaction reads an eighth of the bytes.
+// Bit mode is chosen when vertices > kBitModeRatio x kept edges.
+constexpr int64_t kBitModeRatio = 16;
 
 // One hop, as device arrays.  Host-written: frontier, src_out, fanout.
 // nF and pair_base are written by the host for hop 0 and by the previous
@@ -207,7 +216,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          ExclView X, hipStream_t stream, StageEv ev_sample = {},
-                         StageEv ev_select = {});
+                         StageEv ev_select = {}, bool bit_mode = false);
 
 
 // Compaction pass: per bitmap tile, ranks of the set bits within the node
@@ -227,7 +236,7 @@ hipError_t launch_compact(HopView hv, const TypeStatic *ts, int32_t n_types,
                           int64_t n_tiles, int64_t copy_total, int64_t *tile_sums,
                           uint32_t epoch, uint64_t ticket_base, int64_t *small,
                           int64_t *ticketed, hipStream_t stream, bool collect = false,
-                          StageEv ev = {});
+                          StageEv ev = {}, uint32_t *rbits = nullptr);
 
 // ---- layer-wise (LADIES) sampling (hg_layers.hip) ----------------------------
 

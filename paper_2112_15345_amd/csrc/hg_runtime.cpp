@@ -194,6 +194,7 @@ struct Workspace {
   int32_t *map = nullptr;          // sum of num_nodes: local IDs
   uint8_t *reached = nullptr;      // n_tiles * kTile * 32 bytes: reached this hop
   uint32_t *fbits = nullptr;       // n_tiles * kTile words: in the frontier
+  uint32_t *rbits = nullptr;       // n_tiles * kTile words: reached this hop (bit mode)
   int64_t *dsmall = nullptr;       // readback slots
   int64_t *hsmall = nullptr;       // pinned, coherent mirror of dsmall + a flag word
   uint64_t publish_seq = 0;        // flag value of the last publish
@@ -404,6 +405,7 @@ void free_workspace(Workspace *w) {
   (void)hipFree(w->map);
   (void)hipFree(w->reached);
   (void)hipFree(w->fbits);
+  (void)hipFree(w->rbits);
   (void)hipFree(w->dsmall);
   (void)hipFree(w->d_es);
   (void)hipFree(w->d_ts);
@@ -453,6 +455,8 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
       e = hipMalloc(&w->reached, size_t(std::max<int64_t>(g->n_tiles * kTile * 32, 1)));
     if (e == hipSuccess)
       e = hipMalloc(&w->fbits, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
+    if (e == hipSuccess)
+      e = hipMalloc(&w->rbits, sizeof(uint32_t) * size_t(std::max<int64_t>(g->n_tiles * kTile, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->dsmall, sizeof(int64_t) * small_n);
     if (e == hipSuccess) e = hipMalloc(&w->d_es, sizeof(EtypeStatic) * size_t(std::max(g->R, 1)));
     if (e == hipSuccess) e = hipMalloc(&w->d_ts, sizeof(TypeStatic) * size_t(g->T));
@@ -472,19 +476,22 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
       e = launch_fill_u32(reinterpret_cast<uint32_t *>(w->reached), g->n_tiles * kTile * 8, 0u,
                           stream);
     if (e == hipSuccess) e = launch_fill_u32(w->fbits, g->n_tiles * kTile, 0u, stream);
+    if (e == hipSuccess) e = launch_fill_u32(w->rbits, g->n_tiles * kTile, 0u, stream);
     if (e == hipSuccess) {
       std::vector<EtypeStatic> es(size_t(std::max(g->R, 1)));
       for (int32_t i = 0; i < g->R; ++i) {
         const ETypeInfo &E = g->et[i];
         es[i] = EtypeStatic{E.indptr, E.indices, w->map + g->map_off[E.src],
                             w->reached + g->tile_base[E.src] * kTile * 32,
+                            w->rbits + g->tile_base[E.src] * kTile,
                             g->nt[E.dst].num_nodes, E.src, E.dst,
                             E.nz_mask, E.nz_words, E.nz_slot};
       }
       std::vector<TypeStatic> ts(g->T);
       for (int32_t t = 0; t < g->T; ++t)
         ts[t] = TypeStatic{w->map + g->map_off[t], w->reached + g->tile_base[t] * kTile * 32,
-                           w->fbits + g->tile_base[t] * kTile, g->nt[t].num_nodes};
+                           w->fbits + g->tile_base[t] * kTile, g->nt[t].num_nodes,
+                           w->rbits + g->tile_base[t] * kTile};
       e = hipMemcpy(w->d_es, es.data(), sizeof(EtypeStatic) * es.size(), hipMemcpyHostToDevice);
       if (e == hipSuccess)
         e = hipMemcpy(w->d_ts, ts.data(), sizeof(TypeStatic) * ts.size(), hipMemcpyHostToDevice);
@@ -777,9 +784,11 @@ struct SampleRun {
   // meaningful.)
   void finish(bool ok) {
     if (!ws->poisoned) {
-      if (reached_dirty)
+      if (reached_dirty) {
         (void)launch_fill_u32(reinterpret_cast<uint32_t *>(ws->reached), g->n_tiles * kTile * 8, 0u,
                               stream);
+        (void)launch_fill_u32(ws->rbits, g->n_tiles * kTile, 0u, stream);
+      }
       (void)launch_fill_u32(ws->fbits, g->n_tiles * kTile, 0u, stream);
       if (!small_clean)
         (void)launch_fill_i32(reinterpret_cast<int32_t *>(ws->dsmall),
@@ -1418,19 +1427,22 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     reached_dirty = true;
     int64_t copy_total = 0;
     for (int64_t n : nF) copy_total += n;
+    // bit mode when the call's vertices far outnumber the hop's kept edges
+    const bool bit_mode = g->map_off[T] > kBitModeRatio * std::max<int64_t>(S, 1);
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
                            dsigmas(), g->key_R, h, key_bits, gid_tmp, eid_all, dstl_all,
                            indptr_all,
                            src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream,
-                           stage_ev(h, HG_STAGE_SAMPLE), stage_ev(h, HG_STAGE_SELECT))) !=
-        hipSuccess)
+                           stage_ev(h, HG_STAGE_SAMPLE), stage_ev(h, HG_STAGE_SELECT),
+                           bit_mode)) != hipSuccess)
       return fail_device(e, "sample");
     int64_t ticketed = 0;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
         (e = launch_compact(hv, ws->d_ts, T, ws->reached, ws->fbits, g->d_tile_base, g->n_tiles,
                             copy_total,
                             ws->tile_sums, epoch, ticket_base, ws->dsmall, &ticketed,
-                            stream, false, stage_ev(h, HG_STAGE_COMPACT))) != hipSuccess)
+                            stream, false, stage_ev(h, HG_STAGE_COMPACT),
+                            bit_mode ? ws->rbits : nullptr)) != hipSuccess)
       return fail_device(e, "compact");
     ticket_base += uint64_t(ticketed);
     reached_dirty = false;

@@ -342,6 +342,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 struct EmitCtx {
   const int64_t *indices;
   uint8_t *src_reached;
+  uint32_t *src_rbits;  // non-NULL: the hop marks reached bits instead of bytes
   int64_t *src_gid;
   int64_t *eid;
   int32_t *dst_local;
@@ -350,8 +351,18 @@ struct EmitCtx {
 
 __device__ __forceinline__ EmitCtx make_ctx(const EtypeStatic &E, int64_t *src_gid,
                                             int64_t *eid, int32_t *dst_local,
-                                            int64_t dst) {
-  return EmitCtx{E.indices, E.src_reached, src_gid, eid, dst_local, int32_t(dst)};
+                                            int64_t dst, bool bits) {
+  return EmitCtx{E.indices, E.src_reached, bits ? E.src_rbits : nullptr, src_gid, eid,
+                 dst_local, int32_t(dst)};
+}
+
+// Marks source g reached: a plain byte store, or in bit mode an atomic OR
+// whose result is not used.
+__device__ __forceinline__ void mark_reached(uint8_t *bytes, uint32_t *bits, int64_t g) {
+  if (bits)
+    atomicOr(bits + (g >> 5), 1u << (g & 31));
+  else
+    bytes[g] = 1;
 }
 
 // Writes kept edge `e` at output slot `pos`; its source is reached.
@@ -361,7 +372,7 @@ __device__ __forceinline__ void emit_edge(const EmitCtx &c, int64_t pos,
   c.src_gid[pos] = g;
   c.eid[pos] = e;
   c.dst_local[pos] = c.dst;
-  c.src_reached[g] = 1;
+  mark_reached(c.src_reached, c.src_rbits, g);
 }
 
 // Keys of the four edges 4g .. 4g+3 (g < 2^30: edge IDs are below 2^32).
@@ -484,6 +495,7 @@ struct SampleArgs {
   const uint64_t *sigmas;
   int32_t key_R;
   int32_t hop, key_bits;
+  bool bits;  // the hop marks reached bits (bit mode) instead of bytes
   int64_t *src_gid, *eid;
   int32_t *dst_local;
   int64_t *indptr_all;
@@ -517,6 +529,7 @@ struct GroupLds {
   int64_t lo[kWave];           // first in-edge slot
   const int64_t *src[kWave];   // the pair's in-edge sources (indices + lo)
   uint8_t *reached[kWave];     // reached flags of its source type
+  uint32_t *rbits[kWave];      // or its reached bits (bit mode)
   int32_t tpre[kWave + 1];     // prefix of take-all slots over the group
   int32_t dst[kWave];
 };
@@ -545,6 +558,7 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
       L.lo[lane] = lo;
       L.src[lane] = A.es[e].indices + lo;
       L.reached[lane] = A.es[e].src_reached;
+      L.rbits[lane] = A.bits ? A.es[e].src_rbits : nullptr;
       L.dst[lane] = int32_t(i);
     }
   }
@@ -586,7 +600,7 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
       A.src_gid[pos] = g[u];
       A.eid[pos] = L.lo[q[u]] + k[u];
       A.dst_local[pos] = L.dst[q[u]];
-      L.reached[q[u]][g[u]] = 1;
+      mark_reached(L.reached[q[u]], L.rbits[q[u]], g[u]);
     }
   }
 }
@@ -609,7 +623,7 @@ __device__ __forceinline__ WavePair wave_pair(const SampleArgs &A, int64_t p) {
   WavePair P;
   P.e = A.pa.pet[p];
   const int64_t i = p - A.hv.pair_base[P.e];
-  P.c = make_ctx(A.es[P.e], A.src_gid, A.eid, A.dst_local, i);
+  P.c = make_ctx(A.es[P.e], A.src_gid, A.eid, A.dst_local, i, A.bits);
   P.kc = key_ctx(A, P.e);
   P.lo = A.pa.plo[p];
   P.deg = A.pa.pdeg[p];
@@ -877,7 +891,7 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w, uint64_t *buf) {
     const int64_t r_hi = min(H.lo + (run_end - H.first_chunk) * kHubChunk, H.lo + H.deg);
     chunk = run_end;
     if (H.take_all()) {
-      const EmitCtx c = make_ctx(A.es[H.e], A.src_gid, A.eid, A.dst_local, H.dst);
+      const EmitCtx c = make_ctx(A.es[H.e], A.src_gid, A.eid, A.dst_local, H.dst, A.bits);
       for (int64_t j = r_lo + lane_id(); j < r_hi; j += kWave) emit_edge(c, H.o + (j - H.lo), j);
       continue;
     }
@@ -928,7 +942,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   const KeyCtx kc = key_ctx(A, e);
   const uint64_t tau = cand_threshold(K, deg, key_space);
   const EmitCtx c = make_ctx(A.es[e], A.src_gid, A.eid, A.dst_local,
-                             p - A.hv.pair_base[e]);
+                             p - A.hv.pair_base[e], A.bits);
   const int64_t n_cand = A.pa.hub_cnt[hub];
   if (n_cand >= K && n_cand <= kCandCap) {
     const uint64_t *list = A.cand + hub * kCandCap;
@@ -1154,7 +1168,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          ExclView X, hipStream_t stream, StageEv ev_sample,
-                         StageEv ev_select) {
+                         StageEv ev_select, bool bit_mode) {
   if (n_src_out > kInlineSrcOut) return hipErrorInvalidValue;
   SampleArgs A;
   A.X = X;
@@ -1185,6 +1199,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.key_R = key_R > 0 ? key_R : 1;
   A.hop = hop;
   A.key_bits = key_bits;
+  A.bits = bit_mode;
   A.src_gid = src_gid;
   A.eid = eid;
   A.dst_local = dst_local;

@@ -354,3 +354,37 @@ def test_block_counts_and_keys(olib):
         want += expected_keys(gen.host_etypes(), ref, fan)
     for blocks in got:
         assert list(blocks.counts()[2]) == list(want)
+
+
+@pytest.mark.parametrize("pad", [0, 3_000_000])
+def test_reached_bit_mode(olib, pad):
+    """Hops whose kept edges are few next to the graph's vertices mark reached
+    sources with bits (atomicOr) instead of bytes; the tiny workload with and
+    without 3M isolated extra vertices of each type (every hop in bit mode,
+    or a mix) equals the oracle, blocks and gathered bytes."""
+    wl = W.WORKLOADS[1]
+    gen = W.make_graph(wl)
+    nn = [n + pad for n in gen.num_nodes]
+    ets = []
+    for s, d, ip, ix in gen.host_etypes():
+        ets.append((s, d, np.concatenate([ip, np.full(pad, ip[-1], np.int64)]), ix))
+    feats = [np.concatenate([f, np.zeros((pad,) + f.shape[1:], f.dtype)])
+             for _, f in gen.host_ntypes()]
+    g = gpu_graph(nn, ets, feats)
+    host = oracle.HostGraph(list(zip(nn, feats)), ets, lib=olib)
+    fan = wl.fanout_matrix()
+    for b in range(3):
+        seeds = W.seeds_per_type(wl, b)
+        blocks = g.sample_blocks(gpu_seeds(seeds), fan, b, gather="all")
+        ref = host.sample_blocks(seeds, fan, b)
+        diffs = compare(ref, result_dict(g, blocks), g.T, g.R, len(fan))
+        assert not diffs, f"pad {pad} batch {b}: " + "\n".join(diffs[:5])
+        for t in range(g.T):
+            assert blocks.features(t).cpu().numpy().tobytes() == \
+                host.gather(t, ref["input"][t]).tobytes()
+    # a bundle of 4 on the same graph (the virtual graph has 4x the vertices)
+    got = g.sample_bundle([gpu_seeds(W.seeds_per_type(wl, b)) for b in range(4)], fan,
+                          list(range(4)))
+    for b, blocks in enumerate(got):
+        ref = host.sample_blocks(W.seeds_per_type(wl, b), fan, b)
+        assert not compare(ref, result_dict(g, blocks), g.T, g.R, len(fan))
