@@ -51,7 +51,7 @@ PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 
 # Per-workload defaults (workers, bundle, steps): the launch that gives each
 # workload its best throughput on one MI355X.
-DEFAULTS = {1: (2, 32, 320), 2: (2, 32, 320), 3: (2, 2, 20), 4: (0, 8, 64), 5: (2, 8, 64)}
+DEFAULTS = {1: (2, 32, 320), 2: (2, 32, 320), 3: (3, 2, 40), 4: (0, 8, 64), 5: (2, 8, 64)}
 
 # HBM bytes counted by rocprofv3 (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, the
 # factors a 1 GiB device copy gives) per mini-batch, for the kernel sources and
@@ -299,7 +299,11 @@ def vertex_main(args, wl, gen, g):
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
     args.gather_types = feat_types
     row_bytes = {t: gen.feats[t].shape[1] * gen.feats[t].element_size() for t in feat_types}
-    stage_ev = {u[0]: hg.StageEvents(H) for u in timed}
+    # the timed region's launches carry events only on the sampler (the
+    # dominant kernel) and the gather: events on every stage's launches cost
+    # about 12% of a step here.  Every stage is timed in a profile pass after
+    # the clock stops.
+    stage_ev = {u[0]: hg.StageEvents(H, stages=("sample",)) for u in timed}
 
     if args.copy_calibration_mb > 0:
         # a copy of known size, untimed, for scaling the memory counters
@@ -311,9 +315,9 @@ def vertex_main(args, wl, gen, g):
         log(f"calibration copy of {args.copy_calibration_mb} MiB done")
         del src, dst
 
-    def direct(u):
+    def direct(u, ev=None):
         return g.sample_bundle([seeds[b] for b in u], fan, u, gather=feat_types,
-                               stage_events=stage_ev.get(u[0]))
+                               stage_events=ev or stage_ev.get(u[0]))
 
     def submit(pipe, u):
         pipe.submit_bundle([seeds[b] for b in u], fan, u, stage_events=stage_ev.get(u[0]))
@@ -353,23 +357,38 @@ def vertex_main(args, wl, gen, g):
         prev = t_done
     p10, p50, p90 = percentiles(per_step)
 
-    # device time of every stage, from the events its own launches carried
-    stage_ms = {name: 0.0 for name in hg.STAGE_NAMES}
-    launches = {name: 0 for name in hg.STAGE_NAMES}
-    gather_ms = 0.0
-    for u in timed:
-        ev = stage_ev[u[0]]
-        for h in range(H):
-            for st, name in enumerate(hg.STAGE_NAMES):
-                stage_ms[name] += ev.stage_ms(h, st)
-                launches[name] += 1
-        gather_ms += ev.gather_ms()
-    sc_ms = sum(stage_ms.values())
-    alg_sc = sum(step_bytes_model(g, r[4], r[5], r[7]) for r in rec)
+    # device time of the sampler's and the gather's launches over the timed
+    # region, from the events those launches carried
+    sample_ms = sum(stage_ev[u[0]].stage_ms(h, hg.HG_STAGE_SAMPLE) for u in timed
+                    for h in range(H))
+    sample_launches = len(timed) * H
+    gather_ms = sum(stage_ev[u[0]].gather_ms() for u in timed)
     keys = sum(int(r[6].sum()) for r in rec)
     g_alg = sum(n * (2 * row_bytes[t] + 8) for r in rec for t, n in r[3].items())
     if args.host_features:
         g_alg = gbytes  # the rows cross the host link once; that link is the roof
+
+    # profile pass (untimed): the first timed units again, direct calls on one
+    # stream, every stage's launches carrying events
+    prof_units = timed[:max(1, min(len(timed), args.profile_units))]
+    stage_ms = {name: 0.0 for name in hg.STAGE_NAMES}
+    prof_alg = prof_steps = 0
+    prof_gather_ms = 0.0
+    for u in prof_units:
+        ev = hg.StageEvents(H)
+        blist = direct(u, ev)
+        torch.cuda.synchronize()
+        for h in range(H):
+            for st, name in enumerate(hg.STAGE_NAMES):
+                stage_ms[name] += ev.stage_ms(h, st)
+        prof_gather_ms += ev.gather_ms()
+        nd = sum(b.counts()[0] for b in blist)
+        ns = sum(b.counts()[1] for b in blist)
+        ne = sum(np.asarray(b.edge_counts(), np.int64).reshape(H, g.R) for b in blist)
+        prof_alg += step_bytes_model(g, nd, ns, ne)
+        prof_steps += len(u)
+        del blist
+    sc_ms = sum(stage_ms.values())
 
     # the sampler's key loop alone, over as many keys as a timed step
     hip_ev = hg.HipEvents(2)
@@ -407,7 +426,7 @@ def vertex_main(args, wl, gen, g):
               "ms_per_step": gather_ms / steps,
               "algorithmic_bytes_per_step": g_alg / steps,
               "traffic_per_step": traffic["gather"] if traffic else None}
-    sample_s = stage_ms["sample"] / 1e3
+    sample_s = sample_ms / 1e3
     philox = {"keys_per_step": keys / steps,
               "keys_per_s": keys / sample_s if sample_s > 0 else None,
               "peak_keys_per_s": PHILOX_PEAK_KEYS,
@@ -417,33 +436,25 @@ def vertex_main(args, wl, gen, g):
               "peak_derivation": f"{VALU_LANE_OPS:.4g} lane-ops/s x 4 keys / "
                                  f"{PHILOX_VALU_PER_CALL} vector instructions per call"}
     sc = {"kernels": "counting pass, sampler, hub selection, compaction, relabel",
-          "ms_per_step": sc_ms / steps,
-          "stage_ms_per_step": {k: v / steps for k, v in stage_ms.items()},
-          "algorithmic_bytes_per_step": alg_sc / steps,
-          "algorithmic_GBps": alg_sc / (sc_ms / 1e3) / 1e9 if sc_ms > 0 else None,
-          "algorithmic_frac": alg_sc / (sc_ms / 1e3) / 1e9 / HBM_PEAK_GBS if sc_ms > 0 else None,
-          "counter_bytes_per_step": traffic["sample_compact"] if traffic else None,
-          "sampled_edges_per_s": edges / (sc_ms / 1e3) if sc_ms > 0 else None}
+          "measured": f"profile pass: {prof_steps} of the timed mini-batches again, direct "
+                      f"calls on one stream, every stage's launches carrying HIP events",
+          "ms_per_step": sc_ms / prof_steps,
+          "stage_ms_per_step": {k: v / prof_steps for k, v in stage_ms.items()},
+          "gather_ms_per_step": prof_gather_ms / prof_steps,
+          "algorithmic_bytes_per_step": prof_alg / prof_steps,
+          "algorithmic_GBps": prof_alg / (sc_ms / 1e3) / 1e9 if sc_ms > 0 else None,
+          "algorithmic_frac": prof_alg / (sc_ms / 1e3) / 1e9 / HBM_PEAK_GBS if sc_ms > 0 else None,
+          "counter_bytes_per_step": traffic["sample_compact"] if traffic else None}
     if traffic:
-        rate = traffic["sample_compact"] / (sc_ms / steps / 1e3) / 1e9
+        rate = traffic["sample_compact"] / (sc_ms / prof_steps / 1e3) / 1e9
         sc["counter_GBps"] = rate
         sc["counter_frac"] = rate / HBM_PEAK_GBS
-        sc["counter_over_algorithmic"] = traffic["sample_compact"] / (alg_sc / steps)
-    # the roofline of the kernel with the most device time
-    per_kernel = dict(stage_ms, gather=gather_ms)
+        sc["counter_over_algorithmic"] = traffic["sample_compact"] / (prof_alg / prof_steps)
+    # the roofline of the kernel with the most device time (from the profile
+    # pass), its rate measured over the timed region
+    per_kernel = dict(stage_ms, gather=prof_gather_ms)
     dominant = max(per_kernel, key=per_kernel.get)
-    if dominant == "sample":
-        n_l = launches["sample"]
-        achieved = keys / sample_s / 1e9
-        roofline = {"bound": "alu", "kernel": "k_sample (the sampler: random keys of every "
-                    "in-edge of a selecting pair, then the kept edges)",
-                    "achieved": achieved, "peak": PHILOX_PEAK_KEYS / 1e9, "unit": "Gkeys/s",
-                    "frac": achieved / (PHILOX_PEAK_KEYS / 1e9),
-                    "traffic": traffic["k_sample_per_launch"] if traffic else None,
-                    "algorithmic_per_launch": keys / n_l,
-                    "avg_launch_us": stage_ms["sample"] / n_l * 1e3,
-                    "peak_source": philox["peak_derivation"]}
-    elif dominant == "gather":
+    if dominant == "gather":
         n_l = len(timed)
         roofline = {"bound": gather["bound"], "kernel": gather["kernel"],
                     "achieved": g_gbps, "peak": peak, "unit": "GB/s", "frac": g_gbps / peak,
@@ -451,10 +462,18 @@ def vertex_main(args, wl, gen, g):
                     "algorithmic_per_launch": g_alg / n_l,
                     "avg_launch_us": gather_ms / n_l * 1e3}
     else:
-        n_l = launches[dominant]
-        roofline = {"bound": "hbm", "kernel": f"{dominant} stage", "achieved": None,
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": None, "traffic": None,
-                    "avg_launch_us": per_kernel[dominant] / n_l * 1e3}
+        achieved = keys / sample_s / 1e9 if sample_s > 0 else 0.0
+        roofline = {"bound": "alu", "kernel": "k_sample (the sampler: random keys of every "
+                    "in-edge of a selecting pair, then the kept edges)",
+                    "achieved": achieved, "peak": PHILOX_PEAK_KEYS / 1e9, "unit": "Gkeys/s",
+                    "frac": achieved / (PHILOX_PEAK_KEYS / 1e9),
+                    "traffic": traffic["k_sample_per_launch"] if traffic else None,
+                    "algorithmic_per_launch": keys / sample_launches,
+                    "avg_launch_us": sample_ms / sample_launches * 1e3,
+                    "peak_source": philox["peak_derivation"]}
+        if dominant != "sample":
+            roofline["note"] = (f"the {dominant} stage has the most device time; the sampler's "
+                                f"roofline is reported")
     roofline["device_copy_GBps"] = copy_gbps
     result = {
         "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
@@ -686,7 +705,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
-                    help="timed mini-batches (default per workload: 20 for workload 3)")
+                    help="timed mini-batches (default per workload: 40 for workload 3)")
     ap.add_argument("--warmup", type=int, default=5,
                     help="untimed mini-batches first, at least; every unit size the timed "
                          "region uses is also warmed up twice per worker stream")
@@ -705,6 +724,8 @@ def main():
     ap.add_argument("--check-batches", type=int, default=None,
                     help="timed mini-batches compared with the oracle (default 2 for workload "
                          "3, else 8); 0 skips the check")
+    ap.add_argument("--profile-units", type=int, default=4,
+                    help="timed units re-run after the timed region with every stage timed")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle time after which the check stops")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,

@@ -878,28 +878,40 @@ class HipEvents:
 
 
 class StageEvents:
-    """Timing events for every stage of up to n_hops hops and the gather of one
-    call (hg_stage_events), created through the HIP runtime; durations in ms."""
+    """Timing events for the stages of up to n_hops hops and the gather of one
+    call (hg_stage_events), created through the HIP runtime; durations in ms.
+    stages: the names (STAGE_NAMES) that get events, default all; gather:
+    whether the gather gets them.  A stage without events is not timed (its
+    launches stay plain) and reports None."""
 
-    def __init__(self, n_hops: int):
+    def __init__(self, n_hops: int, stages=STAGE_NAMES, gather: bool = True):
         if n_hops > HG_MAX_TIMED_HOPS:
             raise ValueError(f"at most {HG_MAX_TIMED_HOPS} timed hops")
         self.n_hops = n_hops
-        self._ev = HipEvents(2 * n_hops * HG_NUM_STAGES + 2)
+        self.stages = tuple(stages)
+        self.gather = gather
+        n = 2 * n_hops * len(self.stages) + (2 if gather else 0)
+        self._ev = HipEvents(n)
         self.struct = StageEventsStruct()
         k = 0
         for h in range(n_hops):
-            for st in range(HG_NUM_STAGES):
-                self.struct.start[h][st] = self._ev.events[k]
-                self.struct.stop[h][st] = self._ev.events[k + 1]
-                k += 2
-        self.struct.gather_start = self._ev.events[k]
-        self.struct.gather_stop = self._ev.events[k + 1]
+            for st, name in enumerate(STAGE_NAMES):
+                if name in self.stages:
+                    self.struct.start[h][st] = self._ev.events[k]
+                    self.struct.stop[h][st] = self._ev.events[k + 1]
+                    k += 2
+        if gather:
+            self.struct.gather_start = self._ev.events[k]
+            self.struct.gather_stop = self._ev.events[k + 1]
 
-    def stage_ms(self, hop: int, stage: int) -> float:
+    def stage_ms(self, hop: int, stage: int):
+        if STAGE_NAMES[stage] not in self.stages:
+            return None
         return self._ev.elapsed_ms(self.struct.start[hop][stage], self.struct.stop[hop][stage])
 
-    def gather_ms(self) -> float:
+    def gather_ms(self):
+        if not self.gather:
+            return None
         return self._ev.elapsed_ms(self.struct.gather_start, self.struct.gather_stop)
 
 

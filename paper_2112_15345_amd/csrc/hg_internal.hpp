@@ -44,6 +44,11 @@ constexpr int64_t kThreadTakeAll = 32;
 // chunks of kHubChunk edges, handed to wavefronts in runs of chunks.
 constexpr int64_t kHubChunk = 2048;
 
+// Pairs that keep K < deg edges with deg <= kLaneSelect (and nothing
+// excluded) are sampled by one lane each, among the pairs of the take-all
+// groups: all their keys fit in registers.
+constexpr int64_t kLaneSelect = 16;
+
 // Readback slots of the small device buffer (int64 each).
 constexpr int kSlotErr = 0;     // error bits in the low int32
 constexpr int kSlotTicket = 1;  // tile tickets of the single-pass scans

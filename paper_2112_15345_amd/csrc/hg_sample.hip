@@ -108,7 +108,8 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
 // Per pair: kept edges s, hub chunks, "one wavefront" flag, hub flag.
 struct PairCounts {
   int64_t s, nch, wave, hub;
-  int64_t keys;  // random keys the sampler evaluates for the pair
+  int64_t keys;   // random keys the sampler evaluates for the pair
+  int32_t small;  // sampled by one lane (K < deg <= kLaneSelect, nothing excluded)
 };
 
 // Per edge type, what the counting pass reads for every pair; staged in
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
     const int64_t p = base + k;
-    c[k] = PairCounts{0, 0, 0, 0, 0};
+    c[k] = PairCounts{0, 0, 0, 0, 0, 0};
     if (!fp[k]) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
     const int64_t deg = hi[k] - lo[k];
     const int64_t K = V.fanout(etype[k]);
@@ -266,6 +267,8 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     if (deg > kHubChunk && (s < avail || nx == 0)) {
       c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
       c[k].hub = 1;
+    } else if (nx == 0 && s < deg && deg <= kLaneSelect) {
+      c[k].small = 1;
     } else if (s > 0 && !(nx == 0 && s == deg && deg <= kThreadTakeAll)) {
       c[k].wave = 1;  // pairs with excluded edges always take this role
     }
@@ -519,20 +522,85 @@ __device__ __forceinline__ KeyCtx key_ctx(const SampleArgs &A, int e) {
 }
 
 // Role A: a wavefront per 64 consecutive pairs.  Each lane writes its pair's
-// block-CSC entry; then the wavefront copies the in-edges of the small
-// take-all pairs among the 64, one output slot per lane and kGroupSlots slots
-// per lane at a time (their source loads are issued together, before any
-// store).  The first block of this role also writes each etype's closing CSC
-// entry.
+// block-CSC entry; a lane whose pair selects K of at most kLaneSelect in-edges
+// (nothing excluded) ranks their keys in registers.  Then the wavefront writes
+// the kept edges of the small take-all pairs and of those small selections,
+// one output slot per lane and kGroupSlots slots per lane at a time (their
+// source loads are issued together, before any store), so that neighbouring
+// lanes write neighbouring slots.  The first block of this role also writes
+// each etype's closing CSC entry.
 struct GroupLds {
   int64_t start[kWave];        // first output slot of the pair
   int64_t lo[kWave];           // first in-edge slot
   const int64_t *src[kWave];   // the pair's in-edge sources (indices + lo)
   uint8_t *reached[kWave];     // reached flags of its source type
   uint32_t *rbits[kWave];      // or its reached bits (bit mode)
+  // a small selection's kept in-edges, ascending: nibble k is the in-edge
+  // (offset from lo) of its output slot k; 0 for a take-all pair, whose slot k
+  // is in-edge k (a selection that keeps only in-edge 0 is 0 as well, and
+  // means the same)
+  uint64_t pick[kWave];
   int32_t tpre[kWave + 1];     // prefix of take-all slots over the group
   int32_t dst[kWave];
 };
+
+// The K smallest (key, j) of the deg <= kLaneSelect in-edges lo .. lo+deg-1 of
+// one pair, for one lane: their offsets j, ascending, packed 4 bits each.
+__device__ uint64_t lane_select(const SampleArgs &A, int e, int64_t lo, int deg, int K) {
+  static_assert(kLaneSelect == 16, "the unrolled loops cover 16 in-edges");
+  const int b = e / A.key_R;
+  const uint64_t sig = A.sigmas[b];
+  const uint32_t k0 = uint32_t(sig), k1 = uint32_t(sig >> 32), ke = uint32_t(e - b * A.key_R);
+  const uint32_t shift = uint32_t(32 - A.key_bits);
+  // key groups g0 .. g0+4 hold the in-edges, from word lo & 3
+  const uint64_t g0 = uint64_t(lo) >> 2;
+  uint32_t w[20];
+#pragma unroll
+  for (int q = 0; q < 5; ++q) {
+    U32x4 r{0, 0, 0, 0};
+    if (4 * (g0 + q) < uint64_t(lo + deg))
+      r = philox4x32_10(U32x4{uint32_t(g0 + q), uint32_t((g0 + q) >> 32), uint32_t(A.hop), ke},
+                        k0, k1);
+    w[4 * q] = r.x;
+    w[4 * q + 1] = r.y;
+    w[4 * q + 2] = r.z;
+    w[4 * q + 3] = r.w;
+  }
+  uint32_t key[16];
+  switch (int(lo & 3)) {  // constant register indices in every branch
+    case 0:
+#pragma unroll
+      for (int j = 0; j < 16; ++j) key[j] = w[j] >> shift;
+      break;
+    case 1:
+#pragma unroll
+      for (int j = 0; j < 16; ++j) key[j] = w[j + 1] >> shift;
+      break;
+    case 2:
+#pragma unroll
+      for (int j = 0; j < 16; ++j) key[j] = w[j + 2] >> shift;
+      break;
+    default:
+#pragma unroll
+      for (int j = 0; j < 16; ++j) key[j] = w[j + 3] >> shift;
+      break;
+  }
+  // in-edge j is kept when fewer than K in-edges have a smaller (key, j)
+  uint64_t pick = 0;
+  int n = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    int rank = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      rank += (i < deg && (key[i] < key[j] || (key[i] == key[j] && i < j))) ? 1 : 0;
+    if (j < deg && rank < K) {
+      pick |= uint64_t(j) << (4 * n);
+      ++n;
+    }
+  }
+  return pick;
+}
 constexpr int kGroupSlots = 4;
 
 __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group,
@@ -551,14 +619,22 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
     const int64_t o = A.pa.off[p];
     A.indptr_all[pb[e] + e + i] = o - ebase[e];
     const int64_t s = A.pa.off[p + 1] - o;
-    if (s > 0 && s == A.pa.pdeg[p] && s <= kThreadTakeAll) {
-      take = int(s);
+    const int64_t deg = s > 0 ? A.pa.pdeg[p] : 0;
+    uint64_t pick = 0;
+    if (s > 0 && s == deg && s <= kThreadTakeAll) {
+      take = int(s);  // every in-edge
+    } else if (s > 0 && s < deg && deg <= kLaneSelect && excl_count(A.X, e, i) == 0) {
+      take = int(s);  // K of at most kLaneSelect in-edges
+      pick = lane_select(A, e, A.pa.plo[p], int(deg), int(s));
+    }
+    if (take) {
       const int64_t lo = A.pa.plo[p];
       L.start[lane] = o;
       L.lo[lane] = lo;
       L.src[lane] = A.es[e].indices + lo;
       L.reached[lane] = A.es[e].src_reached;
       L.rbits[lane] = A.bits ? A.es[e].src_rbits : nullptr;
+      L.pick[lane] = pick;
       L.dst[lane] = int32_t(i);
     }
   }
@@ -588,6 +664,8 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
         }
         q[u] = a;
         k[u] = t - L.tpre[a];
+        // a small selection's slot k holds its k-th kept in-edge
+        if (L.pick[a]) k[u] = int((L.pick[a] >> (4 * k[u])) & 15);
       }
     }
     int64_t g[kGroupSlots];
@@ -596,7 +674,7 @@ __device__ void role_pair_groups(const SampleArgs &A, GroupLds &L, int64_t group
 #pragma unroll
     for (int u = 0; u < kGroupSlots; ++u) {
       if (q[u] < 0) continue;
-      const int64_t pos = L.start[q[u]] + k[u];
+      const int64_t pos = L.start[q[u]] + (t0 + u * kWave + lane - L.tpre[q[u]]);
       A.src_gid[pos] = g[u];
       A.eid[pos] = L.lo[q[u]] + k[u];
       A.dst_local[pos] = L.dst[q[u]];
@@ -765,22 +843,32 @@ struct HubParams {
   __device__ bool take_all() const { return K == deg; }
 };
 
+// A value that is the same on every lane, in a scalar register.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint64_t u = uint64_t(x);
+  return int64_t(uint64_t(__builtin_amdgcn_readfirstlane(uint32_t(u))) |
+                 (uint64_t(__builtin_amdgcn_readfirstlane(uint32_t(u >> 32))) << 32));
+}
+
+// A hub's parameters; the same on every lane of the wavefront (scalar
+// registers, so that the key loop keeps its vector registers to itself).
 __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   HubParams H;
-  H.hub = hub;
-  H.first_chunk = A.pa.hub_choff[hub];
-  H.end_chunk = hub + 1 < A.n_hubs ? A.pa.hub_choff[hub + 1] : A.n_chunks;
-  const int64_t p = A.pa.hub_pair[hub];
-  H.e = A.pa.pet[p];
+  H.hub = uniform64(hub);
+  H.first_chunk = uniform64(A.pa.hub_choff[hub]);
+  H.end_chunk = uniform64(hub + 1 < A.n_hubs ? A.pa.hub_choff[hub + 1] : A.n_chunks);
+  const int64_t p = uniform64(A.pa.hub_pair[hub]);
+  H.e = int(__builtin_amdgcn_readfirstlane(uint32_t(A.pa.pet[p])));
   H.kc = key_ctx(A, H.e);
   H.L = philox_line(H.kc.k0, H.kc.k1, uint32_t(A.hop), uint32_t(H.kc.ke));
-  H.lo = A.pa.plo[p];
-  H.deg = A.pa.pdeg[p];
-  H.o = A.pa.off[p];
-  H.K = A.pa.off[p + 1] - H.o;
-  H.dst = p - A.hv.pair_base[H.e];
-  H.tau = cand_threshold(H.K, H.deg, uint64_t(1) << A.key_bits);
-  H.nx = excl_count(A.X, H.e, p - A.hv.pair_base[H.e]);
+  H.lo = uniform64(A.pa.plo[p]);
+  H.deg = uniform64(A.pa.pdeg[p]);
+  H.o = uniform64(A.pa.off[p]);
+  H.K = uniform64(A.pa.off[p + 1]) - H.o;
+  H.dst = uniform64(p - A.hv.pair_base[H.e]);
+  H.tau = uint64_t(uniform64(int64_t(cand_threshold(H.K, H.deg, uint64_t(1) << A.key_bits))));
+  H.nx = int32_t(__builtin_amdgcn_readfirstlane(
+      uint32_t(excl_count(A.X, H.e, p - A.hv.pair_base[H.e]))));
   return H;
 }
 
