@@ -108,8 +108,7 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
 // Per pair: kept edges s, hub chunks, "one wavefront" flag, hub flag.
 struct PairCounts {
   int64_t s, nch, wave, hub;
-  int64_t keys;   // random keys the sampler evaluates for the pair
-  int32_t small;  // sampled by one lane (K < deg <= kLaneSelect, nothing excluded)
+  int64_t keys;  // random keys the sampler evaluates for the pair
 };
 
 // Per edge type, what the counting pass reads for every pair; staged in
@@ -254,7 +253,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
     const int64_t p = base + k;
-    c[k] = PairCounts{0, 0, 0, 0, 0, 0};
+    c[k] = PairCounts{0, 0, 0, 0, 0};
     if (!fp[k]) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
     const int64_t deg = hi[k] - lo[k];
     const int64_t K = V.fanout(etype[k]);
@@ -268,7 +267,7 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
       c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
       c[k].hub = 1;
     } else if (nx == 0 && s < deg && deg <= kLaneSelect) {
-      c[k].small = 1;
+      // one lane of the pair-group role ranks its keys
     } else if (s > 0 && !(nx == 0 && s == deg && deg <= kThreadTakeAll)) {
       c[k].wave = 1;  // pairs with excluded edges always take this role
     }
@@ -279,15 +278,15 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
   }
 
   // the keys the sampler will evaluate: every in-edge of a pair that selects
-  // among its in-edges (one wavefront-wide sum, one atomic per wavefront)
+  // among its in-edges (wavefront sums in LDS, added up by thread 0 after the
+  // block scan's barriers: one atomic per tile)
+  __shared__ int64_t s_keys[kTileThreads / kWave];
   {
     int64_t keys = 0;
 #pragma unroll
     for (int k = 0; k < kPairItems; ++k) keys += c[k].keys;
     keys = wave_sum_i64(keys);
-    if (lane_id() == 0 && keys)
-      atomicAdd(reinterpret_cast<unsigned long long *>(small + kSlotKeys),
-                (unsigned long long)keys);
+    if (lane_id() == 0) s_keys[threadIdx.x / kWave] = keys;
   }
 
   // block scan of the per-thread sums, then the tile's prefix by look-back
@@ -301,6 +300,14 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
   }
   int64_t pre[4], agg[4];
   block_excl_scan4_256(sum, pre, agg, lds);
+  if (threadIdx.x == 0) {
+    int64_t keys = 0;
+#pragma unroll
+    for (int w = 0; w < kTileThreads / kWave; ++w) keys += s_keys[w];
+    if (keys)
+      atomicAdd(reinterpret_cast<unsigned long long *>(small + kSlotKeys),
+                (unsigned long long)keys);
+  }
   int64_t ex[4];
   tile_lookback<4>(lb, tile, 0, epoch, agg, ex, small);
 #pragma unroll
@@ -360,12 +367,18 @@ __device__ __forceinline__ EmitCtx make_ctx(const EtypeStatic &E, int64_t *src_g
 }
 
 // Marks source g reached: a plain byte store, or in bit mode an atomic OR
-// whose result is not used.
+// whose result is not used.  Both are skipped when the mark is already seen:
+// a popular source (a hub of the forward edge type, seen through its reverse)
+// is reached by many lanes of many wavefronts, and their stores to one line
+// would queue one behind the other in its L2 channel.  A stale read only
+// costs a redundant store of the same value.
 __device__ __forceinline__ void mark_reached(uint8_t *bytes, uint32_t *bits, int64_t g) {
-  if (bits)
-    atomicOr(bits + (g >> 5), 1u << (g & 31));
-  else
+  if (bits) {
+    const uint32_t m = 1u << (g & 31);
+    if ((bits[g >> 5] & m) == 0) atomicOr(bits + (g >> 5), m);
+  } else if (bytes[g] == 0) {
     bytes[g] = 1;
+  }
 }
 
 // Writes kept edge `e` at output slot `pos`; its source is reached.
