@@ -42,11 +42,12 @@ HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 # instruction occupies its SIMD for 4 cycles).  One Philox4x32-10 call of the
 # sampler (counter (g, 0, hop, etype), the lane-independent parts of rounds 0
 # and 1 in scalar registers) is 37 vector instructions (18 v_mad_u64_u32, 15
-# v_bitop3_b32, 4 v_xor_b32) and gives 4 keys; the hub loop adds 3 per call
-# (min, min3, compare) and 3 of loop control.
+# v_bitop3_b32, 4 v_xor_b32) and gives 4 keys; the hub loop adds 4 per call
+# (the lane's key group, min, min3, compare), its loop control runs on the
+# scalar unit.
 VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
 PHILOX_VALU_PER_CALL = 37
-PHILOX_LOOP_VALU_PER_CALL = 43
+PHILOX_LOOP_VALU_PER_CALL = 41
 PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 
 # Per-workload defaults (workers, bundle, steps): the launch that gives each

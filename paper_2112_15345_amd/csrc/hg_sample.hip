@@ -863,6 +863,28 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
                  (uint64_t(__builtin_amdgcn_readfirstlane(uint32_t(u >> 32))) << 32));
 }
 
+// A copy of x in a vector register.  The key loop of the hub role reads its
+// round keys from vector registers: uniform as they are, in scalar registers
+// they outnumber what the role has left, and the compiler would then fetch
+// some of them back from vector lanes on every step.
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t x) {
+  uint32_t y = x;
+  asm("" : "+v"(y));
+  return y;
+}
+__device__ __forceinline__ PhiloxLine vgpr_line(PhiloxLine L) {
+  L.ek1 = in_vgpr(L.ek1);
+  L.x1k0 = in_vgpr(L.x1k0);
+  L.hk1 = in_vgpr(L.hk1);
+  L.x3k1 = in_vgpr(L.x3k1);
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    L.k0[r] = in_vgpr(L.k0[r]);
+    L.k1[r] = in_vgpr(L.k1[r]);
+  }
+  return L;
+}
+
 // A hub's parameters; the same on every lane of the wavefront (scalar
 // registers, so that the key loop keeps its vector registers to itself).
 __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
@@ -873,7 +895,7 @@ __device__ HubParams hub_params(const SampleArgs &A, int64_t hub) {
   const int64_t p = uniform64(A.pa.hub_pair[hub]);
   H.e = int(__builtin_amdgcn_readfirstlane(uint32_t(A.pa.pet[p])));
   H.kc = key_ctx(A, H.e);
-  H.L = philox_line(H.kc.k0, H.kc.k1, uint32_t(A.hop), uint32_t(H.kc.ke));
+  H.L = vgpr_line(philox_line(H.kc.k0, H.kc.k1, uint32_t(A.hop), uint32_t(H.kc.ke)));
   H.lo = uniform64(A.pa.plo[p]);
   H.deg = uniform64(A.pa.pdeg[p]);
   H.o = uniform64(A.pa.off[p]);
@@ -1002,9 +1024,11 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w, uint64_t *buf) {
     // steps over the key groups g_first .. g_last, 64 at a time; a step whose
     // groups all lie inside the range (g_first <= ... < g_in_end) needs no
     // bounds, so only a partial first and the last steps are checked
-    const uint32_t g_first = uint32_t(uint64_t(r_lo) >> 2);
-    const uint32_t g_last = uint32_t(uint64_t(r_hi - 1) >> 2);
-    const uint32_t g_in_end = uint32_t(uint64_t(r_hi) >> 2);
+    // (wavefront-uniform: scalar registers, so that the loop below is
+    // counted and branched on by the scalar unit)
+    const uint32_t g_first = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(r_lo) >> 2));
+    const uint32_t g_last = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(r_hi - 1) >> 2));
+    const uint32_t g_in_end = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(r_hi) >> 2));
     uint32_t gb = g_first;
     if (4 * uint64_t(gb) < uint64_t(r_lo)) {
       hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, B);
@@ -1085,7 +1109,8 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   __shared__ __align__(16) uint32_t s_cand[kSampleWaves][2][kCandCap];
   static_assert(sizeof(GroupLds) <= sizeof(s_cand[0]), "a group's table fits a wavefront's LDS");
   const int64_t b = blockIdx.x;
-  const int wave = threadIdx.x / kWave;
+  // the same on every lane: what depends on it stays in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
   if (b == 0 && int(threadIdx.x) < A.n_src_out)
     A.src_out_slot[threadIdx.x] = A.src_out_new[threadIdx.x];
   // the longest wavefronts first: groups of small take-all pairs (a
