@@ -1086,13 +1086,18 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
       sel[q] = rank < K ? 1 : 0;
     }
     wave_sync();
-    // output position = kept candidates with a smaller edge ID
+    // output position = kept candidates with a smaller edge ID (below K
+    // while the list holds each edge once; a position past the pair's K
+    // slots is reported rather than written)
     for (int q = lane; q < nc; q += kWave) {
       if (!sel[q]) continue;
       const uint32_t jq = cj[q];
       int pos = 0;
       for (int t = 0; t < nc; ++t) pos += (sel[t] && cj[t] < jq) ? 1 : 0;
-      emit_edge(c, o + pos, lo + jq);
+      if (pos < K)
+        emit_edge(c, o + pos, lo + jq);
+      else
+        atomicOr(reinterpret_cast<int32_t *>(const_cast<int64_t *>(A.small) + kSlotErr), kErrBound);
     }
     return;
   }
