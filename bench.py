@@ -55,11 +55,22 @@ PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 DEFAULTS = {1: (2, 32, 320), 2: (2, 32, 320), 3: (3, 2, 40), 4: (0, 8, 64), 5: (2, 8, 64)}
 
 # HBM bytes counted by rocprofv3 (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, the
-# factors a 1 GiB device copy gives) per mini-batch, for the kernel sources and
-# launch they were measured on (profiles/ holds the runs).  Keyed by a digest
-# of the kernel and runtime sources, the workload and the bundle size; any
-# other run reports them as null.
-COUNTER_TRAFFIC = []
+# factors a 1 GiB device copy gives) per mini-batch and per launch, and the L2
+# hit rates (TCC_HIT / (TCC_HIT + TCC_MISS)), for the kernel sources and
+# launch they were measured on (profiles/ holds the runs; every dispatch of
+# the run, warm-up and profile pass included, over its mini-batches).  Keyed
+# by a digest of the kernel and runtime sources, the workload and the bundle
+# size; any other run reports them as null.
+COUNTER_TRAFFIC = [
+    {"sources": "4970012b85add24e", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 562935683, "k_sample_per_launch": 116731236,
+     "gather": 176182666, "gather_per_launch": 352365333,
+     "sample_compact_l2_hit_rate": 0.5469, "gather_l2_hit_rate": 0.3311},
+    {"sources": "4970012b85add24e", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 127596352, "k_sample_per_launch": 1087793625,
+     "gather": 249271683, "gather_per_launch": 1994173465,
+     "sample_compact_l2_hit_rate": 0.648, "gather_l2_hit_rate": 0.3327},
+]
 
 
 def kernel_sources_digest():
@@ -426,7 +437,8 @@ def vertex_main(args, wl, gen, g):
               "bound": "host link" if args.host_features else "hbm",
               "ms_per_step": gather_ms / steps,
               "algorithmic_bytes_per_step": g_alg / steps,
-              "traffic_per_step": traffic["gather"] if traffic else None}
+              "traffic_per_step": traffic["gather"] if traffic else None,
+              "l2_hit_rate": traffic.get("gather_l2_hit_rate") if traffic else None}
     sample_s = sample_ms / 1e3
     philox = {"keys_per_step": keys / steps,
               "keys_per_s": keys / sample_s if sample_s > 0 else None,
@@ -451,6 +463,7 @@ def vertex_main(args, wl, gen, g):
         sc["counter_GBps"] = rate
         sc["counter_frac"] = rate / HBM_PEAK_GBS
         sc["counter_over_algorithmic"] = traffic["sample_compact"] / (prof_alg / prof_steps)
+        sc["l2_hit_rate"] = traffic.get("sample_compact_l2_hit_rate")
     # the roofline of the kernel with the most device time (from the profile
     # pass), its rate measured over the timed region
     per_kernel = dict(stage_ms, gather=prof_gather_ms)
