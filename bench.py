@@ -54,7 +54,7 @@ PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 
 # Per-workload defaults (workers, bundle, steps): the launch that gives each
 # workload its best throughput on one MI355X.
-DEFAULTS = {1: (2, 32, 320), 2: (2, 32, 320), 3: (3, 2, 40), 4: (0, 8, 64), 5: (2, 8, 64)}
+DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (3, 8, 96)}
 
 # HBM bytes counted by rocprofv3 (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, the
 # factors a 1 GiB device copy gives) per mini-batch and per launch, and the L2
