@@ -43,13 +43,13 @@ HOST_LINK_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 # sampler (counter (g, 0, hop, etype), the lane-independent parts of rounds 0
 # and 1 in scalar registers) is 37 vector instructions (18 v_mad_u64_u32, 15
 # v_bitop3_b32, 4 v_xor_b32) and gives 4 keys.  The key-loop kernel of
-# --mode philox adds 3 per call (min, min3, compare: the candidate test), the
-# sampler's hub loop 4 (also the lane's key group); both loops are counted and
-# branched on by the scalar unit.
+# --mode philox and the sampler's hub loop add 3 per call (min, min3, compare:
+# the candidate test); both loops are counted and branched on by the scalar
+# unit.
 VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
 PHILOX_VALU_PER_CALL = 37
 PHILOX_LOOP_VALU_PER_CALL = 40
-PHILOX_HUB_VALU_PER_CALL = 41
+PHILOX_HUB_VALU_PER_CALL = 40
 PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 
 # Per-workload defaults (workers, bundle, steps): the launch that gives each

@@ -382,9 +382,8 @@ __device__ __forceinline__ PhiloxLine philox_line(uint32_t k0, uint32_t k1, uint
   return L;
 }
 
-__device__ __forceinline__ U32x4 philox_keys(const PhiloxLine &L, uint32_t g) {
-  // round 0: p0 = M0 * g
-  uint64_t p0 = uint64_t(0xD2511F53u) * g;
+// The keys of group g given round 0's product p0 = M0 * g (64 bits).
+__device__ __forceinline__ U32x4 philox_keys_p0(const PhiloxLine &L, uint64_t p0) {
   uint32_t x2 = uint32_t(p0 >> 32) ^ L.ek1;
   uint32_t x3 = uint32_t(p0);
   // round 1: p1 = M1 * x2 (p0 is the line's)
@@ -409,6 +408,10 @@ __device__ __forceinline__ U32x4 philox_keys(const PhiloxLine &L, uint32_t g) {
     x3 = uint32_t(p0);
   }
   return U32x4{x0, x1, x2, x3};
+}
+
+__device__ __forceinline__ U32x4 philox_keys(const PhiloxLine &L, uint32_t g) {
+  return philox_keys_p0(L, uint64_t(0xD2511F53u) * g);  // round 0: p0 = M0 * g
 }
 
 }  // namespace hg

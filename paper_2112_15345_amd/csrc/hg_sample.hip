@@ -940,10 +940,14 @@ __device__ void hub_flush(const SampleArgs &A, int64_t hub, HubBuf &B) {
 template <bool kChecked>
 __device__ __forceinline__ void hub_step(const SampleArgs &A, const HubParams &H,
                                          uint32_t gb, int64_t c_lo, int64_t c_hi,
-                                         uint32_t lim, uint32_t shift, HubBuf &B) {
+                                         uint32_t lim, uint32_t shift, uint32_t m0v,
+                                         HubBuf &B) {
   const int lane = lane_id();
   const uint32_t g = gb + uint32_t(lane);
-  const U32x4 r = philox_keys(H.L, g);
+  // round 0's product M0 * (gb + lane) as one multiply-add: M0 (m0v, in a
+  // vector register) * lane plus the wavefront's M0 * gb (scalar registers),
+  // so the step needs no add for g
+  const U32x4 r = philox_keys_p0(H.L, uint64_t(m0v) * uint32_t(lane) + uint64_t(0xD2511F53u) * gb);
   if (!kChecked) {
     const uint32_t m = min(min(r.x, r.y), min(r.z, r.w));
     if (__ballot(m <= lim) == 0) return;
@@ -1029,14 +1033,15 @@ __device__ void role_hub_chunks(const SampleArgs &A, int64_t w, uint64_t *buf) {
     const uint32_t g_first = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(r_lo) >> 2));
     const uint32_t g_last = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(r_hi - 1) >> 2));
     const uint32_t g_in_end = __builtin_amdgcn_readfirstlane(uint32_t(uint64_t(r_hi) >> 2));
+    const uint32_t m0v = in_vgpr(0xD2511F53u);
     uint32_t gb = g_first;
     if (4 * uint64_t(gb) < uint64_t(r_lo)) {
-      hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, B);
+      hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, m0v, B);
       gb += kWave;
     }
     for (; gb + kWave <= g_in_end; gb += kWave)
-      hub_step<false>(A, H, gb, r_lo, r_hi, lim, shift, B);
-    for (; gb <= g_last; gb += kWave) hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, B);
+      hub_step<false>(A, H, gb, r_lo, r_hi, lim, shift, m0v, B);
+    for (; gb <= g_last; gb += kWave) hub_step<true>(A, H, gb, r_lo, r_hi, lim, shift, m0v, B);
   }
   hub_flush(A, H.hub, B);
 }
