@@ -57,21 +57,22 @@ PHILOX_PEAK_KEYS = VALU_LANE_OPS * 4 / PHILOX_VALU_PER_CALL
 DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (3, 8, 96)}
 
 # HBM bytes counted by rocprofv3 (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000, the
-# factors a 1 GiB device copy gives) per mini-batch and per launch, and the L2
+# factors a 1 GiB device copy gives) per mini-batch and per launch (the gather's:
+# per bundle, all its launches), and the L2
 # hit rates (TCC_HIT / (TCC_HIT + TCC_MISS)), for the kernel sources and
 # launch they were measured on (profiles/ holds the runs; every dispatch of
 # the run, warm-up and profile pass included, over its mini-batches).  Keyed
 # by a digest of the kernel and runtime sources, the workload and the bundle
 # size; any other run reports them as null.
 COUNTER_TRAFFIC = [
-    {"sources": "4970012b85add24e", "workload": 3, "bundle": 2, "task": "vertex",
-     "sample_compact": 562935683, "k_sample_per_launch": 116731236,
-     "gather": 176182666, "gather_per_launch": 352365333,
-     "sample_compact_l2_hit_rate": 0.5469, "gather_l2_hit_rate": 0.3311},
-    {"sources": "4970012b85add24e", "workload": 2, "bundle": 32, "task": "vertex",
-     "sample_compact": 127596352, "k_sample_per_launch": 1087793625,
-     "gather": 249271683, "gather_per_launch": 1994173465,
-     "sample_compact_l2_hit_rate": 0.648, "gather_l2_hit_rate": 0.3327},
+    {"sources": "d9c6b4ba0cbd6560", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 562774068, "k_sample_per_launch": 116748555,
+     "gather": 176202856, "gather_per_launch": 352405712,
+     "sample_compact_l2_hit_rate": 0.5466, "gather_l2_hit_rate": 0.3311},
+    {"sources": "d9c6b4ba0cbd6560", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 127725346, "k_sample_per_launch": 1088521471,
+     "gather": 249219173, "gather_per_launch": 7975013536,
+     "sample_compact_l2_hit_rate": 0.6487, "gather_l2_hit_rate": 0.3327},
 ]
 
 
