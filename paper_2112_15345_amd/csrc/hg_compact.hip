@@ -3,11 +3,11 @@
 // compaction relabels vertices and edges).
 //
 // The newly reached vertices of a node type are deduplicated and put in
-// ascending ID order with one flag per vertex: the sampler stores 1 into the
-// reached byte of every kept source v, and the new vertices are the reached
-// vertices whose frontier bit is clear; a prefix count of those (per node
-// type) then gives each one its rank, which is its position among the new
-// vertices.
+// ascending ID order with one mark per vertex: the sampler marks every kept
+// source v reached (a byte, or a bit laid out as the frontier bits), and the
+// new vertices are the reached vertices whose frontier bit is clear; a prefix
+// count of those (per node type) then gives each one its rank, which is its
+// position among the new vertices.
 // The count is a reduce-then-scan over kTile-word tiles in three launches
 // (count per tile; scan of the tile counts; rank and assign), which needs no
 // inter-block waiting.  A dense int32 map (vertex -> local ID, meaningful while

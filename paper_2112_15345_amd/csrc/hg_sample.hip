@@ -8,14 +8,18 @@
 // under the sampling seed.  Kept edges are written grouped by pair, ascending
 // edge ID within a pair.
 //
-// Work is split by pair shape: small take-all pairs run one per thread; other
-// pairs one per wavefront; pairs that select among more than kHubChunk edges
-// ("hubs") are cut into chunks of kHubChunk edges, handed to wavefronts in
-// runs of consecutive chunks, which append their candidates to a per-hub
-// list; a second launch then selects each hub's K edges from its list.  Every
-// edge key is computed once.  Pairs of more than kHubChunk edges that keep
-// all of them (none excluded) are hubs too: their chunks are copied straight
-// to the output, and the second launch skips them.
+// Work is split by pair shape: a wavefront takes 64 consecutive pairs and
+// writes the kept edges of those that keep every one of at most
+// kThreadTakeAll in-edges or select among at most kLaneSelect (one lane ranks
+// such a pair's keys); other pairs run one per wavefront; pairs that select
+// among more than kHubChunk edges ("hubs") are cut into chunks of kHubChunk
+// edges, handed to wavefronts in runs of consecutive chunks, which append
+// their candidates to a per-hub list; a second launch then selects each hub's
+// K edges from its list.  Every edge key is computed once.  Pairs of more
+// than kHubChunk edges that keep all of them (none excluded) are hubs too:
+// their chunks are copied straight to the output, and the second launch skips
+// them.  Every kept edge marks its source reached (a byte, or a bit on hops
+// that keep few edges next to the graph's vertices) for the compaction.
 #include <hip/hip_ext.h>
 
 #include <algorithm>
