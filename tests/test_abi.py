@@ -57,3 +57,40 @@ def test_library_argument_checks_without_device(lib):
     assert hg._lib.hg_pipeline_submit_layers(None, 1, None, None, 1, None, None) == hg.HG_EINVAL
     assert hg._lib.hg_pipeline_submit_edges(None, 1, None, 1, None, None) == hg.HG_EINVAL
     hg._lib.hg_pipeline_destroy(None)
+
+
+def test_create_descriptor_checks_without_device(lib):
+    """hg_create validates every descriptor before it makes any HIP call, so
+    these run on the CPU; the pointers are never dereferenced (fake, non-NULL).
+    An edge type of 2^32 edges or more is refused with HG_EUNSUPPORTED: edge
+    IDs enter the key counter as (eid >> 2) below 2^30, and the sampler's
+    per-hub edge offsets are 32-bit."""
+    import paper_2112_15345_amd as hg
+    hg.load_library()
+    fake = ctypes.c_void_p(0x1000)
+    out = ctypes.c_void_p()
+
+    def create(nt, et):
+        nts = (hg.NTypeDesc * len(nt))(*nt)
+        ets = (hg.ETypeDesc * max(len(et), 1))(*et)
+        return hg._lib.hg_create(nts, len(nt), ets, len(et), None, None, ctypes.byref(out))
+
+    def nt(n=10, feat=None, dtype=0, dim=0):
+        return hg.NTypeDesc(n, feat, dtype, dim)
+
+    def et(src=0, dst=0, nnz=5, indptr=fake, indices=fake):
+        return hg.ETypeDesc(src, dst, nnz, indptr, indices)
+
+    assert create([nt(-1)], []) == hg.HG_EINVAL
+    assert b"negative num_nodes" in hg._lib.hg_last_error()
+    assert create([nt(dtype=7, dim=4, feat=fake)], []) == hg.HG_EINVAL
+    assert create([nt(dtype=hg.HG_DT_F32, dim=0, feat=fake)], []) == hg.HG_EINVAL
+    assert create([nt(dtype=hg.HG_DT_F32, dim=4, feat=None)], []) == hg.HG_EINVAL
+    assert create([nt()], [et(src=1)]) == hg.HG_EINVAL
+    assert b"node type out of range" in hg._lib.hg_last_error()
+    assert create([nt()], [et(indptr=None)]) == hg.HG_EINVAL
+    assert create([nt()], [et(indices=None)]) == hg.HG_EINVAL
+    assert create([nt()], [et(nnz=-1)]) == hg.HG_EINVAL
+    assert create([nt()], [et(nnz=1 << 32)]) == hg.HG_EUNSUPPORTED
+    assert b"below 2^32" in hg._lib.hg_last_error()
+    assert out.value is None
