@@ -238,11 +238,35 @@ def step_bytes_model(g, nd, ns, ne):
     return total
 
 
-def oracle_check(args, wl, gen, fan, kept, cpu):
-    """The oracle's OpenMP build (the same oracle.c on every host core) on the
-    first timed mini-batches: their timing is the CPU baseline, and every block
-    array of the GPU's result must equal the oracle's; the gathered feature
-    bytes must equal the rows of the oracle's input frontier."""
+def blocks_equal(a, b, H, T, R, feat_types):
+    """Every block array and every gathered feature byte of two results."""
+    import torch
+    for h in range(H):
+        for t in range(T):
+            na, sa = a.nodes(h, t)
+            nb, sb = b.nodes(h, t)
+            if na != nb or not torch.equal(sa, sb):
+                return False
+        for e in range(R):
+            for x, y in zip(a.edges(h, e), b.edges(h, e)):
+                if x.dtype != y.dtype or not torch.equal(x, y):
+                    return False
+    for t in feat_types:
+        if not torch.equal(a.features(t).view(torch.uint8), b.features(t).view(torch.uint8)):
+            return False
+    return True
+
+
+def oracle_check(args, wl, gen, fan, kept, cpu, timed, recompute):
+    """Every timed mini-batch (or the first --check-batches of them) against
+    the oracle's OpenMP build (the same oracle.c on every host core): every
+    block array must equal the oracle's and the gathered feature bytes the
+    rows of the oracle's input frontier.  The timed region keeps only its
+    first results (a whole run's gathered rows would not fit), so each timed
+    unit is made again after the clock, with the same bundles, seeds and
+    sampling seeds; the results the timed region kept must equal those made
+    again, bit for bit.  The oracle's time over the first batches, up to
+    --cpu-budget seconds, is the CPU baseline."""
     import numpy as np
     import torch
 
@@ -254,52 +278,77 @@ def oracle_check(args, wl, gen, fan, kept, cpu):
     host = oracle.HostGraph(host_nt, gen.host_etypes(), check=False, lib=oracle.load_omp())
     log(f"oracle host copy of the graph in {time.perf_counter() - t0:.1f}s")
     threads = oracle.threads(host.lib)
-    spent, edges, checked, bad = 0.0, 0, [], []
-    for b, blocks in kept:
-        seeds = W.seeds_per_type(wl, b)
-        t = time.perf_counter()
-        ref = host.sample_blocks(seeds, fan, b)
-        spent += time.perf_counter() - t
-        edges += sum(v[3].size for v in ref["edges"].values())
-        ok = True
-        for h in range(len(fan)):
-            for ti in range(len(gen.num_nodes)):
-                n_dst, sg = blocks.nodes(h, ti)
-                if n_dst != ref["nodes"][(h, ti)][0] or \
-                        not np.array_equal(sg.cpu().numpy(), ref["nodes"][(h, ti)][1]):
-                    ok = False
-            for e in range(len(gen.etypes)):
-                for x, y in zip(blocks.edges(h, e), ref["edges"][(h, e)]):
-                    xn = x.cpu().numpy()
-                    if xn.dtype != y.dtype or not np.array_equal(xn, y):
-                        ok = False
-        for ti, f in enumerate(gen.feats):
-            if f is None:
-                continue
-            ids = torch.as_tensor(ref["input"][ti], device=f.device)
-            got = blocks.features(ti)
-            want = f.index_select(0, ids).to(got.device)
-            if not torch.equal(got.view(torch.uint8), want.view(torch.uint8)):
-                ok = False
-        checked.append(b)
-        if not ok:
-            bad.append(b)
-        log(f"oracle batch {b}: {'equal' if ok else 'DIFFERENT'} "
-            f"({time.perf_counter() - t:.1f}s on {threads} threads)")
-        if cpu and spent >= args.cpu_budget:
+    feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
+    H, T, R = len(fan), len(gen.num_nodes), len(gen.etypes)
+    kept_map = dict(kept)
+    n_timed = sum(len(u) for u in timed)
+    limit = n_timed if args.check_batches < 0 else min(args.check_batches, n_timed)
+    spent, edges, timed_b, checked, bad, same = 0.0, 0, [], [], [], []
+    for u in timed:
+        if len(checked) >= limit:
             break
-    parity = {"batches": checked, "equal": not bad, "different": bad,
+        blist = recompute(u)
+        for b, blocks in zip(u, blist):
+            if len(checked) >= limit:
+                break
+            ok = True
+            if b in kept_map:
+                same.append(b)
+                if not blocks_equal(kept_map[b], blocks, H, T, R, feat_types):
+                    ok = False
+                    log(f"batch {b}: the timed result and the one made again differ")
+            seeds = W.seeds_per_type(wl, b)
+            t = time.perf_counter()
+            ref = host.sample_blocks(seeds, fan, b)
+            dt = time.perf_counter() - t
+            if cpu and spent < args.cpu_budget:
+                spent += dt
+                edges += sum(v[3].size for v in ref["edges"].values())
+                timed_b.append(b)
+            for h in range(H):
+                for ti in range(T):
+                    n_dst, sg = blocks.nodes(h, ti)
+                    if n_dst != ref["nodes"][(h, ti)][0] or \
+                            not np.array_equal(sg.cpu().numpy(), ref["nodes"][(h, ti)][1]):
+                        ok = False
+                for e in range(R):
+                    for x, y in zip(blocks.edges(h, e), ref["edges"][(h, e)]):
+                        xn = x.cpu().numpy()
+                        if xn.dtype != y.dtype or not np.array_equal(xn, y):
+                            ok = False
+            for ti in feat_types:
+                f = gen.feats[ti]
+                ids = torch.as_tensor(ref["input"][ti], device=f.device)
+                got = blocks.features(ti)
+                want = f.index_select(0, ids).to(got.device)
+                if not torch.equal(got.view(torch.uint8), want.view(torch.uint8)):
+                    ok = False
+            checked.append(b)
+            if not ok:
+                bad.append(b)
+            log(f"oracle batch {b}: {'equal' if ok else 'DIFFERENT'} "
+                f"({dt:.1f}s on {threads} threads)")
+            del ref
+        del blist
+    parity = {"batches": checked, "of_timed": n_timed, "equal": not bad, "different": bad,
+              "timed_results_equal_remade": same,
               "what": "every block array (frontiers, source lists, CSC, COO local IDs, edge "
-                      "IDs) and every gathered feature byte, element by element"}
-    base = {"value": edges / spent if spent > 0 else None, "unit": "sampled edges/s",
-            "cores": threads, "kind": "oracle",
-            "sample": f"{len(checked)} whole timed mini-batches (batches {checked[0]}.."
-                      f"{checked[-1]}) of the same workload: sampling and compaction by the "
-                      f"OpenMP build of the oracle (pairs, relabel and gather loops on every "
-                      f"host core), {edges} sampled edges in {spent:.2f} s; the feature "
-                      f"gather is checked on the GPU against the oracle's input frontier "
-                      f"rather than timed on the host",
-            **host_info()}
+                      "IDs) and every gathered feature byte, element by element; the timed "
+                      "units are made again after the clock (same bundles, seeds and "
+                      "sampling seeds) and the results the timed region kept equal them bit "
+                      "for bit"}
+    base = None
+    if cpu and timed_b:
+        base = {"value": edges / spent if spent > 0 else None, "unit": "sampled edges/s",
+                "cores": threads, "kind": "oracle",
+                "sample": f"{len(timed_b)} whole timed mini-batches (batches {timed_b[0]}.."
+                          f"{timed_b[-1]}) of the same workload, about {args.cpu_budget:.0f} s "
+                          f"of CPU work: sampling and compaction by the OpenMP build of the "
+                          f"oracle (pairs, relabel and gather loops on every host core), "
+                          f"{edges} sampled edges in {spent:.2f} s; the feature gather is "
+                          f"checked on the GPU against the oracle's input frontier rather than "
+                          f"timed on the host",
+                **host_info()}
     return parity, base
 
 
@@ -361,7 +410,7 @@ def vertex_main(args, wl, gen, g):
             ne += np.asarray(blocks.edge_counts(), np.int64).reshape(H, g.R)
             for t in feat_types:
                 rows[t] += blocks.num_input_nodes(t)
-            if len(kept) < args.check_batches:
+            if len(kept) < 2:  # compared with the same units made again after the clock
                 kept.append((b, blocks))
         rec.append((u, t_done, int(ne.sum()), rows, nd, ns, keys, ne))
 
@@ -529,8 +578,13 @@ def vertex_main(args, wl, gen, g):
         "sample_compact": sc,
         "philox": philox,
     }
-    if not args.no_cpu_baseline or args.check_batches > 0:
-        parity, base = oracle_check(args, wl, gen, fan, kept, cpu=not args.no_cpu_baseline)
+    if not args.no_cpu_baseline or args.check_batches != 0:
+        def remake(u):  # the timed unit again: direct call, no events
+            blist = g.sample_bundle([seeds[b] for b in u], fan, u, gather=feat_types)
+            torch.cuda.synchronize()
+            return blist
+        parity, base = oracle_check(args, wl, gen, fan, kept, not args.no_cpu_baseline, timed,
+                                    remake)
         result["parity"] = parity
         if not args.no_cpu_baseline:
             result["cpu_baseline"] = base
@@ -749,8 +803,8 @@ def main():
                          "bundle)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check-batches", type=int, default=None,
-                    help="timed mini-batches compared with the oracle (default 2 for workload "
-                         "3, else 8); 0 skips the check")
+                    help="timed mini-batches compared with the oracle, from the first (default "
+                         "-1: every one); 0 skips the check")
     ap.add_argument("--profile-units", type=int, default=4,
                     help="timed units re-run after the timed region with every stage timed")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
@@ -781,7 +835,7 @@ def main():
     if args.steps is None:
         args.steps = ds
     if args.check_batches is None:
-        args.check_batches = 2 if args.workload == 3 else 8
+        args.check_batches = -1  # every timed mini-batch
 
     import torch
 
