@@ -339,6 +339,28 @@ def oracle_check(args, wl, gen, fan, kept, cpu, timed, recompute):
                       "for bit"}
     base = None
     if cpu and timed_b:
+        # the plain (one-thread) build too, when a mini-batch fits the budget
+        # on one core (the OpenMP time times its threads bounds it from above)
+        per_batch = spent / len(timed_b)
+        if per_batch * threads <= args.cpu_budget:
+            plain = oracle.HostGraph(host_nt, [(a, b_, ip, ix) for a, b_, ip, ix in host.etypes],
+                                     check=False, lib=oracle.load())
+            s_spent, s_edges, s_b = 0.0, 0, []
+            for b in timed_b:
+                t = time.perf_counter()
+                ref = plain.sample_blocks(W.seeds_per_type(wl, b), fan, b)
+                s_spent += time.perf_counter() - t
+                s_edges += sum(v[3].size for v in ref["edges"].values())
+                s_b.append(b)
+                if s_spent >= args.cpu_budget:
+                    break
+            single = {"value": s_edges / s_spent if s_spent > 0 else None,
+                      "unit": "sampled edges/s", "cores": 1,
+                      "sample": f"{len(s_b)} of the same mini-batches, the plain build"}
+        else:
+            single = {"value": None, "cores": 1,
+                      "sample": f"not run: one mini-batch would take up to "
+                                f"{per_batch * threads:.0f} s on one core"}
         base = {"value": edges / spent if spent > 0 else None, "unit": "sampled edges/s",
                 "cores": threads, "kind": "oracle",
                 "sample": f"{len(timed_b)} whole timed mini-batches (batches {timed_b[0]}.."
@@ -348,6 +370,7 @@ def oracle_check(args, wl, gen, fan, kept, cpu, timed, recompute):
                           f"{edges} sampled edges in {spent:.2f} s; the feature gather is "
                           f"checked on the GPU against the oracle's input frontier rather than "
                           f"timed on the host",
+                "single_thread": single,
                 **host_info()}
     return parity, base
 
