@@ -494,10 +494,10 @@ def vertex_main(args, wl, gen, g):
     loop_keys_s = 4 * n_groups / (loop_ms / 1e3)
     del cnt
 
-    # context for the peak: a plain 1 GiB device-to-device copy, best of 6
+    # context for the peak: a plain 4 GiB device-to-device copy, best of 6
     copy_gbps = None
     if not args.host_features:
-        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        src = torch.ones(1 << 32, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         best = None
