@@ -370,17 +370,18 @@ __device__ __forceinline__ EmitCtx make_ctx(const EtypeStatic &E, int64_t *src_g
                  dst_local, int32_t(dst)};
 }
 
-// Marks source g reached: a plain byte store, or in bit mode an atomic OR
-// whose result is not used.  Both are skipped when the mark is already seen:
-// a popular source (a hub of the forward edge type, seen through its reverse)
-// is reached by many lanes of many wavefronts, and their stores to one line
-// would queue one behind the other in its L2 channel.  A stale read only
-// costs a redundant store of the same value.
+// Marks source g reached: in bit mode an atomic OR whose result is not used,
+// skipped when the bit is already seen; otherwise a plain byte store.  A
+// popular source (a hub of the forward edge type, seen through its reverse)
+// is reached by many lanes of many wavefronts, and atomics on one word queue
+// one behind the other in its L2 channel; reading first lets all but the
+// first few pass by (a stale read only costs a redundant atomic).  Plain byte
+// stores do not wait on each other, and reading first would cost them a load.
 __device__ __forceinline__ void mark_reached(uint8_t *bytes, uint32_t *bits, int64_t g) {
   if (bits) {
     const uint32_t m = 1u << (g & 31);
     if ((bits[g >> 5] & m) == 0) atomicOr(bits + (g >> 5), m);
-  } else if (bytes[g] == 0) {
+  } else {
     bytes[g] = 1;
   }
 }
