@@ -65,14 +65,14 @@ DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (
 # by a digest of the kernel and runtime sources, the workload and the bundle
 # size; any other run reports them as null.
 COUNTER_TRAFFIC = [
-    {"sources": "a8cb687331824b69", "workload": 3, "bundle": 2, "task": "vertex",
-     "sample_compact": 562774068, "k_sample_per_launch": 116748555,
-     "gather": 176202856, "gather_per_launch": 352405712,
-     "sample_compact_l2_hit_rate": 0.5466, "gather_l2_hit_rate": 0.3311},
-    {"sources": "a8cb687331824b69", "workload": 2, "bundle": 32, "task": "vertex",
-     "sample_compact": 127725346, "k_sample_per_launch": 1088521471,
-     "gather": 249219173, "gather_per_launch": 7975013536,
-     "sample_compact_l2_hit_rate": 0.6487, "gather_l2_hit_rate": 0.3327},
+    {"sources": "502b89d8976af3d0", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 562718768, "k_sample_per_launch": 116732933,
+     "gather": 176188015, "gather_per_launch": 352376030,
+     "sample_compact_l2_hit_rate": 0.5475, "gather_l2_hit_rate": 0.3311},
+    {"sources": "502b89d8976af3d0", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 98874838, "k_sample_per_launch": 645459349,
+     "gather": 249219134, "gather_per_launch": 7975012288,
+     "sample_compact_l2_hit_rate": 0.6117, "gather_l2_hit_rate": 0.3327},
 ]
 
 
