@@ -188,7 +188,7 @@ def test_tiny_workload_batches(olib):
     hgraph = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes(), lib=olib)
     g = hg.Graph([(n, f.cuda()) for n, f in zip(gen.num_nodes, gen.feats)],
                  [(s, d, ip.cuda(), ix.cuda()) for s, d, ip, ix in gen.etypes])
-    for bno in range(10):
+    for bno in range(20):
         seeds = W.seeds_per_type(wl, bno)
         say(f"tiny workload batch {bno}")
         b = g.sample_blocks(gpu_seeds(seeds), wl.fanout_matrix(), bno)
