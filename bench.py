@@ -466,7 +466,7 @@ def vertex_main(args, wl, gen, g):
     # stream, every stage's launches carrying events
     prof_units = timed[:max(1, min(len(timed), args.profile_units))]
     stage_ms = {name: 0.0 for name in hg.STAGE_NAMES}
-    prof_alg = prof_steps = 0
+    prof_alg = prof_steps = prof_keys = 0
     prof_gather_ms = 0.0
     for u in prof_units:
         ev = hg.StageEvents(H)
@@ -480,6 +480,7 @@ def vertex_main(args, wl, gen, g):
         ns = sum(b.counts()[1] for b in blist)
         ne = sum(np.asarray(b.edge_counts(), np.int64).reshape(H, g.R) for b in blist)
         prof_alg += step_bytes_model(g, nd, ns, ne)
+        prof_keys += int(np.asarray(blist[0].counts()[2]).sum())  # the bundle's keys
         prof_steps += len(u)
         del blist
     sc_ms = sum(stage_ms.values())
@@ -568,6 +569,13 @@ def vertex_main(args, wl, gen, g):
                     "algorithmic_per_launch": keys / sample_launches,
                     "avg_launch_us": sample_ms / sample_launches * 1e3,
                     "peak_source": philox["peak_derivation"]}
+        # the same launches alone on the GPU: the profile pass (one stream)
+        if stage_ms["sample"] > 0:
+            alone = prof_keys / (stage_ms["sample"] / 1e3) / 1e9
+            roofline["alone"] = {
+                "achieved": alone, "frac": alone / (PHILOX_PEAK_KEYS / 1e9),
+                "measured": "profile pass (the first timed units again, direct calls on one "
+                            "stream): k_sample launches with nothing beside them"}
         if dominant != "sample":
             roofline["note"] = (f"the {dominant} stage has the most device time; the sampler's "
                                 f"roofline is reported")
