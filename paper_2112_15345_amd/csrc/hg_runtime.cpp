@@ -246,7 +246,6 @@ struct hg_graph {
 };
 
 namespace {
-void dev_free(hg_graph *g, void *p, hipStream_t s);
 void layout_types(hg_graph *g);
 void free_graph(hg_graph *g);
 // Mini-batches per bundle at most.
@@ -319,14 +318,6 @@ void *dev_alloc(hg_graph *g, size_t bytes, hipStream_t s) {
     return nullptr;
   }
   return p;
-}
-
-void dev_free(hg_graph *g, void *p, hipStream_t s) {
-  if (!p) return;
-  if (g->has_alloc)
-    g->alloc.free(g->alloc.ctx, p, s);
-  else
-    (void)hipFreeAsync(p, s);
 }
 
 }  // namespace
