@@ -65,14 +65,14 @@ DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (
 # by a digest of the kernel and runtime sources, the workload and the bundle
 # size; any other run reports them as null.
 COUNTER_TRAFFIC = [
-    {"sources": "502b89d8976af3d0", "workload": 3, "bundle": 2, "task": "vertex",
-     "sample_compact": 562718768, "k_sample_per_launch": 116732933,
-     "gather": 176188015, "gather_per_launch": 352376030,
-     "sample_compact_l2_hit_rate": 0.5475, "gather_l2_hit_rate": 0.3311},
-    {"sources": "502b89d8976af3d0", "workload": 2, "bundle": 32, "task": "vertex",
-     "sample_compact": 98874838, "k_sample_per_launch": 645459349,
-     "gather": 249219134, "gather_per_launch": 7975012288,
-     "sample_compact_l2_hit_rate": 0.6117, "gather_l2_hit_rate": 0.3327},
+    {"sources": "5da65d0a0d0bd4da", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 562763614, "k_sample_per_launch": 116733800,
+     "gather": 176184806, "gather_per_launch": 352369612,
+     "sample_compact_l2_hit_rate": 0.5468, "gather_l2_hit_rate": 0.3311},
+    {"sources": "5da65d0a0d0bd4da", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 98869314, "k_sample_per_launch": 645453349,
+     "gather": 249220461, "gather_per_launch": 7975054752,
+     "sample_compact_l2_hit_rate": 0.6124, "gather_l2_hit_rate": 0.3328},
 ]
 
 
