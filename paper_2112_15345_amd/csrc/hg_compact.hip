@@ -20,9 +20,6 @@ namespace hg {
 
 namespace {
 
-__device__ __forceinline__ int64_t gs_start() {
-  return int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-}
 __device__ __forceinline__ int64_t gs_step() {
   return int64_t(gridDim.x) * blockDim.x;
 }
@@ -264,7 +261,7 @@ __global__ __launch_bounds__(256) void k_relabel(HopView hv, HopView next, const
                                                  const int64_t *tile_base, const int64_t *small,
                                                  int32_t n_types, int32_t n_etypes,
                                                  int64_t n_edges, const int64_t *src_gid,
-                                                 int32_t *src_local) {
+                                                 int32_t *src_local, bool xcd) {
   extern __shared__ __align__(16) char relabel_lds[];
   if (blockIdx.x == 0)
     plan_next_hop(hv, next, es, tile_base, small, n_types, n_etypes);
@@ -278,8 +275,11 @@ __global__ __launch_bounds__(256) void k_relabel(HopView hv, HopView next, const
     }
     __syncthreads();
   }
+  // the grid is a multiple of kXcds blocks, so that its blocks can be ordered
+  // per XCD (xcd_block): a mini-batch's map lines then stay in one L2
   const int64_t step = gs_step();
-  for (int64_t j0 = gs_start(); j0 < n_edges; j0 += kRelabelItems * step) {
+  for (int64_t j0 = xcd_block(blockIdx.x, gridDim.x, xcd) * blockDim.x + threadIdx.x;
+       j0 < n_edges; j0 += kRelabelItems * step) {
     int64_t g[kRelabelItems];
     int32_t *m[kRelabelItems];
 #pragma unroll
@@ -339,16 +339,17 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
-                          hipStream_t stream, StageEv ev) {
+                          hipStream_t stream, StageEv ev, bool xcd_order) {
   // at least one block: block 0 plans the next hop
-  const unsigned grid = grid_for((n_edges + kRelabelItems - 1) / kRelabelItems, 256, 1 << 20);
+  const unsigned grid =
+      unsigned(xcd_round(grid_for((n_edges + kRelabelItems - 1) / kRelabelItems, 256, 1 << 20)));
   if (n_etypes <= kRelabelMaxEtypes)
     launch_k(k_relabel<true>, dim3(grid), dim3(256), size_t(16) * (n_etypes + 1), stream,
              ev.start, ev.stop, hv, next, es, tile_base, small, n_types, n_etypes, n_edges,
-             src_gid, src_local);
+             src_gid, src_local, xcd_order);
   else
     launch_k(k_relabel<false>, dim3(grid), dim3(256), 0, stream, ev.start, ev.stop, hv, next,
-             es, tile_base, small, n_types, n_etypes, n_edges, src_gid, src_local);
+             es, tile_base, small, n_types, n_etypes, n_edges, src_gid, src_local, xcd_order);
   return hipGetLastError();
 }
 

@@ -24,6 +24,18 @@ inline void launch_k(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t st
     hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
 }
 
+// Workgroup b goes to XCD b % kXcds.  A range of n blocks that starts at a
+// multiple of kXcds, with n a multiple of kXcds, is reordered by xcd_block so
+// that XCD x runs the x-th eighth of the range's work, in order: lines that a
+// stretch of consecutive work shares (reached marks and map entries of the same
+// mini-batch) are then cached, and written back, by one L2 instead of all
+// eight.  A bijection of [0, n): any dispatch order still does every block once.
+// With `on` false it is the identity.
+inline int64_t xcd_round(int64_t n) { return (n + kXcds - 1) / kXcds * kXcds; }
+__device__ __forceinline__ int64_t xcd_block(int64_t r, int64_t n, bool on) {
+  return on ? (r % kXcds) * (n / kXcds) + r / kXcds : r;
+}
+
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 // Bit mask of the lanes below this one.

@@ -113,6 +113,10 @@ struct TypeStatic {
 // without return), so that the compaction reads an eighth of the bytes.
 // Bit mode is chosen when vertices > kBitModeRatio x kept edges.
 constexpr int64_t kBitModeRatio = 16;
+// The chip's XCDs, each with its own L2; workgroups are handed to them in turn.
+// A call of at least kXcds mini-batches orders its sampler and relabel blocks
+// per XCD, so that each XCD runs whole mini-batches.
+constexpr int kXcds = 8;
 
 // One hop, as device arrays.  Host-written: frontier, src_out, fanout.
 // nF and pair_base are written by the host for hop 0 and by the previous
@@ -221,7 +225,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          ExclView X, hipStream_t stream, StageEv ev_sample = {},
-                         StageEv ev_select = {}, bool bit_mode = false);
+                         StageEv ev_select = {}, bool bit_mode = false, bool xcd_order = false);
 
 
 // Compaction pass: per bitmap tile, ranks of the set bits within the node
@@ -321,7 +325,7 @@ hipError_t launch_relabel(HopView hv, HopView next, const EtypeStatic *es,
                           const int64_t *tile_base, const int64_t *small,
                           int32_t n_types, int32_t n_etypes, int64_t n_edges,
                           const int64_t *src_gid, int32_t *src_local,
-                          hipStream_t stream, StageEv ev = {});
+                          hipStream_t stream, StageEv ev = {}, bool xcd_order = false);
 
 // Fill helpers (kernels, so that they are safe under graph capture).
 // One block copies small[0..n) to pinned host memory host[0..n) and then

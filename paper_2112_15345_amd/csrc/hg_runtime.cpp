@@ -1420,12 +1420,15 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     for (int64_t n : nF) copy_total += n;
     // bit mode when the call's vertices far outnumber the hop's kept edges
     const bool bit_mode = g->map_off[T] > kBitModeRatio * std::max<int64_t>(S, 1);
+    // blocks ordered per XCD when each XCD's share is whole mini-batches
+    // (pairs and kept edges are in mini-batch order)
+    const bool xcd_order = g->R / std::max(g->key_R, 1) >= kXcds;
     if ((e = launch_sample(hv, ws->d_es, R, T, P, n_wave, n_chunks, n_hubs, pa, cand, ws->dsmall,
                            dsigmas(), g->key_R, h, key_bits, gid_tmp, eid_all, dstl_all,
                            indptr_all,
                            src_slot, src_out.data(), inline_ptrs ? T : 0, X, stream,
                            stage_ev(h, HG_STAGE_SAMPLE), stage_ev(h, HG_STAGE_SELECT),
-                           bit_mode)) != hipSuccess)
+                           bit_mode, xcd_order)) != hipSuccess)
       return fail_device(e, "sample");
     int64_t ticketed = 0;
     if ((e = next_epoch(&epoch)) != hipSuccess ||
@@ -1438,7 +1441,8 @@ hg_status SampleRun::hops(std::vector<int64_t> &nF, int64_t n_items) {
     ticket_base += uint64_t(ticketed);
     reached_dirty = false;
     if ((e = launch_relabel(hv, nv, ws->d_es, g->d_tile_base, ws->dsmall, T, R, S, gid_tmp,
-                            srcl_all, stream, stage_ev(h, HG_STAGE_RELABEL))) != hipSuccess)
+                            srcl_all, stream, stage_ev(h, HG_STAGE_RELABEL),
+                            xcd_order)) != hipSuccess)
       return fail_device(e, "relabel");
     // the map now holds the source lists of this hop, which are region h+1's
     // frontier; the relabel pass wrote their sizes into that region

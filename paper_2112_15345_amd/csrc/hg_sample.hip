@@ -517,6 +517,7 @@ struct SampleArgs {
   int32_t key_R;
   int32_t hop, key_bits;
   bool bits;  // the hop marks reached bits (bit mode) instead of bytes
+  bool xcd;   // blocks ordered per XCD (xcd_block)
   int64_t *src_gid, *eid;
   int32_t *dst_local;
   int64_t *indptr_all;
@@ -1060,7 +1061,7 @@ __global__ __launch_bounds__(kSampleThreads) void k_hub_finish(SampleArgs A) {
   __shared__ uint8_t s_sel[kSampleWaves][kCandCap];
   const int wave = threadIdx.x / kWave;
   const int lane = lane_id();
-  const int64_t hub = int64_t(blockIdx.x) * kSampleWaves + wave;
+  const int64_t hub = xcd_block(blockIdx.x, gridDim.x, A.xcd) * kSampleWaves + wave;
   if (hub >= A.n_hubs) return;
   uint32_t *ck = s_key[wave];
   uint32_t *cj = s_j[wave];
@@ -1131,16 +1132,19 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   // the longest wavefronts first: groups of small take-all pairs (a
   // wavefront per 64 pairs), then hub chunks, then wavefront pairs, so that
   // short wavefronts fill in behind long ones
+  // each role's block count is a multiple of kXcds, so that its blocks can be
+  // ordered per XCD (xcd_block)
   if (b < A.blocks_a) {
     // the candidate lists are not used by this role: reuse their LDS
     GroupLds *g = reinterpret_cast<GroupLds *>(&s_cand[wave][0][0]);
-    role_pair_groups(A, *g, b * kSampleWaves + wave, b == 0);
+    role_pair_groups(A, *g, xcd_block(b, A.blocks_a, A.xcd) * kSampleWaves + wave, b == 0);
   } else if (b < A.blocks_a + A.blocks_c) {
-    const int64_t w = (b - A.blocks_a) * kSampleWaves + wave;
+    const int64_t w = xcd_block(b - A.blocks_a, A.blocks_c, A.xcd) * kSampleWaves + wave;
     if (w * A.chunks_per_wave < A.n_chunks)
       role_hub_chunks(A, w, reinterpret_cast<uint64_t *>(&s_cand[wave][0][0]));
   } else {
-    const int64_t w = (b - A.blocks_a - A.blocks_c) * kSampleWaves + wave;
+    const int64_t w =
+        xcd_block(b - A.blocks_a - A.blocks_c, A.blocks_b, A.xcd) * kSampleWaves + wave;
     if (w * kWavePairs < A.n_wave) role_wave_pairs(A, s_cand[wave][0], s_cand[wave][1], w);
   }
 }
@@ -1309,7 +1313,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
                          int64_t *eid, int32_t *dst_local, int64_t *indptr_all,
                          int64_t **src_out_slot, int64_t *const *src_out, int32_t n_src_out,
                          ExclView X, hipStream_t stream, StageEv ev_sample,
-                         StageEv ev_select, bool bit_mode) {
+                         StageEv ev_select, bool bit_mode, bool xcd_order) {
   if (n_src_out > kInlineSrcOut) return hipErrorInvalidValue;
   SampleArgs A;
   A.X = X;
@@ -1324,14 +1328,15 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.n_wave = n_wave;
   A.n_chunks = n_chunks;
   A.n_hubs = n_hubs;
-  // role A always has a block, for the closing CSC entries
-  A.blocks_a = std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads);
-  A.blocks_b = ((n_wave + kWavePairs - 1) / kWavePairs + kSampleWaves - 1) / kSampleWaves;
+  // role A always has blocks, for the closing CSC entries; every role's block
+  // count is rounded up to a multiple of kXcds (its spare blocks find no work)
+  A.blocks_a = xcd_round(std::max<int64_t>(1, (n_pairs + kSampleThreads - 1) / kSampleThreads));
+  A.blocks_b = xcd_round(((n_wave + kWavePairs - 1) / kWavePairs + kSampleWaves - 1) / kSampleWaves);
   // runs of chunks per wavefront: long enough to amortise finding the hub,
   // short enough to leave about kHubWaves wavefronts for the chip
   A.chunks_per_wave = std::min<int64_t>(kMaxChunksPerWave, std::max<int64_t>(1, n_chunks / kHubWaves));
   const int64_t waves_c = (n_chunks + A.chunks_per_wave - 1) / A.chunks_per_wave;
-  const int64_t blocks_c = (waves_c + kSampleWaves - 1) / kSampleWaves;
+  const int64_t blocks_c = xcd_round((waves_c + kSampleWaves - 1) / kSampleWaves);
   A.blocks_c = blocks_c;
   A.pa = pa;
   A.cand = cand;
@@ -1341,6 +1346,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
   A.hop = hop;
   A.key_bits = key_bits;
   A.bits = bit_mode;
+  A.xcd = xcd_order;
   A.src_gid = src_gid;
   A.eid = eid;
   A.dst_local = dst_local;
@@ -1350,7 +1356,7 @@ hipError_t launch_sample(HopView hv, const EtypeStatic *es, int32_t n_etypes,
            ev_sample.stop, A);
   if (n_hubs > 0) {
     // the hub lists are complete once the first launch has finished
-    const int64_t hb = (n_hubs + kSampleWaves - 1) / kSampleWaves;
+    const int64_t hb = xcd_round((n_hubs + kSampleWaves - 1) / kSampleWaves);
     launch_k(k_hub_finish, dim3(unsigned(hb)), dim3(kSampleThreads), 0, stream,
              ev_select.start, ev_select.stop, A);
   } else if (ev_select.any()) {
