@@ -65,14 +65,14 @@ DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (
 # by a digest of the kernel and runtime sources, the workload and the bundle
 # size; any other run reports them as null.
 COUNTER_TRAFFIC = [
-    {"sources": "5da65d0a0d0bd4da", "workload": 3, "bundle": 2, "task": "vertex",
-     "sample_compact": 562763614, "k_sample_per_launch": 116733800,
-     "gather": 176184806, "gather_per_launch": 352369612,
-     "sample_compact_l2_hit_rate": 0.5468, "gather_l2_hit_rate": 0.3311},
-    {"sources": "5da65d0a0d0bd4da", "workload": 2, "bundle": 32, "task": "vertex",
-     "sample_compact": 98869314, "k_sample_per_launch": 645453349,
-     "gather": 249220461, "gather_per_launch": 7975054752,
-     "sample_compact_l2_hit_rate": 0.6124, "gather_l2_hit_rate": 0.3328},
+    {"sources": "0982f5d7e6678e34", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 562659669, "k_sample_per_launch": 116752254,
+     "gather": 176182242, "gather_per_launch": 352364484,
+     "sample_compact_l2_hit_rate": 0.5481, "gather_l2_hit_rate": 0.3311},
+    {"sources": "0982f5d7e6678e34", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 76071441, "k_sample_per_launch": 553588432,
+     "gather": 249220086, "gather_per_launch": 7975042752,
+     "sample_compact_l2_hit_rate": 0.7293, "gather_l2_hit_rate": 0.3328},
 ]
 
 

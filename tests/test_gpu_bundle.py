@@ -57,6 +57,59 @@ def test_bundle_tiny_workload(B):
     assert not compare(first, result_dict(g, bundle[0]), g.T, g.R, len(fan))
 
 
+@pytest.mark.parametrize("B", [8, 13, 32])
+def test_bundle_tiny_workload_per_xcd(B):
+    """Bundles of 8 or more mini-batches order the sampler's and the relabel's
+    blocks per XCD (each XCD takes a contiguous eighth of every role); 8 gives
+    one block per XCD and role, 13 splits mini-batches between XCDs, 32 is the
+    largest bundle.  Every mini-batch equals its own single call and the
+    oracle."""
+    wl = W.WORKLOADS[1]
+    gen = W.make_graph(wl)
+    g = hg.Graph([(n, f.cuda()) for n, f in zip(gen.num_nodes, gen.feats)],
+                 [(s, d, ip.cuda(), ix.cuda()) for s, d, ip, ix in gen.etypes])
+    fan = wl.fanout_matrix()
+    batches = list(range(3, 3 + B))
+    bundle = check_bundle(g, [gpu_seeds(W.seeds_per_type(wl, b)) for b in batches], fan,
+                          batches, len(fan))
+    host = oracle.HostGraph(gen.host_ntypes(), gen.host_etypes())
+    for b, blocks in zip(batches, bundle):
+        ref = host.sample_blocks(W.seeds_per_type(wl, b), fan, b)
+        diffs = compare(ref, result_dict(g, blocks), g.T, g.R, len(fan))
+        assert not diffs, f"batch {b}: " + "\n".join(diffs[:10])
+
+
+def test_bundle_random_heterographs_per_xcd():
+    """Random heterographs (selections, take-all, empty seed lists) in bundles
+    of 8 to 12, then a graph with hubs of 2900 in-edges (chunked hub
+    sampling) in a bundle of 9: the per-XCD block order against single
+    calls."""
+    rng = np.random.default_rng(2024)
+    for c in range(6):
+        nn, ets, feats, seeds, fanouts, sigma, bits = pins.random_case(rng, max_nodes=300,
+                                                                       max_deg=300)
+        g = gpu_graph(nn, ets, feats)
+        B = int(rng.integers(8, 13))
+        seeds_list = []
+        for k in range(B):
+            s = [np.sort(rng.choice(n, size=min(n, int(rng.integers(0, 12))), replace=False))
+                 if n else np.zeros(0, np.int64) for n in nn]
+            seeds_list.append(gpu_seeds(s))
+        say(f"case {c}: T={len(nn)} R={len(ets)} H={len(fanouts)} B={B}")
+        check_bundle(g, seeds_list, fanouts, [sigma + 7 * k for k in range(B)], len(fanouts))
+    n = 3000
+    deg = np.where(np.arange(n) % 97 == 0, 2900, rng.integers(0, 40, n))
+    indptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int64)
+    indices = np.concatenate([np.sort(rng.choice(n, size=int(d), replace=False))
+                              for d in deg]).astype(np.int64)
+    g = gpu_graph([n], [(0, 0, indptr, indices)], [None])
+    # every seed list holds a hub; hop 1 reaches more of them
+    seeds_list = [gpu_seeds([np.unique(np.append(rng.choice(n, size=39, replace=False),
+                                                 97 * k))]) for k in range(9)]
+    say("hub case: B=9")
+    check_bundle(g, seeds_list, [[10], [5]], [3 + k for k in range(9)], 2)
+
+
 def test_bundle_random_heterographs():
     rng = np.random.default_rng(77)
     for c in range(12):

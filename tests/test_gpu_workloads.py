@@ -69,20 +69,21 @@ def test_workload_parity(idx, batches):
             f"({sum(v[3].size for v in ref['edges'].values())} edges)")
 
 
-def test_workload_pipeline_launch():
-    """The academic workload as bench.py runs it by default: bundles of 32
-    mini-batches submitted to a pipeline of 3 worker streams (at most 192
-    outstanding), here the first three timed bundles (batches 192..287).  Every
-    mini-batch comes back in order and equals its own single call (blocks and
-    gathered bytes); every mini-batch of the first bundle, and the first and
-    last of the others, also equal the oracle."""
-    wl, gen, g, host = workload_graph(2)
+@pytest.mark.parametrize("idx,B,first", [(2, 32, 192), (5, 8, 48)])
+def test_workload_pipeline_launch(idx, B, first):
+    """A workload as bench.py runs it by default: bundles of B mini-batches
+    (32 on the academic graph, 8 on the gather-heavy one) submitted to a
+    pipeline of 3 worker streams (at most 6 B outstanding), here the first
+    three timed bundles.  Every mini-batch comes back in order and equals its
+    own single call (blocks and gathered bytes); every mini-batch of the first
+    bundle, and the first and last of the others, also equal the oracle."""
+    wl, gen, g, host = workload_graph(idx)
     fan = wl.fanout_matrix()
     feat_types = [t for t, f in enumerate(gen.feats) if f is not None]
-    batches = list(range(192, 288))
-    bundles = [batches[i:i + 32] for i in range(0, len(batches), 32)]
+    batches = list(range(first, first + 3 * B))
+    bundles = [batches[i:i + B] for i in range(0, len(batches), B)]
     seeds = {b: gpu_seeds(W.seeds_per_type(wl, b)) for b in batches}
-    pipe = hg.Pipeline(g, workers=3, capacity=192, gather=feat_types)
+    pipe = hg.Pipeline(g, workers=3, capacity=6 * B, gather=feat_types)
     try:
         for u in bundles:
             pipe.submit_bundle([seeds[b] for b in u], fan, u)
