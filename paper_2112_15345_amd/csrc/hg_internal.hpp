@@ -338,6 +338,10 @@ hipError_t launch_publish(int64_t *small, int64_t *host, int32_t n, uint64_t seq
 hipError_t launch_store_ptrs(void **dst, void *const *vals, int32_t n, hipStream_t stream);
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t stream);
 hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t stream);
+// dst[0..n) = src[0..n) by a kernel that reads src, pinned host memory, over
+// the host link (no DMA copy on the stream); dst and src 8-byte aligned, else
+// hipErrorInvalidValue.  The host must not rewrite src until the kernel ran.
+hipError_t launch_upload(void *dst, const void *src, int64_t n, hipStream_t stream);
 
 // The non-empty mask of one destination type: for v < n, bit k of row v
 // (words per row) is set when indptrs[k][v + 1] > indptrs[k][v]; indptrs is a

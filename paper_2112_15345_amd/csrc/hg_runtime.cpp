@@ -507,7 +507,10 @@ hg_status acquire_workspace(hg_graph *g, size_t tab_bytes, hipStream_t stream,
     if (w->htab) (void)hipHostFree(w->htab);
     w->htab = nullptr;
     w->htab_cap = 0;
-    if (hipHostMalloc(reinterpret_cast<void **>(&w->htab), tab_bytes, 0) == hipSuccess)
+    // coherent: the upload kernel reads it over the host link, and no GPU
+    // cache may keep an earlier call's lines of it
+    if (hipHostMalloc(reinterpret_cast<void **>(&w->htab), tab_bytes, hipHostMallocCoherent) ==
+        hipSuccess)
       w->htab_cap = tab_bytes;
     else
       ok = false;
@@ -713,9 +716,14 @@ struct SampleRun {
   template <typename T>
   T *hfield(int r, size_t off) { return reinterpret_cast<T *>(hreg(r) + off); }
 
+  // The tables' bytes [from, to) to the device copy, read from the pinned,
+  // coherent host tables by a kernel: a DMA copy here has stalled every worker
+  // stream at once for several ms.  The host rewrites these bytes only in a
+  // later call on this workspace, and each call waits on the device (its
+  // readbacks) after its upload, so the kernel has read them by then.
   hipError_t upload(size_t from, size_t to) {
-    return hipMemcpyAsync(static_cast<char *>(ws->tab.p) + from, ws->htab + from,
-                          to - from, hipMemcpyHostToDevice, stream);
+    return launch_upload(static_cast<char *>(ws->tab.p) + from, ws->htab + from,
+                         int64_t(to - from), stream);
   }
 
   // A fresh epoch for a look-back launch.  Before epochs repeat, every

@@ -1158,6 +1158,16 @@ __global__ void k_fill_u32(uint32_t *p, int64_t n, uint32_t v) {
   for (int64_t i = grid_stride_start(); i < n; i += grid_stride_step()) p[i] = v;
 }
 
+// dst[0..n) = src[0..n) for 8-byte aligned dst and src, src in pinned host
+// memory (read over the host link).
+__global__ void k_upload(uint8_t *dst, const uint8_t *src, int64_t n) {
+  const int64_t words = n >> 3;
+  for (int64_t i = grid_stride_start(); i < words; i += grid_stride_step())
+    reinterpret_cast<uint64_t *>(dst)[i] = reinterpret_cast<const uint64_t *>(src)[i];
+  if (blockIdx.x == 0 && int64_t(threadIdx.x) < (n & 7))
+    dst[words * 8 + threadIdx.x] = src[words * 8 + threadIdx.x];
+}
+
 __global__ void k_check_etype(const int64_t *indptr, int64_t n_dst,
                               const int64_t *indices, int64_t nnz,
                               int64_t n_src, int32_t *err) {
@@ -1402,6 +1412,15 @@ hipError_t launch_fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t strea
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(n, 256, 8192)), dim3(256), 0,
                      stream, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_upload(void *dst, const void *src, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 7)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_upload, dim3(grid_for((n >> 3) + 1, 256, 64)), dim3(256), 0, stream,
+                     static_cast<uint8_t *>(dst), static_cast<const uint8_t *>(src), n);
   return hipGetLastError();
 }
 
