@@ -221,21 +221,44 @@ def run_units(args, g, units, timed, direct, submit, account):
 # ---------------------------------------------------------------------------
 # The vertex-seeded mini-batch (the default task)
 
-def step_bytes_model(g, nd, ns, ne):
-    """Algorithmic HBM bytes of sampling and compaction for one mini-batch:
-    per hop, with D frontier vertices, P (vertex, edge type) pairs, S kept
-    edges and U new vertices: 8 D (read the frontier) + 16 P (indptr pairs) +
-    8 S (read the kept sources) + 8 (P + R) (block CSC) + 16 S (edge ID and the
-    two local IDs) + 8 (D + U) (source lists)."""
-    total = 0
+def stage_bytes_model(g, nd, ns, ne, n_batches=1):
+    """Algorithmic HBM bytes of sampling and compaction for n_batches
+    mini-batches (nd, ns, ne summed over them), per stage.  Per hop, with D
+    frontier vertices, P (vertex, edge type) pairs, S kept edges, U new
+    vertices and R edge types per mini-batch: 8 D (read the frontier) + 16 P
+    (indptr pairs) + 8 S (read the kept sources) + 8 (P + R) (block CSC) + 16 S
+    (edge ID and the two local IDs) + 8 (D + U) (source lists).  The counting
+    pass reads the frontier and the indptr pairs; the sampler reads the kept
+    sources and writes the block CSC, the edge IDs and the destination IDs;
+    the compaction writes the source lists; the relabel writes the source
+    IDs."""
+    out = {name: 0 for name in ("count", "sample", "select", "compact", "relabel")}
+    R = g.R * n_batches
     for h in range(nd.shape[0]):
         D = int(nd[h].sum())
         U = int(ns[h].sum()) - D
         P = sum(int(nd[h, d]) for (_, d, _, _) in g.etypes)
         S = int(ne[h].sum())
-        R = g.R
-        total += 8 * D + 16 * P + 8 * S + 8 * (P + R) + 16 * S + 8 * (D + U)
-    return total
+        out["count"] += 8 * D + 16 * P
+        out["sample"] += 8 * S + 8 * (P + R) + 12 * S
+        out["compact"] += 8 * (D + U)
+        out["relabel"] += 4 * S
+    return out
+
+
+# Timed units that carry events on a memory-bound dominant stage: one in
+# ROOF_EVERY (the sampler's and the gather's launches carry them in every unit).
+ROOF_EVERY = 8
+
+# The kernels behind each stage, for the roofline of the dominant one.
+STAGE_KERNELS = {
+    "count": "k_count_scan (the counting pass: in-degree and kept count of every (vertex, "
+             "edge type) pair, the sampler's work lists, one single-pass scan)",
+    "select": "k_hub_finish (the K smallest candidates of every hub)",
+    "compact": "k_bits_count, k_bits_scan, k_bits_assign (the new frontier: reached marks "
+               "ranked into local IDs and source lists)",
+    "relabel": "k_relabel (the source local ID of every kept edge)",
+}
 
 
 def blocks_equal(a, b, H, T, R, feat_types):
@@ -397,7 +420,6 @@ def vertex_main(args, wl, gen, g):
     # dominant kernel) and the gather: events on every stage's launches cost
     # about 12% of a step here.  Every stage is timed in a profile pass after
     # the clock stops.
-    stage_ev = {u[0]: hg.StageEvents(H, stages=("sample",)) for u in timed}
 
     if args.copy_calibration_mb > 0:
         # a copy of known size, untimed, for scaling the memory counters
@@ -415,6 +437,28 @@ def vertex_main(args, wl, gen, g):
 
     def submit(pipe, u):
         pipe.submit_bundle([seeds[b] for b in u], fan, u, stage_events=stage_ev.get(u[0]))
+
+    # the stage with the most device time, found before the clock on the first
+    # unit (direct calls with every stage timed, twice: the first call's setup
+    # is left out); the timed region also carries events on that stage's
+    # launches, for the roofline of the dominant kernel
+    probe_u = (units or timed)[0]
+    for _ in range(2):
+        ev = hg.StageEvents(H)
+        blist = direct(probe_u, ev)
+        torch.cuda.synchronize()
+        probe_ms = {name: sum(ev.stage_ms(h, st) for h in range(H))
+                    for st, name in enumerate(hg.STAGE_NAMES)}
+        probe_ms["gather"] = ev.gather_ms()
+        del blist
+    probe_dom = max(probe_ms, key=probe_ms.get)
+    timed_stages = ("sample",) if probe_dom in ("sample", "gather") else ("sample", probe_dom)
+    # events on a memory-bound stage's launches slow the timed run (on the
+    # knowledge graph, the counting pass's on every unit cost 45% of a step),
+    # so only every ROOF_EVERY-th timed unit carries them
+    roof_units = [u for i, u in enumerate(timed) if i % ROOF_EVERY == 0]
+    stage_ev = {u[0]: hg.StageEvents(H, stages=timed_stages if i % ROOF_EVERY == 0
+                                     else ("sample",)) for i, u in enumerate(timed)}
 
     rec = []   # per timed unit: (unit, done_s, edges, rows_by_type, nd, ns, keys, ne)
     kept = []  # (batch, Blocks) checked against the oracle afterwards
@@ -467,6 +511,7 @@ def vertex_main(args, wl, gen, g):
     prof_units = timed[:max(1, min(len(timed), args.profile_units))]
     stage_ms = {name: 0.0 for name in hg.STAGE_NAMES}
     prof_alg = prof_steps = prof_keys = 0
+    prof_stage_alg = {name: 0 for name in hg.STAGE_NAMES}
     prof_gather_ms = 0.0
     for u in prof_units:
         ev = hg.StageEvents(H)
@@ -479,7 +524,9 @@ def vertex_main(args, wl, gen, g):
         nd = sum(b.counts()[0] for b in blist)
         ns = sum(b.counts()[1] for b in blist)
         ne = sum(np.asarray(b.edge_counts(), np.int64).reshape(H, g.R) for b in blist)
-        prof_alg += step_bytes_model(g, nd, ns, ne)
+        for name, v in stage_bytes_model(g, nd, ns, ne, len(u)).items():
+            prof_stage_alg[name] += v
+            prof_alg += v
         prof_keys += int(np.asarray(blist[0].counts()[2]).sum())  # the bundle's keys
         prof_steps += len(u)
         del blist
@@ -549,16 +596,42 @@ def vertex_main(args, wl, gen, g):
         sc["counter_over_algorithmic"] = traffic["sample_compact"] / (prof_alg / prof_steps)
         sc["l2_hit_rate"] = traffic.get("sample_compact_l2_hit_rate")
     # the roofline of the kernel with the most device time (from the profile
-    # pass), its rate measured over the timed region
+    # pass), its rate measured over the timed region; a stage whose launches
+    # carried no events there (the probe before the clock chose another) is
+    # passed over for the largest one that did
     per_kernel = dict(stage_ms, gather=prof_gather_ms)
     dominant = max(per_kernel, key=per_kernel.get)
-    if dominant == "gather":
+    timed_kinds = ("gather",) + timed_stages
+    reported = dominant if dominant in timed_kinds else max(timed_kinds, key=per_kernel.get)
+    if reported == "gather":
         n_l = len(timed)
         roofline = {"bound": gather["bound"], "kernel": gather["kernel"],
                     "achieved": g_gbps, "peak": peak, "unit": "GB/s", "frac": g_gbps / peak,
                     "traffic": traffic["gather_per_launch"] if traffic else None,
                     "algorithmic_per_launch": g_alg / n_l,
                     "avg_launch_us": gather_ms / n_l * 1e3}
+    elif reported != "sample":
+        # a memory-bound stage: its share of the byte model over its launches
+        st = hg.STAGE_NAMES.index(reported)
+        d_ms = sum(stage_ev[u[0]].stage_ms(h, st) for u in roof_units for h in range(H))
+        n_l = len(roof_units) * H
+        first = {u[0] for u in roof_units}
+        alg = sum(stage_bytes_model(g, r[4], r[5], r[7], len(r[0]))[reported]
+                  for r in rec if r[0][0] in first)
+        a_gbps = alg / (d_ms / 1e3) / 1e9 if d_ms > 0 else 0.0
+        roofline = {"bound": "hbm", "kernel": STAGE_KERNELS[reported],
+                    "achieved": a_gbps, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": a_gbps / HBM_PEAK_GBS, "traffic": None,
+                    "algorithmic_per_launch": alg / n_l, "avg_launch_us": d_ms / n_l * 1e3,
+                    "per_launch": "one hop of one call (a bundle's mini-batches together)",
+                    "measured_on": f"{len(roof_units)} of the {len(timed)} timed units "
+                                   f"(every {ROOF_EVERY}th carries events on this stage)"}
+        if stage_ms[reported] > 0:
+            alone = prof_stage_alg[reported] / (stage_ms[reported] / 1e3) / 1e9
+            roofline["alone"] = {
+                "achieved": alone, "frac": alone / HBM_PEAK_GBS,
+                "measured": f"profile pass (the first timed units again, direct calls on one "
+                            f"stream): the {reported} stage's launches with nothing beside them"}
     else:
         achieved = keys / sample_s / 1e9 if sample_s > 0 else 0.0
         roofline = {"bound": "alu", "kernel": "k_sample (the sampler: random keys of every "
@@ -576,9 +649,11 @@ def vertex_main(args, wl, gen, g):
                 "achieved": alone, "frac": alone / (PHILOX_PEAK_KEYS / 1e9),
                 "measured": "profile pass (the first timed units again, direct calls on one "
                             "stream): k_sample launches with nothing beside them"}
-        if dominant != "sample":
-            roofline["note"] = (f"the {dominant} stage has the most device time; the sampler's "
-                                f"roofline is reported")
+    if reported != dominant:
+        roofline["note"] = (f"the {dominant} stage had the most device time in the profile "
+                            f"pass, but the probe before the clock found {probe_dom}: the "
+                            f"roofline of {reported}, whose launches carried events, is "
+                            f"reported")
     roofline["device_copy_GBps"] = copy_gbps
     result = {
         "metric": "sampled edges/s + gathered feature GB/s per mini-batch (1 GPU), % of HBM peak",
