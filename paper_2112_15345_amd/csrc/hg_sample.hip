@@ -110,10 +110,10 @@ __global__ void k_insert_frontier(HopView hv, const TypeStatic *ts,
 // ---- counting pass ---------------------------------------------------------
 
 // Per pair: kept edges s, hub chunks, "one wavefront" flag, hub flag.
-struct PairCounts {
-  int64_t s, nch, wave, hub;
-  int64_t keys;  // random keys the sampler evaluates for the pair
-};
+// What the counting pass keeps of a pair until its outputs are written, next
+// to its kept count: its hub chunk count (a pair has fewer than 2^32 in-edges,
+// so fewer than 2^21 chunks) and whether it takes the wavefront or the hub role.
+constexpr uint32_t kPairWave = 1u << 30, kPairHub = 1u << 31, kPairChunks = kPairWave - 1;
 
 // Per edge type, what the counting pass reads for every pair; staged in
 // (dynamic) LDS, 52 bytes per edge type, when the graph has at most
@@ -194,9 +194,10 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
   int32_t *err = reinterpret_cast<int32_t *>(small + kSlotErr);
   if (tile == 0 && threadIdx.x == 0 && P + 1 > n_items) atomicOr(err, kErrBound);
 
-  // edge type and frontier slot of every item
+  // edge type of every item; bit k of `valid` says item k is a pair (not past
+  // the pairs), bit k of `reads` that it reads its indptr entries
   int etype[kPairItems];
-  const int64_t *fp[kPairItems];
+  uint32_t valid = 0, reads = 0;
   {
     int e = 0;
     if (base < P) {
@@ -213,24 +214,23 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 #pragma unroll
     for (int k = 0; k < kPairItems; ++k) {
       const int64_t p = base + k;
-      fp[k] = nullptr;
       if (p < P) {
         while (V.pbase(e + 1) <= p) ++e;
-        fp[k] = V.front(e) + (p - V.pbase(e));
+        valid |= 1u << k;
       }
       etype[k] = e;
     }
   }
+  // the frontier vertex of every item (all loads issued together)
   int64_t v[kPairItems];
 #pragma unroll
-  for (int k = 0; k < kPairItems; ++k) v[k] = fp[k] ? load_global(fp[k]) : 0;
-  const int64_t *ip[kPairItems];
+  for (int k = 0; k < kPairItems; ++k)
+    v[k] = (valid >> k) & 1 ? load_global(V.front(etype[k]) + (base + k - V.pbase(etype[k]))) : 0;
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
-    ip[k] = nullptr;
-    if (fp[k]) {
+    if ((valid >> k) & 1) {
       if (v[k] >= 0 && v[k] < V.n_dst(etype[k]))
-        ip[k] = V.indptr(etype[k]) + v[k];
+        reads |= 1u << k;
       else
         atomicOr(err, kErrSeedRange);
     }
@@ -239,41 +239,47 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
   // type reads no indptr (one mask word, shared by the vertex's edge types)
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
-    const uint32_t *m = ip[k] ? V.nz_mask(etype[k]) : nullptr;
+    const uint32_t *m = (reads >> k) & 1 ? V.nz_mask(etype[k]) : nullptr;
     if (m) {
       const int32_t slot = V.nz_slot(etype[k]);
       const uint32_t w = load_global(m + v[k] * V.nz_words(etype[k]) + (slot >> 5));
-      if (((w >> (slot & 31)) & 1u) == 0) ip[k] = nullptr;
+      if (((w >> (slot & 31)) & 1u) == 0) reads &= ~(1u << k);
     }
   }
   int64_t lo[kPairItems], hi[kPairItems];
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
-    lo[k] = ip[k] ? load_global(ip[k]) : 0;
-    hi[k] = ip[k] ? load_global(ip[k] + 1) : 0;
+    const int64_t *ip = V.indptr(etype[k]) + v[k];
+    lo[k] = (reads >> k) & 1 ? load_global(ip) : 0;
+    hi[k] = (reads >> k) & 1 ? load_global(ip + 1) : 0;
   }
 
-  PairCounts c[kPairItems];
+  // per item: kept count cs and the packed chunk count and role flags cf;
+  // the keys the sampler will evaluate (every in-edge of a pair that selects
+  // among its in-edges) summed per thread
+  int64_t cs[kPairItems];
+  uint32_t cf[kPairItems];
+  int64_t keys = 0;
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
     const int64_t p = base + k;
-    c[k] = PairCounts{0, 0, 0, 0, 0};
-    if (!fp[k]) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
+    cs[k] = 0;
+    cf[k] = 0;
+    if (!((valid >> k) & 1)) continue;  // past the pairs (an out-of-range vertex counts as deg 0)
     const int64_t deg = hi[k] - lo[k];
     const int64_t K = V.fanout(etype[k]);
     // in-edges that take part: all but the excluded ones
     const int32_t nx = excl_count(X, etype[k], p - V.pbase(etype[k]));
     const int64_t avail = deg - nx;
     const int64_t s = (K < 0 || avail <= K) ? avail : K;
-    c[k].s = s;
-    if (s < avail) c[k].keys = deg;  // a selection keys every in-edge
+    cs[k] = s;
+    if (s < avail) keys += deg;  // a selection keys every in-edge
     if (deg > kHubChunk && (s < avail || nx == 0)) {
-      c[k].nch = (deg + kHubChunk - 1) / kHubChunk;
-      c[k].hub = 1;
+      cf[k] = uint32_t((deg + kHubChunk - 1) / kHubChunk) | kPairHub;
     } else if (nx == 0 && s < deg && deg <= kLaneSelect) {
       // one lane of the pair-group role ranks its keys
     } else if (s > 0 && !(nx == 0 && s == deg && deg <= kThreadTakeAll)) {
-      c[k].wave = 1;  // pairs with excluded edges always take this role
+      cf[k] = kPairWave;  // pairs with excluded edges always take this role
     }
     if (deg > 0) {  // nothing reads these for an empty pair
       pa.plo[p] = lo[k];
@@ -281,26 +287,20 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
     }
   }
 
-  // the keys the sampler will evaluate: every in-edge of a pair that selects
-  // among its in-edges (wavefront sums in LDS, added up by thread 0 after the
-  // block scan's barriers: one atomic per tile)
+  // the keys: wavefront sums in LDS, added up by thread 0 after the block
+  // scan's barriers (one atomic per tile)
   __shared__ int64_t s_keys[kTileThreads / kWave];
-  {
-    int64_t keys = 0;
-#pragma unroll
-    for (int k = 0; k < kPairItems; ++k) keys += c[k].keys;
-    keys = wave_sum_i64(keys);
-    if (lane_id() == 0) s_keys[threadIdx.x / kWave] = keys;
-  }
+  keys = wave_sum_i64(keys);
+  if (lane_id() == 0) s_keys[threadIdx.x / kWave] = keys;
 
   // block scan of the per-thread sums, then the tile's prefix by look-back
   int64_t sum[4] = {0, 0, 0, 0};
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
-    sum[0] += c[k].s;
-    sum[1] += c[k].nch;
-    sum[2] += c[k].wave;
-    sum[3] += c[k].hub;
+    sum[0] += cs[k];
+    sum[1] += cf[k] & kPairChunks;
+    sum[2] += (cf[k] & kPairWave) ? 1 : 0;
+    sum[3] += (cf[k] & kPairHub) ? 1 : 0;
   }
   int64_t pre[4], agg[4];
   block_excl_scan4_256(sum, pre, agg, lds);
@@ -321,11 +321,12 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
 #pragma unroll
   for (int k = 0; k < kPairItems; ++k) {
     const int64_t p = base + k;
+    const bool wave = (cf[k] & kPairWave) != 0, hub = (cf[k] & kPairHub) != 0;
     if (p < n_items) {
       pa.off[p] = pre[0];
       pa.pet[p] = etype[k];
-      if (c[k].wave) pa.wlist[pre[2]] = p;
-      if (c[k].hub) {
+      if (wave) pa.wlist[pre[2]] = p;
+      if (hub) {
         pa.hub_cnt[pre[3]] = 0;
         pa.hub_pair[pre[3]] = p;
         pa.hub_choff[pre[3]] = pre[1];
@@ -336,10 +337,10 @@ __global__ __launch_bounds__(kTileThreads) void k_count_scan(
         for (int e2 = e; e2 >= 0 && V.pbase(e2) == p; --e2) ebase[e2] = pre[0];
       }
     }
-    pre[0] += c[k].s;
-    pre[1] += c[k].nch;
-    pre[2] += c[k].wave;
-    pre[3] += c[k].hub;
+    pre[0] += cs[k];
+    pre[1] += cf[k] & kPairChunks;
+    pre[2] += wave ? 1 : 0;
+    pre[3] += hub ? 1 : 0;
   }
   // the last tile holds the totals
   if (tile == int64_t(gridDim.x) - 1 && threadIdx.x == kTileThreads - 1) {
