@@ -61,18 +61,18 @@ DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (
 # per bundle, all its launches), and the L2
 # hit rates (TCC_HIT / (TCC_HIT + TCC_MISS)), for the kernel sources and
 # launch they were measured on (profiles/ holds the runs; every dispatch of
-# the run, warm-up and profile pass included, over its mini-batches).  Keyed
+# the run, probe, warm-up and profile pass included, over its mini-batches).  Keyed
 # by a digest of the kernel and runtime sources, the workload and the bundle
 # size; any other run reports them as null.
 COUNTER_TRAFFIC = [
-    {"sources": "0982f5d7e6678e34", "workload": 3, "bundle": 2, "task": "vertex",
-     "sample_compact": 562659669, "k_sample_per_launch": 116752254,
-     "gather": 176182242, "gather_per_launch": 352364484,
-     "sample_compact_l2_hit_rate": 0.5481, "gather_l2_hit_rate": 0.3311},
-    {"sources": "0982f5d7e6678e34", "workload": 2, "bundle": 32, "task": "vertex",
-     "sample_compact": 76071441, "k_sample_per_launch": 553588432,
-     "gather": 249220086, "gather_per_launch": 7975042752,
-     "sample_compact_l2_hit_rate": 0.7293, "gather_l2_hit_rate": 0.3328},
+    {"sources": "0f1be5e0dbd03baa", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 560705638, "k_sample_per_launch": 116773195,
+     "gather": 176146218, "gather_per_launch": 352292437,
+     "sample_compact_l2_hit_rate": 0.5396, "gather_l2_hit_rate": 0.3311},
+    {"sources": "0f1be5e0dbd03baa", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 76112670, "k_sample_per_launch": 553784110,
+     "gather": 249191543, "gather_per_launch": 7974129376,
+     "sample_compact_l2_hit_rate": 0.7272, "gather_l2_hit_rate": 0.3327},
 ]
 
 
@@ -665,6 +665,9 @@ def vertex_main(args, wl, gen, g):
         "warmup_run": warm_n,
         "ms_per_step": ms_per_step,
         "ms_per_step_p10": p10, "ms_per_step_p50": p50, "ms_per_step_p90": p90,
+        "probe": {"dominant": probe_dom, "calls": 2, "mini_batches": 2 * len(probe_u),
+                  "measured": "before warm-up: the first unit twice, direct calls, every "
+                              "stage timed"},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
