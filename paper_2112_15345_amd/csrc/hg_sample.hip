@@ -1133,14 +1133,35 @@ __global__ __launch_bounds__(kSampleThreads) void k_sample(SampleArgs A) {
   // the longest wavefronts first: groups of small take-all pairs (a
   // wavefront per 64 pairs), then hub chunks, then wavefront pairs, so that
   // short wavefronts fill in behind long ones
-  // each role's block count is a multiple of kXcds, so that its blocks can be
-  // ordered per XCD (xcd_block)
-  if (b < A.blocks_a) {
+  // Roles A and C share the first blocks_a + blocks_c blocks.  Ordered per
+  // XCD, each role keeps its own range (its block count a multiple of kXcds,
+  // xcd_block); otherwise role A's blocks are spread evenly among role C's, so
+  // that the pair groups' memory waits overlap the hub chunks' key work:
+  // block x of the shared range is role A's block f(x) when f(x + 1) > f(x),
+  // with f(x) = floor(x blocks_a / (blocks_a + blocks_c)), else role C's
+  // block x - f(x).
+  const int64_t n_ac = A.blocks_a + A.blocks_c;
+  int64_t ra = -1, rc = -1;
+  if (b < n_ac) {
+    if (A.xcd) {
+      if (b < A.blocks_a)
+        ra = xcd_block(b, A.blocks_a, true);
+      else
+        rc = xcd_block(b - A.blocks_a, A.blocks_c, true);
+    } else {
+      const int64_t f0 = b * A.blocks_a / n_ac, f1 = (b + 1) * A.blocks_a / n_ac;
+      if (f1 > f0)
+        ra = f0;
+      else
+        rc = b - f0;
+    }
+  }
+  if (ra >= 0) {
     // the candidate lists are not used by this role: reuse their LDS
     GroupLds *g = reinterpret_cast<GroupLds *>(&s_cand[wave][0][0]);
-    role_pair_groups(A, *g, xcd_block(b, A.blocks_a, A.xcd) * kSampleWaves + wave, b == 0);
-  } else if (b < A.blocks_a + A.blocks_c) {
-    const int64_t w = xcd_block(b - A.blocks_a, A.blocks_c, A.xcd) * kSampleWaves + wave;
+    role_pair_groups(A, *g, ra * kSampleWaves + wave, ra == 0);
+  } else if (rc >= 0) {
+    const int64_t w = rc * kSampleWaves + wave;
     if (w * A.chunks_per_wave < A.n_chunks)
       role_hub_chunks(A, w, reinterpret_cast<uint64_t *>(&s_cand[wave][0][0]));
   } else {
