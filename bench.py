@@ -65,14 +65,14 @@ DEFAULTS = {1: (2, 32, 320), 2: (3, 32, 384), 3: (3, 2, 40), 4: (3, 4, 96), 5: (
 # by a digest of the kernel and runtime sources, the workload and the bundle
 # size; any other run reports them as null.
 COUNTER_TRAFFIC = [
-    {"sources": "0f1be5e0dbd03baa", "workload": 3, "bundle": 2, "task": "vertex",
-     "sample_compact": 560705638, "k_sample_per_launch": 116773195,
-     "gather": 176146218, "gather_per_launch": 352292437,
-     "sample_compact_l2_hit_rate": 0.5396, "gather_l2_hit_rate": 0.3311},
-    {"sources": "0f1be5e0dbd03baa", "workload": 2, "bundle": 32, "task": "vertex",
-     "sample_compact": 76112670, "k_sample_per_launch": 553784110,
-     "gather": 249191543, "gather_per_launch": 7974129376,
-     "sample_compact_l2_hit_rate": 0.7272, "gather_l2_hit_rate": 0.3327},
+    {"sources": "56dfd8cef016cf90", "workload": 3, "bundle": 2, "task": "vertex",
+     "sample_compact": 556421428, "k_sample_per_launch": 113970779,
+     "gather": 176148581, "gather_per_launch": 352297162,
+     "sample_compact_l2_hit_rate": 0.5455, "gather_l2_hit_rate": 0.3312},
+    {"sources": "56dfd8cef016cf90", "workload": 2, "bundle": 32, "task": "vertex",
+     "sample_compact": 76145261, "k_sample_per_launch": 553555963,
+     "gather": 249191661, "gather_per_launch": 7974133152,
+     "sample_compact_l2_hit_rate": 0.727, "gather_l2_hit_rate": 0.3327},
 ]
 
 
