@@ -114,7 +114,7 @@ struct TypeStatic {
 // Bit mode is chosen when vertices > kBitModeRatio x kept edges.
 constexpr int64_t kBitModeRatio = 16;
 // The chip's XCDs, each with its own L2; workgroups are handed to them in turn.
-// A call of at least kXcds mini-batches orders its sampler and relabel blocks
+// A call of at least kXcds mini-batches orders its sampler, hub selection and relabel blocks
 // per XCD, so that each XCD runs whole mini-batches.
 constexpr int kXcds = 8;
 
