@@ -512,6 +512,9 @@ def vertex_main(args, wl, gen, g):
     stage_ms = {name: 0.0 for name in hg.STAGE_NAMES}
     prof_alg = prof_steps = prof_keys = 0
     prof_stage_alg = {name: 0 for name in hg.STAGE_NAMES}
+    hop_ms = [{name: 0.0 for name in hg.STAGE_NAMES} for _ in range(H)]
+    hop_keys = np.zeros(H, np.int64)
+    hop_kept = np.zeros(H, np.int64)
     prof_gather_ms = 0.0
     for u in prof_units:
         ev = hg.StageEvents(H)
@@ -520,10 +523,13 @@ def vertex_main(args, wl, gen, g):
         for h in range(H):
             for st, name in enumerate(hg.STAGE_NAMES):
                 stage_ms[name] += ev.stage_ms(h, st)
+                hop_ms[h][name] += ev.stage_ms(h, st)
+        hop_keys += np.asarray(blist[0].counts()[2], np.int64)  # the bundle's keys per hop
         prof_gather_ms += ev.gather_ms()
         nd = sum(b.counts()[0] for b in blist)
         ns = sum(b.counts()[1] for b in blist)
         ne = sum(np.asarray(b.edge_counts(), np.int64).reshape(H, g.R) for b in blist)
+        hop_kept += ne.sum(axis=1)
         for name, v in stage_bytes_model(g, nd, ns, ne, len(u)).items():
             prof_stage_alg[name] += v
             prof_alg += v
@@ -584,6 +590,12 @@ def vertex_main(args, wl, gen, g):
                       f"calls on one stream, every stage's launches carrying HIP events",
           "ms_per_step": sc_ms / prof_steps,
           "stage_ms_per_step": {k: v / prof_steps for k, v in stage_ms.items()},
+          "per_hop": [{"stage_ms_per_step": {k: v / prof_steps for k, v in hop_ms[h].items()},
+                       "kept_edges_per_step": int(hop_kept[h]) / prof_steps,
+                       "keys_per_step": int(hop_keys[h]) / prof_steps,
+                       "sampler_keys_per_s": (int(hop_keys[h]) / (hop_ms[h]["sample"] / 1e3)
+                                              if hop_ms[h]["sample"] > 0 else None)}
+                      for h in range(H)],
           "gather_ms_per_step": prof_gather_ms / prof_steps,
           "algorithmic_bytes_per_step": prof_alg / prof_steps,
           "algorithmic_GBps": prof_alg / (sc_ms / 1e3) / 1e9 if sc_ms > 0 else None,
