@@ -453,9 +453,9 @@ def vertex_main(args, wl, gen, g):
         del blist
     probe_dom = max(probe_ms, key=probe_ms.get)
     timed_stages = ("sample",) if probe_dom in ("sample", "gather") else ("sample", probe_dom)
-    # events on a memory-bound stage's launches slow the timed run (on the
-    # knowledge graph, the counting pass's on every unit cost 45% of a step),
-    # so only every ROOF_EVERY-th timed unit carries them
+    # events cost time on the launches that carry them (on every stage's
+    # launches about 12% of a step), so on this stage only every ROOF_EVERY-th
+    # timed unit carries them
     roof_units = [u for i, u in enumerate(timed) if i % ROOF_EVERY == 0]
     stage_ev = {u[0]: hg.StageEvents(H, stages=timed_stages if i % ROOF_EVERY == 0
                                      else ("sample",)) for i, u in enumerate(timed)}
